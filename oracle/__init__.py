@@ -1,0 +1,240 @@
+"""fp64 CPU oracle of the Carryover drafter step.  TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  It shares no code with the HIP path:
+the two meet only in the seeded input generator (``synth``).
+
+What it computes (paper: Section 2.1, Eqs. 1-2; Appendix A, Algorithm 1 and
+the "Cache semantics" paragraph; Section 2 "Preliminaries"):
+
+* greedy verification accepts the longest prefix m on which the draft agrees
+  with the target's greedy tokens;
+* the carryover update projects all B verified rows in one pass, with the
+  carry embedding E added to the rejected rows m..B-1 *before* the fusion
+  projection F; keys and values of layer l are K_l(F(x)) and V_l(F(x));
+* keys are rotated once, at the row's absolute position, when projected;
+* rows 0..m-1 are appended to the committed context C_l; rows m..B-1 replace
+  the carryover segment U_l wholesale (U starts empty; full acceptance leaves
+  it empty; it never holds more than B rows);
+* the next draft's block queries (position ctx_len + i) attend to [C_l ; U_l]
+  with a plain softmax; the baseline update (left column of Algorithm 1)
+  projects only rows 0..m-1 and has no U.
+
+Readings where the paper is silent (each also listed in the design doc): no norm
+and no bias in F, K_l, V_l; rotate-half RoPE with inverse frequency
+theta^(-2i/hd); softmax scale 1/sqrt(hd); query head h reads KV head
+h // (Hq/Hkv); window row j sits at position ctx_len_before + j; block queries
+see every committed and carried key (no position mask).
+
+All arithmetic is float64 on exact widenings of the stored inputs; nothing is
+rounded in between.  Parity pins: see tests/test_oracle_*.py.  Every function
+below is pinned by at least one of those tests.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+# status codes (mirrors of the library's data-dependent error codes)
+OK, ERR_CAPACITY, ERR_PAGE_RANGE, ERR_LENGTH = 0, 4, 5, 7
+SKIP = -(2 ** 31)
+PAGE = 16
+
+
+# ------------------------------------------------------------------ routing
+
+def accept_len(draft: np.ndarray, target: np.ndarray) -> int:
+    """Greedy verification: number of leading draft tokens equal to the
+    target's greedy tokens (Section 2 "Preliminaries"; Section 2.2)."""
+    m = 0
+    while m < len(draft) and draft[m] == target[m]:
+        m += 1
+    return m
+
+
+def route(draft, target, ctx_len, carry_len, page_table, num_pages, mode="carry"):
+    """Split every verified window by its accepted prefix (Eq. 1, Algorithm 1).
+
+    mode: 'carry' (Carryover column), 'baseline' (Baseline column),
+    'accept_all' (every row committed: building context by prefill),
+    'carry_only' (rows 0..m-1 are already committed elsewhere and are skipped).
+
+    Returns a dict with accept_len [S], row_pos [S][B], row_dst [S][B]
+    (>= 0: global committed slot page*16 + pos % 16; -1-r: carry row r;
+    SKIP: not stored), new ctx_len [S], new carry_len [S] and a per-sequence
+    status.  A sequence that fails a check keeps its lengths, stores no row
+    and reports accept_len 0.
+    """
+    draft = np.asarray(draft)
+    S, B = draft.shape
+    out = dict(accept_len=np.zeros(S, np.int32), row_pos=np.zeros((S, B), np.int32),
+               row_dst=np.full((S, B), SKIP, np.int32), ctx_len=np.array(ctx_len, np.int32).copy(),
+               carry_len=np.array(carry_len, np.int32).copy(), status=np.zeros(S, np.int32),
+               touched=np.ones(S, bool))
+    cap = page_table.shape[1] * PAGE
+    for s in range(S):
+        p0 = int(ctx_len[s])
+        m = B if mode == "accept_all" else accept_len(draft[s], target[s])
+        if p0 < 0:
+            out["status"][s] = ERR_LENGTH
+        elif p0 + B > cap:
+            out["status"][s] = ERR_CAPACITY
+        else:
+            for j in range(m if mode in ("carry", "baseline", "accept_all") else 0):
+                page = int(page_table[s][(p0 + j) // PAGE])
+                if page < 0 or page >= num_pages:
+                    out["status"][s] = ERR_PAGE_RANGE
+                    break
+        if out["status"][s] != OK:
+            out["touched"][s] = False
+            out["row_pos"][s] = p0 + np.arange(B) if p0 >= 0 else 0
+            continue
+        out["accept_len"][s] = m
+        for j in range(B):
+            pos = p0 + j
+            out["row_pos"][s, j] = pos
+            if j < m:
+                if mode != "carry_only":
+                    page = int(page_table[s][pos // PAGE])
+                    out["row_dst"][s, j] = page * PAGE + pos % PAGE
+            elif mode in ("carry", "carry_only"):
+                out["row_dst"][s, j] = -1 - (j - m)
+        out["ctx_len"][s] = p0 + m
+        out["carry_len"][s] = (B - m) if mode in ("carry", "carry_only") else 0
+    return out
+
+
+# --------------------------------------------------------------- projection
+
+def rope(x: np.ndarray, pos, theta: float) -> np.ndarray:
+    """Rotate-half rotary embedding of the last axis at absolute position(s) pos.
+
+    Pairs (i, i + hd/2) are rotated by the angle pos * theta^(-2i/hd).
+    ``pos`` broadcasts against x.shape[:-1].
+    """
+    x = np.asarray(x, dtype=np.float64)
+    hd = x.shape[-1]
+    half = hd // 2
+    inv = theta ** (-2.0 * np.arange(half, dtype=np.float64) / hd)
+    ang = np.asarray(pos, dtype=np.float64)[..., None] * inv
+    c, s = np.cos(ang), np.sin(ang)
+    a, b = x[..., :half], x[..., half:]
+    return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+
+
+def project(H, E, add_e, WF, WKV, pos, L, Hkv, hd, theta):
+    """Phi_l(H) of Eq. 1 for every layer, with E added to flagged rows before F
+    (Eq. 2) and RoPE applied to the keys at each row's position.
+
+    H [M][Dcat], E [Dcat], add_e [M] (bool), WF [d][Dcat], WKV [L*2*Hkv*hd][d]
+    ordered (layer, K|V, head, dim), pos [M].
+    Returns K, V as [M][L][Hkv][hd] float64.
+    """
+    H = np.asarray(H, np.float64)
+    x = H + np.asarray(add_e, np.float64)[:, None] * np.asarray(E, np.float64)[None, :]
+    z = x @ np.asarray(WF, np.float64).T                         # F
+    kv = (z @ np.asarray(WKV, np.float64).T).reshape(len(H), L, 2, Hkv, hd)
+    k = rope(kv[:, :, 0], np.asarray(pos)[:, None, None], theta)
+    return k, kv[:, :, 1].copy()
+
+
+# ---------------------------------------------------------------- attention
+
+def attend(q, qpos, k, v, theta):
+    """Softmax attention of unrotated queries q [nq][hd] at positions qpos over
+    already-rotated keys k [nk][hd] and values v [nk][hd]; dense, two-pass.
+    Returns (O [nq][hd], LSE [nq]); an empty key set gives O = 0, LSE = -inf."""
+    q = rope(np.asarray(q, np.float64), np.asarray(qpos), theta)
+    nq, hd = q.shape
+    if len(k) == 0:
+        return np.zeros((nq, hd)), np.full(nq, -np.inf)
+    s = (q @ np.asarray(k, np.float64).T) / math.sqrt(hd)
+    mx = s.max(axis=1, keepdims=True)
+    w = np.exp(s - mx)
+    den = w.sum(axis=1, keepdims=True)
+    return (w @ np.asarray(v, np.float64)) / den, (mx + np.log(den))[:, 0]
+
+
+# ------------------------------------------------------------ drafter state
+
+class State:
+    """Logical (unpaged) drafter KV of S sequences: committed C_l and carryover U_l."""
+
+    def __init__(self, S, L, Hkv, hd, store=np.float64):
+        self.S, self.L, self.Hkv, self.hd, self.store = S, L, Hkv, hd, store
+        empty = lambda: np.zeros((L, 0, Hkv, hd), store)
+        self.ck = [empty() for _ in range(S)]
+        self.cv = [empty() for _ in range(S)]
+        self.uk = [empty() for _ in range(S)]
+        self.uv = [empty() for _ in range(S)]
+
+    def ctx_len(self):
+        return np.array([c.shape[1] for c in self.ck], np.int32)
+
+    def carry_len(self):
+        return np.array([u.shape[1] for u in self.uk], np.int32)
+
+    def set_committed(self, s, k, v):
+        """Install committed K/V [L][n][Hkv][hd] of sequence s (already rotated)."""
+        self.ck[s] = np.asarray(k, self.store)
+        self.cv[s] = np.asarray(v, self.store)
+
+    def commit_and_replace(self, s, k_acc, v_acc, k_rej, v_rej):
+        """C_l <- [C_l ; J_acc];  U_l <- J_rej (old U dropped).  Inputs [n][L][Hkv][hd]."""
+        t = lambda a: np.asarray(a, self.store).transpose(1, 0, 2, 3)
+        self.ck[s] = np.concatenate([self.ck[s], t(k_acc)], axis=1)
+        self.cv[s] = np.concatenate([self.cv[s], t(v_acc)], axis=1)
+        self.uk[s] = t(k_rej).copy()
+        self.uv[s] = t(v_rej).copy()
+
+    def context(self, s, layer, g):
+        """ctx_l = [C_l ; U_l] for KV head g: (keys, values) [n][hd]."""
+        k = np.concatenate([self.ck[s][layer, :, g], self.uk[s][layer, :, g]], axis=0)
+        v = np.concatenate([self.cv[s][layer, :, g], self.uv[s][layer, :, g]], axis=0)
+        return k.astype(np.float64), v.astype(np.float64)
+
+
+def attend_state(state: State, Q, Hq, theta, seqs=None, layers=None):
+    """Block attention of every (layer, sequence, query row, query head) over
+    ctx = [C;U].  Q [L][S][B][Hq][hd] unrotated; query i sits at ctx_len + i.
+    Returns O [L][S][B][Hq][hd], LSE [L][S][B][Hq] (NaN where not computed)."""
+    L, S, B, _, hd = Q.shape
+    G = Hq // state.Hkv
+    O = np.full(Q.shape, np.nan)
+    LSE = np.full(Q.shape[:-1], np.nan)
+    ctx = state.ctx_len()
+    for s in (range(S) if seqs is None else seqs):
+        for layer in (range(L) if layers is None else layers):
+            for g in range(state.Hkv):
+                k, v = state.context(s, layer, g)
+                heads = list(range(g * G, (g + 1) * G))
+                q = Q[layer, s][:, heads].reshape(B * G, hd)
+                qpos = np.repeat(ctx[s] + np.arange(B), G)
+                o, lse = attend(q, qpos, k, v, theta)
+                O[layer, s][:, heads] = o.reshape(B, G, hd)
+                LSE[layer, s][:, heads] = lse.reshape(B, G)
+    return O, LSE
+
+
+def round_update(state: State, r, H, E, WF, WKV, theta, mode="carry", seqs=None):
+    """Post-verification update of Algorithm 1 for the sequences in ``seqs``,
+    given a route result ``r`` (see ``route``).  H [S][B][Dcat]."""
+    S, B, _ = H.shape
+    for s in (range(S) if seqs is None else seqs):
+        if not r["touched"][s]:
+            continue
+        m = int(r["accept_len"][s])
+        rows = np.arange(B) if mode in ("carry", "carry_only") else np.arange(m)
+        pos = r["row_pos"][s][rows]
+        k, v = project(H[s][rows], E, rows >= m, WF, WKV, pos, state.L, state.Hkv,
+                       state.hd, theta)
+        if mode == "carry_only":
+            k_acc, v_acc = k[:0], v[:0]
+        else:
+            k_acc, v_acc = k[:m], v[:m]
+        if mode in ("carry", "carry_only"):
+            k_rej, v_rej = k[m:], v[m:]
+        else:
+            k_rej, v_rej = k[:0], v[:0]
+        state.commit_and_replace(s, k_acc, v_acc, k_rej, v_rej)

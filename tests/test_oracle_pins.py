@@ -1,0 +1,420 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+None of these re-types an oracle formula and compares it with itself: each
+check is a closed form, an invariant stated by the paper, a textbook special
+case, or a brute-force recomputation by a different route on tiny inputs.
+The paper prints no worked example for this computation, so there is no
+value from the paper itself to compare against.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from synth import workloads as wl
+
+RNG = np.random.default_rng(1234)
+
+
+# ---------------------------------------------------------------- RoPE
+
+def test_rope_position_zero_is_identity():
+    x = RNG.standard_normal((5, 64))
+    np.testing.assert_array_equal(oracle.rope(x, 0, 1e4), x)
+
+
+def test_rope_two_dims_is_plane_rotation():
+    # hd = 2: one pair with inverse frequency theta^0 = 1 -> rotation by angle p
+    for p in (1, 7, 123):
+        y = oracle.rope(np.array([1.0, 0.0]), p, 1e4)
+        np.testing.assert_allclose(y, [math.cos(p), math.sin(p)], rtol=0, atol=1e-15)
+        y = oracle.rope(np.array([0.0, 1.0]), p, 1e4)
+        np.testing.assert_allclose(y, [-math.sin(p), math.cos(p)], rtol=0, atol=1e-15)
+
+
+def test_rope_pairing_and_frequencies():
+    # hd = 4, theta = 100: pair (0, 2) turns at rate 1, pair (1, 3) at 100^(-2/4) = 0.1
+    p = 3
+    y = oracle.rope(np.array([1.0, 0, 0, 0]), p, 100.0)
+    np.testing.assert_allclose(y, [math.cos(p), 0, math.sin(p), 0], atol=1e-15)
+    y = oracle.rope(np.array([0, 1.0, 0, 0]), p, 100.0)
+    np.testing.assert_allclose(y, [0, math.cos(0.1 * p), 0, math.sin(0.1 * p)], atol=1e-15)
+
+
+def test_rope_norm_and_relative_position():
+    q = RNG.standard_normal(128)
+    k = RNG.standard_normal(128)
+    for p, pp in ((5, 3), (3000, 17), (40000, 39999)):
+        rq, rk = oracle.rope(q, p, 1e6), oracle.rope(k, pp, 1e6)
+        assert abs(np.linalg.norm(rq) - np.linalg.norm(q)) < 1e-12
+        # <R(q,p), R(k,p')> depends only on p - p'
+        np.testing.assert_allclose(rq @ rk, oracle.rope(q, p - pp, 1e6) @ k, rtol=1e-10)
+
+
+# ------------------------------------------------------------- attention
+
+def test_attend_single_key_returns_its_value():
+    q, k, v = RNG.standard_normal((3, 64)), RNG.standard_normal((1, 64)), RNG.standard_normal((1, 64))
+    o, lse = oracle.attend(q, np.arange(3), k, v, 1e4)
+    np.testing.assert_allclose(o, np.repeat(v, 3, axis=0), rtol=0, atol=1e-14)
+    rq = oracle.rope(q, np.arange(3), 1e4)
+    np.testing.assert_allclose(lse, rq @ k[0] / 8.0, rtol=1e-13)
+
+
+def test_attend_zero_query_and_identical_keys_give_mean():
+    v = RNG.standard_normal((9, 64))
+    o, lse = oracle.attend(np.zeros((2, 64)), [0, 1], RNG.standard_normal((9, 64)), v, 1e4)
+    np.testing.assert_allclose(o, np.repeat(v.mean(0, keepdims=True), 2, 0), atol=1e-14)
+    np.testing.assert_allclose(lse, math.log(9), rtol=1e-14)
+    k = np.repeat(RNG.standard_normal((1, 64)), 9, 0)
+    o, _ = oracle.attend(RNG.standard_normal((2, 64)), [4, 5], k, v, 1e4)
+    np.testing.assert_allclose(o, np.repeat(v.mean(0, keepdims=True), 2, 0), atol=1e-13)
+
+
+def test_attend_two_keys_closed_form_scale():
+    # q at position 0 (no rotation), keys e0*a and e0*b: logits a/sqrt(hd), b/sqrt(hd)
+    hd = 16
+    q = np.zeros((1, hd)); q[0, 0] = 1.0
+    k = np.zeros((2, hd)); k[0, 0] = 3.0; k[1, 0] = -1.0
+    # keys are stored rotated; position 0 keeps them as they are
+    v = RNG.standard_normal((2, hd))
+    o, lse = oracle.attend(q, [0], k, v, 1e4)
+    a, b = 3.0 / 4.0, -1.0 / 4.0
+    w0 = 1.0 / (1.0 + math.exp(b - a))
+    np.testing.assert_allclose(o[0], w0 * v[0] + (1 - w0) * v[1], rtol=1e-14)
+    np.testing.assert_allclose(lse[0], math.log(math.exp(a) + math.exp(b)), rtol=1e-14)
+
+
+def test_attend_one_dominant_logit_selects_value():
+    hd = 64
+    q = np.zeros((1, hd)); q[0, 3] = 1.0
+    k = RNG.standard_normal((20, hd)) * 0.01
+    k[11, 3] = 2000.0
+    v = RNG.standard_normal((20, hd))
+    o, _ = oracle.attend(q, [0], k, v, 1e4)
+    np.testing.assert_allclose(o[0], v[11], rtol=0, atol=1e-12)
+
+
+def test_attend_empty_key_set():
+    o, lse = oracle.attend(RNG.standard_normal((4, 64)), np.arange(4), np.zeros((0, 64)),
+                           np.zeros((0, 64)), 1e4)
+    assert np.all(o == 0) and np.all(np.isneginf(lse))
+
+
+def test_attend_shift_of_all_positions_and_key_order_invariance():
+    hd, n = 64, 37
+    q = RNG.standard_normal((4, hd))
+    kraw = RNG.standard_normal((n, hd))
+    v = RNG.standard_normal((n, hd))
+    kpos = np.arange(n)
+    o1, l1 = oracle.attend(q, 40 + np.arange(4), oracle.rope(kraw, kpos, 1e4), v, 1e4)
+    d = 1234
+    o2, l2 = oracle.attend(q, 40 + d + np.arange(4), oracle.rope(kraw, kpos + d, 1e4), v, 1e4)
+    np.testing.assert_allclose(o1, o2, rtol=1e-9, atol=1e-11)
+    np.testing.assert_allclose(l1, l2, rtol=1e-10)
+    perm = RNG.permutation(n)
+    o3, l3 = oracle.attend(q, 40 + np.arange(4), oracle.rope(kraw, kpos, 1e4)[perm], v[perm], 1e4)
+    np.testing.assert_allclose(o1, o3, rtol=1e-12, atol=1e-14)
+
+
+def _merge(parts):
+    """Closed-form merge of softmax partials (O_i, LSE_i) over disjoint key sets."""
+    lses = np.array([p[1] for p in parts])
+    M = lses.max(axis=0)
+    M = np.where(np.isneginf(M), 0.0, M)
+    w = np.exp(lses - M)
+    O = sum(wi[:, None] * p[0] for wi, p in zip(w, parts))
+    den = w.sum(axis=0)
+    return O / den[:, None], M + np.log(den)
+
+
+def test_concatenated_context_equals_two_segment_merge():
+    """Attention over [C;U] equals the softmax merge of attention over C and over U,
+    including arbitrary splits of C (with empty pieces)."""
+    hd = 64
+    q = RNG.standard_normal((32, hd))
+    qpos = 500 + np.arange(32)
+    C = oracle.rope(RNG.standard_normal((300, hd)), np.arange(300), 1e4)
+    U = oracle.rope(RNG.standard_normal((9, hd)), 300 + np.arange(9), 1e4)
+    VC, VU = RNG.standard_normal((300, hd)), RNG.standard_normal((9, hd))
+    full = oracle.attend(q, qpos, np.concatenate([C, U]), np.concatenate([VC, VU]), 1e4)
+    two = _merge([oracle.attend(q, qpos, C, VC, 1e4), oracle.attend(q, qpos, U, VU, 1e4)])
+    np.testing.assert_allclose(two[0], full[0], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(two[1], full[1], rtol=1e-12)
+    cuts = [0, 0, 17, 128, 128, 299, 300]
+    parts = [oracle.attend(q, qpos, C[a:b], VC[a:b], 1e4) for a, b in zip(cuts[:-1], cuts[1:])]
+    parts.append(oracle.attend(q, qpos, U, VU, 1e4))
+    many = _merge(parts)
+    np.testing.assert_allclose(many[0], full[0], rtol=1e-12, atol=1e-13)
+
+
+# ------------------------------------------------------------- projection
+
+def _brute_project_row(h, e, add, WF, WKV, pos, L, Hkv, hd, theta):
+    """One row by plain Python loops, slicing the weights per (layer, K|V, head)."""
+    Dcat, d = len(h), WF.shape[0]
+    x = [h[c] + (e[c] if add else 0.0) for c in range(Dcat)]
+    z = [sum(WF[r][c] * x[c] for c in range(Dcat)) for r in range(d)]
+    K = np.zeros((L, Hkv, hd)); V = np.zeros((L, Hkv, hd))
+    for layer in range(L):
+        for kind in range(2):
+            for g in range(Hkv):
+                base = ((layer * 2 + kind) * Hkv + g) * hd
+                vec = [sum(WKV[base + t][r] * z[r] for r in range(d)) for t in range(hd)]
+                if kind == 0:
+                    half = hd // 2
+                    out = [0.0] * hd
+                    for i in range(half):
+                        ang = pos * theta ** (-2.0 * i / hd)
+                        out[i] = vec[i] * math.cos(ang) - vec[i + half] * math.sin(ang)
+                        out[i + half] = vec[i + half] * math.cos(ang) + vec[i] * math.sin(ang)
+                    K[layer, g] = out
+                else:
+                    V[layer, g] = vec
+    return K, V
+
+
+def test_project_matches_loop_brute_force():
+    L, Hkv, hd, Dcat, d = 2, 2, 8, 12, 6
+    M = 5
+    H = RNG.standard_normal((M, Dcat)); E = RNG.standard_normal(Dcat)
+    WF = RNG.standard_normal((d, Dcat)); WKV = RNG.standard_normal((2 * L * Hkv * hd, d))
+    add = np.array([0, 0, 1, 1, 1], bool)
+    pos = np.array([3, 4, 5, 6, 70])
+    K, V = oracle.project(H, E, add, WF, WKV, pos, L, Hkv, hd, 1e4)
+    for r in range(M):
+        bk, bv = _brute_project_row(H[r], E, add[r], WF, WKV, pos[r], L, Hkv, hd, 1e4)
+        np.testing.assert_allclose(K[r], bk, rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(V[r], bv, rtol=1e-12, atol=1e-12)
+
+
+def test_e_carry_placement_by_linearity():
+    """(carry K/V of a row) - (committed-path K/V of the same row and position)
+    = RoPE(W_K W_F E) and W_V W_F E; E = 0 makes them identical (Eq. 2)."""
+    L, Hkv, hd, Dcat, d = 2, 2, 16, 48, 32
+    H = RNG.standard_normal((4, Dcat)); E = RNG.standard_normal(Dcat)
+    WF = RNG.standard_normal((d, Dcat)); WKV = RNG.standard_normal((2 * L * Hkv * hd, d))
+    pos = np.array([10, 11, 12, 13])
+    kc, vc = oracle.project(H, E, np.ones(4, bool), WF, WKV, pos, L, Hkv, hd, 1e4)
+    k0, v0 = oracle.project(H, E, np.zeros(4, bool), WF, WKV, pos, L, Hkv, hd, 1e4)
+    fe = WF @ E
+    for layer in range(L):
+        for g in range(Hkv):
+            wk = WKV[((layer * 2 + 0) * Hkv + g) * hd:((layer * 2 + 0) * Hkv + g + 1) * hd]
+            wv = WKV[((layer * 2 + 1) * Hkv + g) * hd:((layer * 2 + 1) * Hkv + g + 1) * hd]
+            for r in range(4):
+                np.testing.assert_allclose(kc[r, layer, g] - k0[r, layer, g],
+                                           oracle.rope(wk @ fe, pos[r], 1e4), rtol=1e-9, atol=1e-9)
+                np.testing.assert_allclose(vc[r, layer, g] - v0[r, layer, g], wv @ fe,
+                                           rtol=1e-9, atol=1e-9)
+    kz, vz = oracle.project(H, np.zeros(Dcat), np.ones(4, bool), WF, WKV, pos, L, Hkv, hd, 1e4)
+    np.testing.assert_array_equal(kz, k0)
+    np.testing.assert_array_equal(vz, v0)
+
+
+# ------------------------------------------------------------------ route
+
+def test_route_recovers_constructed_accept_lengths_exhaustively():
+    """Tokens are built from a chosen m (draft == target on 0..m-1, differs at m);
+    greedy verification must return exactly m, for every m in 0..B."""
+    for B in (1, 4, 8, 16):
+        w = wl.TINY.replace(B=B, S=B + 1)
+        m = np.arange(B + 1, dtype=np.int32)
+        draft, target = wl.tokens_for(w, 0, m)
+        for s in range(B + 1):
+            assert oracle.accept_len(draft[s], target[s]) == m[s]
+
+
+def test_route_slots_and_lengths():
+    S, B, P = 3, 8, 10
+    pt = np.array([RNG.permutation(40)[:P] for _ in range(S)], np.int32)
+    m = np.array([0, 5, 8], np.int32)
+    w = wl.TINY.replace(B=B, S=S)
+    draft, target = wl.tokens_for(w, 0, m)
+    ctx = np.array([0, 37, 140], np.int32)
+    r = oracle.route(draft, target, ctx, np.array([3, 3, 3]), pt, 40)
+    np.testing.assert_array_equal(r["accept_len"], m)
+    np.testing.assert_array_equal(r["ctx_len"], ctx + m)
+    np.testing.assert_array_equal(r["carry_len"], B - m)
+    # physical slot of logical position t: page_table[t // 16] * 16 + t % 16, as a dense map
+    for s in range(S):
+        phys = np.concatenate([np.arange(16) + 16 * pt[s][p] for p in range(P)])
+        for j in range(B):
+            if j < m[s]:
+                assert r["row_dst"][s, j] == phys[ctx[s] + j]
+            else:
+                assert r["row_dst"][s, j] == -1 - (j - m[s])
+    rb = oracle.route(draft, target, ctx, np.array([3, 3, 3]), pt, 40, mode="baseline")
+    assert np.all(rb["carry_len"] == 0) and np.all(rb["row_dst"][1, 5:] == oracle.SKIP)
+    ra = oracle.route(draft, target, ctx, np.array([3, 3, 3]), pt, 40, mode="accept_all")
+    np.testing.assert_array_equal(ra["ctx_len"], ctx + B)
+
+
+def test_route_errors_leave_sequence_unchanged():
+    S, B, P = 3, 8, 4
+    pt = np.tile(np.arange(P, dtype=np.int32), (S, 1))
+    pt[2, 1] = 99                                    # out of the pool of 40 pages
+    w = wl.TINY.replace(B=B, S=S)
+    draft, target = wl.tokens_for(w, 0, np.array([8, 8, 8], np.int32))
+    ctx = np.array([P * 16 - B + 1, -1, 10], np.int32)
+    r = oracle.route(draft, target, ctx, np.array([2, 2, 2]), pt, 40)
+    assert list(r["status"]) == [oracle.ERR_CAPACITY, oracle.ERR_LENGTH, oracle.ERR_PAGE_RANGE]
+    np.testing.assert_array_equal(r["ctx_len"], ctx)
+    np.testing.assert_array_equal(r["carry_len"], [2, 2, 2])
+    assert np.all(r["row_dst"] == oracle.SKIP)
+
+
+# ------------------------------------------------------------ whole rounds
+
+def _tiny_setup(S=2, B=4, Dcat=12, d=8, L=2, Hq=4, Hkv=2, hd=8, seed=7):
+    rng = np.random.default_rng(seed)
+    return dict(S=S, B=B, Dcat=Dcat, d=d, L=L, Hq=Hq, Hkv=Hkv, hd=hd,
+                WF=rng.standard_normal((d, Dcat)) * 0.3,
+                WKV=rng.standard_normal((2 * L * Hkv * hd, d)) * 0.3,
+                E=rng.standard_normal(Dcat), rng=rng)
+
+
+def _run_incremental(t, ctx0_h, rounds, mode="carry", poison=False):
+    """Drive the oracle through rounds; returns per-round (route, O, LSE)."""
+    S, B, L, Hkv, hd, Hq = t["S"], t["B"], t["L"], t["Hkv"], t["hd"], t["Hq"]
+    st = oracle.State(S, L, Hkv, hd)
+    pt = np.tile(np.arange(64, dtype=np.int32), (S, 1))
+    for s in range(S):
+        n = len(ctx0_h[s])
+        k, v = oracle.project(ctx0_h[s], t["E"], np.zeros(n, bool), t["WF"], t["WKV"],
+                              np.arange(n), L, Hkv, hd, 1e4)
+        st.commit_and_replace(s, k, v, k[:0], v[:0])
+    outs = []
+    for rnd in rounds:
+        if poison:
+            for s in range(S):
+                st.uk[s][:] = np.nan
+                st.uv[s][:] = np.nan
+        r = oracle.route(rnd["draft"], rnd["target"], st.ctx_len(), st.carry_len(), pt, 64, mode)
+        oracle.round_update(st, r, rnd["H"], t["E"], t["WF"], t["WKV"], 1e4, mode)
+        O, LSE = oracle.attend_state(st, rnd["Q"], Hq, 1e4)
+        outs.append((r, O, LSE, st.ctx_len(), st.carry_len()))
+    return outs
+
+
+def _make_rounds(t, n_rounds, ms):
+    S, B, Dcat, L, Hq, hd = t["S"], t["B"], t["Dcat"], t["L"], t["Hq"], t["hd"]
+    rng = t["rng"]
+    out = []
+    for r in range(n_rounds):
+        m = np.array(ms[r], np.int32)
+        target = rng.integers(0, 50, (S, B))
+        draft = target.copy()
+        for s in range(S):
+            if m[s] < B:
+                draft[s, m[s]] = (target[s, m[s]] + 1) % 50
+        out.append(dict(draft=draft, target=target, m=m,
+                        H=rng.standard_normal((S, B, Dcat)),
+                        Q=rng.standard_normal((L, S, B, Hq, hd))))
+    return out
+
+
+def _brute_force_rounds(t, ctx0_h, rounds):
+    """Full-history recomputation: every round, re-project every row ever
+    committed from its stored state and position, plus the current carried rows,
+    then attend with a dense mask over all rows ever seen and an unshifted exp."""
+    S, B, L, Hkv, hd, Hq = t["S"], t["B"], t["L"], t["Hkv"], t["hd"], t["Hq"]
+    G = Hq // Hkv
+    hist = [[(ctx0_h[s][j], j, "acc", -1) for j in range(len(ctx0_h[s]))] for s in range(S)]
+    res = []
+    for ri, rnd in enumerate(rounds):
+        for s in range(S):
+            p0 = sum(1 for h in hist[s] if h[2] == "acc")
+            m = 0
+            while m < B and rnd["draft"][s][m] == rnd["target"][s][m]:
+                m += 1
+            for j in range(B):
+                hist[s].append((rnd["H"][s][j], p0 + j, "acc" if j < m else "rej", ri))
+        O = np.zeros((L, S, B, Hq, hd)); LSE = np.zeros((L, S, B, Hq))
+        for s in range(S):
+            rows = hist[s]
+            ctx = sum(1 for h in rows if h[2] == "acc")
+            # a row is visible iff committed, or rejected in *this* round
+            vis = [h[2] == "acc" or h[3] == ri for h in rows]
+            KV = [_brute_project_row(h[0], t["E"], h[2] == "rej", t["WF"], t["WKV"], h[1], L,
+                                     Hkv, hd, 1e4) for h in rows]
+            for layer in range(L):
+                for i in range(B):
+                    for h in range(Hq):
+                        g = h // G
+                        q = rnd["Q"][layer, s, i, h]
+                        qp = ctx + i
+                        half = hd // 2
+                        rq = np.zeros(hd)
+                        for a in range(half):
+                            ang = qp * 1e4 ** (-2.0 * a / hd)
+                            rq[a] = q[a] * math.cos(ang) - q[a + half] * math.sin(ang)
+                            rq[a + half] = q[a + half] * math.cos(ang) + q[a] * math.sin(ang)
+                        num = np.zeros(hd); den = 0.0
+                        for kvr, ok in zip(KV, vis):
+                            if not ok:
+                                continue
+                            wgt = math.exp(float(rq @ kvr[0][layer, g]) / math.sqrt(hd))
+                            num += wgt * kvr[1][layer, g]
+                            den += wgt
+                        O[layer, s, i, h] = num / den
+                        LSE[layer, s, i, h] = math.log(den)
+        res.append((O, LSE))
+    return res
+
+
+def test_whole_rounds_match_full_history_brute_force():
+    t = _tiny_setup()
+    ctx0 = [t["rng"].standard_normal((n, t["Dcat"])) for n in (3, 6)]
+    ms = [[1, 4], [0, 2], [4, 0], [2, 3], [4, 4], [3, 1]]
+    rounds = _make_rounds(t, 6, ms)
+    inc = _run_incremental(t, ctx0, rounds)
+    bf = _brute_force_rounds(t, ctx0, rounds)
+    for r, (a, b) in enumerate(zip(inc, bf)):
+        np.testing.assert_array_equal(a[0]["accept_len"], ms[r])
+        np.testing.assert_allclose(a[1], b[0], rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(a[2], b[1], rtol=1e-12, atol=1e-12)
+
+
+def test_lengths_over_a_chain():
+    t = _tiny_setup(B=4)
+    ctx0 = [t["rng"].standard_normal((n, t["Dcat"])) for n in (2, 5)]
+    ms = t["rng"].integers(0, 5, (12, 2))
+    outs = _run_incremental(t, ctx0, _make_rounds(t, 12, ms))
+    for r, o in enumerate(outs):
+        np.testing.assert_array_equal(o[3], np.array([2, 5]) + ms[: r + 1].sum(0))
+        np.testing.assert_array_equal(o[4], 4 - ms[r])
+        assert np.all(o[4] <= 4)
+
+
+def test_zero_rejected_equals_baseline_exactly():
+    t = _tiny_setup()
+    ctx0 = [t["rng"].standard_normal((n, t["Dcat"])) for n in (3, 6)]
+    rounds = _make_rounds(t, 4, [[4, 4]] * 4)
+    a = _run_incremental(t, ctx0, rounds, "carry")
+    b = _run_incremental(t, ctx0, rounds, "baseline")
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x[1], y[1])
+        np.testing.assert_array_equal(x[2], y[2])
+        assert np.all(x[4] == 0)
+
+
+def test_carry_segment_is_replaced_never_read_stale():
+    t = _tiny_setup()
+    ctx0 = [t["rng"].standard_normal((n, t["Dcat"])) for n in (3, 6)]
+    rounds = _make_rounds(t, 5, [[1, 2], [0, 4], [3, 1], [2, 2], [0, 0]])
+    a = _run_incremental(t, ctx0, rounds, "carry", poison=False)
+    b = _run_incremental(t, ctx0, rounds, "carry", poison=True)
+    for x, y in zip(a, b):
+        assert np.all(np.isfinite(y[1]))
+        np.testing.assert_array_equal(x[1], y[1])
+
+
+def test_baseline_differs_when_rows_are_rejected():
+    t = _tiny_setup()
+    ctx0 = [t["rng"].standard_normal((n, t["Dcat"])) for n in (3, 6)]
+    rounds = _make_rounds(t, 2, [[1, 2], [0, 3]])
+    a = _run_incremental(t, ctx0, rounds, "carry")
+    b = _run_incremental(t, ctx0, rounds, "baseline")
+    assert np.abs(a[0][1] - b[0][1]).max() > 1e-3
