@@ -1,0 +1,215 @@
+/*
+ * carryover.h -- C ABI of the Carryover drafter step on MI355X (gfx950).
+ *
+ * One drafting round of a block-diffusion speculative drafter with Carryover
+ * (paper: Section 2.1, Eqs. 1-2; Appendix A, Algorithm 1 and its "Cache
+ * semantics" paragraph):
+ *
+ *   route      split each verified window of B rows by its accepted prefix m
+ *              (greedy verification, Section 2 "Preliminaries");
+ *   project    x = h (+ E_carry on rejected rows), z = F x, and for every
+ *              drafter layer l: k = K_l z, v = V_l z; keys are rotated once at
+ *              the row's absolute position; accepted rows are appended to the
+ *              paged committed cache C_l, rejected rows replace the carryover
+ *              segment U_l (at most B rows);
+ *   attention  the next block's queries attend to ctx_l = [C_l ; U_l].
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Ownership: every pointer is caller-owned device memory unless a comment says
+ *   "host".  The library allocates nothing, frees nothing, keeps no pointer
+ *   past the call and holds no global state besides per-device attributes.
+ * Streams: every call only enqueues work on `stream` and returns; nothing
+ *   synchronises except carryover_read_status.  Calls on distinct states are
+ *   re-entrant.
+ * Errors: problems visible on the host (null or misaligned pointer,
+ *   unsupported shape or dtype, small workspace) return a non-zero co_status
+ *   and enqueue nothing.  Problems that depend on device-resident data
+ *   (capacity, page ids, negative lengths) are written to *state->status
+ *   (first error wins); the offending sequence is left unchanged and the other
+ *   sequences proceed.  The caller zeroes *status before first use.
+ * Dtype: one element type per call for hidden states, weights, queries,
+ *   caches and outputs (dims.dtype).  Accumulation, softmax and the optional
+ *   LSE output are fp32.
+ * Supported shapes: head_dim in {64, 128}; page_size == 16; num_q_heads a
+ *   multiple of num_kv_heads with block * (num_q_heads / num_kv_heads) <= 64;
+ *   feat_dim and model_dim multiples of 64; block >= 1.
+ *
+ * Memory layouts (row-major, innermost last; P = page_size = 16,
+ * CP = ceil(block / 16), NKV = 2 * num_layers * num_kv_heads * head_dim):
+ *   hidden      [num_seqs][block][feat_dim]         target features H, Eq. 1
+ *   w_f         [model_dim][feat_dim]               fusion projection F
+ *   w_kv        [NKV][model_dim], rows ordered (layer, K|V, kv head, dim)
+ *   e_carry     [feat_dim]                          E_carry, Eq. 2
+ *   q           [layers][num_seqs][block][num_q_heads][head_dim], un-rotated
+ *   out         same shape as q
+ *   lse         [layers][num_seqs][block][num_q_heads] fp32, natural log
+ *   page_table  int32 [num_seqs][max_pages_per_seq]
+ *   k_cache     [num_layers][num_pages][num_kv_heads][P][head_dim]
+ *   v_cache     [num_layers][num_pages][num_kv_heads][head_dim][P]  (slot fastest)
+ *   k_carry     [num_layers][num_seqs][CP][num_kv_heads][P][head_dim]
+ *   v_carry     [num_layers][num_seqs][CP][num_kv_heads][head_dim][P]
+ * Logical position t of sequence s lives in page page_table[s][t / 16], slot
+ * t % 16.  Carry row r of sequence s lives in carry page r / 16, slot r % 16.
+ */
+#ifndef CARRYOVER_H
+#define CARRYOVER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* hipStream_t;
+
+typedef int32_t co_status;
+enum {
+  CO_OK = 0,
+  CO_ERR_INVALID_ARG = 1,   /* null/misaligned pointer, negative count        */
+  CO_ERR_UNSUPPORTED = 2,   /* shape or dtype outside the supported set        */
+  CO_ERR_WORKSPACE = 3,     /* workspace smaller than carryover_workspace_bytes */
+  CO_ERR_CAPACITY = 4,      /* device: ctx_len + block > max_pages_per_seq * 16 */
+  CO_ERR_PAGE_RANGE = 5,    /* device: page id outside [0, num_pages)          */
+  CO_ERR_HIP = 6,           /* a HIP runtime call or launch failed             */
+  CO_ERR_LENGTH = 7         /* device: ctx_len outside [0, max_pages_per_seq * 16] or
+                               carry_len outside [0, 16 * ceil(block / 16)]        */
+};
+
+enum { CO_DTYPE_F32 = 0, CO_DTYPE_BF16 = 1 };
+
+/* flags */
+#define CO_BASELINE_MODE    (1u << 0) /* Algorithm 1 left column: commit 0..m-1, no carry      */
+#define CO_ROUTE_ACCEPT_ALL (1u << 1) /* m := block for every sequence (build context)         */
+#define CO_ROUTE_CARRY_ONLY (1u << 2) /* rows 0..m-1 are already committed: store only carries */
+#define CO_Q_PREROTATED     (1u << 3) /* queries already carry their rotary embedding          */
+
+typedef struct co_dims {
+  int32_t num_seqs;           /* S: sequences in the batch                           */
+  int32_t block;              /* B: verified-window rows = block queries per sequence */
+  int32_t feat_dim;           /* width of a concatenated target feature row h        */
+  int32_t model_dim;          /* d: width of F's output                              */
+  int32_t num_layers;         /* L: drafter layers                                   */
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t page_size;          /* must be 16                                          */
+  int32_t max_pages_per_seq;  /* columns of page_table                               */
+  int32_t num_pages;          /* pages in the cache pool                             */
+  int32_t dtype;              /* CO_DTYPE_F32 or CO_DTYPE_BF16                       */
+  float rope_theta;           /* rotary base; inverse frequency theta^(-2i/head_dim) */
+} co_dims;
+
+typedef struct co_weights {
+  const void* w_f;            /* F:  [model_dim][feat_dim]                 */
+  const void* w_kv;           /* K_l, V_l of all layers: [NKV][model_dim]  */
+  const void* e_carry;        /* E_carry: [feat_dim]                       */
+} co_weights;
+
+typedef struct co_state {
+  int32_t* ctx_len;           /* [num_seqs] committed rows |C_l|           */
+  int32_t* carry_len;         /* [num_seqs] carryover rows |U_l| <= block  */
+  const int32_t* page_table;  /* [num_seqs][max_pages_per_seq]             */
+  void* k_cache;
+  void* v_cache;
+  void* k_carry;
+  void* v_carry;
+  int32_t* status;            /* one int32: first data-dependent error     */
+} co_state;
+
+typedef struct co_route {
+  int32_t* accept_len;        /* [num_seqs] m                                              */
+  int32_t* row_pos;           /* [num_seqs][block] absolute position of window row j       */
+  int32_t* row_dst;           /* [num_seqs][block] >= 0: global committed slot page*16+t%16;
+                                 -1-r: carry row r; INT32_MIN: not stored                   */
+} co_route;
+
+/*
+ * Route (Algorithm 1 "Given"; greedy verification, Section 2
+ * "Preliminaries").  For every sequence s: m = length of the longest prefix on
+ * which draft_tok[s][:] equals target_tok[s][:] (m = block with
+ * CO_ROUTE_ACCEPT_ALL, where the token pointers may be NULL); p0 = ctx_len[s];
+ * window row j sits at position p0 + j.  Rows j < m go to the committed slot of
+ * position p0 + j (skipped under CO_ROUTE_CARRY_ONLY); rows j >= m become carry
+ * row j - m (skipped under CO_BASELINE_MODE).  Then ctx_len[s] = p0 + m and
+ * carry_len[s] = block - m (0 in baseline mode), which replaces the old
+ * carryover segment.  Tokens: int32 [num_seqs][block], device.
+ * Device errors: CO_ERR_LENGTH (p0 < 0), CO_ERR_CAPACITY
+ * (p0 + block > max_pages_per_seq * 16), CO_ERR_PAGE_RANGE (a committed row's
+ * page id outside [0, num_pages)); the sequence then keeps its lengths, stores
+ * nothing (row_dst = INT32_MIN) and reports accept_len 0.
+ */
+co_status carryover_route(const co_dims* dims, const int32_t* draft_tok, const int32_t* target_tok,
+                          uint32_t flags, co_state* state, const co_route* out, hipStream_t stream);
+
+/*
+ * Project (Eq. 1, Eq. 2; Algorithm 1 Carryover steps 1-6; "Cache semantics").
+ * For every window row r = s * block + j described by `route`:
+ * x = hidden[r] (+ e_carry when row_dst[r] names a carry row, Eq. 2), z = F x,
+ * and for every layer l and KV head g: k = K_{l,g} z rotated at row_pos[r],
+ * v = V_{l,g} z; the row is written to its committed slot or carry row in
+ * every layer, or dropped when row_dst[r] == INT32_MIN.  F, K_l, V_l have no
+ * bias and no normalisation.  `ws` must hold
+ * carryover_workspace_bytes(dims, CO_WS_PROJECT) bytes (256-byte aligned).
+ */
+co_status carryover_project_kv(const co_dims* dims, const co_weights* w, const void* hidden,
+                               const co_route* route, const co_state* state, void* ws,
+                               size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Block attention over ctx_l = [C_l ; U_l] (Eq. 2; Algorithm 1 step 7;
+ * "Preliminaries": draft positions attend to KV built from target states).
+ * For layers layer_begin .. layer_begin + layer_count - 1, every sequence s,
+ * block query i and query head h: the query q[l'][s][i][h] (l' = l -
+ * layer_begin) is rotated at position ctx_len[s] + i (unless
+ * CO_Q_PREROTATED), scaled by 1/sqrt(head_dim) and attends, with no position
+ * mask, to the ctx_len[s] committed keys of KV head h / (num_q_heads /
+ * num_kv_heads) followed by its carry_len[s] carry keys.  out has q's layout;
+ * lse (optional, may be NULL) receives the natural-log normaliser.  An empty
+ * key set gives out = 0 and lse = -inf.  `ws` must hold
+ * carryover_workspace_bytes(dims, CO_WS_ATTENTION) bytes.
+ */
+co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int32_t layer_count,
+                                  const void* q, const co_state* state, void* out, float* lse,
+                                  uint32_t flags, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * One full drafter round (Algorithm 1, Carryover column, or the Baseline
+ * column with CO_BASELINE_MODE): route, project all layers, then attend with
+ * every layer's queries q [num_layers][num_seqs][block][num_q_heads][head_dim].
+ * `scratch` receives the route result.  All state stays on the device; there
+ * is no host synchronisation.  `ws`: carryover_workspace_bytes(dims, CO_WS_ROUND).
+ */
+co_status carryover_round(const co_dims* dims, const co_weights* w, const void* hidden,
+                          const int32_t* draft_tok, const int32_t* target_tok, const void* q,
+                          co_state* state, const co_route* scratch, void* out, float* lse,
+                          uint32_t flags, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Write already-projected (keys already rotated) committed rows of one
+ * sequence into the paged cache: k_rows, v_rows [num_layers][num_kv_heads]
+ * [n_rows][head_dim] are stored at positions pos0 .. pos0 + n_rows - 1 of
+ * sequence `seq`.  Lengths are not changed.  Host errors: seq or positions
+ * outside the table (CO_ERR_INVALID_ARG); device: CO_ERR_PAGE_RANGE.
+ */
+co_status carryover_import_kv(const co_dims* dims, int32_t seq, int32_t pos0, int32_t n_rows,
+                              const void* k_rows, const void* v_rows, const co_state* state,
+                              hipStream_t stream);
+
+enum { CO_WS_PROJECT = 0, CO_WS_ATTENTION = 1, CO_WS_ROUND = 2 };
+
+/* Workspace bytes a call needs for these dims (0 on unsupported dims). */
+size_t carryover_workspace_bytes(const co_dims* dims, int32_t which);
+
+/* Synchronise `stream` and copy *state->status to *host_out (host pointer). */
+co_status carryover_read_status(const co_state* state, int32_t* host_out, hipStream_t stream);
+
+/* Static message for a status code. */
+const char* carryover_status_string(co_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CARRYOVER_H */

@@ -1,0 +1,229 @@
+"""Python binding of libcarryover (the Carryover drafter step on MI355X).
+
+Argument marshalling only: every step runs in the library's HIP kernels.
+PyTorch supplies device memory and streams.  The entry points have the names
+and meaning of the C ABI in ``include/carryover.h``; each takes torch tensors
+(or raw device pointers) and an optional stream, and raises ``CarryoverError``
+on a non-zero status.  There is no CPU fallback: importing works anywhere, but
+every call needs the built library and a GPU.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libcarryover.so")
+
+CO_OK, CO_ERR_INVALID_ARG, CO_ERR_UNSUPPORTED, CO_ERR_WORKSPACE = 0, 1, 2, 3
+CO_ERR_CAPACITY, CO_ERR_PAGE_RANGE, CO_ERR_HIP, CO_ERR_LENGTH = 4, 5, 6, 7
+CO_DTYPE_F32, CO_DTYPE_BF16 = 0, 1
+CO_BASELINE_MODE, CO_ROUTE_ACCEPT_ALL, CO_ROUTE_CARRY_ONLY, CO_Q_PREROTATED = 1, 2, 4, 8
+CO_WS_PROJECT, CO_WS_ATTENTION, CO_WS_ROUND = 0, 1, 2
+SKIP = -(2 ** 31)
+PAGE = 16
+
+
+class CarryoverError(RuntimeError):
+    def __init__(self, code, where):
+        self.code = code
+        super().__init__(f"{where}: {status_string(code)} ({code})")
+
+
+class co_dims(ctypes.Structure):
+    _fields_ = [("num_seqs", ctypes.c_int32), ("block", ctypes.c_int32),
+                ("feat_dim", ctypes.c_int32), ("model_dim", ctypes.c_int32),
+                ("num_layers", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("max_pages_per_seq", ctypes.c_int32),
+                ("num_pages", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("rope_theta", ctypes.c_float)]
+
+
+class co_weights(ctypes.Structure):
+    _fields_ = [("w_f", ctypes.c_void_p), ("w_kv", ctypes.c_void_p), ("e_carry", ctypes.c_void_p)]
+
+
+class co_state(ctypes.Structure):
+    _fields_ = [("ctx_len", ctypes.c_void_p), ("carry_len", ctypes.c_void_p),
+                ("page_table", ctypes.c_void_p), ("k_cache", ctypes.c_void_p),
+                ("v_cache", ctypes.c_void_p), ("k_carry", ctypes.c_void_p),
+                ("v_carry", ctypes.c_void_p), ("status", ctypes.c_void_p)]
+
+
+class co_route(ctypes.Structure):
+    _fields_ = [("accept_len", ctypes.c_void_p), ("row_pos", ctypes.c_void_p),
+                ("row_dst", ctypes.c_void_p)]
+
+
+_lib = None
+_P = ctypes.POINTER
+_v = ctypes.c_void_p
+
+
+def lib():
+    """The loaded shared library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2609_14717_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        sig = {
+            "carryover_route": [_P(co_dims), _v, _v, ctypes.c_uint32, _P(co_state), _P(co_route), _v],
+            "carryover_project_kv": [_P(co_dims), _P(co_weights), _v, _P(co_route), _P(co_state),
+                                     _v, ctypes.c_size_t, _v],
+            "drafter_block_attention": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, _v,
+                                        _P(co_state), _v, _v, ctypes.c_uint32, _v, ctypes.c_size_t,
+                                        _v],
+            "carryover_round": [_P(co_dims), _P(co_weights), _v, _v, _v, _v, _P(co_state),
+                                _P(co_route), _v, _v, ctypes.c_uint32, _v, ctypes.c_size_t, _v],
+            "carryover_import_kv": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _v,
+                                    _v, _P(co_state), _v],
+            "carryover_workspace_bytes": [_P(co_dims), ctypes.c_int32],
+            "carryover_read_status": [_P(co_state), _P(ctypes.c_int32), _v],
+            "carryover_status_string": [ctypes.c_int32],
+        }
+        for name, args in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = ctypes.c_int32
+        L.carryover_workspace_bytes.restype = ctypes.c_size_t
+        L.carryover_status_string.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+EXPORTED = ("carryover_route", "carryover_project_kv", "drafter_block_attention",
+            "carryover_round", "carryover_import_kv", "carryover_workspace_bytes",
+            "carryover_read_status", "carryover_status_string")
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(rc, where):
+    if rc != CO_OK:
+        raise CarryoverError(rc, where)
+
+
+def status_string(code: int) -> str:
+    return lib().carryover_status_string(code).decode()
+
+
+def make_dims(S, B, Dcat, d, L, Hq, Hkv, hd, max_pages_per_seq, num_pages, dtype, theta):
+    return co_dims(S, B, Dcat, d, L, Hq, Hkv, hd, PAGE, max_pages_per_seq, num_pages,
+                   CO_DTYPE_BF16 if dtype in ("bf16", CO_DTYPE_BF16) else CO_DTYPE_F32,
+                   float(theta))
+
+
+def weights(w_f, w_kv, e_carry):
+    return co_weights(_ptr(w_f), _ptr(w_kv), _ptr(e_carry))
+
+
+def state(t):
+    """co_state over a dict of tensors (see ``alloc_state``)."""
+    return co_state(_ptr(t["ctx_len"]), _ptr(t["carry_len"]), _ptr(t["page_table"]),
+                    _ptr(t["k_cache"]), _ptr(t["v_cache"]), _ptr(t["k_carry"]),
+                    _ptr(t["v_carry"]), _ptr(t["status"]))
+
+
+def route(t):
+    return co_route(_ptr(t["accept_len"]), _ptr(t["row_pos"]), _ptr(t["row_dst"]))
+
+
+def workspace_bytes(dims, which=CO_WS_ROUND) -> int:
+    return lib().carryover_workspace_bytes(ctypes.byref(dims), which)
+
+
+def alloc_state(dims, page_table, device="cuda"):
+    """Zero-initialised device buffers for one drafter state (layouts of carryover.h)."""
+    import torch
+    dt = torch.bfloat16 if dims.dtype == CO_DTYPE_BF16 else torch.float32
+    L, Hkv, hd, S = dims.num_layers, dims.num_kv_heads, dims.head_dim, dims.num_seqs
+    CP = -(-dims.block // PAGE)
+    pt = torch.as_tensor(page_table, dtype=torch.int32).to(device).contiguous()
+    assert tuple(pt.shape) == (S, dims.max_pages_per_seq)
+    return dict(
+        ctx_len=torch.zeros(S, dtype=torch.int32, device=device),
+        carry_len=torch.zeros(S, dtype=torch.int32, device=device),
+        page_table=pt,
+        k_cache=torch.zeros((L, dims.num_pages, Hkv, PAGE, hd), dtype=dt, device=device),
+        v_cache=torch.zeros((L, dims.num_pages, Hkv, hd, PAGE), dtype=dt, device=device),
+        k_carry=torch.zeros((L, S, CP, Hkv, PAGE, hd), dtype=dt, device=device),
+        v_carry=torch.zeros((L, S, CP, Hkv, hd, PAGE), dtype=dt, device=device),
+        status=torch.zeros(1, dtype=torch.int32, device=device),
+    )
+
+
+def alloc_route(S, B, device="cuda"):
+    import torch
+    return dict(accept_len=torch.zeros(S, dtype=torch.int32, device=device),
+                row_pos=torch.zeros((S, B), dtype=torch.int32, device=device),
+                row_dst=torch.zeros((S, B), dtype=torch.int32, device=device))
+
+
+# ---------------------------------------------------------------- entry points
+
+def carryover_route(dims, draft_tok, target_tok, flags, st, rt, stream=None):
+    s, r = state(st), route(rt)
+    _check(lib().carryover_route(ctypes.byref(dims), _ptr(draft_tok), _ptr(target_tok), flags,
+                                 ctypes.byref(s), ctypes.byref(r), _stream(stream)),
+           "carryover_route")
+
+
+def carryover_project_kv(dims, w, hidden, rt, st, ws, stream=None, ws_bytes=None):
+    s, r = state(st), route(rt)
+    nb = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    _check(lib().carryover_project_kv(ctypes.byref(dims), ctypes.byref(w), _ptr(hidden),
+                                      ctypes.byref(r), ctypes.byref(s), _ptr(ws), nb,
+                                      _stream(stream)), "carryover_project_kv")
+
+
+def drafter_block_attention(dims, layer_begin, layer_count, q, st, out, lse, flags, ws,
+                            stream=None, ws_bytes=None):
+    s = state(st)
+    nb = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    _check(lib().drafter_block_attention(ctypes.byref(dims), layer_begin, layer_count, _ptr(q),
+                                         ctypes.byref(s), _ptr(out), _ptr(lse), flags, _ptr(ws),
+                                         nb, _stream(stream)), "drafter_block_attention")
+
+
+def carryover_round(dims, w, hidden, draft_tok, target_tok, q, st, rt, out, lse, flags, ws,
+                    stream=None, ws_bytes=None):
+    s, r = state(st), route(rt)
+    nb = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    _check(lib().carryover_round(ctypes.byref(dims), ctypes.byref(w), _ptr(hidden),
+                                 _ptr(draft_tok), _ptr(target_tok), _ptr(q), ctypes.byref(s),
+                                 ctypes.byref(r), _ptr(out), _ptr(lse), flags, _ptr(ws), nb,
+                                 _stream(stream)), "carryover_round")
+
+
+def carryover_import_kv(dims, seq, pos0, k_rows, v_rows, st, stream=None):
+    s = state(st)
+    n = k_rows.shape[2]
+    _check(lib().carryover_import_kv(ctypes.byref(dims), seq, pos0, n, _ptr(k_rows),
+                                     _ptr(v_rows), ctypes.byref(s), _stream(stream)),
+           "carryover_import_kv")
+
+
+def carryover_read_status(st, stream=None) -> int:
+    s = state(st)
+    out = ctypes.c_int32(0)
+    _check(lib().carryover_read_status(ctypes.byref(s), ctypes.byref(out), _stream(stream)),
+           "carryover_read_status")
+    return out.value

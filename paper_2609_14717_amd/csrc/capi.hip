@@ -1,0 +1,273 @@
+// C ABI of libcarryover: argument validation, workspace planning and launches.
+// Every entry point validates what the host can see, then only enqueues work on
+// the caller's stream.
+#include <math.h>
+#include <string.h>
+
+#include "co_kernels.h"
+
+using namespace co;
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+int g_num_cus[kMaxDevices];   // per-device compute-unit count, filled on first use
+
+int num_cus() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+  if (g_num_cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    g_num_cus[dev] = n;
+  }
+  return g_num_cus[dev];
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+co_status check_dims(const co_dims* d) {
+  if (!d) return CO_ERR_INVALID_ARG;
+  if (d->num_seqs < 0 || d->block < 1 || d->num_layers < 1 || d->num_kv_heads < 1 ||
+      d->num_q_heads < 1 || d->max_pages_per_seq < 1 || d->num_pages < 1 || d->feat_dim < 1 ||
+      d->model_dim < 1)
+    return CO_ERR_INVALID_ARG;
+  if (!(d->rope_theta > 0.f)) return CO_ERR_INVALID_ARG;
+  if (d->page_size != kPage) return CO_ERR_UNSUPPORTED;
+  if (d->dtype != CO_DTYPE_F32 && d->dtype != CO_DTYPE_BF16) return CO_ERR_UNSUPPORTED;
+  if (d->head_dim != 64 && d->head_dim != 128) return CO_ERR_UNSUPPORTED;
+  if (d->num_q_heads % d->num_kv_heads) return CO_ERR_UNSUPPORTED;
+  if (d->feat_dim % 64 || d->model_dim % 64) return CO_ERR_UNSUPPORTED;
+  if (static_cast<int64_t>(d->num_seqs) * d->block > INT32_MAX / 2) return CO_ERR_UNSUPPORTED;
+  return CO_OK;
+}
+
+co_status check_attention_dims(const co_dims* d) {
+  const int nq = d->block * (d->num_q_heads / d->num_kv_heads);
+  return nq > 64 ? CO_ERR_UNSUPPORTED : CO_OK;
+}
+
+size_t elem_bytes(const co_dims* d) { return d->dtype == CO_DTYPE_BF16 ? 2 : 4; }
+
+int carry_pages(const co_dims* d) { return (d->block + kPage - 1) / kPage; }
+
+KvDest make_dest(const co_dims* d, const co_route* rt, const co_state* st) {
+  KvDest e{};
+  e.S = d->num_seqs;
+  e.B = d->block;
+  e.L = d->num_layers;
+  e.Hkv = d->num_kv_heads;
+  e.hd = d->head_dim;
+  e.num_pages = d->num_pages;
+  e.CP = carry_pages(d);
+  e.log2_theta = log2(static_cast<double>(d->rope_theta));
+  e.row_pos = rt ? rt->row_pos : nullptr;
+  e.row_dst = rt ? rt->row_dst : nullptr;
+  e.k_cache = st->k_cache;
+  e.v_cache = st->v_cache;
+  e.k_carry = st->k_carry;
+  e.v_carry = st->v_carry;
+  e.status = st->status;
+  return e;
+}
+
+bool state_ok(const co_state* st) {
+  return st && st->ctx_len && st->carry_len && st->page_table && st->k_cache && st->v_cache &&
+         st->k_carry && st->v_carry && st->status && aligned(st->k_cache, 16) &&
+         aligned(st->v_cache, 16) && aligned(st->k_carry, 16) && aligned(st->v_carry, 16);
+}
+
+bool route_ok(const co_route* rt) { return rt && rt->accept_len && rt->row_pos && rt->row_dst; }
+
+ProjectPlan project_plan(const co_dims* d) {
+  return plan_project(d->num_seqs * d->block, d->feat_dim, d->model_dim,
+                      2 * d->num_layers * d->num_kv_heads * d->head_dim, d->dtype, num_cus());
+}
+
+AttnPlan attention_plan(const co_dims* d) {
+  return plan_attention(d->num_seqs, d->block, d->num_layers, d->num_q_heads, d->num_kv_heads,
+                        d->head_dim, d->max_pages_per_seq, d->dtype);
+}
+
+co_status hip_status(hipError_t e) { return e == hipSuccess ? CO_OK : CO_ERR_HIP; }
+
+co_status do_attention(const co_dims* d, int32_t layer_begin, int32_t layer_count, const void* q,
+                       const co_state* st, void* out, float* lse, uint32_t flags, void* ws,
+                       hipStream_t stream) {
+  AttnArgs a{};
+  a.S = d->num_seqs;
+  a.B = d->block;
+  a.L = d->num_layers;
+  a.layer_begin = layer_begin;
+  a.Hq = d->num_q_heads;
+  a.Hkv = d->num_kv_heads;
+  a.hd = d->head_dim;
+  a.num_pages = d->num_pages;
+  a.max_pages = d->max_pages_per_seq;
+  a.CP = carry_pages(d);
+  a.dtype = d->dtype;
+  a.flags = flags;
+  a.log2_theta = log2(static_cast<double>(d->rope_theta));
+  a.q = q;
+  a.ctx_len = st->ctx_len;
+  a.carry_len = st->carry_len;
+  a.page_table = st->page_table;
+  a.k_cache = st->k_cache;
+  a.v_cache = st->v_cache;
+  a.k_carry = st->k_carry;
+  a.v_carry = st->v_carry;
+  a.out = out;
+  a.lse = lse;
+  a.status = st->status;
+  a.ws = static_cast<float*>(ws);
+  return hip_status(launch_attention(a, attention_plan(d), layer_count, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t carryover_workspace_bytes(const co_dims* dims, int32_t which) {
+  if (check_dims(dims) != CO_OK) return 0;
+  const size_t pw = project_plan(dims).total;
+  const size_t aw = check_attention_dims(dims) == CO_OK ? attention_plan(dims).bytes : 0;
+  switch (which) {
+    case CO_WS_PROJECT: return pw;
+    case CO_WS_ATTENTION: return aw;
+    case CO_WS_ROUND: return pw > aw ? pw : aw;
+    default: return 0;
+  }
+}
+
+co_status carryover_route(const co_dims* dims, const int32_t* draft_tok, const int32_t* target_tok,
+                          uint32_t flags, co_state* state, const co_route* out,
+                          hipStream_t stream) {
+  co_status s = check_dims(dims);
+  if (s != CO_OK) return s;
+  if (!state || !state->ctx_len || !state->carry_len || !state->page_table || !state->status ||
+      !route_ok(out))
+    return CO_ERR_INVALID_ARG;
+  if (!(flags & CO_ROUTE_ACCEPT_ALL) && (!draft_tok || !target_tok)) return CO_ERR_INVALID_ARG;
+  RouteArgs a{};
+  a.S = dims->num_seqs;
+  a.B = dims->block;
+  a.max_pages = dims->max_pages_per_seq;
+  a.num_pages = dims->num_pages;
+  a.flags = flags;
+  a.draft = draft_tok;
+  a.target = target_tok;
+  a.ctx_len = state->ctx_len;
+  a.carry_len = state->carry_len;
+  a.page_table = state->page_table;
+  a.accept_len = out->accept_len;
+  a.row_pos = out->row_pos;
+  a.row_dst = out->row_dst;
+  a.status = state->status;
+  return hip_status(launch_route(a, stream));
+}
+
+co_status carryover_project_kv(const co_dims* dims, const co_weights* w, const void* hidden,
+                               const co_route* route, const co_state* state, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  co_status s = check_dims(dims);
+  if (s != CO_OK) return s;
+  if (!w || !w->w_f || !w->w_kv || !w->e_carry || !hidden || !route_ok(route) || !state_ok(state))
+    return CO_ERR_INVALID_ARG;
+  if (!aligned(hidden, 16) || !aligned(w->w_f, 16) || !aligned(w->w_kv, 16) ||
+      !aligned(w->e_carry, 16))
+    return CO_ERR_INVALID_ARG;
+  const ProjectPlan p = project_plan(dims);
+  if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
+  if (ws_bytes < p.total) return CO_ERR_WORKSPACE;
+  ProjectArgs a{};
+  a.M = dims->num_seqs * dims->block;
+  a.Dcat = dims->feat_dim;
+  a.d = dims->model_dim;
+  a.dtype = dims->dtype;
+  a.hidden = hidden;
+  a.wf = w->w_f;
+  a.wkv = w->w_kv;
+  a.e = w->e_carry;
+  a.dst = make_dest(dims, route, state);
+  a.ws = ws;
+  return hip_status(launch_project(a, p, stream));
+}
+
+co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int32_t layer_count,
+                                  const void* q, const co_state* state, void* out, float* lse,
+                                  uint32_t flags, void* ws, size_t ws_bytes, hipStream_t stream) {
+  co_status s = check_dims(dims);
+  if (s != CO_OK) return s;
+  if ((s = check_attention_dims(dims)) != CO_OK) return s;
+  if (layer_begin < 0 || layer_count < 0 || layer_begin + layer_count > dims->num_layers)
+    return CO_ERR_INVALID_ARG;
+  if (!q || !out || !state_ok(state) || !aligned(q, 16) || !aligned(out, 16) ||
+      (lse && !aligned(lse, 4)))
+    return CO_ERR_INVALID_ARG;
+  const AttnPlan p = attention_plan(dims);
+  if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
+  if (ws_bytes < p.bytes) return CO_ERR_WORKSPACE;
+  return do_attention(dims, layer_begin, layer_count, q, state, out, lse, flags, ws, stream);
+}
+
+co_status carryover_round(const co_dims* dims, const co_weights* w, const void* hidden,
+                          const int32_t* draft_tok, const int32_t* target_tok, const void* q,
+                          co_state* state, const co_route* scratch, void* out, float* lse,
+                          uint32_t flags, void* ws, size_t ws_bytes, hipStream_t stream) {
+  co_status s = check_dims(dims);
+  if (s != CO_OK) return s;
+  if ((s = check_attention_dims(dims)) != CO_OK) return s;
+  if (!w || !w->w_f || !w->w_kv || !w->e_carry || !hidden || !q || !out || !route_ok(scratch) ||
+      !state_ok(state))
+    return CO_ERR_INVALID_ARG;
+  if (!(flags & CO_ROUTE_ACCEPT_ALL) && (!draft_tok || !target_tok)) return CO_ERR_INVALID_ARG;
+  if (!aligned(hidden, 16) || !aligned(w->w_f, 16) || !aligned(w->w_kv, 16) ||
+      !aligned(w->e_carry, 16) || !aligned(q, 16) || !aligned(out, 16))
+    return CO_ERR_INVALID_ARG;
+  if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
+  if (ws_bytes < carryover_workspace_bytes(dims, CO_WS_ROUND)) return CO_ERR_WORKSPACE;
+  if ((s = carryover_route(dims, draft_tok, target_tok, flags, state, scratch, stream)) != CO_OK)
+    return s;
+  if ((s = carryover_project_kv(dims, w, hidden, scratch, state, ws, ws_bytes, stream)) != CO_OK)
+    return s;
+  return do_attention(dims, 0, dims->num_layers, q, state, out, lse, flags, ws, stream);
+}
+
+co_status carryover_import_kv(const co_dims* dims, int32_t seq, int32_t pos0, int32_t n_rows,
+                              const void* k_rows, const void* v_rows, const co_state* state,
+                              hipStream_t stream) {
+  co_status s = check_dims(dims);
+  if (s != CO_OK) return s;
+  if (!state_ok(state) || !k_rows || !v_rows || seq < 0 || seq >= dims->num_seqs || pos0 < 0 ||
+      n_rows < 0 ||
+      static_cast<int64_t>(pos0) + n_rows > static_cast<int64_t>(dims->max_pages_per_seq) * kPage)
+    return CO_ERR_INVALID_ARG;
+  const KvDest e = make_dest(dims, nullptr, state);
+  return hip_status(launch_import(e, dims->dtype, seq, pos0, n_rows, k_rows, v_rows,
+                                  state->page_table, dims->max_pages_per_seq, stream));
+}
+
+co_status carryover_read_status(const co_state* state, int32_t* host_out, hipStream_t stream) {
+  if (!state || !state->status || !host_out) return CO_ERR_INVALID_ARG;
+  if (hipMemcpyAsync(host_out, state->status, sizeof(int32_t), hipMemcpyDeviceToHost, stream) !=
+      hipSuccess)
+    return CO_ERR_HIP;
+  return hip_status(hipStreamSynchronize(stream));
+}
+
+const char* carryover_status_string(co_status status) {
+  switch (status) {
+    case CO_OK: return "ok";
+    case CO_ERR_INVALID_ARG: return "invalid argument";
+    case CO_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case CO_ERR_WORKSPACE: return "workspace too small";
+    case CO_ERR_CAPACITY: return "sequence capacity exceeded";
+    case CO_ERR_PAGE_RANGE: return "page id out of range";
+    case CO_ERR_HIP: return "HIP runtime error";
+    case CO_ERR_LENGTH: return "invalid sequence length";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

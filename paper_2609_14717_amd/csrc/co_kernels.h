@@ -1,0 +1,90 @@
+// Launch interfaces of the gfx950 kernels (internal to libcarryover).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "co_device.h"
+
+namespace co {
+
+struct RouteArgs {
+  int S, B, max_pages, num_pages;
+  uint32_t flags;
+  const int32_t* draft;
+  const int32_t* target;
+  int32_t* ctx_len;
+  int32_t* carry_len;
+  const int32_t* page_table;
+  int32_t* accept_len;
+  int32_t* row_pos;
+  int32_t* row_dst;
+  int32_t* status;
+};
+
+// Where projected K/V rows go: the paged committed cache or the carry segment.
+struct KvDest {
+  int S, B, L, Hkv, hd, num_pages, CP;
+  double log2_theta;
+  const int32_t* row_pos;
+  const int32_t* row_dst;
+  void* k_cache;
+  void* v_cache;
+  void* k_carry;
+  void* v_carry;
+  int32_t* status;
+};
+
+struct ProjectArgs {
+  int M, Dcat, d, dtype;
+  const void* hidden;
+  const void* wf;
+  const void* wkv;
+  const void* e;
+  KvDest dst;
+  void* ws;
+};
+
+struct ProjectPlan {
+  int f_tile, f_split;     // tile variant and K-splits of the F GEMM
+  int kv_tile, kv_split;   // same for the K/V GEMM
+  size_t z_bytes, part_bytes, total;
+};
+
+ProjectPlan plan_project(int M, int Dcat, int d, int n_kv, int dtype, int num_cus);
+
+struct AttnArgs {
+  int S, B, L, layer_begin, Hq, Hkv, hd, num_pages, max_pages, CP, dtype;
+  uint32_t flags;
+  double log2_theta;
+  const void* q;
+  const int32_t* ctx_len;
+  const int32_t* carry_len;
+  const int32_t* page_table;
+  const void* k_cache;
+  const void* v_cache;
+  const void* k_carry;
+  const void* v_carry;
+  void* out;
+  float* lse;
+  int32_t* status;
+  float* ws;
+};
+
+struct AttnPlan {
+  int chunk_pages, n_chunks, nq_pad;
+  size_t bytes;
+};
+
+AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int dtype);
+
+hipError_t launch_route(const RouteArgs& a, hipStream_t stream);
+hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_t stream);
+hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_count,
+                            hipStream_t stream);
+hipError_t launch_import(const KvDest& d, int dtype, int seq, int pos0, int n, const void* k_rows,
+                         const void* v_rows, const int32_t* page_table, int max_pages,
+                         hipStream_t stream);
+
+}  // namespace co

@@ -1,0 +1,148 @@
+"""Host-side checks of the C ABI: the library loads, exports every function
+that include/carryover.h declares, and rejects bad arguments before it
+enqueues anything (no compute call runs here)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2609_14717_amd as co
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "carryover.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(co.LIB_PATH), reason="library not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:co_status|size_t|const char\*)\s+(\w+)\s*\(", text,
+                                 flags=re.M)))
+
+
+def test_header_declares_the_four_calls_and_helpers():
+    names = declared_functions()
+    for n in ("carryover_route", "carryover_project_kv", "drafter_block_attention",
+              "carryover_round"):
+        assert n in names
+    assert set(names) == set(co.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    out = subprocess.run(["nm", "-D", "--defined-only", co.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    for n in declared_functions():
+        assert n in exported, n
+        assert hasattr(co.lib(), n)
+
+
+def _dims(**kw):
+    base = dict(S=2, B=16, Dcat=768, d=256, L=1, Hq=4, Hkv=2, hd=64, max_pages_per_seq=8,
+                num_pages=16, dtype="bf16", theta=1e4)
+    base.update(kw)
+    return co.make_dims(**base)
+
+
+FAKE = 1 << 20      # an aligned, non-null address that is never dereferenced here
+
+
+def _fake_state():
+    return {k: FAKE for k in ("ctx_len", "carry_len", "page_table", "k_cache", "v_cache",
+                              "k_carry", "v_carry", "status")}
+
+
+def _fake_route():
+    return {k: FAKE for k in ("accept_len", "row_pos", "row_dst")}
+
+
+def _rc(fn):
+    try:
+        fn()
+    except co.CarryoverError as e:
+        return e.code
+    return co.CO_OK
+
+
+def test_status_strings():
+    for code in range(8):
+        assert co.status_string(code) != "unknown status"
+    assert co.status_string(99) == "unknown status"
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(hd=96), co.CO_ERR_UNSUPPORTED),
+    (dict(Hq=6, Hkv=4), co.CO_ERR_UNSUPPORTED),
+    (dict(Dcat=700), co.CO_ERR_UNSUPPORTED),
+    (dict(B=0), co.CO_ERR_INVALID_ARG),
+    (dict(theta=0.0), co.CO_ERR_INVALID_ARG),
+])
+def test_bad_dims_rejected_by_every_call(kw, code):
+    d = _dims(**kw)
+    st, rt = _fake_state(), _fake_route()
+    W = co.weights(FAKE, FAKE, FAKE)
+    assert _rc(lambda: co.carryover_route(d, FAKE, FAKE, 0, st, rt, stream=0)) == code
+    assert _rc(lambda: co.carryover_project_kv(d, W, FAKE, rt, st, FAKE, stream=0,
+                                               ws_bytes=1 << 30)) == code
+    assert _rc(lambda: co.drafter_block_attention(d, 0, 1, FAKE, st, FAKE, None, 0, FAKE,
+                                                  stream=0, ws_bytes=1 << 30)) == code
+    assert co.workspace_bytes(d) == 0
+
+
+def test_page_size_must_be_16():
+    d = _dims()
+    d.page_size = 32
+    assert _rc(lambda: co.carryover_route(d, FAKE, FAKE, 0, _fake_state(), _fake_route(),
+                                          stream=0)) == co.CO_ERR_UNSUPPORTED
+
+
+def test_attention_query_rows_limit():
+    d = _dims(B=32, Hq=8, Hkv=2)          # 32 * 4 = 128 query rows per KV head
+    assert _rc(lambda: co.drafter_block_attention(d, 0, 1, FAKE, _fake_state(), FAKE, None, 0,
+                                                  FAKE, stream=0, ws_bytes=1 << 30)) \
+        == co.CO_ERR_UNSUPPORTED
+
+
+def test_null_and_misaligned_pointers():
+    d = _dims()
+    st = _fake_state()
+    st["k_cache"] = 0
+    W = co.weights(FAKE, FAKE, FAKE)
+    assert _rc(lambda: co.carryover_project_kv(d, W, FAKE, _fake_route(), st, FAKE, stream=0,
+                                               ws_bytes=1 << 30)) == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: co.carryover_route(d, None, FAKE, 0, _fake_state(), _fake_route(),
+                                          stream=0)) == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: co.carryover_project_kv(d, W, FAKE + 2, _fake_route(), _fake_state(),
+                                               FAKE, stream=0, ws_bytes=1 << 30)) \
+        == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: co.drafter_block_attention(d, 0, 2, FAKE, _fake_state(), FAKE, None, 0,
+                                                  FAKE, stream=0, ws_bytes=1 << 30)) \
+        == co.CO_ERR_INVALID_ARG
+
+
+def test_small_workspace_rejected():
+    d = _dims()
+    need_p = co.workspace_bytes(d, co.CO_WS_PROJECT)
+    need_a = co.workspace_bytes(d, co.CO_WS_ATTENTION)
+    assert need_p > 0 and need_a > 0
+    assert co.workspace_bytes(d, co.CO_WS_ROUND) == max(need_p, need_a)
+    W = co.weights(FAKE, FAKE, FAKE)
+    assert _rc(lambda: co.carryover_project_kv(d, W, FAKE, _fake_route(), _fake_state(), FAKE,
+                                               stream=0, ws_bytes=need_p - 1)) \
+        == co.CO_ERR_WORKSPACE
+    assert _rc(lambda: co.drafter_block_attention(d, 0, 1, FAKE, _fake_state(), FAKE, None, 0,
+                                                  FAKE, stream=0, ws_bytes=need_a - 1)) \
+        == co.CO_ERR_WORKSPACE
+
+
+def test_import_range_checked_on_host():
+    d = _dims()
+    lib = co.lib()
+    s = co.state(_fake_state())
+    for seq, pos0, n in ((2, 0, 1), (-1, 0, 1), (0, 120, 9), (0, -1, 1)):
+        rc = lib.carryover_import_kv(ctypes.byref(d), seq, pos0, n, FAKE, FAKE, ctypes.byref(s),
+                                     None)
+        assert rc == co.CO_ERR_INVALID_ARG
