@@ -168,7 +168,8 @@ co_status carryover_project_kv(const co_dims* dims, const co_weights* w, const v
  * num_kv_heads) followed by its carry_len[s] carry keys.  out has q's layout;
  * lse (optional, may be NULL) receives the natural-log normaliser.  An empty
  * key set gives out = 0 and lse = -inf.  `ws` must hold
- * carryover_workspace_bytes(dims, CO_WS_ATTENTION) bytes.
+ * carryover_workspace_bytes(dims, CO_WS_ATTENTION) bytes (scratch; any
+ * contents).  A workspace serves one call at a time.
  */
 co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int32_t layer_count,
                                   const void* q, const co_state* state, void* out, float* lse,
@@ -179,7 +180,8 @@ co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int3
  * column with CO_BASELINE_MODE): route, project all layers, then attend with
  * every layer's queries q [num_layers][num_seqs][block][num_q_heads][head_dim].
  * `scratch` receives the route result.  All state stays on the device; there
- * is no host synchronisation.  `ws`: carryover_workspace_bytes(dims, CO_WS_ROUND).
+ * is no host synchronisation.  `ws`: carryover_workspace_bytes(dims,
+ * CO_WS_ROUND) bytes of scratch.
  */
 co_status carryover_round(const co_dims* dims, const co_weights* w, const void* hidden,
                           const int32_t* draft_tok, const int32_t* target_tok, const void* q,

@@ -82,7 +82,8 @@ bool route_ok(const co_route* rt) { return rt && rt->accept_len && rt->row_pos &
 
 ProjectPlan project_plan(const co_dims* d) {
   return plan_project(d->num_seqs * d->block, d->feat_dim, d->model_dim,
-                      2 * d->num_layers * d->num_kv_heads * d->head_dim, d->dtype, num_cus());
+                      2 * d->num_layers * d->num_kv_heads * d->head_dim, d->head_dim, d->dtype,
+                      num_cus());
 }
 
 AttnPlan attention_plan(const co_dims* d) {
@@ -135,7 +136,7 @@ size_t carryover_workspace_bytes(const co_dims* dims, int32_t which) {
   switch (which) {
     case CO_WS_PROJECT: return pw;
     case CO_WS_ATTENTION: return aw;
-    case CO_WS_ROUND: return pw > aw ? pw : aw;
+    case CO_WS_ROUND: return aw ? pw + aw : 0;   // projection scratch, then attention area
     default: return 0;
   }
 }
@@ -231,7 +232,8 @@ co_status carryover_round(const co_dims* dims, const co_weights* w, const void* 
     return s;
   if ((s = carryover_project_kv(dims, w, hidden, scratch, state, ws, ws_bytes, stream)) != CO_OK)
     return s;
-  return do_attention(dims, 0, dims->num_layers, q, state, out, lse, flags, ws, stream);
+  void* attn_ws = static_cast<char*>(ws) + project_plan(dims).total;
+  return do_attention(dims, 0, dims->num_layers, q, state, out, lse, flags, attn_ws, stream);
 }
 
 co_status carryover_import_kv(const co_dims* dims, int32_t seq, int32_t pos0, int32_t n_rows,

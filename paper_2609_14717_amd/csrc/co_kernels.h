@@ -52,7 +52,7 @@ struct ProjectPlan {
   size_t z_bytes, part_bytes, total;
 };
 
-ProjectPlan plan_project(int M, int Dcat, int d, int n_kv, int dtype, int num_cus);
+ProjectPlan plan_project(int M, int Dcat, int d, int n_kv, int hd, int dtype, int num_cus);
 
 struct AttnArgs {
   int S, B, L, layer_begin, Hq, Hkv, hd, num_pages, max_pages, CP, dtype;
@@ -69,7 +69,7 @@ struct AttnArgs {
   void* out;
   float* lse;
   int32_t* status;
-  float* ws;
+  float* ws;        // partial records of multi-chunk sequences
 };
 
 struct AttnPlan {

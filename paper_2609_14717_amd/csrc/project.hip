@@ -7,9 +7,16 @@
 //   epilogue: rotate the K half of every head at row_pos, round, and scatter
 //             each row to its committed page slot or carry row (or drop it).
 //
-// bf16: LDS-staged, double-buffered MFMA (v_mfma_f32_16x16x32_bf16) GEMM,
-// 256 threads = 4 wavefronts per 2-D tile, optional deterministic split-K
-// through an fp32 workspace for skinny shapes (few rows, long K).
+// bf16: MFMA (v_mfma_f32_16x16x32_bf16) GEMM, 256 threads = 4 wavefronts per
+// 2-D tile.  Operands stream global -> LDS with direct-to-LDS 16-byte loads
+// (global_load_lds_dwordx4) into an NSTAGE-deep ring of 128-wide K stages, so
+// several stages are in flight without holding registers; each wavefront
+// issues the same number of loads per stage and waits with an exact vmcnt.
+// Rows are stored with their 16-byte chunks XOR-swizzled by (row mod 16) so
+// that the 16 lanes reading one MFMA fragment hit distinct LDS banks.
+// E_carry is staged with the operands and added to the A fragments of carry
+// rows as they are read.  Skinny shapes (few rows, long K) split K across
+// workgroups deterministically through an fp32 workspace.
 // fp32: a plain LDS-tiled VALU GEMM feeding the same epilogues.
 #include "co_kernels.h"
 
@@ -36,10 +43,11 @@ __device__ __forceinline__ bool is_carry_row(int32_t dst) { return dst < 0 && ds
 // ------------------------------------------------------------- K/V stores
 
 // Store pairs (i0+p, i0+p+hd/2), p < NP, of head segment `seg` = (layer, K|V, head)
-// of window row `row`.  lo/hi hold the unrotated fp32 values of those dims.
+// of window row `row`.  lo/hi hold the unrotated fp32 values of those dims;
+// inv_freq[i] = theta^(-2i/hd).
 template <typename T, int NP>
 __device__ void kv_store(const KvDest& e, int row, int seg, int i0, const float* lo,
-                         const float* hi) {
+                         const float* hi, const double* inv_freq) {
   const int32_t dst = e.row_dst[row];
   if (dst == kSkip) return;
   const int hd = e.hd, half = hd / 2;
@@ -79,7 +87,7 @@ __device__ void kv_store(const KvDest& e, int row, int seg, int i0, const float*
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
       float c, s;
-      rope_cos_sin(pos, rope_inv_freq(i0 + p, hd, e.log2_theta), &c, &s);
+      rope_cos_sin(pos, inv_freq[i0 + p], &c, &s);
       kptr[kbase + i0 + p] = to_elem<T>(lo[p] * c - hi[p] * s);
       kptr[kbase + i0 + p + half] = to_elem<T>(hi[p] * c + lo[p] * s);
     }
@@ -92,77 +100,137 @@ __device__ void kv_store(const KvDest& e, int row, int seg, int i0, const float*
   }
 }
 
+// s_waitcnt vmcnt(n) on gfx9: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14;
+// expcnt (6:4) and lgkmcnt (11:8) left at "no wait".
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+template <int NL, int NSTAGE>
+__device__ __forceinline__ void wait_stages_ahead(int ahead) {
+  // at most NSTAGE-1 later stages may stay in flight
+  if constexpr (NSTAGE >= 4) {
+    if (ahead >= 3) { wait_vmcnt<3 * NL>(); return; }
+  }
+  if constexpr (NSTAGE >= 3) {
+    if (ahead >= 2) { wait_vmcnt<2 * NL>(); return; }
+  }
+  if (ahead >= 1) { wait_vmcnt<NL>(); return; }
+  wait_vmcnt<0>();
+}
+
+// Workgroup barrier for the staged ring.  Each wavefront has already waited
+// (vmcnt) for its own direct-to-LDS loads of the stage it is about to read, and
+// LDS reads are complete once their values feed the MFMAs, so no memory fence
+// is needed -- a fence here would make every wavefront wait for all the later
+// stages still in flight.  The empty asm keeps the compiler from moving LDS
+// accesses across the barrier.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Groups of 16-byte LDS reads issued as inline asm, each group ending with its
+// own lgkmcnt(0) so that the outputs are complete when the statement ends.
+// The compiler cannot tell which ring slot an in-flight direct-to-LDS load
+// targets and would otherwise wait for all of them (vmcnt(0)) before every LDS
+// read; readiness of the slot being read is guaranteed by the explicit vmcnt
+// wait and barrier of each stage instead.
+__device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
+  typedef __attribute__((address_space(3))) const unsigned char* lds_ptr;
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr)p));
+}
+
+template <int N>
+__device__ __forceinline__ void lds_read_group(u16x8 (&v)[N], const uint32_t (&a)[N]);
+
+template <>
+__device__ __forceinline__ void lds_read_group<1>(u16x8 (&v)[1], const uint32_t (&a)[1]) {
+  asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)"
+               : "=&v"(v[0]) : "v"(a[0]) : "memory");
+}
+
+template <>
+__device__ __forceinline__ void lds_read_group<2>(u16x8 (&v)[2], const uint32_t (&a)[2]) {
+  asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %3\n\ts_waitcnt lgkmcnt(0)"
+               : "=&v"(v[0]), "=&v"(v[1]) : "v"(a[0]), "v"(a[1]) : "memory");
+}
+
+template <>
+__device__ __forceinline__ void lds_read_group<4>(u16x8 (&v)[4], const uint32_t (&a)[4]) {
+  asm volatile(
+      "ds_read_b128 %0, %4\n\tds_read_b128 %1, %5\n\tds_read_b128 %2, %6\n\t"
+      "ds_read_b128 %3, %7\n\ts_waitcnt lgkmcnt(0)"
+      : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3])
+      : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3])
+      : "memory");
+}
+
 // ------------------------------------------------------------ bf16 MFMA GEMM
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, int NSTAGE, bool HAS_E>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
-  constexpr int BK = 64, LDK = BK + 8;
+  constexpr int BK = 128;                 // K elements per stage
+  constexpr int ROWB = BK * 2;            // bytes per staged row
   constexpr int TM = BM / WM / 16, TN = BN / WN / 16;
-  static_assert(WM * WN == 4 && TM >= 1 && TN >= 1, "tile");
-  constexpr int kSmemU16 = 2 * (BM + BN) * LDK;
-  __shared__ __align__(16) uint16_t smem[kSmemU16];
+  constexpr int ROWS = BM + BN;           // A rows, then B rows
+  constexpr int LPW = ROWS / 16;          // 1 KiB loads (4 rows) per wave per stage
+  constexpr int NL = LPW + (HAS_E ? 1 : 0);
+  constexpr int E_OFF = ROWS * ROWB;
+  constexpr int STAGE_BYTES = ROWS * ROWB + (HAS_E ? 4 * 1024 : 0);
+  static_assert(WM * WN == 4 && TM >= 1 && TN >= 1 && ROWS % 16 == 0, "tile");
+  static_assert(NL * (NSTAGE - 1) < 64, "vmcnt");
+  constexpr int LDC = BN + 4;
+  static_assert(BM * LDC * 4 <= NSTAGE * STAGE_BYTES, "C tile must fit in the ring");
+  __shared__ __align__(16) unsigned char smem[NSTAGE * STAGE_BYTES];
+  __shared__ double inv_tab[64];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
   const int kbeg = blockIdx.z * g.k_per_split;
-  const int kend = min(g.K, kbeg + g.k_per_split);
-  const int nk = (kend - kbeg) / BK;
+  const int klen = min(g.K - kbeg, g.k_per_split);
+  const int nk = (klen + BK - 1) / BK;
+  const int last_ks = (klen - (nk - 1) * BK) / 32;      // k-steps in the last stage
   const uint16_t* A = static_cast<const uint16_t*>(g.A);
   const uint16_t* Bw = static_cast<const uint16_t*>(g.B);
   const uint16_t* E = static_cast<const uint16_t*>(g.e);
 
-  constexpr int kAChunks = BM * BK / 8, kBChunks = BN * BK / 8;
-  constexpr int kAPer = (kAChunks + 255) / 256, kBPer = (kBChunks + 255) / 256;
-  u16x8 ra[kAPer], rb[kBPer];
+  // carry flags of this lane's A rows (read before any staged load is issued)
+  bool carry[TM];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    carry[tm] = false;
+    if constexpr (HAS_E) {
+      const int gr = m0 + (wm * TM + tm) * 16 + (lane & 15);
+      carry[tm] = gr < g.M && is_carry_row(g.row_dst[gr]);
+    }
+  }
 
-  auto load_global = [&](int kt) {
+  auto issue = [&](int kt, int slot) {
+    unsigned char* st = smem + slot * STAGE_BYTES;
     const int k0 = kbeg + kt * BK;
 #pragma unroll
-    for (int i = 0; i < kAPer; ++i) {
-      const int c = tid + i * 256;
-      u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
-      if (c < kAChunks) {
-        const int row = c / (BK / 8), kc = c % (BK / 8);
-        const int gr = m0 + row;
-        if (gr < g.M) {
-          v = *reinterpret_cast<const u16x8*>(A + static_cast<int64_t>(gr) * g.K + k0 + kc * 8);
-          if (E && is_carry_row(g.row_dst[gr])) {
-            const u16x8 ev = *reinterpret_cast<const u16x8*>(E + k0 + kc * 8);
-#pragma unroll
-            for (int t = 0; t < 8; ++t) v[t] = f2bf(bf2f(v[t]) + bf2f(ev[t]));
-          }
-        }
+    for (int j = 0; j < LPW; ++j) {
+      const int i = wave * LPW + j;                    // 1 KiB block index (uniform)
+      const int row = i * 4 + (lane >> 4);
+      const int chunk = (lane & 15) ^ (row & 15);      // logical chunk landing at lane & 15
+      const int kk = min(k0 + chunk * 8, g.K - 8);     // a short last stage reads in bounds
+      const uint16_t* src;
+      if (row < BM) {
+        src = A + static_cast<int64_t>(min(m0 + row, g.M - 1)) * g.K + kk;
+      } else {
+        src = Bw + static_cast<int64_t>(min(n0 + row - BM, g.N - 1)) * g.K + kk;
       }
-      ra[i] = v;
+      __builtin_amdgcn_global_load_lds(src, st + i * 1024, 16, 0, 0);
     }
-#pragma unroll
-    for (int i = 0; i < kBPer; ++i) {
-      const int c = tid + i * 256;
-      u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
-      if (c < kBChunks) {
-        const int row = c / (BK / 8), kc = c % (BK / 8);
-        const int gn = n0 + row;
-        if (gn < g.N)
-          v = *reinterpret_cast<const u16x8*>(Bw + static_cast<int64_t>(gn) * g.K + k0 + kc * 8);
-      }
-      rb[i] = v;
-    }
-  };
-  auto store_lds = [&](int buf) {
-    uint16_t* sa = smem + buf * (BM + BN) * LDK;
-    uint16_t* sb = sa + BM * LDK;
-#pragma unroll
-    for (int i = 0; i < kAPer; ++i) {
-      const int c = tid + i * 256;
-      if (c < kAChunks)
-        *reinterpret_cast<u16x8*>(sa + (c / (BK / 8)) * LDK + (c % (BK / 8)) * 8) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < kBPer; ++i) {
-      const int c = tid + i * 256;
-      if (c < kBChunks)
-        *reinterpret_cast<u16x8*>(sb + (c / (BK / 8)) * LDK + (c % (BK / 8)) * 8) = rb[i];
+    if constexpr (HAS_E) {
+      const int kk = min(k0 + (lane & 15) * 8, g.K - 8);
+      __builtin_amdgcn_global_load_lds(E + kk, st + E_OFF + wave * 1024, 16, 0, 0);
     }
   };
 
@@ -172,35 +240,57 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
 #pragma unroll
     for (int b = 0; b < TN; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (nk > 0) {
-    load_global(0);
-    store_lds(0);
-  }
-  __syncthreads();
+#pragma unroll
+  for (int st = 0; st < NSTAGE - 1; ++st)
+    if (st < nk) issue(st, st);
+
   for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load_global(kt + 1);
-    const uint16_t* sa = smem + buf * (BM + BN) * LDK;
-    const uint16_t* sb = sa + BM * LDK;
-#pragma unroll
-    for (int ks = 0; ks < BK / 32; ++ks) {
+    if (kt + NSTAGE - 1 < nk) issue(kt + NSTAGE - 1, (kt + NSTAGE - 1) % NSTAGE);
+    wait_stages_ahead<NL, NSTAGE>(min(NSTAGE - 1, nk - 1 - kt));
+    stage_barrier();
+    const unsigned char* st = smem + (kt % NSTAGE) * STAGE_BYTES;
+    const int ksteps = kt == nk - 1 ? last_ks : BK / 32;
+    auto kstep = [&](int ks) {
+      const int c = ks * 4 + (lane >> 4);
       u16x8 af[TM], bfr[TN];
+      uint32_t aa[TM], ba[TN];
 #pragma unroll
-      for (int a = 0; a < TM; ++a)
-        af[a] = *reinterpret_cast<const u16x8*>(
-            sa + ((wm * TM + a) * 16 + (lane & 15)) * LDK + ks * 32 + (lane >> 4) * 8);
+      for (int a = 0; a < TM; ++a) {
+        const int row = (wm * TM + a) * 16 + (lane & 15);
+        aa[a] = lds_addr(st + row * ROWB + ((c ^ (row & 15)) << 4));
+      }
 #pragma unroll
-      for (int b = 0; b < TN; ++b)
-        bfr[b] = *reinterpret_cast<const u16x8*>(
-            sb + ((wn * TN + b) * 16 + (lane & 15)) * LDK + ks * 32 + (lane >> 4) * 8);
+      for (int b = 0; b < TN; ++b) {
+        const int row = BM + (wn * TN + b) * 16 + (lane & 15);
+        ba[b] = lds_addr(st + row * ROWB + ((c ^ (row & 15)) << 4));
+      }
+      lds_read_group<TM>(af, aa);
+      lds_read_group<TN>(bfr, ba);
+      if constexpr (HAS_E) {
+        u16x8 ev[1];
+        const uint32_t ea[1] = {lds_addr(st + E_OFF + (c << 4))};
+        lds_read_group<1>(ev, ea);
+#pragma unroll
+        for (int a = 0; a < TM; ++a)
+          if (carry[a]) {
+#pragma unroll
+            for (int t = 0; t < 8; ++t) af[a][t] = f2bf(bf2f(af[a][t]) + bf2f(ev[0][t]));
+          }
+      }
 #pragma unroll
       for (int a = 0; a < TM; ++a)
 #pragma unroll
         for (int b = 0; b < TN; ++b) acc[a][b] = mfma16x16x32(af[a], bfr[b], acc[a][b]);
+    };
+    if (ksteps == BK / 32) {
+#pragma unroll
+      for (int ks = 0; ks < BK / 32; ++ks) kstep(ks);
+    } else {
+      for (int ks = 0; ks < ksteps; ++ks) kstep(ks);
     }
-    if (kt + 1 < nk) store_lds(buf ^ 1);
-    __syncthreads();
+    stage_barrier();
   }
+  __syncthreads();
 
   if (g.mode == kModePartial) {
     float* out = g.partial + static_cast<int64_t>(blockIdx.z) * g.M * g.N;
@@ -218,8 +308,6 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
   }
 
   // Stage the fp32 tile through LDS so the epilogue can work on whole rows.
-  constexpr int LDC = BN + 4;
-  static_assert(BM * LDC * 4 <= kSmemU16 * 2, "C tile must fit in the staging LDS");
   float* sc = reinterpret_cast<float*>(smem);
 #pragma unroll
   for (int a = 0; a < TM; ++a)
@@ -229,6 +317,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
       for (int r = 0; r < 4; ++r)
         sc[((wm * TM + a) * 16 + (lane >> 4) * 4 + r) * LDC + (wn * TN + b) * 16 + (lane & 15)] =
             acc[a][b][r];
+  if (g.mode == kModeKV && tid < g.kv.hd / 2) inv_tab[tid] = rope_inv_freq(tid, g.kv.hd, g.kv.log2_theta);
   __syncthreads();
 
   if (g.mode == kModeZ) {
@@ -255,7 +344,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
         lo[p] = sc[row * LDC + seg_local * hd + i0 + p];
         hi[p] = sc[row * LDC + seg_local * hd + hd / 2 + i0 + p];
       }
-      kv_store<uint16_t, 4>(g.kv, gr, gc0 / hd, i0, lo, hi);
+      kv_store<uint16_t, 4>(g.kv, gr, gc0 / hd, i0, lo, hi, inv_tab);
     }
   }
 }
@@ -324,7 +413,10 @@ __global__ __launch_bounds__(256) void epi_z_kernel(const float* part, int split
 template <typename T>
 __global__ __launch_bounds__(256) void epi_kv_kernel(const float* part, int splits, int M, int N,
                                                      KvDest e) {
+  __shared__ double inv_tab[64];
   const int half = e.hd / 2;
+  if (threadIdx.x < half) inv_tab[threadIdx.x] = rope_inv_freq(threadIdx.x, e.hd, e.log2_theta);
+  __syncthreads();
   const int64_t items = static_cast<int64_t>(M) * (N / 2);   // one pair per thread
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (i >= items) return;
@@ -337,45 +429,87 @@ __global__ __launch_bounds__(256) void epi_kv_kernel(const float* part, int spli
     lo += part[static_cast<int64_t>(s) * M * N + c_lo];
     hi += part[static_cast<int64_t>(s) * M * N + c_lo + half];
   }
-  kv_store<T, 1>(e, row, seg, p, &lo, &hi);
+  kv_store<T, 1>(e, row, seg, p, &lo, &hi, inv_tab);
 }
 
-// Tile variants: 0 = 16x128 (1x4 waves), 1 = 64x128 (2x2), 2 = 128x128 (2x2).
-constexpr int kTileBM[3] = {16, 64, 128};
-constexpr int kTileBN = 128;
+// Tile variants (BM x BN, waves WM x WN, ring depth):
+//   0: 16 x 64, 1x4, 4 stages   skinny or few-row shapes, N tiles of 64
+//   1: 16 x 128, 1x4, 3 stages  skinny shapes whose K/V heads are 128 wide
+//   2: 64 x 128, 2x2, 2 stages  medium row counts
+//   3: 128 x 128, 2x2, 2 stages many rows (prefill, training-shaped forward)
+constexpr int kTileBM[4] = {16, 16, 64, 128};
+constexpr int kTileBN[4] = {64, 128, 128, 128};
 
-hipError_t launch_gemm_bf16(const GemmArgs& g, int tile, int splits, hipStream_t stream) {
-  const dim3 grid((g.N + kTileBN - 1) / kTileBN, (g.M + kTileBM[tile] - 1) / kTileBM[tile],
-                  splits);
+template <bool HAS_E>
+hipError_t launch_gemm_bf16_t(const GemmArgs& g, int tile, int splits, hipStream_t stream) {
+  const dim3 grid((g.N + kTileBN[tile] - 1) / kTileBN[tile],
+                  (g.M + kTileBM[tile] - 1) / kTileBM[tile], splits);
   switch (tile) {
-    case 0: hipLaunchKernelGGL((gemm_bf16_kernel<16, 128, 1, 4>), grid, dim3(256), 0, stream, g); break;
-    case 1: hipLaunchKernelGGL((gemm_bf16_kernel<64, 128, 2, 2>), grid, dim3(256), 0, stream, g); break;
-    default: hipLaunchKernelGGL((gemm_bf16_kernel<128, 128, 2, 2>), grid, dim3(256), 0, stream, g); break;
+    case 0: hipLaunchKernelGGL((gemm_bf16_kernel<16, 64, 1, 4, 4, HAS_E>), grid, dim3(256), 0, stream, g); break;
+    case 1: hipLaunchKernelGGL((gemm_bf16_kernel<16, 128, 1, 4, 3, HAS_E>), grid, dim3(256), 0, stream, g); break;
+    case 2: hipLaunchKernelGGL((gemm_bf16_kernel<64, 128, 2, 2, 2, HAS_E>), grid, dim3(256), 0, stream, g); break;
+    default: hipLaunchKernelGGL((gemm_bf16_kernel<128, 128, 2, 2, 2, HAS_E>), grid, dim3(256), 0, stream, g); break;
   }
   return hipGetLastError();
 }
 
-int pick_tile(int M) { return M <= 16 ? 0 : (M <= 1024 ? 1 : 2); }
+hipError_t launch_gemm_bf16(const GemmArgs& g, int tile, int splits, hipStream_t stream) {
+  return g.e ? launch_gemm_bf16_t<true>(g, tile, splits, stream)
+             : launch_gemm_bf16_t<false>(g, tile, splits, stream);
+}
+
+int tiles_of(int M, int N, int tile) {
+  return ((N + kTileBN[tile] - 1) / kTileBN[tile]) * ((M + kTileBM[tile] - 1) / kTileBM[tile]);
+}
 
 // Split K when the 2-D grid alone leaves most CUs idle and K is long enough.
 int pick_split(int M, int N, int K, int tile, int num_cus) {
-  const int tiles = ((N + kTileBN - 1) / kTileBN) * ((M + kTileBM[tile] - 1) / kTileBM[tile]);
+  const int tiles = tiles_of(M, N, tile);
   int split = 1;
-  while (tiles * split * 2 <= 2 * num_cus && (K / (split * 2)) % 64 == 0 && K / (split * 2) >= 512)
+  while (tiles * split * 2 <= 2 * num_cus && (K / (split * 2)) % 128 == 0 &&
+         K / (split * 2) >= 512)
     split *= 2;
   return split;
 }
 
+// Largest tile (fewest re-reads of the weights) whose grid, after splitting K,
+// still gives at least half of the CUs work; otherwise the most parallel one.
+// Tiles taller than the row count are skipped, and the 64-wide tile only holds
+// whole heads when they are 64 wide.
+void pick_gemm(int M, int N, int K, bool kv, int hd, int num_cus, int* tile, int* split) {
+  const int narrow = (!kv || hd == 64) ? 0 : 1;
+  int cand[3], nc = 0;
+  if (M > 64) cand[nc++] = 3;
+  if (M > 16) cand[nc++] = 2;
+  cand[nc++] = narrow;
+  int best = -1, best_wgs = -1, best_split = 1;
+  for (int i = 0; i < nc; ++i) {
+    const int t = cand[i];
+    const int sp = pick_split(M, N, K, t, num_cus);
+    const int wgs = tiles_of(M, N, t) * sp;
+    if (wgs >= num_cus / 2) {
+      *tile = t;
+      *split = sp;
+      return;
+    }
+    if (wgs > best_wgs) {
+      best = t;
+      best_wgs = wgs;
+      best_split = sp;
+    }
+  }
+  *tile = best;
+  *split = best_split;
+}
+
 }  // namespace
 
-ProjectPlan plan_project(int M, int Dcat, int d, int n_kv, int dtype, int num_cus) {
+ProjectPlan plan_project(int M, int Dcat, int d, int n_kv, int hd, int dtype, int num_cus) {
   ProjectPlan p{};
   const size_t es = dtype == CO_DTYPE_BF16 ? 2 : 4;
   if (dtype == CO_DTYPE_BF16) {
-    p.f_tile = pick_tile(M);
-    p.f_split = pick_split(M, d, Dcat, p.f_tile, num_cus);
-    p.kv_tile = pick_tile(M);
-    p.kv_split = pick_split(M, n_kv, d, p.kv_tile, num_cus);
+    pick_gemm(M, d, Dcat, false, hd, num_cus, &p.f_tile, &p.f_split);
+    pick_gemm(M, n_kv, d, true, hd, num_cus, &p.kv_tile, &p.kv_split);
   } else {
     p.f_tile = p.kv_tile = -1;
     p.f_split = p.kv_split = 1;

@@ -26,8 +26,9 @@ class Scenario:
         self.wkv = sdev.materialise(w, wl.spec_wkv(w), device)
         self.e = sdev.materialise(w, wl.spec_e(w), device)
         self.W = co.weights(self.wf, self.wkv, self.e)
-        self.ws = torch.empty(max(co.workspace_bytes(self.dims, co.CO_WS_ROUND), 256),
+        self.ws = torch.zeros(max(co.workspace_bytes(self.dims, co.CO_WS_ROUND), 256),
                               dtype=torch.uint8, device=device)
+        self.ws_project = co.workspace_bytes(self.dims, co.CO_WS_PROJECT)
         self.ctx0 = wl.initial_ctx(w)
         self.torch = torch
         self.co = co

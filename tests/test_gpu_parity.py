@@ -22,6 +22,8 @@ SMALL_RAGGED = wl.RAGGED32.replace(name="small_ragged", S=3, L=2, ctx_lo=100, ct
 SMALL_G4 = wl.Workload("small_g4_hd128", S=2, B=16, Dcat=512, d=256, L=2, Hq=8, Hkv=2, hd=128,
                        dtype="bf16", theta=1e6, ctx_lo=1500, ctx_hi=1500, ctx_mode="projected",
                        accept=("uniform",), rounds=4, seed=0x5EED02)
+BATCH3_8B = wl.BATCH1_8B.replace(name="batch3_8b_short", S=3, ctx_lo=300, ctx_hi=300, rounds=4,
+                                 seed=0x5EED04)
 SMALL_F32 = wl.Workload("small_f32", S=2, B=8, Dcat=256, d=128, L=2, Hq=4, Hkv=1, hd=128,
                         dtype="f32", theta=1e4, ctx_lo=300, ctx_hi=300, ctx_mode="projected",
                         accept=("uniform",), rounds=4, seed=0x5EED03)
@@ -92,7 +94,7 @@ def run_rounds(w, n_rounds, mode="carry", seqs=None, check_context=True):
     return sc, orc
 
 
-@pytest.mark.parametrize("w", [SMALL_RAGGED, SMALL_G4, SMALL_F32], ids=lambda w: w.name)
+@pytest.mark.parametrize("w", [SMALL_RAGGED, SMALL_G4, SMALL_F32, BATCH3_8B], ids=lambda w: w.name)
 def test_small_chains(w):
     run_rounds(w, 4)
 
