@@ -4,26 +4,30 @@
 // table, the carryover segment U from the per-sequence carry pages; both are
 // consumed by one online softmax, so the concatenation is never materialised.
 //
-// Work split (flash-decoding style): the logical pages of a sequence --
-// ceil(ctx/16) committed pages followed by ceil(carry/16) carry pages -- are
-// cut into chunks of `chunk_pages`; one workgroup per (chunk, sequence,
-// layer x KV head) computes all B * (Hq/Hkv) query rows of that KV head over
-// its chunk.  A sequence that fits in one chunk is finished in place; otherwise
-// each chunk leaves an unnormalised partial (O, running max, running sum) in
-// the workspace and a second, light kernel combines the chunks of every such
-// (layer, sequence, head) with the log-sum-exp rule.  (Combining inside the
-// first kernel would need a device-scope release per workgroup, which on this
-// part writes back the whole L2 of the XCD; the kernel boundary is cheaper.)
-//
-// bf16 path (gfx950 MFMA, wave64):
-//   S^T = K . Q^T   per 32-key tile: two 16-key M-tiles whose rows are the
-//                   keys {8q+r} and {8q+4+r} (q = lane/16, r < 4), so that the
-//                   softmax'ed scores of lane group q are keys 8q..8q+7;
-//   O^T += V^T . P^T with V pages stored [head_dim][16 slots]: every lane
-//                   reads its 8 keys of one V row with one 16-byte load.
-// Keys and values stream from HBM straight into registers, one tile ahead of
-// the tile being computed; wavefronts of a workgroup take alternate tiles and
-// are merged through LDS.  Queries are rotated once per workgroup into LDS.
+// bf16 path (the serving path), a persistent load-balanced kernel:
+//   * the keys of every (layer, KV head, sequence) -- ceil(ctx/16) committed
+//     pages followed by ceil(carry/16) carry pages -- are cut into 32-key tiles,
+//     and all tiles of all segments form one global sequence;
+//   * one workgroup per CU takes an equal contiguous slice of that sequence
+//     (no idle workgroups, no tail from ragged lengths), walking the segments
+//     its slice touches; for each it rotates the B * (Hq/Hkv) queries of that KV
+//     head into LDS once, then its wavefronts stream alternate tiles;
+//   * keys and values go global -> LDS with direct-to-LDS 16-byte loads into a
+//     ring private to each wavefront (NS tiles deep, exact vmcnt waits, no
+//     workgroup barrier in the loop), K rows XOR-swizzled for conflict-free
+//     fragment reads;
+//   * S^T = K . Q^T per tile uses two 16-key MFMA M-tiles whose rows are keys
+//     {8q+r} and {8q+4+r} (q = lane/16), so the softmax'ed scores a lane holds
+//     are exactly the 8 keys it needs for O^T += V^T . P^T, with V pages stored
+//     [head_dim][16 slots] -- no data movement between the two products;
+//   * a segment finished inside one slice is normalised and written in place;
+//     a segment split across slices leaves one unnormalised (O, max, sum)
+//     record per slice and a small kernel combines them (log-sum-exp rule).
+//     Combining inside the persistent kernel would need a device-scope release
+//     per workgroup, which on this part writes back the L2 of the XCD.
+// fp32 path: per-chunk workgroups with plain VALU arithmetic through LDS.
+#include <stdlib.h>
+
 #include "co_kernels.h"
 
 namespace co {
@@ -32,7 +36,7 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-constexpr int kMaxChunkPages = 64;
+constexpr int kMaxChunkPages = 256;   // page-id staging capacity (fp32 chunk / bf16 sub-chunk)
 
 struct SeqInfo {
   int ctx, carry, npc, npt, nch;
@@ -60,8 +64,8 @@ __device__ __forceinline__ float wave_sum_across_groups(float v) {
   return v + __shfl_xor(v, 32);
 }
 
-// Partial record of (layer, seq, kv head, chunk): O[nq_pad][hd], m[nq_pad], l[nq_pad]
-// (m in log2 units of the scaled logits; O unnormalised).
+// Partial record of (layer, seq, kv head, chunk) on the fp32 path: O[nq_pad][hd],
+// m[nq_pad], l[nq_pad] (m in log2 units of the scaled logits; O unnormalised).
 __device__ __forceinline__ float* record_ptr(const AttnArgs& a, int layer_local, int s, int g,
                                              int c, int n_chunks, int nq_pad) {
   const int64_t rec = ((static_cast<int64_t>(layer_local) * a.S + s) * a.Hkv + g) * n_chunks + c;
@@ -74,355 +78,67 @@ __device__ __forceinline__ int64_t out_row(const AttnArgs& a, int layer_local, i
   return ((static_cast<int64_t>(layer_local) * a.S + s) * a.B + i) * a.Hq + g * G + hh;
 }
 
-// Combine the chunk records of every (layer, sequence, KV head) whose key set
-// spans more than one chunk, and write O (+ LSE).  One thread per (query row,
-// 4 output dims); each thread issues all of its record loads at once.
+// fp32 path: combine the chunk records of every (layer, sequence, KV head)
+// whose key set spans more than one chunk, and write O (+ LSE).  The running
+// maxima and sums of all chunks are staged in LDS with one round of independent
+// loads and turned into per-(chunk, query) weights.
+constexpr int kMaxMergeChunks = 64;
+
 template <typename T>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a, int chunk_pages,
+__global__ __launch_bounds__(256) void attn_chunk_merge_kernel(AttnArgs a, int chunk_pages,
                                                          int n_chunks, int nq_pad) {
+  __shared__ float w_lds[kMaxMergeChunks * 64];
+  __shared__ float l_lds[kMaxMergeChunks * 64];
   const int s = blockIdx.x;
   const int layer_local = blockIdx.y / a.Hkv, g = blockIdx.y % a.Hkv;
   const SeqInfo si = seq_info(a, s, chunk_pages);
   if (si.nch <= 1) return;                 // finished by the chunk kernel
-  const int hd = a.hd, G = a.Hq / a.Hkv, nq = a.B * G, q4 = hd / 4;
+  const int hd = a.hd, G = a.Hq / a.Hkv, nq = a.B * G, q4 = hd / 4, nch = si.nch;
+  const int tid = threadIdx.x;
   const float* base = record_ptr(a, layer_local, s, g, 0, n_chunks, nq_pad);
   const int64_t rec = static_cast<int64_t>(nq_pad) * (hd + 2);
-  T* out = static_cast<T*>(a.out);
-  for (int idx = threadIdx.x + blockIdx.z * 256; idx < nq * q4; idx += 256 * gridDim.z) {
-    const int n = idx / q4, d = (idx % q4) * 4;
-    float M = -INFINITY;
-    for (int c = 0; c < si.nch; ++c) M = fmaxf(M, base[c * rec + nq_pad * hd + n]);
-    float den = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int c = 0; c < si.nch; ++c) {
-      const float m = base[c * rec + nq_pad * hd + n];
-      const float wgt = (m == -INFINITY) ? 0.f : exp2f(m - M);
-      den += wgt * base[c * rec + nq_pad * hd + nq_pad + n];
-      acc += wgt * *reinterpret_cast<const f32x4*>(base + c * rec + n * hd + d);
-    }
-    const float inv = den > 0.f ? 1.f / den : 0.f;
-    const int64_t row = out_row(a, layer_local, s, g, n, G);
-    T* o = out + row * hd + d;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) o[r] = to_elem<T>(acc[r] * inv);
-    if (a.lse && d == 0) a.lse[row] = den > 0.f ? (M + log2f(den)) * kLn2 : -INFINITY;
-  }
-}
-
-template <int HD>
-struct Tile {
-  u16x8 ka[HD / 32], kb[HD / 32], va[HD / 16];
-  int nv;
-};
-
-template <int HD, int NT, int NW>
-__global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int chunk_pages,
-                                                             int n_chunks) {
-  constexpr int KS = HD / 32;   // k-steps of S^T
-  constexpr int MT = HD / 16;   // M-tiles of O^T
-  constexpr int NQP = NT * 16;
-  constexpr int NTHR = 64 * NW;
-  constexpr int QLD = HD + 8;   // padded LDS row of rotated queries (bf16)
-  constexpr int NRED = NW > 1 ? NW - 1 : 1;
-  __shared__ __align__(16) uint16_t q_lds[NQP * QLD];
-  __shared__ int pg_lds[kMaxChunkPages];
-  __shared__ float red_o[NRED][NQP][HD + 1];
-  __shared__ float red_m[NRED][NQP], red_l[NRED][NQP];
-
-  const int c = blockIdx.x, s = blockIdx.y;
-  const int layer_local = blockIdx.z / a.Hkv, g = blockIdx.z % a.Hkv;
-  const int layer = a.layer_begin + layer_local;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int grp = lane >> 4, col = lane & 15;
-
-  const SeqInfo si = seq_info(a, s, chunk_pages);
-  if (!si.ok) {
-    if (c == 0 && tid == 0) set_status(a.status, CO_ERR_LENGTH);
-    return;
-  }
-  const int G = a.Hq / a.Hkv, nq = a.B * G;
-  if (si.npt == 0) {            // no keys at all: O = 0, LSE = -inf
-    if (c != 0) return;
-    uint16_t* out = static_cast<uint16_t*>(a.out);
-    for (int idx = tid; idx < nq * HD; idx += NTHR)
-      out[out_row(a, layer_local, s, g, idx / HD, G) * HD + idx % HD] = 0;
-    if (a.lse)
-      for (int n = tid; n < nq; n += NTHR) a.lse[out_row(a, layer_local, s, g, n, G)] = -INFINITY;
-    return;
-  }
-  const int p_begin = c * chunk_pages;
-  if (p_begin >= si.npt) return;
-  const int p_end = min(p_begin + chunk_pages, si.npt);
-  const int n_tiles = (p_end - p_begin + 1) / 2;
-
-  // ---- physical ids of this chunk's committed pages (-1: carry page, -2: bad id)
-  for (int i = tid; i < p_end - p_begin; i += NTHR) {
-    const int lp = p_begin + i;
-    int phys = -1;
-    if (lp < si.npc) {
-      phys = a.page_table[static_cast<int64_t>(s) * a.max_pages + lp];
-      if (phys < 0 || phys >= a.num_pages) {
-        set_status(a.status, CO_ERR_PAGE_RANGE);
-        phys = -2;
-      }
-    }
-    pg_lds[i] = phys;
-  }
-  // ---- queries: rotate at ctx + i, fold 1/sqrt(hd) * log2(e), store bf16 in LDS
-  {
-    const float qscale = rsqrtf(static_cast<float>(HD)) * kLog2e;
-    const uint16_t* Q = static_cast<const uint16_t*>(a.q);
-    for (int idx = tid; idx < NQP * (HD / 2); idx += NTHR) {
-      const int n = idx / (HD / 2), p = idx % (HD / 2);
-      float lo = 0.f, hi = 0.f;
-      if (n < nq) {
-        const uint16_t* qrow = Q + out_row(a, layer_local, s, g, n, G) * HD;
-        lo = bf2f(qrow[p]);
-        hi = bf2f(qrow[p + HD / 2]);
-        if (!(a.flags & CO_Q_PREROTATED)) {
-          float cs, sn;
-          rope_cos_sin(si.ctx + n / G, rope_inv_freq(p, HD, a.log2_theta), &cs, &sn);
-          const float l2 = lo * cs - hi * sn, h2 = hi * cs + lo * sn;
-          lo = l2;
-          hi = h2;
-        }
-      }
-      q_lds[n * QLD + p] = f2bf(lo * qscale);
-      q_lds[n * QLD + p + HD / 2] = f2bf(hi * qscale);
-    }
+  for (int idx = tid; idx < nch * nq_pad; idx += 256) {
+    const int c = idx / nq_pad, n = idx % nq_pad;
+    w_lds[idx] = base[c * rec + nq_pad * hd + n];
+    l_lds[idx] = base[c * rec + nq_pad * hd + nq_pad + n];
   }
   __syncthreads();
-  // Query fragments (B operand of S^T) stay in registers unless that would
-  // crowd out the double-buffered K/V tiles; then they are re-read from LDS.
-  constexpr bool kQInRegs = NT * KS <= 8;
-  u16x8 qf[kQInRegs ? NT : 1][KS];
-  if constexpr (kQInRegs) {
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        qf[nt][ks] = *reinterpret_cast<const u16x8*>(q_lds + (nt * 16 + col) * QLD + ks * 32 + grp * 8);
+  for (int n = tid; n < nq; n += 256) {
+    float M = -INFINITY;
+    for (int c = 0; c < nch; ++c) M = fmaxf(M, w_lds[c * nq_pad + n]);
+    float den = 0.f;
+    for (int c = 0; c < nch; ++c) {
+      const float m = w_lds[c * nq_pad + n];
+      const float wgt = (m == -INFINITY) ? 0.f : exp2f(m - M);
+      w_lds[c * nq_pad + n] = wgt;
+      den += wgt * l_lds[c * nq_pad + n];
+    }
+    const float inv = den > 0.f ? 1.f / den : 0.f;
+    for (int c = 0; c < nch; ++c) w_lds[c * nq_pad + n] *= inv;
+    if (a.lse && blockIdx.z == 0)
+      a.lse[out_row(a, layer_local, s, g, n, G)] = den > 0.f ? (M + log2f(den)) * kLn2 : -INFINITY;
   }
-  auto qfrag = [&](int nt, int ks) -> u16x8 {
-    if constexpr (kQInRegs) return qf[nt][ks];
-    return *reinterpret_cast<const u16x8*>(q_lds + (nt * 16 + col) * QLD + ks * 32 + grp * 8);
-  };
-
-  // key of S^T M-tile a / b at row rho = lane % 16
-  const int key_a = 8 * (col >> 2) + (col & 3);
-  const int key_b = key_a + 4;
-  const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
-  const uint16_t* vc = static_cast<const uint16_t*>(a.v_cache);
-  const uint16_t* kk = static_cast<const uint16_t*>(a.k_carry);
-  const uint16_t* vk = static_cast<const uint16_t*>(a.v_carry);
-
-  auto page = [&](int lp, const uint16_t*& kp, const uint16_t*& vp, int& nvalid) {
-    kp = kk;
-    vp = vk;
-    nvalid = 0;
-    if (lp >= p_end) return;
-    if (lp < si.npc) {
-      const int phys = pg_lds[lp - p_begin];
-      if (phys < 0) return;
-      const int64_t off = ((static_cast<int64_t>(layer) * a.num_pages + phys) * a.Hkv + g) * kPage * HD;
-      kp = kc + off;
-      vp = vc + off;
-      nvalid = min(kPage, si.ctx - lp * kPage);
-    } else {
-      const int cp = lp - si.npc;
-      const int64_t off =
-          (((static_cast<int64_t>(layer) * a.S + s) * a.CP + cp) * a.Hkv + g) * kPage * HD;
-      kp = kk + off;
-      vp = vk + off;
-      nvalid = min(kPage, si.carry - cp * kPage);
+  __syncthreads();
+  T* out = static_cast<T*>(a.out);
+  for (int idx = tid + blockIdx.z * 256; idx < nq * q4; idx += 256 * gridDim.z) {
+    const int n = idx / q4, d = (idx % q4) * 4;
+    const float* p = base + n * hd + d;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    int c = 0;
+    for (; c + 4 <= nch; c += 4) {
+      const f32x4 v0 = *reinterpret_cast<const f32x4*>(p + (c + 0) * rec);
+      const f32x4 v1 = *reinterpret_cast<const f32x4*>(p + (c + 1) * rec);
+      const f32x4 v2 = *reinterpret_cast<const f32x4*>(p + (c + 2) * rec);
+      const f32x4 v3 = *reinterpret_cast<const f32x4*>(p + (c + 3) * rec);
+      acc += w_lds[(c + 0) * nq_pad + n] * v0;
+      acc += w_lds[(c + 1) * nq_pad + n] * v1;
+      acc += w_lds[(c + 2) * nq_pad + n] * v2;
+      acc += w_lds[(c + 3) * nq_pad + n] * v3;
     }
-  };
-  auto load_tile = [&](int t, Tile<HD>& T) {
-    const int lp0 = p_begin + 2 * t;
-    const uint16_t *k0, *v0, *k1, *v1;
-    int n0, n1;
-    page(lp0, k0, v0, n0);
-    page(lp0 + 1, k1, v1, n1);
-    const uint16_t* pa = ((key_a >> 4) ? k1 : k0) + (key_a & 15) * HD + grp * 8;
-    const uint16_t* pb = ((key_b >> 4) ? k1 : k0) + (key_b & 15) * HD + grp * 8;
+    for (; c < nch; ++c) acc += w_lds[c * nq_pad + n] * *reinterpret_cast<const f32x4*>(p + c * rec);
+    T* o = out + out_row(a, layer_local, s, g, n, G) * hd + d;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      T.ka[ks] = *reinterpret_cast<const u16x8*>(pa + ks * 32);
-      T.kb[ks] = *reinterpret_cast<const u16x8*>(pb + ks * 32);
-    }
-    // V (A operand of O^T): hd row 16*mt + col, keys 8*grp .. +7 (page grp/2)
-    T.nv = (grp >> 1) ? n1 : n0;
-    const uint16_t* pv = ((grp >> 1) ? v1 : v0) + col * kPage + (grp & 1) * 8;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) T.va[mt] = *reinterpret_cast<const u16x8*>(pv + mt * 16 * kPage);
-  };
-
-  f32x4 o[MT][NT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) o[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[NT], l_run[NT];
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    m_run[nt] = -INFINITY;
-    l_run[nt] = 0.f;
-  }
-
-  auto compute_tile = [&](Tile<HD>& T) {
-    const int slot_base = (grp & 1) * 8;
-    // zero the values of invalid keys (their slots may hold anything)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (slot_base + e >= T.nv) T.va[mt][e] = 0;
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const u16x8 qv = qfrag(nt, ks);
-        sa = mfma16x16x32(T.ka[ks], qv, sa);
-        sb = mfma16x16x32(T.kb[ks], qv, sb);
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        sa[r] = (slot_base + r < T.nv) ? sa[r] : -INFINITY;
-        sb[r] = (slot_base + 4 + r < T.nv) ? sb[r] : -INFINITY;
-        mx = fmaxf(mx, fmaxf(sa[r], sb[r]));
-      }
-      mx = wave_max_across_groups(mx);
-      const float m_new = fmaxf(m_run[nt], mx);
-      const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m_run[nt] - m_new);
-      const float base = (m_new == -INFINITY) ? 0.f : m_new;
-      u16x8 pk;
-      float psum = 0.f;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float pa = exp2f(sa[r] - base), pb = exp2f(sb[r] - base);
-        psum += pa + pb;
-        pk[r] = f2bf(pa);
-        pk[4 + r] = f2bf(pb);
-      }
-      l_run[nt] = l_run[nt] * alpha + psum;
-      m_run[nt] = m_new;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        o[mt][nt] *= alpha;
-        o[mt][nt] = mfma16x16x32(T.va[mt], pk, o[mt][nt]);
-      }
-    }
-  };
-
-  // tiles wave, wave + NW, ...; the next tile's loads are in flight during compute
-  // (when the register file allows a second tile buffer)
-  constexpr bool kPrefetch = MT * NT <= 16;
-  if constexpr (!kPrefetch) {
-    Tile<HD> t0;
-    for (int t = wave; t < n_tiles; t += NW) {
-      load_tile(t, t0);
-      compute_tile(t0);
-    }
-  } else {
-    Tile<HD> t0, t1;
-    int t = wave;
-    if (t < n_tiles) load_tile(t, t0);
-    while (t < n_tiles) {
-      if (t + NW < n_tiles) load_tile(t + NW, t1);
-      compute_tile(t0);
-      t += NW;
-      if (t >= n_tiles) break;
-      if (t + NW < n_tiles) load_tile(t + NW, t0);
-      compute_tile(t1);
-      t += NW;
-    }
-  }
-
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) l_run[nt] = wave_sum_across_groups(l_run[nt]);
-
-  // ---- merge the wavefronts of this workgroup through LDS into wave 0
-  if constexpr (NW > 1) {
-    if (wave > 0) {
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int n = nt * 16 + col;
-        if (grp == 0) {
-          red_m[wave - 1][n] = m_run[nt];
-          red_l[wave - 1][n] = l_run[nt];
-        }
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) red_o[wave - 1][n][mt * 16 + grp * 4 + r] = o[mt][nt][r];
-      }
-    }
-    __syncthreads();
-    if (wave == 0) {
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int n = nt * 16 + col;
-        float M = m_run[nt];
-#pragma unroll
-        for (int w = 1; w < NW; ++w) M = fmaxf(M, red_m[w - 1][n]);
-        const float f0 = (m_run[nt] == -INFINITY) ? 0.f : exp2f(m_run[nt] - M);
-        float lsum = l_run[nt] * f0;
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) o[mt][nt] *= f0;
-#pragma unroll
-        for (int w = 1; w < NW; ++w) {
-          const float mw = red_m[w - 1][n];
-          const float fw = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
-          lsum += red_l[w - 1][n] * fw;
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) o[mt][nt][r] += fw * red_o[w - 1][n][mt * 16 + grp * 4 + r];
-        }
-        m_run[nt] = M;
-        l_run[nt] = lsum;
-      }
-    }
-  }
-
-  if (si.nch == 1) {
-    // the whole key set is in this chunk: normalise and write O / LSE directly
-    if (wave != 0) return;
-    uint16_t* out = static_cast<uint16_t*>(a.out);
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int n = nt * 16 + col;
-      if (n >= nq) continue;
-      const float inv = l_run[nt] > 0.f ? 1.f / l_run[nt] : 0.f;
-      const int64_t row = out_row(a, layer_local, s, g, n, G);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        u16x4 v;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = f2bf(o[mt][nt][r] * inv);
-        *reinterpret_cast<u16x4*>(out + row * HD + mt * 16 + grp * 4) = v;
-      }
-      if (a.lse && grp == 0)
-        a.lse[row] = l_run[nt] > 0.f ? (m_run[nt] + log2f(l_run[nt])) * kLn2 : -INFINITY;
-    }
-    return;
-  }
-
-  if (wave == 0) {
-    float* part = record_ptr(a, layer_local, s, g, c, n_chunks, NQP);
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int n = nt * 16 + col;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-        *reinterpret_cast<f32x4*>(part + n * HD + mt * 16 + grp * 4) = o[mt][nt];
-      if (grp == 0) {
-        part[NQP * HD + n] = m_run[nt];
-        part[NQP * HD + NQP + n] = l_run[nt];
-      }
-    }
+    for (int r = 0; r < 4; ++r) o[r] = to_elem<T>(acc[r]);
   }
 }
 
@@ -580,60 +296,609 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnArgs a, int chunk_pag
   }
 }
 
+// ------------------------------------------------------- bf16 persistent path
+
+// Tiles (32 keys = 2 logical pages) of sequence s; sequences with invalid
+// lengths have none (the combine kernel reports them).
+__device__ __forceinline__ int seq_tiles(const AttnArgs& a, int s) {
+  const SeqInfo q = seq_info(a, s, 1);
+  return (q.npt + 1) / 2;
+}
+
+// First tile of workgroup w's slice of T tiles split over n_wg workgroups.
+__device__ __forceinline__ int64_t slice_begin(int64_t T, int w, int n_wg) {
+  return T * w / n_wg;
+}
+
+// Workgroup whose slice holds global tile x.
+__device__ __forceinline__ int slice_owner(int64_t T, int64_t x, int n_wg) {
+  int w = static_cast<int>(x * n_wg / T);
+  while (w + 1 < n_wg && slice_begin(T, w + 1, n_wg) <= x) ++w;
+  while (w > 0 && slice_begin(T, w, n_wg) > x) --w;
+  return w;
+}
+
+// Workspace of the persistent path: tile prefix sums (S+1 ints, written by
+// workgroup 0 for the combine kernel), then one record per (slice, segment)
+// pair: O[NQP][hd] unnormalised, m[NQP], l[NQP].
+__device__ __forceinline__ float* slot_ptr(const AttnArgs& a, int hdr_floats, int64_t slot,
+                                           int nqp) {
+  return a.ws + hdr_floats + slot * nqp * (a.hd + 2);
+}
+
+template <int HD, int NT, int NW, int NS>
+__global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int layer_count, int n_wg,
+                                                             int hdr_floats) {
+  constexpr int KS = HD / 32;              // k-steps of S^T
+  constexpr int MT = HD / 16;              // M-tiles of O^T
+  constexpr int NQP = NT * 16;
+  constexpr int NTHR = 64 * NW;
+  constexpr int QLD = HD + 8;              // padded LDS row of rotated queries (bf16)
+  constexpr int NRED = NW > 1 ? NW - 1 : 1;
+  constexpr int ROWB = HD * 2;             // bytes of one key row
+  constexpr int CPR = ROWB / 16;           // 16-byte chunks per key row
+  constexpr int PAGE_BYTES = kPage * ROWB; // one page of K (or of V)
+  constexpr int LPP = PAGE_BYTES / 1024;   // 1 KiB wave loads per page
+  constexpr int TILE_BYTES = 4 * PAGE_BYTES;   // K page 0, K page 1, V page 0, V page 1
+  constexpr int NL = 4 * LPP;              // direct-to-LDS loads per tile per wave
+  constexpr int RING_BYTES = NW * NS * TILE_BYTES;
+  constexpr int RED_BYTES = (NRED * NQP * (HD + 1) + 2 * NRED * NQP) * 4;
+  constexpr int SMEM_BYTES = RING_BYTES > RED_BYTES ? RING_BYTES : RED_BYTES;
+  constexpr int SUB_TILES = kMaxChunkPages / 2;
+  static_assert(NL * (NS - 1) < 64, "vmcnt");
+  // the ring, reused for the cross-wave merge once a segment is done
+  __shared__ __align__(16) unsigned char smem[SMEM_BYTES];
+  __shared__ __align__(16) uint16_t q_lds[NQP * QLD];
+  __shared__ int pg_lds[kMaxChunkPages];
+  __shared__ int tstart[kMaxAttnSeqs + 1];
+  __shared__ double inv_lds[HD / 2];
+  __shared__ int wave_tot[NW];
+  float* red_o = reinterpret_cast<float*>(smem);                 // [NRED][NQP][HD + 1]
+  float* red_m = red_o + NRED * NQP * (HD + 1);                  // [NRED][NQP]
+  float* red_l = red_m + NRED * NQP;                             // [NRED][NQP]
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = lane >> 4, col = lane & 15;
+  const int S = a.S, G = a.Hq / a.Hkv, nq = a.B * G;
+
+  // ---- tiles per sequence and their prefix sums (the same for every segment row)
+  {
+    const int per = (S + NTHR - 1) / NTHR, s0 = tid * per;
+    int local = 0;
+    for (int i = 0; i < per; ++i)
+      if (s0 + i < S) local += seq_tiles(a, s0 + i);
+    int v = local;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int u = __shfl_up(v, off);
+      if (lane >= off) v += u;
+    }
+    if (lane == 63) wave_tot[wave] = v;
+    if (tid < HD / 2) inv_lds[tid] = rope_inv_freq(tid, HD, a.log2_theta);
+    __syncthreads();
+    int run = v - local;
+    for (int w = 0; w < wave; ++w) run += wave_tot[w];
+    for (int i = 0; i < per; ++i)
+      if (s0 + i < S) {
+        tstart[s0 + i] = run;
+        run += seq_tiles(a, s0 + i);
+      }
+    if (tid == NTHR - 1) tstart[S] = run;
+    __syncthreads();
+  }
+  const int T1 = tstart[S];
+  const int64_t T = static_cast<int64_t>(layer_count) * a.Hkv * T1;
+  if (blockIdx.x == 0) {
+    int* hdr = reinterpret_cast<int*>(a.ws);
+    for (int i = tid; i <= S; i += NTHR) hdr[i] = tstart[i];
+  }
+  const int w = blockIdx.x;
+  const int64_t r1 = slice_begin(T, w + 1, n_wg);
+
+  const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
+  const uint16_t* vc = static_cast<const uint16_t*>(a.v_cache);
+  const uint16_t* kk = static_cast<const uint16_t*>(a.k_carry);
+  const uint16_t* vk = static_cast<const uint16_t*>(a.v_carry);
+  const float qscale = rsqrtf(static_cast<float>(HD)) * kLog2e;
+  const uint16_t* Q = static_cast<const uint16_t*>(a.q);
+  // key of S^T M-tile a / b at row rho = lane % 16: keys {8q + r} and {8q + 4 + r}
+  const int key_a = 8 * (col >> 2) + (col & 3);
+  const int key_b = key_a + 4;
+  const int slot_base = (grp & 1) * 8;
+  unsigned char* my_ring = smem + wave * NS * TILE_BYTES;
+  // Per-lane source offsets (elements) of the direct-to-LDS loads of one page:
+  // K rows land XOR-swizzled by (row mod CPR), V pages are copied as they are.
+  int k_off[LPP], v_off[LPP];
+#pragma unroll
+  for (int q = 0; q < LPP; ++q) {
+    const int byte = q * 1024 + lane * 16;
+    const int r = byte / ROWB, pch = (byte % ROWB) / 16;
+    k_off[q] = r * HD + (pch ^ (r & (CPR - 1))) * 8;
+    v_off[q] = byte / 2;
+  }
+  // LDS byte offsets (within a tile) of this lane's K and V fragments
+  uint32_t ka_off[KS], kb_off[KS], v_frag_off;
+  {
+    const int ra = key_a & 15, rb = key_b & 15;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int ch = ks * 4 + grp;
+      ka_off[ks] = (key_a >> 4) * PAGE_BYTES + ra * ROWB + ((ch ^ (ra & (CPR - 1))) << 4);
+      kb_off[ks] = (key_b >> 4) * PAGE_BYTES + rb * ROWB + ((ch ^ (rb & (CPR - 1))) << 4);
+    }
+    v_frag_off = (2 + (grp >> 1)) * PAGE_BYTES + col * 32 + slot_base * 2;
+  }
+  // Running maxima are kept as a lazily updated reference: p = 2^(s - ref) may
+  // exceed 1 by up to 2^kRescale before the accumulators are rescaled, which
+  // leaves the normalised result unchanged and skips most rescales.
+  constexpr float kRescale = 8.f;
+
+  for (int64_t cur = slice_begin(T, w, n_wg); cur < r1;) {
+    // ---- locate the segment (layer, kv head, sequence) holding global tile cur
+    const int seg = static_cast<int>(cur / T1);
+    const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
+    const int layer = a.layer_begin + layer_local;
+    const int rr = static_cast<int>(cur % T1);
+    int lo = 0, hi = S;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (tstart[mid] <= rr) lo = mid; else hi = mid;
+    }
+    const int s = lo;
+    const int j0 = rr - tstart[s];
+    const int nts = tstart[s + 1] - tstart[s];
+    const int n = static_cast<int>(min(r1 - cur, static_cast<int64_t>(nts - j0)));
+    const bool whole = j0 == 0 && n == nts;
+    const SeqInfo si = seq_info(a, s, 1);
+    const int64_t kv_layer = (static_cast<int64_t>(layer) * a.num_pages) * a.Hkv + g;
+    const int64_t carry_base = ((static_cast<int64_t>(layer) * a.S + s) * a.CP) * a.Hkv + g;
+
+    // ---- queries of this segment: rotate at ctx + i, fold 1/sqrt(hd)*log2(e), bf16 in LDS
+    for (int idx = tid; idx < NQP * (HD / 2); idx += NTHR) {
+      const int qn = idx / (HD / 2), p = idx % (HD / 2);
+      float qlo = 0.f, qhi = 0.f;
+      if (qn < nq) {
+        const uint16_t* qrow = Q + out_row(a, layer_local, s, g, qn, G) * HD;
+        qlo = bf2f(qrow[p]);
+        qhi = bf2f(qrow[p + HD / 2]);
+        if (!(a.flags & CO_Q_PREROTATED)) {
+          float cs, sn;
+          rope_cos_sin(si.ctx + qn / G, inv_lds[p], &cs, &sn);
+          const float l2 = qlo * cs - qhi * sn, h2 = qhi * cs + qlo * sn;
+          qlo = l2;
+          qhi = h2;
+        }
+      }
+      q_lds[qn * QLD + p] = f2bf(qlo * qscale);
+      q_lds[qn * QLD + p + HD / 2] = f2bf(qhi * qscale);
+    }
+
+    f32x4 o[MT][NT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) o[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run[NT], l_run[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      m_run[nt] = -INFINITY;
+      l_run[nt] = 0.f;
+    }
+    u16x8 qf[NT][KS];
+
+    for (int sub = 0; sub < n; sub += SUB_TILES) {
+      const int sn_t = min(n - sub, SUB_TILES);            // tiles in this sub-chunk
+      const int pbeg = 2 * (j0 + sub);                      // its first logical page
+      const int pend = min(pbeg + 2 * sn_t, si.npt);
+      __syncthreads();                                      // previous readers of pg_lds done
+      for (int i = tid; i < pend - pbeg; i += NTHR) {
+        const int lp = pbeg + i;
+        int phys = -1;
+        if (lp < si.npc) {
+          phys = a.page_table[static_cast<int64_t>(s) * a.max_pages + lp];
+          if (phys < 0 || phys >= a.num_pages) {
+            set_status(a.status, CO_ERR_PAGE_RANGE);
+            phys = -2;
+          }
+        }
+        pg_lds[i] = phys;
+      }
+      __syncthreads();
+      if (sub == 0) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+            qf[nt][ks] =
+                *reinterpret_cast<const u16x8*>(q_lds + (nt * 16 + col) * QLD + ks * 32 + grp * 8);
+      }
+
+      // Logical page lp -> K/V page addresses (wave-uniform) and valid slots.
+      auto page = [&](int lp, const uint16_t*& kp, const uint16_t*& vp) -> int {
+        kp = kk;
+        vp = vk;
+        if (lp >= pend) return 0;
+        if (lp < si.npc) {
+          const int phys = __builtin_amdgcn_readfirstlane(pg_lds[lp - pbeg]);
+          if (phys < 0) return 0;
+          const int64_t off = (kv_layer + static_cast<int64_t>(phys) * a.Hkv) * kPage * HD;
+          kp = kc + off;
+          vp = vc + off;
+          return min(kPage, si.ctx - lp * kPage);
+        }
+        const int cp = lp - si.npc;
+        const int64_t off = (carry_base + static_cast<int64_t>(cp) * a.Hkv) * kPage * HD;
+        kp = kk + off;
+        vp = vk + off;
+        return min(kPage, si.carry - cp * kPage);
+      };
+      const int my_tiles = wave < sn_t ? (sn_t - 1 - wave) / NW + 1 : 0;
+      auto issue = [&](int jj) {
+        const int lp0 = pbeg + 2 * (wave + jj * NW);
+        unsigned char* dst = my_ring + (jj % NS) * TILE_BYTES;
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const uint16_t *kp, *vp;
+          page(lp0 + half, kp, vp);
+#pragma unroll
+          for (int q = 0; q < LPP; ++q) {
+            lds_dma16(kp + k_off[q], dst + half * PAGE_BYTES + q * 1024);
+            lds_dma16(vp + v_off[q], dst + (2 + half) * PAGE_BYTES + q * 1024);
+          }
+        }
+      };
+#pragma unroll
+      for (int jj = 0; jj < NS - 1; ++jj)
+        if (jj < my_tiles) issue(jj);
+
+      for (int jj = 0; jj < my_tiles; ++jj) {
+        if (jj + NS - 1 < my_tiles) issue(jj + NS - 1);
+        // valid slots of the tile's two pages (pages past the end have none)
+        const int lp0 = pbeg + 2 * (wave + jj * NW);
+        int n0 = 0, n1 = 0;
+        if (lp0 < pend)
+          n0 = lp0 < si.npc ? min(kPage, si.ctx - lp0 * kPage)
+                            : min(kPage, si.carry - (lp0 - si.npc) * kPage);
+        if (lp0 + 1 < pend)
+          n1 = lp0 + 1 < si.npc ? min(kPage, si.ctx - (lp0 + 1) * kPage)
+                                : min(kPage, si.carry - (lp0 + 1 - si.npc) * kPage);
+        if (lp0 < si.npc && pg_lds[lp0 - pbeg] < 0) n0 = 0;
+        if (lp0 + 1 < si.npc && lp0 + 1 < pend && pg_lds[lp0 + 1 - pbeg] < 0) n1 = 0;
+        const bool partial = n0 < kPage || n1 < kPage;      // wave-uniform
+        const int nv = (grp >> 1) ? n1 : n0;   // valid slots of the page holding my keys
+        wait_stages_ahead<NL, NS>(min(NS - 1, my_tiles - 1 - jj));
+        const unsigned char* tb = my_ring + (jj % NS) * TILE_BYTES;
+
+        u16x8 ka[KS], kb[KS];
+        {
+          uint32_t aa[KS], ab[KS];
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            aa[ks] = lds_addr(tb + ka_off[ks]);
+            ab[ks] = lds_addr(tb + kb_off[ks]);
+          }
+          if constexpr (KS == 2) {
+            u16x8 v4[4];
+            const uint32_t a4[4] = {aa[0], aa[1], ab[0], ab[1]};
+            lds_read_group<4>(v4, a4);
+            ka[0] = v4[0]; ka[1] = v4[1]; kb[0] = v4[2]; kb[1] = v4[3];
+          } else {
+            lds_read_group<KS>(ka, aa);
+            lds_read_group<KS>(kb, ab);
+          }
+        }
+        u16x8 va[MT];
+        {
+          const unsigned char* vb = tb + v_frag_off;
+#pragma unroll
+          for (int m4 = 0; m4 < MT; m4 += 4) {
+            u16x8 v4[4];
+            const uint32_t a4[4] = {lds_addr(vb + (m4 + 0) * 16 * 32), lds_addr(vb + (m4 + 1) * 16 * 32),
+                                    lds_addr(vb + (m4 + 2) * 16 * 32), lds_addr(vb + (m4 + 3) * 16 * 32)};
+            lds_read_group<4>(v4, a4);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) va[m4 + i] = v4[i];
+          }
+          if (partial) {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+              for (int e = 0; e < 8; ++e)
+                if (slot_base + e >= nv) va[mt][e] = 0;   // invalid keys may hold anything
+          }
+        }
+
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            sa = mfma16x16x32(ka[ks], qf[nt][ks], sa);
+            sb = mfma16x16x32(kb[ks], qf[nt][ks], sb);
+          }
+          if (partial) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              sa[r] = (slot_base + r < nv) ? sa[r] : -INFINITY;
+              sb[r] = (slot_base + 4 + r < nv) ? sb[r] : -INFINITY;
+            }
+          }
+          float mx = fmaxf(fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])),
+                           fmaxf(fmaxf(sb[0], sb[1]), fmaxf(sb[2], sb[3])));
+          mx = max_across_rows(mx);
+          if (__any(mx > m_run[nt] + kRescale)) {
+            // move the reference up (only where the tile exceeds it) and rescale
+            const float m_new = mx > m_run[nt] + kRescale ? mx : m_run[nt];
+            const float alpha = (m_new == m_run[nt]) ? 1.f : exp2f(m_run[nt] - m_new);
+            l_run[nt] *= alpha;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) o[mt][nt] *= alpha;
+            m_run[nt] = m_new;
+          }
+          const float base = (m_run[nt] == -INFINITY) ? 0.f : m_run[nt];
+          float pa[4], pb[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {   // v_exp_f32: arguments are <= kRescale or -inf
+            pa[r] = __builtin_amdgcn_exp2f(sa[r] - base);
+            pb[r] = __builtin_amdgcn_exp2f(sb[r] - base);
+          }
+          l_run[nt] += (pa[0] + pa[1]) + (pa[2] + pa[3]) + (pb[0] + pb[1]) + (pb[2] + pb[3]);
+          typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+          const u32x4v pk32 = {pack_bf16x2(pa[0], pa[1]), pack_bf16x2(pa[2], pa[3]),
+                               pack_bf16x2(pb[0], pb[1]), pack_bf16x2(pb[2], pb[3])};
+          const u16x8 pk = __builtin_bit_cast(u16x8, pk32);
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) o[mt][nt] = mfma16x16x32(va[mt], pk, o[mt][nt]);
+        }
+      }
+    }
+
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) l_run[nt] = wave_sum_across_groups(l_run[nt]);
+
+    // ---- merge the wavefronts through LDS (the drained ring) into wave 0
+    __syncthreads();
+    if constexpr (NW > 1) {
+      if (wave > 0) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int qn = nt * 16 + col;
+          if (grp == 0) {
+            red_m[(wave - 1) * NQP + qn] = m_run[nt];
+            red_l[(wave - 1) * NQP + qn] = l_run[nt];
+          }
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              red_o[((wave - 1) * NQP + qn) * (HD + 1) + mt * 16 + grp * 4 + r] = o[mt][nt][r];
+        }
+      }
+      __syncthreads();
+      if (wave == 0) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int qn = nt * 16 + col;
+          float M = m_run[nt];
+#pragma unroll
+          for (int wv = 1; wv < NW; ++wv) M = fmaxf(M, red_m[(wv - 1) * NQP + qn]);
+          const float f0 = (m_run[nt] == -INFINITY) ? 0.f : exp2f(m_run[nt] - M);
+          float lsum = l_run[nt] * f0;
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) o[mt][nt] *= f0;
+#pragma unroll
+          for (int wv = 1; wv < NW; ++wv) {
+            const float mw = red_m[(wv - 1) * NQP + qn];
+            const float fw = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
+            lsum += red_l[(wv - 1) * NQP + qn] * fw;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                o[mt][nt][r] += fw * red_o[((wv - 1) * NQP + qn) * (HD + 1) + mt * 16 + grp * 4 + r];
+          }
+          m_run[nt] = M;
+          l_run[nt] = lsum;
+        }
+      }
+    }
+
+    if (wave == 0) {
+      if (whole) {
+        // the whole segment is in this slice: normalise and write O / LSE directly
+        uint16_t* out = static_cast<uint16_t*>(a.out);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int qn = nt * 16 + col;
+          if (qn >= nq) continue;
+          const float inv = l_run[nt] > 0.f ? 1.f / l_run[nt] : 0.f;
+          const int64_t row = out_row(a, layer_local, s, g, qn, G);
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            u16x4 v;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = f2bf(o[mt][nt][r] * inv);
+            *reinterpret_cast<u16x4*>(out + row * HD + mt * 16 + grp * 4) = v;
+          }
+          if (a.lse && grp == 0)
+            a.lse[row] = l_run[nt] > 0.f ? (m_run[nt] + log2f(l_run[nt])) * kLn2 : -INFINITY;
+        }
+      } else {
+        float* part = slot_ptr(a, hdr_floats, w + static_cast<int64_t>(seg) * S + s, NQP);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int qn = nt * 16 + col;
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+            *reinterpret_cast<f32x4*>(part + qn * HD + mt * 16 + grp * 4) = o[mt][nt];
+          if (grp == 0) {
+            part[NQP * HD + qn] = m_run[nt];
+            part[NQP * HD + NQP + qn] = l_run[nt];
+          }
+        }
+      }
+    }
+    __syncthreads();                                        // q_lds and smem are reused
+    cur += n;
+  }
+}
+
+// Combine the slice records of every (layer, KV head, sequence) split across
+// slices, write O/LSE of segments without keys, and report invalid lengths.
+// One thread per (query row, 4 output dims); record loads are issued in
+// batches of kBatch so that their latencies overlap.
+__global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int layer_count,
+                                                                int n_wg, int hdr_floats,
+                                                                int nq_pad) {
+  constexpr int kBatch = 8;
+  const int s = blockIdx.x, seg = blockIdx.y;
+  const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
+  const int hd = a.hd, G = a.Hq / a.Hkv, nq = a.B * G, q4 = hd / 4;
+  const int tid = threadIdx.x;
+  const int* hdr = reinterpret_cast<const int*>(a.ws);
+  const SeqInfo si = seq_info(a, s, 1);
+  if (!si.ok && seg == 0 && tid == 0 && blockIdx.z == 0) set_status(a.status, CO_ERR_LENGTH);
+  const int T1 = hdr[a.S];
+  const int nts = hdr[s + 1] - hdr[s];
+  uint16_t* out = static_cast<uint16_t*>(a.out);
+  if (nts == 0) {                      // no keys: O = 0, LSE = -inf
+    for (int idx = tid + blockIdx.z * 256; idx < nq * hd; idx += 256 * gridDim.z)
+      out[out_row(a, layer_local, s, g, idx / hd, G) * hd + idx % hd] = 0;
+    if (a.lse && blockIdx.z == 0)
+      for (int qn = tid; qn < nq; qn += 256) a.lse[out_row(a, layer_local, s, g, qn, G)] = -INFINITY;
+    return;
+  }
+  const int64_t T = static_cast<int64_t>(layer_count) * a.Hkv * T1;
+  const int64_t A = static_cast<int64_t>(seg) * T1 + hdr[s];
+  const int w_lo = slice_owner(T, A, n_wg), w_hi = slice_owner(T, A + nts - 1, n_wg);
+  if (w_lo == w_hi) return;            // finished in place
+  const int nrec = w_hi - w_lo + 1;
+  const int64_t rec = static_cast<int64_t>(nq_pad) * (hd + 2);
+  // records of consecutive slices are consecutive slots; a slice can be empty when
+  // there are fewer tiles than workgroups, and then it left no record
+  const float* base = slot_ptr(a, hdr_floats, w_lo + static_cast<int64_t>(seg) * a.S + s, nq_pad);
+  for (int idx = tid + blockIdx.z * 256; idx < nq * q4; idx += 256 * gridDim.z) {
+    const int qn = idx / q4, d = (idx % q4) * 4;
+    const float* pm = base + nq_pad * hd + qn;
+    float M = -INFINITY;
+    for (int r0 = 0; r0 < nrec; r0 += kBatch) {
+      float mv[kBatch];
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) mv[i] = r0 + i < nrec ? pm[(r0 + i) * rec] : -INFINITY;
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i)
+        if (r0 + i < nrec && slice_begin(T, w_lo + r0 + i, n_wg) < slice_begin(T, w_lo + r0 + i + 1, n_wg))
+          M = fmaxf(M, mv[i]);
+    }
+    float den = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int r0 = 0; r0 < nrec; r0 += kBatch) {
+      float mv[kBatch], lv[kBatch];
+      f32x4 ov[kBatch];
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) {
+        const bool in = r0 + i < nrec;
+        mv[i] = in ? pm[(r0 + i) * rec] : -INFINITY;
+        lv[i] = in ? pm[(r0 + i) * rec + nq_pad] : 0.f;
+        ov[i] = in ? *reinterpret_cast<const f32x4*>(base + (r0 + i) * rec + qn * hd + d)
+                   : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) {
+        const bool live = r0 + i < nrec &&
+                          slice_begin(T, w_lo + r0 + i, n_wg) < slice_begin(T, w_lo + r0 + i + 1, n_wg);
+        const float wgt = (!live || mv[i] == -INFINITY) ? 0.f : exp2f(mv[i] - M);
+        den += wgt * lv[i];
+        acc += wgt * ov[i];
+      }
+    }
+    const float inv = den > 0.f ? 1.f / den : 0.f;
+    const int64_t row = out_row(a, layer_local, s, g, qn, G);
+    u16x4 v;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[r] = f2bf(acc[r] * inv);
+    *reinterpret_cast<u16x4*>(out + row * hd + d) = v;
+    if (a.lse && d == 0) a.lse[row] = den > 0.f ? (M + log2f(den)) * kLn2 : -INFINITY;
+  }
+}
+
 }  // namespace
 
-AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int dtype) {
-  (void)dtype;
+AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int dtype,
+                        int num_cus) {
   AttnPlan p{};
   const int nq = B * (Hq / Hkv);
   p.nq_pad = (nq + 15) / 16 * 16;
   const int cp = (B + kPage - 1) / kPage;
   const int max_lp = max_pages + cp;
-  // Larger records (many query rows, wide heads) get longer chunks so that the
-  // partial records stay a small fraction of the key/value bytes they summarise.
-  p.chunk_pages = (hd == 64 && p.nq_pad <= 32) ? 32 : kMaxChunkPages;
-  p.n_chunks = (max_lp + p.chunk_pages - 1) / p.chunk_pages;
-  p.bytes = static_cast<size_t>(L) * S * Hkv * p.n_chunks * p.nq_pad * (hd + 2) * 4;
+  p.ok = true;
+  if (dtype == CO_DTYPE_BF16) {
+    // persistent path: one workgroup per CU, records for (slice, segment) pairs
+    p.n_wg = num_cus;
+    if (const char* env = getenv("CO_ATTN_WORKGROUPS")) {   // tuning override
+      const int v = atoi(env);
+      if (v >= 1 && v <= 65536) p.n_wg = v;
+    }
+    p.hdr_floats = (S + 1 + 63) / 64 * 64;
+    p.ok = S <= kMaxAttnSeqs;
+    p.bytes = (static_cast<size_t>(p.hdr_floats) +
+               (static_cast<size_t>(p.n_wg) + static_cast<size_t>(L) * Hkv * S) * p.nq_pad *
+                   (hd + 2)) * 4;
+  } else {
+    // fp32 path: chunks of pages, one workgroup each
+    p.chunk_pages = 32;
+    while ((max_lp + p.chunk_pages - 1) / p.chunk_pages > kMaxMergeChunks) p.chunk_pages *= 2;
+    p.ok = p.chunk_pages <= kMaxChunkPages;
+    p.n_chunks = (max_lp + p.chunk_pages - 1) / p.chunk_pages;
+    p.bytes = static_cast<size_t>(L) * S * Hkv * p.n_chunks * p.nq_pad * (hd + 2) * 4;
+  }
   p.bytes = (p.bytes + 255) / 256 * 256;
   return p;
 }
 
-hipError_t launch_attention(const AttnArgs& a_in, const AttnPlan& p, int layer_count,
+hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_count,
                             hipStream_t stream) {
-  if (a_in.S == 0 || layer_count == 0) return hipSuccess;
-  const AttnArgs& a = a_in;
-  const dim3 grid(p.n_chunks, a.S, layer_count * a.Hkv);
+  if (a.S == 0 || layer_count == 0) return hipSuccess;
   const int nt = p.nq_pad / 16;
+  const int items = (a.B * (a.Hq / a.Hkv)) * (a.hd / 4);
+  const dim3 mgrid(a.S, layer_count * a.Hkv, (items + 255) / 256);
   if (a.dtype == CO_DTYPE_BF16) {
+    const dim3 grid(p.n_wg);
+#define CO_ATTN_LAUNCH(HD, NT, NW, NS)                                                         \
+  hipLaunchKernelGGL((attn_bf16_kernel<HD, NT, NW, NS>), grid, dim3(64 * NW), 0, stream, a,     \
+                     layer_count, p.n_wg, p.hdr_floats)
     if (a.hd == 64) {
       switch (nt) {
-        case 1: hipLaunchKernelGGL((attn_bf16_kernel<64, 1, 4>), grid, dim3(256), 0, stream, a, p.chunk_pages, p.n_chunks); break;
-        case 2: hipLaunchKernelGGL((attn_bf16_kernel<64, 2, 4>), grid, dim3(256), 0, stream, a, p.chunk_pages, p.n_chunks); break;
-        case 3: hipLaunchKernelGGL((attn_bf16_kernel<64, 3, 4>), grid, dim3(256), 0, stream, a, p.chunk_pages, p.n_chunks); break;
-        default: hipLaunchKernelGGL((attn_bf16_kernel<64, 4, 4>), grid, dim3(256), 0, stream, a, p.chunk_pages, p.n_chunks); break;
+        case 1: CO_ATTN_LAUNCH(64, 1, 4, 4); break;
+        case 2: CO_ATTN_LAUNCH(64, 2, 4, 4); break;
+        case 3: CO_ATTN_LAUNCH(64, 3, 4, 4); break;
+        default: CO_ATTN_LAUNCH(64, 4, 4, 4); break;
       }
     } else {
       switch (nt) {
-        case 1: hipLaunchKernelGGL((attn_bf16_kernel<128, 1, 2>), grid, dim3(128), 0, stream, a, p.chunk_pages, p.n_chunks); break;
-        case 2: hipLaunchKernelGGL((attn_bf16_kernel<128, 2, 2>), grid, dim3(128), 0, stream, a, p.chunk_pages, p.n_chunks); break;
-        case 3: hipLaunchKernelGGL((attn_bf16_kernel<128, 3, 2>), grid, dim3(128), 0, stream, a, p.chunk_pages, p.n_chunks); break;
-        default: hipLaunchKernelGGL((attn_bf16_kernel<128, 4, 2>), grid, dim3(128), 0, stream, a, p.chunk_pages, p.n_chunks); break;
+        case 1: CO_ATTN_LAUNCH(128, 1, 2, 3); break;
+        case 2: CO_ATTN_LAUNCH(128, 2, 2, 3); break;
+        case 3: CO_ATTN_LAUNCH(128, 3, 2, 3); break;
+        default: CO_ATTN_LAUNCH(128, 4, 2, 3); break;
       }
     }
-  } else {
-    if (a.hd == 64)
-      hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(256), 0, stream, a, p.chunk_pages, p.n_chunks, p.nq_pad);
-    else
-      hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(256), 0, stream, a, p.chunk_pages, p.n_chunks, p.nq_pad);
+#undef CO_ATTN_LAUNCH
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(attn_bf16_combine_kernel, mgrid, dim3(256), 0, stream, a, layer_count,
+                       p.n_wg, p.hdr_floats, p.nq_pad);
+    return hipGetLastError();
   }
+  const dim3 grid(p.n_chunks, a.S, layer_count * a.Hkv);
+  if (a.hd == 64)
+    hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(256), 0, stream, a, p.chunk_pages, p.n_chunks, p.nq_pad);
+  else
+    hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(256), 0, stream, a, p.chunk_pages, p.n_chunks, p.nq_pad);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || p.n_chunks <= 1) return err;
-  const int items = (a.B * (a.Hq / a.Hkv)) * (a.hd / 4);
-  const dim3 mgrid(a.S, layer_count * a.Hkv, (items + 255) / 256);
-  if (a.dtype == CO_DTYPE_BF16)
-    hipLaunchKernelGGL(attn_merge_kernel<uint16_t>, mgrid, dim3(256), 0, stream, a, p.chunk_pages, p.n_chunks, p.nq_pad);
-  else
-    hipLaunchKernelGGL(attn_merge_kernel<float>, mgrid, dim3(256), 0, stream, a, p.chunk_pages, p.n_chunks, p.nq_pad);
+  hipLaunchKernelGGL(attn_chunk_merge_kernel<float>, mgrid, dim3(256), 0, stream, a, p.chunk_pages,
+                     p.n_chunks, p.nq_pad);
   return hipGetLastError();
 }
 

@@ -43,9 +43,12 @@ co_status check_dims(const co_dims* d) {
   return CO_OK;
 }
 
+AttnPlan attention_plan(const co_dims* d);
+
 co_status check_attention_dims(const co_dims* d) {
   const int nq = d->block * (d->num_q_heads / d->num_kv_heads);
-  return nq > 64 ? CO_ERR_UNSUPPORTED : CO_OK;
+  if (nq > 64) return CO_ERR_UNSUPPORTED;
+  return attention_plan(d).ok ? CO_OK : CO_ERR_UNSUPPORTED;
 }
 
 size_t elem_bytes(const co_dims* d) { return d->dtype == CO_DTYPE_BF16 ? 2 : 4; }
@@ -88,7 +91,7 @@ ProjectPlan project_plan(const co_dims* d) {
 
 AttnPlan attention_plan(const co_dims* d) {
   return plan_attention(d->num_seqs, d->block, d->num_layers, d->num_q_heads, d->num_kv_heads,
-                        d->head_dim, d->max_pages_per_seq, d->dtype);
+                        d->head_dim, d->max_pages_per_seq, d->dtype, num_cus());
 }
 
 co_status hip_status(hipError_t e) { return e == hipSuccess ? CO_OK : CO_ERR_HIP; }

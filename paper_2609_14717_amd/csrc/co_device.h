@@ -32,6 +32,32 @@ template <typename T> __device__ __forceinline__ T to_elem(float v);
 template <> __device__ __forceinline__ float to_elem<float>(float v) { return v; }
 template <> __device__ __forceinline__ uint16_t to_elem<uint16_t>(float v) { return f2bf(v); }
 
+// Direct-to-LDS 16-byte load (global_load_lds_dwordx4): every lane supplies a
+// global address; the 64 x 16 bytes land contiguously at lds_dst (uniform).  A
+// plain function so that kernel templates do not instantiate the builtin in
+// their host-side pass (where it would silently drop the kernel).
+__device__ __forceinline__ void lds_dma16(const void* src, void* lds_dst) {
+  __builtin_amdgcn_global_load_lds(src, lds_dst, 16, 0, 0);
+}
+
+// Two fp32 values -> packed bf16 pair (round to nearest even, v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const __bf16 a = static_cast<__bf16>(lo), b = static_cast<__bf16>(hi);
+  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a)) |
+         (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b)) << 16);
+}
+
+// Max over the four 16-lane rows holding the same column (lanes l, l^16, l^32, l^48),
+// with the gfx950 row-swap permutes instead of LDS permutes.
+__device__ __forceinline__ float max_across_rows(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 __device__ __forceinline__ bf16x8 as_bf16x8(u16x8 v) { return __builtin_bit_cast(bf16x8, v); }
 
 // v_mfma_f32_16x16x32_bf16: acc[16x16] += A[16x32] * B[32x16].
@@ -58,6 +84,63 @@ __device__ __forceinline__ void rope_cos_sin(int pos, double inv_freq, float* c,
 
 __device__ __forceinline__ void set_status(int32_t* status, int32_t code) {
   if (status) atomicCAS(status, 0, code);
+}
+
+// s_waitcnt vmcnt(n) on gfx9: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14;
+// expcnt (6:4) and lgkmcnt (11:8) left at "no wait".
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+template <int NL, int NSTAGE>
+__device__ __forceinline__ void wait_stages_ahead(int ahead) {
+  // at most NSTAGE-1 later stages may stay in flight
+  if constexpr (NSTAGE >= 4) {
+    if (ahead >= 3) { wait_vmcnt<3 * NL>(); return; }
+  }
+  if constexpr (NSTAGE >= 3) {
+    if (ahead >= 2) { wait_vmcnt<2 * NL>(); return; }
+  }
+  if (ahead >= 1) { wait_vmcnt<NL>(); return; }
+  wait_vmcnt<0>();
+}
+
+// Groups of 16-byte LDS reads issued as inline asm, each group ending with its
+// own lgkmcnt(0) so that the outputs are complete when the statement ends.
+// The compiler cannot tell which ring slot an in-flight direct-to-LDS load
+// targets and would otherwise wait for all of them (vmcnt(0)) before every LDS
+// read; callers guarantee readiness of the slot they read with explicit vmcnt
+// waits (and a barrier where other wavefronts filled the slot).
+__device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
+  typedef __attribute__((address_space(3))) const unsigned char* lds_ptr;
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr)p));
+}
+
+template <int N>
+__device__ __forceinline__ void lds_read_group(u16x8 (&v)[N], const uint32_t (&a)[N]);
+
+template <>
+__device__ __forceinline__ void lds_read_group<1>(u16x8 (&v)[1], const uint32_t (&a)[1]) {
+  asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)"
+               : "=&v"(v[0]) : "v"(a[0]) : "memory");
+}
+
+template <>
+__device__ __forceinline__ void lds_read_group<2>(u16x8 (&v)[2], const uint32_t (&a)[2]) {
+  asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %3\n\ts_waitcnt lgkmcnt(0)"
+               : "=&v"(v[0]), "=&v"(v[1]) : "v"(a[0]), "v"(a[1]) : "memory");
+}
+
+template <>
+__device__ __forceinline__ void lds_read_group<4>(u16x8 (&v)[4], const uint32_t (&a)[4]) {
+  asm volatile(
+      "ds_read_b128 %0, %4\n\tds_read_b128 %1, %5\n\tds_read_b128 %2, %6\n\t"
+      "ds_read_b128 %3, %7\n\ts_waitcnt lgkmcnt(0)"
+      : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3])
+      : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3])
+      : "memory");
 }
 
 }  // namespace co

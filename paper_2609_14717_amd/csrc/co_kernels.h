@@ -72,12 +72,18 @@ struct AttnArgs {
   float* ws;        // partial records of multi-chunk sequences
 };
 
+constexpr int kMaxAttnSeqs = 2048;   // sequences one bf16 attention launch can cover
+
 struct AttnPlan {
-  int chunk_pages, n_chunks, nq_pad;
+  int chunk_pages, n_chunks;   // fp32 path
+  int n_wg, hdr_floats;        // bf16 persistent path
+  int nq_pad;
+  bool ok;                     // false: shapes beyond what one launch can cover
   size_t bytes;
 };
 
-AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int dtype);
+AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int dtype,
+                        int num_cus);
 
 hipError_t launch_route(const RouteArgs& a, hipStream_t stream);
 hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_t stream);

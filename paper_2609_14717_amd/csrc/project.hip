@@ -100,27 +100,6 @@ __device__ void kv_store(const KvDest& e, int row, int seg, int i0, const float*
   }
 }
 
-// s_waitcnt vmcnt(n) on gfx9: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14;
-// expcnt (6:4) and lgkmcnt (11:8) left at "no wait".
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
-template <int NL, int NSTAGE>
-__device__ __forceinline__ void wait_stages_ahead(int ahead) {
-  // at most NSTAGE-1 later stages may stay in flight
-  if constexpr (NSTAGE >= 4) {
-    if (ahead >= 3) { wait_vmcnt<3 * NL>(); return; }
-  }
-  if constexpr (NSTAGE >= 3) {
-    if (ahead >= 2) { wait_vmcnt<2 * NL>(); return; }
-  }
-  if (ahead >= 1) { wait_vmcnt<NL>(); return; }
-  wait_vmcnt<0>();
-}
-
 // Workgroup barrier for the staged ring.  Each wavefront has already waited
 // (vmcnt) for its own direct-to-LDS loads of the stage it is about to read, and
 // LDS reads are complete once their values feed the MFMAs, so no memory fence
@@ -131,42 +110,6 @@ __device__ __forceinline__ void stage_barrier() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
-}
-
-// Groups of 16-byte LDS reads issued as inline asm, each group ending with its
-// own lgkmcnt(0) so that the outputs are complete when the statement ends.
-// The compiler cannot tell which ring slot an in-flight direct-to-LDS load
-// targets and would otherwise wait for all of them (vmcnt(0)) before every LDS
-// read; readiness of the slot being read is guaranteed by the explicit vmcnt
-// wait and barrier of each stage instead.
-__device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
-  typedef __attribute__((address_space(3))) const unsigned char* lds_ptr;
-  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr)p));
-}
-
-template <int N>
-__device__ __forceinline__ void lds_read_group(u16x8 (&v)[N], const uint32_t (&a)[N]);
-
-template <>
-__device__ __forceinline__ void lds_read_group<1>(u16x8 (&v)[1], const uint32_t (&a)[1]) {
-  asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)"
-               : "=&v"(v[0]) : "v"(a[0]) : "memory");
-}
-
-template <>
-__device__ __forceinline__ void lds_read_group<2>(u16x8 (&v)[2], const uint32_t (&a)[2]) {
-  asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %3\n\ts_waitcnt lgkmcnt(0)"
-               : "=&v"(v[0]), "=&v"(v[1]) : "v"(a[0]), "v"(a[1]) : "memory");
-}
-
-template <>
-__device__ __forceinline__ void lds_read_group<4>(u16x8 (&v)[4], const uint32_t (&a)[4]) {
-  asm volatile(
-      "ds_read_b128 %0, %4\n\tds_read_b128 %1, %5\n\tds_read_b128 %2, %6\n\t"
-      "ds_read_b128 %3, %7\n\ts_waitcnt lgkmcnt(0)"
-      : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3])
-      : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3])
-      : "memory");
 }
 
 // ------------------------------------------------------------ bf16 MFMA GEMM
@@ -226,11 +169,11 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
       } else {
         src = Bw + static_cast<int64_t>(min(n0 + row - BM, g.N - 1)) * g.K + kk;
       }
-      __builtin_amdgcn_global_load_lds(src, st + i * 1024, 16, 0, 0);
+      lds_dma16(src, st + i * 1024);
     }
     if constexpr (HAS_E) {
       const int kk = min(k0 + (lane & 15) * 8, g.K - 8);
-      __builtin_amdgcn_global_load_lds(E + kk, st + E_OFF + wave * 1024, 16, 0, 0);
+      lds_dma16(E + kk, st + E_OFF + wave * 1024);
     }
   };
 

@@ -128,7 +128,7 @@ def test_small_workspace_rejected():
     need_p = co.workspace_bytes(d, co.CO_WS_PROJECT)
     need_a = co.workspace_bytes(d, co.CO_WS_ATTENTION)
     assert need_p > 0 and need_a > 0
-    assert co.workspace_bytes(d, co.CO_WS_ROUND) == max(need_p, need_a)
+    assert co.workspace_bytes(d, co.CO_WS_ROUND) == need_p + need_a
     W = co.weights(FAKE, FAKE, FAKE)
     assert _rc(lambda: co.carryover_project_kv(d, W, FAKE, _fake_route(), _fake_state(), FAKE,
                                                stream=0, ws_bytes=need_p - 1)) \
@@ -146,3 +146,11 @@ def test_import_range_checked_on_host():
         rc = lib.carryover_import_kv(ctypes.byref(d), seq, pos0, n, FAKE, FAKE, ctypes.byref(s),
                                      None)
         assert rc == co.CO_ERR_INVALID_ARG
+
+
+def test_library_has_no_undefined_kernel_stubs():
+    """Every kernel launched by the host code has its host-side stub (a kernel
+    template whose host pass fails is otherwise dropped without a diagnostic)."""
+    out = subprocess.run(["nm", "-D", "--undefined-only", co.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    assert "device_stub" not in out, out
