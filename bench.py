@@ -16,6 +16,8 @@ attention kernel's roofline fraction and an fp64 CPU oracle baseline.
 from __future__ import annotations
 
 import argparse
+import csv
+import hashlib
 import json
 import os
 import sys
@@ -27,6 +29,12 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+# sources of the attention kernels: traffic counters taken on another version
+# of these are not reported
+ATTN_SOURCES = [os.path.join(ROOT, "paper_2609_14717_amd", "csrc", f)
+                for f in ("attention.hip", "co_device.h", "co_kernels.h")]
+ATTN_KERNELS = ("attn_bf16_kernel", "attn_bf16_combine_kernel")
 
 
 def parse():
@@ -37,7 +45,136 @@ def parse():
     ap.add_argument("--workload", default="ragged_batch32")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mb", type=int, default=0,
+                    help="after the timed region, run one plain copy of this many MiB "
+                         "(the reference kernel for byte-counter calibration)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write the attention traffic summary from two rocprofv3 --pmc runs "
+                         "(FETCH_SIZE, then WRITE_SIZE) and exit")
+    ap.add_argument("--summarize-stats", metavar="STATS_CSV",
+                    help="write the kernel-time summary of a rocprofv3 --stats run and exit")
+    ap.add_argument("--command", default="", help="command recorded in a summary")
     return ap.parse_args()
+
+
+def attention_digest():
+    h = hashlib.sha256()
+    for f in ATTN_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_file(workload):
+    return os.path.join(PROFILES, f"attention_traffic_{workload}.txt")
+
+
+def recorded_traffic(workload):
+    """HBM bytes per attention launch from the committed counter summary, or
+    None when there is none or the kernels changed since it was taken."""
+    path = traffic_file(workload)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line:
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("attention_source_digest") != attention_digest():
+        return None
+    try:
+        return float(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def _counter_means(run_dir):
+    """Mean counter value per dispatch, per kernel name, from a --pmc run."""
+    import glob
+    files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {run_dir}")
+    acc = {}
+    for f in files:
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                per = acc.setdefault((r["Kernel_Name"], r["Counter_Name"]), {})
+                did = r["Dispatch_Id"]
+                per[did] = per.get(did, 0.0) + float(r["Counter_Value"])
+    return {k: (sum(v.values()) / len(v), len(v)) for k, v in acc.items()}
+
+
+def summarize_pmc(args):
+    fetch = _counter_means(args.summarize_pmc[0])
+    write = _counter_means(args.summarize_pmc[1])
+    copy_bytes = args.calibrate_copy_mb * (1 << 20)
+    if copy_bytes <= 0:
+        raise SystemExit("--calibrate-copy-mb must give the copy size of the profiled runs")
+
+    def pick(table, counter, pattern):
+        rows = [(k[0], v) for k, v in table.items() if k[1] == counter and pattern in k[0]]
+        if not rows:
+            raise SystemExit(f"no {counter} rows for {pattern}")
+        return rows
+
+    def one(table, counter, name):
+        rows = pick(table, counter, name)
+        return sum(v[0] for _, v in rows), sum(v[1] for _, v in rows)
+
+    cf, _ = one(fetch, "FETCH_SIZE", "copy16_kernel")
+    cw, _ = one(write, "WRITE_SIZE", "copy16_kernel")
+    f_fac = copy_bytes / (cf * 1024.0)
+    w_fac = copy_bytes / (cw * 1024.0)
+    lines = [f"# HBM traffic of drafter_block_attention, workload {args.workload}",
+             f"command (FETCH_SIZE pass): {args.command.replace('{COUNTER}', 'FETCH_SIZE')}",
+             f"command (WRITE_SIZE pass): {args.command.replace('{COUNTER}', 'WRITE_SIZE')}",
+             f"attention_source_digest: {attention_digest()}",
+             f"copy_kernel_bytes: {copy_bytes}",
+             f"copy FETCH_SIZE KiB: {cf:.1f}  (factor {f_fac:.4f})",
+             f"copy WRITE_SIZE KiB: {cw:.1f}  (factor {w_fac:.4f})"]
+    tot = 0.0
+    for kn in ATTN_KERNELS:
+        kf, nf = one(fetch, "FETCH_SIZE", kn)
+        kw, nw = one(write, "WRITE_SIZE", kn)
+        b = kf * 1024.0 * f_fac + kw * 1024.0 * w_fac
+        tot += b
+        lines.append(f"{kn}: FETCH_SIZE {kf:.1f} KiB/dispatch ({nf} dispatches), "
+                     f"WRITE_SIZE {kw:.1f} KiB/dispatch ({nw} dispatches), "
+                     f"calibrated {b / 1e6:.3f} MB")
+    lines.append(f"traffic_bytes_per_launch: {tot:.0f}")
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(traffic_file(args.workload), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def summarize_stats(args):
+    rows = []
+    with open(args.summarize_stats) as fh:
+        for r in csv.DictReader(fh):
+            rows.append((r["Name"], int(r["Calls"]), float(r["AverageNs"]) / 1e3,
+                         float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3,
+                         float(r["Percentage"])))
+    rows.sort(key=lambda x: -x[1] * x[2])
+    lines = [f"# rocprofv3 kernel statistics, workload {args.workload}",
+             f"command: {args.command}",
+             "",
+             f"{'kernel':90s} {'calls':>6s} {'avg_us':>8s} {'min_us':>8s} {'max_us':>8s} {'pct':>6s}"]
+    for n, c, a, lo, hi, pct in rows:
+        short = n if len(n) <= 90 else n[:87] + "..."
+        lines.append(f"{short:90s} {c:6d} {a:8.2f} {lo:8.2f} {hi:8.2f} {pct:6.2f}")
+    att = [(k, r) for k in ATTN_KERNELS for r in rows
+           if "::" + k + "<" in r[0] or "::" + k + "(" in r[0]]
+    if att:
+        lines += ["", "drafter_block_attention = " + " + ".join(
+            f"{k} {r[2]:.2f} us" for k, r in att) +
+            f" = {sum(r[2] for _, r in att):.2f} us per launch (kernel time, no launch gaps)"]
+    os.makedirs(PROFILES, exist_ok=True)
+    out = os.path.join(PROFILES, f"kernel_stats_{args.workload}.txt")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
 
 
 def attention_bytes(w, ctx, carry):
@@ -73,6 +210,10 @@ def cpu_baseline(w, budget_s):
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        return summarize_pmc(args)
+    if args.summarize_stats:
+        return summarize_stats(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the drafter step "
               "shards by sequence with no exchange, so multi-GPU runs are not part of this "
@@ -143,6 +284,15 @@ def main():
     status = co.carryover_read_status(sc.st)
     if status:
         raise RuntimeError(f"device status {co.status_string(status)}")
+    if args.calibrate_copy_mb > 0:
+        from synth import device as sdev
+        nb = args.calibrate_copy_mb << 20
+        src = torch.ones(nb // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        sdev.copy_bytes(dst, src, nb)
+        torch.cuda.synchronize()
+        del src, dst
 
     att_ms = [a.elapsed_time(b) for a, b in ev]
     att_s = float(np.sum(att_ms)) / 1e3
@@ -167,9 +317,11 @@ def main():
                    "model_dim": w.d, "layers": w.L, "q_heads": w.Hq, "kv_heads": w.Hkv,
                    "head_dim": w.hd, "ctx0": [w.ctx_lo, w.ctx_hi], "accept": list(w.accept),
                    "chained_rounds": total, "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": "drafter_block_attention",
+        "roofline": {"bound": "hbm",
+                     "kernel": "drafter_block_attention (" + " + ".join(ATTN_KERNELS) + ")",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": recorded_traffic(w.name),
                      "algorithmic_bytes_per_launch": per_launch,
                      "avg_launch_us": att_s / args.steps * 1e6},
     }

@@ -83,6 +83,7 @@ __device__ __forceinline__ int64_t out_row(const AttnArgs& a, int layer_local, i
 // maxima and sums of all chunks are staged in LDS with one round of independent
 // loads and turned into per-(chunk, query) weights.
 constexpr int kMaxMergeChunks = 64;
+constexpr int kMaxMergeSlices = 4096;   // workgroups of one persistent launch
 
 template <typename T>
 __global__ __launch_bounds__(256) void attn_chunk_merge_kernel(AttnArgs a, int chunk_pages,
@@ -310,17 +311,13 @@ __device__ __forceinline__ int64_t slice_begin(int64_t T, int w, int n_wg) {
   return T * w / n_wg;
 }
 
-// Workgroup whose slice holds global tile x.
-__device__ __forceinline__ int slice_owner(int64_t T, int64_t x, int n_wg) {
-  int w = static_cast<int>(x * n_wg / T);
-  while (w + 1 < n_wg && slice_begin(T, w + 1, n_wg) <= x) ++w;
-  while (w > 0 && slice_begin(T, w, n_wg) > x) --w;
-  return w;
-}
+// Workspace of the persistent path: a header with the tile prefix sums (S+1
+// ints, written by workgroup 0) and the first global tile of every slice
+// (n_wg+1 int64 from int offset slice_bounds_off(S), each written by its
+// workgroup), both for the combine kernel; then one record per (slice,
+// segment) pair: O[NQP][hd] unnormalised, m[NQP], l[NQP].
+__host__ __device__ __forceinline__ int slice_bounds_off(int S) { return (S + 2) & ~1; }
 
-// Workspace of the persistent path: tile prefix sums (S+1 ints, written by
-// workgroup 0 for the combine kernel), then one record per (slice, segment)
-// pair: O[NQP][hd] unnormalised, m[NQP], l[NQP].
 __device__ __forceinline__ float* slot_ptr(const AttnArgs& a, int hdr_floats, int64_t slot,
                                            int nqp) {
   return a.ws + hdr_floats + slot * nqp * (a.hd + 2);
@@ -389,12 +386,16 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
   }
   const int T1 = tstart[S];
   const int64_t T = static_cast<int64_t>(layer_count) * a.Hkv * T1;
-  if (blockIdx.x == 0) {
-    int* hdr = reinterpret_cast<int*>(a.ws);
-    for (int i = tid; i <= S; i += NTHR) hdr[i] = tstart[i];
-  }
   const int w = blockIdx.x;
   const int64_t r1 = slice_begin(T, w + 1, n_wg);
+  {
+    int* hdr = reinterpret_cast<int*>(a.ws);
+    if (w == 0)
+      for (int i = tid; i <= S; i += NTHR) hdr[i] = tstart[i];
+    int64_t* bounds = reinterpret_cast<int64_t*>(hdr + slice_bounds_off(S));
+    if (tid == 0) bounds[w + 1] = r1;
+    if (tid == 0 && w == 0) bounds[0] = 0;
+  }
 
   const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
   const uint16_t* vc = static_cast<const uint16_t*>(a.v_cache);
@@ -769,14 +770,27 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
       for (int qn = tid; qn < nq; qn += 256) a.lse[out_row(a, layer_local, s, g, qn, G)] = -INFINITY;
     return;
   }
-  const int64_t T = static_cast<int64_t>(layer_count) * a.Hkv * T1;
   const int64_t A = static_cast<int64_t>(seg) * T1 + hdr[s];
-  const int w_lo = slice_owner(T, A, n_wg), w_hi = slice_owner(T, A + nts - 1, n_wg);
+  const int64_t* bounds = reinterpret_cast<const int64_t*>(hdr + slice_bounds_off(a.S));
+  // slice w holds global tiles [bounds[w], bounds[w+1]); find the owners of the
+  // segment's first and last tile (bounds is non-decreasing)
+  auto owner = [&](int64_t x) {
+    int lo = 0, hi = n_wg;                  // bounds[lo] <= x < bounds[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (bounds[mid] <= x) lo = mid; else hi = mid;
+    }
+    return lo;
+  };
+  const int w_lo = owner(A), w_hi = owner(A + nts - 1);
   if (w_lo == w_hi) return;            // finished in place
   const int nrec = w_hi - w_lo + 1;
+  __shared__ float live_lds[kMaxMergeSlices];
+  for (int i = tid; i < nrec; i += 256)   // an empty slice left no record
+    live_lds[i] = bounds[w_lo + i] < bounds[w_lo + i + 1] ? 1.f : 0.f;
+  __syncthreads();
   const int64_t rec = static_cast<int64_t>(nq_pad) * (hd + 2);
-  // records of consecutive slices are consecutive slots; a slice can be empty when
-  // there are fewer tiles than workgroups, and then it left no record
+  // records of consecutive slices of one segment are consecutive slots
   const float* base = slot_ptr(a, hdr_floats, w_lo + static_cast<int64_t>(seg) * a.S + s, nq_pad);
   for (int idx = tid + blockIdx.z * 256; idx < nq * q4; idx += 256 * gridDim.z) {
     const int qn = idx / q4, d = (idx % q4) * 4;
@@ -788,8 +802,7 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
       for (int i = 0; i < kBatch; ++i) mv[i] = r0 + i < nrec ? pm[(r0 + i) * rec] : -INFINITY;
 #pragma unroll
       for (int i = 0; i < kBatch; ++i)
-        if (r0 + i < nrec && slice_begin(T, w_lo + r0 + i, n_wg) < slice_begin(T, w_lo + r0 + i + 1, n_wg))
-          M = fmaxf(M, mv[i]);
+        if (r0 + i < nrec && live_lds[r0 + i] != 0.f) M = fmaxf(M, mv[i]);
     }
     float den = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -806,8 +819,7 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
       }
 #pragma unroll
       for (int i = 0; i < kBatch; ++i) {
-        const bool live = r0 + i < nrec &&
-                          slice_begin(T, w_lo + r0 + i, n_wg) < slice_begin(T, w_lo + r0 + i + 1, n_wg);
+        const bool live = r0 + i < nrec && live_lds[r0 + i] != 0.f;
         const float wgt = (!live || mv[i] == -INFINITY) ? 0.f : exp2f(mv[i] - M);
         den += wgt * lv[i];
         acc += wgt * ov[i];
@@ -834,14 +846,13 @@ AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pa
   const int max_lp = max_pages + cp;
   p.ok = true;
   if (dtype == CO_DTYPE_BF16) {
-    // persistent path: one workgroup per CU, records for (slice, segment) pairs
-    p.n_wg = num_cus;
-    if (const char* env = getenv("CO_ATTN_WORKGROUPS")) {   // tuning override
-      const int v = atoi(env);
-      if (v >= 1 && v <= 65536) p.n_wg = v;
-    }
-    p.hdr_floats = (S + 1 + 63) / 64 * 64;
-    p.ok = S <= kMaxAttnSeqs;
+    // persistent path: a fixed number of workgroups per CU, records for
+    // (slice, segment) pairs
+    p.variant = 1;
+    if (const char* env = getenv("CO_ATTN_VARIANT")) p.variant = atoi(env) & 3;   // tuning
+    p.n_wg = num_cus * (p.variant == 1 && hd == 64 ? 2 : 1);
+    p.hdr_floats = (slice_bounds_off(S) + 2 * (p.n_wg + 1) + 63) / 64 * 64;
+    p.ok = S <= kMaxAttnSeqs && p.n_wg <= kMaxMergeSlices;
     p.bytes = (static_cast<size_t>(p.hdr_floats) +
                (static_cast<size_t>(p.n_wg) + static_cast<size_t>(L) * Hkv * S) * p.nq_pad *
                    (hd + 2)) * 4;
@@ -868,12 +879,16 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
 #define CO_ATTN_LAUNCH(HD, NT, NW, NS)                                                         \
   hipLaunchKernelGGL((attn_bf16_kernel<HD, NT, NW, NS>), grid, dim3(64 * NW), 0, stream, a,     \
                      layer_count, p.n_wg, p.hdr_floats)
-    if (a.hd == 64) {
+    if (a.hd == 64 && nt == 2 && p.variant == 0) {
+      CO_ATTN_LAUNCH(64, 2, 4, 4);
+    } else if (a.hd == 64 && nt == 2 && p.variant == 2) {
+      CO_ATTN_LAUNCH(64, 2, 8, 2);
+    } else if (a.hd == 64) {
       switch (nt) {
-        case 1: CO_ATTN_LAUNCH(64, 1, 4, 4); break;
-        case 2: CO_ATTN_LAUNCH(64, 2, 4, 4); break;
-        case 3: CO_ATTN_LAUNCH(64, 3, 4, 4); break;
-        default: CO_ATTN_LAUNCH(64, 4, 4, 4); break;
+        case 1: CO_ATTN_LAUNCH(64, 1, 4, 2); break;
+        case 2: CO_ATTN_LAUNCH(64, 2, 4, 2); break;
+        case 3: CO_ATTN_LAUNCH(64, 3, 4, 2); break;
+        default: CO_ATTN_LAUNCH(64, 4, 4, 2); break;
       }
     } else {
       switch (nt) {

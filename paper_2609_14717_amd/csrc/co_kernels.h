@@ -77,6 +77,7 @@ constexpr int kMaxAttnSeqs = 2048;   // sequences one bf16 attention launch can 
 struct AttnPlan {
   int chunk_pages, n_chunks;   // fp32 path
   int n_wg, hdr_floats;        // bf16 persistent path
+  int variant;                 // bf16 persistent path: wavefronts / ring depth / occupancy
   int nq_pad;
   bool ok;                     // false: shapes beyond what one launch can cover
   size_t bytes;

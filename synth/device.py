@@ -36,7 +36,22 @@ def _load():
                                            ctypes.POINTER(ctypes.c_int64),
                                            ctypes.POINTER(ctypes.c_int64), ctypes.c_int64,
                                            ctypes.c_uint64, ctypes.c_float, ctypes.c_void_p]
+        _lib.synth_copy.restype = ctypes.c_int
+        _lib.synth_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                    ctypes.c_void_p]
     return _lib
+
+
+def copy_bytes(dst, src, nbytes: int, stream=None):
+    """Plain device copy of ``nbytes`` (a multiple of 16) between CUDA tensors."""
+    import torch
+    assert dst.is_cuda and src.is_cuda and nbytes % 16 == 0
+    assert dst.numel() * dst.element_size() >= nbytes <= src.numel() * src.element_size()
+    s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+    rc = _load().synth_copy(ctypes.c_void_p(dst.data_ptr()), ctypes.c_void_p(src.data_ptr()),
+                            nbytes, ctypes.c_void_p(s))
+    if rc != 0:
+        raise RuntimeError(f"synth_copy failed ({rc})")
 
 
 def fill(tensor, key: int, spec_shape, spec_strides, base: int, sigma: float, stream=None):

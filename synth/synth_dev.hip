@@ -41,7 +41,26 @@ __global__ void fill_normal_kernel(void* out, int bf16, int64_t n, Layout lay, i
   }
 }
 
+// Plain 16-byte copy: the reference kernel of known traffic against which
+// hardware byte counters are calibrated.
+__global__ void copy16_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst, int64_t n) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride)
+    dst[i] = src[i];
+}
+
 }  // namespace
+
+extern "C" int synth_copy(void* dst, const void* src, int64_t bytes, hipStream_t stream) {
+  if (!dst || !src || bytes < 0 || bytes % 16) return 1;
+  const int64_t n = bytes / 16;
+  if (n == 0) return 0;
+  const int64_t want = (n + 255) / 256;
+  const unsigned blocks = static_cast<unsigned>(want < 8192 ? want : 8192);
+  hipLaunchKernelGGL(copy16_kernel, dim3(blocks), dim3(256), 0, stream,
+                     static_cast<const uint4*>(src), static_cast<uint4*>(dst), n);
+  return hipGetLastError() == hipSuccess ? 0 : 2;
+}
 
 extern "C" int synth_fill_normal(void* out, int bf16, int ndim, const int64_t* shape,
                                  const int64_t* stride, int64_t base, uint64_t key, float scale,
