@@ -20,7 +20,7 @@ the "Cache semantics" paragraph; Section 2 "Preliminaries"):
   with a plain softmax; the baseline update (left column of Algorithm 1)
   projects only rows 0..m-1 and has no U.
 
-Readings where the paper is silent (each also listed in the design doc): no norm
+Readings where the paper is silent (each one a stated choice of this oracle): no norm
 and no bias in F, K_l, V_l; rotate-half RoPE with inverse frequency
 theta^(-2i/hd); softmax scale 1/sqrt(hd); query head h reads KV head
 h // (Hq/Hkv); window row j sits at position ctx_len_before + j; block queries

@@ -84,6 +84,8 @@ __device__ __forceinline__ int64_t out_row(const AttnArgs& a, int layer_local, i
 // loads and turned into per-(chunk, query) weights.
 constexpr int kMaxMergeChunks = 64;
 constexpr int kMaxMergeSlices = 4096;   // workgroups of one persistent launch
+constexpr int kAttnWaves64 = 8, kAttnWaves128 = 4;             // wavefronts per workgroup
+constexpr int kAttnRoundTiles64 = 64, kAttnRoundTiles128 = 128; // tiles per wavefront per round
 
 template <typename T>
 __global__ __launch_bounds__(256) void attn_chunk_merge_kernel(AttnArgs a, int chunk_pages,
@@ -189,7 +191,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnArgs a, int chunk_pag
     float lo = qrow[p], hi = qrow[p + HD / 2];
     if (!(a.flags & CO_Q_PREROTATED)) {
       float cs, sn;
-      rope_cos_sin(ctx + n / G, rope_inv_freq(p, HD, a.log2_theta), &cs, &sn);
+      rope_cos_sin(ctx + n / G, a.rope_inv[p], &cs, &sn);
       const float l2 = lo * cs - hi * sn, h2 = hi * cs + lo * sn;
       lo = l2;
       hi = h2;
@@ -298,40 +300,63 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnArgs a, int chunk_pag
 }
 
 // ------------------------------------------------------- bf16 persistent path
-
-// Tiles (32 keys = 2 logical pages) of sequence s; sequences with invalid
-// lengths have none (the combine kernel reports them).
-__device__ __forceinline__ int seq_tiles(const AttnArgs& a, int s) {
-  const SeqInfo q = seq_info(a, s, 1);
-  return (q.npt + 1) / 2;
-}
-
-// First tile of workgroup w's slice of T tiles split over n_wg workgroups.
-__device__ __forceinline__ int64_t slice_begin(int64_t T, int w, int n_wg) {
-  return T * w / n_wg;
-}
-
-// Workspace of the persistent path: a header with the tile prefix sums (S+1
-// ints, written by workgroup 0) and the first global tile of every slice
-// (n_wg+1 int64 from int offset slice_bounds_off(S), each written by its
-// workgroup), both for the combine kernel; then one record per (slice,
-// segment) pair: O[NQP][hd] unnormalised, m[NQP], l[NQP].
-__host__ __device__ __forceinline__ int slice_bounds_off(int S) { return (S + 2) & ~1; }
+//
+// The key tiles (32 keys = two logical pages) of all segments form one global
+// order: segment (layer_local * Hkv + g) major, then sequence, then tile
+// (committed pages first, then carry pages).  Global tile indices fit in int32
+// (checked on the host).  Workgroup w owns the slice [T*w/n_wg, T*(w+1)/n_wg).
+//
+// Workspace of this path:
+//   header (ints): tstart[S+1], the tiles before each sequence within a segment
+//     (written by workgroup 0), then bounds[n_wg+1], the first tile of every
+//     slice (each written by its workgroup);
+//   records: one per (slice w, segment sigma = seg*S + s) pair, at slot
+//     w + sigma -- injective over the pairs that occur because slices and
+//     segments both follow the tile order: O[NQP][hd] unnormalised, m[NQP],
+//     l[NQP] (m in log2 units of the scaled logits);
+//   parked partials (large query tiles only): one record-shaped area per
+//     wavefront, for a piece that another wavefront of the workgroup merges.
 
 __device__ __forceinline__ float* slot_ptr(const AttnArgs& a, int hdr_floats, int64_t slot,
                                            int nqp) {
   return a.ws + hdr_floats + slot * nqp * (a.hd + 2);
 }
 
-template <int HD, int NT, int NW, int NS>
+// The part of one segment that lies in one slice (global tile indices).
+struct Piece {
+  int seg_begin, seg_end;   // the segment
+  int begin, end;           // the piece
+  int s, seg, ctx, carry;
+};
+
+template <int N>
+__device__ __forceinline__ int pick_reg(const int (&v)[N], int i) {
+  int r = v[0];
+#pragma unroll
+  for (int k = 1; k < N; ++k) r = (i == k) ? v[k] : r;
+  return r;
+}
+
+// cos/sin of pos * inv_freq with the angle reduced to revolutions in fp64 and
+// the hardware sine/cosine (which take revolutions); bf16 queries only.
+__device__ __forceinline__ void rope_cos_sin_rev(int pos, double inv_freq_rev, float* c, float* s) {
+  double r = static_cast<double>(pos) * inv_freq_rev;
+  r -= rint(r);
+  const float rf = static_cast<float>(r);
+  *c = __builtin_amdgcn_cosf(rf);
+  *s = __builtin_amdgcn_sinf(rf);
+}
+
+template <int HD, int NT, int NW, int NS, int PQ, int RTM>
 __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int layer_count, int n_wg,
-                                                             int hdr_floats) {
+                                                             int hdr_floats, int round_tiles,
+                                                             int64_t park_off) {
   constexpr int KS = HD / 32;              // k-steps of S^T
   constexpr int MT = HD / 16;              // M-tiles of O^T
   constexpr int NQP = NT * 16;
   constexpr int NTHR = 64 * NW;
   constexpr int QLD = HD + 8;              // padded LDS row of rotated queries (bf16)
-  constexpr int NRED = NW > 1 ? NW - 1 : 1;
+  constexpr int QSZ = NQP * QLD;
   constexpr int ROWB = HD * 2;             // bytes of one key row
   constexpr int CPR = ROWB / 16;           // 16-byte chunks per key row
   constexpr int PAGE_BYTES = kPage * ROWB; // one page of K (or of V)
@@ -339,63 +364,36 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
   constexpr int TILE_BYTES = 4 * PAGE_BYTES;   // K page 0, K page 1, V page 0, V page 1
   constexpr int NL = 4 * LPP;              // direct-to-LDS loads per tile per wave
   constexpr int RING_BYTES = NW * NS * TILE_BYTES;
-  constexpr int RED_BYTES = (NRED * NQP * (HD + 1) + 2 * NRED * NQP) * 4;
-  constexpr int SMEM_BYTES = RING_BYTES > RED_BYTES ? RING_BYTES : RED_BYTES;
-  constexpr int SUB_TILES = kMaxChunkPages / 2;
+  constexpr int SLOT_LD = HD + 4;          // 16-byte aligned rows
+  constexpr int SLOT_FLOATS = NQP * SLOT_LD + 2 * NQP;
+  constexpr bool PARK_REGS = HD * NT <= 128;   // parked partial fits in 32 registers
+  constexpr int RQ = RTM / 32;             // page-descriptor registers (64 pages each)
+  constexpr int PMAX = 64;                 // pieces enumerated per pass
+  constexpr int QV = (PQ * NQP * (HD / 8) + NTHR - 1) / NTHR;   // 4-pair query groups per thread
+  constexpr int SPT = (kMaxAttnSeqs + NTHR - 1) / NTHR;         // sequences per thread (max)
   static_assert(NL * (NS - 1) < 64, "vmcnt");
-  // the ring, reused for the cross-wave merge once a segment is done
-  __shared__ __align__(16) unsigned char smem[SMEM_BYTES];
-  __shared__ __align__(16) uint16_t q_lds[NQP * QLD];
-  __shared__ int pg_lds[kMaxChunkPages];
-  __shared__ int tstart[kMaxAttnSeqs + 1];
+  static_assert(!PARK_REGS || NW * SLOT_FLOATS * 4 <= RING_BYTES, "merge slots");
+  static_assert((5 * kMaxAttnSeqs + 2) * 4 <= RING_BYTES, "set-up arrays");
+  static_assert(RTM % 32 == 0 && PQ <= PMAX, "round shape");
+  // the ring; the set-up arrays and the merge slots overlay it
+  __shared__ __align__(16) unsigned char smem[RING_BYTES];
+  __shared__ __align__(16) uint16_t q_lds[PQ * QSZ];
+  __shared__ Piece pc[PMAX];
   __shared__ double inv_lds[HD / 2];
-  __shared__ int wave_tot[NW];
-  float* red_o = reinterpret_cast<float*>(smem);                 // [NRED][NQP][HD + 1]
-  float* red_m = red_o + NRED * NQP * (HD + 1);                  // [NRED][NQP]
-  float* red_l = red_m + NRED * NQP;                             // [NRED][NQP]
+  __shared__ int scan_tot[2 * NW];
+  __shared__ int next_rot, first_seq;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = lane >> 4, col = lane & 15;
   const int S = a.S, G = a.Hq / a.Hkv, nq = a.B * G;
-
-  // ---- tiles per sequence and their prefix sums (the same for every segment row)
-  {
-    const int per = (S + NTHR - 1) / NTHR, s0 = tid * per;
-    int local = 0;
-    for (int i = 0; i < per; ++i)
-      if (s0 + i < S) local += seq_tiles(a, s0 + i);
-    int v = local;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int u = __shfl_up(v, off);
-      if (lane >= off) v += u;
-    }
-    if (lane == 63) wave_tot[wave] = v;
-    if (tid < HD / 2) inv_lds[tid] = rope_inv_freq(tid, HD, a.log2_theta);
-    __syncthreads();
-    int run = v - local;
-    for (int w = 0; w < wave; ++w) run += wave_tot[w];
-    for (int i = 0; i < per; ++i)
-      if (s0 + i < S) {
-        tstart[s0 + i] = run;
-        run += seq_tiles(a, s0 + i);
-      }
-    if (tid == NTHR - 1) tstart[S] = run;
-    __syncthreads();
-  }
-  const int T1 = tstart[S];
-  const int64_t T = static_cast<int64_t>(layer_count) * a.Hkv * T1;
   const int w = blockIdx.x;
-  const int64_t r1 = slice_begin(T, w + 1, n_wg);
-  {
-    int* hdr = reinterpret_cast<int*>(a.ws);
-    if (w == 0)
-      for (int i = tid; i <= S; i += NTHR) hdr[i] = tstart[i];
-    int64_t* bounds = reinterpret_cast<int64_t*>(hdr + slice_bounds_off(S));
-    if (tid == 0) bounds[w + 1] = r1;
-    if (tid == 0 && w == 0) bounds[0] = 0;
-  }
+  const int n_segs = layer_count * a.Hkv;
+  int* tstart = reinterpret_cast<int*>(smem);   // [S+1]
+  int* nstart = tstart + (S + 1);               // [S+1] non-empty sequences before s
+  int* ne_seq = nstart + (S + 1);               // [S]   the k-th non-empty sequence
+  int* ctx_s = ne_seq + S;                      // [S]
+  int* carry_s = ctx_s + S;                     // [S]
 
   const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
   const uint16_t* vc = static_cast<const uint16_t*>(a.v_cache);
@@ -403,6 +401,9 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
   const uint16_t* vk = static_cast<const uint16_t*>(a.v_carry);
   const float qscale = rsqrtf(static_cast<float>(HD)) * kLog2e;
   const uint16_t* Q = static_cast<const uint16_t*>(a.q);
+  const bool rotate_q = !(a.flags & CO_Q_PREROTATED);
+  if (tid < HD / 2)   // in revolutions per position
+    inv_lds[tid] = a.rope_inv[tid] * 0.15915494309189533577;
   // key of S^T M-tile a / b at row rho = lane % 16: keys {8q + r} and {8q + 4 + r}
   const int key_a = 8 * (col >> 2) + (col & 3);
   const int key_b = key_a + 4;
@@ -421,12 +422,12 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
   // LDS byte offsets (within a tile) of this lane's K and V fragments
   uint32_t ka_off[KS], kb_off[KS], v_frag_off;
   {
-    const int ra = key_a & 15, rb = key_b & 15;
+    const int ra_ = key_a & 15, rb_ = key_b & 15;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const int ch = ks * 4 + grp;
-      ka_off[ks] = (key_a >> 4) * PAGE_BYTES + ra * ROWB + ((ch ^ (ra & (CPR - 1))) << 4);
-      kb_off[ks] = (key_b >> 4) * PAGE_BYTES + rb * ROWB + ((ch ^ (rb & (CPR - 1))) << 4);
+      ka_off[ks] = (key_a >> 4) * PAGE_BYTES + ra_ * ROWB + ((ch ^ (ra_ & (CPR - 1))) << 4);
+      kb_off[ks] = (key_b >> 4) * PAGE_BYTES + rb_ * ROWB + ((ch ^ (rb_ & (CPR - 1))) << 4);
     }
     v_frag_off = (2 + (grp >> 1)) * PAGE_BYTES + col * 32 + slot_base * 2;
   }
@@ -435,113 +436,344 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
   // leaves the normalised result unchanged and skips most rescales.
   constexpr float kRescale = 8.f;
 
-  for (int64_t cur = slice_begin(T, w, n_wg); cur < r1;) {
-    // ---- locate the segment (layer, kv head, sequence) holding global tile cur
-    const int seg = static_cast<int>(cur / T1);
-    const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
-    const int layer = a.layer_begin + layer_local;
-    const int rr = static_cast<int>(cur % T1);
-    int lo = 0, hi = S;
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (tstart[mid] <= rr) lo = mid; else hi = mid;
-    }
-    const int s = lo;
-    const int j0 = rr - tstart[s];
-    const int nts = tstart[s + 1] - tstart[s];
-    const int n = static_cast<int>(min(r1 - cur, static_cast<int64_t>(nts - j0)));
-    const bool whole = j0 == 0 && n == nts;
-    const SeqInfo si = seq_info(a, s, 1);
-    const int64_t kv_layer = (static_cast<int64_t>(layer) * a.num_pages) * a.Hkv + g;
-    const int64_t carry_base = ((static_cast<int64_t>(layer) * a.S + s) * a.CP) * a.Hkv + g;
-
-    // ---- queries of this segment: rotate at ctx + i, fold 1/sqrt(hd)*log2(e), bf16 in LDS
-    for (int idx = tid; idx < NQP * (HD / 2); idx += NTHR) {
-      const int qn = idx / (HD / 2), p = idx % (HD / 2);
-      float qlo = 0.f, qhi = 0.f;
-      if (qn < nq) {
-        const uint16_t* qrow = Q + out_row(a, layer_local, s, g, qn, G) * HD;
-        qlo = bf2f(qrow[p]);
-        qhi = bf2f(qrow[p + HD / 2]);
-        if (!(a.flags & CO_Q_PREROTATED)) {
-          float cs, sn;
-          rope_cos_sin(si.ctx + qn / G, inv_lds[p], &cs, &sn);
-          const float l2 = qlo * cs - qhi * sn, h2 = qhi * cs + qlo * sn;
-          qlo = l2;
-          qhi = h2;
-        }
-      }
-      q_lds[qn * QLD + p] = f2bf(qlo * qscale);
-      q_lds[qn * QLD + p + HD / 2] = f2bf(qhi * qscale);
-    }
-
-    f32x4 o[MT][NT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) o[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float m_run[NT], l_run[NT];
+  f32x4 o[MT][NT];
+  float m_run[NT], l_run[NT];   // l_run: per-lane partial sums (reduce across groups to use)
+  f32x4 o_pk[PARK_REGS ? MT : 1][PARK_REGS ? NT : 1];
+  float m_pk[NT], l_pk[NT];
+  u16x8 qf[NT][KS];
+  auto reset = [&]() {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) o[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
       m_run[nt] = -INFINITY;
       l_run[nt] = 0.f;
     }
-    u16x8 qf[NT][KS];
-
-    for (int sub = 0; sub < n; sub += SUB_TILES) {
-      const int sn_t = min(n - sub, SUB_TILES);            // tiles in this sub-chunk
-      const int pbeg = 2 * (j0 + sub);                      // its first logical page
-      const int pend = min(pbeg + 2 * sn_t, si.npt);
-      __syncthreads();                                      // previous readers of pg_lds done
-      for (int i = tid; i < pend - pbeg; i += NTHR) {
-        const int lp = pbeg + i;
-        int phys = -1;
-        if (lp < si.npc) {
-          phys = a.page_table[static_cast<int64_t>(s) * a.max_pages + lp];
-          if (phys < 0 || phys >= a.num_pages) {
-            set_status(a.status, CO_ERR_PAGE_RANGE);
-            phys = -2;
-          }
+  };
+  // queries of round piece slot j into the MFMA B fragments (after DMA has begun)
+  auto load_q = [&](int j) {
+    const uint16_t* qb = q_lds + j * QSZ;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      uint32_t ad[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        ad[ks] = lds_addr(reinterpret_cast<const unsigned char*>(qb + (nt * 16 + col) * QLD + ks * 32 + grp * 8));
+      lds_read_group<KS>(qf[nt], ad);
+    }
+  };
+  // a piece this wavefront merged completely: final output, or a slice record
+  auto emit = [&](bool whole, int s, int seg, const float (&l_tot)[NT]) {
+    const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
+    if (whole) {
+      uint16_t* out = static_cast<uint16_t*>(a.out);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int qn = nt * 16 + col;
+        if (qn >= nq) continue;
+        const float inv = l_tot[nt] > 0.f ? 1.f / l_tot[nt] : 0.f;
+        const int64_t row = out_row(a, layer_local, s, g, qn, G);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          u16x4 v;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] = f2bf(o[mt][nt][r] * inv);
+          *reinterpret_cast<u16x4*>(out + row * HD + mt * 16 + grp * 4) = v;
         }
-        pg_lds[i] = phys;
+        if (a.lse && grp == 0)
+          a.lse[row] = l_tot[nt] > 0.f ? (m_run[nt] + log2f(l_tot[nt])) * kLn2 : -INFINITY;
+      }
+    } else {
+      float* part = slot_ptr(a, hdr_floats, w + static_cast<int64_t>(seg) * S + s, NQP);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int qn = nt * 16 + col;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+          *reinterpret_cast<f32x4*>(part + qn * HD + mt * 16 + grp * 4) = o[mt][nt];
+        if (grp == 0) {
+          part[NQP * HD + qn] = m_run[nt];
+          part[NQP * HD + NQP + qn] = l_tot[nt];
+        }
+      }
+    }
+  };
+  // fold a parked partial (O[NQP][ld], m[NQP], l[NQP]) into the accumulators
+  auto absorb = [&](const float* p, int ld) {
+    f32x4 po[MT][NT];
+    float mo[NT], lo[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {   // one round trip for the whole partial
+      const int qn = nt * 16 + col;
+      mo[nt] = p[NQP * ld + qn];
+      lo[nt] = p[NQP * ld + NQP + qn];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        po[mt][nt] = *reinterpret_cast<const f32x4*>(p + qn * ld + mt * 16 + grp * 4);
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const float M = fmaxf(m_run[nt], mo[nt]);
+      const float f0 = (m_run[nt] == -INFINITY) ? 0.f : exp2f(m_run[nt] - M);
+      const float f1 = (mo[nt] == -INFINITY) ? 0.f : exp2f(mo[nt] - M);
+      const float lt = wave_sum_across_groups(l_run[nt]) * f0 + lo[nt] * f1;
+      l_run[nt] = grp == 0 ? lt : 0.f;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) o[mt][nt] = o[mt][nt] * f0 + po[mt][nt] * f1;
+      m_run[nt] = M;
+    }
+  };
+
+  reset();
+  bool carrying = false;   // this wavefront holds a piece continued from the previous round
+  int rot = 0;             // wavefront that takes the first sub-slice of a round
+  int r0 = 0, r1 = 0;
+  for (int pass_begin = -1;;) {
+    if (pass_begin >= r1) break;                        // after the last pass
+    // ---- per-sequence tiles, their prefix sums and the non-empty sequences
+    __syncthreads();                                    // smem is reused
+    int T1, NE, seg0;
+    {
+      const int per = (S + NTHR - 1) / NTHR, s0 = tid * per;
+      int nts[SPT], cx[SPT], cr[SPT];
+      int tl = 0, nl = 0;
+#pragma unroll
+      for (int i = 0; i < SPT; ++i) {
+        nts[i] = cx[i] = cr[i] = 0;
+        if (i < per && s0 + i < S) {
+          const SeqInfo q = seq_info(a, s0 + i, 1);
+          nts[i] = (q.npt + 1) / 2;
+          cx[i] = q.ctx;
+          cr[i] = q.carry;
+          tl += nts[i];
+          nl += nts[i] > 0;
+        }
+      }
+      int vt = tl, vn = nl;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const int ut = __shfl_up(vt, off), un = __shfl_up(vn, off);
+        if (lane >= off) {
+          vt += ut;
+          vn += un;
+        }
+      }
+      if (lane == 63) {
+        scan_tot[wave] = vt;
+        scan_tot[NW + wave] = vn;
       }
       __syncthreads();
-      if (sub == 0) {
+      int rt = vt - tl, rn = vn - nl;
+      T1 = 0;
+      NE = 0;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
+      for (int v = 0; v < NW; ++v) {
+        if (v < wave) {
+          rt += scan_tot[v];
+          rn += scan_tot[NW + v];
+        }
+        T1 += scan_tot[v];
+        NE += scan_tot[NW + v];
+      }
+      const int T = n_segs * T1;
+      if (pass_begin < 0) {
+        r0 = static_cast<int>(static_cast<int64_t>(T) * w / n_wg);
+        r1 = static_cast<int>(static_cast<int64_t>(T) * (w + 1) / n_wg);
+        int* hdr = reinterpret_cast<int*>(a.ws);
+        if (tid == 0) {
+          hdr[S + 1 + w + 1] = r1;
+          if (w == 0) {
+            hdr[S + 1] = 0;
+            hdr[S] = T1;
+          }
+        }
+        if (w == 0) {
+          int x = rt;
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks)
-            qf[nt][ks] =
-                *reinterpret_cast<const u16x8*>(q_lds + (nt * 16 + col) * QLD + ks * 32 + grp * 8);
+          for (int i = 0; i < SPT; ++i)
+            if (i < per && s0 + i < S) {
+              hdr[s0 + i] = x;
+              x += nts[i];
+            }
+        }
+        pass_begin = r0;
+        if (r0 >= r1) break;                            // an empty slice
+      }
+      seg0 = pass_begin / T1;
+      const int rr = pass_begin - seg0 * T1;
+#pragma unroll
+      for (int i = 0; i < SPT; ++i)
+        if (i < per && s0 + i < S) {
+          tstart[s0 + i] = rt;
+          nstart[s0 + i] = rn;
+          ctx_s[s0 + i] = cx[i];
+          carry_s[s0 + i] = cr[i];
+          if (nts[i]) ne_seq[rn] = s0 + i;
+          if (rt <= rr && rr < rt + nts[i]) first_seq = s0 + i;
+          rt += nts[i];
+          rn += nts[i] > 0;
+        }
+      if (tid == NTHR - 1) tstart[S] = rt;
+      __syncthreads();
+    }
+
+    // ---- the next (up to PMAX) pieces of the slice, from pass_begin
+    if (tid < PMAX) {
+      const int gp = seg0 * NE + nstart[first_seq] + tid;   // global index of its segment
+      Piece p;
+      p.seg_begin = p.seg_end = p.begin = p.end = r1;
+      p.s = p.seg = p.ctx = p.carry = 0;
+      const int seg = gp / NE;
+      if (seg < n_segs) {
+        const int s = ne_seq[gp - seg * NE];
+        p.seg_begin = seg * T1 + tstart[s];
+        p.seg_end = seg * T1 + tstart[s + 1];
+        p.begin = max(p.seg_begin, pass_begin);
+        p.end = min(p.seg_end, r1);
+        p.s = s;
+        p.seg = seg;
+        p.ctx = ctx_s[s];
+        p.carry = carry_s[s];
+        if (p.begin >= p.end) p.begin = p.end = r1;
+      }
+      pc[tid] = p;
+    }
+    __syncthreads();
+    const int n_p = __popcll(__ballot(lane < PMAX && pc[lane].begin < pc[lane].end));
+    const int pass_end = pc[n_p - 1].end;
+
+    for (int ra = pass_begin, pa = 0; ra < pass_end;) {
+      // ---- the round [ra, rb): pieces [pa, pb), at most PQ of them
+      int rb = min(pass_end, ra + NW * round_tiles);
+      if (pa + PQ < n_p) rb = min(rb, pc[pa + PQ].begin);
+      int pb = pa + 1;
+      while (pb < n_p && pc[pb].begin < rb) ++pb;
+      const int nr = rb - ra;
+
+      // stage the queries of the round's pieces, rotated at ctx + i and scaled
+      {
+        u16x4 qlo[QV], qhi[QV];
+#pragma unroll
+        for (int i = 0; i < QV; ++i) {   // loads first: one round trip for all
+          const int idx = tid + i * NTHR;
+          const int j = idx / (NQP * (HD / 8)), rem = idx % (NQP * (HD / 8));
+          const int qn = rem / (HD / 8), p4 = (rem % (HD / 8)) * 4;
+          int64_t off = 0;
+          if (j < pb - pa && qn < nq) {
+            const Piece& P = pc[pa + j];
+            off = out_row(a, P.seg / a.Hkv, P.s, P.seg % a.Hkv, qn, G) * HD + p4;
+          }
+          qlo[i] = *reinterpret_cast<const u16x4*>(Q + off);
+          qhi[i] = *reinterpret_cast<const u16x4*>(Q + off + HD / 2);
+        }
+#pragma unroll
+        for (int i = 0; i < QV; ++i) {
+          const int idx = tid + i * NTHR;
+          const int j = idx / (NQP * (HD / 8)), rem = idx % (NQP * (HD / 8));
+          const int qn = rem / (HD / 8), p4 = (rem % (HD / 8)) * 4;
+          if (j >= pb - pa) continue;
+          const bool live = qn < nq;
+          const int pos = pc[pa + j].ctx + qn / G;
+          u16x4 lo4, hi4;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float x = live ? bf2f(qlo[i][e]) : 0.f, y = live ? bf2f(qhi[i][e]) : 0.f;
+            if (rotate_q) {
+              float cs, sn;
+              rope_cos_sin_rev(pos, inv_lds[p4 + e], &cs, &sn);
+              const float x2 = x * cs - y * sn, y2 = y * cs + x * sn;
+              x = x2;
+              y = y2;
+            }
+            lo4[e] = f2bf(x * qscale);
+            hi4[e] = f2bf(y * qscale);
+          }
+          uint16_t* dst = q_lds + j * QSZ + qn * QLD + p4;
+          *reinterpret_cast<u16x4*>(dst) = lo4;
+          *reinterpret_cast<u16x4*>(dst + HD / 2) = hi4;
+        }
       }
 
-      // Logical page lp -> K/V page addresses (wave-uniform) and valid slots.
-      auto page = [&](int lp, const uint16_t*& kp, const uint16_t*& vp) -> int {
-        kp = kk;
-        vp = vk;
-        if (lp >= pend) return 0;
-        if (lp < si.npc) {
-          const int phys = __builtin_amdgcn_readfirstlane(pg_lds[lp - pbeg]);
-          if (phys < 0) return 0;
-          const int64_t off = (kv_layer + static_cast<int64_t>(phys) * a.Hkv) * kPage * HD;
-          kp = kc + off;
-          vp = vc + off;
-          return min(kPage, si.ctx - lp * kPage);
+      // this wavefront's sub-slice [sb, se) and the descriptors of its pages:
+      // row >= 0 committed K/V row, -1-r carry row r, INT_MIN nothing to read
+      const int k = (wave - rot + NW) % NW;
+      const int sb = ra + static_cast<int>(static_cast<int64_t>(nr) * k / NW);
+      const int se = ra + static_cast<int>(static_cast<int64_t>(nr) * (k + 1) / NW);
+      int pg_row[RQ], pg_nv[RQ];
+      {
+        int pt[RQ], pidx[RQ], lpv[RQ];
+#pragma unroll
+        for (int q = 0; q < RQ; ++q) {   // page-table loads first
+          const int jp = lane + 64 * q, t = sb + (jp >> 1);
+          int i = pa;
+          while (i + 1 < pb && pc[i].end <= t) ++i;
+          pidx[q] = i;
+          lpv[q] = 2 * (t - pc[i].seg_begin) + (jp & 1);
+          const bool com = t < se && lpv[q] < (pc[i].ctx + kPage - 1) / kPage;
+          pt[q] = a.page_table[com ? static_cast<int64_t>(pc[i].s) * a.max_pages + lpv[q] : 0];
         }
-        const int cp = lp - si.npc;
-        const int64_t off = (carry_base + static_cast<int64_t>(cp) * a.Hkv) * kPage * HD;
-        kp = kk + off;
-        vp = vk + off;
-        return min(kPage, si.carry - cp * kPage);
-      };
-      const int my_tiles = wave < sn_t ? (sn_t - 1 - wave) / NW + 1 : 0;
+#pragma unroll
+        for (int q = 0; q < RQ; ++q) {
+          const int t = sb + ((lane + 64 * q) >> 1);
+          const Piece& P = pc[pidx[q]];
+          const int lp = lpv[q];
+          const int npc = (P.ctx + kPage - 1) / kPage, npt = npc + (P.carry + kPage - 1) / kPage;
+          const int layer = a.layer_begin + P.seg / a.Hkv, g = P.seg % a.Hkv;
+          int row = INT_MIN, nv = 0;
+          if (t < se && lp < npc) {
+            const int phys = pt[q];
+            if (phys >= 0 && phys < a.num_pages) {
+              row = (layer * a.num_pages + phys) * a.Hkv + g;
+              nv = min(kPage, P.ctx - lp * kPage);
+            } else {
+              set_status(a.status, CO_ERR_PAGE_RANGE);
+            }
+          } else if (t < se && lp < npt) {
+            const int cp = lp - npc;
+            row = -1 - (((layer * S + P.s) * a.CP + cp) * a.Hkv + g);
+            nv = min(kPage, P.carry - cp * kPage);
+          }
+          pg_row[q] = row;
+          pg_nv[q] = nv;
+        }
+      }
+      // fields of the round's pieces, lane i for piece pa + i
+      int f_beg = 0, f_end = 0, f_sbeg = 0, f_send = 0, f_s = 0, f_seg = 0;
+      if (lane < pb - pa) {
+        const Piece& P = pc[pa + lane];
+        f_beg = P.begin;
+        f_end = P.end;
+        f_sbeg = P.seg_begin;
+        f_send = P.seg_end;
+        f_s = P.s;
+        f_seg = P.seg;
+      }
+
+      // ---- stream the sub-slice
+      const int ntw = se - sb;
+      int pj = 0;                                       // current piece, relative to pa
+      while (pj + 1 < pb - pa && __builtin_amdgcn_readlane(f_end, pj) <= sb) ++pj;
+      int c_beg = __builtin_amdgcn_readlane(f_beg, pj), c_end = __builtin_amdgcn_readlane(f_end, pj);
+      bool merger = carrying || sb == c_beg;
+      bool holding = carrying;                          // accumulators hold a piece this wave merges
+      bool parked = false;
+      if (!carrying) reset();
+      carrying = false;
+
       auto issue = [&](int jj) {
-        const int lp0 = pbeg + 2 * (wave + jj * NW);
         unsigned char* dst = my_ring + (jj % NS) * TILE_BYTES;
+        const int rv = pick_reg(pg_row, jj >> 5);
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
-          const uint16_t *kp, *vp;
-          page(lp0 + half, kp, vp);
+          const int row = __builtin_amdgcn_readlane(rv, (2 * jj + half) & 63);
+          const uint16_t *kp = kk, *vp = vk;
+          if (row >= 0) {
+            kp = kc + static_cast<int64_t>(row) * (kPage * HD);
+            vp = vc + static_cast<int64_t>(row) * (kPage * HD);
+          } else if (row != INT_MIN) {
+            kp = kk + static_cast<int64_t>(-1 - row) * (kPage * HD);
+            vp = vk + static_cast<int64_t>(-1 - row) * (kPage * HD);
+          }
 #pragma unroll
           for (int q = 0; q < LPP; ++q) {
             lds_dma16(kp + k_off[q], dst + half * PAGE_BYTES + q * 1024);
@@ -550,26 +782,23 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
         }
       };
 #pragma unroll
-      for (int jj = 0; jj < NS - 1; ++jj)
-        if (jj < my_tiles) issue(jj);
+      for (int jj = 0; jj < NS - 1; ++jj)   // the first tiles load while the queries are staged
+        if (jj < ntw) issue(jj);
+      if (tid == 0) next_rot = -1;
+      lds_barrier();                                    // queries staged
+      if (ntw > 0) load_q(pj);
 
-      for (int jj = 0; jj < my_tiles; ++jj) {
-        if (jj + NS - 1 < my_tiles) issue(jj + NS - 1);
-        // valid slots of the tile's two pages (pages past the end have none)
-        const int lp0 = pbeg + 2 * (wave + jj * NW);
-        int n0 = 0, n1 = 0;
-        if (lp0 < pend)
-          n0 = lp0 < si.npc ? min(kPage, si.ctx - lp0 * kPage)
-                            : min(kPage, si.carry - (lp0 - si.npc) * kPage);
-        if (lp0 + 1 < pend)
-          n1 = lp0 + 1 < si.npc ? min(kPage, si.ctx - (lp0 + 1) * kPage)
-                                : min(kPage, si.carry - (lp0 + 1 - si.npc) * kPage);
-        if (lp0 < si.npc && pg_lds[lp0 - pbeg] < 0) n0 = 0;
-        if (lp0 + 1 < si.npc && lp0 + 1 < pend && pg_lds[lp0 + 1 - pbeg] < 0) n1 = 0;
+      for (int j = 0; j < ntw; ++j) {
+        if (j + NS - 1 < ntw) issue(j + NS - 1);
+        const int t = sb + j;
+        const int nvr = pick_reg(pg_nv, j >> 5);
+        const int n0 = __builtin_amdgcn_readlane(nvr, (2 * j) & 63);
+        const int n1 = __builtin_amdgcn_readlane(nvr, (2 * j + 1) & 63);
         const bool partial = n0 < kPage || n1 < kPage;      // wave-uniform
         const int nv = (grp >> 1) ? n1 : n0;   // valid slots of the page holding my keys
-        wait_stages_ahead<NL, NS>(min(NS - 1, my_tiles - 1 - jj));
-        const unsigned char* tb = my_ring + (jj % NS) * TILE_BYTES;
+        wait_stages_ahead<NL, NS>(min(NS - 1, ntw - 1 - j));
+        const unsigned char* tb = my_ring + (j % NS) * TILE_BYTES;
+        if (t == c_beg && !carrying) holding = merger;
 
         u16x8 ka[KS], kb[KS];
         {
@@ -612,21 +841,21 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
 
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-          f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+          f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int ks = 0; ks < KS; ++ks) {
             sa = mfma16x16x32(ka[ks], qf[nt][ks], sa);
-            sb = mfma16x16x32(kb[ks], qf[nt][ks], sb);
+            sb4 = mfma16x16x32(kb[ks], qf[nt][ks], sb4);
           }
           if (partial) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               sa[r] = (slot_base + r < nv) ? sa[r] : -INFINITY;
-              sb[r] = (slot_base + 4 + r < nv) ? sb[r] : -INFINITY;
+              sb4[r] = (slot_base + 4 + r < nv) ? sb4[r] : -INFINITY;
             }
           }
           float mx = fmaxf(fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])),
-                           fmaxf(fmaxf(sb[0], sb[1]), fmaxf(sb[2], sb[3])));
+                           fmaxf(fmaxf(sb4[0], sb4[1]), fmaxf(sb4[2], sb4[3])));
           mx = max_across_rows(mx);
           if (__any(mx > m_run[nt] + kRescale)) {
             // move the reference up (only where the tile exceeds it) and rescale
@@ -638,130 +867,152 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
             m_run[nt] = m_new;
           }
           const float base = (m_run[nt] == -INFINITY) ? 0.f : m_run[nt];
-          float pa[4], pb[4];
+          float pa4[4], pb4[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {   // v_exp_f32: arguments are <= kRescale or -inf
-            pa[r] = __builtin_amdgcn_exp2f(sa[r] - base);
-            pb[r] = __builtin_amdgcn_exp2f(sb[r] - base);
+            pa4[r] = __builtin_amdgcn_exp2f(sa[r] - base);
+            pb4[r] = __builtin_amdgcn_exp2f(sb4[r] - base);
           }
-          l_run[nt] += (pa[0] + pa[1]) + (pa[2] + pa[3]) + (pb[0] + pb[1]) + (pb[2] + pb[3]);
+          l_run[nt] += (pa4[0] + pa4[1]) + (pa4[2] + pa4[3]) + (pb4[0] + pb4[1]) + (pb4[2] + pb4[3]);
           typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
-          const u32x4v pk32 = {pack_bf16x2(pa[0], pa[1]), pack_bf16x2(pa[2], pa[3]),
-                               pack_bf16x2(pb[0], pb[1]), pack_bf16x2(pb[2], pb[3])};
+          const u32x4v pk32 = {pack_bf16x2(pa4[0], pa4[1]), pack_bf16x2(pa4[2], pa4[3]),
+                               pack_bf16x2(pb4[0], pb4[1]), pack_bf16x2(pb4[2], pb4[3])};
           const u16x8 pk = __builtin_bit_cast(u16x8, pk32);
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) o[mt][nt] = mfma16x16x32(va[mt], pk, o[mt][nt]);
         }
-      }
-    }
 
+        // ---- the end of a piece, or of the sub-slice inside a piece
+        if (t + 1 == c_end || j + 1 == ntw) {
+          float l_tot[NT];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) l_run[nt] = wave_sum_across_groups(l_run[nt]);
-
-    // ---- merge the wavefronts through LDS (the drained ring) into wave 0
-    __syncthreads();
-    if constexpr (NW > 1) {
-      if (wave > 0) {
+          for (int nt = 0; nt < NT; ++nt) l_tot[nt] = wave_sum_across_groups(l_run[nt]);
+          const bool ends = t + 1 == c_end;
+          if (merger && ends) {
+            const int sbeg = __builtin_amdgcn_readlane(f_sbeg, pj);
+            const int send = __builtin_amdgcn_readlane(f_send, pj);
+            emit(c_beg == sbeg && c_end == send, __builtin_amdgcn_readlane(f_s, pj),
+                 __builtin_amdgcn_readlane(f_seg, pj), l_tot);
+            holding = false;
+          } else if (!merger) {
+            // the first piece of a sub-slice that began inside it: merged by the
+            // wavefront that holds its beginning
+            parked = true;
+            if constexpr (PARK_REGS) {
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const int qn = nt * 16 + col;
-          if (grp == 0) {
-            red_m[(wave - 1) * NQP + qn] = m_run[nt];
-            red_l[(wave - 1) * NQP + qn] = l_run[nt];
+              for (int nt = 0; nt < NT; ++nt) {
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) o_pk[mt][nt] = o[mt][nt];
+                m_pk[nt] = m_run[nt];
+                l_pk[nt] = l_tot[nt];
+              }
+            } else {
+              float* pp = a.ws + park_off + (static_cast<int64_t>(w) * NW + wave) * NQP * (HD + 2);
+#pragma unroll
+              for (int nt = 0; nt < NT; ++nt) {
+                const int qn = nt * 16 + col;
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                  *reinterpret_cast<f32x4*>(pp + qn * HD + mt * 16 + grp * 4) = o[mt][nt];
+                if (grp == 0) {
+                  pp[NQP * HD + qn] = m_run[nt];
+                  pp[NQP * HD + NQP + qn] = l_tot[nt];
+                }
+              }
+            }
+          } else {
+            // merger whose piece goes on past the sub-slice: merged at the round's end
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) l_run[nt] = grp == 0 ? l_tot[nt] : 0.f;
           }
+          if (ends && j + 1 < ntw) {   // the next piece begins inside this sub-slice
+            ++pj;
+            c_beg = __builtin_amdgcn_readlane(f_beg, pj);
+            c_end = __builtin_amdgcn_readlane(f_end, pj);
+            merger = true;
+            holding = true;
+            reset();
+            load_q(pj);
+          }
+        }
+      }
+
+      // ---- round end: merge the parked partials into the wavefront holding the piece
+      __syncthreads();                                  // every ring is drained
+      if constexpr (PARK_REGS) {
+        if (parked) {
+          float* sp = reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS;
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
+          for (int nt = 0; nt < NT; ++nt) {
+            const int qn = nt * 16 + col;
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-              red_o[((wave - 1) * NQP + qn) * (HD + 1) + mt * 16 + grp * 4 + r] = o[mt][nt][r];
+            for (int mt = 0; mt < MT; ++mt)
+              *reinterpret_cast<f32x4*>(sp + qn * SLOT_LD + mt * 16 + grp * 4) = o_pk[mt][nt];
+            if (grp == 0) {
+              sp[NQP * SLOT_LD + qn] = m_pk[nt];
+              sp[NQP * SLOT_LD + NQP + qn] = l_pk[nt];
+            }
+          }
         }
       }
       __syncthreads();
-      if (wave == 0) {
+      if (holding) {
+        for (int k2 = k + 1; k2 < NW; ++k2) {
+          const int sb2 = ra + static_cast<int>(static_cast<int64_t>(nr) * k2 / NW);
+          const int se2 = ra + static_cast<int>(static_cast<int64_t>(nr) * (k2 + 1) / NW);
+          if (sb2 >= c_end) break;
+          if (sb2 == se2) continue;
+          const int v2 = (k2 + rot) % NW;
+          if constexpr (PARK_REGS)
+            absorb(reinterpret_cast<const float*>(smem) + v2 * SLOT_FLOATS, SLOT_LD);
+          else
+            absorb(a.ws + park_off + (static_cast<int64_t>(w) * NW + v2) * NQP * (HD + 2), HD);
+        }
+        if (c_end > rb) {
+          if (lane == 0) next_rot = wave;               // goes on in the next round
+        } else {
+          float l_tot[NT];
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const int qn = nt * 16 + col;
-          float M = m_run[nt];
-#pragma unroll
-          for (int wv = 1; wv < NW; ++wv) M = fmaxf(M, red_m[(wv - 1) * NQP + qn]);
-          const float f0 = (m_run[nt] == -INFINITY) ? 0.f : exp2f(m_run[nt] - M);
-          float lsum = l_run[nt] * f0;
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) o[mt][nt] *= f0;
-#pragma unroll
-          for (int wv = 1; wv < NW; ++wv) {
-            const float mw = red_m[(wv - 1) * NQP + qn];
-            const float fw = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
-            lsum += red_l[(wv - 1) * NQP + qn] * fw;
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-              for (int r = 0; r < 4; ++r)
-                o[mt][nt][r] += fw * red_o[((wv - 1) * NQP + qn) * (HD + 1) + mt * 16 + grp * 4 + r];
-          }
-          m_run[nt] = M;
-          l_run[nt] = lsum;
+          for (int nt = 0; nt < NT; ++nt) l_tot[nt] = wave_sum_across_groups(l_run[nt]);
+          const int sbeg = __builtin_amdgcn_readlane(f_sbeg, pj);
+          const int send = __builtin_amdgcn_readlane(f_send, pj);
+          emit(c_beg == sbeg && c_end == send, __builtin_amdgcn_readlane(f_s, pj),
+               __builtin_amdgcn_readlane(f_seg, pj), l_tot);
+          holding = false;
         }
       }
+      __syncthreads();                                  // slots consumed, next_rot visible
+      const int nrot = next_rot;
+      carrying = nrot >= 0 && wave == nrot;
+      rot = nrot >= 0 ? nrot : 0;
+      ra = rb;
+      pa = (pc[pb - 1].end > rb) ? pb - 1 : pb;
     }
-
-    if (wave == 0) {
-      if (whole) {
-        // the whole segment is in this slice: normalise and write O / LSE directly
-        uint16_t* out = static_cast<uint16_t*>(a.out);
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const int qn = nt * 16 + col;
-          if (qn >= nq) continue;
-          const float inv = l_run[nt] > 0.f ? 1.f / l_run[nt] : 0.f;
-          const int64_t row = out_row(a, layer_local, s, g, qn, G);
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            u16x4 v;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = f2bf(o[mt][nt][r] * inv);
-            *reinterpret_cast<u16x4*>(out + row * HD + mt * 16 + grp * 4) = v;
-          }
-          if (a.lse && grp == 0)
-            a.lse[row] = l_run[nt] > 0.f ? (m_run[nt] + log2f(l_run[nt])) * kLn2 : -INFINITY;
-        }
-      } else {
-        float* part = slot_ptr(a, hdr_floats, w + static_cast<int64_t>(seg) * S + s, NQP);
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const int qn = nt * 16 + col;
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-            *reinterpret_cast<f32x4*>(part + qn * HD + mt * 16 + grp * 4) = o[mt][nt];
-          if (grp == 0) {
-            part[NQP * HD + qn] = m_run[nt];
-            part[NQP * HD + NQP + qn] = l_run[nt];
-          }
-        }
-      }
-    }
-    __syncthreads();                                        // q_lds and smem are reused
-    cur += n;
+    pass_begin = pass_end;
   }
 }
 
 // Combine the slice records of every (layer, KV head, sequence) split across
 // slices, write O/LSE of segments without keys, and report invalid lengths.
-// One thread per (query row, 4 output dims); record loads are issued in
-// batches of kBatch so that their latencies overlap.
+// The slice bounds are staged in LDS with one round of loads; one thread per
+// (query row, 4 output dims) then merges the records.
 __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int layer_count,
                                                                 int n_wg, int hdr_floats,
                                                                 int nq_pad) {
   constexpr int kBatch = 8;
+  __shared__ int bnd[kMaxMergeSlices + 1];
   const int s = blockIdx.x, seg = blockIdx.y;
   const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
   const int hd = a.hd, G = a.Hq / a.Hkv, nq = a.B * G, q4 = hd / 4;
   const int tid = threadIdx.x;
   const int* hdr = reinterpret_cast<const int*>(a.ws);
+  const int* bounds = hdr + a.S + 1;
+  for (int i = tid; i <= n_wg; i += 256) bnd[i] = bounds[i];
   const SeqInfo si = seq_info(a, s, 1);
   if (!si.ok && seg == 0 && tid == 0 && blockIdx.z == 0) set_status(a.status, CO_ERR_LENGTH);
-  const int T1 = hdr[a.S];
-  const int nts = hdr[s + 1] - hdr[s];
+  const int T1 = hdr[a.S], ts = hdr[s];
+  const int nts = hdr[s + 1] - ts;
+  __syncthreads();
   uint16_t* out = static_cast<uint16_t*>(a.out);
   if (nts == 0) {                      // no keys: O = 0, LSE = -inf
     for (int idx = tid + blockIdx.z * 256; idx < nq * hd; idx += 256 * gridDim.z)
@@ -770,43 +1021,29 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
       for (int qn = tid; qn < nq; qn += 256) a.lse[out_row(a, layer_local, s, g, qn, G)] = -INFINITY;
     return;
   }
-  const int64_t A = static_cast<int64_t>(seg) * T1 + hdr[s];
-  const int64_t* bounds = reinterpret_cast<const int64_t*>(hdr + slice_bounds_off(a.S));
-  // slice w holds global tiles [bounds[w], bounds[w+1]); find the owners of the
-  // segment's first and last tile (bounds is non-decreasing)
-  auto owner = [&](int64_t x) {
-    int lo = 0, hi = n_wg;                  // bounds[lo] <= x < bounds[hi]
+  const int A = seg * T1 + ts;
+  // owner of tile x: the last slice with bnd[w] <= x (bnd is non-decreasing)
+  auto owner = [&](int x) {
+    int lo = 0, hi = n_wg;
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
-      if (bounds[mid] <= x) lo = mid; else hi = mid;
+      if (bnd[mid] <= x) lo = mid; else hi = mid;
     }
     return lo;
   };
   const int w_lo = owner(A), w_hi = owner(A + nts - 1);
   if (w_lo == w_hi) return;            // finished in place
   const int nrec = w_hi - w_lo + 1;
-  __shared__ float live_lds[kMaxMergeSlices];
-  for (int i = tid; i < nrec; i += 256)   // an empty slice left no record
-    live_lds[i] = bounds[w_lo + i] < bounds[w_lo + i + 1] ? 1.f : 0.f;
-  __syncthreads();
   const int64_t rec = static_cast<int64_t>(nq_pad) * (hd + 2);
-  // records of consecutive slices of one segment are consecutive slots
+  // records of consecutive slices of one segment are consecutive slots; a slice
+  // without tiles left none
   const float* base = slot_ptr(a, hdr_floats, w_lo + static_cast<int64_t>(seg) * a.S + s, nq_pad);
   for (int idx = tid + blockIdx.z * 256; idx < nq * q4; idx += 256 * gridDim.z) {
     const int qn = idx / q4, d = (idx % q4) * 4;
     const float* pm = base + nq_pad * hd + qn;
-    float M = -INFINITY;
-    for (int r0 = 0; r0 < nrec; r0 += kBatch) {
-      float mv[kBatch];
-#pragma unroll
-      for (int i = 0; i < kBatch; ++i) mv[i] = r0 + i < nrec ? pm[(r0 + i) * rec] : -INFINITY;
-#pragma unroll
-      for (int i = 0; i < kBatch; ++i)
-        if (r0 + i < nrec && live_lds[r0 + i] != 0.f) M = fmaxf(M, mv[i]);
-    }
-    float den = 0.f;
+    float M = -INFINITY, den = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int r0 = 0; r0 < nrec; r0 += kBatch) {
+    for (int r0 = 0; r0 < nrec; r0 += kBatch) {   // usually one batch: one round trip
       float mv[kBatch], lv[kBatch];
       f32x4 ov[kBatch];
 #pragma unroll
@@ -817,13 +1054,22 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
         ov[i] = in ? *reinterpret_cast<const f32x4*>(base + (r0 + i) * rec + qn * hd + d)
                    : f32x4{0.f, 0.f, 0.f, 0.f};
       }
+      float Mb = M;
 #pragma unroll
       for (int i = 0; i < kBatch; ++i) {
-        const bool live = r0 + i < nrec && live_lds[r0 + i] != 0.f;
-        const float wgt = (!live || mv[i] == -INFINITY) ? 0.f : exp2f(mv[i] - M);
+        if (!(r0 + i < nrec && bnd[w_lo + r0 + i] < bnd[w_lo + r0 + i + 1])) mv[i] = -INFINITY;
+        Mb = fmaxf(Mb, mv[i]);
+      }
+      const float f = (M == -INFINITY) ? 0.f : exp2f(M - Mb);
+      den *= f;
+      acc *= f;
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) {
+        const float wgt = (mv[i] == -INFINITY) ? 0.f : exp2f(mv[i] - Mb);
         den += wgt * lv[i];
         acc += wgt * ov[i];
       }
+      M = Mb;
     }
     const float inv = den > 0.f ? 1.f / den : 0.f;
     const int64_t row = out_row(a, layer_local, s, g, qn, G);
@@ -837,8 +1083,8 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
 
 }  // namespace
 
-AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int dtype,
-                        int num_cus) {
+AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int num_pages,
+                        int dtype, int num_cus) {
   AttnPlan p{};
   const int nq = B * (Hq / Hkv);
   p.nq_pad = (nq + 15) / 16 * 16;
@@ -846,16 +1092,32 @@ AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pa
   const int max_lp = max_pages + cp;
   p.ok = true;
   if (dtype == CO_DTYPE_BF16) {
-    // persistent path: a fixed number of workgroups per CU, records for
-    // (slice, segment) pairs
-    p.variant = 1;
-    if (const char* env = getenv("CO_ATTN_VARIANT")) p.variant = atoi(env) & 3;   // tuning
-    p.n_wg = num_cus * (p.variant == 1 && hd == 64 ? 2 : 1);
-    p.hdr_floats = (slice_bounds_off(S) + 2 * (p.n_wg + 1) + 63) / 64 * 64;
-    p.ok = S <= kMaxAttnSeqs && p.n_wg <= kMaxMergeSlices;
-    p.bytes = (static_cast<size_t>(p.hdr_floats) +
-               (static_cast<size_t>(p.n_wg) + static_cast<size_t>(L) * Hkv * S) * p.nq_pad *
-                   (hd + 2)) * 4;
+    // persistent path: one workgroup per CU; a record per (slice, segment) pair
+    // and, for large query tiles, a parking area per wavefront
+    const int nw = hd == 64 ? kAttnWaves64 : kAttnWaves128;
+    const int rtm = hd == 64 ? kAttnRoundTiles64 : kAttnRoundTiles128;
+    p.n_wg = num_cus;
+    p.round_tiles = rtm;
+    if (const char* env = getenv("CO_ATTN_WORKGROUPS")) {     // tuning and test override
+      const int v = atoi(env);
+      if (v >= 1 && v <= kMaxMergeSlices) p.n_wg = v;
+    }
+    if (const char* env = getenv("CO_ATTN_ROUND_TILES")) {    // tuning and test override
+      const int v = atoi(env);
+      if (v >= 1 && v <= rtm) p.round_tiles = v;
+    }
+    p.hdr_floats = (S + 1 + p.n_wg + 1 + 63) / 64 * 64;
+    const size_t rec = static_cast<size_t>(p.nq_pad) * (hd + 2);
+    const size_t records = (static_cast<size_t>(p.n_wg) + static_cast<size_t>(L) * Hkv * S) * rec;
+    const size_t park =
+        hd * (p.nq_pad / 16) > 128 ? static_cast<size_t>(p.n_wg) * nw * rec : 0;
+    p.park_off = static_cast<int64_t>(p.hdr_floats + records);
+    p.bytes = (p.hdr_floats + records + park) * 4;
+    // global tile indices, committed and carry K/V row indices are int32
+    const int64_t tiles = static_cast<int64_t>(L) * Hkv * S * ((max_lp + 1) / 2);
+    const int64_t rows_c = static_cast<int64_t>(L) * num_pages * Hkv;
+    const int64_t rows_u = static_cast<int64_t>(L) * S * cp * Hkv;
+    p.ok = S <= kMaxAttnSeqs && tiles < INT32_MAX && rows_c < INT32_MAX && rows_u < INT32_MAX;
   } else {
     // fp32 path: chunks of pages, one workgroup each
     p.chunk_pages = 32;
@@ -876,26 +1138,22 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
   const dim3 mgrid(a.S, layer_count * a.Hkv, (items + 255) / 256);
   if (a.dtype == CO_DTYPE_BF16) {
     const dim3 grid(p.n_wg);
-#define CO_ATTN_LAUNCH(HD, NT, NW, NS)                                                         \
-  hipLaunchKernelGGL((attn_bf16_kernel<HD, NT, NW, NS>), grid, dim3(64 * NW), 0, stream, a,     \
-                     layer_count, p.n_wg, p.hdr_floats)
-    if (a.hd == 64 && nt == 2 && p.variant == 0) {
-      CO_ATTN_LAUNCH(64, 2, 4, 4);
-    } else if (a.hd == 64 && nt == 2 && p.variant == 2) {
-      CO_ATTN_LAUNCH(64, 2, 8, 2);
-    } else if (a.hd == 64) {
+#define CO_ATTN_LAUNCH(HD, NT, NW, NS, PQ, RTM)                                                 \
+  hipLaunchKernelGGL((attn_bf16_kernel<HD, NT, NW, NS, PQ, RTM>), grid, dim3(64 * NW), 0, stream, \
+                     a, layer_count, p.n_wg, p.hdr_floats, p.round_tiles, p.park_off)
+    if (a.hd == 64) {
       switch (nt) {
-        case 1: CO_ATTN_LAUNCH(64, 1, 4, 2); break;
-        case 2: CO_ATTN_LAUNCH(64, 2, 4, 2); break;
-        case 3: CO_ATTN_LAUNCH(64, 3, 4, 2); break;
-        default: CO_ATTN_LAUNCH(64, 4, 4, 2); break;
+        case 1: CO_ATTN_LAUNCH(64, 1, kAttnWaves64, 2, 4, kAttnRoundTiles64); break;
+        case 2: CO_ATTN_LAUNCH(64, 2, kAttnWaves64, 2, 4, kAttnRoundTiles64); break;
+        case 3: CO_ATTN_LAUNCH(64, 3, kAttnWaves64, 2, 2, kAttnRoundTiles64); break;
+        default: CO_ATTN_LAUNCH(64, 4, kAttnWaves64, 2, 2, kAttnRoundTiles64); break;
       }
     } else {
       switch (nt) {
-        case 1: CO_ATTN_LAUNCH(128, 1, 2, 3); break;
-        case 2: CO_ATTN_LAUNCH(128, 2, 2, 3); break;
-        case 3: CO_ATTN_LAUNCH(128, 3, 2, 3); break;
-        default: CO_ATTN_LAUNCH(128, 4, 2, 3); break;
+        case 1: CO_ATTN_LAUNCH(128, 1, kAttnWaves128, 2, 4, kAttnRoundTiles128); break;
+        case 2: CO_ATTN_LAUNCH(128, 2, kAttnWaves128, 2, 2, kAttnRoundTiles128); break;
+        case 3: CO_ATTN_LAUNCH(128, 3, kAttnWaves128, 2, 1, kAttnRoundTiles128); break;
+        default: CO_ATTN_LAUNCH(128, 4, kAttnWaves128, 2, 1, kAttnRoundTiles128); break;
       }
     }
 #undef CO_ATTN_LAUNCH

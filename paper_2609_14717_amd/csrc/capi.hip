@@ -55,6 +55,13 @@ size_t elem_bytes(const co_dims* d) { return d->dtype == CO_DTYPE_BF16 ? 2 : 4; 
 
 int carry_pages(const co_dims* d) { return (d->block + kPage - 1) / kPage; }
 
+// RoPE inverse frequencies theta^(-2i/hd), i < hd/2, in double (rotate-half pairs)
+void fill_rope_table(double* t, const co_dims* d) {
+  const double lt = log2(static_cast<double>(d->rope_theta));
+  for (int i = 0; i < kMaxHeadDim / 2; ++i)
+    t[i] = i < d->head_dim / 2 ? exp2(-(2.0 * i / d->head_dim) * lt) : 0.0;
+}
+
 KvDest make_dest(const co_dims* d, const co_route* rt, const co_state* st) {
   KvDest e{};
   e.S = d->num_seqs;
@@ -64,7 +71,7 @@ KvDest make_dest(const co_dims* d, const co_route* rt, const co_state* st) {
   e.hd = d->head_dim;
   e.num_pages = d->num_pages;
   e.CP = carry_pages(d);
-  e.log2_theta = log2(static_cast<double>(d->rope_theta));
+  fill_rope_table(e.rope_inv, d);
   e.row_pos = rt ? rt->row_pos : nullptr;
   e.row_dst = rt ? rt->row_dst : nullptr;
   e.k_cache = st->k_cache;
@@ -91,7 +98,7 @@ ProjectPlan project_plan(const co_dims* d) {
 
 AttnPlan attention_plan(const co_dims* d) {
   return plan_attention(d->num_seqs, d->block, d->num_layers, d->num_q_heads, d->num_kv_heads,
-                        d->head_dim, d->max_pages_per_seq, d->dtype, num_cus());
+                        d->head_dim, d->max_pages_per_seq, d->num_pages, d->dtype, num_cus());
 }
 
 co_status hip_status(hipError_t e) { return e == hipSuccess ? CO_OK : CO_ERR_HIP; }
@@ -112,7 +119,7 @@ co_status do_attention(const co_dims* d, int32_t layer_begin, int32_t layer_coun
   a.CP = carry_pages(d);
   a.dtype = d->dtype;
   a.flags = flags;
-  a.log2_theta = log2(static_cast<double>(d->rope_theta));
+  fill_rope_table(a.rope_inv, d);
   a.q = q;
   a.ctx_len = st->ctx_len;
   a.carry_len = st->carry_len;

@@ -70,10 +70,6 @@ __device__ __forceinline__ f32x4 mfma16x16x32(u16x8 a, u16x8 b, f32x4 c) {
 // Rotary angle of pair index i at position pos: pos * theta^(-2i/hd).  The product
 // and the reduction to [-pi, pi] are done in fp64 so that positions of 10^5 keep
 // fp32 accuracy after the reduction; sin/cos are then taken in fp32.
-__device__ __forceinline__ double rope_inv_freq(int i, int hd, double log2_theta) {
-  return exp2(-(2.0 * i / hd) * log2_theta);
-}
-
 __device__ __forceinline__ void rope_cos_sin(int pos, double inv_freq, float* c, float* s) {
   const double two_pi = 6.283185307179586476925286766559;
   double a = static_cast<double>(pos) * inv_freq;
@@ -105,6 +101,14 @@ __device__ __forceinline__ void wait_stages_ahead(int ahead) {
   }
   if (ahead >= 1) { wait_vmcnt<NL>(); return; }
   wait_vmcnt<0>();
+}
+
+// Workgroup barrier that waits for this wavefront's LDS traffic only, leaving
+// its direct-to-LDS global loads in flight.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 // Groups of 16-byte LDS reads issued as inline asm, each group ending with its

@@ -9,6 +9,8 @@
 
 namespace co {
 
+constexpr int kMaxHeadDim = 128;
+
 struct RouteArgs {
   int S, B, max_pages, num_pages;
   uint32_t flags;
@@ -26,7 +28,7 @@ struct RouteArgs {
 // Where projected K/V rows go: the paged committed cache or the carry segment.
 struct KvDest {
   int S, B, L, Hkv, hd, num_pages, CP;
-  double log2_theta;
+  double rope_inv[kMaxHeadDim / 2];   // RoPE inverse frequencies theta^(-2i/hd)
   const int32_t* row_pos;
   const int32_t* row_dst;
   void* k_cache;
@@ -57,7 +59,7 @@ ProjectPlan plan_project(int M, int Dcat, int d, int n_kv, int hd, int dtype, in
 struct AttnArgs {
   int S, B, L, layer_begin, Hq, Hkv, hd, num_pages, max_pages, CP, dtype;
   uint32_t flags;
-  double log2_theta;
+  double rope_inv[kMaxHeadDim / 2];   // RoPE inverse frequencies theta^(-2i/hd)
   const void* q;
   const int32_t* ctx_len;
   const int32_t* carry_len;
@@ -76,15 +78,16 @@ constexpr int kMaxAttnSeqs = 2048;   // sequences one bf16 attention launch can 
 
 struct AttnPlan {
   int chunk_pages, n_chunks;   // fp32 path
-  int n_wg, hdr_floats;        // bf16 persistent path
-  int variant;                 // bf16 persistent path: wavefronts / ring depth / occupancy
+  int n_wg, hdr_floats;        // bf16 persistent path: workgroups, header floats
+  int round_tiles;             // bf16 persistent path: tiles per wavefront per round
+  int64_t park_off;            // bf16 persistent path: parked partials (workspace floats)
   int nq_pad;
   bool ok;                     // false: shapes beyond what one launch can cover
   size_t bytes;
 };
 
-AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int dtype,
-                        int num_cus);
+AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int num_pages,
+                        int dtype, int num_cus);
 
 hipError_t launch_route(const RouteArgs& a, hipStream_t stream);
 hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_t stream);

@@ -260,7 +260,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
       for (int r = 0; r < 4; ++r)
         sc[((wm * TM + a) * 16 + (lane >> 4) * 4 + r) * LDC + (wn * TN + b) * 16 + (lane & 15)] =
             acc[a][b][r];
-  if (g.mode == kModeKV && tid < g.kv.hd / 2) inv_tab[tid] = rope_inv_freq(tid, g.kv.hd, g.kv.log2_theta);
+  if (g.mode == kModeKV && tid < g.kv.hd / 2) inv_tab[tid] = g.kv.rope_inv[tid];
   __syncthreads();
 
   if (g.mode == kModeZ) {
@@ -358,7 +358,7 @@ __global__ __launch_bounds__(256) void epi_kv_kernel(const float* part, int spli
                                                      KvDest e) {
   __shared__ double inv_tab[64];
   const int half = e.hd / 2;
-  if (threadIdx.x < half) inv_tab[threadIdx.x] = rope_inv_freq(threadIdx.x, e.hd, e.log2_theta);
+  if (threadIdx.x < half) inv_tab[threadIdx.x] = e.rope_inv[threadIdx.x];
   __syncthreads();
   const int64_t items = static_cast<int64_t>(M) * (N / 2);   // one pair per thread
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;

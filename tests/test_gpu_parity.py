@@ -114,3 +114,20 @@ def test_ragged_batch32_full():
 
 def test_batch1_8b_full():
     run_rounds(wl.BATCH1_8B, 2)
+
+
+# Workgroup counts and round sizes forced far from the defaults, so that one
+# workgroup walks many segments in several passes and rounds, wavefronts park
+# and merge partial segments, and rounds hand a segment on to the next.
+MANY_SEQS = wl.RAGGED32.replace(name="many_seqs", S=70, L=1, ctx_lo=1, ctx_hi=700, rounds=3,
+                                accept=("geom", 0.25), seed=0x5EED05)
+SLICINGS = [("1", "1"), ("1", "3"), ("3", "2"), ("7", "64"), ("1000", "")]
+
+
+@pytest.mark.parametrize("w", [SMALL_RAGGED, SMALL_G4, MANY_SEQS], ids=lambda w: w.name)
+@pytest.mark.parametrize("slicing", SLICINGS, ids=lambda s: f"wg{s[0]}_rt{s[1] or 'dflt'}")
+def test_attention_slicings(w, slicing, monkeypatch):
+    monkeypatch.setenv("CO_ATTN_WORKGROUPS", slicing[0])
+    if slicing[1]:
+        monkeypatch.setenv("CO_ATTN_ROUND_TILES", slicing[1])
+    run_rounds(w, 2)
