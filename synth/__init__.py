@@ -122,6 +122,58 @@ def bernoulli(key: int, idx, p: float) -> np.ndarray:
     return (draw_u64(key, idx) >> np.uint64(32)) < thr
 
 
+_HOST_LIB = None
+
+
+def host_lib():
+    """The C build of ``normal`` over a dense block (``synth_host.c``), or None."""
+    global _HOST_LIB
+    if _HOST_LIB is None:
+        import ctypes
+        import os
+        path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsynth_host.so")
+        if not os.path.exists(path):
+            return None
+        lib = ctypes.CDLL(path)
+        lib.synth_host_fill.restype = ctypes.c_int
+        lib.synth_host_fill.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                                        ctypes.POINTER(ctypes.c_int64),
+                                        ctypes.POINTER(ctypes.c_int64), ctypes.c_int64,
+                                        ctypes.c_uint64, ctypes.c_float]
+        _HOST_LIB = lib
+    return _HOST_LIB
+
+
+def build_host() -> str:
+    """Compile synth_host.c into libsynth_host.so next to it."""
+    import os
+    import subprocess
+    here = os.path.dirname(os.path.abspath(__file__))
+    out = os.path.join(here, "libsynth_host.so")
+    subprocess.run(["gcc", "-O3", "-fopenmp", "-fPIC", "-shared", "-std=c11",
+                    os.path.join(here, "synth_host.c"), "-o", out + ".tmp"], check=True)
+    os.replace(out + ".tmp", out)
+    return out
+
+
+def normal_block(key: int, shape, strides, base: int, sigma: float, dtype: str,
+                 use_c: bool = True) -> np.ndarray:
+    """``normal`` over a dense block (logical index base + sum coord * stride),
+    through the C build when present, else numpy; both give identical bits."""
+    lib = host_lib() if use_c else None
+    if lib is None:
+        return normal(key, grid_index(shape, strides, base), sigma, dtype)
+    import ctypes
+    out = np.empty(tuple(shape), dtype=np.float32 if dtype == "f32" else np.uint16)
+    nd = len(shape)
+    rc = lib.synth_host_fill(out.ctypes.data_as(ctypes.c_void_p), 0 if dtype == "f32" else 1, nd,
+                             (ctypes.c_int64 * nd)(*shape), (ctypes.c_int64 * nd)(*strides),
+                             int(base), ctypes.c_uint64(key), float(normal_scale(sigma)))
+    if rc != 0:
+        raise RuntimeError("synth_host_fill failed")
+    return out
+
+
 def grid_index(shape, strides, base: int = 0) -> np.ndarray:
     """Flat logical indices of a dense block: base + sum_k coord_k * strides_k."""
     idx = np.full(tuple(shape), base, dtype=np.int64)

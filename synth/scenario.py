@@ -91,3 +91,76 @@ class Scenario:
         out = torch.empty((w.L, w.S, w.B, w.Hq, w.hd), dtype=self.tdtype, device=self.device)
         lse = torch.empty((w.L, w.S, w.B, w.Hq), dtype=torch.float32, device=self.device)
         return out, lse
+
+
+class TrainScenario:
+    """Training-shaped forward of the second drafter pass (Algorithm 2): the
+    recorded responses are committed once by prefill; every anchored block is
+    a virtual sequence whose page-table row is its response's (pages are
+    shared), whose window starts at a + 1 and whose u rejected rows become its
+    carry segment through a carry-only route, so that its committed length is
+    the shifted anchor a' and its queries sit at a' + i."""
+
+    def __init__(self, w: wl.Workload, device: str = "cuda"):
+        import torch
+        import paper_2609_14717_amd as co
+        assert w.anchors and w.seq_len
+        self.w, self.device, self.torch, self.co = w, device, torch, co
+        S, A, B = w.S, w.anchors, w.B
+        V = S * A
+        P = w.max_pages_per_seq
+        self.pt = wl.page_table(w)
+        self.dims = co.make_dims(S, w.seq_len, w.Dcat, w.d, w.L, w.Hq, w.Hkv, w.hd, P,
+                                 self.pt.size, w.dtype, w.theta)
+        self.st = co.alloc_state(self.dims, self.pt, device)
+        self.wf = sdev.materialise(w, wl.spec_wf(w), device)
+        self.wkv = sdev.materialise(w, wl.spec_wkv(w), device)
+        self.e = sdev.materialise(w, wl.spec_e(w), device)
+        self.W = co.weights(self.wf, self.wkv, self.e)
+        dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        # prefill: every recorded position of every response, committed, no E
+        h = torch.empty((S, w.seq_len, w.Dcat), dtype=dt, device=device)
+        for s in range(S):
+            st_, shape, strides, base, sigma = wl.spec_hctx(w, s, 0, w.seq_len)
+            sdev.fill(h[s], w.key(st_), shape, strides, base, sigma)
+        rt = co.alloc_route(S, w.seq_len, device)
+        ws = torch.empty(max(co.workspace_bytes(self.dims, co.CO_WS_PROJECT), 256),
+                         dtype=torch.uint8, device=device)
+        co.carryover_route(self.dims, None, None, co.CO_ROUTE_ACCEPT_ALL, self.st, rt)
+        co.carryover_project_kv(self.dims, self.W, h, rt, self.st, ws)
+        del h, ws
+        # virtual sequences
+        self.a, self.u, self.a2 = wl.anchors(w)
+        self.vdims = co.make_dims(V, B, w.Dcat, w.d, w.L, w.Hq, w.Hkv, w.hd, P, self.pt.size,
+                                  w.dtype, w.theta)
+        self.vpt = np.repeat(self.pt, A, axis=0)
+        CP = -(-B // wl.PAGE)
+        self.vst = dict(
+            ctx_len=torch.from_numpy((self.a.ravel() + 1).astype(np.int32)).to(device),
+            carry_len=torch.zeros(V, dtype=torch.int32, device=device),
+            page_table=torch.from_numpy(self.vpt).to(device),
+            k_cache=self.st["k_cache"], v_cache=self.st["v_cache"],
+            k_carry=torch.zeros((w.L, V, CP, w.Hkv, wl.PAGE, w.hd), dtype=dt, device=device),
+            v_carry=torch.zeros((w.L, V, CP, w.Hkv, w.hd, wl.PAGE), dtype=dt, device=device),
+            status=torch.zeros(1, dtype=torch.int32, device=device))
+        self.vrt = co.alloc_route(V, B, device)
+        m = (B - self.u.ravel()).astype(np.int32)
+        draft, target = wl.tokens_for(w, 0, m)
+        self.draft = torch.from_numpy(draft).to(device)
+        self.target = torch.from_numpy(target).to(device)
+        self.hidden = sdev.materialise(w, wl.spec_h(w, 0, S=V), device)   # first-pass states
+        self.q = sdev.materialise(w, wl.spec_q(w, 0, S=V), device)
+        self.ws = torch.zeros(max(co.workspace_bytes(self.vdims, co.CO_WS_ROUND), 256),
+                              dtype=torch.uint8, device=device)
+        self.out = torch.empty((w.L, V, B, w.Hq, w.hd), dtype=dt, device=device)
+        self.lse = torch.empty((w.L, V, B, w.Hq), dtype=torch.float32, device=device)
+
+    def forward(self):
+        """Carry rows of every anchored block, then the block attention of all of them."""
+        co = self.co
+        co.carryover_route(self.vdims, self.draft, self.target, co.CO_ROUTE_CARRY_ONLY,
+                           self.vst, self.vrt)
+        co.carryover_project_kv(self.vdims, self.W, self.hidden, self.vrt, self.vst, self.ws)
+        co.drafter_block_attention(self.vdims, 0, self.w.L, self.q, self.vst, self.out, self.lse,
+                                   0, self.ws)
+        return self.out, self.lse

@@ -161,16 +161,20 @@ def tokens_for(w: Workload, rnd: int, m: np.ndarray) -> tuple[np.ndarray, np.nda
     return draft.astype(np.int32), target.astype(np.int32)
 
 
-def anchors(w: Workload) -> tuple[np.ndarray, np.ndarray]:
-    """Training-shaped forward: shifted anchors a' [S][A] (sorted, distinct, in
-    [1, seq_len - B]) and rejected counts u [S][A] ~ U{0..B}."""
-    hi = w.seq_len - w.B
+def anchors(w: Workload) -> tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Training-shaped forward (Algorithm 2): initial anchors a [S][A], sorted
+    and distinct in [0, seq_len - B - 1]; rejected counts u [S][A] ~ U{0..B};
+    accepted m = B - u; shifted anchors a' = a + m + 1 (Algorithm 2 step 3).
+    The verified window of anchor a starts at position a + 1, so its rejected
+    rows sit at a' + r, r < u."""
+    hi = w.seq_len - w.B                      # a in [0, hi - 1]
     a = np.empty((w.S, w.anchors), dtype=np.int32)
     for s in range(w.S):
         keys = draw_u64(w.key(ST_ANCHOR), s * TCAP + np.arange(hi))
-        a[s] = np.sort(np.argsort(keys, kind="stable")[: w.anchors] + 1)
+        a[s] = np.sort(np.argsort(keys, kind="stable")[: w.anchors])
     u = uniform_int(w.key(ST_U), np.arange(w.S * w.anchors), 0, w.B).astype(np.int32)
-    return a, u.reshape(w.S, w.anchors)
+    u = u.reshape(w.S, w.anchors)
+    return a, u, a + (w.B - u) + 1
 
 
 # ------------------------------------------------- logical layouts of big tensors
@@ -220,6 +224,6 @@ def spec_kv_direct(w, which, s, t0, n):
 
 def host_block(w: Workload, spec, dtype: str | None = None) -> np.ndarray:
     """Materialise a described block on the host (fp32 array or bf16 bits)."""
-    from . import normal, grid_index
+    from . import normal_block
     st, shape, strides, base, sigma = spec
-    return normal(w.key(st), grid_index(shape, strides, base), sigma, dtype or w.dtype)
+    return normal_block(w.key(st), shape, strides, base, sigma, dtype or w.dtype)

@@ -12,8 +12,67 @@ from synth import workloads as wl
 TOL = {"bf16": 2e-2, "f32": 1e-4}
 
 
-def host(w, spec, dtype=None):
-    return synth.to_f64(wl.host_block(w, spec, dtype), dtype or w.dtype)
+def host(w, spec, dtype=None, out=np.float64):
+    """A described block, widened exactly to ``out`` (float64, or float32 for
+    bf16/fp32 data that a float32 store keeps exactly)."""
+    raw = wl.host_block(w, spec, dtype)
+    if out == np.float32:
+        return raw if (dtype or w.dtype) == "f32" else synth.bf16_bits_to_f32(raw)
+    return synth.to_f64(raw, dtype or w.dtype)
+
+
+def seq_block(w, spec, axis, seqs):
+    """A described block with only the rows ``seqs`` of axis ``axis`` drawn (others zero)."""
+    st_, shape, strides, base, sigma = spec
+    if len(seqs) == shape[axis]:
+        return host(w, spec)
+    out = np.zeros(shape, np.float64)
+    sub = tuple(1 if i == axis else n for i, n in enumerate(shape))
+    for s in seqs:
+        blk = host(w, (st_, sub, strides, base + s * strides[axis], sigma))
+        idx = [slice(None)] * len(shape)
+        idx[axis] = slice(s, s + 1)
+        out[tuple(idx)] = blk
+    return out
+
+
+class OracleTrain:
+    """The oracle's view of the training-shaped forward (Algorithm 2, second
+    pass) for a sample of anchored blocks (virtual sequences)."""
+
+    def __init__(self, w, sample):
+        self.w = w
+        S, A, B = w.S, w.anchors, w.B
+        V = S * A
+        self.sample = list(sample)
+        self.WF = host(w, wl.spec_wf(w))
+        self.WKV = host(w, wl.spec_wkv(w))
+        self.E = host(w, wl.spec_e(w))
+        self.a, self.u, self.a2 = wl.anchors(w)
+        self.pt = wl.page_table(w)
+        self.vpt = np.repeat(self.pt, A, axis=0)
+        # the recorded responses, projected without E at positions 0..seq_len-1
+        self.parent = {}
+        for s in sorted({v // A for v in self.sample}):
+            h = host(w, wl.spec_hctx(w, s, 0, w.seq_len))
+            self.parent[s] = oracle.project(h, self.E, np.zeros(w.seq_len, bool), self.WF,
+                                            self.WKV, np.arange(w.seq_len), w.L, w.Hkv, w.hd,
+                                            w.theta)
+        self.st = oracle.State(V, w.L, w.Hkv, w.hd)
+        a2 = self.a2.ravel()
+        for v in self.sample:
+            k, vv = self.parent[v // A]
+            n = int(a2[v])
+            self.st.set_committed(v, k[:n].transpose(1, 0, 2, 3), vv[:n].transpose(1, 0, 2, 3))
+        m = (B - self.u.ravel()).astype(np.int32)
+        draft, target = wl.tokens_for(w, 0, m)
+        self.rr = oracle.route(draft, target, self.a.ravel() + 1, np.zeros(V, np.int32), self.vpt,
+                               self.pt.size, "carry_only")
+        H = seq_block(w, wl.spec_h(w, 0, S=V), 0, self.sample)
+        oracle.round_update(self.st, self.rr, H, self.E, self.WF, self.WKV, w.theta, "carry_only",
+                            seqs=self.sample)
+        Q = seq_block(w, wl.spec_q(w, 0, S=V), 1, self.sample)
+        self.O, self.LSE = oracle.attend_state(self.st, Q, w.Hq, w.theta, seqs=self.sample)
 
 
 class OracleRun:
@@ -29,12 +88,15 @@ class OracleRun:
         self.num_pages = self.pt.size
         self.st = oracle.State(w.S, w.L, w.Hkv, w.hd, store)
         self.ctx0 = wl.initial_ctx(w)
+        # integer lengths of every sequence (the float state covers self.seqs only)
+        self._ctx = self.ctx0.astype(np.int32).copy()
         self._carry = np.zeros(w.S, np.int32)
         for s in self.seqs:
             n = int(self.ctx0[s])
             if w.ctx_mode == "direct":
-                k = host(w, wl.spec_kv_direct(w, "k", s, 0, n)).transpose(0, 2, 1, 3)
-                v = host(w, wl.spec_kv_direct(w, "v", s, 0, n)).transpose(0, 2, 1, 3)
+                wide = np.float32 if store == np.float32 else np.float64
+                k = host(w, wl.spec_kv_direct(w, "k", s, 0, n), out=wide).transpose(0, 2, 1, 3)
+                v = host(w, wl.spec_kv_direct(w, "v", s, 0, n), out=wide).transpose(0, 2, 1, 3)
                 self.st.set_committed(s, k, v)
             elif n:
                 h = host(w, wl.spec_hctx(w, s, 0, n))
@@ -43,16 +105,17 @@ class OracleRun:
                 self.st.commit_and_replace(s, k, v, k[:0], v[:0])
 
     def ctx_len(self):
-        c = self.ctx0.copy()
         for s in self.seqs:
-            c[s] = self.st.ck[s].shape[1]
-        return c
+            assert self.st.ck[s].shape[1] == self._ctx[s]
+        return self._ctx.copy()
 
     def carry_len(self):
-        c = self._carry.copy()
         for s in self.seqs:
-            c[s] = self.st.uk[s].shape[1]
-        return c
+            assert self.st.uk[s].shape[1] == self._carry[s]
+        return self._carry.copy()
+
+    def seq_block(self, spec, axis):
+        return seq_block(self.w, spec, axis, self.seqs)
 
     def round(self, r, mode="carry", attend=True, layers=None):
         w = self.w
@@ -60,12 +123,14 @@ class OracleRun:
         draft, target = wl.tokens_for(w, r, m)
         rr = oracle.route(draft, target, self.ctx_len(), self.carry_len(), self.pt,
                           self.num_pages, mode)
-        H = host(w, wl.spec_h(w, r))
+        H = self.seq_block(wl.spec_h(w, r), 0)
         oracle.round_update(self.st, rr, H, self.E, self.WF, self.WKV, w.theta, mode,
                             seqs=self.seqs)
+        self._ctx = np.asarray(rr["ctx_len"], np.int32).copy()
+        self._carry = np.asarray(rr["carry_len"], np.int32).copy()
         if not attend:
             return rr, None, None
-        Q = host(w, wl.spec_q(w, r))
+        Q = self.seq_block(wl.spec_q(w, r), 1)
         O, LSE = oracle.attend_state(self.st, Q, w.Hq, w.theta, seqs=self.seqs, layers=layers)
         return rr, O, LSE
 

@@ -131,3 +131,110 @@ def test_attention_slicings(w, slicing, monkeypatch):
     if slicing[1]:
         monkeypatch.setenv("CO_ATTN_ROUND_TILES", slicing[1])
     run_rounds(w, 2)
+
+
+def test_long_chain_5layer_sampled():
+    """The 64-round, 5-layer chain at full size (16 sequences, contexts of
+    16K-32K tokens, head_dim 128, 32/8 heads), in the launch configuration of
+    a serving round.  Every round: routing, accepted lengths, descriptors and
+    lengths of all 16 sequences bit-exact; the committed rows written and the
+    carry rows of one sampled sequence within tolerance.  At rounds 0, 1, 31
+    and 63 also the attention output of that sequence in layers 0 and 4."""
+    import paper_2609_14717_amd as co
+    Scenario = _gpu()
+    w = wl.LONG_CHAIN
+    sample, layers, check = 5, [0, 4], {0, 1, 31, 63}
+    tol = TOL[w.dtype]
+    print(f"[parity] workload={w.name} rounds={w.rounds} sample={sample}", flush=True)
+    sc = Scenario(w)
+    orc = OracleRun(w, seqs=[sample], store=np.float32)
+    for r in range(w.rounds):
+        hidden, q, draft, target, m = sc.round_inputs(r)
+        out, lse = sc.new_output()
+        co.carryover_round(sc.dims, sc.W, hidden, draft, target, q, sc.st, sc.rt, out, lse, 0,
+                           sc.ws)
+        torch.cuda.synchronize()
+        assert co.carryover_read_status(sc.st) == 0
+        att = r in check
+        rr, O, LSE = orc.round(r, attend=att, layers=layers if att else None)
+        for key in ("accept_len", "row_pos", "row_dst"):
+            np.testing.assert_array_equal(sc.rt[key].cpu().numpy(), rr[key], err_msg=f"r{r} {key}")
+        np.testing.assert_array_equal(sc.st["ctx_len"].cpu().numpy(), rr["ctx_len"])
+        np.testing.assert_array_equal(sc.st["carry_len"].cpu().numpy(), rr["carry_len"])
+        s = sample
+        mm = int(rr["accept_len"][s])
+        p0 = int(rr["ctx_len"][s]) - mm
+        u = int(rr["carry_len"][s])
+        for layer in range(w.L):
+            if mm:
+                gk, gv = gather_committed(sc.st, sc.pt, s, layer, p0, p0 + mm)
+                assert_heads_close(gk, orc.st.ck[s][layer, p0:p0 + mm], tol, f"r{r} C_k l{layer}")
+                assert_heads_close(gv, orc.st.cv[s][layer, p0:p0 + mm], tol, f"r{r} C_v l{layer}")
+            if u:
+                gk, gv = gather_carry(sc.st, s, layer, u)
+                assert_heads_close(gk, orc.st.uk[s][layer], tol, f"r{r} U_k l{layer}")
+                assert_heads_close(gv, orc.st.uv[s][layer], tol, f"r{r} U_v l{layer}")
+        if att:
+            g = to_np(out[:, s])
+            gl = lse[:, s].cpu().numpy().astype(np.float64)
+            for layer in layers:
+                assert_heads_close(g[layer], O[layer, s], tol, f"r{r} O layer {layer}")
+                err = np.abs(gl[layer] - LSE[layer, s]).max()
+                assert err <= tol, f"r{r} LSE layer {layer}: {err}"
+            print(f"[parity] {w.name} round {r} checked", flush=True)
+
+
+def test_train_fwd_sampled():
+    """The training-shaped parallel forward at full size: 8 responses x 4096
+    positions committed by prefill, 256 anchored blocks each (2048 virtual
+    sequences sharing their response's pages), every block's rejected rows
+    projected with E into its own carry segment, then block attention of all
+    2048 blocks over their recorded prefix [0, a') plus their carry rows.
+    Routing of all 2048 blocks bit-exact; for a sample of blocks the carry rows
+    and the attention output; for the sampled responses the prefilled rows."""
+    from helpers import OracleTrain
+    Scenario = _gpu()
+    from synth.scenario import TrainScenario
+    import paper_2609_14717_amd as co
+    w = wl.TRAIN_FWD
+    tol = TOL[w.dtype]
+    A = w.anchors
+    a, u, a2 = wl.anchors(w)
+    uf, a2f = u.ravel(), a2.ravel()
+    sample = {0, A - 1, 7 * A, 8 * A - 1, int(np.argmin(a2f)), int(np.argmax(a2f))}
+    for want in (0, w.B):                       # full acceptance, full rejection
+        hit = np.flatnonzero(uf == want)
+        if hit.size:
+            sample.add(int(hit[0]))
+    sample |= {int(x) for x in np.random.default_rng(5).choice(8 * A, 6, replace=False)}
+    sample = sorted(sample)
+    print(f"[parity] workload={w.name} sample={sample}", flush=True)
+    sc = TrainScenario(w)
+    out, lse = sc.forward()
+    torch.cuda.synchronize()
+    assert co.carryover_read_status(sc.vst) == 0 and co.carryover_read_status(sc.st) == 0
+    orc = OracleTrain(w, sample)
+    rr = orc.rr
+    for key in ("accept_len", "row_pos", "row_dst"):
+        np.testing.assert_array_equal(sc.vrt[key].cpu().numpy(), rr[key], err_msg=key)
+    np.testing.assert_array_equal(sc.vst["ctx_len"].cpu().numpy(), rr["ctx_len"])
+    np.testing.assert_array_equal(sc.vst["carry_len"].cpu().numpy(), rr["carry_len"])
+    np.testing.assert_array_equal(rr["ctx_len"], a2f)
+    g = to_np(out)
+    gl = lse.cpu().numpy().astype(np.float64)
+    for v in sample:
+        nu = int(rr["carry_len"][v])
+        for layer in range(w.L):
+            if nu:
+                gk, gv = gather_carry(sc.vst, v, layer, nu)
+                assert_heads_close(gk, orc.st.uk[v][layer], tol, f"U_k v{v}")
+                assert_heads_close(gv, orc.st.uv[v][layer], tol, f"U_v v{v}")
+        assert_heads_close(g[:, v], orc.O[:, v], tol, f"O v{v}")
+        err = np.abs(gl[:, v] - orc.LSE[:, v]).max()
+        assert err <= tol, f"LSE v{v}: {err}"
+    for s, (k, vv) in orc.parent.items():
+        for layer in range(w.L):
+            for t0, t1 in ((0, 40), (w.seq_len - 40, w.seq_len)):
+                gk, gv = gather_committed(sc.st, sc.pt, s, layer, t0, t1)
+                assert_heads_close(gk, k[t0:t1, layer], tol, f"prefill K s{s}")
+                assert_heads_close(gv, vv[t0:t1, layer], tol, f"prefill V s{s}")

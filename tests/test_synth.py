@@ -57,13 +57,32 @@ def test_page_table_is_a_permutation():
 
 
 def test_anchors_sorted_distinct_in_range():
-    a, u = wl.anchors(wl.TRAIN_FWD)
-    assert a.shape == (8, 256) and u.shape == (8, 256)
+    a, u, a2 = wl.anchors(wl.TRAIN_FWD)
+    assert a.shape == (8, 256) and u.shape == (8, 256) and a2.shape == (8, 256)
     for row in a:
-        assert np.all(np.diff(row) > 0) and row[0] >= 1 and row[-1] <= 4096 - 16
+        assert np.all(np.diff(row) > 0) and row[0] >= 0 and row[-1] <= 4096 - 16 - 1
     assert u.min() >= 0 and u.max() <= 16
+    # shifted anchor: the next correction/bonus position, never past the response
+    np.testing.assert_array_equal(a2, a + (16 - u) + 1)
+    assert a2.min() >= 1 and a2.max() <= 4096
 
 
 def test_grid_index_matches_layout():
     idx = synth.grid_index((2, 3, 4), (100, 10, 1), 5)
     assert idx[1, 2, 3] == 5 + 100 + 20 + 3
+
+
+def test_c_host_generator_matches_numpy_definition():
+    """The C build of the block generator gives the numpy definition's bits."""
+    import synth
+    if synth.host_lib() is None:
+        synth.build_host()
+    cases = [((3, 5, 7), (1000, 11, 1), 17), ((4, 2, 9, 16), (5000, 800, 16, 1), 123456789),
+             ((64,), (3,), 0), ((2, 1, 130), (1 << 20, 7, 1), 5)]
+    for shape, strides, base in cases:
+        for dtype in ("f32", "bf16"):
+            a = synth.normal_block(0x1234567890ABCDEF, shape, strides, base, 0.37, dtype, True)
+            b = synth.normal_block(0x1234567890ABCDEF, shape, strides, base, 0.37, dtype, False)
+            assert a.dtype == b.dtype and a.shape == b.shape
+            np.testing.assert_array_equal(a.view(np.uint16 if dtype == "bf16" else np.uint32),
+                                          b.view(np.uint16 if dtype == "bf16" else np.uint32))
