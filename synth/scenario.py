@@ -76,10 +76,11 @@ class Scenario:
         co.carryover_project_kv(pd, self.W, hidden, rt, self.st, ws)
         return rt
 
-    def round_inputs(self, r: int):
-        """(hidden, q, draft, target, m) of round r on the device; m on the host."""
+    def round_inputs(self, r: int, m=None):
+        """(hidden, q, draft, target, m) of round r on the device; m on the host
+        (the workload's draw, or the given accepted lengths)."""
         w, torch = self.w, self.torch
-        m = wl.accepted_lengths(w, r)
+        m = wl.accepted_lengths(w, r) if m is None else np.asarray(m, np.int32)
         draft, target = wl.tokens_for(w, r, m)
         hidden = sdev.materialise(w, wl.spec_h(w, r), self.device)
         q = sdev.materialise(w, wl.spec_q(w, r), self.device)

@@ -117,9 +117,9 @@ class OracleRun:
     def seq_block(self, spec, axis):
         return seq_block(self.w, spec, axis, self.seqs)
 
-    def round(self, r, mode="carry", attend=True, layers=None):
+    def round(self, r, mode="carry", attend=True, layers=None, m=None):
         w = self.w
-        m = wl.accepted_lengths(w, r)
+        m = wl.accepted_lengths(w, r) if m is None else np.asarray(m, np.int32)
         draft, target = wl.tokens_for(w, r, m)
         rr = oracle.route(draft, target, self.ctx_len(), self.carry_len(), self.pt,
                           self.num_pages, mode)
@@ -177,3 +177,35 @@ def gather_carry(st, s, layer, n):
     k = st["k_carry"][layer, s][r // 16, :, r % 16, :]
     v = st["v_carry"][layer, s][r // 16, :, :, r % 16]
     return to_np(k), to_np(v)
+
+
+def compare_round(sc, orc, rr, O, LSE, out, lse, rt, seqs, what):
+    w = sc.w
+    tol = TOL[w.dtype]
+    # integer results: bit-exact
+    np.testing.assert_array_equal(rt["accept_len"].cpu().numpy()[seqs], rr["accept_len"][seqs])
+    np.testing.assert_array_equal(rt["row_pos"].cpu().numpy()[seqs], rr["row_pos"][seqs])
+    np.testing.assert_array_equal(rt["row_dst"].cpu().numpy()[seqs], rr["row_dst"][seqs])
+    np.testing.assert_array_equal(sc.st["ctx_len"].cpu().numpy()[seqs], rr["ctx_len"][seqs])
+    np.testing.assert_array_equal(sc.st["carry_len"].cpu().numpy()[seqs], rr["carry_len"][seqs])
+    # attention
+    g = to_np(out)
+    gl = lse.cpu().numpy().astype(np.float64)
+    for s in seqs:
+        assert_heads_close(g[:, s], O[:, s], tol, f"{what} O seq {s}")
+        err = np.abs(gl[:, s] - LSE[:, s]).max()
+        assert err <= tol, f"{what} LSE seq {s}: {err}"
+    # rows written this round
+    for s in seqs:
+        m = int(rr["accept_len"][s])
+        p0 = int(rr["ctx_len"][s]) - m
+        for layer in range(w.L):
+            if m:
+                gk, gv = gather_committed(sc.st, sc.pt, s, layer, p0, p0 + m)
+                assert_heads_close(gk, orc.st.ck[s][layer, p0:p0 + m], tol, f"{what} C_k s{s}")
+                assert_heads_close(gv, orc.st.cv[s][layer, p0:p0 + m], tol, f"{what} C_v s{s}")
+            u = int(rr["carry_len"][s])
+            if u:
+                gk, gv = gather_carry(sc.st, s, layer, u)
+                assert_heads_close(gk, orc.st.uk[s][layer], tol, f"{what} U_k s{s}")
+                assert_heads_close(gv, orc.st.uv[s][layer], tol, f"{what} U_v s{s}")

@@ -14,8 +14,8 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-from helpers import (TOL, OracleRun, assert_heads_close, gather_carry, gather_committed,  # noqa: E402
-                     to_np)
+from helpers import (TOL, OracleRun, assert_heads_close, compare_round, gather_carry,  # noqa: E402
+                     gather_committed, to_np)
 
 SMALL_RAGGED = wl.RAGGED32.replace(name="small_ragged", S=3, L=2, ctx_lo=100, ctx_hi=2500,
                                    rounds=6, accept=("geom", 0.3), seed=0x5EED01)
@@ -34,38 +34,6 @@ def _gpu():
         pytest.skip("no GPU")
     from synth.scenario import Scenario
     return Scenario
-
-
-def compare_round(sc, orc, rr, O, LSE, out, lse, rt, seqs, what):
-    w = sc.w
-    tol = TOL[w.dtype]
-    # integer results: bit-exact
-    np.testing.assert_array_equal(rt["accept_len"].cpu().numpy()[seqs], rr["accept_len"][seqs])
-    np.testing.assert_array_equal(rt["row_pos"].cpu().numpy()[seqs], rr["row_pos"][seqs])
-    np.testing.assert_array_equal(rt["row_dst"].cpu().numpy()[seqs], rr["row_dst"][seqs])
-    np.testing.assert_array_equal(sc.st["ctx_len"].cpu().numpy()[seqs], rr["ctx_len"][seqs])
-    np.testing.assert_array_equal(sc.st["carry_len"].cpu().numpy()[seqs], rr["carry_len"][seqs])
-    # attention
-    g = to_np(out)
-    gl = lse.cpu().numpy().astype(np.float64)
-    for s in seqs:
-        assert_heads_close(g[:, s], O[:, s], tol, f"{what} O seq {s}")
-        err = np.abs(gl[:, s] - LSE[:, s]).max()
-        assert err <= tol, f"{what} LSE seq {s}: {err}"
-    # rows written this round
-    for s in seqs:
-        m = int(rr["accept_len"][s])
-        p0 = int(rr["ctx_len"][s]) - m
-        for layer in range(w.L):
-            if m:
-                gk, gv = gather_committed(sc.st, sc.pt, s, layer, p0, p0 + m)
-                assert_heads_close(gk, orc.st.ck[s][layer, p0:p0 + m], tol, f"{what} C_k s{s}")
-                assert_heads_close(gv, orc.st.cv[s][layer, p0:p0 + m], tol, f"{what} C_v s{s}")
-            u = int(rr["carry_len"][s])
-            if u:
-                gk, gv = gather_carry(sc.st, s, layer, u)
-                assert_heads_close(gk, orc.st.uk[s][layer], tol, f"{what} U_k s{s}")
-                assert_heads_close(gv, orc.st.uv[s][layer], tol, f"{what} U_v s{s}")
 
 
 def run_rounds(w, n_rounds, mode="carry", seqs=None, check_context=True):
