@@ -577,8 +577,14 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
       }
       const int T = n_segs * T1;
       if (pass_begin < 0) {
-        r0 = static_cast<int>(static_cast<int64_t>(T) * w / n_wg);
-        r1 = static_cast<int>(static_cast<int64_t>(T) * (w + 1) / n_wg);
+        const int64_t tw1 = static_cast<int64_t>(T) * (w + 1);
+        if (tw1 <= 0xFFFFFFFFll) {   // 32-bit divisions
+          r0 = static_cast<int>(static_cast<uint32_t>(tw1 - T) / static_cast<uint32_t>(n_wg));
+          r1 = static_cast<int>(static_cast<uint32_t>(tw1) / static_cast<uint32_t>(n_wg));
+        } else {
+          r0 = static_cast<int>((tw1 - T) / n_wg);
+          r1 = static_cast<int>(tw1 / n_wg);
+        }
         int* hdr = reinterpret_cast<int*>(a.ws);
         if (tid == 0) {
           hdr[S + 1 + w + 1] = r1;
@@ -650,6 +656,25 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
       while (pb < n_p && pc[pb].begin < rb) ++pb;
       const int nr = rb - ra;
 
+      // this wavefront's sub-slice [sb, se) and the descriptors of its pages:
+      // row >= 0 committed K/V row, -1-r carry row r, INT_MIN nothing to read
+      const int k = (wave - rot + NW) % NW;
+      const int sb = ra + static_cast<int>(static_cast<int64_t>(nr) * k / NW);
+      const int se = ra + static_cast<int>(static_cast<int64_t>(nr) * (k + 1) / NW);
+      int pg_row[RQ], pg_nv[RQ];
+      int pt[RQ], pidx[RQ], lpv[RQ];
+      {
+#pragma unroll
+        for (int q = 0; q < RQ; ++q) {   // page-table loads first
+          const int jp = lane + 64 * q, t = sb + (jp >> 1);
+          int i = pa;
+          while (i + 1 < pb && pc[i].end <= t) ++i;
+          pidx[q] = i;
+          lpv[q] = 2 * (t - pc[i].seg_begin) + (jp & 1);
+          const bool com = t < se && lpv[q] < (pc[i].ctx + kPage - 1) / kPage;
+          pt[q] = a.page_table[com ? static_cast<int64_t>(pc[i].s) * a.max_pages + lpv[q] : 0];
+        }
+      }
       // stage the queries of the round's pieces, rotated at ctx + i and scaled
       {
         u16x4 qlo[QV], qhi[QV];
@@ -694,24 +719,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
         }
       }
 
-      // this wavefront's sub-slice [sb, se) and the descriptors of its pages:
-      // row >= 0 committed K/V row, -1-r carry row r, INT_MIN nothing to read
-      const int k = (wave - rot + NW) % NW;
-      const int sb = ra + static_cast<int>(static_cast<int64_t>(nr) * k / NW);
-      const int se = ra + static_cast<int>(static_cast<int64_t>(nr) * (k + 1) / NW);
-      int pg_row[RQ], pg_nv[RQ];
       {
-        int pt[RQ], pidx[RQ], lpv[RQ];
-#pragma unroll
-        for (int q = 0; q < RQ; ++q) {   // page-table loads first
-          const int jp = lane + 64 * q, t = sb + (jp >> 1);
-          int i = pa;
-          while (i + 1 < pb && pc[i].end <= t) ++i;
-          pidx[q] = i;
-          lpv[q] = 2 * (t - pc[i].seg_begin) + (jp & 1);
-          const bool com = t < se && lpv[q] < (pc[i].ctx + kPage - 1) / kPage;
-          pt[q] = a.page_table[com ? static_cast<int64_t>(pc[i].s) * a.max_pages + lpv[q] : 0];
-        }
 #pragma unroll
         for (int q = 0; q < RQ; ++q) {
           const int t = sb + ((lane + 64 * q) >> 1);

@@ -51,7 +51,7 @@ struct ProjectArgs {
 struct ProjectPlan {
   int f_tile, f_split;     // tile variant and K-splits of the F GEMM
   int kv_tile, kv_split;   // same for the K/V GEMM
-  size_t z_bytes, part_bytes, total;
+  size_t z_bytes, part_bytes, pe_bytes, total;
 };
 
 ProjectPlan plan_project(int M, int Dcat, int d, int n_kv, int hd, int dtype, int num_cus);

@@ -30,9 +30,10 @@ struct GemmArgs {
   int M, N, K, k_per_split;
   const void* A;           // [M][K]
   const void* B;           // [N][K]
-  const void* e;           // E added to carry rows of A (null: none)
+  const void* e;           // E: F(E) is added to carry rows (null: none)
   const int32_t* row_dst;  // carry rows: -1-r
   float* partial;          // [splits][M][N]
+  float* partial_e;        // [splits][N]: F(E) per K-split (split-K with E only)
   void* z_out;             // [M][N]
   int mode;
   KvDest kv;
@@ -46,9 +47,8 @@ __device__ __forceinline__ bool is_carry_row(int32_t dst) { return dst < 0 && ds
 // of window row `row`.  lo/hi hold the unrotated fp32 values of those dims;
 // inv_freq[i] = theta^(-2i/hd).
 template <typename T, int NP>
-__device__ void kv_store(const KvDest& e, int row, int seg, int i0, const float* lo,
-                         const float* hi, const double* inv_freq) {
-  const int32_t dst = e.row_dst[row];
+__device__ void kv_store(const KvDest& e, int row, int32_t dst, int pos, int seg, int i0,
+                         const float* lo, const float* hi, const double* inv_freq) {
   if (dst == kSkip) return;
   const int hd = e.hd, half = hd / 2;
   const int g = seg % e.Hkv;
@@ -83,7 +83,6 @@ __device__ void kv_store(const KvDest& e, int row, int seg, int i0, const float*
     vptr = static_cast<T*>(e.v_carry);
   }
   if (kind == 0) {
-    const int pos = e.row_pos[row];
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
       float c, s;
@@ -143,15 +142,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
   const uint16_t* Bw = static_cast<const uint16_t*>(g.B);
   const uint16_t* E = static_cast<const uint16_t*>(g.e);
 
-  // carry flags of this lane's A rows (read before any staged load is issued)
-  bool carry[TM];
-#pragma unroll
-  for (int tm = 0; tm < TM; ++tm) {
-    carry[tm] = false;
-    if constexpr (HAS_E) {
-      const int gr = m0 + (wm * TM + tm) * 16 + (lane & 15);
-      carry[tm] = gr < g.M && is_carry_row(g.row_dst[gr]);
-    }
+  // row descriptors of the tile's rows (thread t: row t % BM), consumed only by
+  // the epilogue; kept opaque until then so no wait lands before the main loop
+  const bool need_rows = HAS_E || g.mode == kModeKV;
+  int rd_dst = 0, rd_pos = 0;
+  if (need_rows) {
+    const int r = min(m0 + (tid % BM), g.M - 1);
+    rd_dst = g.row_dst[r];
+    if (g.mode == kModeKV) rd_pos = g.kv.row_pos[r];
   }
 
   auto issue = [&](int kt, int slot) {
@@ -182,6 +180,11 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
   for (int a = 0; a < TM; ++a)
 #pragma unroll
     for (int b = 0; b < TN; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // F(E) for this wavefront's columns: an extra M-tile whose rows all hold E
+  // (F is linear, so F(h + E) = F(h) + F(E); added to carried rows at the end)
+  f32x4 acc_e[HAS_E ? TN : 1];
+#pragma unroll
+  for (int b = 0; b < (HAS_E ? TN : 1); ++b) acc_e[b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
 #pragma unroll
   for (int st = 0; st < NSTAGE - 1; ++st)
@@ -194,36 +197,31 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
     const unsigned char* st = smem + (kt % NSTAGE) * STAGE_BYTES;
     const int ksteps = kt == nk - 1 ? last_ks : BK / 32;
     auto kstep = [&](int ks) {
+      // every fragment of the k-step in one group of LDS reads, one wait
+      constexpr int NR = TM + TN + (HAS_E ? 1 : 0);
       const int c = ks * 4 + (lane >> 4);
-      u16x8 af[TM], bfr[TN];
-      uint32_t aa[TM], ba[TN];
+      u16x8 fr[NR];
+      uint32_t ad[NR];
 #pragma unroll
       for (int a = 0; a < TM; ++a) {
         const int row = (wm * TM + a) * 16 + (lane & 15);
-        aa[a] = lds_addr(st + row * ROWB + ((c ^ (row & 15)) << 4));
+        ad[a] = lds_addr(st + row * ROWB + ((c ^ (row & 15)) << 4));
       }
 #pragma unroll
       for (int b = 0; b < TN; ++b) {
         const int row = BM + (wn * TN + b) * 16 + (lane & 15);
-        ba[b] = lds_addr(st + row * ROWB + ((c ^ (row & 15)) << 4));
+        ad[TM + b] = lds_addr(st + row * ROWB + ((c ^ (row & 15)) << 4));
       }
-      lds_read_group<TM>(af, aa);
-      lds_read_group<TN>(bfr, ba);
-      if constexpr (HAS_E) {
-        u16x8 ev[1];
-        const uint32_t ea[1] = {lds_addr(st + E_OFF + (c << 4))};
-        lds_read_group<1>(ev, ea);
-#pragma unroll
-        for (int a = 0; a < TM; ++a)
-          if (carry[a]) {
-#pragma unroll
-            for (int t = 0; t < 8; ++t) af[a][t] = f2bf(bf2f(af[a][t]) + bf2f(ev[0][t]));
-          }
-      }
+      if constexpr (HAS_E) ad[TM + TN] = lds_addr(st + E_OFF + (c << 4));
+      lds_read_group<NR>(fr, ad);
 #pragma unroll
       for (int a = 0; a < TM; ++a)
 #pragma unroll
-        for (int b = 0; b < TN; ++b) acc[a][b] = mfma16x16x32(af[a], bfr[b], acc[a][b]);
+        for (int b = 0; b < TN; ++b) acc[a][b] = mfma16x16x32(fr[a], fr[TM + b], acc[a][b]);
+      if constexpr (HAS_E) {
+#pragma unroll
+        for (int b = 0; b < TN; ++b) acc_e[b] = mfma16x16x32(fr[TM + TN], fr[TM + b], acc_e[b]);
+      }
     };
     if (ksteps == BK / 32) {
 #pragma unroll
@@ -247,6 +245,15 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
           const int col = n0 + (wn * TN + b) * 16 + (lane & 15);
           if (row < g.M && col < g.N) out[static_cast<int64_t>(row) * g.N + col] = acc[a][b][r];
         }
+    if constexpr (HAS_E) {
+      if (blockIdx.y == 0 && wm == 0 && lane < 16) {
+#pragma unroll
+        for (int b = 0; b < TN; ++b) {
+          const int col = n0 + (wn * TN + b) * 16 + lane;
+          if (col < g.N) g.partial_e[static_cast<int64_t>(blockIdx.z) * g.N + col] = acc_e[b][0];
+        }
+      }
+    }
     return;
   }
 
@@ -261,6 +268,19 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
         sc[((wm * TM + a) * 16 + (lane >> 4) * 4 + r) * LDC + (wn * TN + b) * 16 + (lane & 15)] =
             acc[a][b][r];
   if (g.mode == kModeKV && tid < g.kv.hd / 2) inv_tab[tid] = g.kv.rope_inv[tid];
+  __shared__ float fe_lds[HAS_E ? BN : 1];
+  __shared__ int dst_lds[BM], pos_lds[BM];
+  asm volatile("" : "+v"(rd_dst), "+v"(rd_pos));
+  if (need_rows && tid < BM) {
+    dst_lds[tid] = rd_dst;
+    pos_lds[tid] = rd_pos;
+  }
+  if constexpr (HAS_E) {
+    if (wm == 0 && lane < 16) {
+#pragma unroll
+      for (int b = 0; b < TN; ++b) fe_lds[(wn * TN + b) * 16 + lane] = acc_e[b][0];
+    }
+  }
   __syncthreads();
 
   if (g.mode == kModeZ) {
@@ -270,8 +290,15 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
       const int gr = m0 + row, gc = n0 + cc * 8;
       if (gr >= g.M || gc >= g.N) continue;
       u16x8 v;
+      if constexpr (HAS_E) {
+        const bool cy = is_carry_row(dst_lds[row]);
 #pragma unroll
-      for (int t = 0; t < 8; ++t) v[t] = f2bf(sc[row * LDC + cc * 8 + t]);
+        for (int t = 0; t < 8; ++t)
+          v[t] = f2bf(sc[row * LDC + cc * 8 + t] + (cy ? fe_lds[cc * 8 + t] : 0.f));
+      } else {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) v[t] = f2bf(sc[row * LDC + cc * 8 + t]);
+      }
       *reinterpret_cast<u16x8*>(z + static_cast<int64_t>(gr) * g.N + gc) = v;
     }
   } else {
@@ -287,7 +314,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
         lo[p] = sc[row * LDC + seg_local * hd + i0 + p];
         hi[p] = sc[row * LDC + seg_local * hd + hd / 2 + i0 + p];
       }
-      kv_store<uint16_t, 4>(g.kv, gr, gc0 / hd, i0, lo, hi, inv_tab);
+      kv_store<uint16_t, 4>(g.kv, gr, dst_lds[row], pos_lds[row], gc0 / hd, i0, lo, hi, inv_tab);
     }
   }
 }
@@ -345,11 +372,16 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
 
 template <typename T>
 __global__ __launch_bounds__(256) void epi_z_kernel(const float* part, int splits, int M, int N,
-                                                    T* z) {
+                                                    T* z, const float* part_e,
+                                                    const int32_t* row_dst) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (i >= static_cast<int64_t>(M) * N) return;
   float v = 0.f;
   for (int s = 0; s < splits; ++s) v += part[static_cast<int64_t>(s) * M * N + i];
+  if (part_e && is_carry_row(row_dst[i / N])) {
+    const int col = static_cast<int>(i % N);
+    for (int s = 0; s < splits; ++s) v += part_e[static_cast<int64_t>(s) * N + col];
+  }
   z[i] = to_elem<T>(v);
 }
 
@@ -372,7 +404,7 @@ __global__ __launch_bounds__(256) void epi_kv_kernel(const float* part, int spli
     lo += part[static_cast<int64_t>(s) * M * N + c_lo];
     hi += part[static_cast<int64_t>(s) * M * N + c_lo + half];
   }
-  kv_store<T, 1>(e, row, seg, p, &lo, &hi, inv_tab);
+  kv_store<T, 1>(e, row, e.row_dst[row], e.row_pos[row], seg, p, &lo, &hi, inv_tab);
 }
 
 // Tile variants (BM x BN, waves WM x WN, ring depth):
@@ -463,7 +495,8 @@ ProjectPlan plan_project(int M, int Dcat, int d, int n_kv, int hd, int dtype, in
   p.z_bytes = (static_cast<size_t>(M) * d * es + 255) / 256 * 256;
   const size_t pf = part(p.f_split, d), pk = part(p.kv_split, n_kv);
   p.part_bytes = ((pf > pk ? pf : pk) + 255) / 256 * 256;
-  p.total = p.z_bytes + p.part_bytes;
+  p.pe_bytes = (static_cast<size_t>(p.f_split) * d * 4 + 255) / 256 * 256;
+  p.total = p.z_bytes + p.part_bytes + p.pe_bytes;
   return p;
 }
 
@@ -479,6 +512,7 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
   f.M = a.M; f.N = a.d; f.K = a.Dcat;
   f.A = a.hidden; f.B = a.wf; f.e = a.e; f.row_dst = a.dst.row_dst;
   f.partial = part; f.z_out = z; f.kv = a.dst;
+  f.partial_e = reinterpret_cast<float*>(ws + p.z_bytes + p.part_bytes);
   GemmArgs kv{};
   kv.M = a.M; kv.N = n_kv; kv.K = a.d;
   kv.A = z; kv.B = a.wkv; kv.e = nullptr; kv.row_dst = a.dst.row_dst;
@@ -492,7 +526,8 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
                        stream, f);
     const int64_t nz = static_cast<int64_t>(a.M) * a.d;
     hipLaunchKernelGGL(epi_z_kernel<float>, dim3(static_cast<unsigned>((nz + 255) / 256)),
-                       dim3(256), 0, stream, part, 1, a.M, a.d, static_cast<float*>(z));
+                       dim3(256), 0, stream, part, 1, a.M, a.d, static_cast<float*>(z),
+                       static_cast<const float*>(nullptr), a.dst.row_dst);
     hipLaunchKernelGGL(gemm_f32_kernel, dim3((kv.N + 63) / 64, (kv.M + 31) / 32), dim3(256), 0,
                        stream, kv);
     const int64_t items = static_cast<int64_t>(a.M) * (n_kv / 2);
@@ -507,7 +542,8 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
   if (p.f_split > 1) {
     const int64_t nz = static_cast<int64_t>(a.M) * a.d;
     hipLaunchKernelGGL(epi_z_kernel<uint16_t>, dim3(static_cast<unsigned>((nz + 255) / 256)),
-                       dim3(256), 0, stream, part, p.f_split, a.M, a.d, static_cast<uint16_t*>(z));
+                       dim3(256), 0, stream, part, p.f_split, a.M, a.d, static_cast<uint16_t*>(z),
+                       static_cast<const float*>(a.e ? f.partial_e : nullptr), a.dst.row_dst);
   }
   kv.k_per_split = a.d / p.kv_split;
   kv.mode = p.kv_split > 1 ? kModePartial : kModeKV;
