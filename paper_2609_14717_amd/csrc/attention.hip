@@ -513,11 +513,12 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
     }
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
+      // arguments are <= 0 or -inf: the hardware exp2 is exact enough and gives 0 at -inf
       const float M = fmaxf(m_run[nt], mo[nt]);
-      const float f0 = (m_run[nt] == -INFINITY) ? 0.f : exp2f(m_run[nt] - M);
-      const float f1 = (mo[nt] == -INFINITY) ? 0.f : exp2f(mo[nt] - M);
-      const float lt = wave_sum_across_groups(l_run[nt]) * f0 + lo[nt] * f1;
-      l_run[nt] = grp == 0 ? lt : 0.f;
+      const float f0 = (m_run[nt] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run[nt] - M);
+      const float f1 = (mo[nt] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mo[nt] - M);
+      // l_run stays a per-lane partial; the parked row total joins lane group 0
+      l_run[nt] = l_run[nt] * f0 + (grp == 0 ? lo[nt] * f1 : 0.f);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) o[mt][nt] = o[mt][nt] * f0 + po[mt][nt] * f1;
       m_run[nt] = M;

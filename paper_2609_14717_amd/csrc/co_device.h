@@ -195,4 +195,28 @@ __device__ __forceinline__ void lds_read_group<9>(u16x8 (&v)[9], const uint32_t 
                : "memory");
 }
 
+template <>
+__device__ __forceinline__ void lds_read_group<10>(u16x8 (&v)[10], const uint32_t (&a)[10]) {
+  asm volatile("ds_read_b128 %0, %10\n\tds_read_b128 %1, %11\n\tds_read_b128 %2, %12\n\tds_read_b128 %3, %13\n\tds_read_b128 %4, %14\n\tds_read_b128 %5, %15\n\tds_read_b128 %6, %16\n\tds_read_b128 %7, %17\n\tds_read_b128 %8, %18\n\tds_read_b128 %9, %19\n\ts_waitcnt lgkmcnt(0)"
+               : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]), "=&v"(v[7]), "=&v"(v[8]), "=&v"(v[9])
+               : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7]), "v"(a[8]), "v"(a[9])
+               : "memory");
+}
+
+template <>
+__device__ __forceinline__ void lds_read_group<11>(u16x8 (&v)[11], const uint32_t (&a)[11]) {
+  asm volatile("ds_read_b128 %0, %11\n\tds_read_b128 %1, %12\n\tds_read_b128 %2, %13\n\tds_read_b128 %3, %14\n\tds_read_b128 %4, %15\n\tds_read_b128 %5, %16\n\tds_read_b128 %6, %17\n\tds_read_b128 %7, %18\n\tds_read_b128 %8, %19\n\tds_read_b128 %9, %20\n\tds_read_b128 %10, %21\n\ts_waitcnt lgkmcnt(0)"
+               : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]), "=&v"(v[7]), "=&v"(v[8]), "=&v"(v[9]), "=&v"(v[10])
+               : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7]), "v"(a[8]), "v"(a[9]), "v"(a[10])
+               : "memory");
+}
+
+template <>
+__device__ __forceinline__ void lds_read_group<12>(u16x8 (&v)[12], const uint32_t (&a)[12]) {
+  asm volatile("ds_read_b128 %0, %12\n\tds_read_b128 %1, %13\n\tds_read_b128 %2, %14\n\tds_read_b128 %3, %15\n\tds_read_b128 %4, %16\n\tds_read_b128 %5, %17\n\tds_read_b128 %6, %18\n\tds_read_b128 %7, %19\n\tds_read_b128 %8, %20\n\tds_read_b128 %9, %21\n\tds_read_b128 %10, %22\n\tds_read_b128 %11, %23\n\ts_waitcnt lgkmcnt(0)"
+               : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]), "=&v"(v[7]), "=&v"(v[8]), "=&v"(v[9]), "=&v"(v[10]), "=&v"(v[11])
+               : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7]), "v"(a[8]), "v"(a[9]), "v"(a[10]), "v"(a[11])
+               : "memory");
+}
+
 }  // namespace co

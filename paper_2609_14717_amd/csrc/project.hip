@@ -196,38 +196,78 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
     stage_barrier();
     const unsigned char* st = smem + (kt % NSTAGE) * STAGE_BYTES;
     const int ksteps = kt == nk - 1 ? last_ks : BK / 32;
-    auto kstep = [&](int ks) {
-      // every fragment of the k-step in one group of LDS reads, one wait
-      constexpr int NR = TM + TN + (HAS_E ? 1 : 0);
-      const int c = ks * 4 + (lane >> 4);
-      u16x8 fr[NR];
-      uint32_t ad[NR];
+    // KG k-steps' fragments are read as one group of LDS reads with one wait
+    constexpr int NR = TM + TN + (HAS_E ? 1 : 0);
+    constexpr int KG = 4 * NR <= 12 ? 4 : (2 * NR <= 12 ? 2 : 1);
+    auto kgroup = [&](int ks0) {
+      u16x8 fr[KG * NR];
+      uint32_t ad[KG * NR];
 #pragma unroll
-      for (int a = 0; a < TM; ++a) {
-        const int row = (wm * TM + a) * 16 + (lane & 15);
-        ad[a] = lds_addr(st + row * ROWB + ((c ^ (row & 15)) << 4));
+      for (int kk = 0; kk < KG; ++kk) {
+        const int c = (ks0 + kk) * 4 + (lane >> 4);
+#pragma unroll
+        for (int a = 0; a < TM; ++a) {
+          const int row = (wm * TM + a) * 16 + (lane & 15);
+          ad[kk * NR + a] = lds_addr(st + row * ROWB + ((c ^ (row & 15)) << 4));
+        }
+#pragma unroll
+        for (int b = 0; b < TN; ++b) {
+          const int row = BM + (wn * TN + b) * 16 + (lane & 15);
+          ad[kk * NR + TM + b] = lds_addr(st + row * ROWB + ((c ^ (row & 15)) << 4));
+        }
+        if constexpr (HAS_E) ad[kk * NR + TM + TN] = lds_addr(st + E_OFF + (c << 4));
       }
+      lds_read_group<KG * NR>(fr, ad);
 #pragma unroll
-      for (int b = 0; b < TN; ++b) {
-        const int row = BM + (wn * TN + b) * 16 + (lane & 15);
-        ad[TM + b] = lds_addr(st + row * ROWB + ((c ^ (row & 15)) << 4));
-      }
-      if constexpr (HAS_E) ad[TM + TN] = lds_addr(st + E_OFF + (c << 4));
-      lds_read_group<NR>(fr, ad);
+      for (int kk = 0; kk < KG; ++kk) {
+        const u16x8* f = fr + kk * NR;
 #pragma unroll
-      for (int a = 0; a < TM; ++a)
+        for (int a = 0; a < TM; ++a)
 #pragma unroll
-        for (int b = 0; b < TN; ++b) acc[a][b] = mfma16x16x32(fr[a], fr[TM + b], acc[a][b]);
-      if constexpr (HAS_E) {
+          for (int b = 0; b < TN; ++b) acc[a][b] = mfma16x16x32(f[a], f[TM + b], acc[a][b]);
+        if constexpr (HAS_E) {
 #pragma unroll
-        for (int b = 0; b < TN; ++b) acc_e[b] = mfma16x16x32(fr[TM + TN], fr[TM + b], acc_e[b]);
+          for (int b = 0; b < TN; ++b) acc_e[b] = mfma16x16x32(f[TM + TN], f[TM + b], acc_e[b]);
+        }
       }
     };
     if (ksteps == BK / 32) {
 #pragma unroll
-      for (int ks = 0; ks < BK / 32; ++ks) kstep(ks);
+      for (int ks = 0; ks < BK / 32; ks += KG) kgroup(ks);
     } else {
-      for (int ks = 0; ks < ksteps; ++ks) kstep(ks);
+      // a short last stage: whole groups, then single k-steps
+      for (int ks = 0; ks < ksteps; ks += KG) {
+        if (ks + KG <= ksteps) {
+          kgroup(ks);
+        } else {
+          for (int k1 = ks; k1 < ksteps; ++k1) {
+            constexpr int NR1 = NR;
+            u16x8 fr[NR1];
+            uint32_t ad[NR1];
+            const int c = k1 * 4 + (lane >> 4);
+#pragma unroll
+            for (int a = 0; a < TM; ++a) {
+              const int row = (wm * TM + a) * 16 + (lane & 15);
+              ad[a] = lds_addr(st + row * ROWB + ((c ^ (row & 15)) << 4));
+            }
+#pragma unroll
+            for (int b = 0; b < TN; ++b) {
+              const int row = BM + (wn * TN + b) * 16 + (lane & 15);
+              ad[TM + b] = lds_addr(st + row * ROWB + ((c ^ (row & 15)) << 4));
+            }
+            if constexpr (HAS_E) ad[TM + TN] = lds_addr(st + E_OFF + (c << 4));
+            lds_read_group<NR1>(fr, ad);
+#pragma unroll
+            for (int a = 0; a < TM; ++a)
+#pragma unroll
+              for (int b = 0; b < TN; ++b) acc[a][b] = mfma16x16x32(fr[a], fr[TM + b], acc[a][b]);
+            if constexpr (HAS_E) {
+#pragma unroll
+              for (int b = 0; b < TN; ++b) acc_e[b] = mfma16x16x32(fr[TM + TN], fr[TM + b], acc_e[b]);
+            }
+          }
+        }
+      }
     }
     stage_barrier();
   }
