@@ -1,0 +1,71 @@
+// K/V row stores shared by the projection kernels: rotate the key half of a
+// head at the row's absolute position (RoPE applied once, when the row is
+// projected: Appendix A, "Cache semantics") and scatter the row to its
+// committed page slot or carry row.
+#pragma once
+
+#include "co_kernels.h"
+
+namespace co {
+
+__device__ __forceinline__ bool is_carry_row(int32_t dst) { return dst < 0 && dst != kSkip; }
+
+// ------------------------------------------------------------- K/V stores
+
+// Store pairs (i0+p, i0+p+hd/2), p < NP, of head segment `seg` = (layer, K|V, head)
+// of window row `row`.  lo/hi hold the unrotated fp32 values of those dims;
+// inv_freq[i] = theta^(-2i/hd).
+template <typename T, int NP>
+__device__ inline void kv_store(const KvDest& e, int row, int32_t dst, int pos, int seg, int i0,
+                         const float* lo, const float* hi, const double* inv_freq) {
+  if (dst == kSkip) return;
+  const int hd = e.hd, half = hd / 2;
+  const int g = seg % e.Hkv;
+  const int kind = (seg / e.Hkv) & 1;
+  const int layer = seg / (2 * e.Hkv);
+  int64_t kbase, vbase;   // element offsets of dim 0 of this row in the K and V layouts
+  T* kptr;
+  T* vptr;
+  if (dst >= 0) {
+    const int page = dst / kPage, t = dst % kPage;
+    if (page >= e.num_pages) {
+      set_status(e.status, CO_ERR_PAGE_RANGE);
+      return;
+    }
+    const int64_t pg = (static_cast<int64_t>(layer) * e.num_pages + page) * e.Hkv + g;
+    kbase = (pg * kPage + t) * hd;
+    vbase = pg * hd * kPage + t;
+    kptr = static_cast<T*>(e.k_cache);
+    vptr = static_cast<T*>(e.v_cache);
+  } else {
+    const int r = -1 - dst;
+    if (r >= e.CP * kPage) {
+      set_status(e.status, CO_ERR_LENGTH);
+      return;
+    }
+    const int s = row / e.B;
+    const int cp = r / kPage, t = r % kPage;
+    const int64_t pg = ((static_cast<int64_t>(layer) * e.S + s) * e.CP + cp) * e.Hkv + g;
+    kbase = (pg * kPage + t) * hd;
+    vbase = pg * hd * kPage + t;
+    kptr = static_cast<T*>(e.k_carry);
+    vptr = static_cast<T*>(e.v_carry);
+  }
+  if (kind == 0) {
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      float c, s;
+      rope_cos_sin(pos, inv_freq[i0 + p], &c, &s);
+      kptr[kbase + i0 + p] = to_elem<T>(lo[p] * c - hi[p] * s);
+      kptr[kbase + i0 + p + half] = to_elem<T>(hi[p] * c + lo[p] * s);
+    }
+  } else {
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      vptr[vbase + static_cast<int64_t>(i0 + p) * kPage] = to_elem<T>(lo[p]);
+      vptr[vbase + static_cast<int64_t>(i0 + p + half) * kPage] = to_elem<T>(hi[p]);
+    }
+  }
+}
+
+}  // namespace co

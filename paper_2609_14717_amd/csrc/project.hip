@@ -2,7 +2,7 @@
 // Algorithm 1 Carryover steps 1-6; "Cache semantics": keys rotated once at
 // the row's absolute position).
 //
-//   F GEMM:   Z[M][d]   = (H + [carry row] E) . W_F^T        (E added before F)
+//   F GEMM:   Z[M][d]   = H . W_F^T + [carry row] (E . W_F^T)  (F(H + E) by linearity)
 //   K/V GEMM: J[M][NKV] = Z . W_KV^T, NKV = 2 * L * Hkv * hd (all layers at once)
 //   epilogue: rotate the K half of every head at row_pos, round, and scatter
 //             each row to its committed page slot or carry row (or drop it).
@@ -14,11 +14,12 @@
 // issues the same number of loads per stage and waits with an exact vmcnt.
 // Rows are stored with their 16-byte chunks XOR-swizzled by (row mod 16) so
 // that the 16 lanes reading one MFMA fragment hit distinct LDS banks.
-// E_carry is staged with the operands and added to the A fragments of carry
-// rows as they are read.  Skinny shapes (few rows, long K) split K across
-// workgroups deterministically through an fp32 workspace.
+// E_carry is staged with the operands; one extra MFMA tile whose rows all
+// hold E accumulates F(E), added to carried rows in the epilogue.  Skinny
+// shapes (few rows, long K) split K across workgroups deterministically
+// through an fp32 workspace.
 // fp32: a plain LDS-tiled VALU GEMM feeding the same epilogues.
-#include "co_kernels.h"
+#include "co_store.h"
 
 namespace co {
 
@@ -38,66 +39,6 @@ struct GemmArgs {
   int mode;
   KvDest kv;
 };
-
-__device__ __forceinline__ bool is_carry_row(int32_t dst) { return dst < 0 && dst != kSkip; }
-
-// ------------------------------------------------------------- K/V stores
-
-// Store pairs (i0+p, i0+p+hd/2), p < NP, of head segment `seg` = (layer, K|V, head)
-// of window row `row`.  lo/hi hold the unrotated fp32 values of those dims;
-// inv_freq[i] = theta^(-2i/hd).
-template <typename T, int NP>
-__device__ void kv_store(const KvDest& e, int row, int32_t dst, int pos, int seg, int i0,
-                         const float* lo, const float* hi, const double* inv_freq) {
-  if (dst == kSkip) return;
-  const int hd = e.hd, half = hd / 2;
-  const int g = seg % e.Hkv;
-  const int kind = (seg / e.Hkv) & 1;
-  const int layer = seg / (2 * e.Hkv);
-  int64_t kbase, vbase;   // element offsets of dim 0 of this row in the K and V layouts
-  T* kptr;
-  T* vptr;
-  if (dst >= 0) {
-    const int page = dst / kPage, t = dst % kPage;
-    if (page >= e.num_pages) {
-      set_status(e.status, CO_ERR_PAGE_RANGE);
-      return;
-    }
-    const int64_t pg = (static_cast<int64_t>(layer) * e.num_pages + page) * e.Hkv + g;
-    kbase = (pg * kPage + t) * hd;
-    vbase = pg * hd * kPage + t;
-    kptr = static_cast<T*>(e.k_cache);
-    vptr = static_cast<T*>(e.v_cache);
-  } else {
-    const int r = -1 - dst;
-    if (r >= e.CP * kPage) {
-      set_status(e.status, CO_ERR_LENGTH);
-      return;
-    }
-    const int s = row / e.B;
-    const int cp = r / kPage, t = r % kPage;
-    const int64_t pg = ((static_cast<int64_t>(layer) * e.S + s) * e.CP + cp) * e.Hkv + g;
-    kbase = (pg * kPage + t) * hd;
-    vbase = pg * hd * kPage + t;
-    kptr = static_cast<T*>(e.k_carry);
-    vptr = static_cast<T*>(e.v_carry);
-  }
-  if (kind == 0) {
-#pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      float c, s;
-      rope_cos_sin(pos, inv_freq[i0 + p], &c, &s);
-      kptr[kbase + i0 + p] = to_elem<T>(lo[p] * c - hi[p] * s);
-      kptr[kbase + i0 + p + half] = to_elem<T>(hi[p] * c + lo[p] * s);
-    }
-  } else {
-#pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      vptr[vbase + static_cast<int64_t>(i0 + p) * kPage] = to_elem<T>(lo[p]);
-      vptr[vbase + static_cast<int64_t>(i0 + p + half) * kPage] = to_elem<T>(hi[p]);
-    }
-  }
-}
 
 // Workgroup barrier for the staged ring.  Each wavefront has already waited
 // (vmcnt) for its own direct-to-LDS loads of the stage it is about to read, and

@@ -17,6 +17,9 @@ from helpers import TOL, OracleRun, assert_heads_close, compare_round, to_np  # 
 
 EDGE = wl.RAGGED32.replace(name="edge", S=4, L=2, ctx_lo=40, ctx_hi=900, rounds=8,
                            accept=("geom", 0.25), seed=0x5EED10)
+# one drafter layer (K/V width 256): the shape of the batch-32 serving workload
+EDGE1 = EDGE.replace(name="edge_l1", L=1, seed=0x5EED11)
+BOTH = pytest.mark.parametrize("w", [EDGE, EDGE1], ids=lambda w: w.name)
 
 
 def _gpu():
@@ -36,11 +39,11 @@ def _round(co, sc, r, m=None, flags=0):
     return out, lse, q
 
 
-def test_full_and_zero_acceptance():
+@BOTH
+def test_full_and_zero_acceptance(w):
     """m = B everywhere (carry segment empty), m = 0 everywhere (nothing
     committed, a full block carried), then a mix of both extremes."""
     Scenario, co = _gpu()
-    w = EDGE
     B = w.B
     sc, orc = Scenario(w), OracleRun(w)
     for r, m in enumerate([[B] * 4, [0] * 4, [0, B, 1, B - 1], [B, 0, B, 0]]):
@@ -50,11 +53,11 @@ def test_full_and_zero_acceptance():
         compare_round(sc, orc, rr, O, LSE, out, lse, sc.rt, orc.seqs, f"edge m={m}")
 
 
-def test_zero_carry_equals_baseline_bitexact():
+@BOTH
+def test_zero_carry_equals_baseline_bitexact(w):
     """With every proposal accepted, the carryover update equals the baseline
     update (Algorithm 1's two columns coincide): identical bits on the GPU."""
     Scenario, co = _gpu()
-    w = EDGE
     a, b = Scenario(w), Scenario(w)
     for r in range(3):
         m = [w.B] * w.S
@@ -81,12 +84,12 @@ def _poison(sc):
     st["v_cache"].masked_fill_(dead[None, :, None, None, :], float("nan"))
 
 
-def test_stale_rows_are_never_read():
+@BOTH
+def test_stale_rows_are_never_read(w):
     """Replace, never grow: the previous carry segment and every slot past a
     sequence's committed length may hold anything (NaN here); the next round's
     results are finite and identical to the unpoisoned run's."""
     Scenario, co = _gpu()
-    w = EDGE
     a, b = Scenario(w), Scenario(w)
     orc = OracleRun(w)
     for r in range(4):
@@ -135,12 +138,12 @@ def oracle_attend(orc, q):
     return oracle.attend_state(orc.st, Q, orc.w.Hq, orc.w.theta)
 
 
-def test_capacity_error_leaves_sequence_unchanged():
+@BOTH
+def test_capacity_error_leaves_sequence_unchanged(w):
     """A window that would pass the sequence's capacity is refused
     (CO_ERR_CAPACITY): that sequence keeps its lengths and stores nothing,
     the others proceed."""
     Scenario, co = _gpu()
-    w = EDGE
     bad = 2
     sc = Scenario(w)
     orc = OracleRun(w, seqs=[0, 1, 3])
@@ -158,11 +161,11 @@ def test_capacity_error_leaves_sequence_unchanged():
     assert int(sc.st["ctx_len"][bad]) == cap - w.B + 1 and int(sc.st["carry_len"][bad]) == 0
 
 
-def test_page_range_error_leaves_sequence_unchanged():
+@BOTH
+def test_page_range_error_leaves_sequence_unchanged(w):
     """A committed row whose page id is outside the pool is refused
     (CO_ERR_PAGE_RANGE): that sequence keeps its lengths, the others proceed."""
     Scenario, co = _gpu()
-    w = EDGE
     bad = 3
     sc = Scenario(w)
     orc = OracleRun(w, seqs=[0, 1, 2])
@@ -225,11 +228,11 @@ def test_layer_subset():
         assert np.abs(lse1[0, s].cpu().numpy() - LSE[1, s]).max() <= TOL[w.dtype]
 
 
-def test_round_equals_its_three_calls_bitexact():
+@BOTH
+def test_round_equals_its_three_calls_bitexact(w):
     """carryover_round == carryover_route + carryover_project_kv +
     drafter_block_attention on the same stream, bit for bit."""
     Scenario, co = _gpu()
-    w = EDGE
     a, b = Scenario(w), Scenario(w)
     for r in range(3):
         oa, la, _ = _round(co, a, r)
