@@ -36,6 +36,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense bf16 MFMA; fp32 vector (cfg1 path)
 PROFILES = os.path.join(ROOT, "profiles")
 # sources of the attention kernels: traffic counters taken on another version
 # of these are not reported
@@ -204,6 +205,46 @@ def attention_bytes(w, ctx, carry):
     return kv + 2 * q + w.L * w.S * w.B * w.Hq * 4
 
 
+def projection_work(w, M):
+    """Algorithmic flops and HBM bytes of one carryover_project_kv call over M
+    window rows: both products (F over Dcat, then K/V of every layer over d),
+    weights and rows read once, K/V rows written once."""
+    es = 2 if w.dtype == "bf16" else 4
+    flops = 2.0 * M * (w.Dcat * w.d + w.d * w.n_kv)
+    nbytes = (w.d * w.Dcat + w.n_kv * w.d + M * w.Dcat + M * w.n_kv) * es
+    return flops, float(nbytes)
+
+
+def attention_flops(w, keys_total):
+    """q.k and p.v products of every query row against every key of its KV head."""
+    return 2.0 * 2.0 * keys_total * w.L * w.B * w.Hq * w.hd
+
+
+def timed_calls(torch, stream, n, call):
+    """Average duration (s) of ``call`` over n calls, each bracketed by HIP events
+    recorded on ``stream``."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(n)]
+    for _ in range(3):
+        call()
+    for a, b in ev:
+        a.record(stream)
+        call()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return float(np.mean([a.elapsed_time(b) for a, b in ev])) / 1e3
+
+
+def projection_result(w, flops, nbytes, sec):
+    peak = MFMA_PEAK_TFLOPS[w.dtype]
+    tflops = flops / sec / 1e12
+    gbs = nbytes / sec / 1e9
+    return {"call": "carryover_project_kv", "rows": w.S * w.B, "flops_per_call": flops,
+            "bytes_per_call": nbytes, "avg_call_us": sec * 1e6, "tflops": tflops,
+            "mfma_peak_tflops": peak, "mfma_frac": tflops / peak, "gbs": gbs,
+            "hbm_frac": gbs / HBM_PEAK_GBS}
+
+
 def cpu_baseline(w, budget_s):
     """The fp64 oracle on this host: full rounds of the same workload."""
     import oracle  # noqa: F401  (test infrastructure: CPU baseline leg only)
@@ -242,6 +283,8 @@ def main():
     from synth.scenario import Scenario
 
     w = wl.WORKLOADS[args.workload]
+    if w.anchors:
+        return run_train(args, w)
     total = args.warmup + args.steps
     w = w.replace(rounds=max(w.rounds, total))
     torch.cuda.set_device(0)
@@ -321,6 +364,19 @@ def main():
     att_ms = [a.elapsed_time(b) for a, b in ev]
     att_s = float(np.sum(att_ms)) / 1e3
     achieved = per_launch * args.steps / att_s / 1e9
+
+    # The projection entry point, timed the same way: the last round's rows
+    # projected again into the slots they already occupy (same values).
+    h_last = inputs[total - 1][0]
+
+    def project():
+        rc = lib.carryover_project_kv(dims_p, W_p, h_last.data_ptr(), rt_p, st_p, ws_ptr,
+                                      sc.ws_project, sptr)
+        if rc:
+            raise RuntimeError(f"carryover_project_kv failed ({rc})")
+
+    proj_s = timed_calls(torch, stream, min(args.steps, 100), project)
+    pflops, pbytes = projection_work(w, w.S * w.B)
     if args.calibrate_copy_mb > 0:
         from synth import device as sdev
         nb = args.calibrate_copy_mb << 20
@@ -331,8 +387,10 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    metric = ("drafter rounds/s (block-16) at batch 32" if w.name == "ragged_batch32"
+              else f"drafter rounds/s ({w.name})")
     result = {
-        "metric": "drafter rounds/s (block-16) at batch 32",
+        "metric": metric,
         "value": args.steps / dt,
         "unit": "rounds/s",
         "n_gpus": 1,
@@ -354,10 +412,79 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": recorded_traffic(w.name),
                      "algorithmic_bytes_per_launch": per_launch,
-                     "avg_launch_us": att_s / args.steps * 1e6},
+                     "avg_launch_us": att_s / args.steps * 1e6,
+                     "tflops": attention_flops(w, float(np.sum(ctx_f + car_f))) /
+                     (att_s / args.steps) / 1e12},
+        "projection": projection_result(w, pflops, pbytes, proj_s),
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w.replace(rounds=w.rounds), args.cpu_baseline_seconds)
+    print(json.dumps(result), flush=True)
+
+
+def run_train(args, w):
+    """The training-shaped forward (second drafter pass of Algorithm 2): every
+    anchored block's rejected rows projected into its carry segment, then block
+    attention of all blocks; one step = one forward over all blocks."""
+    import torch
+    import paper_2609_14717_amd as co
+    from synth.scenario import TrainScenario
+    torch.cuda.set_device(0)
+    sc = TrainScenario(w)
+    stream = torch.cuda.current_stream()
+    ctx0 = sc.vst["ctx_len"].clone()
+
+    def step():
+        sc.vst["ctx_len"].copy_(ctx0)            # every forward starts from the windows at a + 1
+        sc.forward()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    if co.carryover_read_status(sc.vst) or co.carryover_read_status(sc.st):
+        raise RuntimeError("device status")
+    V = w.S * w.anchors
+    vw = w.replace(S=V)
+    n = min(args.steps, 100)
+    att_s = timed_calls(torch, stream, n, lambda: co.drafter_block_attention(
+        sc.vdims, 0, w.L, sc.q, sc.vst, sc.out, sc.lse, 0, sc.ws))
+    wsp = co.workspace_bytes(sc.vdims, co.CO_WS_PROJECT)
+    proj_s = timed_calls(torch, stream, n, lambda: co.carryover_project_kv(
+        sc.vdims, sc.W, sc.hidden, sc.vrt, sc.vst, sc.ws, ws_bytes=wsp))
+    keys = float(np.sum(sc.vst["ctx_len"].cpu().numpy().astype(np.int64) +
+                        sc.vst["carry_len"].cpu().numpy().astype(np.int64)))
+    aflops = attention_flops(vw, keys)
+    pflops, pbytes = projection_work(vw, V * w.B)
+    atfl = aflops / att_s / 1e12
+    result = {
+        "metric": f"training-shaped forwards/s ({w.name})",
+        "value": args.steps / dt,
+        "unit": "forwards/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": dt * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "responses": w.S, "positions": w.seq_len,
+                   "anchored_blocks": V, "block": w.B, "feat_dim": w.Dcat, "model_dim": w.d,
+                   "layers": w.L, "q_heads": w.Hq, "kv_heads": w.Hkv, "head_dim": w.hd,
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "kernel": "drafter_block_attention (" +
+                     " + ".join(ATTN_KERNELS) + ")", "achieved": atfl,
+                     "peak": MFMA_PEAK_TFLOPS[w.dtype], "unit": "TFLOP/s",
+                     "frac": atfl / MFMA_PEAK_TFLOPS[w.dtype], "traffic": None,
+                     "algorithmic_flops_per_launch": aflops, "avg_launch_us": att_s * 1e6},
+        "projection": projection_result(vw, pflops, pbytes, proj_s),
+    }
     print(json.dumps(result), flush=True)
 
 
