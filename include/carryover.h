@@ -105,6 +105,8 @@ typedef struct co_weights {
   const void* w_f;            /* F:  [model_dim][feat_dim]                 */
   const void* w_kv;           /* K_l, V_l of all layers: [NKV][model_dim]  */
   const void* e_carry;        /* E_carry: [feat_dim]                       */
+  const float* f_e;           /* optional F e_carry, fp32 [model_dim], from carryover_fold_e;
+                                 NULL: computed within every bf16 projection           */
 } co_weights;
 
 typedef struct co_state {
@@ -156,6 +158,17 @@ co_status carryover_route(const co_dims* dims, const int32_t* draft_tok, const i
 co_status carryover_project_kv(const co_dims* dims, const co_weights* w, const void* hidden,
                                const co_route* route, const co_state* state, void* ws,
                                size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Fold the carry embedding through F once per set of weights (Eq. 2 with F
+ * linear, no bias): f_e[i] = sum_k w_f[i][k] * e_carry[k] for i < model_dim,
+ * accumulated in fp32 from the stored values.  A bf16 projection then adds
+ * f_e to F h of carry rows (F(h + E) = F h + F E) instead of recomputing F E
+ * from e_carry; fp32 projections add e_carry to h and ignore f_e.  f_e:
+ * caller-owned device memory, fp32 [model_dim], 16-byte aligned.
+ */
+co_status carryover_fold_e(const co_dims* dims, const co_weights* w, float* f_e,
+                           hipStream_t stream);
 
 /*
  * Block attention over ctx_l = [C_l ; U_l] (Eq. 2; Algorithm 1 step 7;

@@ -41,7 +41,8 @@ class co_dims(ctypes.Structure):
 
 
 class co_weights(ctypes.Structure):
-    _fields_ = [("w_f", ctypes.c_void_p), ("w_kv", ctypes.c_void_p), ("e_carry", ctypes.c_void_p)]
+    _fields_ = [("w_f", ctypes.c_void_p), ("w_kv", ctypes.c_void_p), ("e_carry", ctypes.c_void_p),
+                ("f_e", ctypes.c_void_p)]
 
 
 class co_state(ctypes.Structure):
@@ -78,6 +79,7 @@ def lib():
                                         _v],
             "carryover_round": [_P(co_dims), _P(co_weights), _v, _v, _v, _v, _P(co_state),
                                 _P(co_route), _v, _v, ctypes.c_uint32, _v, ctypes.c_size_t, _v],
+            "carryover_fold_e": [_P(co_dims), _P(co_weights), _v, _v],
             "carryover_import_kv": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _v,
                                     _v, _P(co_state), _v],
             "carryover_workspace_bytes": [_P(co_dims), ctypes.c_int32],
@@ -95,7 +97,7 @@ def lib():
 
 
 EXPORTED = ("carryover_route", "carryover_project_kv", "drafter_block_attention",
-            "carryover_round", "carryover_import_kv", "carryover_workspace_bytes",
+            "carryover_round", "carryover_fold_e", "carryover_import_kv", "carryover_workspace_bytes",
             "carryover_read_status", "carryover_status_string")
 
 
@@ -131,8 +133,9 @@ def make_dims(S, B, Dcat, d, L, Hq, Hkv, hd, max_pages_per_seq, num_pages, dtype
                    float(theta))
 
 
-def weights(w_f, w_kv, e_carry):
-    return co_weights(_ptr(w_f), _ptr(w_kv), _ptr(e_carry))
+def weights(w_f, w_kv, e_carry, f_e=None):
+    """co_weights over device tensors; f_e (fp32 [model_dim], optional) from ``carryover_fold_e``."""
+    return co_weights(_ptr(w_f), _ptr(w_kv), _ptr(e_carry), _ptr(f_e))
 
 
 def state(t):
@@ -211,6 +214,12 @@ def carryover_round(dims, w, hidden, draft_tok, target_tok, q, st, rt, out, lse,
                                  _ptr(draft_tok), _ptr(target_tok), _ptr(q), ctypes.byref(s),
                                  ctypes.byref(r), _ptr(out), _ptr(lse), flags, _ptr(ws), nb,
                                  _stream(stream)), "carryover_round")
+
+
+def carryover_fold_e(dims, w, f_e, stream=None):
+    """f_e[:] = F e_carry (fp32 [model_dim]), once per set of weights."""
+    _check(lib().carryover_fold_e(ctypes.byref(dims), ctypes.byref(w), _ptr(f_e), _stream(stream)),
+           "carryover_fold_e")
 
 
 def carryover_import_kv(dims, seq, pos0, k_rows, v_rows, st, stream=None):

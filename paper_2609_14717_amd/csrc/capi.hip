@@ -186,7 +186,7 @@ co_status carryover_project_kv(const co_dims* dims, const co_weights* w, const v
   if (!w || !w->w_f || !w->w_kv || !w->e_carry || !hidden || !route_ok(route) || !state_ok(state))
     return CO_ERR_INVALID_ARG;
   if (!aligned(hidden, 16) || !aligned(w->w_f, 16) || !aligned(w->w_kv, 16) ||
-      !aligned(w->e_carry, 16))
+      !aligned(w->e_carry, 16) || !aligned(w->f_e, 16))
     return CO_ERR_INVALID_ARG;
   const ProjectPlan p = project_plan(dims);
   if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
@@ -200,9 +200,21 @@ co_status carryover_project_kv(const co_dims* dims, const co_weights* w, const v
   a.wf = w->w_f;
   a.wkv = w->w_kv;
   a.e = w->e_carry;
+  a.fe = dims->dtype == CO_DTYPE_BF16 ? w->f_e : nullptr;
   a.dst = make_dest(dims, route, state);
   a.ws = ws;
   return hip_status(launch_project(a, p, stream));
+}
+
+co_status carryover_fold_e(const co_dims* dims, const co_weights* w, float* f_e,
+                           hipStream_t stream) {
+  co_status s = check_dims(dims);
+  if (s != CO_OK) return s;
+  if (!w || !w->w_f || !w->e_carry || !f_e || !aligned(w->w_f, 16) || !aligned(w->e_carry, 16) ||
+      !aligned(f_e, 16))
+    return CO_ERR_INVALID_ARG;
+  return hip_status(launch_fold_e(w->w_f, w->e_carry, dims->model_dim, dims->feat_dim,
+                                  dims->dtype, f_e, stream));
 }
 
 co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int32_t layer_count,

@@ -40,6 +40,26 @@ __device__ __forceinline__ void lds_dma16(const void* src, void* lds_dst) {
   __builtin_amdgcn_global_load_lds(src, lds_dst, 16, 0, 0);
 }
 
+// The same load issued as inline asm.  The compiler does not see it as a write
+// to LDS, so it neither waits for it before LDS reads nor counts it in its own
+// vmcnt waits (which therefore only ever wait longer than they need to); the
+// caller orders it with the reads of its LDS slot through explicit vmcnt waits
+// and barriers.  lds_dst must be wavefront-uniform.
+__device__ __forceinline__ void lds_dma16_opaque(const void* src, uint32_t lds_dst) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(lds_dst)
+               : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(N) lgkmcnt(0), then a workgroup barrier, as one statement that
+// no memory access is moved across.
+template <int N>
+__device__ __forceinline__ void wait_vm_lgkm_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" : : "n"(N) : "memory");
+}
+
 // Two fp32 values -> packed bf16 pair (round to nearest even, v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const __bf16 a = static_cast<__bf16>(lo), b = static_cast<__bf16>(hi);
@@ -59,6 +79,15 @@ __device__ __forceinline__ float max_across_rows(float v) {
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u16x8 v) { return __builtin_bit_cast(bf16x8, v); }
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// v_mfma_f32_32x32x16_bf16: acc[32x32] += A[32x16] * B[16x32].
+// Lane l holds A row (l % 32), k = 8*(l/32) .. +7; B column (l % 32), same k;
+// acc register r: column (l % 32), row 8*(r/4) + 4*(l/32) + (r % 4).
+__device__ __forceinline__ f32x16 mfma32x32x16(u16x8 a, u16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+}
 
 // v_mfma_f32_16x16x32_bf16: acc[16x16] += A[16x32] * B[32x16].
 // Lane l holds A row (l % 16), k = 8*(l/16) .. +7; B column (l % 16), same k;

@@ -44,6 +44,7 @@ struct ProjectArgs {
   const void* wf;
   const void* wkv;
   const void* e;
+  const float* fe;   // precomputed F(E) [d] (bf16 path), or null
   KvDest dst;
   void* ws;
 };
@@ -93,6 +94,8 @@ hipError_t launch_route(const RouteArgs& a, hipStream_t stream);
 hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_t stream);
 hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_count,
                             hipStream_t stream);
+hipError_t launch_fold_e(const void* wf, const void* e, int d, int Dcat, int dtype, float* out,
+                         hipStream_t stream);
 hipError_t launch_import(const KvDest& d, int dtype, int seq, int pos0, int n, const void* k_rows,
                          const void* v_rows, const int32_t* page_table, int max_pages,
                          hipStream_t stream);

@@ -19,6 +19,8 @@
 // shapes (few rows, long K) split K across workgroups deterministically
 // through an fp32 workspace.
 // fp32: a plain LDS-tiled VALU GEMM feeding the same epilogues.
+#include <stdlib.h>
+
 #include "co_store.h"
 
 namespace co {
@@ -35,6 +37,7 @@ struct GemmArgs {
   const int32_t* row_dst;  // carry rows: -1-r
   float* partial;          // [splits][M][N]
   float* partial_e;        // [splits][N]: F(E) per K-split (split-K with E only)
+  const float* fe;         // precomputed F(E) [N], added to carry rows (e must be null)
   void* z_out;             // [M][N]
   int mode;
   KvDest kv;
@@ -85,7 +88,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
 
   // row descriptors of the tile's rows (thread t: row t % BM), consumed only by
   // the epilogue; kept opaque until then so no wait lands before the main loop
-  const bool need_rows = HAS_E || g.mode == kModeKV;
+  const bool carry_add = HAS_E || g.fe != nullptr;
+  const bool need_rows = carry_add || g.mode == kModeKV;
   int rd_dst = 0, rd_pos = 0;
   if (need_rows) {
     const int r = min(m0 + (tid % BM), g.M - 1);
@@ -249,7 +253,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
         sc[((wm * TM + a) * 16 + (lane >> 4) * 4 + r) * LDC + (wn * TN + b) * 16 + (lane & 15)] =
             acc[a][b][r];
   if (g.mode == kModeKV && tid < g.kv.hd / 2) inv_tab[tid] = g.kv.rope_inv[tid];
-  __shared__ float fe_lds[HAS_E ? BN : 1];
+  __shared__ float fe_lds[BN];
   __shared__ int dst_lds[BM], pos_lds[BM];
   asm volatile("" : "+v"(rd_dst), "+v"(rd_pos));
   if (need_rows && tid < BM) {
@@ -261,6 +265,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
 #pragma unroll
       for (int b = 0; b < TN; ++b) fe_lds[(wn * TN + b) * 16 + lane] = acc_e[b][0];
     }
+  } else {
+    if (g.fe != nullptr && g.mode == kModeZ)
+      for (int c = tid; c < BN; c += 256) fe_lds[c] = n0 + c < g.N ? g.fe[n0 + c] : 0.f;
   }
   __syncthreads();
 
@@ -271,7 +278,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
       const int gr = m0 + row, gc = n0 + cc * 8;
       if (gr >= g.M || gc >= g.N) continue;
       u16x8 v;
-      if constexpr (HAS_E) {
+      if (carry_add) {
         const bool cy = is_carry_row(dst_lds[row]);
 #pragma unroll
         for (int t = 0; t < 8; ++t)
@@ -297,6 +304,298 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
       }
       kv_store<uint16_t, 4>(g.kv, gr, dst_lds[row], pos_lds[row], gc0 / hd, i0, lo, hi, inv_tab);
     }
+  }
+}
+
+// ------------------------------------------------- bf16 MFMA GEMM, large tiles
+//
+// For row counts in the hundreds and up.  Four wavefronts (2 x 2) each own a
+// (TMW*32) x (TNW*32) block of v_mfma_f32_32x32x16_bf16 tiles, so a workgroup
+// tile is (64*TMW) x (64*TNW) and every fragment read from LDS feeds TMW or
+// TNW MFMAs.  K advances in BK-wide stages through an NS-deep LDS ring filled
+// by direct-to-LDS loads issued as opaque inline asm: the compiler then
+// schedules the LDS fragment reads freely around the MFMAs, while each
+// wavefront waits for its own loads with an exact vmcnt and a barrier
+// publishes a stage to the others.  A staged row holds BK bf16 (2*BK bytes);
+// its 16-byte chunks are XOR-permuted so that the 16 lanes of one read phase
+// (16 consecutive rows, one logical chunk) hit 16 distinct bank groups.
+// Fragments are software-pipelined: k16 step h+1 is read while step h
+// multiplies, and the next stage is published (and its slot refilled) during
+// the stage's last step.  F(E) is accumulated on the VALU from the B fragments
+// in registers (a lane holds 8 k values of one column), alternate k16 steps
+// on the two wavefront rows; when F(E) is supplied precomputed (g.fe) the
+// main loop carries no E at all.  Workgroup ids are renumbered so that each
+// XCD (ids congruent mod 8) works on consecutive tiles, which share the same
+// A panel and K range.
+template <int TMW, int TNW, int BK, int NS, bool HAS_E>
+__global__ __launch_bounds__(256, 1) void gemm_wide_kernel(GemmArgs g, int tiles_m, int tiles_n) {
+  constexpr int ROWB = 2 * BK;                     // bytes per staged row
+  constexpr int CPR = BK / 8;                      // 16-byte chunks per row
+  constexpr int RPI = 64 / CPR;                    // rows per 1 KiB load
+  constexpr int RPL = 256 / ROWB;                  // rows per 256-byte bank line
+  constexpr int H = BK / 16;                       // k16 steps per stage
+  constexpr int BM = 64 * TMW, BN = 64 * TNW;
+  constexpr int ROWS = BM + BN;
+  constexpr int LPW = ROWS / RPI / 4;              // 1 KiB loads per wavefront per stage
+  constexpr int NL = LPW + (HAS_E ? 1 : 0);
+  constexpr int E_OFF = ROWS * ROWB;
+  constexpr int STAGE = ROWS * ROWB + (HAS_E ? 4 * 1024 : 0);
+  constexpr int PASS = 64, LDC = BN + 4;           // epilogue: 64 fp32 rows at a time
+  static_assert((BK == 32 || BK == 64) && ROWS % (4 * RPI) == 0 && NS >= 2, "tile");
+  static_assert(NL * (NS - 1) < 64, "vmcnt");
+  static_assert(PASS * LDC * 4 <= NS * STAGE, "C staging must fit in the ring");
+  __shared__ __align__(16) unsigned char smem[NS * STAGE];
+  __shared__ double inv_tab[64];
+  __shared__ float fe_lds[2][BN];
+  __shared__ int dst_lds[BM], pos_lds[BM];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  // Tile order: K-split major; within a split, groups of up to 4 row tiles
+  // sweep the column tiles, so that consecutive indices form compact blocks
+  // of tiles (4 x 8 for 32 indices) that share A and B panels.  Workgroup ids
+  // are dealt to the 8 XCDs round-robin; renumbering them gives every XCD a
+  // run of consecutive indices, whose shared panels then stay in its L2.
+  const int total = gridDim.x;
+  int t = blockIdx.x;
+  if ((total & 7) == 0) t = (t & 7) * (total >> 3) + (t >> 3);
+  const int per_split = tiles_m * tiles_n;
+  const int sp = t / per_split, r = t % per_split;
+  const int gm = min(4, tiles_m), grp = r / (gm * tiles_n);
+  const int gsz = min(gm, tiles_m - grp * gm), rg = r % (gm * tiles_n);
+  const int mt = grp * gm + rg % gsz, nt = rg / gsz;
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int kbeg = sp * g.k_per_split;
+  const int nk = min(g.K - kbeg, g.k_per_split) / BK;
+  const uint16_t* A = static_cast<const uint16_t*>(g.A);
+  const uint16_t* Bw = static_cast<const uint16_t*>(g.B);
+
+  const bool carry_add = HAS_E || g.fe != nullptr;
+  const bool need_rows = carry_add || g.mode == kModeKV;
+  int rd_dst = 0, rd_pos = 0;
+  if (need_rows) {
+    const int r = min(m0 + (tid % BM), g.M - 1);
+    rd_dst = g.row_dst[r];
+    if (g.mode == kModeKV) rd_pos = g.kv.row_pos[r];
+  }
+
+  // this lane's source rows: load j of the wavefront fills rows RPI*(wave*LPW+j) ..
+  const uint16_t* src[LPW];
+#pragma unroll
+  for (int j = 0; j < LPW; ++j) {
+    const int row = (wave * LPW + j) * RPI + lane / CPR;
+    const int chunk = (lane % CPR) ^ ((row / RPL) % CPR);
+    const uint16_t* base = row < BM ? A + static_cast<int64_t>(min(m0 + row, g.M - 1)) * g.K
+                                    : Bw + static_cast<int64_t>(min(n0 + row - BM, g.N - 1)) * g.K;
+    src[j] = base + kbeg + chunk * 8;
+  }
+  // E: every wavefront keeps its own copy of the stage's BK values (chunk c at c*16)
+  const uint16_t* src_e =
+      HAS_E ? static_cast<const uint16_t*>(g.e) + kbeg + (lane % CPR) * 8 : nullptr;
+  const uint32_t ring = lds_addr(smem);
+
+  auto issue = [&](int kt) {
+    const uint32_t st = ring + (kt % NS) * STAGE;
+#pragma unroll
+    for (int j = 0; j < LPW; ++j)
+      lds_dma16_opaque(src[j] + kt * BK, st + (wave * LPW + j) * 1024);
+    if constexpr (HAS_E) lds_dma16_opaque(src_e + kt * BK, st + E_OFF + wave * 1024);
+  };
+
+  f32x16 acc[TMW][TNW];
+#pragma unroll
+  for (int a = 0; a < TMW; ++a)
+#pragma unroll
+    for (int b = 0; b < TNW; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+  float fe[TNW];
+#pragma unroll
+  for (int b = 0; b < TNW; ++b) fe[b] = 0.f;
+
+  // fragment offsets within a stage: row (lane % 32) of each 32-row tile; the
+  // logical chunk of k16 step h is 2h + lane/32, stored permuted
+  const int frow = (lane & 31) * ROWB;
+  const int fswz = ((lane & 31) / RPL) % CPR;
+
+  struct Frags {
+    u16x8 a[TMW], b[TNW], e;
+  };
+  auto load = [&](int kt, int h, Frags& f) {
+    const unsigned char* st = smem + (kt % NS) * STAGE;
+    const int c = 2 * h + (lane >> 5);
+    const int off = frow + ((c ^ fswz) << 4);
+#pragma unroll
+    for (int a = 0; a < TMW; ++a)
+      f.a[a] = *reinterpret_cast<const u16x8*>(st + (wm * TMW + a) * 32 * ROWB + off);
+#pragma unroll
+    for (int b = 0; b < TNW; ++b)
+      f.b[b] = *reinterpret_cast<const u16x8*>(st + (BM + (wn * TNW + b) * 32) * ROWB + off);
+    if (HAS_E && (h & 1) == wm)
+      f.e = *reinterpret_cast<const u16x8*>(st + E_OFF + wave * 1024 + c * 16);
+  };
+  // Marks fragments as read: the compiler places its LDS wait for them here (the
+  // barrier that follows waits for all LDS reads anyway), so the MFMAs that
+  // consume them do not also wait for the next stage's reads issued meanwhile.
+  auto settle = [&](int h, Frags& f) {
+#pragma unroll
+    for (int a = 0; a < TMW; ++a) asm volatile("" : "+v"(f.a[a]));
+#pragma unroll
+    for (int b = 0; b < TNW; ++b) asm volatile("" : "+v"(f.b[b]));
+    if (HAS_E && (h & 1) == wm) asm volatile("" : "+v"(f.e));
+  };
+  auto compute = [&](int h, const Frags& f) {
+#pragma unroll
+    for (int a = 0; a < TMW; ++a)
+#pragma unroll
+      for (int b = 0; b < TNW; ++b) acc[a][b] = mfma32x32x16(f.a[a], f.b[b], acc[a][b]);
+    if (HAS_E && (h & 1) == wm) {
+#pragma unroll
+      for (int b = 0; b < TNW; ++b)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) fe[b] = fmaf(bf2f(f.b[b][i]), bf2f(f.e[i]), fe[b]);
+    }
+  };
+  // Wait until this wavefront's loads of the stage `ahead` stages before the
+  // newest one issued have landed, then publish through the barrier.
+  auto wait_stage = [&](int ahead) {
+    if (NS >= 4 && ahead >= 3) wait_vm_lgkm_barrier<(NS >= 4 ? 3 * NL : 0)>();
+    else if (NS >= 3 && ahead >= 2) wait_vm_lgkm_barrier<(NS >= 3 ? 2 * NL : 0)>();
+    else if (ahead >= 1) wait_vm_lgkm_barrier<NL>();
+    else wait_vm_lgkm_barrier<0>();
+  };
+
+  // Stage kt+1 is published by the barrier taken during the last k16 step of
+  // stage kt; by then every wavefront holds all of stage kt in registers, so
+  // its slot takes the loads of stage kt+NS.
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    if (s < nk) issue(s);
+  Frags f0, f1;
+  if (nk > 0) {
+    wait_stage(min(NS - 1, nk - 1));
+    load(0, 0, f0);
+  }
+  for (int kt = 0; kt < nk; ++kt) {
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+      Frags& cur = (h & 1) ? f1 : f0;
+      Frags& nxt = (h & 1) ? f0 : f1;
+      if (h + 1 < H) load(kt, h + 1, nxt);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(h, cur);
+      __builtin_amdgcn_sched_barrier(0);
+      if (h + 2 == H) {
+        settle(h + 1, nxt);
+        if (kt + 1 < nk) {
+          wait_stage(min(NS - 2, nk - 2 - kt));
+          if (kt + NS < nk) issue(kt + NS);
+          load(kt + 1, 0, cur);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
+  // the ring is reused below: every wavefront must be done with its last stage
+  wait_vm_lgkm_barrier<0>();
+
+  if constexpr (HAS_E) {
+    // the two k halves of each column sit in lanes l and l ^ 32
+#pragma unroll
+    for (int b = 0; b < TNW; ++b) fe[b] += __shfl_xor(fe[b], 32);
+    if (lane < 32) {
+#pragma unroll
+      for (int b = 0; b < TNW; ++b) fe_lds[wm][(wn * TNW + b) * 32 + lane] = fe[b];
+    }
+  } else {
+    if (g.fe != nullptr && g.mode == kModeZ)
+      for (int c = tid; c < BN; c += 256) fe_lds[0][c] = n0 + c < g.N ? g.fe[n0 + c] : 0.f;
+  }
+
+  if (g.mode == kModePartial) {
+    float* out = g.partial + static_cast<int64_t>(sp) * g.M * g.N;
+#pragma unroll
+    for (int a = 0; a < TMW; ++a)
+#pragma unroll
+      for (int b = 0; b < TNW; ++b) {
+        const int col = n0 + (wn * TNW + b) * 32 + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + (wm * TMW + a) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (row < g.M && col < g.N) out[static_cast<int64_t>(row) * g.N + col] = acc[a][b][r];
+        }
+      }
+    if constexpr (HAS_E) {
+      __syncthreads();
+      if (mt == 0)
+        for (int c = tid; c < BN; c += 256)
+          if (n0 + c < g.N)
+            g.partial_e[static_cast<int64_t>(sp) * g.N + n0 + c] = fe_lds[0][c] + fe_lds[1][c];
+    }
+    return;
+  }
+
+  if (g.mode == kModeKV && tid < g.kv.hd / 2) inv_tab[tid] = g.kv.rope_inv[tid];
+  asm volatile("" : "+v"(rd_dst), "+v"(rd_pos));
+  if (need_rows && tid < BM) {
+    dst_lds[tid] = rd_dst;
+    pos_lds[tid] = rd_pos;
+  }
+  float* sc = reinterpret_cast<float*>(smem);
+#pragma unroll
+  for (int p = 0; p < BM / PASS; ++p) {
+    // the wavefronts holding rows p*64 .. +63 stage them as fp32
+#pragma unroll
+    for (int a = 0; a < TMW; ++a) {
+      if ((wm * TMW + a) * 32 / PASS != p) continue;
+#pragma unroll
+      for (int b = 0; b < TNW; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = (wm * TMW + a) * 32 - p * PASS + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          sc[row * LDC + (wn * TNW + b) * 32 + (lane & 31)] = acc[a][b][r];
+        }
+    }
+    __syncthreads();
+    if (g.mode == kModeZ) {
+      uint16_t* z = static_cast<uint16_t*>(g.z_out);
+      for (int c = tid; c < PASS * BN / 8; c += 256) {
+        const int rl = c / (BN / 8), cc = c % (BN / 8);
+        const int row = p * PASS + rl;
+        const int gr = m0 + row, gc = n0 + cc * 8;
+        if (gr >= g.M || gc >= g.N) continue;
+        u16x8 v;
+        if (carry_add && is_carry_row(dst_lds[row])) {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const float f = HAS_E ? fe_lds[0][cc * 8 + q] + fe_lds[1][cc * 8 + q] : fe_lds[0][cc * 8 + q];
+            v[q] = f2bf(sc[rl * LDC + cc * 8 + q] + f);
+          }
+        } else {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) v[q] = f2bf(sc[rl * LDC + cc * 8 + q]);
+        }
+        *reinterpret_cast<u16x8*>(z + static_cast<int64_t>(gr) * g.N + gc) = v;
+      }
+    } else {
+      const int hd = g.kv.hd, q_per_seg = hd / 8;
+      for (int c = tid; c < PASS * BN / 8; c += 256) {
+        const int rl = c / (BN / 8), q = c % (BN / 8);
+        const int row = p * PASS + rl;
+        const int seg_local = q / q_per_seg, i0 = (q % q_per_seg) * 4;
+        const int gr = m0 + row, gc0 = n0 + seg_local * hd;
+        if (gr >= g.M || gc0 >= g.N) continue;
+        float lo[4], hi[4];
+#pragma unroll
+        for (int pp = 0; pp < 4; ++pp) {
+          lo[pp] = sc[rl * LDC + seg_local * hd + i0 + pp];
+          hi[pp] = sc[rl * LDC + seg_local * hd + hd / 2 + i0 + pp];
+        }
+        kv_store<uint16_t, 4>(g.kv, gr, dst_lds[row], pos_lds[row], gc0 / hd, i0, lo, hi, inv_tab);
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -353,15 +652,21 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
 
 template <typename T>
 __global__ __launch_bounds__(256) void epi_z_kernel(const float* part, int splits, int M, int N,
-                                                    T* z, const float* part_e,
+                                                    T* z, const float* part_e, const float* fe,
                                                     const int32_t* row_dst) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (i >= static_cast<int64_t>(M) * N) return;
   float v = 0.f;
   for (int s = 0; s < splits; ++s) v += part[static_cast<int64_t>(s) * M * N + i];
-  if (part_e && is_carry_row(row_dst[i / N])) {
+  if ((part_e || fe) && is_carry_row(row_dst[i / N])) {
     const int col = static_cast<int>(i % N);
-    for (int s = 0; s < splits; ++s) v += part_e[static_cast<int64_t>(s) * N + col];
+    if (fe) {
+      v += fe[col];
+    } else {
+      float e = 0.f;
+      for (int s = 0; s < splits; ++s) e += part_e[static_cast<int64_t>(s) * N + col];
+      v += e;
+    }
   }
   z[i] = to_elem<T>(v);
 }
@@ -409,7 +714,34 @@ hipError_t launch_gemm_bf16_t(const GemmArgs& g, int tile, int splits, hipStream
   return hipGetLastError();
 }
 
+// Large-tile variants: wavefront blocks TMW x TNW of 32 x 32 tiles, stage depth
+// BK, ring depth NS.
+//   0: 256 x 256, BK 32 x 4   1: 256 x 128, BK 32 x 4   2: 128 x 256, BK 32 x 4
+//   3: 256 x 256, BK 64 x 2   4: 256 x 128, BK 64 x 3   5: 128 x 256, BK 64 x 3
+constexpr int kWide = 4, kWideVariants = 6;
+constexpr int kWideBM[kWideVariants] = {256, 256, 128, 256, 256, 128};
+constexpr int kWideBN[kWideVariants] = {256, 128, 256, 256, 128, 256};
+
+template <bool HAS_E>
+hipError_t launch_gemm_wide_t(const GemmArgs& g, int variant, int splits, hipStream_t stream) {
+  const int tm = (g.M + kWideBM[variant] - 1) / kWideBM[variant];
+  const int tn = (g.N + kWideBN[variant] - 1) / kWideBN[variant];
+  const dim3 grid(tm * tn * splits);
+  switch (variant) {
+    case 0: hipLaunchKernelGGL((gemm_wide_kernel<4, 4, 32, 4, HAS_E>), grid, dim3(256), 0, stream, g, tm, tn); break;
+    case 1: hipLaunchKernelGGL((gemm_wide_kernel<4, 2, 32, 4, HAS_E>), grid, dim3(256), 0, stream, g, tm, tn); break;
+    case 2: hipLaunchKernelGGL((gemm_wide_kernel<2, 4, 32, 4, HAS_E>), grid, dim3(256), 0, stream, g, tm, tn); break;
+    case 3: hipLaunchKernelGGL((gemm_wide_kernel<4, 4, 64, 2, HAS_E>), grid, dim3(256), 0, stream, g, tm, tn); break;
+    case 4: hipLaunchKernelGGL((gemm_wide_kernel<4, 2, 64, 3, HAS_E>), grid, dim3(256), 0, stream, g, tm, tn); break;
+    default: hipLaunchKernelGGL((gemm_wide_kernel<2, 4, 64, 3, HAS_E>), grid, dim3(256), 0, stream, g, tm, tn); break;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm_bf16(const GemmArgs& g, int tile, int splits, hipStream_t stream) {
+  if (tile >= kWide)
+    return g.e ? launch_gemm_wide_t<true>(g, tile - kWide, splits, stream)
+               : launch_gemm_wide_t<false>(g, tile - kWide, splits, stream);
   return g.e ? launch_gemm_bf16_t<true>(g, tile, splits, stream)
              : launch_gemm_bf16_t<false>(g, tile, splits, stream);
 }
@@ -432,7 +764,55 @@ int pick_split(int M, int N, int K, int tile, int num_cus) {
 // still gives at least half of the CUs work; otherwise the most parallel one.
 // Tiles taller than the row count are skipped, and the 64-wide tile only holds
 // whole heads when they are 64 wide.
+// Large-tile choice for shapes with hundreds of rows or more: the variant and
+// K-split with the least estimated time, counting whole waves of workgroups at
+// a per-CU MFMA rate (the 256 x 256 tile reads LDS least per flop) plus the
+// fp32 partials that a split writes and reads back.  Returns false when no
+// choice fills at least half of the CUs.  CO_GEMM_WIDE_VARIANT=v restricts
+// the choice to variant v at any size from 256 rows (tests and tuning).
+// K elements per split: the stage depth of the tile variant divides it.
+int split_len(int K, int split, int tile) {
+  const int bk = tile >= kWide + 3 ? 64 : 32;
+  return ((K + split - 1) / split + bk - 1) / bk * bk;
+}
+
+bool pick_wide(int M, int N, int K, int num_cus, int* tile, int* split) {
+  if (M < 256 || K % 64 != 0) return false;
+  double best = 1e30;
+  int bv = -1, bs = 1;
+  const char* force = getenv("CO_GEMM_WIDE_VARIANT");
+  for (int v = 0; v < kWideVariants; ++v) {
+    if (force != nullptr && atoi(force) != v) continue;
+    const int64_t tiles = static_cast<int64_t>((M + kWideBM[v] - 1) / kWideBM[v]) *
+                          ((N + kWideBN[v] - 1) / kWideBN[v]);
+    // relative main-loop rates measured on MI355X (the 64-deep stages and the
+    // square tile move the fewest bytes per flop through LDS)
+    const double eff = v == 3 ? 1.0 : v > 3 ? 0.95 : v == 0 ? 0.9 : 0.8;
+    for (int s = 1; s <= 16; ++s) {
+      const int kps = split_len(K, s, kWide + v);
+      if (kps < 256 || (K + kps - 1) / kps != s) continue;
+      const int64_t wgs = tiles * s;
+      if (wgs < num_cus / 2 && force == nullptr) continue;
+      const int64_t waves = (wgs + num_cus - 1) / num_cus;
+      const double t_mfma = static_cast<double>(waves) * kWideBM[v] * kWideBN[v] * kps * 2.0 /
+                            (7.0e12 * eff);
+      // split partials: written, read back and reduced by a second kernel
+      const double t_part = s > 1 ? static_cast<double>(s) * M * N * 8.0 / 3.0e12 + 3e-6 : 0.0;
+      if (t_mfma + t_part < best) {
+        best = t_mfma + t_part;
+        bv = v;
+        bs = s;
+      }
+    }
+  }
+  if (bv < 0) return false;
+  *tile = kWide + bv;
+  *split = bs;
+  return true;
+}
+
 void pick_gemm(int M, int N, int K, bool kv, int hd, int num_cus, int* tile, int* split) {
+  if (getenv("CO_GEMM_NO_WIDE") == nullptr && pick_wide(M, N, K, num_cus, tile, split)) return;
   const int narrow = (!kv || hd == 64) ? 0 : 1;
   int cand[3], nc = 0;
   if (M > 64) cand[nc++] = 3;
@@ -491,7 +871,7 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
 
   GemmArgs f{};
   f.M = a.M; f.N = a.d; f.K = a.Dcat;
-  f.A = a.hidden; f.B = a.wf; f.e = a.e; f.row_dst = a.dst.row_dst;
+  f.A = a.hidden; f.B = a.wf; f.e = a.e; f.fe = nullptr; f.row_dst = a.dst.row_dst;
   f.partial = part; f.z_out = z; f.kv = a.dst;
   f.partial_e = reinterpret_cast<float*>(ws + p.z_bytes + p.part_bytes);
   GemmArgs kv{};
@@ -508,7 +888,8 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
     const int64_t nz = static_cast<int64_t>(a.M) * a.d;
     hipLaunchKernelGGL(epi_z_kernel<float>, dim3(static_cast<unsigned>((nz + 255) / 256)),
                        dim3(256), 0, stream, part, 1, a.M, a.d, static_cast<float*>(z),
-                       static_cast<const float*>(nullptr), a.dst.row_dst);
+                       static_cast<const float*>(nullptr), static_cast<const float*>(nullptr),
+                       a.dst.row_dst);
     hipLaunchKernelGGL(gemm_f32_kernel, dim3((kv.N + 63) / 64, (kv.M + 31) / 32), dim3(256), 0,
                        stream, kv);
     const int64_t items = static_cast<int64_t>(a.M) * (n_kv / 2);
@@ -517,16 +898,20 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
     return hipGetLastError();
   }
 
-  f.k_per_split = a.Dcat / p.f_split;
+  if (a.fe != nullptr) {   // F(E) folded beforehand: the GEMM carries no E
+    f.e = nullptr;
+    f.fe = a.fe;
+  }
+  f.k_per_split = split_len(a.Dcat, p.f_split, p.f_tile);
   f.mode = p.f_split > 1 ? kModePartial : kModeZ;
   if ((err = launch_gemm_bf16(f, p.f_tile, p.f_split, stream)) != hipSuccess) return err;
   if (p.f_split > 1) {
     const int64_t nz = static_cast<int64_t>(a.M) * a.d;
     hipLaunchKernelGGL(epi_z_kernel<uint16_t>, dim3(static_cast<unsigned>((nz + 255) / 256)),
                        dim3(256), 0, stream, part, p.f_split, a.M, a.d, static_cast<uint16_t*>(z),
-                       static_cast<const float*>(a.e ? f.partial_e : nullptr), a.dst.row_dst);
+                       static_cast<const float*>(f.e ? f.partial_e : nullptr), f.fe, a.dst.row_dst);
   }
-  kv.k_per_split = a.d / p.kv_split;
+  kv.k_per_split = split_len(a.d, p.kv_split, p.kv_tile);
   kv.mode = p.kv_split > 1 ? kModePartial : kModeKV;
   if ((err = launch_gemm_bf16(kv, p.kv_tile, p.kv_split, stream)) != hipSuccess) return err;
   if (p.kv_split > 1) {
@@ -534,6 +919,44 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
     hipLaunchKernelGGL(epi_kv_kernel<uint16_t>, dim3(static_cast<unsigned>((items + 255) / 256)),
                        dim3(256), 0, stream, part, p.kv_split, a.M, n_kv, a.dst);
   }
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------- F(E) fold
+
+// One wavefront per output: f_e[row] = sum_k wf[row][k] * e[k] in fp32, lanes
+// striding over k in 8-element chunks, then a butterfly sum.
+template <typename T>
+__global__ __launch_bounds__(256) void fold_e_kernel(const T* wf, const T* e, int d, int Dcat,
+                                                     float* out) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= d) return;
+  const T* w = wf + static_cast<int64_t>(row) * Dcat;
+  float acc = 0.f;
+  for (int k = lane * 8; k < Dcat; k += 512) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if constexpr (sizeof(T) == 2)
+        acc = fmaf(bf2f(w[k + i]), bf2f(e[k + i]), acc);
+      else
+        acc = fmaf(w[k + i], e[k + i], acc);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+  if (lane == 0) out[row] = acc;
+}
+
+hipError_t launch_fold_e(const void* wf, const void* e, int d, int Dcat, int dtype, float* out,
+                         hipStream_t stream) {
+  const dim3 grid((d + 3) / 4);
+  if (dtype == CO_DTYPE_BF16)
+    hipLaunchKernelGGL(fold_e_kernel<uint16_t>, grid, dim3(256), 0, stream,
+                       static_cast<const uint16_t*>(wf), static_cast<const uint16_t*>(e), d, Dcat,
+                       out);
+  else
+    hipLaunchKernelGGL(fold_e_kernel<float>, grid, dim3(256), 0, stream,
+                       static_cast<const float*>(wf), static_cast<const float*>(e), d, Dcat, out);
   return hipGetLastError();
 }
 

@@ -12,8 +12,20 @@ from . import workloads as wl
 from . import device as sdev
 
 
+def make_weights(co, dims, wf, wkv, e, fold_e):
+    """co_weights of the drafter; with fold_e (bf16) F(E) is folded once, as a
+    serving setup would when it loads the weights."""
+    import torch
+    f_e = None
+    if fold_e and dims.dtype == co.CO_DTYPE_BF16:
+        f_e = torch.empty(dims.model_dim, dtype=torch.float32, device=wf.device)
+        co.carryover_fold_e(dims, co.weights(wf, wkv, e), f_e)
+    return co.weights(wf, wkv, e, f_e), f_e
+
+
 class Scenario:
-    def __init__(self, w: wl.Workload, device: str = "cuda", build_context: bool = True):
+    def __init__(self, w: wl.Workload, device: str = "cuda", build_context: bool = True,
+                 fold_e: bool = True):
         import torch
         import paper_2609_14717_amd as co
         self.w, self.device = w, device
@@ -25,7 +37,7 @@ class Scenario:
         self.wf = sdev.materialise(w, wl.spec_wf(w), device)
         self.wkv = sdev.materialise(w, wl.spec_wkv(w), device)
         self.e = sdev.materialise(w, wl.spec_e(w), device)
-        self.W = co.weights(self.wf, self.wkv, self.e)
+        self.W, self.f_e = make_weights(co, self.dims, self.wf, self.wkv, self.e, fold_e)
         self.ws = torch.zeros(max(co.workspace_bytes(self.dims, co.CO_WS_ROUND), 256),
                               dtype=torch.uint8, device=device)
         self.ws_project = co.workspace_bytes(self.dims, co.CO_WS_PROJECT)
@@ -102,7 +114,7 @@ class TrainScenario:
     carry segment through a carry-only route, so that its committed length is
     the shifted anchor a' and its queries sit at a' + i."""
 
-    def __init__(self, w: wl.Workload, device: str = "cuda"):
+    def __init__(self, w: wl.Workload, device: str = "cuda", fold_e: bool = True):
         import torch
         import paper_2609_14717_amd as co
         assert w.anchors and w.seq_len
@@ -117,7 +129,7 @@ class TrainScenario:
         self.wf = sdev.materialise(w, wl.spec_wf(w), device)
         self.wkv = sdev.materialise(w, wl.spec_wkv(w), device)
         self.e = sdev.materialise(w, wl.spec_e(w), device)
-        self.W = co.weights(self.wf, self.wkv, self.e)
+        self.W, self.f_e = make_weights(co, self.dims, self.wf, self.wkv, self.e, fold_e)
         dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
         # prefill: every recorded position of every response, committed, no E
         h = torch.empty((S, w.seq_len, w.Dcat), dtype=dt, device=device)

@@ -36,11 +36,11 @@ def _gpu():
     return Scenario
 
 
-def run_rounds(w, n_rounds, mode="carry", seqs=None, check_context=True):
+def run_rounds(w, n_rounds, mode="carry", seqs=None, check_context=True, fold_e=True):
     import paper_2609_14717_amd as co
     Scenario = _gpu()
-    print(f"[parity] workload={w.name} rounds={n_rounds} mode={mode}", flush=True)
-    sc = Scenario(w)
+    print(f"[parity] workload={w.name} rounds={n_rounds} mode={mode} fold_e={fold_e}", flush=True)
+    sc = Scenario(w, fold_e=fold_e)
     orc = OracleRun(w, seqs=seqs)
     seqs = orc.seqs
     if check_context and w.ctx_mode == "projected" and w.ctx_lo:
@@ -70,6 +70,49 @@ def test_small_chains(w):
 @pytest.mark.parametrize("w", [SMALL_RAGGED, SMALL_G4], ids=lambda w: w.name)
 def test_small_chains_baseline_mode(w):
     run_rounds(w, 3, mode="baseline")
+
+
+@pytest.mark.parametrize("w", [SMALL_RAGGED, SMALL_G4, BATCH3_8B], ids=lambda w: w.name)
+def test_small_chains_e_in_kernel(w):
+    """F(E) accumulated inside the projection instead of folded beforehand."""
+    run_rounds(w, 3, fold_e=False)
+
+
+# 256-row windows (16 sequences x 16) and a 3200-row prefill, small enough for
+# the oracle, run through every large-tile GEMM variant, with F(E) folded
+# beforehand and accumulated in the kernel.
+WIDE64 = wl.Workload("wide_hd64", S=16, B=16, Dcat=1024, d=256, L=2, Hq=4, Hkv=2, hd=64,
+                     dtype="bf16", theta=1e4, ctx_lo=200, ctx_hi=200, ctx_mode="projected",
+                     accept=("geom", 0.3), rounds=3, seed=0x5EED06)
+WIDE128 = wl.Workload("wide_hd128", S=16, B=16, Dcat=1536, d=512, L=1, Hq=8, Hkv=2, hd=128,
+                      dtype="bf16", theta=1e6, ctx_lo=200, ctx_hi=200, ctx_mode="projected",
+                      accept=("uniform",), rounds=3, seed=0x5EED07)
+
+
+@pytest.mark.parametrize("fold", [True, False], ids=["folded", "in_kernel"])
+@pytest.mark.parametrize("variant", range(6), ids=lambda v: f"v{v}")
+@pytest.mark.parametrize("w", [WIDE64, WIDE128], ids=lambda w: w.name)
+def test_wide_gemm_variants(w, variant, fold, monkeypatch):
+    monkeypatch.setenv("CO_GEMM_WIDE_VARIANT", str(variant))
+    run_rounds(w, 2, fold_e=fold)
+
+
+@pytest.mark.parametrize("w", [SMALL_G4, WIDE128, wl.RAGGED32], ids=lambda w: w.name)
+def test_fold_e(w):
+    """carryover_fold_e against F E in fp64 (fp32 accumulation of exact products)."""
+    import paper_2609_14717_amd as co
+    Scenario = _gpu()
+    from helpers import host
+    sc = Scenario(w, build_context=False)
+    torch.cuda.synchronize()
+    WF, E = host(w, wl.spec_wf(w)), host(w, wl.spec_e(w))
+    ref = WF @ E
+    mag = np.abs(WF) @ np.abs(E)
+    got = sc.f_e.cpu().numpy().astype(np.float64)
+    assert got.shape == ref.shape
+    err = np.max(np.abs(got - ref) / mag)
+    assert err <= 1e-5, err
+    assert co.carryover_read_status(sc.st) == 0
 
 
 def test_tiny_fp32_full():
