@@ -337,16 +337,6 @@ __device__ __forceinline__ int pick_reg(const int (&v)[N], int i) {
   return r;
 }
 
-// cos/sin of pos * inv_freq with the angle reduced to revolutions in fp64 and
-// the hardware sine/cosine (which take revolutions); bf16 queries only.
-__device__ __forceinline__ void rope_cos_sin_rev(int pos, double inv_freq_rev, float* c, float* s) {
-  double r = static_cast<double>(pos) * inv_freq_rev;
-  r -= rint(r);
-  const float rf = static_cast<float>(r);
-  *c = __builtin_amdgcn_cosf(rf);
-  *s = __builtin_amdgcn_sinf(rf);
-}
-
 template <int HD, int NT, int NW, int NS, int PQ, int RTM>
 __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int layer_count, int n_wg,
                                                              int hdr_floats, int round_tiles,
@@ -403,7 +393,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
   const uint16_t* Q = static_cast<const uint16_t*>(a.q);
   const bool rotate_q = !(a.flags & CO_Q_PREROTATED);
   if (tid < HD / 2)   // in revolutions per position
-    inv_lds[tid] = a.rope_inv[tid] * 0.15915494309189533577;
+    inv_lds[tid] = a.rope_inv[tid] * kInv2Pi;
   // key of S^T M-tile a / b at row rho = lane % 16: keys {8q + r} and {8q + 4 + r}
   const int key_a = 8 * (col >> 2) + (col & 3);
   const int key_b = key_a + 4;

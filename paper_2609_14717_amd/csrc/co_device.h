@@ -107,6 +107,19 @@ __device__ __forceinline__ void rope_cos_sin(int pos, double inv_freq, float* c,
   sincosf(r, s, c);
 }
 
+// cos/sin of pos * inv_freq with the angle reduced to revolutions in fp64 and
+// the hardware sine/cosine (which take revolutions; absolute error near 1e-6,
+// far below bf16 rounding); used where results are stored as bf16.
+__device__ __forceinline__ void rope_cos_sin_rev(int pos, double inv_freq_rev, float* c, float* s) {
+  double r = static_cast<double>(pos) * inv_freq_rev;
+  r -= rint(r);
+  const float rf = static_cast<float>(r);
+  *c = __builtin_amdgcn_cosf(rf);
+  *s = __builtin_amdgcn_sinf(rf);
+}
+
+constexpr double kInv2Pi = 0.15915494309189533577;
+
 __device__ __forceinline__ void set_status(int32_t* status, int32_t code) {
   if (status) atomicCAS(status, 0, code);
 }

@@ -8,13 +8,21 @@
 
 namespace co {
 
+// The table kv_store<T> expects for head pair i: radians (fp32) or revolutions
+// (bf16) per position.
+template <typename T>
+__device__ __forceinline__ double rope_table(const KvDest& e, int i) {
+  return sizeof(T) == 2 ? e.rope_inv[i] * kInv2Pi : e.rope_inv[i];
+}
+
 __device__ __forceinline__ bool is_carry_row(int32_t dst) { return dst < 0 && dst != kSkip; }
 
 // ------------------------------------------------------------- K/V stores
 
 // Store pairs (i0+p, i0+p+hd/2), p < NP, of head segment `seg` = (layer, K|V, head)
 // of window row `row`.  lo/hi hold the unrotated fp32 values of those dims;
-// inv_freq[i] = theta^(-2i/hd).
+// inv_freq[i] = theta^(-2i/hd) in radians per position for fp32 stores, in
+// revolutions per position (rope_table) for bf16 stores.
 template <typename T, int NP>
 __device__ inline void kv_store(const KvDest& e, int row, int32_t dst, int pos, int seg, int i0,
                          const float* lo, const float* hi, const double* inv_freq) {
@@ -55,7 +63,10 @@ __device__ inline void kv_store(const KvDest& e, int row, int32_t dst, int pos, 
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
       float c, s;
-      rope_cos_sin(pos, inv_freq[i0 + p], &c, &s);
+      if constexpr (sizeof(T) == 2)
+        rope_cos_sin_rev(pos, inv_freq[i0 + p], &c, &s);
+      else
+        rope_cos_sin(pos, inv_freq[i0 + p], &c, &s);
       kptr[kbase + i0 + p] = to_elem<T>(lo[p] * c - hi[p] * s);
       kptr[kbase + i0 + p + half] = to_elem<T>(hi[p] * c + lo[p] * s);
     }

@@ -252,7 +252,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
       for (int r = 0; r < 4; ++r)
         sc[((wm * TM + a) * 16 + (lane >> 4) * 4 + r) * LDC + (wn * TN + b) * 16 + (lane & 15)] =
             acc[a][b][r];
-  if (g.mode == kModeKV && tid < g.kv.hd / 2) inv_tab[tid] = g.kv.rope_inv[tid];
+  if (g.mode == kModeKV && tid < g.kv.hd / 2) inv_tab[tid] = rope_table<uint16_t>(g.kv, tid);
   __shared__ float fe_lds[BN];
   __shared__ int dst_lds[BM], pos_lds[BM];
   asm volatile("" : "+v"(rd_dst), "+v"(rd_pos));
@@ -536,7 +536,7 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_kernel(GemmArgs g, int tiles
     return;
   }
 
-  if (g.mode == kModeKV && tid < g.kv.hd / 2) inv_tab[tid] = g.kv.rope_inv[tid];
+  if (g.mode == kModeKV && tid < g.kv.hd / 2) inv_tab[tid] = rope_table<uint16_t>(g.kv, tid);
   asm volatile("" : "+v"(rd_dst), "+v"(rd_pos));
   if (need_rows && tid < BM) {
     dst_lds[tid] = rd_dst;
@@ -650,25 +650,28 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
 
 // -------------------------------------------- epilogues over fp32 partials
 
+// Four consecutive columns per thread (N is a multiple of 64).
 template <typename T>
 __global__ __launch_bounds__(256) void epi_z_kernel(const float* part, int splits, int M, int N,
                                                     T* z, const float* part_e, const float* fe,
                                                     const int32_t* row_dst) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (i >= static_cast<int64_t>(M) * N) return;
-  float v = 0.f;
-  for (int s = 0; s < splits; ++s) v += part[static_cast<int64_t>(s) * M * N + i];
+  const int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
+  const int64_t MN = static_cast<int64_t>(M) * N;
+  if (i >= MN) return;
+  f32x4 v = *reinterpret_cast<const f32x4*>(part + i);
+  for (int s = 1; s < splits; ++s) v += *reinterpret_cast<const f32x4*>(part + s * MN + i);
   if ((part_e || fe) && is_carry_row(row_dst[i / N])) {
     const int col = static_cast<int>(i % N);
     if (fe) {
-      v += fe[col];
+      v += *reinterpret_cast<const f32x4*>(fe + col);
     } else {
-      float e = 0.f;
-      for (int s = 0; s < splits; ++s) e += part_e[static_cast<int64_t>(s) * N + col];
+      f32x4 e = *reinterpret_cast<const f32x4*>(part_e + col);
+      for (int s = 1; s < splits; ++s) e += *reinterpret_cast<const f32x4*>(part_e + static_cast<int64_t>(s) * N + col);
       v += e;
     }
   }
-  z[i] = to_elem<T>(v);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) z[i + q] = to_elem<T>(v[q]);
 }
 
 template <typename T>
@@ -676,7 +679,7 @@ __global__ __launch_bounds__(256) void epi_kv_kernel(const float* part, int spli
                                                      KvDest e) {
   __shared__ double inv_tab[64];
   const int half = e.hd / 2;
-  if (threadIdx.x < half) inv_tab[threadIdx.x] = e.rope_inv[threadIdx.x];
+  if (threadIdx.x < half) inv_tab[threadIdx.x] = rope_table<T>(e, threadIdx.x);
   __syncthreads();
   const int64_t items = static_cast<int64_t>(M) * (N / 2);   // one pair per thread
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
@@ -794,10 +797,11 @@ bool pick_wide(int M, int N, int K, int num_cus, int* tile, int* split) {
       const int64_t wgs = tiles * s;
       if (wgs < num_cus / 2 && force == nullptr) continue;
       const int64_t waves = (wgs + num_cus - 1) / num_cus;
+      // main loop at the per-CU rate measured with operands streaming from HBM
       const double t_mfma = static_cast<double>(waves) * kWideBM[v] * kWideBN[v] * kps * 2.0 /
-                            (7.0e12 * eff);
+                            (4.5e12 * eff);
       // split partials: written, read back and reduced by a second kernel
-      const double t_part = s > 1 ? static_cast<double>(s) * M * N * 8.0 / 3.0e12 + 3e-6 : 0.0;
+      const double t_part = s > 1 ? static_cast<double>(s) * M * N * 8.0 / 4.0e12 + 2e-6 : 0.0;
       if (t_mfma + t_part < best) {
         best = t_mfma + t_part;
         bv = v;
@@ -885,7 +889,7 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
     f.mode = kv.mode = kModePartial;
     hipLaunchKernelGGL(gemm_f32_kernel, dim3((f.N + 63) / 64, (f.M + 31) / 32), dim3(256), 0,
                        stream, f);
-    const int64_t nz = static_cast<int64_t>(a.M) * a.d;
+    const int64_t nz = static_cast<int64_t>(a.M) * a.d / 4;
     hipLaunchKernelGGL(epi_z_kernel<float>, dim3(static_cast<unsigned>((nz + 255) / 256)),
                        dim3(256), 0, stream, part, 1, a.M, a.d, static_cast<float*>(z),
                        static_cast<const float*>(nullptr), static_cast<const float*>(nullptr),
@@ -906,7 +910,7 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
   f.mode = p.f_split > 1 ? kModePartial : kModeZ;
   if ((err = launch_gemm_bf16(f, p.f_tile, p.f_split, stream)) != hipSuccess) return err;
   if (p.f_split > 1) {
-    const int64_t nz = static_cast<int64_t>(a.M) * a.d;
+    const int64_t nz = static_cast<int64_t>(a.M) * a.d / 4;
     hipLaunchKernelGGL(epi_z_kernel<uint16_t>, dim3(static_cast<unsigned>((nz + 255) / 256)),
                        dim3(256), 0, stream, part, p.f_split, a.M, a.d, static_cast<uint16_t*>(z),
                        static_cast<const float*>(f.e ? f.partial_e : nullptr), f.fe, a.dst.row_dst);
