@@ -452,7 +452,7 @@ def run_train(args, w):
     vw = w.replace(S=V)
     n = min(args.steps, 100)
     att_s = timed_calls(torch, stream, n, lambda: co.drafter_block_attention(
-        sc.vdims, 0, w.L, sc.q, sc.vst, sc.out, sc.lse, 0, sc.ws))
+        sc.vdims, 0, w.L, sc.q, sc.vst, sc.out, sc.lse, co.CO_ATTN_SHARED_PREFIX, sc.ws))
     wsp = co.workspace_bytes(sc.vdims, co.CO_WS_PROJECT)
     proj_s = timed_calls(torch, stream, n, lambda: co.carryover_project_kv(
         sc.vdims, sc.W, sc.hidden, sc.vrt, sc.vst, sc.ws, ws_bytes=wsp))
@@ -478,8 +478,8 @@ def run_train(args, w):
                    "anchored_blocks": V, "block": w.B, "feat_dim": w.Dcat, "model_dim": w.d,
                    "layers": w.L, "q_heads": w.Hq, "kv_heads": w.Hkv, "head_dim": w.hd,
                    "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma", "kernel": "drafter_block_attention (" +
-                     " + ".join(ATTN_KERNELS) + ")", "achieved": atfl,
+        "roofline": {"bound": "mfma", "kernel": "drafter_block_attention, shared prefixes "
+                     "(attn_group_kernel)", "achieved": atfl,
                      "peak": MFMA_PEAK_TFLOPS[w.dtype], "unit": "TFLOP/s",
                      "frac": atfl / MFMA_PEAK_TFLOPS[w.dtype], "traffic": None,
                      "algorithmic_flops_per_launch": aflops, "avg_launch_us": att_s * 1e6},

@@ -84,6 +84,12 @@ enum { CO_DTYPE_F32 = 0, CO_DTYPE_BF16 = 1 };
 #define CO_ROUTE_ACCEPT_ALL (1u << 1) /* m := block for every sequence (build context)         */
 #define CO_ROUTE_CARRY_ONLY (1u << 2) /* rows 0..m-1 are already committed: store only carries */
 #define CO_Q_PREROTATED     (1u << 3) /* queries already carry their rotary embedding          */
+#define CO_ATTN_SHARED_PREFIX (1u << 4) /* bf16 attention: consecutive sequences are blocks of one
+                                         recorded response whose committed keys are prefixes of
+                                         the same pages (Algorithm 2); key tiles are read once
+                                         per group of four (head_dim 64, or head_dim 128 with up
+                                         to 32 query rows per KV head; other shapes ignore the
+                                         flag).  Results do not depend on the flag.             */
 
 typedef struct co_dims {
   int32_t num_seqs;           /* S: sequences in the batch                           */

@@ -19,6 +19,7 @@ CO_OK, CO_ERR_INVALID_ARG, CO_ERR_UNSUPPORTED, CO_ERR_WORKSPACE = 0, 1, 2, 3
 CO_ERR_CAPACITY, CO_ERR_PAGE_RANGE, CO_ERR_HIP, CO_ERR_LENGTH = 4, 5, 6, 7
 CO_DTYPE_F32, CO_DTYPE_BF16 = 0, 1
 CO_BASELINE_MODE, CO_ROUTE_ACCEPT_ALL, CO_ROUTE_CARRY_ONLY, CO_Q_PREROTATED = 1, 2, 4, 8
+CO_ATTN_SHARED_PREFIX = 16
 CO_WS_PROJECT, CO_WS_ATTENTION, CO_WS_ROUND = 0, 1, 2
 SKIP = -(2 ** 31)
 PAGE = 16

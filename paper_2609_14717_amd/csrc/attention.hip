@@ -1080,6 +1080,507 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
   }
 }
 
+// ------------------------------------------------ bf16 grouped-prefix path
+//
+// Blocks anchored in one recorded response (the training-shaped forward,
+// Algorithm 2) are sequences whose committed keys are prefixes of the same
+// pages.  Under CO_ATTN_SHARED_PREFIX a workgroup takes four consecutive
+// sequences, one per wavefront, so that each key tile is read once for all of
+// their block queries:
+//   * the page ids of a chunk of pages are staged in LDS; the chunk is shared
+//     when every wavefront's pages agree with those of the longest sequence
+//     wherever its own keys reach;
+//   * shared chunks stream through a 4-deep ring of 32-key tiles, each
+//     wavefront loading one of a tile's four pages (K0, K1, V0, V1) with
+//     direct-to-LDS loads and a barrier publishing the tile; a wavefront skips
+//     tiles beyond its own length and masks the keys of its last one;
+//   * chunks that are not shared are streamed by each wavefront on its own;
+//   * the carry pages of each sequence come last; the result is normalised and
+//     written in place (no partial records).
+// Per tile the arithmetic is that of the persistent path (S^T = K . Q^T on
+// permuted keys, lazily rescaled online softmax, O^T += V^T . P^T).
+constexpr int kGroupSeqs = 4;       // sequences (wavefronts) per workgroup
+constexpr int kGroupChunk = 128;    // pages whose ids are staged at a time
+
+
+// Workgroups per CU the grouped kernel is built for (the second launch bound):
+// with head_dim 64 and 32 query rows it fits 168 VGPRs and about 35 KiB of
+// LDS, so three share a CU and hide each other's dependency latencies.
+//
+// Per tile the products use v_mfma_f32_32x32x16_bf16 on 32 keys x 32 query
+// rows.  S^T = K . Q^T takes K row rho from key pi(rho), pi swapping bits 2
+// and 3 of the key index; then lane l holds, for query l % 32, the keys
+// 8*(l/32) .. +7 of both pages of the tile (registers 0-7: page 0, 8-15:
+// page 1), which is exactly the B operand of O^T += V^T . P^T over those
+// keys, and V pages stored [head_dim][16 slots] give the matching A operand
+// with one 16-byte read.  The row maximum is a maximum over 16 registers and
+// one exchange between the two halves of the wavefront.
+template <int HD, int NQT>
+__global__ __launch_bounds__(256, HD == 64 ? (NQT == 1 ? 3 : 2) : 1)
+void attn_group_kernel(AttnArgs a, int split_tiles, int n_splits) {
+  constexpr int KK = HD / 16, MO = HD / 32, NQP = NQT * 32;
+  constexpr int QLD = HD + 8;
+  constexpr int ROWB = HD * 2, CPR = ROWB / 16;
+  constexpr int PAGE_BYTES = kPage * ROWB, LPP = PAGE_BYTES / 1024;
+  constexpr int TILE_BYTES = 4 * PAGE_BYTES;
+  constexpr int NS = 4;                          // ring tiles; one per wavefront when private
+  constexpr float kRescale = 8.f;
+  static_assert(LPP * (NS - 1) < 64, "vmcnt");
+  // the rotated queries are staged in the ring before the first tile lands
+  constexpr int RING_BYTES = NS * TILE_BYTES;
+  constexpr int Q_BYTES = kGroupSeqs * NQP * QLD * 2;
+  __shared__ __align__(16) unsigned char ring[RING_BYTES > Q_BYTES ? RING_BYTES : Q_BYTES];
+  uint16_t* q_lds = reinterpret_cast<uint16_t*>(ring);
+  __shared__ int pid_lds[kGroupSeqs][kGroupChunk];
+  __shared__ double inv_lds[HD / 2];
+  __shared__ int npc_lds[kGroupSeqs];
+  __shared__ int mismatch;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int half = lane >> 5, r32 = lane & 31;
+  const int G = a.Hq / a.Hkv, nq = a.B * G;
+  const int n_groups = (a.S + kGroupSeqs - 1) / kGroupSeqs;
+  // Workgroup ids are dealt to the 8 XCDs round-robin; renumbered, every XCD
+  // takes a run of consecutive groups, whose shared pages then stay in its L2.
+  int bx = blockIdx.x;
+  if ((gridDim.x & 7) == 0) bx = (bx & 7) * (gridDim.x >> 3) + (bx >> 3);
+  const int split = bx % n_splits;
+  const int group = n_groups - 1 - bx / n_splits;   // later blocks reach furthest
+  const int g = blockIdx.y, layer_local = blockIdx.z, layer = a.layer_begin + layer_local;
+  const int s = group * kGroupSeqs + wave;
+  const bool live = s < a.S;
+  const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
+  const uint16_t* vc = static_cast<const uint16_t*>(a.v_cache);
+  const uint16_t* kk = static_cast<const uint16_t*>(a.k_carry);
+  const uint16_t* vk = static_cast<const uint16_t*>(a.v_carry);
+  if (tid < HD / 2) inv_lds[tid] = a.rope_inv[tid] * kInv2Pi;
+
+  // this wavefront's sequence
+  int ctx = 0, carry = 0;
+  if (live) {
+    const SeqInfo si = seq_info(a, s, 1);
+    if (si.ok) {
+      ctx = si.ctx;
+      carry = si.carry;
+    } else if (lane == 0 && g == 0 && layer_local == 0) {
+      set_status(a.status, CO_ERR_LENGTH);
+    }
+  }
+  const int npc = (ctx + kPage - 1) / kPage;
+  if (lane == 0) npc_lds[wave] = npc;
+  if (tid == 0) mismatch = 0;
+  __syncthreads();   // inv_lds, npc_lds
+
+  int npc_max = 0, leader = 0;
+#pragma unroll
+  for (int v = 0; v < kGroupSeqs; ++v)
+    if (npc_lds[v] > npc_max) {
+      npc_max = npc_lds[v];
+      leader = v;
+    }
+  // this workgroup's share of the group's committed tiles; the last share also
+  // takes the carry keys.  Shares past the group's keys have nothing to do.
+  const int t_all = (npc_max + 1) / 2;
+  const int n_used = max(1, (t_all + split_tiles - 1) / split_tiles);
+  if (split >= n_used) return;   // uniform, and no barrier follows for this workgroup
+  const int t_beg = split * split_tiles, t_end = min(t_all, t_beg + split_tiles);
+  const bool last_share = split == n_used - 1;
+
+  // rotated, scaled queries of this wavefront -> LDS -> MFMA B fragments
+  {
+    const uint16_t* Q = static_cast<const uint16_t*>(a.q);
+    const bool rotate_q = !(a.flags & CO_Q_PREROTATED);
+    const float qscale = rsqrtf(static_cast<float>(HD)) * kLog2e;
+    uint16_t* qw = q_lds + wave * NQP * QLD;
+    for (int idx = lane; idx < NQP * (HD / 8); idx += 64) {
+      const int qn = idx / (HD / 8), p4 = (idx % (HD / 8)) * 4;
+      u16x4 lo4 = {0, 0, 0, 0}, hi4 = {0, 0, 0, 0};
+      if (live && qn < nq) {
+        const int64_t off = out_row(a, layer_local, s, g, qn, G) * HD + p4;
+        const u16x4 ql = *reinterpret_cast<const u16x4*>(Q + off);
+        const u16x4 qh = *reinterpret_cast<const u16x4*>(Q + off + HD / 2);
+        const int pos = ctx + qn / G;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float x = bf2f(ql[e]), y = bf2f(qh[e]);
+          if (rotate_q) {
+            float cs, sn;
+            rope_cos_sin_rev(pos, inv_lds[p4 + e], &cs, &sn);
+            const float x2 = x * cs - y * sn, y2 = y * cs + x * sn;
+            x = x2;
+            y = y2;
+          }
+          lo4[e] = f2bf(x * qscale);
+          hi4[e] = f2bf(y * qscale);
+        }
+      }
+      *reinterpret_cast<u16x4*>(qw + qn * QLD + p4) = lo4;
+      *reinterpret_cast<u16x4*>(qw + qn * QLD + p4 + HD / 2) = hi4;
+    }
+  }
+  __syncthreads();
+  u16x8 qf[NQT][KK];
+#pragma unroll
+  for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+    for (int k = 0; k < KK; ++k)
+      qf[qt][k] = *reinterpret_cast<const u16x8*>(q_lds + (wave * NQP + qt * 32 + r32) * QLD +
+                                                   k * 16 + half * 8);
+
+  // fragment offsets within a tile.  K: row rho = lane % 32 holds key pi(rho);
+  // its 16-byte chunk 2k + lane/32 sits XOR-swizzled by the slot.  V: head
+  // dims 32m + lane % 32, keys 8*(lane/32) .. +7 of page j.
+  const int key = 16 * (r32 >> 4) + 8 * ((r32 >> 2) & 1) + 4 * ((r32 >> 3) & 1) + (r32 & 3);
+  const int kslot = key & 15;
+  uint32_t kf_off[KK];
+#pragma unroll
+  for (int k = 0; k < KK; ++k) {
+    const int ch = 2 * k + half;
+    kf_off[k] = (key >> 4) * PAGE_BYTES + kslot * ROWB + ((ch ^ (kslot & (CPR - 1))) << 4);
+  }
+  const uint32_t vf_off = 2 * PAGE_BYTES + r32 * 32 + half * 16;
+  const int slot_base = 8 * half;   // the slots of each page this lane's scores cover
+  // per-lane source offsets (elements) of the loads of one page: K rows land
+  // XOR-swizzled, V pages are copied as they are
+  int k_off[LPP], v_off[LPP];
+#pragma unroll
+  for (int q = 0; q < LPP; ++q) {
+    const int byte = q * 1024 + lane * 16;
+    const int r = byte / ROWB, pch = (byte % ROWB) / 16;
+    k_off[q] = r * HD + (pch ^ (r & (CPR - 1))) * 8;
+    v_off[q] = byte / 2;
+  }
+  const uint32_t ring_lds = lds_addr(ring);
+  // one page (K or V) of a committed page id, or of carry page cp of this
+  // sequence, or a harmless dummy (id < 0) -> LDS
+  // page `phys` of this layer and KV head: base + phys * page_stride elements
+  const int64_t page_stride = static_cast<int64_t>(a.Hkv) * kPage * HD;
+  const int64_t head0 = (static_cast<int64_t>(layer) * a.num_pages * a.Hkv + g) * (kPage * HD);
+  const uint16_t* kbase = kc + head0;
+  const uint16_t* vbase = vc + head0;
+  auto load_page = [&](bool is_v, int phys, uint32_t dst) {
+    const uint16_t* src = is_v ? vk : kk;   // dummy: carry page 0 of layer 0
+    if (phys >= 0) src = (is_v ? vbase : kbase) + phys * page_stride;
+#pragma unroll
+    for (int q = 0; q < LPP; ++q)
+      lds_dma16_opaque(src + (is_v ? v_off[q] : k_off[q]), dst + q * 1024);
+  };
+  auto load_carry_page = [&](bool is_v, int cp, uint32_t dst) {
+    const int64_t row = ((static_cast<int64_t>(layer) * a.S + s) * a.CP + cp) * a.Hkv + g;
+    const uint16_t* src = (is_v ? vk : kk) + row * (kPage * HD);
+#pragma unroll
+    for (int q = 0; q < LPP; ++q)
+      lds_dma16_opaque(src + (is_v ? v_off[q] : k_off[q]), dst + q * 1024);
+  };
+
+  f32x16 o[NQT][MO];
+  float m_run[NQT], l_run[NQT];   // l_run: this half-wavefront's keys (summed at the end)
+#pragma unroll
+  for (int qt = 0; qt < NQT; ++qt) {
+#pragma unroll
+    for (int m = 0; m < MO; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[qt][m][r] = 0.f;
+    m_run[qt] = -INFINITY;
+    l_run[qt] = 0.f;
+  }
+  // one 32-key tile at tb: n0 / n1 valid keys in its two pages
+  auto tile = [&](const unsigned char* tb, int n0, int n1) {
+    const bool partial = n0 < kPage || n1 < kPage;
+    u16x8 kf[KK], vf[MO][2];
+#pragma unroll
+    for (int k = 0; k < KK; ++k) kf[k] = *reinterpret_cast<const u16x8*>(tb + kf_off[k]);
+#pragma unroll
+    for (int m = 0; m < MO; ++m)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        vf[m][j] = *reinterpret_cast<const u16x8*>(tb + vf_off + j * PAGE_BYTES + m * 32 * 32);
+    // scores relative to the running reference: the accumulators start at -base
+    f32x16 sc[NQT];
+    float base[NQT];
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
+      base[qt] = (m_run[qt] == -INFINITY) ? 0.f : m_run[qt];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[qt][r] = -base[qt];
+    }
+#pragma unroll
+    for (int k = 0; k < KK; ++k)
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt) sc[qt] = mfma32x32x16(kf[k], qf[qt][k], sc[qt]);
+    if (partial) {
+#pragma unroll
+      for (int m = 0; m < MO; ++m)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (slot_base + e >= (j ? n1 : n0)) vf[m][j][e] = 0;   // invalid keys may hold anything
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (slot_base + (r & 7) >= ((r >> 3) ? n1 : n0)) sc[qt][r] = -INFINITY;
+    }
+    float mx[NQT];
+    bool up = false;
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
+      float v = fmaxf(fmaxf(fmaxf(sc[qt][0], sc[qt][1]), fmaxf(sc[qt][2], sc[qt][3])),
+                      fmaxf(fmaxf(sc[qt][4], sc[qt][5]), fmaxf(sc[qt][6], sc[qt][7])));
+      v = fmaxf(v, fmaxf(fmaxf(fmaxf(sc[qt][8], sc[qt][9]), fmaxf(sc[qt][10], sc[qt][11])),
+                         fmaxf(fmaxf(sc[qt][12], sc[qt][13]), fmaxf(sc[qt][14], sc[qt][15]))));
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v),
+                                                       false, false);
+      mx[qt] = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) + base[qt];
+      up |= mx[qt] > m_run[qt] + kRescale;
+    }
+    if (__any(up)) {
+      // move the reference up (only where the tile exceeds it) and rescale
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt) {
+        const float m_new = mx[qt] > m_run[qt] + kRescale ? mx[qt] : m_run[qt];
+        const float alpha = (m_new == m_run[qt]) ? 1.f : exp2f(m_run[qt] - m_new);
+        l_run[qt] *= alpha;
+#pragma unroll
+        for (int m = 0; m < MO; ++m) o[qt][m] *= alpha;
+        m_run[qt] = m_new;
+        const float shift = (m_new == -INFINITY) ? 0.f : m_new - base[qt];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sc[qt][r] -= shift;
+      }
+    }
+    u16x8 pk[NQT][2];
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
+      float p[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r)   // v_exp_f32: arguments are <= kRescale or -inf
+        p[r] = __builtin_amdgcn_exp2f(sc[qt][r]);
+      l_run[qt] += (((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]))) +
+                   (((p[8] + p[9]) + (p[10] + p[11])) + ((p[12] + p[13]) + (p[14] + p[15])));
+      typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const u32x4v w4 = {cvt_pk_bf16(p[8 * j + 0], p[8 * j + 1]), cvt_pk_bf16(p[8 * j + 2], p[8 * j + 3]),
+                           cvt_pk_bf16(p[8 * j + 4], p[8 * j + 5]), cvt_pk_bf16(p[8 * j + 6], p[8 * j + 7])};
+        pk[qt][j] = __builtin_bit_cast(u16x8, w4);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int m = 0; m < MO; ++m)
+#pragma unroll
+        for (int qt = 0; qt < NQT; ++qt) o[qt][m] = mfma32x32x16(vf[m][j], pk[qt][j], o[qt][m]);
+  };
+  auto valid = [&](int limit, int t, int half_) {
+    return min(kPage, max(0, limit - (2 * t + half_) * kPage));
+  };
+
+  // ---- committed keys of this share, chunk by chunk
+  const int p_end = min(npc_max, 2 * t_end);
+  for (int c0 = 2 * t_beg; c0 < p_end; c0 += kGroupChunk) {
+    const int cn = min(kGroupChunk, p_end - c0);
+    __syncthreads();   // the previous chunk's tiles, page ids and flag are consumed
+    if (tid == 0) mismatch = 0;
+    for (int i = lane; i < cn; i += 64) {
+      int id = -1;
+      if (live && c0 + i < npc) {
+        id = a.page_table[static_cast<int64_t>(s) * a.max_pages + c0 + i];
+        if (id < 0 || id >= a.num_pages) {   // read as a dummy page, its keys masked
+          set_status(a.status, CO_ERR_PAGE_RANGE);
+          id = -1;
+        }
+      }
+      pid_lds[wave][i] = id;
+    }
+    __syncthreads();
+    bool bad = false;
+    for (int i = lane; i < cn; i += 64)
+      if (c0 + i < npc && pid_lds[wave][i] != pid_lds[leader][i]) bad = true;
+    if (__any(bad) && lane == 0) mismatch = 1;
+    __syncthreads();
+    const int t0 = c0 / 2, t1 = min(t_end, (c0 + cn + 1) / 2);
+    // the chunk's page ids of this wavefront and of the leader in registers,
+    // lane i holding pages i and i + 64 (-1 past the chunk)
+    const int my0 = lane < cn ? pid_lds[wave][lane] : -1;
+    const int my1 = lane + 64 < cn ? pid_lds[wave][lane + 64] : -1;
+    const int ld0 = lane < cn ? pid_lds[leader][lane] : -1;
+    const int ld1 = lane + 64 < cn ? pid_lds[leader][lane + 64] : -1;
+    auto pid_of = [&](int r0, int r1, int p) {   // p uniform, < kGroupChunk
+      const int x0 = __builtin_amdgcn_readlane(r0, p & 63);
+      const int x1 = __builtin_amdgcn_readlane(r1, p & 63);
+      return p < 64 ? x0 : x1;
+    };
+    // keys of tile t in this wavefront: [32t, 32t + 32) clipped to ctx, and pages
+    // whose id was rejected hold no valid keys
+    auto keys = [&](int t, int half_) {
+      const int p = 2 * t + half_ - c0;
+      if (p >= cn || pid_of(my0, my1, p) < 0) return 0;
+      return valid(ctx, t, half_);
+    };
+    if (!mismatch) {
+      // shared: wavefront w loads page w of each tile (K0, K1, V0, V1) of the leader
+      auto issue = [&](int t) {
+        const int p = 2 * t + (wave & 1) - c0;
+        const int phys = p < cn ? pid_of(ld0, ld1, p) : -1;
+        load_page(wave >= 2, phys, ring_lds + (t % NS) * TILE_BYTES + wave * PAGE_BYTES);
+      };
+      for (int t = t0; t < min(t1, t0 + NS - 1); ++t) issue(t);
+      for (int t = t0; t < t1; ++t) {
+        const int ahead = min(NS - 2, t1 - 1 - t);
+        if (ahead >= 2) wait_vm_lgkm_barrier<2 * LPP>();
+        else if (ahead == 1) wait_vm_lgkm_barrier<LPP>();
+        else wait_vm_lgkm_barrier<0>();
+        if (t + NS - 1 < t1) issue(t + NS - 1);   // into the slot of tile t-1, read by all
+        const int n0 = keys(t, 0), n1 = keys(t, 1);
+        if (n0 + n1 > 0) tile(ring + (t % NS) * TILE_BYTES, n0, n1);
+      }
+    } else {
+      // pages differ between the sequences: each wavefront on its own, one slot each
+      const int my_t1 = min(t1, (min(npc, c0 + cn) + 1) / 2);
+      const uint32_t slot = ring_lds + wave * TILE_BYTES;
+      for (int t = t0; t < my_t1; ++t) {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the previous tile is consumed
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int p = 2 * t + h - c0;
+          const int phys = p < cn ? pid_of(my0, my1, p) : -1;
+          load_page(false, phys, slot + h * PAGE_BYTES);
+          load_page(true, phys, slot + (2 + h) * PAGE_BYTES);
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        const int n0 = keys(t, 0), n1 = keys(t, 1);
+        if (n0 + n1 > 0) tile(ring + wave * TILE_BYTES, n0, n1);
+      }
+    }
+  }
+
+  // ---- the carry segment of this sequence, two carry pages per tile
+  __syncthreads();   // the ring is free
+  if (last_share) {
+    const uint32_t slot = ring_lds + wave * TILE_BYTES;
+    const int ncp = (carry + kPage - 1) / kPage;
+    for (int t = 0; 2 * t < ncp; ++t) {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int cp = min(2 * t + h, ncp - 1);   // a missing second page repeats the first
+        load_carry_page(false, cp, slot + h * PAGE_BYTES);
+        load_carry_page(true, cp, slot + (2 + h) * PAGE_BYTES);
+      }
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      tile(ring + wave * TILE_BYTES, valid(carry, t, 0), valid(carry, t, 1));
+    }
+  }
+
+  // ---- normalise and write, or leave this share's record for the merge
+  if (!live) return;
+  if (n_used > 1) {
+    float* rec = a.ws + ((((static_cast<int64_t>(layer_local) * a.Hkv + g) * a.S + s) * n_splits +
+                          split) * (NQP * (HD + 2)));
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
+      const float l_tot = l_run[qt] + __shfl_xor(l_run[qt], 32);
+      const int qn = qt * 32 + r32;
+#pragma unroll
+      for (int m = 0; m < MO; ++m)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          f32x4 v;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) v[c] = o[qt][m][4 * r4 + c];
+          *reinterpret_cast<f32x4*>(rec + qn * HD + 32 * m + 8 * r4 + 4 * half) = v;
+        }
+      if (half == 0) {
+        rec[NQP * HD + qn] = m_run[qt];
+        rec[NQP * HD + NQP + qn] = l_tot;
+      }
+    }
+    return;
+  }
+  uint16_t* out = static_cast<uint16_t*>(a.out);
+#pragma unroll
+  for (int qt = 0; qt < NQT; ++qt) {
+    const float l_tot = l_run[qt] + __shfl_xor(l_run[qt], 32);
+    const int qn = qt * 32 + r32;
+    if (qn >= nq) continue;
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const int64_t row = out_row(a, layer_local, s, g, qn, G);
+#pragma unroll
+    for (int m = 0; m < MO; ++m)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        u16x4 v;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) v[c] = f2bf(o[qt][m][4 * r4 + c] * inv);
+        *reinterpret_cast<u16x4*>(out + row * HD + 32 * m + 8 * r4 + 4 * half) = v;
+      }
+    if (a.lse && half == 0)
+      a.lse[row] = l_tot > 0.f ? (m_run[qt] + log2f(l_tot)) * kLn2 : -INFINITY;
+  }
+}
+
+// Merge of the shares of a grouped launch (log-sum-exp rule), for sequences
+// whose group needed more than one share: one thread per (query row, 4 dims).
+template <int HD>
+__global__ __launch_bounds__(256) void attn_group_merge_kernel(AttnArgs a, int split_tiles,
+                                                               int n_splits, int nqp) {
+  const int s = blockIdx.x, g = blockIdx.y, layer_local = blockIdx.z;
+  const int G = a.Hq / a.Hkv, nq = a.B * G;
+  int npc_max = 0;
+  const int g0 = s / kGroupSeqs * kGroupSeqs;
+  for (int v = g0; v < min(g0 + kGroupSeqs, a.S); ++v) {
+    const SeqInfo si = seq_info(a, v, 1);
+    if (si.ok) npc_max = max(npc_max, si.npc);
+  }
+  const int n_used = max(1, ((npc_max + 1) / 2 + split_tiles - 1) / split_tiles);
+  if (n_used <= 1) return;   // written by the attention kernel
+  const float* base = a.ws + (((static_cast<int64_t>(layer_local) * a.Hkv + g) * a.S + s) *
+                              n_splits) * (nqp * (HD + 2));
+  const int64_t rec = static_cast<int64_t>(nqp) * (HD + 2);
+  uint16_t* out = static_cast<uint16_t*>(a.out);
+  for (int idx = threadIdx.x; idx < nq * (HD / 4); idx += 256) {
+    const int qn = idx / (HD / 4), d = (idx % (HD / 4)) * 4;
+    float M = -INFINITY;
+    for (int k = 0; k < n_used; ++k) M = fmaxf(M, base[k * rec + nqp * HD + qn]);
+    float L = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int k = 0; k < n_used; ++k) {
+      const float* r = base + k * rec;
+      const float m = r[nqp * HD + qn];
+      const float w = (m == -INFINITY) ? 0.f : exp2f(m - M);
+      L += w * r[nqp * HD + nqp + qn];
+      acc += w * *reinterpret_cast<const f32x4*>(r + qn * HD + d);
+    }
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    const int64_t row = out_row(a, layer_local, s, g, qn, G);
+    u16x4 v;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v[c] = f2bf(acc[c] * inv);
+    *reinterpret_cast<u16x4*>(out + row * HD + d) = v;
+    if (a.lse && d == 0) a.lse[row] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+  }
+}
+
+// Committed tiles per share of a grouped launch (CO_ATTN_GROUP_SPLIT_TILES
+// overrides it for tuning and tests), and the number of shares that covers the
+// longest sequence the page table allows.
+constexpr int kGroupSplitTiles = 128;
+int group_split_tiles() {
+  if (const char* env = getenv("CO_ATTN_GROUP_SPLIT_TILES")) {
+    const int v = atoi(env);
+    if (v >= 1 && v <= 4096) return v;
+  }
+  return kGroupSplitTiles;
+}
+int group_splits(int max_pages) {
+  const int tiles = (max_pages + 1) / 2, sp = group_split_tiles();
+  return max(1, (tiles + sp - 1) / sp);
+}
+
 }  // namespace
 
 AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int num_pages,
@@ -1125,6 +1626,15 @@ AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pa
     p.n_chunks = (max_lp + p.chunk_pages - 1) / p.chunk_pages;
     p.bytes = static_cast<size_t>(L) * S * Hkv * p.n_chunks * p.nq_pad * (hd + 2) * 4;
   }
+  if (dtype == CO_DTYPE_BF16) {
+    // records of the grouped-prefix path (CO_ATTN_SHARED_PREFIX), where it applies
+    const int nq = B * (Hq / Hkv);
+    if (hd == 64 || nq <= 32) {
+      const size_t nqp = nq <= 32 ? 32 : 64;
+      const size_t rec = static_cast<size_t>(L) * Hkv * S * group_splits(max_pages) * nqp * (hd + 2) * 4;
+      if (rec > p.bytes) p.bytes = rec;
+    }
+  }
   p.bytes = (p.bytes + 255) / 256 * 256;
   return p;
 }
@@ -1135,6 +1645,28 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
   const int nt = p.nq_pad / 16;
   const int items = (a.B * (a.Hq / a.Hkv)) * (a.hd / 4);
   const dim3 mgrid(a.S, layer_count * a.Hkv, (items + 255) / 256);
+  // grouped kernel: any query count with head_dim 64, up to 32 rows with 128
+  const bool one = a.B * (a.Hq / a.Hkv) <= 32;
+  if (a.dtype == CO_DTYPE_BF16 && (a.flags & CO_ATTN_SHARED_PREFIX) && (a.hd == 64 || one)) {
+    const int ns = group_splits(a.max_pages);
+    const dim3 ggrid((a.S + kGroupSeqs - 1) / kGroupSeqs * ns, a.Hkv, layer_count);
+    const int sp = group_split_tiles();
+    if (a.hd == 64) {
+      if (one) hipLaunchKernelGGL((attn_group_kernel<64, 1>), ggrid, dim3(256), 0, stream, a, sp, ns);
+      else hipLaunchKernelGGL((attn_group_kernel<64, 2>), ggrid, dim3(256), 0, stream, a, sp, ns);
+    } else {
+      hipLaunchKernelGGL((attn_group_kernel<128, 1>), ggrid, dim3(256), 0, stream, a, sp, ns);
+    }
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess || ns == 1) return err;
+    const dim3 cgrid(a.S, a.Hkv, layer_count);
+    const int nqp = one ? 32 : 64;
+    if (a.hd == 64)
+      hipLaunchKernelGGL(attn_group_merge_kernel<64>, cgrid, dim3(256), 0, stream, a, sp, ns, nqp);
+    else
+      hipLaunchKernelGGL(attn_group_merge_kernel<128>, cgrid, dim3(256), 0, stream, a, sp, ns, nqp);
+    return hipGetLastError();
+  }
   if (a.dtype == CO_DTYPE_BF16) {
     const dim3 grid(p.n_wg);
 #define CO_ATTN_LAUNCH(HD, NT, NW, NS, PQ, RTM)                                                 \

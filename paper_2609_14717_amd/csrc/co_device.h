@@ -44,12 +44,16 @@ __device__ __forceinline__ void lds_dma16(const void* src, void* lds_dst) {
 // to LDS, so it neither waits for it before LDS reads nor counts it in its own
 // vmcnt waits (which therefore only ever wait longer than they need to); the
 // caller orders it with the reads of its LDS slot through explicit vmcnt waits
-// and barriers.  lds_dst must be wavefront-uniform.
+// and barriers.  lds_dst must be wavefront-uniform.  M0 is reserved to the
+// compiler (a clobber would be ignored), so the statement restores it.
 __device__ __forceinline__ void lds_dma16_opaque(const void* src, uint32_t lds_dst) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(src), "s"(lds_dst)
-               : "memory", "m0");
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(lds_dst)
+      : "memory");
 }
 
 // s_waitcnt vmcnt(N) lgkmcnt(0), then a workgroup barrier, as one statement that
@@ -65,6 +69,14 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const __bf16 a = static_cast<__bf16>(lo), b = static_cast<__bf16>(hi);
   return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a)) |
          (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b)) << 16);
+}
+
+// The same pair conversion as one v_cvt_pk_bf16_f32 with both sources (the
+// compiler otherwise converts one value at a time and merges the halves).
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+  uint32_t r;
+  asm("v_cvt_pk_bf16_f32 %0, %1, %2" : "=v"(r) : "v"(lo), "v"(hi));
+  return r;
 }
 
 // Max over the four 16-lane rows holding the same column (lanes l, l^16, l^32, l^48),

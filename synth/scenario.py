@@ -168,12 +168,14 @@ class TrainScenario:
         self.out = torch.empty((w.L, V, B, w.Hq, w.hd), dtype=dt, device=device)
         self.lse = torch.empty((w.L, V, B, w.Hq), dtype=torch.float32, device=device)
 
-    def forward(self):
-        """Carry rows of every anchored block, then the block attention of all of them."""
+    def forward(self, shared_prefix: bool = True):
+        """Carry rows of every anchored block, then the block attention of all of
+        them (blocks of one response share its pages: CO_ATTN_SHARED_PREFIX)."""
         co = self.co
         co.carryover_route(self.vdims, self.draft, self.target, co.CO_ROUTE_CARRY_ONLY,
                            self.vst, self.vrt)
         co.carryover_project_kv(self.vdims, self.W, self.hidden, self.vrt, self.vst, self.ws)
+        flags = co.CO_ATTN_SHARED_PREFIX if shared_prefix else 0
         co.drafter_block_attention(self.vdims, 0, self.w.L, self.q, self.vst, self.out, self.lse,
-                                   0, self.ws)
+                                   flags, self.ws)
         return self.out, self.lse

@@ -36,10 +36,12 @@ def _gpu():
     return Scenario
 
 
-def run_rounds(w, n_rounds, mode="carry", seqs=None, check_context=True, fold_e=True):
+def run_rounds(w, n_rounds, mode="carry", seqs=None, check_context=True, fold_e=True,
+               extra_flags=0):
     import paper_2609_14717_amd as co
     Scenario = _gpu()
-    print(f"[parity] workload={w.name} rounds={n_rounds} mode={mode} fold_e={fold_e}", flush=True)
+    print(f"[parity] workload={w.name} rounds={n_rounds} mode={mode} fold_e={fold_e} "
+          f"flags={extra_flags}", flush=True)
     sc = Scenario(w, fold_e=fold_e)
     orc = OracleRun(w, seqs=seqs)
     seqs = orc.seqs
@@ -49,7 +51,7 @@ def run_rounds(w, n_rounds, mode="carry", seqs=None, check_context=True, fold_e=
             gk, gv = gather_committed(sc.st, sc.pt, s, 0, 0, n)
             assert_heads_close(gk, orc.st.ck[s][0], TOL[w.dtype], "prefill K")
             assert_heads_close(gv, orc.st.cv[s][0], TOL[w.dtype], "prefill V")
-    flags = {"carry": 0, "baseline": co.CO_BASELINE_MODE}[mode]
+    flags = {"carry": 0, "baseline": co.CO_BASELINE_MODE}[mode] | extra_flags
     for r in range(n_rounds):
         hidden, q, draft, target, m = sc.round_inputs(r)
         out, lse = sc.new_output()
@@ -249,3 +251,55 @@ def test_train_fwd_sampled():
                 gk, gv = gather_committed(sc.st, sc.pt, s, layer, t0, t1)
                 assert_heads_close(gk, k[t0:t1, layer], tol, f"prefill K s{s}")
                 assert_heads_close(gv, vv[t0:t1, layer], tol, f"prefill V s{s}")
+
+
+# The grouped-prefix attention kernel on sequences with independent pages
+# (every group streamed per wavefront), a partial last group (70 sequences),
+# head_dim 128 with 32 query rows, and 64 query rows (served by the
+# persistent kernel whatever the flag says).
+SMALL_HD128_G2 = wl.Workload("small_hd128_g2", S=6, B=16, Dcat=512, d=256, L=2, Hq=4, Hkv=2,
+                             hd=128, dtype="bf16", theta=1e6, ctx_lo=700, ctx_hi=700,
+                             ctx_mode="projected", accept=("geom", 0.3), rounds=4, seed=0x5EED08)
+
+
+@pytest.mark.parametrize("split", ["", "1", "3"], ids=lambda v: f"share{v or 'dflt'}")
+@pytest.mark.parametrize("w", [SMALL_RAGGED, MANY_SEQS, SMALL_HD128_G2, SMALL_G4],
+                         ids=lambda w: w.name)
+def test_shared_prefix_flag_independent_pages(w, split, monkeypatch):
+    import paper_2609_14717_amd as co
+    if split:   # committed tiles per workgroup share: many shares, merged afterwards
+        monkeypatch.setenv("CO_ATTN_GROUP_SPLIT_TILES", split)
+    run_rounds(w, 2, extra_flags=co.CO_ATTN_SHARED_PREFIX)
+
+
+# A small training-shaped forward checked for every block: 2 responses of 512
+# positions, 10 anchored blocks each, so that groups of four blocks both share
+# a response's pages and straddle two responses.
+TRAIN_SMALL = wl.TRAIN_FWD.replace(name="train_small", S=2, seq_len=512, anchors=10,
+                                   seed=0x5EED09)
+
+
+@pytest.mark.parametrize("shared", [True, False], ids=["shared_prefix", "persistent"])
+@pytest.mark.parametrize("split", ["", "3"], ids=lambda v: f"share{v or 'dflt'}")
+def test_train_small_full(shared, split, monkeypatch):
+    if split:
+        monkeypatch.setenv("CO_ATTN_GROUP_SPLIT_TILES", split)
+    from helpers import OracleTrain
+    _gpu()
+    from synth.scenario import TrainScenario
+    import paper_2609_14717_amd as co
+    w = TRAIN_SMALL
+    tol = TOL[w.dtype]
+    V = w.S * w.anchors
+    print(f"[parity] workload={w.name} shared_prefix={shared}", flush=True)
+    sc = TrainScenario(w)
+    out, lse = sc.forward(shared_prefix=shared)
+    torch.cuda.synchronize()
+    assert co.carryover_read_status(sc.vst) == 0
+    orc = OracleTrain(w, range(V))
+    g = to_np(out)
+    gl = lse.cpu().numpy().astype(np.float64)
+    for v in range(V):
+        assert_heads_close(g[:, v], orc.O[:, v], tol, f"O v{v}")
+        err = np.abs(gl[:, v] - orc.LSE[:, v]).max()
+        assert err <= tol, f"LSE v{v}: {err}"
