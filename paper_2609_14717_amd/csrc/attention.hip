@@ -27,6 +27,7 @@
 //     per workgroup, which on this part writes back the L2 of the XCD.
 // fp32 path: per-chunk workgroups with plain VALU arithmetic through LDS.
 #include <stdlib.h>
+#include <string.h>
 
 #include "co_kernels.h"
 
@@ -1080,213 +1081,70 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
   }
 }
 
-// ------------------------------------------------ bf16 grouped-prefix path
+// ------------------------------------------------ bf16 32-key tile arithmetic
 //
-// Blocks anchored in one recorded response (the training-shaped forward,
-// Algorithm 2) are sequences whose committed keys are prefixes of the same
-// pages.  Under CO_ATTN_SHARED_PREFIX a workgroup takes four consecutive
-// sequences, one per wavefront, so that each key tile is read once for all of
-// their block queries:
-//   * the page ids of a chunk of pages are staged in LDS; the chunk is shared
-//     when every wavefront's pages agree with those of the longest sequence
-//     wherever its own keys reach;
-//   * shared chunks stream through a 4-deep ring of 32-key tiles, each
-//     wavefront loading one of a tile's four pages (K0, K1, V0, V1) with
-//     direct-to-LDS loads and a barrier publishing the tile; a wavefront skips
-//     tiles beyond its own length and masks the keys of its last one;
-//   * chunks that are not shared are streamed by each wavefront on its own;
-//   * the carry pages of each sequence come last; the result is normalised and
-//     written in place (no partial records).
-// Per tile the arithmetic is that of the persistent path (S^T = K . Q^T on
-// permuted keys, lazily rescaled online softmax, O^T += V^T . P^T).
-constexpr int kGroupSeqs = 4;       // sequences (wavefronts) per workgroup
-constexpr int kGroupChunk = 128;    // pages whose ids are staged at a time
-
-
-// Workgroups per CU the grouped kernel is built for (the second launch bound):
-// with head_dim 64 and 32 query rows it fits 168 VGPRs and about 35 KiB of
-// LDS, so three share a CU and hide each other's dependency latencies.
-//
-// Per tile the products use v_mfma_f32_32x32x16_bf16 on 32 keys x 32 query
-// rows.  S^T = K . Q^T takes K row rho from key pi(rho), pi swapping bits 2
-// and 3 of the key index; then lane l holds, for query l % 32, the keys
-// 8*(l/32) .. +7 of both pages of the tile (registers 0-7: page 0, 8-15:
-// page 1), which is exactly the B operand of O^T += V^T . P^T over those
-// keys, and V pages stored [head_dim][16 slots] give the matching A operand
-// with one 16-byte read.  The row maximum is a maximum over 16 registers and
-// one exchange between the two halves of the wavefront.
+// Used by the grouped-prefix kernel below.  One wavefront
+// owns NQT query tiles of 32 rows; the products use v_mfma_f32_32x32x16_bf16
+// on 32 keys x 32 query rows.  S^T = K . Q^T takes K row rho from key pi(rho),
+// pi swapping bits 2 and 3 of the key index; then lane l holds, for query
+// l % 32, the keys 8*(l/32) .. +7 of both pages of the tile (registers 0-7:
+// page 0, 8-15: page 1), which is exactly the B operand of O^T += V^T . P^T
+// over those keys, and V pages stored [head_dim][16 slots] give the matching
+// A operand with one 16-byte read.  The row maximum is a maximum over 16
+// registers and one exchange between the two halves of the wavefront.  A
+// tile in LDS is [K page 0][K page 1][V page 0][V page 1], K rows with their
+// 16-byte chunks XOR-swizzled by the slot.
 template <int HD, int NQT>
-__global__ __launch_bounds__(256, HD == 64 ? (NQT == 1 ? 3 : 2) : 1)
-void attn_group_kernel(AttnArgs a, int split_tiles, int n_splits) {
-  constexpr int KK = HD / 16, MO = HD / 32, NQP = NQT * 32;
-  constexpr int QLD = HD + 8;
-  constexpr int ROWB = HD * 2, CPR = ROWB / 16;
-  constexpr int PAGE_BYTES = kPage * ROWB, LPP = PAGE_BYTES / 1024;
-  constexpr int TILE_BYTES = 4 * PAGE_BYTES;
-  constexpr int NS = 4;                          // ring tiles; one per wavefront when private
-  constexpr float kRescale = 8.f;
-  static_assert(LPP * (NS - 1) < 64, "vmcnt");
-  // the rotated queries are staged in the ring before the first tile lands
-  constexpr int RING_BYTES = NS * TILE_BYTES;
-  constexpr int Q_BYTES = kGroupSeqs * NQP * QLD * 2;
-  __shared__ __align__(16) unsigned char ring[RING_BYTES > Q_BYTES ? RING_BYTES : Q_BYTES];
-  uint16_t* q_lds = reinterpret_cast<uint16_t*>(ring);
-  __shared__ int pid_lds[kGroupSeqs][kGroupChunk];
-  __shared__ double inv_lds[HD / 2];
-  __shared__ int npc_lds[kGroupSeqs];
-  __shared__ int mismatch;
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int half = lane >> 5, r32 = lane & 31;
-  const int G = a.Hq / a.Hkv, nq = a.B * G;
-  const int n_groups = (a.S + kGroupSeqs - 1) / kGroupSeqs;
-  // Workgroup ids are dealt to the 8 XCDs round-robin; renumbered, every XCD
-  // takes a run of consecutive groups, whose shared pages then stay in its L2.
-  int bx = blockIdx.x;
-  if ((gridDim.x & 7) == 0) bx = (bx & 7) * (gridDim.x >> 3) + (bx >> 3);
-  const int split = bx % n_splits;
-  const int group = n_groups - 1 - bx / n_splits;   // later blocks reach furthest
-  const int g = blockIdx.y, layer_local = blockIdx.z, layer = a.layer_begin + layer_local;
-  const int s = group * kGroupSeqs + wave;
-  const bool live = s < a.S;
-  const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
-  const uint16_t* vc = static_cast<const uint16_t*>(a.v_cache);
-  const uint16_t* kk = static_cast<const uint16_t*>(a.k_carry);
-  const uint16_t* vk = static_cast<const uint16_t*>(a.v_carry);
-  if (tid < HD / 2) inv_lds[tid] = a.rope_inv[tid] * kInv2Pi;
-
-  // this wavefront's sequence
-  int ctx = 0, carry = 0;
-  if (live) {
-    const SeqInfo si = seq_info(a, s, 1);
-    if (si.ok) {
-      ctx = si.ctx;
-      carry = si.carry;
-    } else if (lane == 0 && g == 0 && layer_local == 0) {
-      set_status(a.status, CO_ERR_LENGTH);
-    }
-  }
-  const int npc = (ctx + kPage - 1) / kPage;
-  if (lane == 0) npc_lds[wave] = npc;
-  if (tid == 0) mismatch = 0;
-  __syncthreads();   // inv_lds, npc_lds
-
-  int npc_max = 0, leader = 0;
-#pragma unroll
-  for (int v = 0; v < kGroupSeqs; ++v)
-    if (npc_lds[v] > npc_max) {
-      npc_max = npc_lds[v];
-      leader = v;
-    }
-  // this workgroup's share of the group's committed tiles; the last share also
-  // takes the carry keys.  Shares past the group's keys have nothing to do.
-  const int t_all = (npc_max + 1) / 2;
-  const int n_used = max(1, (t_all + split_tiles - 1) / split_tiles);
-  if (split >= n_used) return;   // uniform, and no barrier follows for this workgroup
-  const int t_beg = split * split_tiles, t_end = min(t_all, t_beg + split_tiles);
-  const bool last_share = split == n_used - 1;
-
-  // rotated, scaled queries of this wavefront -> LDS -> MFMA B fragments
-  {
-    const uint16_t* Q = static_cast<const uint16_t*>(a.q);
-    const bool rotate_q = !(a.flags & CO_Q_PREROTATED);
-    const float qscale = rsqrtf(static_cast<float>(HD)) * kLog2e;
-    uint16_t* qw = q_lds + wave * NQP * QLD;
-    for (int idx = lane; idx < NQP * (HD / 8); idx += 64) {
-      const int qn = idx / (HD / 8), p4 = (idx % (HD / 8)) * 4;
-      u16x4 lo4 = {0, 0, 0, 0}, hi4 = {0, 0, 0, 0};
-      if (live && qn < nq) {
-        const int64_t off = out_row(a, layer_local, s, g, qn, G) * HD + p4;
-        const u16x4 ql = *reinterpret_cast<const u16x4*>(Q + off);
-        const u16x4 qh = *reinterpret_cast<const u16x4*>(Q + off + HD / 2);
-        const int pos = ctx + qn / G;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float x = bf2f(ql[e]), y = bf2f(qh[e]);
-          if (rotate_q) {
-            float cs, sn;
-            rope_cos_sin_rev(pos, inv_lds[p4 + e], &cs, &sn);
-            const float x2 = x * cs - y * sn, y2 = y * cs + x * sn;
-            x = x2;
-            y = y2;
-          }
-          lo4[e] = f2bf(x * qscale);
-          hi4[e] = f2bf(y * qscale);
-        }
-      }
-      *reinterpret_cast<u16x4*>(qw + qn * QLD + p4) = lo4;
-      *reinterpret_cast<u16x4*>(qw + qn * QLD + p4 + HD / 2) = hi4;
-    }
-  }
-  __syncthreads();
-  u16x8 qf[NQT][KK];
-#pragma unroll
-  for (int qt = 0; qt < NQT; ++qt)
-#pragma unroll
-    for (int k = 0; k < KK; ++k)
-      qf[qt][k] = *reinterpret_cast<const u16x8*>(q_lds + (wave * NQP + qt * 32 + r32) * QLD +
-                                                   k * 16 + half * 8);
-
-  // fragment offsets within a tile.  K: row rho = lane % 32 holds key pi(rho);
-  // its 16-byte chunk 2k + lane/32 sits XOR-swizzled by the slot.  V: head
-  // dims 32m + lane % 32, keys 8*(lane/32) .. +7 of page j.
-  const int key = 16 * (r32 >> 4) + 8 * ((r32 >> 2) & 1) + 4 * ((r32 >> 3) & 1) + (r32 & 3);
-  const int kslot = key & 15;
-  uint32_t kf_off[KK];
-#pragma unroll
-  for (int k = 0; k < KK; ++k) {
-    const int ch = 2 * k + half;
-    kf_off[k] = (key >> 4) * PAGE_BYTES + kslot * ROWB + ((ch ^ (kslot & (CPR - 1))) << 4);
-  }
-  const uint32_t vf_off = 2 * PAGE_BYTES + r32 * 32 + half * 16;
-  const int slot_base = 8 * half;   // the slots of each page this lane's scores cover
-  // per-lane source offsets (elements) of the loads of one page: K rows land
-  // XOR-swizzled, V pages are copied as they are
-  int k_off[LPP], v_off[LPP];
-#pragma unroll
-  for (int q = 0; q < LPP; ++q) {
-    const int byte = q * 1024 + lane * 16;
-    const int r = byte / ROWB, pch = (byte % ROWB) / 16;
-    k_off[q] = r * HD + (pch ^ (r & (CPR - 1))) * 8;
-    v_off[q] = byte / 2;
-  }
-  const uint32_t ring_lds = lds_addr(ring);
-  // one page (K or V) of a committed page id, or of carry page cp of this
-  // sequence, or a harmless dummy (id < 0) -> LDS
-  // page `phys` of this layer and KV head: base + phys * page_stride elements
-  const int64_t page_stride = static_cast<int64_t>(a.Hkv) * kPage * HD;
-  const int64_t head0 = (static_cast<int64_t>(layer) * a.num_pages * a.Hkv + g) * (kPage * HD);
-  const uint16_t* kbase = kc + head0;
-  const uint16_t* vbase = vc + head0;
-  auto load_page = [&](bool is_v, int phys, uint32_t dst) {
-    const uint16_t* src = is_v ? vk : kk;   // dummy: carry page 0 of layer 0
-    if (phys >= 0) src = (is_v ? vbase : kbase) + phys * page_stride;
-#pragma unroll
-    for (int q = 0; q < LPP; ++q)
-      lds_dma16_opaque(src + (is_v ? v_off[q] : k_off[q]), dst + q * 1024);
-  };
-  auto load_carry_page = [&](bool is_v, int cp, uint32_t dst) {
-    const int64_t row = ((static_cast<int64_t>(layer) * a.S + s) * a.CP + cp) * a.Hkv + g;
-    const uint16_t* src = (is_v ? vk : kk) + row * (kPage * HD);
-#pragma unroll
-    for (int q = 0; q < LPP; ++q)
-      lds_dma16_opaque(src + (is_v ? v_off[q] : k_off[q]), dst + q * 1024);
-  };
+struct Tile32 {
+  static constexpr int KK = HD / 16, MO = HD / 32;
+  static constexpr int ROWB = HD * 2, CPR = ROWB / 16;
+  static constexpr int PAGE_BYTES = kPage * ROWB, LPP = PAGE_BYTES / 1024;
+  static constexpr int TILE_BYTES = 4 * PAGE_BYTES;
+  static constexpr int QLD = HD + 8;             // padded LDS row of staged queries (bf16)
+  static constexpr float kRescale = 8.f;         // lazy rescale threshold (log2 units)
 
   f32x16 o[NQT][MO];
   float m_run[NQT], l_run[NQT];   // l_run: this half-wavefront's keys (summed at the end)
+  u16x8 qf[NQT][16 > KK ? KK : KK];
+  uint32_t kf_off[KK], vf_off;
+  int slot_base, half, r32;
+
+  __device__ void setup(int lane) {
+    half = lane >> 5;
+    r32 = lane & 31;
+    const int key = 16 * (r32 >> 4) + 8 * ((r32 >> 2) & 1) + 4 * ((r32 >> 3) & 1) + (r32 & 3);
+    const int kslot = key & 15;
 #pragma unroll
-  for (int qt = 0; qt < NQT; ++qt) {
+    for (int k = 0; k < KK; ++k) {
+      const int ch = 2 * k + half;
+      kf_off[k] = (key >> 4) * PAGE_BYTES + kslot * ROWB + ((ch ^ (kslot & (CPR - 1))) << 4);
+    }
+    vf_off = 2 * PAGE_BYTES + r32 * 32 + half * 16;
+    slot_base = 8 * half;
 #pragma unroll
-    for (int m = 0; m < MO; ++m)
+    for (int qt = 0; qt < NQT; ++qt) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[qt][m][r] = 0.f;
-    m_run[qt] = -INFINITY;
-    l_run[qt] = 0.f;
+      for (int m = 0; m < MO; ++m)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[qt][m][r] = 0.f;
+      m_run[qt] = -INFINITY;
+      l_run[qt] = 0.f;
+    }
   }
-  // one 32-key tile at tb: n0 / n1 valid keys in its two pages
-  auto tile = [&](const unsigned char* tb, int n0, int n1) {
+
+  // B fragments of the staged queries: rows qt * 32 + lane % 32 of `rows`
+  __device__ void load_q(const uint16_t* rows) {
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+      for (int k = 0; k < KK; ++k)
+        qf[qt][k] = *reinterpret_cast<const u16x8*>(rows + (qt * 32 + r32) * QLD + k * 16 + half * 8);
+  }
+
+  // one 32-key tile at tb: n0 / n1 valid keys in its two pages.  Scores are
+  // formed relative to the running reference (accumulators start at -base),
+  // then one rescale decision for the tile, the exponentials and the PV products.
+  __device__ void step(const unsigned char* tb, int n0, int n1) {
     const bool partial = n0 < kPage || n1 < kPage;
     u16x8 kf[KK], vf[MO][2];
 #pragma unroll
@@ -1296,7 +1154,6 @@ void attn_group_kernel(AttnArgs a, int split_tiles, int n_splits) {
 #pragma unroll
       for (int j = 0; j < 2; ++j)
         vf[m][j] = *reinterpret_cast<const u16x8*>(tb + vf_off + j * PAGE_BYTES + m * 32 * 32);
-    // scores relative to the running reference: the accumulators start at -base
     f32x16 sc[NQT];
     float base[NQT];
 #pragma unroll
@@ -1374,9 +1231,251 @@ void attn_group_kernel(AttnArgs a, int split_tiles, int n_splits) {
       for (int m = 0; m < MO; ++m)
 #pragma unroll
         for (int qt = 0; qt < NQT; ++qt) o[qt][m] = mfma32x32x16(vf[m][j], pk[qt][j], o[qt][m]);
+  }
+
+  // query tile qt: normalised output rows (bf16) and LSE; rows >= nq skipped
+  __device__ void write_out(const AttnArgs& a, int layer_local, int s, int g, int qrow0, int nq) {
+    uint16_t* out = static_cast<uint16_t*>(a.out);
+    const int G = a.Hq / a.Hkv;
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
+      const float l_tot = l_run[qt] + __shfl_xor(l_run[qt], 32);
+      const int qn = qrow0 + qt * 32 + r32;
+      if (qn >= nq) continue;
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      const int64_t row = out_row(a, layer_local, s, g, qn, G);
+#pragma unroll
+      for (int m = 0; m < MO; ++m)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          u16x4 v;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) v[c] = f2bf(o[qt][m][4 * r4 + c] * inv);
+          *reinterpret_cast<u16x4*>(out + row * HD + 32 * m + 8 * r4 + 4 * half) = v;
+        }
+      if (a.lse && half == 0)
+        a.lse[row] = l_tot > 0.f ? (m_run[qt] + log2f(l_tot)) * kLn2 : -INFINITY;
+    }
+  }
+
+  // unnormalised record rows qrow0 .. of a share: O[nqp][HD], m[nqp], l[nqp]
+  __device__ void write_record(float* rec, int nqp, int qrow0) {
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
+      const float l_tot = l_run[qt] + __shfl_xor(l_run[qt], 32);
+      const int qn = qrow0 + qt * 32 + r32;
+#pragma unroll
+      for (int m = 0; m < MO; ++m)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          f32x4 v;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) v[c] = o[qt][m][4 * r4 + c];
+          *reinterpret_cast<f32x4*>(rec + qn * HD + 32 * m + 8 * r4 + 4 * half) = v;
+        }
+      if (half == 0) {
+        rec[nqp * HD + qn] = m_run[qt];
+        rec[nqp * HD + nqp + qn] = l_tot;
+      }
+    }
+  }
+};
+
+// Rotated (at position ctx + query / G), scaled (1/sqrt(hd), log2 units) bf16
+// queries of rows qrow0 .. qrow0 + nrows - 1 of sequence s into LDS rows
+// [nrows][HD + 8]; rows past the block are zero.  One wavefront.
+template <int HD>
+__device__ void stage_queries(const AttnArgs& a, uint16_t* rows, int nrows, int qrow0, bool live,
+                              int s, int g, int layer_local, int ctx, const double* inv_rev,
+                              int lane) {
+  constexpr int QLD = HD + 8;
+  const int G = a.Hq / a.Hkv, nq = a.B * G;
+  const uint16_t* Q = static_cast<const uint16_t*>(a.q);
+  const bool rotate_q = !(a.flags & CO_Q_PREROTATED);
+  const float qscale = rsqrtf(static_cast<float>(HD)) * kLog2e;
+  for (int idx = lane; idx < nrows * (HD / 8); idx += 64) {
+    const int r = idx / (HD / 8), p4 = (idx % (HD / 8)) * 4;
+    const int qn = qrow0 + r;
+    u16x4 lo4 = {0, 0, 0, 0}, hi4 = {0, 0, 0, 0};
+    if (live && qn < nq) {
+      const int64_t off = out_row(a, layer_local, s, g, qn, G) * HD + p4;
+      const u16x4 ql = *reinterpret_cast<const u16x4*>(Q + off);
+      const u16x4 qh = *reinterpret_cast<const u16x4*>(Q + off + HD / 2);
+      const int pos = ctx + qn / G;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float x = bf2f(ql[e]), y = bf2f(qh[e]);
+        if (rotate_q) {
+          float cs, sn;
+          rope_cos_sin_rev(pos, inv_rev[p4 + e], &cs, &sn);
+          const float x2 = x * cs - y * sn, y2 = y * cs + x * sn;
+          x = x2;
+          y = y2;
+        }
+        lo4[e] = f2bf(x * qscale);
+        hi4[e] = f2bf(y * qscale);
+      }
+    }
+    *reinterpret_cast<u16x4*>(rows + r * QLD + p4) = lo4;
+    *reinterpret_cast<u16x4*>(rows + r * QLD + p4 + HD / 2) = hi4;
+  }
+}
+
+// Keys of page-pair t (pages 2t, 2t+1) below `limit`: the two page counts.
+__device__ __forceinline__ int keys_in(int limit, int t, int h) {
+  return min(kPage, max(0, limit - (2 * t + h) * kPage));
+}
+
+// Committed tiles per share of a grouped launch (CO_ATTN_GROUP_SPLIT_TILES
+// overrides it for tuning and tests), and the number of shares that covers the
+// longest sequence the page table allows.
+constexpr int kGroupSplitTiles = 128;
+int group_split_tiles() {
+  if (const char* env = getenv("CO_ATTN_GROUP_SPLIT_TILES")) {
+    const int v = atoi(env);
+    if (v >= 1 && v <= 4096) return v;
+  }
+  return kGroupSplitTiles;
+}
+int group_splits(int max_pages) {
+  const int tiles = (max_pages + 1) / 2, sp = group_split_tiles();
+  return max(1, (tiles + sp - 1) / sp);
+}
+
+// Record of (layer, KV head, sequence, share) in the workspace.
+__device__ __forceinline__ float* share_record(const AttnArgs& a, int layer_local, int g, int s,
+                                               int n_splits, int split, int nqp, int hd) {
+  return a.ws + ((((static_cast<int64_t>(layer_local) * a.Hkv + g) * a.S + s) * n_splits + split) *
+                 (static_cast<int64_t>(nqp) * (hd + 2)));
+}
+
+// ------------------------------------------------ bf16 grouped-prefix path
+//
+// Blocks anchored in one recorded response (the training-shaped forward,
+// Algorithm 2) are sequences whose committed keys are prefixes of the same
+// pages.  Under CO_ATTN_SHARED_PREFIX a workgroup takes four consecutive
+// sequences, one per wavefront, so that each key tile is read once for all of
+// their block queries:
+//   * the page ids of a chunk of pages are staged in LDS; the chunk is shared
+//     when every wavefront's pages agree with those of the longest sequence
+//     wherever its own keys reach;
+//   * shared chunks stream through a 4-deep ring of 32-key tiles, each
+//     wavefront loading one of a tile's four pages (K0, K1, V0, V1) with
+//     direct-to-LDS loads and a barrier publishing the tile; a wavefront skips
+//     tiles beyond its own length and masks the keys of its last one;
+//   * chunks that are not shared are streamed by each wavefront on its own;
+//   * the carry pages of each sequence come last; the result is normalised and
+//     written in place, or, when the group's keys are split into shares, each
+//     share leaves a record that the merge kernel combines.
+// With head_dim 64 and 32 query rows a workgroup fits 168 VGPRs and about 35
+// KiB of LDS, so three share a CU and hide each other's dependency latencies.
+constexpr int kGroupSeqs = 4;       // sequences (wavefronts) per workgroup
+constexpr int kGroupChunk = 128;    // pages whose ids are staged at a time
+
+template <int HD, int NQT>
+__global__ __launch_bounds__(256, HD == 64 ? (NQT == 1 ? 3 : 2) : 1)
+void attn_group_kernel(AttnArgs a, int split_tiles, int n_splits) {
+  using TT = Tile32<HD, NQT>;
+  constexpr int NQP = NQT * 32, QLD = TT::QLD;
+  constexpr int PAGE_BYTES = TT::PAGE_BYTES, LPP = TT::LPP, TILE_BYTES = TT::TILE_BYTES;
+  constexpr int NS = 4;                          // ring tiles; one per wavefront when private
+  static_assert(LPP * (NS - 1) < 64, "vmcnt");
+  // the rotated queries are staged in the ring before the first tile lands
+  constexpr int RING_BYTES = NS * TILE_BYTES;
+  constexpr int Q_BYTES = kGroupSeqs * NQP * QLD * 2;
+  __shared__ __align__(16) unsigned char ring[RING_BYTES > Q_BYTES ? RING_BYTES : Q_BYTES];
+  uint16_t* q_lds = reinterpret_cast<uint16_t*>(ring);
+  __shared__ int pid_lds[kGroupSeqs][kGroupChunk];
+  __shared__ double inv_lds[HD / 2];
+  __shared__ int npc_lds[kGroupSeqs];
+  __shared__ int mismatch;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n_groups = (a.S + kGroupSeqs - 1) / kGroupSeqs;
+  // Workgroup ids are dealt to the 8 XCDs round-robin; renumbered, every XCD
+  // takes a run of consecutive groups, whose shared pages then stay in its L2.
+  int bx = blockIdx.x;
+  if ((gridDim.x & 7) == 0) bx = (bx & 7) * (gridDim.x >> 3) + (bx >> 3);
+  const int split = bx % n_splits;
+  const int group = n_groups - 1 - bx / n_splits;   // later blocks reach furthest
+  const int g = blockIdx.y, layer_local = blockIdx.z, layer = a.layer_begin + layer_local;
+  const int s = group * kGroupSeqs + wave;
+  const bool live = s < a.S;
+  const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
+  const uint16_t* vc = static_cast<const uint16_t*>(a.v_cache);
+  const uint16_t* kk = static_cast<const uint16_t*>(a.k_carry);
+  const uint16_t* vk = static_cast<const uint16_t*>(a.v_carry);
+  if (tid < HD / 2) inv_lds[tid] = a.rope_inv[tid] * kInv2Pi;
+
+  // this wavefront's sequence
+  int ctx = 0, carry = 0;
+  if (live) {
+    const SeqInfo si = seq_info(a, s, 1);
+    if (si.ok) {
+      ctx = si.ctx;
+      carry = si.carry;
+    } else if (lane == 0 && g == 0 && layer_local == 0) {
+      set_status(a.status, CO_ERR_LENGTH);
+    }
+  }
+  const int npc = (ctx + kPage - 1) / kPage;
+  if (lane == 0) npc_lds[wave] = npc;
+  if (tid == 0) mismatch = 0;
+  __syncthreads();   // inv_lds, npc_lds
+
+  int npc_max = 0, leader = 0;
+#pragma unroll
+  for (int v = 0; v < kGroupSeqs; ++v)
+    if (npc_lds[v] > npc_max) {
+      npc_max = npc_lds[v];
+      leader = v;
+    }
+  // this workgroup's share of the group's committed tiles; the last share also
+  // takes the carry keys.  Shares past the group's keys have nothing to do.
+  const int t_all = (npc_max + 1) / 2;
+  const int n_used = max(1, (t_all + split_tiles - 1) / split_tiles);
+  if (split >= n_used) return;   // uniform, and no barrier follows for this workgroup
+  const int t_beg = split * split_tiles, t_end = min(t_all, t_beg + split_tiles);
+  const bool last_share = split == n_used - 1;
+
+  stage_queries<HD>(a, q_lds + wave * NQP * QLD, NQP, 0, live, s, g, layer_local, ctx, inv_lds,
+                    lane);
+  __syncthreads();
+  TT T;
+  T.setup(lane);
+  T.load_q(q_lds + wave * NQP * QLD);
+
+  // per-lane source offsets (elements) of the loads of one page: K rows land
+  // XOR-swizzled, V pages are copied as they are
+  int k_off[LPP], v_off[LPP];
+#pragma unroll
+  for (int q = 0; q < LPP; ++q) {
+    const int byte = q * 1024 + lane * 16;
+    const int r = byte / TT::ROWB, pch = (byte % TT::ROWB) / 16;
+    k_off[q] = r * HD + (pch ^ (r & (TT::CPR - 1))) * 8;
+    v_off[q] = byte / 2;
+  }
+  const uint32_t ring_lds = lds_addr(ring);
+  // page `phys` of this layer and KV head: base + phys * page_stride elements
+  const int64_t page_stride = static_cast<int64_t>(a.Hkv) * kPage * HD;
+  const int64_t head0 = (static_cast<int64_t>(layer) * a.num_pages * a.Hkv + g) * (kPage * HD);
+  const uint16_t* kbase = kc + head0;
+  const uint16_t* vbase = vc + head0;
+  // one page (K or V) of a committed page id, or a harmless dummy (id < 0) -> LDS
+  auto load_page = [&](bool is_v, int phys, uint32_t dst) {
+    const uint16_t* src = is_v ? vk : kk;   // dummy: carry page 0 of layer 0
+    if (phys >= 0) src = (is_v ? vbase : kbase) + phys * page_stride;
+#pragma unroll
+    for (int q = 0; q < LPP; ++q)
+      lds_dma16_opaque(src + (is_v ? v_off[q] : k_off[q]), dst + q * 1024);
   };
-  auto valid = [&](int limit, int t, int half_) {
-    return min(kPage, max(0, limit - (2 * t + half_) * kPage));
+  auto load_carry_page = [&](bool is_v, int cp, uint32_t dst) {
+    const int64_t row = ((static_cast<int64_t>(layer) * a.S + s) * a.CP + cp) * a.Hkv + g;
+    const uint16_t* src = (is_v ? vk : kk) + row * (kPage * HD);
+#pragma unroll
+    for (int q = 0; q < LPP; ++q)
+      lds_dma16_opaque(src + (is_v ? v_off[q] : k_off[q]), dst + q * 1024);
   };
 
   // ---- committed keys of this share, chunk by chunk
@@ -1416,10 +1515,10 @@ void attn_group_kernel(AttnArgs a, int split_tiles, int n_splits) {
     };
     // keys of tile t in this wavefront: [32t, 32t + 32) clipped to ctx, and pages
     // whose id was rejected hold no valid keys
-    auto keys = [&](int t, int half_) {
-      const int p = 2 * t + half_ - c0;
+    auto keys = [&](int t, int h) {
+      const int p = 2 * t + h - c0;
       if (p >= cn || pid_of(my0, my1, p) < 0) return 0;
-      return valid(ctx, t, half_);
+      return keys_in(ctx, t, h);
     };
     if (!mismatch) {
       // shared: wavefront w loads page w of each tile (K0, K1, V0, V1) of the leader
@@ -1436,7 +1535,7 @@ void attn_group_kernel(AttnArgs a, int split_tiles, int n_splits) {
         else wait_vm_lgkm_barrier<0>();
         if (t + NS - 1 < t1) issue(t + NS - 1);   // into the slot of tile t-1, read by all
         const int n0 = keys(t, 0), n1 = keys(t, 1);
-        if (n0 + n1 > 0) tile(ring + (t % NS) * TILE_BYTES, n0, n1);
+        if (n0 + n1 > 0) T.step(ring + (t % NS) * TILE_BYTES, n0, n1);
       }
     } else {
       // pages differ between the sequences: each wavefront on its own, one slot each
@@ -1453,7 +1552,7 @@ void attn_group_kernel(AttnArgs a, int split_tiles, int n_splits) {
         }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         const int n0 = keys(t, 0), n1 = keys(t, 1);
-        if (n0 + n1 > 0) tile(ring + wave * TILE_BYTES, n0, n1);
+        if (n0 + n1 > 0) T.step(ring + wave * TILE_BYTES, n0, n1);
       }
     }
   }
@@ -1472,74 +1571,36 @@ void attn_group_kernel(AttnArgs a, int split_tiles, int n_splits) {
         load_carry_page(true, cp, slot + (2 + h) * PAGE_BYTES);
       }
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      tile(ring + wave * TILE_BYTES, valid(carry, t, 0), valid(carry, t, 1));
+      T.step(ring + wave * TILE_BYTES, keys_in(carry, t, 0), keys_in(carry, t, 1));
     }
   }
 
   // ---- normalise and write, or leave this share's record for the merge
   if (!live) return;
-  if (n_used > 1) {
-    float* rec = a.ws + ((((static_cast<int64_t>(layer_local) * a.Hkv + g) * a.S + s) * n_splits +
-                          split) * (NQP * (HD + 2)));
-#pragma unroll
-    for (int qt = 0; qt < NQT; ++qt) {
-      const float l_tot = l_run[qt] + __shfl_xor(l_run[qt], 32);
-      const int qn = qt * 32 + r32;
-#pragma unroll
-      for (int m = 0; m < MO; ++m)
-#pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          f32x4 v;
-#pragma unroll
-          for (int c = 0; c < 4; ++c) v[c] = o[qt][m][4 * r4 + c];
-          *reinterpret_cast<f32x4*>(rec + qn * HD + 32 * m + 8 * r4 + 4 * half) = v;
-        }
-      if (half == 0) {
-        rec[NQP * HD + qn] = m_run[qt];
-        rec[NQP * HD + NQP + qn] = l_tot;
-      }
-    }
-    return;
-  }
-  uint16_t* out = static_cast<uint16_t*>(a.out);
-#pragma unroll
-  for (int qt = 0; qt < NQT; ++qt) {
-    const float l_tot = l_run[qt] + __shfl_xor(l_run[qt], 32);
-    const int qn = qt * 32 + r32;
-    if (qn >= nq) continue;
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    const int64_t row = out_row(a, layer_local, s, g, qn, G);
-#pragma unroll
-    for (int m = 0; m < MO; ++m)
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        u16x4 v;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) v[c] = f2bf(o[qt][m][4 * r4 + c] * inv);
-        *reinterpret_cast<u16x4*>(out + row * HD + 32 * m + 8 * r4 + 4 * half) = v;
-      }
-    if (a.lse && half == 0)
-      a.lse[row] = l_tot > 0.f ? (m_run[qt] + log2f(l_tot)) * kLn2 : -INFINITY;
-  }
+  if (n_used > 1)
+    T.write_record(share_record(a, layer_local, g, s, n_splits, split, NQP, HD), NQP, 0);
+  else
+    T.write_out(a, layer_local, s, g, 0, a.B * (a.Hq / a.Hkv));
 }
 
 // Merge of the shares of a grouped launch (log-sum-exp rule), for sequences
-// whose group needed more than one share: one thread per (query row, 4 dims).
+// whose keys took more than one share: one thread per (query row, 4 dims).
+// A share count follows from the longest committed length among the
+// `group` consecutive sequences that shared a workgroup.
 template <int HD>
-__global__ __launch_bounds__(256) void attn_group_merge_kernel(AttnArgs a, int split_tiles,
-                                                               int n_splits, int nqp) {
+__global__ __launch_bounds__(256) void attn_share_merge_kernel(AttnArgs a, int split_tiles,
+                                                               int n_splits, int nqp, int group) {
   const int s = blockIdx.x, g = blockIdx.y, layer_local = blockIdx.z;
   const int G = a.Hq / a.Hkv, nq = a.B * G;
   int npc_max = 0;
-  const int g0 = s / kGroupSeqs * kGroupSeqs;
-  for (int v = g0; v < min(g0 + kGroupSeqs, a.S); ++v) {
+  const int g0 = s / group * group;
+  for (int v = g0; v < min(g0 + group, a.S); ++v) {
     const SeqInfo si = seq_info(a, v, 1);
     if (si.ok) npc_max = max(npc_max, si.npc);
   }
   const int n_used = max(1, ((npc_max + 1) / 2 + split_tiles - 1) / split_tiles);
   if (n_used <= 1) return;   // written by the attention kernel
-  const float* base = a.ws + (((static_cast<int64_t>(layer_local) * a.Hkv + g) * a.S + s) *
-                              n_splits) * (nqp * (HD + 2));
+  const float* base = share_record(a, layer_local, g, s, n_splits, 0, nqp, HD);
   const int64_t rec = static_cast<int64_t>(nqp) * (HD + 2);
   uint16_t* out = static_cast<uint16_t*>(a.out);
   for (int idx = threadIdx.x; idx < nq * (HD / 4); idx += 256) {
@@ -1563,22 +1624,6 @@ __global__ __launch_bounds__(256) void attn_group_merge_kernel(AttnArgs a, int s
     *reinterpret_cast<u16x4*>(out + row * HD + d) = v;
     if (a.lse && d == 0) a.lse[row] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
   }
-}
-
-// Committed tiles per share of a grouped launch (CO_ATTN_GROUP_SPLIT_TILES
-// overrides it for tuning and tests), and the number of shares that covers the
-// longest sequence the page table allows.
-constexpr int kGroupSplitTiles = 128;
-int group_split_tiles() {
-  if (const char* env = getenv("CO_ATTN_GROUP_SPLIT_TILES")) {
-    const int v = atoi(env);
-    if (v >= 1 && v <= 4096) return v;
-  }
-  return kGroupSplitTiles;
-}
-int group_splits(int max_pages) {
-  const int tiles = (max_pages + 1) / 2, sp = group_split_tiles();
-  return max(1, (tiles + sp - 1) / sp);
 }
 
 }  // namespace
@@ -1627,7 +1672,7 @@ AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pa
     p.bytes = static_cast<size_t>(L) * S * Hkv * p.n_chunks * p.nq_pad * (hd + 2) * 4;
   }
   if (dtype == CO_DTYPE_BF16) {
-    // records of the grouped-prefix path (CO_ATTN_SHARED_PREFIX), where it applies
+    // share records of the grouped-prefix path (CO_ATTN_SHARED_PREFIX), where it applies
     const int nq = B * (Hq / Hkv);
     if (hd == 64 || nq <= 32) {
       const size_t nqp = nq <= 32 ? 32 : 64;
@@ -1646,7 +1691,8 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
   const int items = (a.B * (a.Hq / a.Hkv)) * (a.hd / 4);
   const dim3 mgrid(a.S, layer_count * a.Hkv, (items + 255) / 256);
   // grouped kernel: any query count with head_dim 64, up to 32 rows with 128
-  const bool one = a.B * (a.Hq / a.Hkv) <= 32;
+  const int nq = a.B * (a.Hq / a.Hkv);
+  const bool one = nq <= 32;
   if (a.dtype == CO_DTYPE_BF16 && (a.flags & CO_ATTN_SHARED_PREFIX) && (a.hd == 64 || one)) {
     const int ns = group_splits(a.max_pages);
     const dim3 ggrid((a.S + kGroupSeqs - 1) / kGroupSeqs * ns, a.Hkv, layer_count);
@@ -1662,9 +1708,9 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
     const dim3 cgrid(a.S, a.Hkv, layer_count);
     const int nqp = one ? 32 : 64;
     if (a.hd == 64)
-      hipLaunchKernelGGL(attn_group_merge_kernel<64>, cgrid, dim3(256), 0, stream, a, sp, ns, nqp);
+      hipLaunchKernelGGL(attn_share_merge_kernel<64>, cgrid, dim3(256), 0, stream, a, sp, ns, nqp, kGroupSeqs);
     else
-      hipLaunchKernelGGL(attn_group_merge_kernel<128>, cgrid, dim3(256), 0, stream, a, sp, ns, nqp);
+      hipLaunchKernelGGL(attn_share_merge_kernel<128>, cgrid, dim3(256), 0, stream, a, sp, ns, nqp, kGroupSeqs);
     return hipGetLastError();
   }
   if (a.dtype == CO_DTYPE_BF16) {
