@@ -42,7 +42,8 @@ PROFILES = os.path.join(ROOT, "profiles")
 # of these are not reported
 ATTN_SOURCES = [os.path.join(ROOT, "paper_2609_14717_amd", "csrc", f)
                 for f in ("attention.hip", "co_device.h", "co_kernels.h")]
-ATTN_KERNELS = ("attn_bf16_kernel", "attn_bf16_combine_kernel")
+ATTN_KERNELS = ("attn_bf16_kernel", "attn_bf16_combine_kernel", "attn_group_kernel",
+                "attn_share_merge_kernel")
 
 
 def parse():
@@ -153,6 +154,8 @@ def summarize_pmc(args):
              f"copy WRITE_SIZE KiB: {cw:.1f}  (factor {w_fac:.4f})"]
     tot = 0.0
     for kn in ATTN_KERNELS:
+        if not any(k[1] == "FETCH_SIZE" and kn in k[0] for k in fetch):
+            continue                            # a kernel this workload does not launch
         kf, nf = one(fetch, "FETCH_SIZE", kn)
         kw, nw = one(write, "WRITE_SIZE", kn)
         b = kf * 1024.0 * f_fac + kw * 1024.0 * w_fac
@@ -377,15 +380,7 @@ def main():
 
     proj_s = timed_calls(torch, stream, min(args.steps, 100), project)
     pflops, pbytes = projection_work(w, w.S * w.B)
-    if args.calibrate_copy_mb > 0:
-        from synth import device as sdev
-        nb = args.calibrate_copy_mb << 20
-        src = torch.ones(nb // 4, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        sdev.copy_bytes(dst, src, nb)
-        torch.cuda.synchronize()
-        del src, dst
+    calibrate_copy(torch, args)
 
     metric = ("drafter rounds/s (block-16) at batch 32" if w.name == "ragged_batch32"
               else f"drafter rounds/s ({w.name})")
@@ -420,6 +415,21 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w.replace(rounds=w.rounds), args.cpu_baseline_seconds)
     print(json.dumps(result), flush=True)
+
+
+def calibrate_copy(torch, args):
+    """One plain copy of --calibrate-copy-mb MiB: the reference dispatch that the
+    HBM counters of a --pmc run are scaled by."""
+    if args.calibrate_copy_mb <= 0:
+        return
+    from synth import device as sdev
+    nb = args.calibrate_copy_mb << 20
+    src = torch.ones(nb // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    sdev.copy_bytes(dst, src, nb)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def run_train(args, w):
@@ -461,6 +471,7 @@ def run_train(args, w):
     aflops = attention_flops(vw, keys)
     pflops, pbytes = projection_work(vw, V * w.B)
     atfl = aflops / att_s / 1e12
+    calibrate_copy(torch, args)
     result = {
         "metric": f"training-shaped forwards/s ({w.name})",
         "value": args.steps / dt,
@@ -481,7 +492,7 @@ def run_train(args, w):
         "roofline": {"bound": "mfma", "kernel": "drafter_block_attention, shared prefixes "
                      "(attn_group_kernel)", "achieved": atfl,
                      "peak": MFMA_PEAK_TFLOPS[w.dtype], "unit": "TFLOP/s",
-                     "frac": atfl / MFMA_PEAK_TFLOPS[w.dtype], "traffic": None,
+                     "frac": atfl / MFMA_PEAK_TFLOPS[w.dtype], "traffic": recorded_traffic(w.name),
                      "algorithmic_flops_per_launch": aflops, "avg_launch_us": att_s * 1e6},
         "projection": projection_result(vw, pflops, pbytes, proj_s),
     }
