@@ -44,6 +44,9 @@ ATTN_SOURCES = [os.path.join(ROOT, "paper_2609_14717_amd", "csrc", f)
                 for f in ("attention.hip", "co_device.h", "co_kernels.h")]
 ATTN_KERNELS = ("attn_bf16_kernel", "attn_bf16_combine_kernel", "attn_group_kernel",
                 "attn_share_merge_kernel")
+ATTN_WARM = 5       # untimed attention calls before the timed ones
+COLD_CALLS = 50     # cold calls timed (each after a cache scrub)
+TRAIN_ATTN_WARM = 3
 
 
 def parse():
@@ -98,9 +101,19 @@ def recorded_traffic(workload):
         return None
 
 
-def _counter_means(run_dir, last=0):
-    """Mean counter value per dispatch, per kernel name, from a --pmc run; with
-    ``last`` > 0 over the last ``last`` dispatches of each kernel only."""
+def attention_window(args):
+    """(first, count): the timed stand-alone attention calls among each attention
+    kernel's dispatches, in the order bench.py launches them (one dispatch of
+    each of the call's kernels per call)."""
+    from synth import workloads as wl
+    if wl.WORKLOADS[args.workload].anchors:
+        return args.warmup + args.steps + TRAIN_ATTN_WARM, min(args.steps, 100)
+    return args.warmup + args.steps + ATTN_WARM, args.steps
+
+
+def _counter_values(run_dir):
+    """Counter value of every dispatch, in dispatch order, per (kernel name,
+    counter), from a --pmc run."""
     import glob
     files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
     if not files:
@@ -112,43 +125,43 @@ def _counter_means(run_dir, last=0):
                 per = acc.setdefault((r["Kernel_Name"], r["Counter_Name"]), {})
                 did = r["Dispatch_Id"]
                 per[did] = per.get(did, 0.0) + float(r["Counter_Value"])
-    out = {}
-    for k, v in acc.items():
-        vals = [v[d] for d in sorted(v, key=int)]
-        if last > 0:
-            vals = vals[-last:]
-        out[k] = (sum(vals) / len(vals), len(vals))
-    return out
+    return {k: [v[d] for d in sorted(v, key=int)] for k, v in acc.items()}
 
 
 def summarize_pmc(args):
-    # the attention kernels' last --steps dispatches are the timed attention calls
-    fetch = _counter_means(args.summarize_pmc[0], args.steps)
-    write = _counter_means(args.summarize_pmc[1], args.steps)
+    win = attention_window(args)
+    fetch = _counter_values(args.summarize_pmc[0])
+    write = _counter_values(args.summarize_pmc[1])
     copy_bytes = args.calibrate_copy_mb * (1 << 20)
     if copy_bytes <= 0:
         raise SystemExit("--calibrate-copy-mb must give the copy size of the profiled runs")
 
-    def pick(table, counter, pattern):
-        rows = [(k[0], v) for k, v in table.items() if k[1] == counter and pattern in k[0]]
+    def one(table, counter, name, window=None):
+        """Sum over the kernels matching ``name`` of the mean per dispatch (over
+        the window of dispatches if given), and the dispatches averaged."""
+        rows = [v for k, v in table.items() if k[1] == counter and name in k[0]]
         if not rows:
-            raise SystemExit(f"no {counter} rows for {pattern}")
-        return rows
-
-    def one(table, counter, name):
-        rows = pick(table, counter, name)
-        return sum(v[0] for _, v in rows), sum(v[1] for _, v in rows)
+            raise SystemExit(f"no {counter} rows for {name}")
+        tot, cnt = 0.0, 0
+        for vals in rows:
+            if window is not None:
+                vals = vals[window[0]:window[0] + window[1]]
+                if len(vals) != window[1]:
+                    raise SystemExit(f"{name}: fewer dispatches than the attention window")
+            tot += sum(vals) / len(vals)
+            cnt += len(vals)
+        return tot, cnt
 
     cf, _ = one(fetch, "FETCH_SIZE", "copy16_kernel")
-    cw, _ = one(write, "WRITE_SIZE", "copy16_kernel")   # one dispatch: "last" keeps it
+    cw, _ = one(write, "WRITE_SIZE", "copy16_kernel")   # the calibration copy: one dispatch
     f_fac = copy_bytes / (cf * 1024.0)
     w_fac = copy_bytes / (cw * 1024.0)
     lines = [f"# HBM traffic of drafter_block_attention, workload {args.workload}",
              f"command (FETCH_SIZE pass): {args.command.replace('{COUNTER}', 'FETCH_SIZE')}",
              f"command (WRITE_SIZE pass): {args.command.replace('{COUNTER}', 'WRITE_SIZE')}",
              f"attention_source_digest: {attention_digest()}",
-             f"dispatches used: the last {args.steps} of each attention kernel (the timed "
-             f"attention calls on the final state)",
+             f"dispatches used: {win[1]} of each attention kernel from index {win[0]} (the "
+             f"timed stand-alone attention calls on the final state)",
              f"copy_kernel_bytes: {copy_bytes}",
              f"copy FETCH_SIZE KiB: {cf:.1f}  (factor {f_fac:.4f})",
              f"copy WRITE_SIZE KiB: {cw:.1f}  (factor {w_fac:.4f})"]
@@ -156,8 +169,8 @@ def summarize_pmc(args):
     for kn in ATTN_KERNELS:
         if not any(k[1] == "FETCH_SIZE" and kn in k[0] for k in fetch):
             continue                            # a kernel this workload does not launch
-        kf, nf = one(fetch, "FETCH_SIZE", kn)
-        kw, nw = one(write, "WRITE_SIZE", kn)
+        kf, nf = one(fetch, "FETCH_SIZE", kn, win)
+        kw, nw = one(write, "WRITE_SIZE", kn, win)
         b = kf * 1024.0 * f_fac + kw * 1024.0 * w_fac
         tot += b
         lines.append(f"{kn}: FETCH_SIZE {kf:.1f} KiB/dispatch ({nf} dispatches), "
@@ -168,6 +181,10 @@ def summarize_pmc(args):
     with open(traffic_file(args.workload), "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print("\n".join(lines))
+
+
+def is_kernel(name, kernel):
+    return "::" + kernel + "<" in name or "::" + kernel + "(" in name
 
 
 def summarize_stats(args):
@@ -185,12 +202,34 @@ def summarize_stats(args):
     for n, c, a, lo, hi, pct in rows:
         short = n if len(n) <= 90 else n[:87] + "..."
         lines.append(f"{short:90s} {c:6d} {a:8.2f} {lo:8.2f} {hi:8.2f} {pct:6.2f}")
-    att = [(k, r) for k in ATTN_KERNELS for r in rows
-           if "::" + k + "<" in r[0] or "::" + k + "(" in r[0]]
+    att = [(k, r) for k in ATTN_KERNELS for r in rows if is_kernel(r[0], k)]
     if att:
-        lines += ["", "drafter_block_attention = " + " + ".join(
+        lines += ["", "drafter_block_attention, all dispatches = " + " + ".join(
             f"{k} {r[2]:.2f} us" for k, r in att) +
             f" = {sum(r[2] for _, r in att):.2f} us per launch (kernel time, no launch gaps)"]
+    trace = os.path.join(os.path.dirname(args.summarize_stats),
+                         os.path.basename(args.summarize_stats).replace("kernel_stats",
+                                                                        "kernel_trace"))
+    if att and os.path.exists(trace):
+        first, count = attention_window(args)
+        per = {}
+        with open(trace) as fh:
+            for r in csv.DictReader(fh):
+                for k, _ in att:
+                    if is_kernel(r["Kernel_Name"], k):
+                        per.setdefault(k, []).append(
+                            (int(r["Dispatch_Id"]),
+                             (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3))
+        parts = []
+        for k, _ in att:
+            d = [t for _, t in sorted(per.get(k, []))][first:first + count]
+            if len(d) == count:
+                parts.append((k, float(np.mean(d))))
+        if len(parts) == len(att):
+            lines.append("drafter_block_attention, the timed stand-alone calls (dispatches "
+                         f"{first}..{first + count - 1} of each kernel, from the kernel trace) = " +
+                         " + ".join(f"{k} {t:.2f} us" for k, t in parts) +
+                         f" = {sum(t for _, t in parts):.2f} us per launch")
     os.makedirs(PROFILES, exist_ok=True)
     out = os.path.join(PROFILES, f"kernel_stats_{args.workload}.txt")
     with open(out, "w") as fh:
@@ -223,14 +262,16 @@ def attention_flops(w, keys_total):
     return 2.0 * 2.0 * keys_total * w.L * w.B * w.Hq * w.hd
 
 
-def timed_calls(torch, stream, n, call):
+def timed_calls(torch, stream, n, call, warm=3, between=None):
     """Average duration (s) of ``call`` over n calls, each bracketed by HIP events
-    recorded on ``stream``."""
+    recorded on ``stream``; ``between`` (untimed) runs before each call."""
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(n)]
-    for _ in range(3):
+    for _ in range(warm):
         call()
     for a, b in ev:
+        if between is not None:
+            between()
         a.record(stream)
         call()
         b.record(stream)
@@ -238,11 +279,12 @@ def timed_calls(torch, stream, n, call):
     return float(np.mean([a.elapsed_time(b) for a, b in ev])) / 1e3
 
 
-def projection_result(w, flops, nbytes, sec):
+def projection_result(w, flops, nbytes, sec, rows=None):
     peak = MFMA_PEAK_TFLOPS[w.dtype]
     tflops = flops / sec / 1e12
     gbs = nbytes / sec / 1e9
-    return {"call": "carryover_project_kv", "rows": w.S * w.B, "flops_per_call": flops,
+    return {"call": "carryover_project_kv", "rows": w.S * w.B if rows is None else rows,
+            "flops_per_call": flops,
             "bytes_per_call": nbytes, "avg_call_us": sec * 1e6, "tflops": tflops,
             "mfma_peak_tflops": peak, "mfma_frac": tflops / peak, "gbs": gbs,
             "hbm_frac": gbs / HBM_PEAK_GBS}
@@ -322,14 +364,31 @@ def main():
         if rc:
             raise RuntimeError(f"carryover_round failed ({rc})")
 
+    def chain(mode_flags):
+        """The timed rounds warmup..total-1, chained; wall time (s)."""
+        nonlocal flags
+        flags = mode_flags
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            step(args.warmup + i)
+        torch.cuda.synchronize()
+        flags = 0
+        return time.perf_counter() - t0
+
     for r in range(args.warmup):
         step(r)
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(args.warmup + i)
-    torch.cuda.synchronize()
-    dt = time.perf_counter() - t0
+    # lengths after the warm-up rounds: restoring them rewinds the chain (rows
+    # beyond ctx_len are never read and the carry segment is replaced before it
+    # is read, so the timed rounds can be run again from here)
+    snap = (sc.st["ctx_len"].clone(), sc.st["carry_len"].clone())
+
+    def rewind():
+        sc.st["ctx_len"].copy_(snap[0])
+        sc.st["carry_len"].copy_(snap[1])
+
+    dt = chain(0)
     status = co.carryover_read_status(sc.st)
     if status:
         raise RuntimeError(f"device status {co.status_string(status)}")
@@ -339,34 +398,22 @@ def main():
     # call launches its kernels back to back, so they cannot be bracketed there).
     wsa_ptr, wsa_n = ws_ptr + sc.ws_project, ws_n - sc.ws_project
     q_last = inputs[total - 1][1]
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
     out, lse = outs[0]
 
-    def attend(i=None):
-        if i is not None:
-            ev[i][0].record(stream)
+    def attend():
         rc = lib.drafter_block_attention(dims_p, 0, w.L, q_last.data_ptr(), st_p, out.data_ptr(),
-                                         lse.data_ptr(), flags, wsa_ptr, wsa_n, sptr)
-        if i is not None:
-            ev[i][1].record(stream)
+                                         lse.data_ptr(), 0, wsa_ptr, wsa_n, sptr)
         if rc:
             raise RuntimeError(f"drafter_block_attention failed ({rc})")
 
-    for _ in range(5):
-        attend()
-    for i in range(args.steps):
-        attend(i)
-    torch.cuda.synchronize()
+    att_s = timed_calls(torch, stream, args.steps, attend, warm=ATTN_WARM)
     if co.carryover_read_status(sc.st):
         raise RuntimeError("device status after attention")
     ctx_f = sc.st["ctx_len"].cpu().numpy().astype(np.int64)
     car_f = sc.st["carry_len"].cpu().numpy().astype(np.int64)
     assert np.array_equal(ctx_f, ctx), "host replica of the lengths diverged"
     per_launch = float(attention_bytes(w, ctx_f, car_f))
-    att_ms = [a.elapsed_time(b) for a, b in ev]
-    att_s = float(np.sum(att_ms)) / 1e3
-    achieved = per_launch * args.steps / att_s / 1e9
+    achieved = per_launch / att_s / 1e9
 
     # The projection entry point, timed the same way: the last round's rows
     # projected again into the slots they already occupy (same values).
@@ -380,10 +427,35 @@ def main():
 
     proj_s = timed_calls(torch, stream, min(args.steps, 100), project)
     pflops, pbytes = projection_work(w, w.S * w.B)
+
+    # Cold: the same calls with a 512 MiB copy (twice the 256 MB Infinity
+    # Cache) between them, outside the events, so that no K/V, weight or state
+    # byte is served from a cache filled by the previous call.  Attention on
+    # the final state first, then the timed rounds again from the snapshot.
+    n_cold = min(args.steps, COLD_CALLS)
+    scrub = Scrub(torch)
+    cold_att_s = timed_calls(torch, stream, n_cold, attend, warm=0, between=scrub)
+    rewind()
+    cold_r = iter(range(n_cold))
+    cold_round_s = timed_calls(torch, stream, n_cold, lambda: step(args.warmup + next(cold_r)),
+                               warm=0, between=scrub)
+    del scrub
+
+    # t_reuse (the cost of carrying over): the same timed rounds from the same
+    # state in Algorithm 1's baseline mode (commit the accepted rows only, no
+    # carry segment, no E)
+    rewind()
+    dt_base = chain(co.CO_BASELINE_MODE)
+    if co.carryover_read_status(sc.st):
+        raise RuntimeError("device status after baseline rounds")
+    assert np.array_equal(sc.st["ctx_len"].cpu().numpy().astype(np.int64), ctx)
+
+    prefill = prefill_point(torch, co, sc, w) if w.ctx_mode == "projected" else None
     calibrate_copy(torch, args)
 
     metric = ("drafter rounds/s (block-16) at batch 32" if w.name == "ragged_batch32"
               else f"drafter rounds/s ({w.name})")
+    keys = float(np.sum(ctx_f + car_f))
     result = {
         "metric": metric,
         "value": args.steps / dt,
@@ -407,14 +479,65 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": recorded_traffic(w.name),
                      "algorithmic_bytes_per_launch": per_launch,
-                     "avg_launch_us": att_s / args.steps * 1e6,
-                     "tflops": attention_flops(w, float(np.sum(ctx_f + car_f))) /
-                     (att_s / args.steps) / 1e12},
+                     "avg_launch_us": att_s * 1e6,
+                     "tflops": attention_flops(w, keys) / att_s / 1e12,
+                     "cold": {"avg_launch_us": cold_att_s * 1e6,
+                              "achieved": per_launch / cold_att_s / 1e9,
+                              "frac": per_launch / cold_att_s / 1e9 / HBM_PEAK_GBS}},
         "projection": projection_result(w, pflops, pbytes, proj_s),
+        "cold_round_us": cold_round_s * 1e6,
+        "baseline_mode": {"rounds_per_s": args.steps / dt_base,
+                          "t_reuse_us": (dt - dt_base) / args.steps * 1e6},
     }
+    if prefill is not None:
+        result["prefill_projection"] = prefill
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w.replace(rounds=w.rounds), args.cpu_baseline_seconds)
     print(json.dumps(result), flush=True)
+
+
+class Scrub:
+    """A 512 MiB device copy (torch's copy kernel, so that it is never taken for
+    the counter-calibration copy)."""
+
+    def __init__(self, torch):
+        n = (512 << 20) // 4
+        self.a = torch.ones(n, dtype=torch.float32, device="cuda")
+        self.b = torch.empty_like(self.a)
+
+    def __call__(self):
+        self.b.copy_(self.a)
+
+
+def prefill_point(torch, co, sc, w):
+    """The context projection as one call (every row committed, no E) over the
+    initial contexts of all sequences: the rows are projected again into the
+    slots they already hold (same values), timed like the other calls."""
+    from synth import device as sdev
+    from synth import workloads as wl
+    n = int(sc.ctx0[0])
+    h = torch.empty((w.S, n, w.Dcat), dtype=sc.tdtype, device="cuda")
+    for s in range(w.S):
+        st_, shape, strides, base, sigma = wl.spec_hctx(w, s, 0, n)
+        sdev.fill(h[s], w.key(st_), shape, strides, base, sigma)
+    d = sc.dims
+    pd = co.make_dims(w.S, n, d.feat_dim, d.model_dim, d.num_layers, d.num_q_heads,
+                      d.num_kv_heads, d.head_dim, d.max_pages_per_seq, d.num_pages, d.dtype,
+                      d.rope_theta)
+    rt = co.alloc_route(w.S, n)
+    ws = torch.empty(max(co.workspace_bytes(pd, co.CO_WS_PROJECT), 256), dtype=torch.uint8,
+                     device="cuda")
+    saved = (sc.st["ctx_len"].clone(), sc.st["carry_len"].clone())
+    sc.st["ctx_len"].zero_()
+    co.carryover_route(pd, None, None, co.CO_ROUTE_ACCEPT_ALL, sc.st, rt)
+    sec = timed_calls(torch, torch.cuda.current_stream(), 20,
+                      lambda: co.carryover_project_kv(pd, sc.W, h, rt, sc.st, ws))
+    sc.st["ctx_len"].copy_(saved[0])
+    sc.st["carry_len"].copy_(saved[1])
+    if co.carryover_read_status(sc.st):
+        raise RuntimeError("device status after the prefill projection")
+    flops, nbytes = projection_work(w, w.S * n)
+    return projection_result(w, flops, nbytes, sec, rows=w.S * n)
 
 
 def calibrate_copy(torch, args):
@@ -433,27 +556,23 @@ def calibrate_copy(torch, args):
 
 
 def run_train(args, w):
-    """The training-shaped forward (second drafter pass of Algorithm 2): every
-    anchored block's rejected rows projected into its carry segment, then block
-    attention of all blocks; one step = one forward over all blocks."""
+    """The training-shaped forward (second drafter pass of Algorithm 2): one
+    step = one forward: K/V of every recorded position of every response
+    (committed), every anchored block's rejected rows projected with E into its
+    carry segment, then block attention of all blocks."""
     import torch
     import paper_2609_14717_amd as co
     from synth.scenario import TrainScenario
     torch.cuda.set_device(0)
     sc = TrainScenario(w)
     stream = torch.cuda.current_stream()
-    ctx0 = sc.vst["ctx_len"].clone()
-
-    def step():
-        sc.vst["ctx_len"].copy_(ctx0)            # every forward starts from the windows at a + 1
-        sc.forward()
 
     for _ in range(args.warmup):
-        step()
+        sc.forward()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step()
+        sc.forward()
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     if co.carryover_read_status(sc.vst) or co.carryover_read_status(sc.st):
@@ -462,14 +581,22 @@ def run_train(args, w):
     vw = w.replace(S=V)
     n = min(args.steps, 100)
     att_s = timed_calls(torch, stream, n, lambda: co.drafter_block_attention(
-        sc.vdims, 0, w.L, sc.q, sc.vst, sc.out, sc.lse, co.CO_ATTN_SHARED_PREFIX, sc.ws))
+        sc.vdims, 0, w.L, sc.q, sc.vst, sc.out, sc.lse, co.CO_ATTN_SHARED_PREFIX, sc.ws),
+        warm=TRAIN_ATTN_WARM)
+    # the projection of one forward: the committed rows of every response (one
+    # call, every row committed) and the rows of every anchored block (one call,
+    # the rejected rows go to the block's carry segment, the others are skipped)
     wsp = co.workspace_bytes(sc.vdims, co.CO_WS_PROJECT)
-    proj_s = timed_calls(torch, stream, n, lambda: co.carryover_project_kv(
+    pc_s = timed_calls(torch, stream, n, lambda: co.carryover_project_kv(
+        sc.dims, sc.W, sc.h_committed, sc.crt, sc.st, sc.cws))
+    pv_s = timed_calls(torch, stream, n, lambda: co.carryover_project_kv(
         sc.vdims, sc.W, sc.hidden, sc.vrt, sc.vst, sc.ws, ws_bytes=wsp))
     keys = float(np.sum(sc.vst["ctx_len"].cpu().numpy().astype(np.int64) +
                         sc.vst["carry_len"].cpu().numpy().astype(np.int64)))
+    carried = int(sc.vst["carry_len"].sum().item())
     aflops = attention_flops(vw, keys)
-    pflops, pbytes = projection_work(vw, V * w.B)
+    prows = w.S * w.seq_len + carried
+    pflops, pbytes = projection_work(vw, prows)
     atfl = aflops / att_s / 1e12
     calibrate_copy(torch, args)
     result = {
@@ -494,7 +621,10 @@ def run_train(args, w):
                      "peak": MFMA_PEAK_TFLOPS[w.dtype], "unit": "TFLOP/s",
                      "frac": atfl / MFMA_PEAK_TFLOPS[w.dtype], "traffic": recorded_traffic(w.name),
                      "algorithmic_flops_per_launch": aflops, "avg_launch_us": att_s * 1e6},
-        "projection": projection_result(vw, pflops, pbytes, proj_s),
+        "projection": dict(projection_result(vw, pflops, pbytes, pc_s + pv_s, rows=prows),
+                           call="carryover_project_kv x2 (committed rows; anchored blocks' rows)",
+                           committed_call_us=pc_s * 1e6, block_call_us=pv_s * 1e6,
+                           rows_computed=w.S * w.seq_len + V * w.B),
     }
     print(json.dumps(result), flush=True)
 

@@ -131,25 +131,24 @@ class TrainScenario:
         self.e = sdev.materialise(w, wl.spec_e(w), device)
         self.W, self.f_e = make_weights(co, self.dims, self.wf, self.wkv, self.e, fold_e)
         dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
-        # prefill: every recorded position of every response, committed, no E
-        h = torch.empty((S, w.seq_len, w.Dcat), dtype=dt, device=device)
+        # committed rows: every recorded position of every response, no E
+        self.h_committed = torch.empty((S, w.seq_len, w.Dcat), dtype=dt, device=device)
         for s in range(S):
             st_, shape, strides, base, sigma = wl.spec_hctx(w, s, 0, w.seq_len)
-            sdev.fill(h[s], w.key(st_), shape, strides, base, sigma)
-        rt = co.alloc_route(S, w.seq_len, device)
-        ws = torch.empty(max(co.workspace_bytes(self.dims, co.CO_WS_PROJECT), 256),
-                         dtype=torch.uint8, device=device)
-        co.carryover_route(self.dims, None, None, co.CO_ROUTE_ACCEPT_ALL, self.st, rt)
-        co.carryover_project_kv(self.dims, self.W, h, rt, self.st, ws)
-        del h, ws
+            sdev.fill(self.h_committed[s], w.key(st_), shape, strides, base, sigma)
+        self.crt = co.alloc_route(S, w.seq_len, device)
+        self.cws = torch.empty(max(co.workspace_bytes(self.dims, co.CO_WS_PROJECT), 256),
+                               dtype=torch.uint8, device=device)
+        self.project_committed()
         # virtual sequences
         self.a, self.u, self.a2 = wl.anchors(w)
         self.vdims = co.make_dims(V, B, w.Dcat, w.d, w.L, w.Hq, w.Hkv, w.hd, P, self.pt.size,
                                   w.dtype, w.theta)
         self.vpt = np.repeat(self.pt, A, axis=0)
         CP = -(-B // wl.PAGE)
+        self.vctx0 = torch.from_numpy((self.a.ravel() + 1).astype(np.int32)).to(device)
         self.vst = dict(
-            ctx_len=torch.from_numpy((self.a.ravel() + 1).astype(np.int32)).to(device),
+            ctx_len=self.vctx0.clone(),
             carry_len=torch.zeros(V, dtype=torch.int32, device=device),
             page_table=torch.from_numpy(self.vpt).to(device),
             k_cache=self.st["k_cache"], v_cache=self.st["v_cache"],
@@ -168,10 +167,26 @@ class TrainScenario:
         self.out = torch.empty((w.L, V, B, w.Hq, w.hd), dtype=dt, device=device)
         self.lse = torch.empty((w.L, V, B, w.Hq), dtype=torch.float32, device=device)
 
-    def forward(self, shared_prefix: bool = True):
-        """Carry rows of every anchored block, then the block attention of all of
-        them (blocks of one response share its pages: CO_ATTN_SHARED_PREFIX)."""
+    def project_committed(self):
+        """K/V of every recorded position of every response at positions
+        0..seq_len-1, all committed (a prefill through the route and
+        projection entry points)."""
         co = self.co
+        self.st["ctx_len"].zero_()
+        co.carryover_route(self.dims, None, None, co.CO_ROUTE_ACCEPT_ALL, self.st, self.crt)
+        co.carryover_project_kv(self.dims, self.W, self.h_committed, self.crt, self.st, self.cws)
+
+    def forward(self, shared_prefix: bool = True, committed: bool = True):
+        """One forward of the second drafter pass: K/V of the committed rows
+        (recomputed every forward, as in training, where the weights change
+        between steps; ``committed=False`` keeps the cache of the last one),
+        then the carry rows of every anchored block, then the block attention
+        of all of them (blocks of one response share its pages:
+        CO_ATTN_SHARED_PREFIX)."""
+        co = self.co
+        if committed:
+            self.project_committed()
+        self.vst["ctx_len"].copy_(self.vctx0)       # every block's window starts at a + 1
         co.carryover_route(self.vdims, self.draft, self.target, co.CO_ROUTE_CARRY_ONLY,
                            self.vst, self.vrt)
         co.carryover_project_kv(self.vdims, self.W, self.hidden, self.vrt, self.vst, self.ws)

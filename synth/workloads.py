@@ -110,11 +110,17 @@ RAGGED32 = Workload("ragged_batch32", S=32, B=16, Dcat=768, d=256, L=1, Hq=4, Hk
 LONG_CHAIN = Workload("long_chain_5layer", S=16, B=16, Dcat=20480, d=4096, L=5, Hq=32, Hkv=8,
                       hd=128, dtype="bf16", theta=1e6, ctx_lo=16384, ctx_hi=32768,
                       ctx_mode="direct", accept=("geom", 0.3), rounds=64, seed=_seed(4))
+# cfg3's batch, contexts and acceptance with cfg2's widths (and RoPE base):
+# the large-width serving round, whose projection is a compute-bound GEMM.
+RAGGED32_8B = Workload("ragged_batch32_8b", S=32, B=16, Dcat=20480, d=4096, L=1, Hq=32, Hkv=8,
+                       hd=128, dtype="bf16", theta=1e6, ctx_lo=512, ctx_hi=8192,
+                       ctx_mode="direct", accept=("geom", 0.25), rounds=256,
+                       seed=_seed(3) + 500)
 TRAIN_FWD = Workload("train_fwd", S=8, B=16, Dcat=768, d=256, L=1, Hq=4, Hkv=2, hd=64,
                      dtype="bf16", theta=1e4, ctx_lo=0, ctx_hi=0, ctx_mode="projected",
                      accept=("uniform",), rounds=0, seed=_seed(5), anchors=256, seq_len=4096)
 
-WORKLOADS = {w.name: w for w in (TINY, BATCH1_8B, RAGGED32, LONG_CHAIN, TRAIN_FWD)}
+WORKLOADS = {w.name: w for w in (TINY, BATCH1_8B, RAGGED32, RAGGED32_8B, LONG_CHAIN, TRAIN_FWD)}
 
 
 # ----------------------------------------------------------------- host draws

@@ -146,22 +146,19 @@ def test_attention_slicings(w, slicing, monkeypatch):
     run_rounds(w, 2)
 
 
-def test_long_chain_5layer_sampled():
-    """The 64-round, 5-layer chain at full size (16 sequences, contexts of
-    16K-32K tokens, head_dim 128, 32/8 heads), in the launch configuration of
-    a serving round.  Every round: routing, accepted lengths, descriptors and
-    lengths of all 16 sequences bit-exact; the committed rows written and the
-    carry rows of one sampled sequence within tolerance.  At rounds 0, 1, 31
-    and 63 also the attention output of that sequence in layers 0 and 4."""
+def sampled_chain(w, rounds, samples, check, layers):
+    """Chained serving rounds at full size in the launch configuration of a
+    serving round.  Every round: routing, accepted lengths, descriptors and
+    lengths of all sequences bit-exact; the committed rows written and the
+    carry rows of the sampled sequences within tolerance.  At the rounds in
+    ``check`` also the attention output of the sampled sequences in ``layers``."""
     import paper_2609_14717_amd as co
     Scenario = _gpu()
-    w = wl.LONG_CHAIN
-    sample, layers, check = 5, [0, 4], {0, 1, 31, 63}
     tol = TOL[w.dtype]
-    print(f"[parity] workload={w.name} rounds={w.rounds} sample={sample}", flush=True)
+    print(f"[parity] workload={w.name} rounds={rounds} samples={samples}", flush=True)
     sc = Scenario(w)
-    orc = OracleRun(w, seqs=[sample], store=np.float32)
-    for r in range(w.rounds):
+    orc = OracleRun(w, seqs=samples, store=np.float32)
+    for r in range(rounds):
         hidden, q, draft, target, m = sc.round_inputs(r)
         out, lse = sc.new_output()
         co.carryover_round(sc.dims, sc.W, hidden, draft, target, q, sc.st, sc.rt, out, lse, 0,
@@ -174,27 +171,49 @@ def test_long_chain_5layer_sampled():
             np.testing.assert_array_equal(sc.rt[key].cpu().numpy(), rr[key], err_msg=f"r{r} {key}")
         np.testing.assert_array_equal(sc.st["ctx_len"].cpu().numpy(), rr["ctx_len"])
         np.testing.assert_array_equal(sc.st["carry_len"].cpu().numpy(), rr["carry_len"])
-        s = sample
-        mm = int(rr["accept_len"][s])
-        p0 = int(rr["ctx_len"][s]) - mm
-        u = int(rr["carry_len"][s])
-        for layer in range(w.L):
-            if mm:
-                gk, gv = gather_committed(sc.st, sc.pt, s, layer, p0, p0 + mm)
-                assert_heads_close(gk, orc.st.ck[s][layer, p0:p0 + mm], tol, f"r{r} C_k l{layer}")
-                assert_heads_close(gv, orc.st.cv[s][layer, p0:p0 + mm], tol, f"r{r} C_v l{layer}")
-            if u:
-                gk, gv = gather_carry(sc.st, s, layer, u)
-                assert_heads_close(gk, orc.st.uk[s][layer], tol, f"r{r} U_k l{layer}")
-                assert_heads_close(gv, orc.st.uv[s][layer], tol, f"r{r} U_v l{layer}")
+        for s in samples:
+            mm = int(rr["accept_len"][s])
+            p0 = int(rr["ctx_len"][s]) - mm
+            u = int(rr["carry_len"][s])
+            for layer in range(w.L):
+                if mm:
+                    gk, gv = gather_committed(sc.st, sc.pt, s, layer, p0, p0 + mm)
+                    assert_heads_close(gk, orc.st.ck[s][layer, p0:p0 + mm], tol,
+                                       f"r{r} s{s} C_k l{layer}")
+                    assert_heads_close(gv, orc.st.cv[s][layer, p0:p0 + mm], tol,
+                                       f"r{r} s{s} C_v l{layer}")
+                if u:
+                    gk, gv = gather_carry(sc.st, s, layer, u)
+                    assert_heads_close(gk, orc.st.uk[s][layer], tol, f"r{r} s{s} U_k l{layer}")
+                    assert_heads_close(gv, orc.st.uv[s][layer], tol, f"r{r} s{s} U_v l{layer}")
+            if att:
+                g = to_np(out[:, s])
+                gl = lse[:, s].cpu().numpy().astype(np.float64)
+                for layer in layers:
+                    assert_heads_close(g[layer], O[layer, s], tol, f"r{r} s{s} O layer {layer}")
+                    err = np.abs(gl[layer] - LSE[layer, s]).max()
+                    assert err <= tol, f"r{r} s{s} LSE layer {layer}: {err}"
         if att:
-            g = to_np(out[:, s])
-            gl = lse[:, s].cpu().numpy().astype(np.float64)
-            for layer in layers:
-                assert_heads_close(g[layer], O[layer, s], tol, f"r{r} O layer {layer}")
-                err = np.abs(gl[layer] - LSE[layer, s]).max()
-                assert err <= tol, f"r{r} LSE layer {layer}: {err}"
             print(f"[parity] {w.name} round {r} checked", flush=True)
+
+
+def test_long_chain_5layer_sampled():
+    """The 64-round, 5-layer chain at full size (16 sequences, contexts of
+    16K-32K tokens, head_dim 128, 32/8 heads): one sampled sequence every
+    round, its attention output in layers 0 and 4 at rounds 0, 1, 31 and 63."""
+    sampled_chain(wl.LONG_CHAIN, wl.LONG_CHAIN.rounds, [5], {0, 1, 31, 63}, [0, 4])
+
+
+def test_ragged_batch32_8b_sampled():
+    """The batch-32 ragged round at the 8B widths (Dcat 20480 -> d 4096, 32/8
+    heads of 128, contexts of 512-8192 tokens): four rounds, three sampled
+    sequences (the shortest, the longest and one between), their attention
+    output every round."""
+    w = wl.RAGGED32_8B
+    ctx0 = wl.initial_ctx(w)
+    order = np.argsort(ctx0, kind="stable")
+    samples = sorted({int(order[0]), int(order[len(order) // 2]), int(order[-1])})
+    sampled_chain(w, 4, samples, {0, 1, 2, 3}, [0])
 
 
 def test_train_fwd_sampled():
