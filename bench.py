@@ -44,6 +44,7 @@ ATTN_SOURCES = [os.path.join(ROOT, "paper_2609_14717_amd", "csrc", f)
                 for f in ("attention.hip", "co_device.h", "co_kernels.h")]
 ATTN_KERNELS = ("attn_bf16_kernel", "attn_bf16_combine_kernel", "attn_group_kernel",
                 "attn_share_merge_kernel")
+ATTN_KERNELS_F32 = ("attn_f32_kernel", "attn_chunk_merge_kernel")
 ATTN_WARM = 5       # untimed attention calls before the timed ones
 COLD_CALLS = 50     # cold calls timed (each after a cache scrub)
 TRAIN_ATTN_WARM = 3
@@ -474,7 +475,8 @@ def main():
                    "head_dim": w.hd, "ctx0": [w.ctx_lo, w.ctx_hi], "accept": list(w.accept),
                    "chained_rounds": total, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm",
-                     "kernel": "drafter_block_attention (" + " + ".join(ATTN_KERNELS) + ")",
+                     "kernel": "drafter_block_attention (" + " + ".join(
+                         ATTN_KERNELS if w.dtype == "bf16" else ATTN_KERNELS_F32) + ")",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": recorded_traffic(w.name),

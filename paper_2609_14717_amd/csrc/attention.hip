@@ -212,40 +212,53 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnArgs a, int chunk_pag
   const float* kk = static_cast<const float*>(a.k_carry);
   const float* vk = static_cast<const float*>(a.v_carry);
   for (int lp0 = p_begin; lp0 < p_end; lp0 += 2) {
-    // stage 32 keys (two logical pages)
-    for (int idx = tid; idx < KT * HD; idx += 256) {
-      const int key = idx / HD, dd = idx % HD;
-      const int lp = lp0 + (key >> 4), slot = key & 15;
-      float kv = 0.f, vv = 0.f;
-      int valid = 0;
-      if (lp < p_end) {
-        if (lp < npc) {
-          const int phys = a.page_table[static_cast<int64_t>(s) * a.max_pages + lp];
-          if (phys >= 0 && phys < a.num_pages) {
-            valid = lp * kPage + slot < ctx;
-            if (valid) {
-              const int64_t off =
-                  ((static_cast<int64_t>(layer) * a.num_pages + phys) * a.Hkv + g) * kPage * HD;
-              kv = kc[off + slot * HD + dd];
-              vv = vc[off + dd * kPage + slot];
-            }
-          } else if (dd == 0) {
-            set_status(a.status, CO_ERR_PAGE_RANGE);
-          }
-        } else {
-          const int cp = lp - npc;
-          valid = cp * kPage + slot < carry;
-          if (valid) {
-            const int64_t off =
-                (((static_cast<int64_t>(layer) * a.S + s) * a.CP + cp) * a.Hkv + g) * kPage * HD;
-            kv = kk[off + slot * HD + dd];
-            vv = vk[off + dd * kPage + slot];
-          }
+    // stage 32 keys (two logical pages): resolve both pages first, then issue
+    // every element load of the tile before any is used
+    const float* kp[2];
+    const float* vp[2];
+    int nvalid[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int lp = lp0 + q;
+      kp[q] = vp[q] = nullptr;
+      nvalid[q] = 0;
+      if (lp >= p_end) continue;
+      if (lp < npc) {
+        const int phys = a.page_table[static_cast<int64_t>(s) * a.max_pages + lp];
+        if (phys >= 0 && phys < a.num_pages) {
+          const int64_t off =
+              ((static_cast<int64_t>(layer) * a.num_pages + phys) * a.Hkv + g) * kPage * HD;
+          kp[q] = kc + off;
+          vp[q] = vc + off;
+          nvalid[q] = min(kPage, ctx - lp * kPage);
+        } else if (tid == 0) {
+          set_status(a.status, CO_ERR_PAGE_RANGE);
         }
+      } else {
+        const int cp = lp - npc;
+        const int64_t off =
+            (((static_cast<int64_t>(layer) * a.S + s) * a.CP + cp) * a.Hkv + g) * kPage * HD;
+        kp[q] = kk + off;
+        vp[q] = vk + off;
+        nvalid[q] = min(kPage, carry - cp * kPage);
       }
-      ks[key][dd] = kv;
-      vs[key][dd] = vv;
-      if (dd == 0) kvalid[key] = valid;
+    }
+    constexpr int PER = KT * HD / 256;   // elements of the tile staged per thread
+    float kr[PER], vr[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const int idx = tid + e * 256, key = idx / HD, dd = idx % HD;
+      const int q = key >> 4, slot = key & 15;
+      const bool ok = slot < nvalid[q];
+      kr[e] = ok ? kp[q][slot * HD + dd] : 0.f;
+      vr[e] = ok ? vp[q][dd * kPage + slot] : 0.f;
+    }
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const int idx = tid + e * 256, key = idx / HD, dd = idx % HD;
+      ks[key][dd] = kr[e];
+      vs[key][dd] = vr[e];
+      if (dd == 0) kvalid[key] = (key & 15) < nvalid[key >> 4];
     }
     __syncthreads();
     for (int idx = tid; idx < nq * KT; idx += 256) {
@@ -1664,8 +1677,9 @@ AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pa
     const int64_t rows_u = static_cast<int64_t>(L) * S * cp * Hkv;
     p.ok = S <= kMaxAttnSeqs && tiles < INT32_MAX && rows_c < INT32_MAX && rows_u < INT32_MAX;
   } else {
-    // fp32 path: chunks of pages, one workgroup each
-    p.chunk_pages = 32;
+    // fp32 path: chunks of pages, one workgroup each; short chunks, so that a
+    // short context still spreads over many workgroups
+    p.chunk_pages = 4;
     while ((max_lp + p.chunk_pages - 1) / p.chunk_pages > kMaxMergeChunks) p.chunk_pages *= 2;
     p.ok = p.chunk_pages <= kMaxChunkPages;
     p.n_chunks = (max_lp + p.chunk_pages - 1) / p.chunk_pages;

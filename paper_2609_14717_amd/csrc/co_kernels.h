@@ -52,6 +52,7 @@ struct ProjectArgs {
 struct ProjectPlan {
   int f_tile, f_split;     // tile variant and K-splits of the F GEMM
   int kv_tile, kv_split;   // same for the K/V GEMM
+  bool fused;              // both products in one kernel (small widths, many rows)
   size_t z_bytes, part_bytes, pe_bytes, total;
 };
 

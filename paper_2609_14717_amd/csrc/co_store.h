@@ -19,6 +19,46 @@ __device__ __forceinline__ bool is_carry_row(int32_t dst) { return dst < 0 && ds
 
 // ------------------------------------------------------------- K/V stores
 
+// Where a row of segment (layer, head g) lives: element offsets of its dim 0
+// in the K page layout ([16][hd]) and of its token slot in the V page layout
+// ([hd][16]), and which buffers.  ok is false for a skipped row and for a
+// destination out of range (the status word then records it).
+struct KvRow {
+  int64_t kbase, vbase;
+  bool carry, ok;
+};
+
+__device__ __forceinline__ KvRow kv_row(const KvDest& e, int row, int32_t dst, int layer, int g) {
+  KvRow r{0, 0, false, false};
+  if (dst == kSkip) return r;
+  const int hd = e.hd;
+  int64_t pg;
+  int t;
+  if (dst >= 0) {
+    const int page = dst / kPage;
+    t = dst % kPage;
+    if (page >= e.num_pages) {
+      set_status(e.status, CO_ERR_PAGE_RANGE);
+      return r;
+    }
+    pg = (static_cast<int64_t>(layer) * e.num_pages + page) * e.Hkv + g;
+  } else {
+    const int c = -1 - dst;
+    if (c >= e.CP * kPage) {
+      set_status(e.status, CO_ERR_LENGTH);
+      return r;
+    }
+    const int s = row / e.B, cp = c / kPage;
+    t = c % kPage;
+    pg = ((static_cast<int64_t>(layer) * e.S + s) * e.CP + cp) * e.Hkv + g;
+    r.carry = true;
+  }
+  r.kbase = (pg * kPage + t) * hd;
+  r.vbase = pg * hd * kPage + t;
+  r.ok = true;
+  return r;
+}
+
 // Store pairs (i0+p, i0+p+hd/2), p < NP, of head segment `seg` = (layer, K|V, head)
 // of window row `row`.  lo/hi hold the unrotated fp32 values of those dims;
 // inv_freq[i] = theta^(-2i/hd) in radians per position for fp32 stores, in
@@ -26,40 +66,14 @@ __device__ __forceinline__ bool is_carry_row(int32_t dst) { return dst < 0 && ds
 template <typename T, int NP>
 __device__ inline void kv_store(const KvDest& e, int row, int32_t dst, int pos, int seg, int i0,
                          const float* lo, const float* hi, const double* inv_freq) {
-  if (dst == kSkip) return;
-  const int hd = e.hd, half = hd / 2;
+  const int half = e.hd / 2;
   const int g = seg % e.Hkv;
   const int kind = (seg / e.Hkv) & 1;
   const int layer = seg / (2 * e.Hkv);
-  int64_t kbase, vbase;   // element offsets of dim 0 of this row in the K and V layouts
-  T* kptr;
-  T* vptr;
-  if (dst >= 0) {
-    const int page = dst / kPage, t = dst % kPage;
-    if (page >= e.num_pages) {
-      set_status(e.status, CO_ERR_PAGE_RANGE);
-      return;
-    }
-    const int64_t pg = (static_cast<int64_t>(layer) * e.num_pages + page) * e.Hkv + g;
-    kbase = (pg * kPage + t) * hd;
-    vbase = pg * hd * kPage + t;
-    kptr = static_cast<T*>(e.k_cache);
-    vptr = static_cast<T*>(e.v_cache);
-  } else {
-    const int r = -1 - dst;
-    if (r >= e.CP * kPage) {
-      set_status(e.status, CO_ERR_LENGTH);
-      return;
-    }
-    const int s = row / e.B;
-    const int cp = r / kPage, t = r % kPage;
-    const int64_t pg = ((static_cast<int64_t>(layer) * e.S + s) * e.CP + cp) * e.Hkv + g;
-    kbase = (pg * kPage + t) * hd;
-    vbase = pg * hd * kPage + t;
-    kptr = static_cast<T*>(e.k_carry);
-    vptr = static_cast<T*>(e.v_carry);
-  }
+  const KvRow r = kv_row(e, row, dst, layer, g);
+  if (!r.ok) return;
   if (kind == 0) {
+    T* kptr = static_cast<T*>(r.carry ? e.k_carry : e.k_cache);
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
       float c, s;
@@ -67,14 +81,15 @@ __device__ inline void kv_store(const KvDest& e, int row, int32_t dst, int pos, 
         rope_cos_sin_rev(pos, inv_freq[i0 + p], &c, &s);
       else
         rope_cos_sin(pos, inv_freq[i0 + p], &c, &s);
-      kptr[kbase + i0 + p] = to_elem<T>(lo[p] * c - hi[p] * s);
-      kptr[kbase + i0 + p + half] = to_elem<T>(hi[p] * c + lo[p] * s);
+      kptr[r.kbase + i0 + p] = to_elem<T>(lo[p] * c - hi[p] * s);
+      kptr[r.kbase + i0 + p + half] = to_elem<T>(hi[p] * c + lo[p] * s);
     }
   } else {
+    T* vptr = static_cast<T*>(r.carry ? e.v_carry : e.v_cache);
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
-      vptr[vbase + static_cast<int64_t>(i0 + p) * kPage] = to_elem<T>(lo[p]);
-      vptr[vbase + static_cast<int64_t>(i0 + p + half) * kPage] = to_elem<T>(hi[p]);
+      vptr[r.vbase + static_cast<int64_t>(i0 + p) * kPage] = to_elem<T>(lo[p]);
+      vptr[r.vbase + static_cast<int64_t>(i0 + p + half) * kPage] = to_elem<T>(hi[p]);
     }
   }
 }

@@ -21,6 +21,8 @@
 // fp32: a plain LDS-tiled VALU GEMM feeding the same epilogues.
 #include <stdlib.h>
 
+#include <type_traits>
+
 #include "co_store.h"
 
 namespace co {
@@ -611,8 +613,12 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
   const float* A = static_cast<const float*>(g.A);
   const float* Bw = static_cast<const float*>(g.B);
   const float* E = static_cast<const float*>(g.e);
+  // K split blockIdx.z: k in [kb, ke), its partial product in slice blockIdx.z
+  const int kb = blockIdx.z * g.k_per_split;
+  const int ke = min(g.K, kb + g.k_per_split);
+  float* out = g.partial + static_cast<int64_t>(blockIdx.z) * g.M * g.N;
   float acc[2][4] = {};
-  for (int k0 = 0; k0 < g.K; k0 += BK) {
+  for (int k0 = kb; k0 < ke; k0 += BK) {
     for (int c = tid; c < BM * BK; c += 256) {
       const int r = c / BK, k = c % BK, gr = m0 + r;
       float v = 0.f;
@@ -644,8 +650,258 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int row = m0 + tr + 16 * i, col = n0 + tc + 16 * j;
-      if (row < g.M && col < g.N) g.partial[static_cast<int64_t>(row) * g.N + col] = acc[i][j];
+      if (row < g.M && col < g.N) out[static_cast<int64_t>(row) * g.N + col] = acc[i][j];
     }
+}
+
+// ------------------------------------- fused projection, small widths
+// At d = n_kv = 256 (one head_dim-64 segment per 64 K/V columns) and many
+// rows, both products of a block of 128 rows run in one workgroup: Z = F(x)
+// stays in LDS as bf16 and feeds the K/V product directly, whose rotation and
+// scatter follow from registers.  Both products are computed transposed, with
+// the weights as the MFMA A operand: a lane then holds four consecutive
+// columns of one row, so Z rows are written to LDS 8 bytes at a time and the
+// rotation pairs (i, i + 32) of a head lie in one lane.  Wavefront w owns
+// columns 64w .. 64w + 63 of both products (one K/V segment).
+constexpr int kFusedD = 256;                 // d and n_kv of the fused path
+constexpr int kFusedBM = 128;                // rows per workgroup
+constexpr int kFusedZLD = kFusedD * 2 + 16;  // bytes per Z row in LDS (padded against conflicts)
+
+__global__ __launch_bounds__(256, 1) void proj_fused_kernel(ProjectArgs a) {
+  // F stages are 64 deep (3 in the ring), K/V stages 32 deep (4 in the ring
+  // behind the resident Z rows)
+  constexpr int BM = kFusedBM, BK1 = 64, BK2 = 32, NS1 = 3, NS2 = 4;
+  constexpr int ROWB1 = 2 * BK1, CPR1 = BK1 / 8, RPI1 = 64 / CPR1, RPL1 = 256 / ROWB1;
+  constexpr int ROWB2 = 2 * BK2, CPR2 = BK2 / 8, RPI2 = 64 / CPR2, RPL2 = 256 / ROWB2;
+  constexpr int TM = BM / 32, TN = 2;          // activation and weight tiles per wavefront
+  constexpr int WR = kFusedD;                  // weight rows of a stage (both products)
+  constexpr int LPW1 = (WR + BM) / RPI1 / 4;   // 1 KiB loads per wavefront, F stage
+  constexpr int LPW2 = WR / RPI2 / 4;          // same, K/V stage
+  constexpr int STAGE1 = (WR + BM) * ROWB1, STAGE2 = WR * ROWB2;
+  constexpr int Z_BYTES = BM * kFusedZLD;
+  constexpr int RING1 = NS1 * STAGE1, RING2 = Z_BYTES + NS2 * STAGE2;
+  constexpr int LDS_BYTES = RING1 > RING2 ? RING1 : RING2;
+  static_assert((WR + BM) % (4 * RPI1) == 0 && WR % (4 * RPI2) == 0, "tile");
+  static_assert(LPW1 * (NS1 - 1) < 64 && LPW2 * NS2 < 64, "vmcnt");
+  __shared__ __align__(16) unsigned char smem[LDS_BYTES];
+  __shared__ double inv_tab[32];
+  __shared__ __align__(16) float fe_lds[kFusedD];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int m0 = blockIdx.x * BM;
+  const int M = a.M, Dcat = a.Dcat;
+  const uint16_t* X = static_cast<const uint16_t*>(a.hidden);
+  const uint16_t* Wf = static_cast<const uint16_t*>(a.wf);
+  const uint16_t* Wkv = static_cast<const uint16_t*>(a.wkv);
+
+  // descriptors of this lane's rows (row m0 + 32 tm + lane % 32)
+  int rdst[TM], rpos[TM];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    const int r = min(m0 + 32 * tm + (lane & 31), M - 1);
+    rdst[tm] = a.dst.row_dst[r];
+    rpos[tm] = a.dst.row_pos[r];
+  }
+  // the rotation table through scalar loads (indexing the argument by lane
+  // would make it a vector load, and the first wait on it would also wait for
+  // the staged loads issued after it)
+  if (tid == 0) {
+#pragma unroll
+    for (int i = 0; i < 32; ++i) inv_tab[i] = rope_table<uint16_t>(a.dst, i);
+  }
+  // F(E) of this thread's column, written to LDS once the F product is done
+  // (the loads above are waited for there, when no staged load is in flight)
+  float fe_mine = a.fe != nullptr ? a.fe[tid] : 0.f;
+
+  // DMA sources: load j of this wavefront fills stage rows RPI*(wave*LPW+j) ..
+  const uint16_t* src1[LPW1];
+#pragma unroll
+  for (int j = 0; j < LPW1; ++j) {
+    const int row = (wave * LPW1 + j) * RPI1 + lane / CPR1;
+    const int chunk = (lane % CPR1) ^ ((row / RPL1) % CPR1);
+    const uint16_t* base = row < WR ? Wf + static_cast<int64_t>(row) * Dcat
+                                    : X + static_cast<int64_t>(min(m0 + row - WR, M - 1)) * Dcat;
+    src1[j] = base + chunk * 8;
+  }
+  const uint16_t* src2[LPW2];
+#pragma unroll
+  for (int j = 0; j < LPW2; ++j) {
+    const int row = (wave * LPW2 + j) * RPI2 + lane / CPR2;
+    const int chunk = (lane % CPR2) ^ ((row / RPL2) % CPR2);
+    src2[j] = Wkv + static_cast<int64_t>(row) * kFusedD + chunk * 8;
+  }
+  const uint32_t lds0 = lds_addr(smem);
+  // Every workgroup reads the same weights: the workgroups of one XCD (ids
+  // congruent mod 8) start their K loops at different stages, so that they do
+  // not all request the same weight lines from its L2 at the same time.
+  const int nk1 = Dcat / BK1, nk2 = kFusedD / BK2;
+  const int rot1 = (blockIdx.x >> 3) % nk1, rot2 = (blockIdx.x >> 3) % nk2;
+  auto issue1 = [&](int kt) {
+    const uint32_t st = lds0 + (kt % NS1) * STAGE1;
+    const int ks = kt + rot1 < nk1 ? kt + rot1 : kt + rot1 - nk1;
+#pragma unroll
+    for (int j = 0; j < LPW1; ++j) lds_dma16_opaque(src1[j] + ks * BK1, st + (wave * LPW1 + j) * 1024);
+  };
+  auto issue2 = [&](int kt) {
+    const uint32_t st = lds0 + Z_BYTES + (kt % NS2) * STAGE2;
+    const int ks = kt + rot2 < nk2 ? kt + rot2 : kt + rot2 - nk2;
+#pragma unroll
+    for (int j = 0; j < LPW2; ++j) lds_dma16_opaque(src2[j] + ks * BK2, st + (wave * LPW2 + j) * 1024);
+  };
+
+  // fragment offsets within a stage: row lane % 32 of a 32-row tile, logical
+  // 16-byte chunk 2h + lane / 32 of k16 step h, stored permuted
+  const int frow1 = (lane & 31) * ROWB1, fswz1 = ((lane & 31) / RPL1) % CPR1;
+  const int frow2 = (lane & 31) * ROWB2, fswz2 = ((lane & 31) / RPL2) % CPR2;
+  struct Frags {
+    u16x8 w[TN], x[TM];
+  };
+  auto load1 = [&](int kt, int h, Frags& f) {
+    const unsigned char* st = smem + (kt % NS1) * STAGE1;
+    const int off = frow1 + (((2 * h + (lane >> 5)) ^ fswz1) << 4);
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn)
+      f.w[tn] = *reinterpret_cast<const u16x8*>(st + (wave * 64 + tn * 32) * ROWB1 + off);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+      f.x[tm] = *reinterpret_cast<const u16x8*>(st + (WR + tm * 32) * ROWB1 + off);
+  };
+  // K/V stage: weights from the ring, Z (the B operand) from its resident rows
+  auto load2 = [&](int kt, int h, Frags& f) {
+    const unsigned char* st = smem + Z_BYTES + (kt % NS2) * STAGE2;
+    const int off = frow2 + (((2 * h + (lane >> 5)) ^ fswz2) << 4);
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn)
+      f.w[tn] = *reinterpret_cast<const u16x8*>(st + (wave * 64 + tn * 32) * ROWB2 + off);
+    const int ks = kt + rot2 < nk2 ? kt + rot2 : kt + rot2 - nk2;
+    const int zoff = (lane & 31) * kFusedZLD + (ks * BK2 + h * 16 + 8 * (lane >> 5)) * 2;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+      f.x[tm] = *reinterpret_cast<const u16x8*>(smem + tm * 32 * kFusedZLD + zoff);
+  };
+  auto settle = [&](Frags& f) {
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) asm volatile("" : "+v"(f.w[tn]));
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) asm volatile("" : "+v"(f.x[tm]));
+  };
+  f32x16 acc[TN][TM];
+  auto zero = [&]() {
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[tn][tm][r] = 0.f;
+  };
+  auto compute = [&](const Frags& f) {
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) acc[tn][tm] = mfma32x32x16(f.w[tn], f.x[tm], acc[tn][tm]);
+  };
+  // stage kt+1 is published by the barrier taken in the last k16 step of stage
+  // kt, after which stage kt's slot takes the loads of stage kt + NS
+  auto run = [&](int nk, int NS, auto k16_steps, auto issue, auto load, auto wait_ahead) {
+    constexpr int H = decltype(k16_steps)::value;   // k16 steps per stage
+    Frags f0, f1;
+    wait_ahead(min(NS - 1, nk - 1));
+    load(0, 0, f0);
+    for (int kt = 0; kt < nk; ++kt) {
+#pragma unroll
+      for (int h = 0; h < H; ++h) {
+        Frags& cur = (h & 1) ? f1 : f0;
+        Frags& nxt = (h & 1) ? f0 : f1;
+        if (h + 1 < H) load(kt, h + 1, nxt);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(cur);
+        __builtin_amdgcn_sched_barrier(0);
+        if (h + 2 == H) {
+          settle(nxt);
+          if (kt + 1 < nk) {
+            wait_ahead(min(NS - 2, nk - 2 - kt));
+            if (kt + NS < nk) issue(kt + NS);
+            load(kt + 1, 0, cur);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+  };
+  // wait until the loads of the stage `ahead` stages before the newest one
+  // issued have landed (ahead < ring depth), then publish through the barrier
+  auto wait1 = [&](int ahead) {
+    if (ahead >= 2) wait_vm_lgkm_barrier<2 * LPW1>();
+    else if (ahead == 1) wait_vm_lgkm_barrier<LPW1>();
+    else wait_vm_lgkm_barrier<0>();
+  };
+  auto wait2 = [&](int ahead) {
+    if (ahead >= 3) wait_vm_lgkm_barrier<3 * LPW2>();
+    else if (ahead == 2) wait_vm_lgkm_barrier<2 * LPW2>();
+    else if (ahead == 1) wait_vm_lgkm_barrier<LPW2>();
+    else wait_vm_lgkm_barrier<0>();
+  };
+  static_assert(NS1 <= 3 && NS2 <= 4, "wait1/wait2 cover these depths");
+
+  // ---- Z^T = W_F x^T over Dcat
+#pragma unroll
+  for (int s = 0; s < NS1; ++s)
+    if (s < nk1) issue1(s);
+  zero();
+  run(nk1, NS1, std::integral_constant<int, BK1 / 16>{}, issue1, load1, wait1);
+  wait_vm_lgkm_barrier<0>();   // every wavefront is done with the F ring
+  asm volatile("" : "+v"(fe_mine));
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) asm volatile("" : "+v"(rdst[tm]), "+v"(rpos[tm]));
+  fe_lds[tid] = fe_mine;
+  __syncthreads();
+
+  // the K/V weights start streaming into the ring behind Z meanwhile
+#pragma unroll
+  for (int s = 0; s < NS2; ++s) issue2(s);
+
+  // Z rows to LDS as bf16; carried rows get F(E) (added in fp32 before rounding)
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int n = wave * 64 + tn * 32 + 8 * q + 4 * (lane >> 5);
+      const f32x4 fe = *reinterpret_cast<const f32x4*>(fe_lds + n);
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) {
+        const bool carried = is_carry_row(rdst[tm]);
+        u16x4 v;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = f2bf(acc[tn][tm][4 * q + j] + (carried ? fe[j] : 0.f));
+        *reinterpret_cast<u16x4*>(smem + (tm * 32 + (lane & 31)) * kFusedZLD + n * 2) = v;
+      }
+    }
+
+  // ---- K/V^T = W_KV Z^T over d
+  zero();
+  run(nk2, NS2, std::integral_constant<int, BK2 / 16>{}, issue2, load2, wait2);
+
+  // ---- rotate keys at the row's position and store every row to its slot
+  // (stores of a few bytes per lane: staging the rows in LDS for full-line
+  // stores measured no faster, the write burst at the end of the kernel is
+  // what this phase waits on)
+  const int i_base = 4 * (lane >> 5);
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    const int row = m0 + tm * 32 + (lane & 31);
+    if (row >= M) continue;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float lo[4], hi[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        lo[j] = acc[0][tm][4 * q + j];
+        hi[j] = acc[1][tm][4 * q + j];
+      }
+      kv_store<uint16_t, 4>(a.dst, row, rdst[tm], rpos[tm], wave, 8 * q + i_base, lo, hi, inv_tab);
+    }
+  }
 }
 
 // -------------------------------------------- epilogues over fp32 partials
@@ -844,15 +1100,38 @@ void pick_gemm(int M, int N, int K, bool kv, int hd, int num_cus, int* tile, int
 
 }  // namespace
 
+constexpr int kF32SplitK = 64;   // K per split of the fp32 GEMM
+
+// Rows from which the fused small-width projection is used: below, the K-split
+// two-product path spreads the weight reads over more workgroups.
+static int fused_min_rows() {
+  if (getenv("CO_PROJECT_NO_FUSED")) return INT32_MAX;          // test override
+  if (const char* env = getenv("CO_PROJECT_FUSED_MIN_ROWS")) {   // test and tuning override
+    const int v = atoi(env);
+    if (v >= 1) return v;
+  }
+  return 4096;
+}
+
+static int f32_splits(int K) {
+  const int s = (K + kF32SplitK - 1) / kF32SplitK;
+  return s < 1 ? 1 : (s > 32 ? 32 : s);
+}
+
 ProjectPlan plan_project(int M, int Dcat, int d, int n_kv, int hd, int dtype, int num_cus) {
   ProjectPlan p{};
   const size_t es = dtype == CO_DTYPE_BF16 ? 2 : 4;
+  p.fused = dtype == CO_DTYPE_BF16 && d == kFusedD && n_kv == kFusedD && hd == 64 &&
+            Dcat % 64 == 0 && M >= fused_min_rows();
   if (dtype == CO_DTYPE_BF16) {
     pick_gemm(M, d, Dcat, false, hd, num_cus, &p.f_tile, &p.f_split);
     pick_gemm(M, n_kv, d, true, hd, num_cus, &p.kv_tile, &p.kv_split);
   } else {
+    // fp32: K split in pieces of two 32-deep steps, so that few dependent load
+    // rounds lie on any workgroup's path (the shapes it serves are latency-bound)
     p.f_tile = p.kv_tile = -1;
-    p.f_split = p.kv_split = 1;
+    p.f_split = f32_splits(Dcat);
+    p.kv_split = f32_splits(d);
   }
   auto part = [&](int split, int N) -> size_t {
     return (dtype == CO_DTYPE_F32 || split > 1) ? static_cast<size_t>(split) * M * N * 4 : 0;
@@ -884,24 +1163,31 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
   kv.partial = part; kv.z_out = nullptr; kv.kv = a.dst;
 
   if (a.dtype == CO_DTYPE_F32) {
-    f.k_per_split = f.K;
-    kv.k_per_split = kv.K;
+    f.k_per_split = ((f.K + p.f_split - 1) / p.f_split + 31) / 32 * 32;
+    kv.k_per_split = ((kv.K + p.kv_split - 1) / p.kv_split + 31) / 32 * 32;
+    const int fs = (f.K + f.k_per_split - 1) / f.k_per_split;
+    const int ks = (kv.K + kv.k_per_split - 1) / kv.k_per_split;
     f.mode = kv.mode = kModePartial;
-    hipLaunchKernelGGL(gemm_f32_kernel, dim3((f.N + 63) / 64, (f.M + 31) / 32), dim3(256), 0,
+    hipLaunchKernelGGL(gemm_f32_kernel, dim3((f.N + 63) / 64, (f.M + 31) / 32, fs), dim3(256), 0,
                        stream, f);
     const int64_t nz = static_cast<int64_t>(a.M) * a.d / 4;
     hipLaunchKernelGGL(epi_z_kernel<float>, dim3(static_cast<unsigned>((nz + 255) / 256)),
-                       dim3(256), 0, stream, part, 1, a.M, a.d, static_cast<float*>(z),
+                       dim3(256), 0, stream, part, fs, a.M, a.d, static_cast<float*>(z),
                        static_cast<const float*>(nullptr), static_cast<const float*>(nullptr),
                        a.dst.row_dst);
-    hipLaunchKernelGGL(gemm_f32_kernel, dim3((kv.N + 63) / 64, (kv.M + 31) / 32), dim3(256), 0,
-                       stream, kv);
+    hipLaunchKernelGGL(gemm_f32_kernel, dim3((kv.N + 63) / 64, (kv.M + 31) / 32, ks), dim3(256),
+                       0, stream, kv);
     const int64_t items = static_cast<int64_t>(a.M) * (n_kv / 2);
     hipLaunchKernelGGL(epi_kv_kernel<float>, dim3(static_cast<unsigned>((items + 255) / 256)),
-                       dim3(256), 0, stream, part, 1, a.M, n_kv, a.dst);
+                       dim3(256), 0, stream, part, ks, a.M, n_kv, a.dst);
     return hipGetLastError();
   }
 
+  if (p.fused && (a.fe != nullptr || a.e == nullptr)) {   // F(E) folded, or no E at all
+    hipLaunchKernelGGL(proj_fused_kernel, dim3((a.M + kFusedBM - 1) / kFusedBM), dim3(256), 0,
+                       stream, a);
+    return hipGetLastError();
+  }
   if (a.fe != nullptr) {   // F(E) folded beforehand: the GEMM carries no E
     f.e = nullptr;
     f.fe = a.fe;

@@ -19,7 +19,9 @@ EDGE = wl.RAGGED32.replace(name="edge", S=4, L=2, ctx_lo=40, ctx_hi=900, rounds=
                            accept=("geom", 0.25), seed=0x5EED10)
 # one drafter layer (K/V width 256): the shape of the batch-32 serving workload
 EDGE1 = EDGE.replace(name="edge_l1", L=1, seed=0x5EED11)
-BOTH = pytest.mark.parametrize("w", [EDGE, EDGE1], ids=lambda w: w.name)
+# the fp32 path (chunked attention, split-K fp32 GEMM) on the same cases
+EDGE_F32 = EDGE.replace(name="edge_f32", dtype="f32", seed=0x5EED12)
+BOTH = pytest.mark.parametrize("w", [EDGE, EDGE1, EDGE_F32], ids=lambda w: w.name)
 
 
 def _gpu():

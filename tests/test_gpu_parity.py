@@ -298,11 +298,7 @@ TRAIN_SMALL = wl.TRAIN_FWD.replace(name="train_small", S=2, seq_len=512, anchors
                                    seed=0x5EED09)
 
 
-@pytest.mark.parametrize("shared", [True, False], ids=["shared_prefix", "persistent"])
-@pytest.mark.parametrize("split", ["", "3"], ids=lambda v: f"share{v or 'dflt'}")
-def test_train_small_full(shared, split, monkeypatch):
-    if split:
-        monkeypatch.setenv("CO_ATTN_GROUP_SPLIT_TILES", split)
+def train_small_check(shared):
     from helpers import OracleTrain
     _gpu()
     from synth.scenario import TrainScenario
@@ -322,3 +318,39 @@ def test_train_small_full(shared, split, monkeypatch):
         assert_heads_close(g[:, v], orc.O[:, v], tol, f"O v{v}")
         err = np.abs(gl[:, v] - orc.LSE[:, v]).max()
         assert err <= tol, f"LSE v{v}: {err}"
+        nu = int(orc.rr["carry_len"][v])
+        if nu:
+            gk, gv = gather_carry(sc.vst, v, 0, nu)
+            assert_heads_close(gk, orc.st.uk[v][0], tol, f"U_k v{v}")
+            assert_heads_close(gv, orc.st.uv[v][0], tol, f"U_v v{v}")
+    for s, (k, vv) in orc.parent.items():
+        gk, gv = gather_committed(sc.st, sc.pt, s, 0, 0, w.seq_len)
+        assert_heads_close(gk, k[:, 0], tol, f"prefill K s{s}")
+        assert_heads_close(gv, vv[:, 0], tol, f"prefill V s{s}")
+
+
+@pytest.mark.parametrize("shared", [True, False], ids=["shared_prefix", "persistent"])
+@pytest.mark.parametrize("split", ["", "3"], ids=lambda v: f"share{v or 'dflt'}")
+def test_train_small_full(shared, split, monkeypatch):
+    if split:
+        monkeypatch.setenv("CO_ATTN_GROUP_SPLIT_TILES", split)
+    train_small_check(shared)
+
+
+# The fused small-width projection (both products in one kernel, Z in LDS),
+# forced at small row counts: 80 rows (one partial 128-row block), the 512
+# rows of the batch-32 round, and the committed and block calls of a small
+# training-shaped forward.
+FUSED_RAGGED = wl.RAGGED32.replace(name="fused_ragged", S=5, ctx_lo=100, ctx_hi=1500, rounds=3,
+                                   seed=0x5EED0A)
+
+
+@pytest.mark.parametrize("w", [FUSED_RAGGED, wl.RAGGED32], ids=lambda w: w.name)
+def test_fused_projection(w, monkeypatch):
+    monkeypatch.setenv("CO_PROJECT_FUSED_MIN_ROWS", "1")
+    run_rounds(w, 2)
+
+
+def test_fused_projection_train_small(monkeypatch):
+    monkeypatch.setenv("CO_PROJECT_FUSED_MIN_ROWS", "1")
+    train_small_check(True)
