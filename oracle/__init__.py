@@ -20,6 +20,13 @@ the "Cache semantics" paragraph; Section 2 "Preliminaries"):
   with a plain softmax; the baseline update (left column of Algorithm 1)
   projects only rows 0..m-1 and has no U.
 
+Variants next to the path: stochastic verification (T = 1), where m is the run
+of positions the verifier accepted by rejection sampling (Appendix A, "Why
+verification remains valid"); the separate-projector update, where carried
+rows go through a second fusion matrix instead of F + E (Section 4, Table
+3(b)); and the share of attention that falls on the carried rows (Appendix
+"Attention to carried states").
+
 Readings where the paper is silent (each one a stated choice of this oracle): no norm
 and no bias in F, K_l, V_l; rotate-half RoPE with inverse frequency
 theta^(-2i/hd); softmax scale 1/sqrt(hd); query head h reads KV head
@@ -53,12 +60,26 @@ def accept_len(draft: np.ndarray, target: np.ndarray) -> int:
     return m
 
 
-def route(draft, target, ctx_len, carry_len, page_table, num_pages, mode="carry"):
+def accept_len_bits(bits: np.ndarray) -> int:
+    """Stochastic verification (T = 1): the verifier decides acceptance of each
+    proposal by rejection sampling (Appendix A, "Why verification remains
+    valid"); the accepted prefix is the run of accepted positions before the
+    first rejection.  bits[j] != 0 means position j was accepted."""
+    m = 0
+    while m < len(bits) and bits[m] != 0:
+        m += 1
+    return m
+
+
+def route(draft, target, ctx_len, carry_len, page_table, num_pages, mode="carry",
+          accept="tokens"):
     """Split every verified window by its accepted prefix (Eq. 1, Algorithm 1).
 
     mode: 'carry' (Carryover column), 'baseline' (Baseline column),
     'accept_all' (every row committed: building context by prefill),
     'carry_only' (rows 0..m-1 are already committed elsewhere and are skipped).
+    accept: 'tokens' (greedy: draft vs target tokens) or 'bits' (``draft``
+    holds the verifier's per-position accept decisions, ``target`` is unused).
 
     Returns a dict with accept_len [S], row_pos [S][B], row_dst [S][B]
     (>= 0: global committed slot page*16 + pos % 16; -1-r: carry row r;
@@ -75,7 +96,12 @@ def route(draft, target, ctx_len, carry_len, page_table, num_pages, mode="carry"
     cap = page_table.shape[1] * PAGE
     for s in range(S):
         p0 = int(ctx_len[s])
-        m = B if mode == "accept_all" else accept_len(draft[s], target[s])
+        if mode == "accept_all":
+            m = B
+        elif accept == "bits":
+            m = accept_len_bits(draft[s])
+        else:
+            m = accept_len(draft[s], target[s])
         if p0 < 0:
             out["status"][s] = ERR_LENGTH
         elif p0 + B > cap:
@@ -123,17 +149,25 @@ def rope(x: np.ndarray, pos, theta: float) -> np.ndarray:
     return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
 
 
-def project(H, E, add_e, WF, WKV, pos, L, Hkv, hd, theta):
+def project(H, E, add_e, WF, WKV, pos, L, Hkv, hd, theta, WF_carry=None):
     """Phi_l(H) of Eq. 1 for every layer, with E added to flagged rows before F
     (Eq. 2) and RoPE applied to the keys at each row's position.
 
     H [M][Dcat], E [Dcat], add_e [M] (bool), WF [d][Dcat], WKV [L*2*Hkv*hd][d]
     ordered (layer, K|V, head, dim), pos [M].
+    WF_carry [d][Dcat]: the separate-projector variant (Section 4, "How should
+    rejected states be distinguished?"; Table 3(b)): flagged rows are projected
+    by this second fusion matrix instead of F, with no E.
     Returns K, V as [M][L][Hkv][hd] float64.
     """
     H = np.asarray(H, np.float64)
-    x = H + np.asarray(add_e, np.float64)[:, None] * np.asarray(E, np.float64)[None, :]
-    z = x @ np.asarray(WF, np.float64).T                         # F
+    flag = np.asarray(add_e, bool)
+    if WF_carry is None:
+        x = H + flag[:, None].astype(np.float64) * np.asarray(E, np.float64)[None, :]
+        z = x @ np.asarray(WF, np.float64).T                     # F
+    else:
+        z = np.where(flag[:, None], H @ np.asarray(WF_carry, np.float64).T,
+                     H @ np.asarray(WF, np.float64).T)
     kv = (z @ np.asarray(WKV, np.float64).T).reshape(len(H), L, 2, Hkv, hd)
     k = rope(kv[:, :, 0], np.asarray(pos)[:, None, None], theta)
     return k, kv[:, :, 1].copy()
@@ -154,6 +188,22 @@ def attend(q, qpos, k, v, theta):
     w = np.exp(s - mx)
     den = w.sum(axis=1, keepdims=True)
     return (w @ np.asarray(v, np.float64)) / den, (mx + np.log(den))[:, 0]
+
+
+def carry_mass(q, qpos, k_committed, k_carry, theta):
+    """Share of each query's softmax attention that falls on the carried rows
+    (the diagnostic of Appendix "Attention to carried states"): the weights of
+    the attention over [C;U] summed over U.  q [nq][hd] unrotated at qpos; keys
+    already rotated.  Zero when there are no keys at all."""
+    q = rope(np.asarray(q, np.float64), np.asarray(qpos), theta)
+    nq, hd = q.shape
+    kc = np.asarray(k_committed, np.float64).reshape(-1, hd)
+    ku = np.asarray(k_carry, np.float64).reshape(-1, hd)
+    if len(kc) + len(ku) == 0:
+        return np.zeros(nq)
+    s = (q @ np.concatenate([kc, ku], axis=0).T) / math.sqrt(hd)
+    w = np.exp(s - s.max(axis=1, keepdims=True))
+    return w[:, len(kc):].sum(axis=1) / w.sum(axis=1)
 
 
 # ------------------------------------------------------------ drafter state
@@ -217,9 +267,31 @@ def attend_state(state: State, Q, Hq, theta, seqs=None, layers=None):
     return O, LSE
 
 
-def round_update(state: State, r, H, E, WF, WKV, theta, mode="carry", seqs=None):
+def carry_mass_state(state: State, Q, Hq, theta, seqs=None, layers=None):
+    """carry_mass of every (layer, sequence, query row, query head) over the
+    state's [C;U]; query i sits at ctx_len + i.  Returns [L][S][B][Hq] (NaN
+    where not computed)."""
+    L, S, B, _, hd = Q.shape
+    G = Hq // state.Hkv
+    out = np.full(Q.shape[:-1], np.nan)
+    ctx = state.ctx_len()
+    for s in (range(S) if seqs is None else seqs):
+        for layer in (range(L) if layers is None else layers):
+            for g in range(state.Hkv):
+                heads = list(range(g * G, (g + 1) * G))
+                q = Q[layer, s][:, heads].reshape(B * G, hd)
+                qpos = np.repeat(ctx[s] + np.arange(B), G)
+                mass = carry_mass(q, qpos, state.ck[s][layer, :, g], state.uk[s][layer, :, g],
+                                  theta)
+                out[layer, s][:, heads] = mass.reshape(B, G)
+    return out
+
+
+def round_update(state: State, r, H, E, WF, WKV, theta, mode="carry", seqs=None,
+                 WF_carry=None):
     """Post-verification update of Algorithm 1 for the sequences in ``seqs``,
-    given a route result ``r`` (see ``route``).  H [S][B][Dcat]."""
+    given a route result ``r`` (see ``route``).  H [S][B][Dcat].  With
+    ``WF_carry`` the carried rows use the separate projector (see project)."""
     S, B, _ = H.shape
     for s in (range(S) if seqs is None else seqs):
         if not r["touched"][s]:
@@ -228,7 +300,7 @@ def round_update(state: State, r, H, E, WF, WKV, theta, mode="carry", seqs=None)
         rows = np.arange(B) if mode in ("carry", "carry_only") else np.arange(m)
         pos = r["row_pos"][s][rows]
         k, v = project(H[s][rows], E, rows >= m, WF, WKV, pos, state.L, state.Hkv,
-                       state.hd, theta)
+                       state.hd, theta, WF_carry)
         if mode == "carry_only":
             k_acc, v_acc = k[:0], v[:0]
         else:

@@ -418,3 +418,121 @@ def test_baseline_differs_when_rows_are_rejected():
     a = _run_incremental(t, ctx0, rounds, "carry")
     b = _run_incremental(t, ctx0, rounds, "baseline")
     assert np.abs(a[0][1] - b[0][1]).max() > 1e-3
+
+
+# ------------------------------------------------ stochastic verification (T = 1)
+
+def test_accept_bits_give_the_run_before_the_first_rejection():
+    """With accept decisions made by the verifier (rejection sampling at T = 1),
+    m is the number of leading accepted positions, whatever follows the first
+    rejection; bits built from a chosen m return exactly m, for every m."""
+    for B in (1, 4, 8, 16):
+        for m in range(B + 1):
+            for _ in range(3):
+                bits = RNG.integers(0, 2, B)
+                bits[:m] = RNG.integers(1, 5, m)       # any nonzero value accepts
+                if m < B:
+                    bits[m] = 0
+                assert oracle.accept_len_bits(bits) == m
+
+
+def test_accept_bits_route_equals_token_route():
+    """Greedy verification is the special case whose accept decision at each
+    position is 'draft token equals target token': routing by those decisions
+    gives exactly the token route (descriptors, lengths, status)."""
+    w = wl.TINY.replace(B=8, S=9, rounds=2)
+    pt = wl.page_table(w)
+    ctx = wl.initial_ctx(w)
+    m = np.arange(9, dtype=np.int32)
+    draft, target = wl.tokens_for(w, 0, m)
+    a = oracle.route(draft, target, ctx, np.zeros(9, np.int32), pt, pt.size)
+    b = oracle.route((draft == target).astype(np.int32), None, ctx, np.zeros(9, np.int32), pt,
+                     pt.size, accept="bits")
+    for key in a:
+        np.testing.assert_array_equal(a[key], b[key], err_msg=key)
+    np.testing.assert_array_equal(b["accept_len"], m)
+
+
+# --------------------------------------------------- separate projector (Table 3(b))
+
+def _proj_case():
+    L, Hkv, hd, Dcat, d = 2, 2, 16, 48, 32
+    H = RNG.standard_normal((5, Dcat))
+    E = RNG.standard_normal(Dcat)
+    WF = RNG.standard_normal((d, Dcat))
+    WKV = RNG.standard_normal((2 * L * Hkv * hd, d))
+    pos = np.arange(20, 25)
+    flag = np.array([False, False, True, True, True])
+    return L, Hkv, hd, H, E, WF, WKV, pos, flag
+
+
+def test_separate_projector_with_f_itself_is_the_no_embedding_update():
+    """A separate projector equal to F, with no embedding, projects carried
+    rows exactly like committed ones."""
+    L, Hkv, hd, H, E, WF, WKV, pos, flag = _proj_case()
+    k1, v1 = oracle.project(H, E, flag, WF, WKV, pos, L, Hkv, hd, 1e4, WF_carry=WF)
+    k0, v0 = oracle.project(H, E, np.zeros(5, bool), WF, WKV, pos, L, Hkv, hd, 1e4)
+    np.testing.assert_allclose(k1, k0, rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(v1, v0, rtol=1e-13, atol=1e-13)
+
+
+def test_separate_projector_touches_only_carried_rows_and_is_linear():
+    """Committed rows ignore the separate projector; carried rows ignore E and F
+    and scale with the projector (everything after it is linear)."""
+    L, Hkv, hd, H, E, WF, WKV, pos, flag = _proj_case()
+    WC = RNG.standard_normal(WF.shape)
+    ka, va = oracle.project(H, E, flag, WF, WKV, pos, L, Hkv, hd, 1e4, WF_carry=WC)
+    kb, vb = oracle.project(H, E, flag, WF, WKV, pos, L, Hkv, hd, 1e4, WF_carry=3.0 * WC)
+    kc, vc = oracle.project(H, 5.0 * E, flag, 2.0 * WF, WKV, pos, L, Hkv, hd, 1e4, WF_carry=WC)
+    kd, vd = oracle.project(H, E, np.zeros(5, bool), WF, WKV, pos, L, Hkv, hd, 1e4)
+    np.testing.assert_allclose(ka[~flag], kd[~flag], rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(va[~flag], vd[~flag], rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(kb[flag], 3.0 * ka[flag], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(vb[flag], 3.0 * va[flag], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(kc[flag], ka[flag], rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(vc[flag], va[flag], rtol=1e-13, atol=1e-13)
+
+
+# --------------------------------------------- attention mass on carried rows
+
+def test_carry_mass_empty_and_full_segments():
+    q = RNG.standard_normal((6, 16))
+    k = RNG.standard_normal((9, 16))
+    qpos = np.arange(30, 36)
+    np.testing.assert_array_equal(oracle.carry_mass(q, qpos, k, k[:0], 1e4), np.zeros(6))
+    np.testing.assert_allclose(oracle.carry_mass(q, qpos, k[:0], k, 1e4), np.ones(6), rtol=1e-15)
+    np.testing.assert_array_equal(oracle.carry_mass(q, qpos, k[:0], k[:0], 1e4), np.zeros(6))
+
+
+def test_carry_mass_of_identical_keys_is_the_carried_share():
+    """Equal logits everywhere: every key gets 1/n of the weight."""
+    q = RNG.standard_normal((4, 16))
+    k = np.tile(RNG.standard_normal(16), (11, 1))
+    mass = oracle.carry_mass(q, np.arange(4), k[:7], k[7:], 1e4)
+    np.testing.assert_allclose(mass, np.full(4, 4 / 11), rtol=1e-14)
+
+
+def test_carry_mass_equals_exp_of_segment_lse_difference():
+    """Mass on U = exp(LSE over U alone - LSE over [C;U]), with both LSEs taken
+    from the plain attention; the committed share is its complement."""
+    q = RNG.standard_normal((5, 32))
+    kc, ku = RNG.standard_normal((13, 32)), RNG.standard_normal((6, 32))
+    v = RNG.standard_normal((19, 32))
+    qpos = np.arange(100, 105)
+    _, lse_all = oracle.attend(q, qpos, np.concatenate([kc, ku]), v, 1e4)
+    _, lse_u = oracle.attend(q, qpos, ku, v[13:], 1e4)
+    _, lse_c = oracle.attend(q, qpos, kc, v[:13], 1e4)
+    mass = oracle.carry_mass(q, qpos, kc, ku, 1e4)
+    np.testing.assert_allclose(mass, np.exp(lse_u - lse_all), rtol=1e-12)
+    np.testing.assert_allclose(1.0 - mass, np.exp(lse_c - lse_all), rtol=1e-10)
+
+
+def test_carry_mass_one_dominant_carried_logit():
+    hd = 8
+    q = np.zeros((1, hd))
+    q[0, 0] = 1.0
+    kc = np.zeros((5, hd))
+    ku = np.zeros((2, hd))
+    ku[1, 0] = 200.0                   # at position 0 the query is not rotated
+    mass = oracle.carry_mass(q, np.array([0]), kc, ku, 1e4)
+    assert 1.0 - mass[0] < 1e-15
