@@ -90,6 +90,11 @@ enum { CO_DTYPE_F32 = 0, CO_DTYPE_BF16 = 1 };
                                          per group of four (head_dim 64, or head_dim 128 with up
                                          to 32 query rows per KV head; other shapes ignore the
                                          flag).  Results do not depend on the flag.             */
+#define CO_ROUTE_ACCEPT_BITS (1u << 5)  /* stochastic verification (T = 1): draft_tok holds the
+                                         verifier's accept decision of every position (non-zero
+                                         = accepted by its rejection sampling), target_tok is
+                                         unused and may be NULL; m = the accepted positions
+                                         before the first rejection                             */
 
 typedef struct co_dims {
   int32_t num_seqs;           /* S: sequences in the batch                           */
@@ -113,6 +118,12 @@ typedef struct co_weights {
   const void* e_carry;        /* E_carry: [feat_dim]                       */
   const float* f_e;           /* optional F e_carry, fp32 [model_dim], from carryover_fold_e;
                                  NULL: computed within every bf16 projection           */
+  const void* w_f_carry;      /* optional separate projector for carried rows,
+                                 [model_dim][feat_dim] (Section 4, "How should rejected
+                                 states be distinguished?", Table 3(b)): when non-NULL,
+                                 rows routed to the carry segment are projected by it
+                                 instead of by F with E_carry (e_carry and f_e unused;
+                                 costs a second F product)                            */
 } co_weights;
 
 typedef struct co_state {
@@ -137,7 +148,10 @@ typedef struct co_route {
  * Route (Algorithm 1 "Given"; greedy verification, Section 2
  * "Preliminaries").  For every sequence s: m = length of the longest prefix on
  * which draft_tok[s][:] equals target_tok[s][:] (m = block with
- * CO_ROUTE_ACCEPT_ALL, where the token pointers may be NULL); p0 = ctx_len[s];
+ * CO_ROUTE_ACCEPT_ALL, where the token pointers may be NULL; with
+ * CO_ROUTE_ACCEPT_BITS, the run of non-zero accept decisions in draft_tok at the
+ * start of the window, Appendix A "Why verification remains valid");
+ * p0 = ctx_len[s];
  * window row j sits at position p0 + j.  Rows j < m go to the committed slot of
  * position p0 + j (skipped under CO_ROUTE_CARRY_ONLY); rows j >= m become carry
  * row j - m (skipped under CO_BASELINE_MODE).  Then ctx_len[s] = p0 + m and
@@ -202,6 +216,25 @@ co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int3
  * is no host synchronisation.  `ws`: carryover_workspace_bytes(dims,
  * CO_WS_ROUND) bytes of scratch.
  */
+/*
+ * Attention mass on the carried rows (the diagnostic of Appendix "Attention to
+ * carried states"; for the carry segment U of ctx = [C;U], Eq. 2).  For every
+ * (layer, sequence, block row i, query head h) of a drafter_block_attention
+ * call made with the same dims, layers, q, state and CO_Q_PREROTATED flag:
+ * mass = the sum over U of the softmax weights = exp(LSE_U - LSE), where LSE is
+ * that call's LSE output (natural log) and LSE_U the log-sum-exp of the scaled
+ * logits over the carry keys alone; 0 when U is empty or no key exists.
+ * q as for drafter_block_attention; lse (input) and mass (output) fp32
+ * [layer_count][num_seqs][block][num_q_heads].  flags: CO_Q_PREROTATED.
+ * Enqueue after the attention call, before anything changes the state.
+ * Supported shapes: those of drafter_block_attention with block <= 64.
+ * Device errors: CO_ERR_LENGTH (a negative length, or carry_len > the carry
+ * segment); that sequence's mass is then 0.
+ */
+co_status drafter_carry_mass(const co_dims* dims, int32_t layer_begin, int32_t layer_count,
+                             const void* q, const co_state* state, const float* lse, float* mass,
+                             uint32_t flags, hipStream_t stream);
+
 co_status carryover_round(const co_dims* dims, const co_weights* w, const void* hidden,
                           const int32_t* draft_tok, const int32_t* target_tok, const void* q,
                           co_state* state, const co_route* scratch, void* out, float* lse,

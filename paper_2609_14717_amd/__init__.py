@@ -20,6 +20,7 @@ CO_ERR_CAPACITY, CO_ERR_PAGE_RANGE, CO_ERR_HIP, CO_ERR_LENGTH = 4, 5, 6, 7
 CO_DTYPE_F32, CO_DTYPE_BF16 = 0, 1
 CO_BASELINE_MODE, CO_ROUTE_ACCEPT_ALL, CO_ROUTE_CARRY_ONLY, CO_Q_PREROTATED = 1, 2, 4, 8
 CO_ATTN_SHARED_PREFIX = 16
+CO_ROUTE_ACCEPT_BITS = 32
 CO_WS_PROJECT, CO_WS_ATTENTION, CO_WS_ROUND = 0, 1, 2
 SKIP = -(2 ** 31)
 PAGE = 16
@@ -43,7 +44,7 @@ class co_dims(ctypes.Structure):
 
 class co_weights(ctypes.Structure):
     _fields_ = [("w_f", ctypes.c_void_p), ("w_kv", ctypes.c_void_p), ("e_carry", ctypes.c_void_p),
-                ("f_e", ctypes.c_void_p)]
+                ("f_e", ctypes.c_void_p), ("w_f_carry", ctypes.c_void_p)]
 
 
 class co_state(ctypes.Structure):
@@ -81,6 +82,8 @@ def lib():
             "carryover_round": [_P(co_dims), _P(co_weights), _v, _v, _v, _v, _P(co_state),
                                 _P(co_route), _v, _v, ctypes.c_uint32, _v, ctypes.c_size_t, _v],
             "carryover_fold_e": [_P(co_dims), _P(co_weights), _v, _v],
+            "drafter_carry_mass": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, _v, _P(co_state),
+                                   _v, _v, ctypes.c_uint32, _v],
             "carryover_import_kv": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _v,
                                     _v, _P(co_state), _v],
             "carryover_workspace_bytes": [_P(co_dims), ctypes.c_int32],
@@ -98,8 +101,8 @@ def lib():
 
 
 EXPORTED = ("carryover_route", "carryover_project_kv", "drafter_block_attention",
-            "carryover_round", "carryover_fold_e", "carryover_import_kv", "carryover_workspace_bytes",
-            "carryover_read_status", "carryover_status_string")
+            "carryover_round", "carryover_fold_e", "drafter_carry_mass", "carryover_import_kv",
+            "carryover_workspace_bytes", "carryover_read_status", "carryover_status_string")
 
 
 def _ptr(x):
@@ -134,9 +137,10 @@ def make_dims(S, B, Dcat, d, L, Hq, Hkv, hd, max_pages_per_seq, num_pages, dtype
                    float(theta))
 
 
-def weights(w_f, w_kv, e_carry, f_e=None):
-    """co_weights over device tensors; f_e (fp32 [model_dim], optional) from ``carryover_fold_e``."""
-    return co_weights(_ptr(w_f), _ptr(w_kv), _ptr(e_carry), _ptr(f_e))
+def weights(w_f, w_kv, e_carry, f_e=None, w_f_carry=None):
+    """co_weights over device tensors; f_e (fp32 [model_dim], optional) from
+    ``carryover_fold_e``; w_f_carry (optional) the separate carry projector."""
+    return co_weights(_ptr(w_f), _ptr(w_kv), _ptr(e_carry), _ptr(f_e), _ptr(w_f_carry))
 
 
 def state(t):
@@ -205,6 +209,13 @@ def drafter_block_attention(dims, layer_begin, layer_count, q, st, out, lse, fla
     _check(lib().drafter_block_attention(ctypes.byref(dims), layer_begin, layer_count, _ptr(q),
                                          ctypes.byref(s), _ptr(out), _ptr(lse), flags, _ptr(ws),
                                          nb, _stream(stream)), "drafter_block_attention")
+
+
+def drafter_carry_mass(dims, layer_begin, layer_count, q, st, lse, mass, flags=0, stream=None):
+    s = state(st)
+    _check(lib().drafter_carry_mass(ctypes.byref(dims), layer_begin, layer_count, _ptr(q),
+                                    ctypes.byref(s), _ptr(lse), _ptr(mass), flags,
+                                    _stream(stream)), "drafter_carry_mass")
 
 
 def carryover_round(dims, w, hidden, draft_tok, target_tok, q, st, rt, out, lse, flags, ws,

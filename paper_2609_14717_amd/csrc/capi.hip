@@ -159,7 +159,9 @@ co_status carryover_route(const co_dims* dims, const int32_t* draft_tok, const i
   if (!state || !state->ctx_len || !state->carry_len || !state->page_table || !state->status ||
       !route_ok(out))
     return CO_ERR_INVALID_ARG;
-  if (!(flags & CO_ROUTE_ACCEPT_ALL) && (!draft_tok || !target_tok)) return CO_ERR_INVALID_ARG;
+  if (!(flags & CO_ROUTE_ACCEPT_ALL) &&
+      (!draft_tok || (!target_tok && !(flags & CO_ROUTE_ACCEPT_BITS))))
+    return CO_ERR_INVALID_ARG;
   RouteArgs a{};
   a.S = dims->num_seqs;
   a.B = dims->block;
@@ -186,7 +188,7 @@ co_status carryover_project_kv(const co_dims* dims, const co_weights* w, const v
   if (!w || !w->w_f || !w->w_kv || !w->e_carry || !hidden || !route_ok(route) || !state_ok(state))
     return CO_ERR_INVALID_ARG;
   if (!aligned(hidden, 16) || !aligned(w->w_f, 16) || !aligned(w->w_kv, 16) ||
-      !aligned(w->e_carry, 16) || !aligned(w->f_e, 16))
+      !aligned(w->e_carry, 16) || !aligned(w->f_e, 16) || !aligned(w->w_f_carry, 16))
     return CO_ERR_INVALID_ARG;
   const ProjectPlan p = project_plan(dims);
   if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
@@ -201,6 +203,7 @@ co_status carryover_project_kv(const co_dims* dims, const co_weights* w, const v
   a.wkv = w->w_kv;
   a.e = w->e_carry;
   a.fe = dims->dtype == CO_DTYPE_BF16 ? w->f_e : nullptr;
+  a.wfc = w->w_f_carry;
   a.dst = make_dest(dims, route, state);
   a.ws = ws;
   return hip_status(launch_project(a, p, stream));
@@ -234,6 +237,38 @@ co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int3
   return do_attention(dims, layer_begin, layer_count, q, state, out, lse, flags, ws, stream);
 }
 
+co_status drafter_carry_mass(const co_dims* dims, int32_t layer_begin, int32_t layer_count,
+                             const void* q, const co_state* state, const float* lse, float* mass,
+                             uint32_t flags, hipStream_t stream) {
+  co_status s = check_dims(dims);
+  if (s != CO_OK) return s;
+  if ((s = check_attention_dims(dims)) != CO_OK) return s;
+  if (dims->block > kMaxCarryRows) return CO_ERR_UNSUPPORTED;
+  if (layer_begin < 0 || layer_count < 0 || layer_begin + layer_count > dims->num_layers)
+    return CO_ERR_INVALID_ARG;
+  if (!q || !lse || !mass || !state_ok(state) || !aligned(q, 16) || !aligned(lse, 4) ||
+      !aligned(mass, 4))
+    return CO_ERR_INVALID_ARG;
+  MassArgs a{};
+  a.S = dims->num_seqs;
+  a.B = dims->block;
+  a.layer_begin = layer_begin;
+  a.Hq = dims->num_q_heads;
+  a.Hkv = dims->num_kv_heads;
+  a.hd = dims->head_dim;
+  a.CP = (dims->block + kPage - 1) / kPage;
+  a.flags = flags;
+  fill_rope_table(a.rope_inv, dims);
+  a.q = q;
+  a.ctx_len = state->ctx_len;
+  a.carry_len = state->carry_len;
+  a.k_carry = state->k_carry;
+  a.lse = lse;
+  a.mass = mass;
+  a.status = state->status;
+  return hip_status(launch_carry_mass(a, layer_count, dims->dtype, stream));
+}
+
 co_status carryover_round(const co_dims* dims, const co_weights* w, const void* hidden,
                           const int32_t* draft_tok, const int32_t* target_tok, const void* q,
                           co_state* state, const co_route* scratch, void* out, float* lse,
@@ -244,7 +279,9 @@ co_status carryover_round(const co_dims* dims, const co_weights* w, const void* 
   if (!w || !w->w_f || !w->w_kv || !w->e_carry || !hidden || !q || !out || !route_ok(scratch) ||
       !state_ok(state))
     return CO_ERR_INVALID_ARG;
-  if (!(flags & CO_ROUTE_ACCEPT_ALL) && (!draft_tok || !target_tok)) return CO_ERR_INVALID_ARG;
+  if (!(flags & CO_ROUTE_ACCEPT_ALL) &&
+      (!draft_tok || (!target_tok && !(flags & CO_ROUTE_ACCEPT_BITS))))
+    return CO_ERR_INVALID_ARG;
   if (!aligned(hidden, 16) || !aligned(w->w_f, 16) || !aligned(w->w_kv, 16) ||
       !aligned(w->e_carry, 16) || !aligned(q, 16) || !aligned(out, 16))
     return CO_ERR_INVALID_ARG;

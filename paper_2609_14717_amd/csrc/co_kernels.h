@@ -45,6 +45,7 @@ struct ProjectArgs {
   const void* wkv;
   const void* e;
   const float* fe;   // precomputed F(E) [d] (bf16 path), or null
+  const void* wfc;   // separate carry projector [d][Dcat], or null
   KvDest dst;
   void* ws;
 };
@@ -91,7 +92,24 @@ struct AttnPlan {
 AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int num_pages,
                         int dtype, int num_cus);
 
+// Attention mass on the carried rows, from a finished attention call's LSE.
+constexpr int kMaxCarryRows = 64;   // carry rows of one sequence (block <= 64)
+
+struct MassArgs {
+  int S, B, layer_begin, Hq, Hkv, hd, CP;
+  uint32_t flags;
+  double rope_inv[kMaxHeadDim / 2];   // RoPE inverse frequencies theta^(-2i/hd)
+  const void* q;
+  const int32_t* ctx_len;
+  const int32_t* carry_len;
+  const void* k_carry;
+  const float* lse;
+  float* mass;
+  int32_t* status;
+};
+
 hipError_t launch_route(const RouteArgs& a, hipStream_t stream);
+hipError_t launch_carry_mass(const MassArgs& a, int layer_count, int dtype, hipStream_t stream);
 hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_t stream);
 hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_count,
                             hipStream_t stream);

@@ -42,8 +42,15 @@ struct GemmArgs {
   const float* fe;         // precomputed F(E) [N], added to carry rows (e must be null)
   void* z_out;             // [M][N]
   int mode;
+  int z_rows;              // Z mode: 0 every row, 1 rows that are not carry rows, 2 carry rows
   KvDest kv;
 };
+
+// Whether Z row `dst` is written under the row selection of a Z pass (the
+// separate projector computes Z in two passes, one per kind of row).
+__device__ __forceinline__ bool z_row_selected(int z_rows, int32_t dst) {
+  return z_rows == 0 || (z_rows == 2) == is_carry_row(dst);
+}
 
 // Workgroup barrier for the staged ring.  Each wavefront has already waited
 // (vmcnt) for its own direct-to-LDS loads of the stage it is about to read, and
@@ -91,7 +98,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
   // row descriptors of the tile's rows (thread t: row t % BM), consumed only by
   // the epilogue; kept opaque until then so no wait lands before the main loop
   const bool carry_add = HAS_E || g.fe != nullptr;
-  const bool need_rows = carry_add || g.mode == kModeKV;
+  const bool need_rows = carry_add || g.mode == kModeKV || g.z_rows != 0;
   int rd_dst = 0, rd_pos = 0;
   if (need_rows) {
     const int r = min(m0 + (tid % BM), g.M - 1);
@@ -278,7 +285,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
     for (int c = tid; c < BM * BN / 8; c += 256) {
       const int row = c / (BN / 8), cc = c % (BN / 8);
       const int gr = m0 + row, gc = n0 + cc * 8;
-      if (gr >= g.M || gc >= g.N) continue;
+      if (gr >= g.M || gc >= g.N || !z_row_selected(g.z_rows, dst_lds[row])) continue;
       u16x8 v;
       if (carry_add) {
         const bool cy = is_carry_row(dst_lds[row]);
@@ -374,7 +381,7 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_kernel(GemmArgs g, int tiles
   const uint16_t* Bw = static_cast<const uint16_t*>(g.B);
 
   const bool carry_add = HAS_E || g.fe != nullptr;
-  const bool need_rows = carry_add || g.mode == kModeKV;
+  const bool need_rows = carry_add || g.mode == kModeKV || g.z_rows != 0;
   int rd_dst = 0, rd_pos = 0;
   if (need_rows) {
     const int r = min(m0 + (tid % BM), g.M - 1);
@@ -566,7 +573,7 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_kernel(GemmArgs g, int tiles
         const int rl = c / (BN / 8), cc = c % (BN / 8);
         const int row = p * PASS + rl;
         const int gr = m0 + row, gc = n0 + cc * 8;
-        if (gr >= g.M || gc >= g.N) continue;
+        if (gr >= g.M || gc >= g.N || !z_row_selected(g.z_rows, dst_lds[row])) continue;
         u16x8 v;
         if (carry_add && is_carry_row(dst_lds[row])) {
 #pragma unroll
@@ -910,10 +917,10 @@ __global__ __launch_bounds__(256, 1) void proj_fused_kernel(ProjectArgs a) {
 template <typename T>
 __global__ __launch_bounds__(256) void epi_z_kernel(const float* part, int splits, int M, int N,
                                                     T* z, const float* part_e, const float* fe,
-                                                    const int32_t* row_dst) {
+                                                    const int32_t* row_dst, int z_rows) {
   const int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
   const int64_t MN = static_cast<int64_t>(M) * N;
-  if (i >= MN) return;
+  if (i >= MN || !z_row_selected(z_rows, row_dst[i / N])) return;
   f32x4 v = *reinterpret_cast<const f32x4*>(part + i);
   for (int s = 1; s < splits; ++s) v += *reinterpret_cast<const f32x4*>(part + s * MN + i);
   if ((part_e || fe) && is_carry_row(row_dst[i / N])) {
@@ -1161,6 +1168,11 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
   kv.M = a.M; kv.N = n_kv; kv.K = a.d;
   kv.A = z; kv.B = a.wkv; kv.e = nullptr; kv.row_dst = a.dst.row_dst;
   kv.partial = part; kv.z_out = nullptr; kv.kv = a.dst;
+  // Separate projector: Z in two passes, F for the rows that are not carry
+  // rows, then the carry projector for the carry rows; no E either way.
+  const bool sep = a.wfc != nullptr;
+  const int passes = sep ? 2 : 1;
+  if (sep) f.e = nullptr;
 
   if (a.dtype == CO_DTYPE_F32) {
     f.k_per_split = ((f.K + p.f_split - 1) / p.f_split + 31) / 32 * 32;
@@ -1168,13 +1180,16 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
     const int fs = (f.K + f.k_per_split - 1) / f.k_per_split;
     const int ks = (kv.K + kv.k_per_split - 1) / kv.k_per_split;
     f.mode = kv.mode = kModePartial;
-    hipLaunchKernelGGL(gemm_f32_kernel, dim3((f.N + 63) / 64, (f.M + 31) / 32, fs), dim3(256), 0,
-                       stream, f);
     const int64_t nz = static_cast<int64_t>(a.M) * a.d / 4;
-    hipLaunchKernelGGL(epi_z_kernel<float>, dim3(static_cast<unsigned>((nz + 255) / 256)),
-                       dim3(256), 0, stream, part, fs, a.M, a.d, static_cast<float*>(z),
-                       static_cast<const float*>(nullptr), static_cast<const float*>(nullptr),
-                       a.dst.row_dst);
+    for (int pass = 0; pass < passes; ++pass) {
+      if (pass == 1) f.B = a.wfc;
+      hipLaunchKernelGGL(gemm_f32_kernel, dim3((f.N + 63) / 64, (f.M + 31) / 32, fs), dim3(256),
+                         0, stream, f);
+      hipLaunchKernelGGL(epi_z_kernel<float>, dim3(static_cast<unsigned>((nz + 255) / 256)),
+                         dim3(256), 0, stream, part, fs, a.M, a.d, static_cast<float*>(z),
+                         static_cast<const float*>(nullptr), static_cast<const float*>(nullptr),
+                         a.dst.row_dst, sep ? pass + 1 : 0);
+    }
     hipLaunchKernelGGL(gemm_f32_kernel, dim3((kv.N + 63) / 64, (kv.M + 31) / 32, ks), dim3(256),
                        0, stream, kv);
     const int64_t items = static_cast<int64_t>(a.M) * (n_kv / 2);
@@ -1183,23 +1198,29 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
     return hipGetLastError();
   }
 
-  if (p.fused && (a.fe != nullptr || a.e == nullptr)) {   // F(E) folded, or no E at all
+  if (!sep && p.fused && (a.fe != nullptr || a.e == nullptr)) {   // F(E) folded, or no E at all
     hipLaunchKernelGGL(proj_fused_kernel, dim3((a.M + kFusedBM - 1) / kFusedBM), dim3(256), 0,
                        stream, a);
     return hipGetLastError();
   }
-  if (a.fe != nullptr) {   // F(E) folded beforehand: the GEMM carries no E
+  if (a.fe != nullptr && !sep) {   // F(E) folded beforehand: the GEMM carries no E
     f.e = nullptr;
     f.fe = a.fe;
   }
   f.k_per_split = split_len(a.Dcat, p.f_split, p.f_tile);
   f.mode = p.f_split > 1 ? kModePartial : kModeZ;
-  if ((err = launch_gemm_bf16(f, p.f_tile, p.f_split, stream)) != hipSuccess) return err;
-  if (p.f_split > 1) {
-    const int64_t nz = static_cast<int64_t>(a.M) * a.d / 4;
-    hipLaunchKernelGGL(epi_z_kernel<uint16_t>, dim3(static_cast<unsigned>((nz + 255) / 256)),
-                       dim3(256), 0, stream, part, p.f_split, a.M, a.d, static_cast<uint16_t*>(z),
-                       static_cast<const float*>(f.e ? f.partial_e : nullptr), f.fe, a.dst.row_dst);
+  for (int pass = 0; pass < passes; ++pass) {
+    if (pass == 1) f.B = a.wfc;
+    f.z_rows = sep ? pass + 1 : 0;
+    if ((err = launch_gemm_bf16(f, p.f_tile, p.f_split, stream)) != hipSuccess) return err;
+    if (p.f_split > 1) {
+      const int64_t nz = static_cast<int64_t>(a.M) * a.d / 4;
+      hipLaunchKernelGGL(epi_z_kernel<uint16_t>, dim3(static_cast<unsigned>((nz + 255) / 256)),
+                         dim3(256), 0, stream, part, p.f_split, a.M, a.d,
+                         static_cast<uint16_t*>(z),
+                         static_cast<const float*>(f.e ? f.partial_e : nullptr), f.fe,
+                         a.dst.row_dst, f.z_rows);
+    }
   }
   kv.k_per_split = split_len(a.d, p.kv_split, p.kv_tile);
   kv.mode = p.kv_split > 1 ? kModePartial : kModeKV;

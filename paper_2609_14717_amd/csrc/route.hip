@@ -11,14 +11,16 @@ __global__ __launch_bounds__(64) void route_kernel(RouteArgs a) {
   const int B = a.B;
   const int p0 = a.ctx_len[s];
 
-  // m = first index where draft and target disagree (B if none)
+  // m = first index where draft and target disagree (B if none), or, with
+  // accept decisions, the first rejected position
   int m = B;
   if (!(a.flags & CO_ROUTE_ACCEPT_ALL)) {
+    const bool bits = a.flags & CO_ROUTE_ACCEPT_BITS;
     const int32_t* dr = a.draft + static_cast<int64_t>(s) * B;
-    const int32_t* tg = a.target + static_cast<int64_t>(s) * B;
+    const int32_t* tg = bits ? nullptr : a.target + static_cast<int64_t>(s) * B;
     for (int j0 = 0; j0 < B; j0 += 64) {
       const int j = j0 + lane;
-      const bool diff = j < B && dr[j] != tg[j];
+      const bool diff = j < B && (bits ? dr[j] == 0 : dr[j] != tg[j]);
       const unsigned long long mask = __ballot(diff);
       if (mask) {
         m = j0 + __ffsll(static_cast<long long>(mask)) - 1;

@@ -12,20 +12,21 @@ from . import workloads as wl
 from . import device as sdev
 
 
-def make_weights(co, dims, wf, wkv, e, fold_e):
+def make_weights(co, dims, wf, wkv, e, fold_e, wfc=None):
     """co_weights of the drafter; with fold_e (bf16) F(E) is folded once, as a
-    serving setup would when it loads the weights."""
+    serving setup would when it loads the weights; wfc: the separate carry
+    projector (then E is not used)."""
     import torch
     f_e = None
-    if fold_e and dims.dtype == co.CO_DTYPE_BF16:
+    if fold_e and dims.dtype == co.CO_DTYPE_BF16 and wfc is None:
         f_e = torch.empty(dims.model_dim, dtype=torch.float32, device=wf.device)
         co.carryover_fold_e(dims, co.weights(wf, wkv, e), f_e)
-    return co.weights(wf, wkv, e, f_e), f_e
+    return co.weights(wf, wkv, e, f_e, wfc), f_e
 
 
 class Scenario:
     def __init__(self, w: wl.Workload, device: str = "cuda", build_context: bool = True,
-                 fold_e: bool = True):
+                 fold_e: bool = True, separate_projector: bool = False):
         import torch
         import paper_2609_14717_amd as co
         self.w, self.device = w, device
@@ -37,7 +38,9 @@ class Scenario:
         self.wf = sdev.materialise(w, wl.spec_wf(w), device)
         self.wkv = sdev.materialise(w, wl.spec_wkv(w), device)
         self.e = sdev.materialise(w, wl.spec_e(w), device)
-        self.W, self.f_e = make_weights(co, self.dims, self.wf, self.wkv, self.e, fold_e)
+        self.wfc = sdev.materialise(w, wl.spec_wfc(w), device) if separate_projector else None
+        self.W, self.f_e = make_weights(co, self.dims, self.wf, self.wkv, self.e, fold_e,
+                                        self.wfc)
         self.ws = torch.zeros(max(co.workspace_bytes(self.dims, co.CO_WS_ROUND), 256),
                               dtype=torch.uint8, device=device)
         self.ws_project = co.workspace_bytes(self.dims, co.CO_WS_PROJECT)

@@ -29,6 +29,7 @@ TCAP = 1 << 20          # logical position stride of per-sequence index layouts
 # named sub-streams of a workload seed
 ST_WF, ST_WKV, ST_E, ST_H, ST_TGT, ST_DRAFT, ST_M, ST_Q = 1, 2, 3, 4, 5, 6, 7, 8
 ST_CTX0, ST_PAGES, ST_KDIR, ST_VDIR, ST_HCTX, ST_ANCHOR, ST_U = 9, 10, 11, 12, 13, 14, 15
+ST_WFC = 16             # the separate carry projector (a variant next to the path)
 
 
 @dataclass(frozen=True)
@@ -188,6 +189,11 @@ def anchors(w: Workload) -> tuple[np.ndarray, np.ndarray, np.ndarray]:
 
 def spec_wf(w):
     return ST_WF, (w.d, w.Dcat), (w.Dcat, 1), 0, w.w_sigma
+
+
+def spec_wfc(w):
+    """Separate projector for carried rows, shaped like F."""
+    return ST_WFC, (w.d, w.Dcat), (w.Dcat, 1), 0, w.w_sigma
 
 
 def spec_wkv(w):

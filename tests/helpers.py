@@ -78,10 +78,11 @@ class OracleTrain:
 class OracleRun:
     """The oracle's view of a workload: weights, logical state, rounds."""
 
-    def __init__(self, w, seqs=None, store=np.float64):
+    def __init__(self, w, seqs=None, store=np.float64, separate_projector=False):
         self.w = w
         self.seqs = list(range(w.S)) if seqs is None else list(seqs)
         self.WF = host(w, wl.spec_wf(w))
+        self.WFC = host(w, wl.spec_wfc(w)) if separate_projector else None
         self.WKV = host(w, wl.spec_wkv(w))
         self.E = host(w, wl.spec_e(w))
         self.pt = wl.page_table(w)
@@ -117,15 +118,21 @@ class OracleRun:
     def seq_block(self, spec, axis):
         return seq_block(self.w, spec, axis, self.seqs)
 
-    def round(self, r, mode="carry", attend=True, layers=None, m=None):
+    def round(self, r, mode="carry", attend=True, layers=None, m=None, bits=None):
+        """One round; with ``bits`` the route takes the verifier's accept
+        decisions [S][B] instead of the tokens."""
         w = self.w
-        m = wl.accepted_lengths(w, r) if m is None else np.asarray(m, np.int32)
-        draft, target = wl.tokens_for(w, r, m)
-        rr = oracle.route(draft, target, self.ctx_len(), self.carry_len(), self.pt,
-                          self.num_pages, mode)
+        if bits is not None:
+            rr = oracle.route(bits, None, self.ctx_len(), self.carry_len(), self.pt,
+                              self.num_pages, mode, accept="bits")
+        else:
+            m = wl.accepted_lengths(w, r) if m is None else np.asarray(m, np.int32)
+            draft, target = wl.tokens_for(w, r, m)
+            rr = oracle.route(draft, target, self.ctx_len(), self.carry_len(), self.pt,
+                              self.num_pages, mode)
         H = self.seq_block(wl.spec_h(w, r), 0)
         oracle.round_update(self.st, rr, H, self.E, self.WF, self.WKV, w.theta, mode,
-                            seqs=self.seqs)
+                            seqs=self.seqs, WF_carry=self.WFC)
         self._ctx = np.asarray(rr["ctx_len"], np.int32).copy()
         self._carry = np.asarray(rr["carry_len"], np.int32).copy()
         if not attend:

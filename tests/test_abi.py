@@ -89,6 +89,7 @@ def test_bad_dims_rejected_by_every_call(kw, code):
                                                ws_bytes=1 << 30)) == code
     assert _rc(lambda: co.drafter_block_attention(d, 0, 1, FAKE, st, FAKE, None, 0, FAKE,
                                                   stream=0, ws_bytes=1 << 30)) == code
+    assert _rc(lambda: co.drafter_carry_mass(d, 0, 1, FAKE, st, FAKE, FAKE, stream=0)) == code
     assert co.workspace_bytes(d) == 0
 
 
@@ -154,3 +155,36 @@ def test_library_has_no_undefined_kernel_stubs():
     out = subprocess.run(["nm", "-D", "--undefined-only", co.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     assert "device_stub" not in out, out
+
+
+def test_accept_bits_route_needs_no_target_tokens():
+    """Under CO_ROUTE_ACCEPT_BITS the target tokens are unused (NULL accepted);
+    the accept decisions themselves are still required."""
+    d = _dims(S=0)
+    assert _rc(lambda: co.carryover_route(d, FAKE, None, co.CO_ROUTE_ACCEPT_BITS, _fake_state(),
+                                          _fake_route(), stream=0)) == co.CO_OK
+    assert _rc(lambda: co.carryover_route(d, None, None, co.CO_ROUTE_ACCEPT_BITS, _fake_state(),
+                                          _fake_route(), stream=0)) == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: co.carryover_route(d, FAKE, None, 0, _fake_state(), _fake_route(),
+                                          stream=0)) == co.CO_ERR_INVALID_ARG
+
+
+def test_carry_mass_arguments_checked_on_host():
+    d = _dims()
+    st = _fake_state()
+    assert _rc(lambda: co.drafter_carry_mass(d, 0, 1, FAKE, st, None, FAKE, stream=0)) \
+        == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: co.drafter_carry_mass(d, 0, 1, FAKE, st, FAKE, FAKE + 2, stream=0)) \
+        == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: co.drafter_carry_mass(d, 1, 5, FAKE, st, FAKE, FAKE, stream=0)) \
+        == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: co.drafter_carry_mass(_dims(B=80, Hq=2, Hkv=2), 0, 1, FAKE, st, FAKE,
+                                             FAKE, stream=0)) == co.CO_ERR_UNSUPPORTED
+
+
+def test_separate_projector_pointer_alignment_checked():
+    d = _dims()
+    W = co.weights(FAKE, FAKE, FAKE, None, FAKE + 2)
+    assert _rc(lambda: co.carryover_project_kv(d, W, FAKE, _fake_route(), _fake_state(), FAKE,
+                                               stream=0, ws_bytes=1 << 30)) \
+        == co.CO_ERR_INVALID_ARG

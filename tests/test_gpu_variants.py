@@ -1,0 +1,125 @@
+"""GPU parity of the variants next to the drafter step, through the C ABI,
+against the fp64 oracle:
+
+* routing by the verifier's accept decisions (stochastic verification, T = 1;
+  Appendix A, "Why verification remains valid"), whatever follows the first
+  rejection;
+* the separate-projector update (Section 4, Table 3(b)): carried rows through a
+  second fusion matrix, no E, on the small-tile, split-K, large-tile and fp32
+  GEMM paths;
+* the attention mass on the carried rows (Appendix "Attention to carried
+  states"), from a finished attention call's LSE.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from synth import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from helpers import TOL, OracleRun, compare_round  # noqa: E402
+
+EDGE = wl.RAGGED32.replace(name="var_edge", S=4, L=2, ctx_lo=40, ctx_hi=900, rounds=8,
+                           accept=("geom", 0.25), seed=0x5EED20)
+EDGE_F32 = EDGE.replace(name="var_edge_f32", dtype="f32", seed=0x5EED21)
+HD128 = wl.Workload("var_hd128", S=3, B=16, Dcat=512, d=256, L=1, Hq=8, Hkv=2, hd=128,
+                    dtype="bf16", theta=1e6, ctx_lo=60, ctx_hi=700, ctx_mode="direct",
+                    accept=("geom", 0.3), rounds=6, seed=0x5EED22)
+# 256 window rows: the large-tile GEMM; 3 x 16 rows of 20480 features: split-K
+WIDE = wl.Workload("var_wide", S=16, B=16, Dcat=512, d=256, L=1, Hq=4, Hkv=2, hd=64,
+                   dtype="bf16", theta=1e4, ctx_lo=30, ctx_hi=300, ctx_mode="direct",
+                   accept=("geom", 0.25), rounds=4, seed=0x5EED23)
+SPLIT = wl.BATCH1_8B.replace(name="var_split", S=3, ctx_lo=200, ctx_hi=200, rounds=4,
+                             seed=0x5EED24)
+
+
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from synth.scenario import Scenario
+    import paper_2609_14717_amd as co
+    return Scenario, co
+
+
+def accept_bits(w, r, m, seed):
+    """Accept decisions that realise accepted prefixes m: non-zero before m,
+    zero at m, arbitrary (seeded) after the first rejection."""
+    rng = np.random.default_rng(seed + r)
+    bits = rng.integers(0, 2, (len(m), w.B)).astype(np.int32)
+    for s, mm in enumerate(m):
+        bits[s, :mm] = rng.integers(1, 1000, mm)
+        if mm < w.B:
+            bits[s, mm] = 0
+    return bits
+
+
+@pytest.mark.parametrize("w", [EDGE, EDGE_F32], ids=lambda w: w.name)
+def test_accept_bits_rounds(w):
+    Scenario, co = _gpu()
+    print(f"[variants] accept bits {w.name}", flush=True)
+    sc, orc = Scenario(w), OracleRun(w)
+    for r in range(4):
+        hidden, q, _, _, m = sc.round_inputs(r)
+        if r == 1:
+            m = np.array([0, w.B, 1, w.B - 1], np.int32)
+        bits = accept_bits(w, r, m, 0x5EED25)
+        out, lse = sc.new_output()
+        co.carryover_round(sc.dims, sc.W, hidden, torch.from_numpy(bits).cuda(), None, q, sc.st,
+                           sc.rt, out, lse, co.CO_ROUTE_ACCEPT_BITS, sc.ws)
+        torch.cuda.synchronize()
+        assert co.carryover_read_status(sc.st) == 0
+        rr, O, LSE = orc.round(r, bits=bits)
+        np.testing.assert_array_equal(rr["accept_len"], m)
+        compare_round(sc, orc, rr, O, LSE, out, lse, sc.rt, orc.seqs, f"{w.name} bits r{r}")
+
+
+@pytest.mark.parametrize("w", [EDGE, EDGE_F32, WIDE, SPLIT], ids=lambda w: w.name)
+def test_separate_projector_rounds(w, monkeypatch):
+    Scenario, co = _gpu()
+    if w is WIDE:      # the large-tile kernel at any row count from 256
+        monkeypatch.setenv("CO_GEMM_WIDE_VARIANT", "3")
+    print(f"[variants] separate projector {w.name}", flush=True)
+    sc = Scenario(w, separate_projector=True)
+    orc = OracleRun(w, separate_projector=True)
+    for r in range(3):
+        hidden, q, draft, target, m = sc.round_inputs(r)
+        out, lse = sc.new_output()
+        co.carryover_round(sc.dims, sc.W, hidden, draft, target, q, sc.st, sc.rt, out, lse, 0,
+                           sc.ws)
+        torch.cuda.synchronize()
+        assert co.carryover_read_status(sc.st) == 0
+        rr, O, LSE = orc.round(r)
+        compare_round(sc, orc, rr, O, LSE, out, lse, sc.rt, orc.seqs, f"{w.name} sep r{r}")
+
+
+@pytest.mark.parametrize("w", [EDGE, EDGE_F32, HD128], ids=lambda w: w.name)
+def test_carry_mass(w):
+    Scenario, co = _gpu()
+    print(f"[variants] carry mass {w.name}", flush=True)
+    sc, orc = Scenario(w), OracleRun(w)
+    tol = TOL[w.dtype]
+    B, S = w.B, w.S
+    plans = [None, [B] * S, [0] * S, [0, B, 1, B - 1][:S] + [3] * max(0, S - 4), None]
+    for r, m in enumerate(plans):
+        hidden, q, draft, target, m = sc.round_inputs(r, m)
+        out, lse = sc.new_output()
+        co.carryover_round(sc.dims, sc.W, hidden, draft, target, q, sc.st, sc.rt, out, lse, 0,
+                           sc.ws)
+        mass = torch.full_like(lse, float("nan"))
+        co.drafter_carry_mass(sc.dims, 0, w.L, q, sc.st, lse, mass)
+        torch.cuda.synchronize()
+        assert co.carryover_read_status(sc.st) == 0
+        orc.round(r, m=m, attend=False)
+        Q = orc.seq_block(wl.spec_q(w, r), 1)
+        ref = oracle.carry_mass_state(orc.st, Q, w.Hq, w.theta, seqs=orc.seqs)
+        got = mass.cpu().numpy().astype(np.float64)
+        for s in orc.seqs:
+            err = np.abs(got[:, s] - ref[:, s]).max()
+            assert err <= tol, f"{w.name} r{r} mass seq {s}: {err}"
+            if m[s] == B:                      # nothing carried: exactly zero
+                assert np.all(got[:, s] == 0.0)
+        print(f"[variants] {w.name} round {r}: mean carried mass {np.nanmean(ref):.4f}",
+              flush=True)
