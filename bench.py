@@ -451,6 +451,8 @@ def main():
         raise RuntimeError("device status after baseline rounds")
     assert np.array_equal(sc.st["ctx_len"].cpu().numpy().astype(np.int64), ctx)
 
+    variants = variant_costs(torch, co, sc, w, lib, step, rewind, chain, args, stream, attend,
+                             q_last, lse=outs[0][1], dt=dt)
     prefill = prefill_point(torch, co, sc, w) if w.ctx_mode == "projected" else None
     calibrate_copy(torch, args)
 
@@ -491,11 +493,43 @@ def main():
         "baseline_mode": {"rounds_per_s": args.steps / dt_base,
                           "t_reuse_us": (dt - dt_base) / args.steps * 1e6},
     }
+    result["variants"] = variants
     if prefill is not None:
         result["prefill_projection"] = prefill
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w.replace(rounds=w.rounds), args.cpu_baseline_seconds)
     print(json.dumps(result), flush=True)
+
+
+def variant_costs(torch, co, sc, w, lib, step, rewind, chain, args, stream, attend, q_last, lse,
+                  dt):
+    """Costs of the variants next to the path, on the same state:
+    * the attention mass on the carried rows (drafter_carry_mass) after the
+      attention call on the final state, per call;
+    * the separate-projector update: the timed rounds again from the snapshot
+      with a second fusion matrix for carried rows (no E), rounds/s."""
+    from synth import device as sdev
+    from synth import workloads as wl
+    # the rounds read sc.W through a pointer: set its carry projector for them
+    wfc = sdev.materialise(w, wl.spec_wfc(w), "cuda")
+    sc.W.w_f_carry = wfc.data_ptr()
+    rewind()
+    dt_sep = chain(0)
+    sc.W.w_f_carry = None
+    if co.carryover_read_status(sc.st):
+        raise RuntimeError("device status after the separate-projector rounds")
+    del wfc
+    # the chain ends with carry segments again: the mass of the last attention
+    mass = torch.empty_like(lse)
+
+    def mass_call():
+        co.drafter_carry_mass(sc.dims, 0, w.L, q_last, sc.st, lse, mass)
+
+    attend()
+    mass_s = timed_calls(torch, stream, min(args.steps, 100), mass_call)
+    return {"carry_mass_call_us": mass_s * 1e6,
+            "separate_projector": {"rounds_per_s": args.steps / dt_sep,
+                                   "vs_embedding": dt / dt_sep}}
 
 
 class Scrub:

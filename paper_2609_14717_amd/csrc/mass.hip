@@ -12,7 +12,11 @@ namespace {
 
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void carry_mass_kernel(MassArgs a) {
-  __shared__ float ks[kMaxCarryRows][HD + 1];
+  constexpr int LD = HD + 4;                   // fp32 rows, 16-byte aligned
+  constexpr int NQ = 64;                       // query rows per KV head (checked on the host)
+  __shared__ __align__(16) float ks[kMaxCarryRows * LD];
+  __shared__ __align__(16) float qs[NQ * LD];
+  __shared__ float lg[NQ][kMaxCarryRows + 1];
   __shared__ double inv_lds[HD / 2];
   const int s = blockIdx.x, g = blockIdx.y, layer_local = blockIdx.z;
   const int layer = a.layer_begin + layer_local;
@@ -24,6 +28,14 @@ __global__ __launch_bounds__(256) void carry_mass_kernel(MassArgs a) {
     if (tid == 0) set_status(a.status, CO_ERR_LENGTH);
     carry = 0;
   }
+  auto row_of = [&](int n) {   // (layer, sequence, block row, query head) of query row n
+    return ((static_cast<int64_t>(layer_local) * a.S + s) * a.B + n / G) * a.Hq + g * G + n % G;
+  };
+  if (carry == 0) {            // nothing carried
+    for (int n = tid; n < nq; n += 256) a.mass[row_of(n)] = 0.f;
+    return;
+  }
+  // carry keys, fp32
   const T* kk = static_cast<const T*>(a.k_carry);
   for (int idx = tid; idx < carry * HD; idx += 256) {
     const int t = idx / HD, d = idx % HD;
@@ -31,56 +43,61 @@ __global__ __launch_bounds__(256) void carry_mass_kernel(MassArgs a) {
         ((((static_cast<int64_t>(layer) * a.S + s) * a.CP + t / kPage) * a.Hkv + g) * kPage +
          t % kPage) * HD + d;
     if constexpr (sizeof(T) == 2)
-      ks[t][d] = bf2f(kk[off]);
+      ks[t * LD + d] = bf2f(kk[off]);
     else
-      ks[t][d] = kk[off];
+      ks[t * LD + d] = kk[off];
   }
   if (tid < HD / 2)   // revolutions per position for bf16, radians for fp32
     inv_lds[tid] = sizeof(T) == 2 ? a.rope_inv[tid] * kInv2Pi : a.rope_inv[tid];
   __syncthreads();
-
+  // queries rotated at ctx + i and scaled by 1/sqrt(hd), one pair per thread-step
   const T* Q = static_cast<const T*>(a.q);
   const float scale = rsqrtf(static_cast<float>(HD));
-  for (int n = tid; n < nq; n += 256) {
-    const int i = n / G, h = g * G + n % G;
-    const int64_t row = ((static_cast<int64_t>(layer_local) * a.S + s) * a.B + i) * a.Hq + h;
-    float q[HD];
-#pragma unroll
-    for (int d = 0; d < HD; ++d) {
-      if constexpr (sizeof(T) == 2)
-        q[d] = bf2f(Q[row * HD + d]);
-      else
-        q[d] = Q[row * HD + d];
+  for (int idx = tid; idx < nq * (HD / 2); idx += 256) {
+    const int n = idx / (HD / 2), p = idx % (HD / 2);
+    const int64_t base = row_of(n) * HD;
+    float lo, hi;
+    if constexpr (sizeof(T) == 2) {
+      lo = bf2f(Q[base + p]);
+      hi = bf2f(Q[base + p + HD / 2]);
+    } else {
+      lo = Q[base + p];
+      hi = Q[base + p + HD / 2];
     }
     if (!(a.flags & CO_Q_PREROTATED)) {
-#pragma unroll
-      for (int p = 0; p < HD / 2; ++p) {
-        float c, sn;
-        if constexpr (sizeof(T) == 2)
-          rope_cos_sin_rev(ctx + i, inv_lds[p], &c, &sn);
-        else
-          rope_cos_sin(ctx + i, inv_lds[p], &c, &sn);
-        const float lo = q[p], hi = q[p + HD / 2];
-        q[p] = lo * c - hi * sn;
-        q[p + HD / 2] = hi * c + lo * sn;
-      }
+      float c, sn;
+      if constexpr (sizeof(T) == 2)
+        rope_cos_sin_rev(ctx + n / G, inv_lds[p], &c, &sn);
+      else
+        rope_cos_sin(ctx + n / G, inv_lds[p], &c, &sn);
+      const float l2 = lo * c - hi * sn, h2 = hi * c + lo * sn;
+      lo = l2;
+      hi = h2;
     }
-    // log-sum-exp of the scaled logits over the carry keys
-    float mx = -INFINITY, sum = 0.f;
-    for (int t = 0; t < carry; ++t) {
-      float dot = 0.f;
-#pragma unroll
-      for (int d = 0; d < HD; ++d) dot = fmaf(q[d], ks[t][d], dot);
-      const float lg = dot * scale;
-      if (lg > mx) {
-        sum = sum * expf(mx - lg) + 1.f;
-        mx = lg;
-      } else {
-        sum += expf(lg - mx);
-      }
-    }
+    qs[n * LD + p] = lo * scale;
+    qs[n * LD + p + HD / 2] = hi * scale;
+  }
+  __syncthreads();
+  // logits of every (query row, carry key) pair
+  for (int idx = tid; idx < nq * carry; idx += 256) {
+    const int n = idx / carry, t = idx % carry;
+    const f32x4* qv = reinterpret_cast<const f32x4*>(qs + n * LD);
+    const f32x4* kv = reinterpret_cast<const f32x4*>(ks + t * LD);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+    for (int d = 0; d < HD / 4; ++d) acc += qv[d] * kv[d];
+    lg[n][t] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  }
+  __syncthreads();
+  // log-sum-exp over the carry keys, against the attention's LSE
+  for (int n = tid; n < nq; n += 256) {
+    float mx = -INFINITY;
+    for (int t = 0; t < carry; ++t) mx = fmaxf(mx, lg[n][t]);
+    float sum = 0.f;
+    for (int t = 0; t < carry; ++t) sum += expf(lg[n][t] - mx);
+    const int64_t row = row_of(n);
     const float lse = a.lse[row];
-    a.mass[row] = (carry == 0 || lse == -INFINITY) ? 0.f : expf(mx + logf(sum) - lse);
+    a.mass[row] = lse == -INFINITY ? 0.f : expf(mx + logf(sum) - lse);
   }
 }
 
