@@ -24,8 +24,10 @@ Variants next to the path: stochastic verification (T = 1), where m is the run
 of positions the verifier accepted by rejection sampling (Appendix A, "Why
 verification remains valid"); the separate-projector update, where carried
 rows go through a second fusion matrix instead of F + E (Section 4, Table
-3(b)); and the share of attention that falls on the carried rows (Appendix
-"Attention to carried states").
+3(b)); the share of attention that falls on the carried rows (Appendix
+"Attention to carried states"); the block's own rows as a third attention
+segment [C ; U ; S]; and an RMS normalisation of F's output before the K/V
+projections (the paper's equations omit normalisation, Section 2.1).
 
 Readings where the paper is silent (each one a stated choice of this oracle): no norm
 and no bias in F, K_l, V_l; rotate-half RoPE with inverse frequency
@@ -149,7 +151,16 @@ def rope(x: np.ndarray, pos, theta: float) -> np.ndarray:
     return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
 
 
-def project(H, E, add_e, WF, WKV, pos, L, Hkv, hd, theta, WF_carry=None):
+RMS_EPS = 1e-6   # RMSNorm epsilon of the normalisation variant
+
+
+def rms_norm(z, g):
+    """Root-mean-square normalisation of each row of z, then an elementwise gain g."""
+    z = np.asarray(z, np.float64)
+    return z / np.sqrt(np.mean(z * z, axis=-1, keepdims=True) + RMS_EPS) * np.asarray(g, np.float64)
+
+
+def project(H, E, add_e, WF, WKV, pos, L, Hkv, hd, theta, WF_carry=None, z_norm=None):
     """Phi_l(H) of Eq. 1 for every layer, with E added to flagged rows before F
     (Eq. 2) and RoPE applied to the keys at each row's position.
 
@@ -158,6 +169,9 @@ def project(H, E, add_e, WF, WKV, pos, L, Hkv, hd, theta, WF_carry=None):
     WF_carry [d][Dcat]: the separate-projector variant (Section 4, "How should
     rejected states be distinguished?"; Table 3(b)): flagged rows are projected
     by this second fusion matrix instead of F, with no E.
+    z_norm [d]: the normalisation variant: z = F(x) is RMS-normalised (gain
+    z_norm) before the K/V projections (the equations omit normalisation,
+    Section 2.1).
     Returns K, V as [M][L][Hkv][hd] float64.
     """
     H = np.asarray(H, np.float64)
@@ -168,6 +182,8 @@ def project(H, E, add_e, WF, WKV, pos, L, Hkv, hd, theta, WF_carry=None):
     else:
         z = np.where(flag[:, None], H @ np.asarray(WF_carry, np.float64).T,
                      H @ np.asarray(WF, np.float64).T)
+    if z_norm is not None:
+        z = rms_norm(z, z_norm)
     kv = (z @ np.asarray(WKV, np.float64).T).reshape(len(H), L, 2, Hkv, hd)
     k = rope(kv[:, :, 0], np.asarray(pos)[:, None, None], theta)
     return k, kv[:, :, 1].copy()
@@ -267,6 +283,32 @@ def attend_state(state: State, Q, Hq, theta, seqs=None, layers=None):
     return O, LSE
 
 
+def attend_state_with_self(state: State, Q, Kself, Vself, Hq, theta, seqs=None, layers=None):
+    """Block attention over [C ; U ; S]: S is the block's own rows (the drafter's
+    K/V of its B block positions, supplied by the caller), non-causal, with the
+    keys rotated at the query positions ctx_len + i.  Kself, Vself
+    [L][S][B][Hkv][hd] (keys unrotated).  Returns O, LSE like attend_state."""
+    L, S, B, _, hd = Q.shape
+    G = Hq // state.Hkv
+    O = np.full(Q.shape, np.nan)
+    LSE = np.full(Q.shape[:-1], np.nan)
+    ctx = state.ctx_len()
+    for s in (range(S) if seqs is None else seqs):
+        pos = ctx[s] + np.arange(B)
+        for layer in (range(L) if layers is None else layers):
+            for g in range(state.Hkv):
+                k, v = state.context(s, layer, g)
+                ks = rope(np.asarray(Kself[layer, s, :, g], np.float64), pos, theta)
+                k = np.concatenate([k, ks], axis=0)
+                v = np.concatenate([v, np.asarray(Vself[layer, s, :, g], np.float64)], axis=0)
+                heads = list(range(g * G, (g + 1) * G))
+                q = Q[layer, s][:, heads].reshape(B * G, hd)
+                o, lse = attend(q, np.repeat(pos, G), k, v, theta)
+                O[layer, s][:, heads] = o.reshape(B, G, hd)
+                LSE[layer, s][:, heads] = lse.reshape(B, G)
+    return O, LSE
+
+
 def carry_mass_state(state: State, Q, Hq, theta, seqs=None, layers=None):
     """carry_mass of every (layer, sequence, query row, query head) over the
     state's [C;U]; query i sits at ctx_len + i.  Returns [L][S][B][Hq] (NaN
@@ -288,7 +330,7 @@ def carry_mass_state(state: State, Q, Hq, theta, seqs=None, layers=None):
 
 
 def round_update(state: State, r, H, E, WF, WKV, theta, mode="carry", seqs=None,
-                 WF_carry=None):
+                 WF_carry=None, z_norm=None):
     """Post-verification update of Algorithm 1 for the sequences in ``seqs``,
     given a route result ``r`` (see ``route``).  H [S][B][Dcat].  With
     ``WF_carry`` the carried rows use the separate projector (see project)."""
@@ -300,7 +342,7 @@ def round_update(state: State, r, H, E, WF, WKV, theta, mode="carry", seqs=None,
         rows = np.arange(B) if mode in ("carry", "carry_only") else np.arange(m)
         pos = r["row_pos"][s][rows]
         k, v = project(H[s][rows], E, rows >= m, WF, WKV, pos, state.L, state.Hkv,
-                       state.hd, theta, WF_carry)
+                       state.hd, theta, WF_carry, z_norm)
         if mode == "carry_only":
             k_acc, v_acc = k[:0], v[:0]
         else:

@@ -536,3 +536,81 @@ def test_carry_mass_one_dominant_carried_logit():
     ku[1, 0] = 200.0                   # at position 0 the query is not rotated
     mass = oracle.carry_mass(q, np.array([0]), kc, ku, 1e4)
     assert 1.0 - mass[0] < 1e-15
+
+
+# ------------------------------------------- normalisation of F's output (variant)
+
+def test_z_norm_makes_the_update_scale_invariant():
+    """With F's output RMS-normalised, scaling the target features (and E with
+    them) by any c > 0 leaves every key and value unchanged (up to the epsilon),
+    and the gain scales them linearly."""
+    L, Hkv, hd, H, E, WF, WKV, pos, flag = _proj_case()
+    g = RNG.uniform(0.5, 1.5, WF.shape[0])
+    k1, v1 = oracle.project(H, E, flag, WF, WKV, pos, L, Hkv, hd, 1e4, z_norm=g)
+    k2, v2 = oracle.project(7.0 * H, 7.0 * E, flag, WF, WKV, pos, L, Hkv, hd, 1e4, z_norm=g)
+    # the epsilon moves a row by eps / (2 mean(z^2)), about 1e-8 here
+    np.testing.assert_allclose(k2, k1, rtol=1e-7, atol=1e-7)
+    np.testing.assert_allclose(v2, v1, rtol=1e-7, atol=1e-7)
+    k3, v3 = oracle.project(H, E, flag, WF, WKV, pos, L, Hkv, hd, 1e4, z_norm=2.0 * g)
+    np.testing.assert_allclose(k3, 2.0 * k1, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(v3, 2.0 * v1, rtol=1e-12, atol=1e-12)
+
+
+def test_rms_norm_rows_have_unit_rms():
+    z = RNG.standard_normal((6, 40)) * RNG.uniform(0.1, 10.0, (6, 1))
+    y = oracle.rms_norm(z, np.ones(40))
+    ms = np.mean(z * z, axis=1)
+    np.testing.assert_allclose(np.mean(y * y, axis=1), ms / (ms + oracle.RMS_EPS), rtol=1e-12)
+
+
+# --------------------------------------------------- block self-KV segment (variant)
+
+def _self_case(ctx, B=4, L=1, Hkv=1, G=2, hd=16):
+    st = oracle.State(1, L, Hkv, hd)
+    if ctx:
+        st.set_committed(0, RNG.standard_normal((L, ctx, Hkv, hd)),
+                         RNG.standard_normal((L, ctx, Hkv, hd)))
+    Q = RNG.standard_normal((L, 1, B, Hkv * G, hd))
+    Ks = RNG.standard_normal((L, 1, B, Hkv, hd))
+    Vs = RNG.standard_normal((L, 1, B, Hkv, hd))
+    return st, Q, Ks, Vs
+
+
+def test_self_segment_depends_on_relative_positions_only():
+    """With no committed or carried keys, a query at ctx + i against self key j
+    (rotated at ctx + j) sees only i - j: the output does not move with ctx."""
+    st0, Q, Ks, Vs = _self_case(0)
+    O0, L0 = oracle.attend_state_with_self(st0, Q, Ks, Vs, 2, 1e4)
+    st1 = oracle.State(1, 1, 1, 16)
+    st1.ctx_len = lambda: np.array([977], np.int32)       # shift every position by 977
+    O1, L1 = oracle.attend_state_with_self(st1, Q, Ks, Vs, 2, 1e4)
+    np.testing.assert_allclose(O1, O0, rtol=1e-9, atol=1e-11)
+    np.testing.assert_allclose(L1, L0, rtol=1e-9, atol=1e-11)
+
+
+def test_self_segment_merges_with_the_context_by_the_lse_rule():
+    """[C;U;S] in one softmax equals the log-sum-exp merge of the attention over
+    [C;U] and the attention over S alone (Eq. 2's ctx, one more segment)."""
+    st, Q, Ks, Vs = _self_case(37)
+    O, LSE = oracle.attend_state_with_self(st, Q, Ks, Vs, 2, 1e4)
+    Oc, Lc = oracle.attend_state(st, Q, 2, 1e4)
+    empty = oracle.State(1, 1, 1, 16)
+    empty.ctx_len = st.ctx_len                             # same query positions, no keys
+    Os, Ls = oracle.attend_state_with_self(empty, Q, Ks, Vs, 2, 1e4)
+    M = np.maximum(Lc, Ls)
+    wc, ws = np.exp(Lc - M), np.exp(Ls - M)
+    np.testing.assert_allclose(O, (wc[..., None] * Oc + ws[..., None] * Os) /
+                               (wc + ws)[..., None], rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(LSE, M + np.log(wc + ws), rtol=1e-12)
+
+
+def test_self_segment_identical_keys_average_all_values():
+    """All logits equal (zero keys in both segments): every query returns the
+    mean of all committed and self values."""
+    st, Q, Ks, Vs = _self_case(5)
+    st.ck[0][:] = 0.0
+    Ks[:] = 0.0
+    O, _ = oracle.attend_state_with_self(st, Q, Ks, Vs, 2, 1e4)
+    allv = np.concatenate([st.cv[0][0, :, 0], Vs[0, 0, :, 0]], axis=0)
+    np.testing.assert_allclose(O[0, 0], np.broadcast_to(allv.mean(axis=0), O[0, 0].shape),
+                               rtol=1e-12, atol=1e-12)
