@@ -124,6 +124,11 @@ typedef struct co_weights {
                                  rows routed to the carry segment are projected by it
                                  instead of by F with E_carry (e_carry and f_e unused;
                                  costs a second F product)                            */
+  const float* z_norm;        /* optional RMS-norm gain, fp32 [model_dim]: when non-NULL
+                                 every row of z = F x is divided by its root mean square
+                                 (epsilon 1e-6) and multiplied by z_norm before the K/V
+                                 projections (normalisation variant; the equations omit
+                                 normalisation, Section 2.1)                          */
 } co_weights;
 
 typedef struct co_state {
@@ -234,6 +239,26 @@ co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int3
 co_status drafter_carry_mass(const co_dims* dims, int32_t layer_begin, int32_t layer_count,
                              const void* q, const co_state* state, const float* lse, float* mass,
                              uint32_t flags, hipStream_t stream);
+
+/*
+ * The block's own rows as a third attention segment S (the drafter's keys and
+ * values of its B block positions, attended non-causally, next to
+ * ctx = [C;U] of Eq. 2).  For every (layer, sequence, block row i, query head h)
+ * of a drafter_block_attention call made with the same dims, layers, q, state
+ * and CO_Q_PREROTATED flag, and with its lse output: the attention of the query
+ * over the B self keys k_self (rotated here at positions ctx_len + j, j < B)
+ * and values v_self is merged into out and lse in place by the log-sum-exp
+ * rule, so that they hold the attention over [C;U;S] in one softmax.
+ * k_self, v_self: [layer_count][num_seqs][block][num_kv_heads][head_dim] in
+ * the call's dtype, keys unrotated.  out, lse: as written by the attention
+ * call.  flags: CO_Q_PREROTATED.  Supported: the attention call's shapes with
+ * block <= 64.  Device errors: CO_ERR_LENGTH (negative ctx_len); that
+ * sequence is left as it was.
+ */
+co_status drafter_self_merge(const co_dims* dims, int32_t layer_begin, int32_t layer_count,
+                             const void* q, const void* k_self, const void* v_self,
+                             const co_state* state, void* out, float* lse, uint32_t flags,
+                             hipStream_t stream);
 
 co_status carryover_round(const co_dims* dims, const co_weights* w, const void* hidden,
                           const int32_t* draft_tok, const int32_t* target_tok, const void* q,

@@ -44,7 +44,8 @@ class co_dims(ctypes.Structure):
 
 class co_weights(ctypes.Structure):
     _fields_ = [("w_f", ctypes.c_void_p), ("w_kv", ctypes.c_void_p), ("e_carry", ctypes.c_void_p),
-                ("f_e", ctypes.c_void_p), ("w_f_carry", ctypes.c_void_p)]
+                ("f_e", ctypes.c_void_p), ("w_f_carry", ctypes.c_void_p),
+                ("z_norm", ctypes.c_void_p)]
 
 
 class co_state(ctypes.Structure):
@@ -84,6 +85,8 @@ def lib():
             "carryover_fold_e": [_P(co_dims), _P(co_weights), _v, _v],
             "drafter_carry_mass": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, _v, _P(co_state),
                                    _v, _v, ctypes.c_uint32, _v],
+            "drafter_self_merge": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, _v, _v, _v,
+                                   _P(co_state), _v, _v, ctypes.c_uint32, _v],
             "carryover_import_kv": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _v,
                                     _v, _P(co_state), _v],
             "carryover_workspace_bytes": [_P(co_dims), ctypes.c_int32],
@@ -101,7 +104,8 @@ def lib():
 
 
 EXPORTED = ("carryover_route", "carryover_project_kv", "drafter_block_attention",
-            "carryover_round", "carryover_fold_e", "drafter_carry_mass", "carryover_import_kv",
+            "carryover_round", "carryover_fold_e", "drafter_carry_mass", "drafter_self_merge",
+            "carryover_import_kv",
             "carryover_workspace_bytes", "carryover_read_status", "carryover_status_string")
 
 
@@ -137,10 +141,12 @@ def make_dims(S, B, Dcat, d, L, Hq, Hkv, hd, max_pages_per_seq, num_pages, dtype
                    float(theta))
 
 
-def weights(w_f, w_kv, e_carry, f_e=None, w_f_carry=None):
+def weights(w_f, w_kv, e_carry, f_e=None, w_f_carry=None, z_norm=None):
     """co_weights over device tensors; f_e (fp32 [model_dim], optional) from
-    ``carryover_fold_e``; w_f_carry (optional) the separate carry projector."""
-    return co_weights(_ptr(w_f), _ptr(w_kv), _ptr(e_carry), _ptr(f_e), _ptr(w_f_carry))
+    ``carryover_fold_e``; w_f_carry (optional) the separate carry projector;
+    z_norm (fp32 [model_dim], optional) the RMS-norm gain of F's output."""
+    return co_weights(_ptr(w_f), _ptr(w_kv), _ptr(e_carry), _ptr(f_e), _ptr(w_f_carry),
+                      _ptr(z_norm))
 
 
 def state(t):
@@ -216,6 +222,14 @@ def drafter_carry_mass(dims, layer_begin, layer_count, q, st, lse, mass, flags=0
     _check(lib().drafter_carry_mass(ctypes.byref(dims), layer_begin, layer_count, _ptr(q),
                                     ctypes.byref(s), _ptr(lse), _ptr(mass), flags,
                                     _stream(stream)), "drafter_carry_mass")
+
+
+def drafter_self_merge(dims, layer_begin, layer_count, q, k_self, v_self, st, out, lse, flags=0,
+                       stream=None):
+    s = state(st)
+    _check(lib().drafter_self_merge(ctypes.byref(dims), layer_begin, layer_count, _ptr(q),
+                                    _ptr(k_self), _ptr(v_self), ctypes.byref(s), _ptr(out),
+                                    _ptr(lse), flags, _stream(stream)), "drafter_self_merge")
 
 
 def carryover_round(dims, w, hidden, draft_tok, target_tok, q, st, rt, out, lse, flags, ws,

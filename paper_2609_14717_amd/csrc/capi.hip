@@ -188,7 +188,8 @@ co_status carryover_project_kv(const co_dims* dims, const co_weights* w, const v
   if (!w || !w->w_f || !w->w_kv || !w->e_carry || !hidden || !route_ok(route) || !state_ok(state))
     return CO_ERR_INVALID_ARG;
   if (!aligned(hidden, 16) || !aligned(w->w_f, 16) || !aligned(w->w_kv, 16) ||
-      !aligned(w->e_carry, 16) || !aligned(w->f_e, 16) || !aligned(w->w_f_carry, 16))
+      !aligned(w->e_carry, 16) || !aligned(w->f_e, 16) || !aligned(w->w_f_carry, 16) ||
+      !aligned(w->z_norm, 4))
     return CO_ERR_INVALID_ARG;
   const ProjectPlan p = project_plan(dims);
   if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
@@ -204,6 +205,7 @@ co_status carryover_project_kv(const co_dims* dims, const co_weights* w, const v
   a.e = w->e_carry;
   a.fe = dims->dtype == CO_DTYPE_BF16 ? w->f_e : nullptr;
   a.wfc = w->w_f_carry;
+  a.znorm = w->z_norm;
   a.dst = make_dest(dims, route, state);
   a.ws = ws;
   return hip_status(launch_project(a, p, stream));
@@ -267,6 +269,37 @@ co_status drafter_carry_mass(const co_dims* dims, int32_t layer_begin, int32_t l
   a.mass = mass;
   a.status = state->status;
   return hip_status(launch_carry_mass(a, layer_count, dims->dtype, stream));
+}
+
+co_status drafter_self_merge(const co_dims* dims, int32_t layer_begin, int32_t layer_count,
+                             const void* q, const void* k_self, const void* v_self,
+                             const co_state* state, void* out, float* lse, uint32_t flags,
+                             hipStream_t stream) {
+  co_status s = check_dims(dims);
+  if (s != CO_OK) return s;
+  if ((s = check_attention_dims(dims)) != CO_OK) return s;
+  if (dims->block > kMaxCarryRows) return CO_ERR_UNSUPPORTED;
+  if (layer_begin < 0 || layer_count < 0 || layer_begin + layer_count > dims->num_layers)
+    return CO_ERR_INVALID_ARG;
+  if (!q || !k_self || !v_self || !out || !lse || !state_ok(state) || !aligned(q, 16) ||
+      !aligned(k_self, 16) || !aligned(v_self, 16) || !aligned(out, 16) || !aligned(lse, 4))
+    return CO_ERR_INVALID_ARG;
+  SelfArgs a{};
+  a.S = dims->num_seqs;
+  a.B = dims->block;
+  a.Hq = dims->num_q_heads;
+  a.Hkv = dims->num_kv_heads;
+  a.hd = dims->head_dim;
+  a.flags = flags;
+  fill_rope_table(a.rope_inv, dims);
+  a.q = q;
+  a.k_self = k_self;
+  a.v_self = v_self;
+  a.ctx_len = state->ctx_len;
+  a.out = out;
+  a.lse = lse;
+  a.status = state->status;
+  return hip_status(launch_self_merge(a, layer_count, dims->dtype, stream));
 }
 
 co_status carryover_round(const co_dims* dims, const co_weights* w, const void* hidden,

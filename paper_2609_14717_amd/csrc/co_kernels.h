@@ -46,6 +46,7 @@ struct ProjectArgs {
   const void* e;
   const float* fe;   // precomputed F(E) [d] (bf16 path), or null
   const void* wfc;   // separate carry projector [d][Dcat], or null
+  const float* znorm;   // RMS-norm gain of F's output [d], or null
   KvDest dst;
   void* ws;
 };
@@ -108,7 +109,22 @@ struct MassArgs {
   int32_t* status;
 };
 
+// The block's own rows as a third attention segment, merged into (O, LSE).
+struct SelfArgs {
+  int S, B, Hq, Hkv, hd;
+  uint32_t flags;
+  double rope_inv[kMaxHeadDim / 2];   // RoPE inverse frequencies theta^(-2i/hd)
+  const void* q;
+  const void* k_self;
+  const void* v_self;
+  const int32_t* ctx_len;
+  void* out;
+  float* lse;
+  int32_t* status;
+};
+
 hipError_t launch_route(const RouteArgs& a, hipStream_t stream);
+hipError_t launch_self_merge(const SelfArgs& a, int layer_count, int dtype, hipStream_t stream);
 hipError_t launch_carry_mass(const MassArgs& a, int layer_count, int dtype, hipStream_t stream);
 hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_t stream);
 hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_count,

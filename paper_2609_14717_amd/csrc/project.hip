@@ -911,6 +911,33 @@ __global__ __launch_bounds__(256, 1) void proj_fused_kernel(ProjectArgs a) {
   }
 }
 
+// ------------------------------------------------- RMS norm of F's output
+// The normalisation variant: every row of Z is divided by its root mean
+// square (epsilon kRmsEps) and multiplied by the gain g, in place, before the
+// K/V product.  One wavefront per row, fp32 arithmetic.
+constexpr float kRmsEps = 1e-6f;
+
+template <typename T>
+__global__ __launch_bounds__(256) void z_norm_kernel(T* z, int M, int d, const float* g) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= M) return;
+  T* zr = z + static_cast<int64_t>(row) * d;
+  float ss = 0.f;
+  for (int c = lane; c < d; c += 64) {
+    float v;
+    if constexpr (sizeof(T) == 2) v = bf2f(zr[c]); else v = zr[c];
+    ss = fmaf(v, v, ss);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+  const float r = rsqrtf(ss / static_cast<float>(d) + kRmsEps);
+  for (int c = lane; c < d; c += 64) {
+    float v;
+    if constexpr (sizeof(T) == 2) v = bf2f(zr[c]); else v = zr[c];
+    zr[c] = to_elem<T>(v * r * g[c]);
+  }
+}
+
 // -------------------------------------------- epilogues over fp32 partials
 
 // Four consecutive columns per thread (N is a multiple of 64).
@@ -1190,6 +1217,9 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
                          static_cast<const float*>(nullptr), static_cast<const float*>(nullptr),
                          a.dst.row_dst, sep ? pass + 1 : 0);
     }
+    if (a.znorm != nullptr)
+      hipLaunchKernelGGL(z_norm_kernel<float>, dim3((a.M + 3) / 4), dim3(256), 0, stream,
+                         static_cast<float*>(z), a.M, a.d, a.znorm);
     hipLaunchKernelGGL(gemm_f32_kernel, dim3((kv.N + 63) / 64, (kv.M + 31) / 32, ks), dim3(256),
                        0, stream, kv);
     const int64_t items = static_cast<int64_t>(a.M) * (n_kv / 2);
@@ -1198,7 +1228,7 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
     return hipGetLastError();
   }
 
-  if (!sep && p.fused && (a.fe != nullptr || a.e == nullptr)) {   // F(E) folded, or no E at all
+  if (!sep && a.znorm == nullptr && p.fused && (a.fe != nullptr || a.e == nullptr)) {
     hipLaunchKernelGGL(proj_fused_kernel, dim3((a.M + kFusedBM - 1) / kFusedBM), dim3(256), 0,
                        stream, a);
     return hipGetLastError();
@@ -1222,6 +1252,9 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
                          a.dst.row_dst, f.z_rows);
     }
   }
+  if (a.znorm != nullptr)
+    hipLaunchKernelGGL(z_norm_kernel<uint16_t>, dim3((a.M + 3) / 4), dim3(256), 0, stream,
+                       static_cast<uint16_t*>(z), a.M, a.d, a.znorm);
   kv.k_per_split = split_len(a.d, p.kv_split, p.kv_tile);
   kv.mode = p.kv_split > 1 ? kModePartial : kModeKV;
   if ((err = launch_gemm_bf16(kv, p.kv_tile, p.kv_split, stream)) != hipSuccess) return err;

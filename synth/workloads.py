@@ -30,6 +30,7 @@ TCAP = 1 << 20          # logical position stride of per-sequence index layouts
 ST_WF, ST_WKV, ST_E, ST_H, ST_TGT, ST_DRAFT, ST_M, ST_Q = 1, 2, 3, 4, 5, 6, 7, 8
 ST_CTX0, ST_PAGES, ST_KDIR, ST_VDIR, ST_HCTX, ST_ANCHOR, ST_U = 9, 10, 11, 12, 13, 14, 15
 ST_WFC = 16             # the separate carry projector (a variant next to the path)
+ST_ZNORM, ST_KSELF, ST_VSELF = 17, 18, 19   # RMS-norm gain offsets; block self K/V
 
 
 @dataclass(frozen=True)
@@ -66,6 +67,11 @@ class Workload:
     def n_kv(self) -> int:
         """Columns of the concatenated K/V weight: layers x (K, V) x heads x dim."""
         return 2 * self.L * self.Hkv * self.hd
+
+    @property
+    def sigma_z(self) -> float:
+        """Std of an entry of F's output: w * sqrt(Dcat) * h."""
+        return self.w_sigma * math.sqrt(self.Dcat) * self.h_sigma
 
     @property
     def sigma_kv(self) -> float:
@@ -194,6 +200,28 @@ def spec_wf(w):
 def spec_wfc(w):
     """Separate projector for carried rows, shaped like F."""
     return ST_WFC, (w.d, w.Dcat), (w.Dcat, 1), 0, w.w_sigma
+
+
+def spec_znorm(w):
+    """Offsets of the RMS-norm gain of F's output, fp32: the gain is
+    fp32(sigma_z) * (1 + offset), so that normalised rows keep the statistics
+    of F's output (and K/V those of the projection)."""
+    return ST_ZNORM, (w.d,), (1,), 0, 0.1
+
+
+def znorm_gain_host(w, offsets):
+    """The gain from its offsets, in fp32 as on the device."""
+    return np.float32(w.sigma_z) * (np.float32(1.0) + np.asarray(offsets, np.float32))
+
+
+def spec_self(w, which, rnd, S=None):
+    """Block self keys ('k', unrotated) or values ('v') of round ``rnd``:
+    [L][S][B][Hkv][hd], with the statistics of projected K/V."""
+    S = w.S if S is None else S
+    st = ST_KSELF if which == "k" else ST_VSELF
+    shape = (w.L, S, w.B, w.Hkv, w.hd)
+    strides = (S * w.B * w.Hkv * w.hd, w.B * w.Hkv * w.hd, w.Hkv * w.hd, w.hd, 1)
+    return st, shape, strides, rnd * w.L * S * w.B * w.Hkv * w.hd, w.sigma_kv
 
 
 def spec_wkv(w):

@@ -90,6 +90,8 @@ def test_bad_dims_rejected_by_every_call(kw, code):
     assert _rc(lambda: co.drafter_block_attention(d, 0, 1, FAKE, st, FAKE, None, 0, FAKE,
                                                   stream=0, ws_bytes=1 << 30)) == code
     assert _rc(lambda: co.drafter_carry_mass(d, 0, 1, FAKE, st, FAKE, FAKE, stream=0)) == code
+    assert _rc(lambda: co.drafter_self_merge(d, 0, 1, FAKE, FAKE, FAKE, st, FAKE, FAKE,
+                                             stream=0)) == code
     assert co.workspace_bytes(d) == 0
 
 
@@ -187,4 +189,22 @@ def test_separate_projector_pointer_alignment_checked():
     W = co.weights(FAKE, FAKE, FAKE, None, FAKE + 2)
     assert _rc(lambda: co.carryover_project_kv(d, W, FAKE, _fake_route(), _fake_state(), FAKE,
                                                stream=0, ws_bytes=1 << 30)) \
+        == co.CO_ERR_INVALID_ARG
+
+
+def test_self_merge_arguments_checked_on_host():
+    d = _dims()
+    st = _fake_state()
+    assert _rc(lambda: co.drafter_self_merge(d, 0, 1, FAKE, FAKE, FAKE, st, FAKE, None,
+                                             stream=0)) == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: co.drafter_self_merge(d, 0, 1, FAKE, FAKE + 8, FAKE, st, FAKE, FAKE,
+                                             stream=0)) == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: co.drafter_self_merge(d, 0, 2, FAKE, FAKE, FAKE, st, FAKE, FAKE,
+                                             stream=0)) == co.CO_ERR_INVALID_ARG
+
+
+def test_z_norm_pointer_alignment_checked():
+    W = co.weights(FAKE, FAKE, FAKE, None, None, FAKE + 2)
+    assert _rc(lambda: co.carryover_project_kv(_dims(), W, FAKE, _fake_route(), _fake_state(),
+                                               FAKE, stream=0, ws_bytes=1 << 30)) \
         == co.CO_ERR_INVALID_ARG

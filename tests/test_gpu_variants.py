@@ -8,7 +8,10 @@ against the fp64 oracle:
   second fusion matrix, no E, on the small-tile, split-K, large-tile and fp32
   GEMM paths;
 * the attention mass on the carried rows (Appendix "Attention to carried
-  states"), from a finished attention call's LSE.
+  states"), from a finished attention call's LSE;
+* the RMS normalisation of F's output before the K/V product;
+* the block's own rows as a third attention segment, merged into the
+  attention over [C;U].
 """
 import numpy as np
 import pytest
@@ -20,7 +23,7 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-from helpers import TOL, OracleRun, compare_round  # noqa: E402
+from helpers import TOL, OracleRun, assert_heads_close, compare_round, host, to_np  # noqa: E402
 
 EDGE = wl.RAGGED32.replace(name="var_edge", S=4, L=2, ctx_lo=40, ctx_hi=900, rounds=8,
                            accept=("geom", 0.25), seed=0x5EED20)
@@ -123,3 +126,77 @@ def test_carry_mass(w):
                 assert np.all(got[:, s] == 0.0)
         print(f"[variants] {w.name} round {r}: mean carried mass {np.nanmean(ref):.4f}",
               flush=True)
+
+
+@pytest.mark.parametrize("w", [EDGE, EDGE_F32, WIDE, SPLIT], ids=lambda w: w.name)
+def test_z_norm_rounds(w, monkeypatch):
+    """F's output RMS-normalised (gain) before the K/V product."""
+    Scenario, co = _gpu()
+    if w is WIDE:
+        monkeypatch.setenv("CO_GEMM_WIDE_VARIANT", "3")
+    print(f"[variants] z norm {w.name}", flush=True)
+    sc = Scenario(w, z_norm=True)
+    orc = OracleRun(w, z_norm=True)
+    for r in range(3):
+        hidden, q, draft, target, m = sc.round_inputs(r)
+        out, lse = sc.new_output()
+        co.carryover_round(sc.dims, sc.W, hidden, draft, target, q, sc.st, sc.rt, out, lse, 0,
+                           sc.ws)
+        torch.cuda.synchronize()
+        assert co.carryover_read_status(sc.st) == 0
+        rr, O, LSE = orc.round(r)
+        compare_round(sc, orc, rr, O, LSE, out, lse, sc.rt, orc.seqs, f"{w.name} znorm r{r}")
+
+
+def test_z_norm_fused_path(monkeypatch):
+    """Where the fused projection would run (forced at 80 rows), the
+    normalised update takes the two-product path and stays correct."""
+    monkeypatch.setenv("CO_PROJECT_FUSED_MIN_ROWS", "1")
+    _z_norm_small()
+
+
+def _z_norm_small():
+    Scenario, co = _gpu()
+    w = wl.RAGGED32.replace(name="var_znorm_fused", S=5, rounds=3, ctx_lo=100, ctx_hi=900,
+                            seed=0x5EED26)
+    sc, orc = Scenario(w, z_norm=True), OracleRun(w, z_norm=True)
+    for r in range(2):
+        hidden, q, draft, target, m = sc.round_inputs(r)
+        out, lse = sc.new_output()
+        co.carryover_round(sc.dims, sc.W, hidden, draft, target, q, sc.st, sc.rt, out, lse, 0,
+                           sc.ws)
+        torch.cuda.synchronize()
+        assert co.carryover_read_status(sc.st) == 0
+        rr, O, LSE = orc.round(r)
+        compare_round(sc, orc, rr, O, LSE, out, lse, sc.rt, orc.seqs, f"{w.name} r{r}")
+
+
+@pytest.mark.parametrize("w", [EDGE, EDGE_F32, HD128], ids=lambda w: w.name)
+def test_self_merge(w):
+    """The block's own rows as a third segment: attention over [C;U;S]."""
+    Scenario, co = _gpu()
+    print(f"[variants] self segment {w.name}", flush=True)
+    sc, orc = Scenario(w), OracleRun(w)
+    tol = TOL[w.dtype]
+    B, S = w.B, w.S
+    plans = [None, [B] * S, [0] * S, None]
+    for r, m in enumerate(plans):
+        hidden, q, draft, target, m = sc.round_inputs(r, m)
+        out, lse = sc.new_output()
+        co.carryover_round(sc.dims, sc.W, hidden, draft, target, q, sc.st, sc.rt, out, lse, 0,
+                           sc.ws)
+        ks, vs = sc.self_kv(r)
+        co.drafter_self_merge(sc.dims, 0, w.L, q, ks, vs, sc.st, out, lse)
+        torch.cuda.synchronize()
+        assert co.carryover_read_status(sc.st) == 0
+        orc.round(r, m=m, attend=False)
+        Q = orc.seq_block(wl.spec_q(w, r), 1)
+        Ks = host(w, wl.spec_self(w, "k", r))
+        Vs = host(w, wl.spec_self(w, "v", r))
+        O, LSE = oracle.attend_state_with_self(orc.st, Q, Ks, Vs, w.Hq, w.theta, seqs=orc.seqs)
+        g = to_np(out)
+        gl = lse.cpu().numpy().astype(np.float64)
+        for s in orc.seqs:
+            assert_heads_close(g[:, s], O[:, s], tol, f"{w.name} r{r} O seq {s}")
+            err = np.abs(gl[:, s] - LSE[:, s]).max()
+            assert err <= tol, f"{w.name} r{r} LSE seq {s}: {err}"
