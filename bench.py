@@ -504,10 +504,12 @@ def main():
 def variant_costs(torch, co, sc, w, lib, step, rewind, chain, args, stream, attend, q_last, lse,
                   dt):
     """Costs of the variants next to the path, on the same state:
-    * the attention mass on the carried rows (drafter_carry_mass) after the
-      attention call on the final state, per call;
-    * the separate-projector update: the timed rounds again from the snapshot
-      with a second fusion matrix for carried rows (no E), rounds/s."""
+    * the separate-projector update and the RMS-normalised update: the timed
+      rounds again from the snapshot, rounds/s;
+    * the attention mass on the carried rows (drafter_carry_mass) and the
+      block self-segment merge (drafter_self_merge) after the attention call on
+      the final state, per call (the merge repeats on the same output buffer:
+      only its time is used)."""
     from synth import device as sdev
     from synth import workloads as wl
     # the rounds read sc.W through a pointer: set its carry projector for them
@@ -519,17 +521,31 @@ def variant_costs(torch, co, sc, w, lib, step, rewind, chain, args, stream, atte
     if co.carryover_read_status(sc.st):
         raise RuntimeError("device status after the separate-projector rounds")
     del wfc
-    # the chain ends with carry segments again: the mass of the last attention
+    # RMS-normalised F output: the timed rounds again from the snapshot
+    off = sdev.materialise(w.replace(dtype="f32"), wl.spec_znorm(w), "cuda")
+    gain = torch.tensor(np.float32(w.sigma_z), device="cuda") * (1.0 + off)
+    sc.W.z_norm = gain.data_ptr()
+    rewind()
+    dt_norm = chain(0)
+    sc.W.z_norm = None
+    if co.carryover_read_status(sc.st):
+        raise RuntimeError("device status after the normalised rounds")
+    # the chain ends with carry segments again: the mass of the last attention,
+    # and the block's own rows merged in as a third segment
+    n = min(args.steps, 100)
     mass = torch.empty_like(lse)
-
-    def mass_call():
-        co.drafter_carry_mass(sc.dims, 0, w.L, q_last, sc.st, lse, mass)
-
     attend()
-    mass_s = timed_calls(torch, stream, min(args.steps, 100), mass_call)
+    mass_s = timed_calls(torch, stream, n, lambda: co.drafter_carry_mass(
+        sc.dims, 0, w.L, q_last, sc.st, lse, mass))
+    ks, vs = sc.self_kv(0)
+    out = torch.zeros((w.L, w.S, w.B, w.Hq, w.hd), dtype=sc.tdtype, device="cuda")
+    self_s = timed_calls(torch, stream, n, lambda: co.drafter_self_merge(
+        sc.dims, 0, w.L, q_last, ks, vs, sc.st, out, lse))
     return {"carry_mass_call_us": mass_s * 1e6,
+            "self_merge_call_us": self_s * 1e6,
             "separate_projector": {"rounds_per_s": args.steps / dt_sep,
-                                   "vs_embedding": dt / dt_sep}}
+                                   "vs_embedding": dt / dt_sep},
+            "z_norm": {"rounds_per_s": args.steps / dt_norm, "vs_plain": dt / dt_norm}}
 
 
 class Scrub:
