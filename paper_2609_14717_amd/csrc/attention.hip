@@ -1639,7 +1639,264 @@ __global__ __launch_bounds__(256) void attn_share_merge_kernel(AttnArgs a, int s
   }
 }
 
+// ------------------------------------------ bf16 per-wavefront slices path
+//
+// For query tiles too large to stage more than one segment's queries in LDS
+// next to the ring (head_dim 128, 64 query rows), every wavefront takes its
+// own equal slice of the global tile order and walks it alone: no rounds, no
+// barriers, no merging between wavefronts.  Per piece of a segment in the
+// slice, the wavefront loads the queries straight into its MFMA fragments
+// (rotated in registers: at head_dim 128 a lane holds both dims of each
+// rotation pair), streams the piece's tiles through a private two-stage ring
+// and then writes the normalised output (a whole segment) or a record for
+// attn_bf16_combine_kernel (slices are wavefronts: record slot = slice + segment).
+// Tiles of a sequence: its committed pages two by two, then its carry pages
+// two by two.
+constexpr int kWaveWaves = 4;    // wavefronts per workgroup
+constexpr int kWaveRing = 2;     // ring stages per wavefront
+
+template <int HD, int NQT>
+__global__ __launch_bounds__(256, 1) void attn_wave_kernel(AttnArgs a, int layer_count,
+                                                           int n_slices, int hdr_floats) {
+  // NQT tiles of 32 query rows, each its own Tile32 stepping over the same key
+  // tile (one fragment set live at a time keeps the registers within budget)
+  using TT = Tile32<HD, 1>;
+  constexpr int NQP = NQT * 32, NW = kWaveWaves, NS = kWaveRing;
+  constexpr int PAGE_BYTES = TT::PAGE_BYTES, LPP = TT::LPP, TILE_BYTES = TT::TILE_BYTES;
+  constexpr int KK = TT::KK;
+  static_assert(4 * LPP * (NS - 1) < 64, "vmcnt");
+  __shared__ __align__(16) unsigned char ring[NW * NS * TILE_BYTES];
+  __shared__ int tstart[kMaxAttnSeqs + 1];
+  __shared__ int ctx_l[kMaxAttnSeqs], carry_l[kMaxAttnSeqs];
+  __shared__ int part[256];
+  __shared__ double inv_lds[HD / 2];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int S = a.S, G = a.Hq / a.Hkv, nq = a.B * G;
+  if (tid < HD / 2) inv_lds[tid] = a.rope_inv[tid] * kInv2Pi;
+
+  // ---- tiles per sequence and their prefix (the same in every workgroup)
+  constexpr int SPT = (kMaxAttnSeqs + 255) / 256;   // sequences per thread
+  int nts[SPT];
+  int sum = 0;
+#pragma unroll
+  for (int i = 0; i < SPT; ++i) {
+    const int s = tid * SPT + i;
+    nts[i] = 0;
+    if (s < S) {
+      const SeqInfo si = seq_info(a, s, 1);
+      const int ctx = si.ok ? si.ctx : 0, carry = si.ok ? si.carry : 0;
+      if (!si.ok && blockIdx.x == 0) set_status(a.status, CO_ERR_LENGTH);
+      ctx_l[s] = ctx;
+      carry_l[s] = carry;
+      const int npc = (ctx + kPage - 1) / kPage, ncp = (carry + kPage - 1) / kPage;
+      nts[i] = (npc + 1) / 2 + (ncp + 1) / 2;
+    }
+    sum += nts[i];
+  }
+  part[tid] = sum;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {   // inclusive scan of the per-thread sums
+    const int v = tid >= off ? part[tid - off] : 0;
+    __syncthreads();
+    part[tid] += v;
+    __syncthreads();
+  }
+  {
+    int x = part[tid] - sum;
+#pragma unroll
+    for (int i = 0; i < SPT; ++i) {
+      const int s = tid * SPT + i;
+      if (s < S) tstart[s] = x;
+      x += nts[i];
+    }
+    if (tid == 255) tstart[S] = part[255];
+  }
+  __syncthreads();
+  const int T1 = tstart[S];
+  const int n_segs = layer_count * a.Hkv;
+  const int64_t t_all = static_cast<int64_t>(n_segs) * T1;
+  const int w = blockIdx.x * NW + wave;
+  const int t0 = static_cast<int>(t_all * w / n_slices);
+  const int t1 = static_cast<int>(t_all * (w + 1) / n_slices);
+  int* hdr = reinterpret_cast<int*>(a.ws);
+  if (lane == 0) hdr[S + 1 + w] = t0;
+  if (w == 0) {
+    for (int s = lane; s <= S; s += 64) hdr[s] = tstart[s];
+    if (lane == 0) hdr[S + 1 + n_slices] = static_cast<int>(t_all);
+  }
+
+  const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
+  const uint16_t* vc = static_cast<const uint16_t*>(a.v_cache);
+  const uint16_t* kk = static_cast<const uint16_t*>(a.k_carry);
+  const uint16_t* vk = static_cast<const uint16_t*>(a.v_carry);
+  const uint16_t* Q = static_cast<const uint16_t*>(a.q);
+  const bool rotate_q = !(a.flags & CO_Q_PREROTATED);
+  const float qscale = rsqrtf(static_cast<float>(HD)) * kLog2e;
+  // per-lane source offsets (elements) of the loads of one page: K rows land
+  // XOR-swizzled, V pages are copied as they are
+  int k_off[LPP], v_off[LPP];
+#pragma unroll
+  for (int q = 0; q < LPP; ++q) {
+    const int byte = q * 1024 + lane * 16;
+    const int r = byte / TT::ROWB, pch = (byte % TT::ROWB) / 16;
+    k_off[q] = r * HD + (pch ^ (r & (TT::CPR - 1))) * 8;
+    v_off[q] = byte / 2;
+  }
+  const uint32_t my_ring = lds_addr(ring) + wave * NS * TILE_BYTES;
+  const int64_t page_stride = static_cast<int64_t>(a.Hkv) * kPage * HD;
+  auto load_page = [&](const uint16_t* src, bool is_v, uint32_t dst) {
+#pragma unroll
+    for (int q = 0; q < LPP; ++q) lds_dma16_opaque(src + (is_v ? v_off[q] : k_off[q]), dst + q * 1024);
+  };
+
+  TT T[NQT];
+  for (int t = t0; t < t1;) {
+    // ---- the piece of one segment that starts at tile t
+    const int seg = t / T1, local = t - seg * T1;
+    int lo = 0, hi = S;   // the sequence: tstart[s] <= local < tstart[s + 1]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (tstart[mid] <= local) lo = mid; else hi = mid;
+    }
+    const int s = lo;
+    const int j0 = local - tstart[s];
+    const int nts_s = tstart[s + 1] - tstart[s];
+    const int pe = min(t1, seg * T1 + tstart[s + 1]);
+    const int j1 = j0 + (pe - t);
+    const int layer_local = seg / a.Hkv, g = seg % a.Hkv, layer = a.layer_begin + layer_local;
+    const int ctx = ctx_l[s], carry = carry_l[s];
+    const int npc = (ctx + kPage - 1) / kPage, nct = (npc + 1) / 2;
+    const int ncp = (carry + kPage - 1) / kPage;
+
+    // queries of the segment straight into the B fragments, rotated at ctx + i
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
+      T[qt].setup(lane);
+      const int qn = qt * 32 + T[qt].r32;
+      u16x8 raw[KK];
+      const bool live = qn < nq;
+      const int64_t base = live ? out_row(a, layer_local, s, g, qn, G) * HD : 0;
+#pragma unroll
+      for (int k = 0; k < KK; ++k)
+        raw[k] = *reinterpret_cast<const u16x8*>(Q + base + k * 16 + T[qt].half * 8);
+      const int pos = ctx + qn / G;
+#pragma unroll
+      for (int k = 0; k < KK / 2; ++k)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          float x = live ? bf2f(raw[k][e]) : 0.f, y = live ? bf2f(raw[k + KK / 2][e]) : 0.f;
+          if (rotate_q) {
+            float cs, sn;
+            rope_cos_sin_rev(pos, inv_lds[k * 16 + T[qt].half * 8 + e], &cs, &sn);
+            const float x2 = x * cs - y * sn, y2 = y * cs + x * sn;
+            x = x2;
+            y = y2;
+          }
+          T[qt].qf[0][k][e] = f2bf(x * qscale);
+          T[qt].qf[0][k + KK / 2][e] = f2bf(y * qscale);
+        }
+    }
+
+    // tile j of the sequence: two committed pages, or two carry pages
+    const int64_t head0 = (static_cast<int64_t>(layer) * a.num_pages * a.Hkv + g) * (kPage * HD);
+    const int32_t* pt = a.page_table + static_cast<int64_t>(s) * a.max_pages;
+    auto issue = [&](int j, int phys0, int phys1) {
+      const uint32_t dst = my_ring + (j % NS) * TILE_BYTES;
+      const uint16_t *k0, *k1, *v0, *v1;
+      if (j < nct) {
+        k0 = kc + head0 + phys0 * page_stride;
+        v0 = vc + head0 + phys0 * page_stride;
+        k1 = kc + head0 + phys1 * page_stride;
+        v1 = vc + head0 + phys1 * page_stride;
+      } else {
+        const int cp0 = 2 * (j - nct), cp1 = min(cp0 + 1, ncp - 1);
+        const int64_t r0 = ((static_cast<int64_t>(layer) * a.S + s) * a.CP + cp0) * a.Hkv + g;
+        const int64_t r1 = ((static_cast<int64_t>(layer) * a.S + s) * a.CP + cp1) * a.Hkv + g;
+        k0 = kk + r0 * (kPage * HD);
+        v0 = vk + r0 * (kPage * HD);
+        k1 = kk + r1 * (kPage * HD);
+        v1 = vk + r1 * (kPage * HD);
+      }
+      load_page(k0, false, dst);
+      load_page(k1, false, dst + PAGE_BYTES);
+      load_page(v0, true, dst + 2 * PAGE_BYTES);
+      load_page(v1, true, dst + 3 * PAGE_BYTES);
+    };
+    auto keys = [&](int j, int h) {
+      return j < nct ? keys_in(ctx, j, h) : keys_in(carry, j - nct, h);
+    };
+    // committed page ids of tiles [c0, c0 + 64): lane l holds pages 2(c0 + l), 2(c0 + l) + 1;
+    // a rejected id reads page 0 with its keys masked
+    int id0 = 0, id1 = 0, c0 = -(1 << 30), bad = 0;   // no window fetched yet
+    auto fetch_ids = [&](int c) {
+      c0 = c;
+      const int jt = c + lane, p = 2 * jt;
+      id0 = 0;
+      id1 = 0;
+      bad = 0;
+      if (jt < nct) {
+        const int x0 = pt[p];
+        const int x1 = p + 1 < npc ? pt[p + 1] : x0;
+        const bool b0 = x0 < 0 || x0 >= a.num_pages, b1 = x1 < 0 || x1 >= a.num_pages;
+        if (b0 || b1) set_status(a.status, CO_ERR_PAGE_RANGE);
+        id0 = b0 ? 0 : x0;
+        id1 = b1 ? 0 : x1;
+        bad = (b0 ? 1 : 0) | (b1 ? 2 : 0);
+      }
+    };
+    auto tile_ids = [&](int j, int& p0, int& p1, int& b) {   // j uniform, committed
+      if (j >= c0 + 64 || j < c0) fetch_ids(j);
+      p0 = __builtin_amdgcn_readlane(id0, j - c0);
+      p1 = __builtin_amdgcn_readlane(id1, j - c0);
+      b = __builtin_amdgcn_readlane(bad, j - c0);
+    };
+    auto issue_tile = [&](int j, int& b) {
+      int p0 = 0, p1 = 0;
+      b = 0;
+      if (j < nct) tile_ids(j, p0, p1, b);
+      issue(j, p0, p1);
+    };
+
+    int bcur = 0, bnext = 0;
+    issue_tile(j0, bcur);
+    for (int j = j0; j < j1; ++j) {
+      const bool more = j + 1 < j1;
+      if (more) issue_tile(j + 1, bnext);   // into the slot of tile j - 1, consumed
+      if (more) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(4 * LPP) : "memory");
+      else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      const int n0 = (bcur & 1) ? 0 : keys(j, 0), n1 = (bcur & 2) ? 0 : keys(j, 1);
+      if (n0 + n1 > 0) {
+#pragma unroll
+        for (int qt = 0; qt < NQT; ++qt) T[qt].step(ring + (wave * NS + j % NS) * TILE_BYTES, n0, n1);
+      }
+      bcur = bnext;
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the ring's last tile is read
+
+    // ---- a whole segment: normalise and write; else a record for the combine
+    float* rec = slot_ptr(a, hdr_floats, w + static_cast<int64_t>(seg) * S + s, NQP);
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
+      if (j0 == 0 && j1 == nts_s)
+        T[qt].write_out(a, layer_local, s, g, qt * 32, nq);
+      else
+        T[qt].write_record(rec, NQP, qt * 32);
+    }
+    t = pe;
+  }
+}
+
 }  // namespace
+
+// Whether head_dim-128 launches with 64 query rows take the per-wavefront
+// slices path (the default: measured faster at every such shape; CO_ATTN_WAVE=0
+// selects the persistent path, for tests and tuning).
+static bool wave_slices_enabled() {
+  if (const char* env = getenv("CO_ATTN_WAVE")) return atoi(env) != 0;
+  return true;
+}
 
 AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int num_pages,
                         int dtype, int num_cus) {
@@ -1676,6 +1933,20 @@ AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pa
     const int64_t rows_c = static_cast<int64_t>(L) * num_pages * Hkv;
     const int64_t rows_u = static_cast<int64_t>(L) * S * cp * Hkv;
     p.ok = S <= kMaxAttnSeqs && tiles < INT32_MAX && rows_c < INT32_MAX && rows_u < INT32_MAX;
+    // per-wavefront slices for head_dim 128 with 64 query rows: the workspace
+    // covers either path, so that the choice can change between calls
+    const int n_sl = p.n_wg * kWaveWaves;
+    if (hd == 128 && p.nq_pad == 64 && n_sl <= kMaxMergeSlices) {
+      const int hdr_w = (S + 1 + n_sl + 1 + 63) / 64 * 64;
+      const size_t bytes_w =
+          (hdr_w + (static_cast<size_t>(n_sl) + static_cast<size_t>(L) * Hkv * S) * rec) * 4;
+      if (bytes_w > p.bytes) p.bytes = bytes_w;
+      if (wave_slices_enabled()) {
+        p.wave = true;
+        p.n_wg = n_sl;
+        p.hdr_floats = hdr_w;
+      }
+    }
   } else {
     // fp32 path: chunks of pages, one workgroup each; short chunks, so that a
     // short context still spreads over many workgroups
@@ -1725,6 +1996,15 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
       hipLaunchKernelGGL(attn_share_merge_kernel<64>, cgrid, dim3(256), 0, stream, a, sp, ns, nqp, kGroupSeqs);
     else
       hipLaunchKernelGGL(attn_share_merge_kernel<128>, cgrid, dim3(256), 0, stream, a, sp, ns, nqp, kGroupSeqs);
+    return hipGetLastError();
+  }
+  if (a.dtype == CO_DTYPE_BF16 && p.wave) {
+    hipLaunchKernelGGL((attn_wave_kernel<128, 2>), dim3(p.n_wg / kWaveWaves), dim3(256), 0, stream,
+                       a, layer_count, p.n_wg, p.hdr_floats);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(attn_bf16_combine_kernel, mgrid, dim3(256), 0, stream, a, layer_count,
+                       p.n_wg, p.hdr_floats, p.nq_pad);
     return hipGetLastError();
   }
   if (a.dtype == CO_DTYPE_BF16) {

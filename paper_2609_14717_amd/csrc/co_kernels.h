@@ -85,6 +85,7 @@ struct AttnPlan {
   int n_wg, hdr_floats;        // bf16 persistent path: workgroups, header floats
   int round_tiles;             // bf16 persistent path: tiles per wavefront per round
   int64_t park_off;            // bf16 persistent path: parked partials (workspace floats)
+  bool wave;                   // bf16: per-wavefront slices (n_wg = slices, not workgroups)
   int nq_pad;
   bool ok;                     // false: shapes beyond what one launch can cover
   size_t bytes;

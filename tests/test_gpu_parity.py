@@ -354,3 +354,27 @@ def test_fused_projection(w, monkeypatch):
 def test_fused_projection_train_small(monkeypatch):
     monkeypatch.setenv("CO_PROJECT_FUSED_MIN_ROWS", "1")
     train_small_check(True)
+
+
+# Per-wavefront slices (head_dim 128, 64 query rows), forced on: full-size
+# segments, pieces split over many slices (and several pieces per slice, with
+# few workgroups), one-page contexts, carry-only windows and ragged lengths.
+WAVE_RAGGED = wl.Workload("wave_ragged_hd128", S=6, B=16, Dcat=512, d=256, L=2, Hq=8, Hkv=2,
+                          hd=128, dtype="bf16", theta=1e6, ctx_lo=1, ctx_hi=900,
+                          ctx_mode="direct", accept=("geom", 0.3), rounds=4, seed=0x5EED0B)
+
+
+@pytest.mark.parametrize("wgs", ["", "1", "3", "70"], ids=lambda v: f"wg{v or 'dflt'}")
+@pytest.mark.parametrize("w", [SMALL_G4, BATCH3_8B, WAVE_RAGGED], ids=lambda w: w.name)
+def test_wave_slices(w, wgs, monkeypatch):
+    monkeypatch.setenv("CO_ATTN_WAVE", "1")
+    if wgs:
+        monkeypatch.setenv("CO_ATTN_WORKGROUPS", wgs)
+    run_rounds(w, 3)
+
+
+# The persistent path at the same shapes (no longer their default).
+@pytest.mark.parametrize("w", [SMALL_G4, WAVE_RAGGED], ids=lambda w: w.name)
+def test_persistent_hd128_64_rows(w, monkeypatch):
+    monkeypatch.setenv("CO_ATTN_WAVE", "0")
+    run_rounds(w, 3)
