@@ -1652,23 +1652,25 @@ __global__ __launch_bounds__(256) void attn_share_merge_kernel(AttnArgs a, int s
 // attn_bf16_combine_kernel (slices are wavefronts: record slot = slice + segment).
 // Tiles of a sequence: its committed pages two by two, then its carry pages
 // two by two.
-constexpr int kWaveWaves = 4;    // wavefronts per workgroup
 constexpr int kWaveRing = 2;     // ring stages per wavefront
 
+// wavefronts per workgroup: one per SIMD at head_dim 128 (registers), two at 64
+constexpr int wave_waves(int hd) { return hd == 128 ? 4 : 8; }
+
 template <int HD, int NQT>
-__global__ __launch_bounds__(256, 1) void attn_wave_kernel(AttnArgs a, int layer_count,
-                                                           int n_slices, int hdr_floats) {
+__global__ __launch_bounds__(64 * wave_waves(HD), 1) void attn_wave_kernel(
+    AttnArgs a, int layer_count, int n_slices, int hdr_floats) {
   // NQT tiles of 32 query rows, each its own Tile32 stepping over the same key
   // tile (one fragment set live at a time keeps the registers within budget)
   using TT = Tile32<HD, 1>;
-  constexpr int NQP = NQT * 32, NW = kWaveWaves, NS = kWaveRing;
+  constexpr int NQP = NQT * 32, NW = wave_waves(HD), NS = kWaveRing, NTHR = 64 * NW;
   constexpr int PAGE_BYTES = TT::PAGE_BYTES, LPP = TT::LPP, TILE_BYTES = TT::TILE_BYTES;
   constexpr int KK = TT::KK;
   static_assert(4 * LPP * (NS - 1) < 64, "vmcnt");
   __shared__ __align__(16) unsigned char ring[NW * NS * TILE_BYTES];
   __shared__ int tstart[kMaxAttnSeqs + 1];
   __shared__ int ctx_l[kMaxAttnSeqs], carry_l[kMaxAttnSeqs];
-  __shared__ int part[256];
+  __shared__ int part[NTHR];
   __shared__ double inv_lds[HD / 2];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -1677,7 +1679,7 @@ __global__ __launch_bounds__(256, 1) void attn_wave_kernel(AttnArgs a, int layer
   if (tid < HD / 2) inv_lds[tid] = a.rope_inv[tid] * kInv2Pi;
 
   // ---- tiles per sequence and their prefix (the same in every workgroup)
-  constexpr int SPT = (kMaxAttnSeqs + 255) / 256;   // sequences per thread
+  constexpr int SPT = (kMaxAttnSeqs + NTHR - 1) / NTHR;   // sequences per thread
   int nts[SPT];
   int sum = 0;
 #pragma unroll
@@ -1697,7 +1699,7 @@ __global__ __launch_bounds__(256, 1) void attn_wave_kernel(AttnArgs a, int layer
   }
   part[tid] = sum;
   __syncthreads();
-  for (int off = 1; off < 256; off <<= 1) {   // inclusive scan of the per-thread sums
+  for (int off = 1; off < NTHR; off <<= 1) {   // inclusive scan of the per-thread sums
     const int v = tid >= off ? part[tid - off] : 0;
     __syncthreads();
     part[tid] += v;
@@ -1711,7 +1713,7 @@ __global__ __launch_bounds__(256, 1) void attn_wave_kernel(AttnArgs a, int layer
       if (s < S) tstart[s] = x;
       x += nts[i];
     }
-    if (tid == 255) tstart[S] = part[255];
+    if (tid == NTHR - 1) tstart[S] = part[NTHR - 1];
   }
   __syncthreads();
   const int T1 = tstart[S];
@@ -1890,12 +1892,12 @@ __global__ __launch_bounds__(256, 1) void attn_wave_kernel(AttnArgs a, int layer
 
 }  // namespace
 
-// Whether head_dim-128 launches with 64 query rows take the per-wavefront
-// slices path (the default: measured faster at every such shape; CO_ATTN_WAVE=0
-// selects the persistent path, for tests and tuning).
-static bool wave_slices_enabled() {
+// Whether a launch takes the per-wavefront slices path where the shape allows
+// it: by default at head_dim 128 with 64 query rows (measured faster at every
+// such shape); CO_ATTN_WAVE=0/1 chooses, for tests and tuning.
+static bool wave_slices_enabled(int hd) {
   if (const char* env = getenv("CO_ATTN_WAVE")) return atoi(env) != 0;
-  return true;
+  return hd == 128;
 }
 
 AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int num_pages,
@@ -1935,13 +1937,15 @@ AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pa
     p.ok = S <= kMaxAttnSeqs && tiles < INT32_MAX && rows_c < INT32_MAX && rows_u < INT32_MAX;
     // per-wavefront slices for head_dim 128 with 64 query rows: the workspace
     // covers either path, so that the choice can change between calls
-    const int n_sl = p.n_wg * kWaveWaves;
-    if (hd == 128 && p.nq_pad == 64 && n_sl <= kMaxMergeSlices) {
+    const int n_sl = p.n_wg * wave_waves(hd);
+    const bool wave_shape = (hd == 128 && p.nq_pad == 64) ||
+                            (hd == 64 && (p.nq_pad == 32 || p.nq_pad == 64));
+    if (wave_shape && n_sl <= kMaxMergeSlices) {
       const int hdr_w = (S + 1 + n_sl + 1 + 63) / 64 * 64;
       const size_t bytes_w =
           (hdr_w + (static_cast<size_t>(n_sl) + static_cast<size_t>(L) * Hkv * S) * rec) * 4;
       if (bytes_w > p.bytes) p.bytes = bytes_w;
-      if (wave_slices_enabled()) {
+      if (wave_slices_enabled(hd)) {
         p.wave = true;
         p.n_wg = n_sl;
         p.hdr_floats = hdr_w;
@@ -1999,8 +2003,17 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
     return hipGetLastError();
   }
   if (a.dtype == CO_DTYPE_BF16 && p.wave) {
-    hipLaunchKernelGGL((attn_wave_kernel<128, 2>), dim3(p.n_wg / kWaveWaves), dim3(256), 0, stream,
-                       a, layer_count, p.n_wg, p.hdr_floats);
+    const int nw = wave_waves(a.hd);
+    const dim3 wgrid(p.n_wg / nw), wblock(64 * nw);
+    if (a.hd == 128)
+      hipLaunchKernelGGL((attn_wave_kernel<128, 2>), wgrid, wblock, 0, stream, a, layer_count,
+                         p.n_wg, p.hdr_floats);
+    else if (p.nq_pad == 32)
+      hipLaunchKernelGGL((attn_wave_kernel<64, 1>), wgrid, wblock, 0, stream, a, layer_count,
+                         p.n_wg, p.hdr_floats);
+    else
+      hipLaunchKernelGGL((attn_wave_kernel<64, 2>), wgrid, wblock, 0, stream, a, layer_count,
+                         p.n_wg, p.hdr_floats);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(attn_bf16_combine_kernel, mgrid, dim3(256), 0, stream, a, layer_count,

@@ -378,3 +378,14 @@ def test_wave_slices(w, wgs, monkeypatch):
 def test_persistent_hd128_64_rows(w, monkeypatch):
     monkeypatch.setenv("CO_ATTN_WAVE", "0")
     run_rounds(w, 3)
+
+
+# The same path at head_dim 64 (32 and 64 query rows, eight wavefronts per
+# workgroup), forced on.
+@pytest.mark.parametrize("wgs", ["", "1", "5"], ids=lambda v: f"wg{v or 'dflt'}")
+@pytest.mark.parametrize("w", [SMALL_RAGGED, MANY_SEQS, WIDE64], ids=lambda w: w.name)
+def test_wave_slices_hd64(w, wgs, monkeypatch):
+    monkeypatch.setenv("CO_ATTN_WAVE", "1")
+    if wgs:
+        monkeypatch.setenv("CO_ATTN_WORKGROUPS", wgs)
+    run_rounds(w, 3)
