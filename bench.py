@@ -42,8 +42,8 @@ PROFILES = os.path.join(ROOT, "profiles")
 # of these are not reported
 ATTN_SOURCES = [os.path.join(ROOT, "paper_2609_14717_amd", "csrc", f)
                 for f in ("attention.hip", "co_device.h", "co_kernels.h")]
-ATTN_KERNELS = ("attn_bf16_kernel", "attn_bf16_combine_kernel", "attn_group_kernel",
-                "attn_share_merge_kernel")
+ATTN_KERNELS = ("attn_bf16_kernel", "attn_wave_kernel", "attn_bf16_combine_kernel",
+                "attn_group_kernel", "attn_share_merge_kernel")
 ATTN_KERNELS_F32 = ("attn_f32_kernel", "attn_chunk_merge_kernel")
 ATTN_WARM = 5       # untimed attention calls before the timed ones
 COLD_CALLS = 50     # cold calls timed (each after a cache scrub)

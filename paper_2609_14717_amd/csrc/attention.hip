@@ -29,6 +29,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
+
 #include "co_kernels.h"
 
 namespace co {
@@ -1653,6 +1655,7 @@ __global__ __launch_bounds__(256) void attn_share_merge_kernel(AttnArgs a, int s
 // Tiles of a sequence: its committed pages two by two, then its carry pages
 // two by two.
 constexpr int kWaveRing = 2;     // ring stages per wavefront
+constexpr int kWaveMinTiles = 8; // tiles per slice below which fewer slices are launched
 
 // wavefronts per workgroup: one per SIMD at head_dim 128 (registers), two at 64
 constexpr int wave_waves(int hd) { return hd == 128 ? 4 : 8; }
@@ -1937,7 +1940,16 @@ AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pa
     p.ok = S <= kMaxAttnSeqs && tiles < INT32_MAX && rows_c < INT32_MAX && rows_u < INT32_MAX;
     // per-wavefront slices for head_dim 128 with 64 query rows: the workspace
     // covers either path, so that the choice can change between calls
-    const int n_sl = p.n_wg * wave_waves(hd);
+    // slices: one per wavefront of every CU, but no more than one per
+    // kWaveMinTiles tiles the page table allows (few tiles in many slices would
+    // only multiply the records to combine); the workgroup override sets it
+    const int nw_h = wave_waves(hd);
+    const int64_t cap_tiles = static_cast<int64_t>(L) * Hkv * S * ((max_pages + 1) / 2 + (cp + 1) / 2);
+    int n_sl = p.n_wg * nw_h;
+    if (getenv("CO_ATTN_WORKGROUPS") == nullptr) {
+      const int64_t by_tiles = (cap_tiles / kWaveMinTiles + nw_h - 1) / nw_h * nw_h;
+      n_sl = static_cast<int>(std::max<int64_t>(nw_h, std::min<int64_t>(n_sl, by_tiles)));
+    }
     const bool wave_shape = (hd == 128 && p.nq_pad == 64) ||
                             (hd == 64 && (p.nq_pad == 32 || p.nq_pad == 64));
     if (wave_shape && n_sl <= kMaxMergeSlices) {
