@@ -1015,19 +1015,19 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
                                                                 int n_wg, int hdr_floats,
                                                                 int nq_pad) {
   constexpr int kBatch = 8;
-  __shared__ int bnd[kMaxMergeSlices + 1];
   const int s = blockIdx.x, seg = blockIdx.y;
   const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
   const int hd = a.hd, G = a.Hq / a.Hkv, nq = a.B * G, q4 = hd / 4;
   const int tid = threadIdx.x;
   const int* hdr = reinterpret_cast<const int*>(a.ws);
-  const int* bounds = hdr + a.S + 1;
-  for (int i = tid; i <= n_wg; i += 256) bnd[i] = bounds[i];
+  // slice w covers tiles [T w / n_wg, T (w + 1) / n_wg) of the T in the launch
+  // (the launch records T after the slice starts)
+  const int64_t T = hdr[a.S + 1 + n_wg];
+  auto bnd = [&](int w) { return static_cast<int>(T * w / n_wg); };
   const SeqInfo si = seq_info(a, s, 1);
   if (!si.ok && seg == 0 && tid == 0 && blockIdx.z == 0) set_status(a.status, CO_ERR_LENGTH);
   const int T1 = hdr[a.S], ts = hdr[s];
   const int nts = hdr[s + 1] - ts;
-  __syncthreads();
   uint16_t* out = static_cast<uint16_t*>(a.out);
   if (nts == 0) {                      // no keys: O = 0, LSE = -inf
     for (int idx = tid + blockIdx.z * 256; idx < nq * hd; idx += 256 * gridDim.z)
@@ -1037,14 +1037,11 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
     return;
   }
   const int A = seg * T1 + ts;
-  // owner of tile x: the last slice with bnd[w] <= x (bnd is non-decreasing)
+  // owner of tile x: the last slice w with T w / n_wg <= x, i.e. the largest w
+  // with T w < (x + 1) n_wg
   auto owner = [&](int x) {
-    int lo = 0, hi = n_wg;
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (bnd[mid] <= x) lo = mid; else hi = mid;
-    }
-    return lo;
+    const int64_t w = ((static_cast<int64_t>(x) + 1) * n_wg + T - 1) / T - 1;
+    return static_cast<int>(w < n_wg - 1 ? w : n_wg - 1);
   };
   const int w_lo = owner(A), w_hi = owner(A + nts - 1);
   if (w_lo == w_hi) return;            // finished in place
@@ -1072,7 +1069,7 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
       float Mb = M;
 #pragma unroll
       for (int i = 0; i < kBatch; ++i) {
-        if (!(r0 + i < nrec && bnd[w_lo + r0 + i] < bnd[w_lo + r0 + i + 1])) mv[i] = -INFINITY;
+        if (!(r0 + i < nrec && bnd(w_lo + r0 + i) < bnd(w_lo + r0 + i + 1))) mv[i] = -INFINITY;
         Mb = fmaxf(Mb, mv[i]);
       }
       const float f = (M == -INFINITY) ? 0.f : exp2f(M - Mb);
