@@ -26,8 +26,9 @@ verification remains valid"); the separate-projector update, where carried
 rows go through a second fusion matrix instead of F + E (Section 4, Table
 3(b)); the share of attention that falls on the carried rows (Appendix
 "Attention to carried states"); the block's own rows as a third attention
-segment [C ; U ; S]; and an RMS normalisation of F's output before the K/V
-projections (the paper's equations omit normalisation, Section 2.1).
+segment [C ; U ; S]; and RMS normalisations of F's output before the K/V
+projections and of every head's key before its rotation (the paper's
+equations omit normalisation, Section 2.1).
 
 Readings where the paper is silent (each one a stated choice of this oracle): no norm
 and no bias in F, K_l, V_l; rotate-half RoPE with inverse frequency
@@ -160,7 +161,8 @@ def rms_norm(z, g):
     return z / np.sqrt(np.mean(z * z, axis=-1, keepdims=True) + RMS_EPS) * np.asarray(g, np.float64)
 
 
-def project(H, E, add_e, WF, WKV, pos, L, Hkv, hd, theta, WF_carry=None, z_norm=None):
+def project(H, E, add_e, WF, WKV, pos, L, Hkv, hd, theta, WF_carry=None, z_norm=None,
+            k_norm=None):
     """Phi_l(H) of Eq. 1 for every layer, with E added to flagged rows before F
     (Eq. 2) and RoPE applied to the keys at each row's position.
 
@@ -172,6 +174,8 @@ def project(H, E, add_e, WF, WKV, pos, L, Hkv, hd, theta, WF_carry=None, z_norm=
     z_norm [d]: the normalisation variant: z = F(x) is RMS-normalised (gain
     z_norm) before the K/V projections (the equations omit normalisation,
     Section 2.1).
+    k_norm [L][hd]: per-head key normalisation: every head's key is
+    RMS-normalised (gain k_norm[l]) before it is rotated.
     Returns K, V as [M][L][Hkv][hd] float64.
     """
     H = np.asarray(H, np.float64)
@@ -185,7 +189,10 @@ def project(H, E, add_e, WF, WKV, pos, L, Hkv, hd, theta, WF_carry=None, z_norm=
     if z_norm is not None:
         z = rms_norm(z, z_norm)
     kv = (z @ np.asarray(WKV, np.float64).T).reshape(len(H), L, 2, Hkv, hd)
-    k = rope(kv[:, :, 0], np.asarray(pos)[:, None, None], theta)
+    k = kv[:, :, 0]
+    if k_norm is not None:
+        k = rms_norm(k, np.asarray(k_norm, np.float64)[None, :, None, :])
+    k = rope(k, np.asarray(pos)[:, None, None], theta)
     return k, kv[:, :, 1].copy()
 
 
@@ -330,7 +337,7 @@ def carry_mass_state(state: State, Q, Hq, theta, seqs=None, layers=None):
 
 
 def round_update(state: State, r, H, E, WF, WKV, theta, mode="carry", seqs=None,
-                 WF_carry=None, z_norm=None):
+                 WF_carry=None, z_norm=None, k_norm=None):
     """Post-verification update of Algorithm 1 for the sequences in ``seqs``,
     given a route result ``r`` (see ``route``).  H [S][B][Dcat].  With
     ``WF_carry`` the carried rows use the separate projector (see project)."""
@@ -342,7 +349,7 @@ def round_update(state: State, r, H, E, WF, WKV, theta, mode="carry", seqs=None,
         rows = np.arange(B) if mode in ("carry", "carry_only") else np.arange(m)
         pos = r["row_pos"][s][rows]
         k, v = project(H[s][rows], E, rows >= m, WF, WKV, pos, state.L, state.Hkv,
-                       state.hd, theta, WF_carry, z_norm)
+                       state.hd, theta, WF_carry, z_norm, k_norm)
         if mode == "carry_only":
             k_acc, v_acc = k[:0], v[:0]
         else:

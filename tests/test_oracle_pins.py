@@ -614,3 +614,33 @@ def test_self_segment_identical_keys_average_all_values():
     allv = np.concatenate([st.cv[0][0, :, 0], Vs[0, 0, :, 0]], axis=0)
     np.testing.assert_allclose(O[0, 0], np.broadcast_to(allv.mean(axis=0), O[0, 0].shape),
                                rtol=1e-12, atol=1e-12)
+
+
+def test_k_norm_keys_have_the_gain_rms_and_values_are_untouched():
+    """With unit gain every head's key has RMS sqrt(ms / (ms + eps)) after the
+    rotation (which preserves norms); values do not change; scaling K's weights
+    leaves the keys unchanged (up to the epsilon)."""
+    L, Hkv, hd, H, E, WF, WKV, pos, flag = _proj_case()
+    ones = np.ones((L, hd))
+    k0, v0 = oracle.project(H, E, flag, WF, WKV, pos, L, Hkv, hd, 1e4)
+    k1, v1 = oracle.project(H, E, flag, WF, WKV, pos, L, Hkv, hd, 1e4, k_norm=ones)
+    np.testing.assert_array_equal(v1, v0)
+    ms = np.mean(k0 * k0, axis=-1)                      # rotation keeps the norm
+    np.testing.assert_allclose(np.mean(k1 * k1, axis=-1), ms / (ms + oracle.RMS_EPS), rtol=1e-10)
+    W2 = WKV.copy().reshape(L, 2, Hkv * hd, -1)
+    W2[:, 0] *= 5.0                                     # keys only
+    k2, v2 = oracle.project(H, E, flag, WF, W2.reshape(WKV.shape), pos, L, Hkv, hd, 1e4,
+                            k_norm=ones)
+    np.testing.assert_allclose(k2, k1, rtol=1e-7, atol=1e-7)
+    np.testing.assert_array_equal(v2, v1)
+
+
+def test_k_norm_gain_applies_before_the_rotation():
+    """The gain multiplies the unrotated key: at position 0 (no rotation) the
+    key is the normalised key times the gain, elementwise."""
+    L, Hkv, hd, H, E, WF, WKV, pos, flag = _proj_case()
+    g = RNG.uniform(0.5, 1.5, (L, hd))
+    k1, _ = oracle.project(H, E, flag, WF, WKV, np.zeros(5), L, Hkv, hd, 1e4, k_norm=g)
+    k0, _ = oracle.project(H, E, flag, WF, WKV, np.zeros(5), L, Hkv, hd, 1e4)
+    r = np.sqrt(np.mean(k0 * k0, axis=-1, keepdims=True) + oracle.RMS_EPS)
+    np.testing.assert_allclose(k1, k0 / r * g[None, :, None, :], rtol=1e-12, atol=1e-12)
