@@ -129,6 +129,14 @@ typedef struct co_weights {
                                  (epsilon 1e-6) and multiplied by z_norm before the K/V
                                  projections (normalisation variant; the equations omit
                                  normalisation, Section 2.1)                          */
+  const float* k_norm;        /* optional per-head key RMS-norm gain, fp32
+                                 [num_layers][head_dim]: when non-NULL every key head of
+                                 layer l is divided by its root mean square over head_dim
+                                 (epsilon 1e-6) and multiplied by k_norm[l] before it is
+                                 rotated; values are not normalised (normalisation
+                                 variant, as z_norm).  Keys passed in by the caller
+                                 (carryover_import_kv, drafter_self_merge) are taken as
+                                 they are                                             */
 } co_weights;
 
 typedef struct co_state {

@@ -45,7 +45,8 @@ class co_dims(ctypes.Structure):
 class co_weights(ctypes.Structure):
     _fields_ = [("w_f", ctypes.c_void_p), ("w_kv", ctypes.c_void_p), ("e_carry", ctypes.c_void_p),
                 ("f_e", ctypes.c_void_p), ("w_f_carry", ctypes.c_void_p),
-                ("z_norm", ctypes.c_void_p)]
+                ("z_norm", ctypes.c_void_p),
+                ("k_norm", ctypes.c_void_p)]
 
 
 class co_state(ctypes.Structure):
@@ -141,12 +142,13 @@ def make_dims(S, B, Dcat, d, L, Hq, Hkv, hd, max_pages_per_seq, num_pages, dtype
                    float(theta))
 
 
-def weights(w_f, w_kv, e_carry, f_e=None, w_f_carry=None, z_norm=None):
+def weights(w_f, w_kv, e_carry, f_e=None, w_f_carry=None, z_norm=None, k_norm=None):
     """co_weights over device tensors; f_e (fp32 [model_dim], optional) from
     ``carryover_fold_e``; w_f_carry (optional) the separate carry projector;
-    z_norm (fp32 [model_dim], optional) the RMS-norm gain of F's output."""
+    z_norm (fp32 [model_dim], optional) the RMS-norm gain of F's output;
+    k_norm (fp32 [num_layers][head_dim], optional) the per-head key gain."""
     return co_weights(_ptr(w_f), _ptr(w_kv), _ptr(e_carry), _ptr(f_e), _ptr(w_f_carry),
-                      _ptr(z_norm))
+                      _ptr(z_norm), _ptr(k_norm))
 
 
 def state(t):

@@ -189,7 +189,7 @@ co_status carryover_project_kv(const co_dims* dims, const co_weights* w, const v
     return CO_ERR_INVALID_ARG;
   if (!aligned(hidden, 16) || !aligned(w->w_f, 16) || !aligned(w->w_kv, 16) ||
       !aligned(w->e_carry, 16) || !aligned(w->f_e, 16) || !aligned(w->w_f_carry, 16) ||
-      !aligned(w->z_norm, 4))
+      !aligned(w->z_norm, 4) || !aligned(w->k_norm, 4))
     return CO_ERR_INVALID_ARG;
   const ProjectPlan p = project_plan(dims);
   if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
@@ -207,6 +207,7 @@ co_status carryover_project_kv(const co_dims* dims, const co_weights* w, const v
   a.wfc = w->w_f_carry;
   a.znorm = w->z_norm;
   a.dst = make_dest(dims, route, state);
+  a.dst.knorm = w->k_norm;
   a.ws = ws;
   return hip_status(launch_project(a, p, stream));
 }

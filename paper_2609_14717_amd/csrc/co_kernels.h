@@ -36,6 +36,7 @@ struct KvDest {
   void* k_carry;
   void* v_carry;
   int32_t* status;
+  const float* knorm;   // per-head key RMS-norm gain [L][hd], or null
 };
 
 struct ProjectArgs {

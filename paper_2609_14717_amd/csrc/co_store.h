@@ -17,6 +17,34 @@ __device__ __forceinline__ double rope_table(const KvDest& e, int i) {
 
 __device__ __forceinline__ bool is_carry_row(int32_t dst) { return dst < 0 && dst != kSkip; }
 
+constexpr float kRmsEps = 1e-6f;   // epsilon of the RMS normalisation variants
+
+// Per-head key normalisation (a variant; the equations omit normalisation,
+// Section 2.1): the key half of head segment `seg` is divided by its root mean
+// square over the hd dims and multiplied by the layer's gain, before it is
+// rotated.  The segment's hd values are spread over `lanes` consecutive lanes
+// (a power of two, aligned within the wavefront, all of them active and
+// calling with the same seg), NP pairs (i0+p, i0+p+hd/2) per lane; the sum of
+// squares is reduced across them.  Value segments, and calls without a gain,
+// return unchanged.
+template <int NP>
+__device__ __forceinline__ void k_norm(const KvDest& e, int seg, int i0, int lanes, float* lo,
+                                       float* hi) {
+  if (e.knorm == nullptr || ((seg / e.Hkv) & 1) != 0) return;
+  float ss = 0.f;
+#pragma unroll
+  for (int p = 0; p < NP; ++p) ss = fmaf(lo[p], lo[p], fmaf(hi[p], hi[p], ss));
+  for (int off = lanes >> 1; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+  const float r = rsqrtf(ss / static_cast<float>(e.hd) + kRmsEps);
+  const float* g = e.knorm + (seg / (2 * e.Hkv)) * e.hd;
+  const int half = e.hd / 2;
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    lo[p] = lo[p] * r * g[i0 + p];
+    hi[p] = hi[p] * r * g[i0 + p + half];
+  }
+}
+
 // ------------------------------------------------------------- K/V stores
 
 // Where a row of segment (layer, head g) lives: element offsets of its dim 0

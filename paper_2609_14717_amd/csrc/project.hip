@@ -311,6 +311,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
         lo[p] = sc[row * LDC + seg_local * hd + i0 + p];
         hi[p] = sc[row * LDC + seg_local * hd + hd / 2 + i0 + p];
       }
+      // the hd/8 lanes of a head segment are consecutive and take the same branches
+      k_norm<4>(g.kv, gc0 / hd, i0, q_per_seg, lo, hi);
       kv_store<uint16_t, 4>(g.kv, gr, dst_lds[row], pos_lds[row], gc0 / hd, i0, lo, hi, inv_tab);
     }
   }
@@ -601,6 +603,7 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_kernel(GemmArgs g, int tiles
           lo[pp] = sc[rl * LDC + seg_local * hd + i0 + pp];
           hi[pp] = sc[rl * LDC + seg_local * hd + hd / 2 + i0 + pp];
         }
+        k_norm<4>(g.kv, gc0 / hd, i0, q_per_seg, lo, hi);   // hd/8 consecutive lanes per segment
         kv_store<uint16_t, 4>(g.kv, gr, dst_lds[row], pos_lds[row], gc0 / hd, i0, lo, hi, inv_tab);
       }
     }
@@ -915,7 +918,6 @@ __global__ __launch_bounds__(256, 1) void proj_fused_kernel(ProjectArgs a) {
 // The normalisation variant: every row of Z is divided by its root mean
 // square (epsilon kRmsEps) and multiplied by the gain g, in place, before the
 // K/V product.  One wavefront per row, fp32 arithmetic.
-constexpr float kRmsEps = 1e-6f;
 
 template <typename T>
 __global__ __launch_bounds__(256) void z_norm_kernel(T* z, int M, int d, const float* g) {
@@ -983,6 +985,7 @@ __global__ __launch_bounds__(256) void epi_kv_kernel(const float* part, int spli
     lo += part[static_cast<int64_t>(s) * M * N + c_lo];
     hi += part[static_cast<int64_t>(s) * M * N + c_lo + half];
   }
+  k_norm<1>(e, seg, p, half, &lo, &hi);   // a segment's hd/2 pairs: consecutive, aligned lanes
   kv_store<T, 1>(e, row, e.row_dst[row], e.row_pos[row], seg, p, &lo, &hi, inv_tab);
 }
 
@@ -1228,7 +1231,8 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
     return hipGetLastError();
   }
 
-  if (!sep && a.znorm == nullptr && p.fused && (a.fe != nullptr || a.e == nullptr)) {
+  if (!sep && a.znorm == nullptr && a.dst.knorm == nullptr && p.fused &&
+      (a.fe != nullptr || a.e == nullptr)) {
     hipLaunchKernelGGL(proj_fused_kernel, dim3((a.M + kFusedBM - 1) / kFusedBM), dim3(256), 0,
                        stream, a);
     return hipGetLastError();

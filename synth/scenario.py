@@ -12,22 +12,23 @@ from . import workloads as wl
 from . import device as sdev
 
 
-def make_weights(co, dims, wf, wkv, e, fold_e, wfc=None, znorm=None):
+def make_weights(co, dims, wf, wkv, e, fold_e, wfc=None, znorm=None, knorm=None):
     """co_weights of the drafter; with fold_e (bf16) F(E) is folded once, as a
     serving setup would when it loads the weights; wfc: the separate carry
-    projector (then E is not used); znorm: the RMS-norm gain of F's output."""
+    projector (then E is not used); znorm: the RMS-norm gain of F's output;
+    knorm: the per-head key gain [L][hd]."""
     import torch
     f_e = None
     if fold_e and dims.dtype == co.CO_DTYPE_BF16 and wfc is None:
         f_e = torch.empty(dims.model_dim, dtype=torch.float32, device=wf.device)
         co.carryover_fold_e(dims, co.weights(wf, wkv, e), f_e)
-    return co.weights(wf, wkv, e, f_e, wfc, znorm), f_e
+    return co.weights(wf, wkv, e, f_e, wfc, znorm, knorm), f_e
 
 
 class Scenario:
     def __init__(self, w: wl.Workload, device: str = "cuda", build_context: bool = True,
                  fold_e: bool = True, separate_projector: bool = False,
-                 z_norm: bool = False):
+                 z_norm: bool = False, k_norm: bool = False):
         import torch
         import paper_2609_14717_amd as co
         self.w, self.device = w, device
@@ -44,8 +45,12 @@ class Scenario:
         if z_norm:   # fp32(sigma_z) * (1 + offset), in fp32 as on the host
             off = sdev.materialise(w.replace(dtype="f32"), wl.spec_znorm(w), device)
             self.znorm = torch.tensor(np.float32(w.sigma_z), device=device) * (1.0 + off)
+        self.knorm = None
+        if k_norm:   # fp32(sigma_kv) * (1 + offset), [L][hd]
+            off = sdev.materialise(w.replace(dtype="f32"), wl.spec_knorm(w), device)
+            self.knorm = torch.tensor(np.float32(w.sigma_kv), device=device) * (1.0 + off)
         self.W, self.f_e = make_weights(co, self.dims, self.wf, self.wkv, self.e, fold_e,
-                                        self.wfc, self.znorm)
+                                        self.wfc, self.znorm, self.knorm)
         self.ws = torch.zeros(max(co.workspace_bytes(self.dims, co.CO_WS_ROUND), 256),
                               dtype=torch.uint8, device=device)
         self.ws_project = co.workspace_bytes(self.dims, co.CO_WS_PROJECT)

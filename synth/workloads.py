@@ -31,6 +31,7 @@ ST_WF, ST_WKV, ST_E, ST_H, ST_TGT, ST_DRAFT, ST_M, ST_Q = 1, 2, 3, 4, 5, 6, 7, 8
 ST_CTX0, ST_PAGES, ST_KDIR, ST_VDIR, ST_HCTX, ST_ANCHOR, ST_U = 9, 10, 11, 12, 13, 14, 15
 ST_WFC = 16             # the separate carry projector (a variant next to the path)
 ST_ZNORM, ST_KSELF, ST_VSELF = 17, 18, 19   # RMS-norm gain offsets; block self K/V
+ST_KNORM = 20           # per-head key RMS-norm gain offsets
 
 
 @dataclass(frozen=True)
@@ -212,6 +213,18 @@ def spec_znorm(w):
 def znorm_gain_host(w, offsets):
     """The gain from its offsets, in fp32 as on the device."""
     return np.float32(w.sigma_z) * (np.float32(1.0) + np.asarray(offsets, np.float32))
+
+
+def spec_knorm(w):
+    """Offsets of the per-head key RMS-norm gain, fp32 [L][hd]: the gain is
+    fp32(sigma_kv) * (1 + offset), so that normalised keys keep the statistics
+    of projected keys."""
+    return ST_KNORM, (w.L, w.hd), (w.hd, 1), 0, 0.1
+
+
+def knorm_gain_host(w, offsets):
+    """The key gain from its offsets, in fp32 as on the device."""
+    return np.float32(w.sigma_kv) * (np.float32(1.0) + np.asarray(offsets, np.float32))
 
 
 def spec_self(w, which, rnd, S=None):

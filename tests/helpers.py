@@ -78,13 +78,16 @@ class OracleTrain:
 class OracleRun:
     """The oracle's view of a workload: weights, logical state, rounds."""
 
-    def __init__(self, w, seqs=None, store=np.float64, separate_projector=False, z_norm=False):
+    def __init__(self, w, seqs=None, store=np.float64, separate_projector=False, z_norm=False,
+                 k_norm=False):
         self.w = w
         self.seqs = list(range(w.S)) if seqs is None else list(seqs)
         self.WF = host(w, wl.spec_wf(w))
         self.WFC = host(w, wl.spec_wfc(w)) if separate_projector else None
         self.ZN = (wl.znorm_gain_host(w, host(w, wl.spec_znorm(w), dtype="f32", out=np.float32))
                    .astype(np.float64) if z_norm else None)
+        self.KN = (wl.knorm_gain_host(w, host(w, wl.spec_knorm(w), dtype="f32", out=np.float32))
+                   .astype(np.float64) if k_norm else None)
         self.WKV = host(w, wl.spec_wkv(w))
         self.E = host(w, wl.spec_e(w))
         self.pt = wl.page_table(w)
@@ -105,7 +108,7 @@ class OracleRun:
                 h = host(w, wl.spec_hctx(w, s, 0, n))
                 k, v = oracle.project(h, self.E, np.zeros(n, bool), self.WF, self.WKV,
                                       np.arange(n), w.L, w.Hkv, w.hd, w.theta,
-                                      z_norm=self.ZN)
+                                      z_norm=self.ZN, k_norm=self.KN)
                 self.st.commit_and_replace(s, k, v, k[:0], v[:0])
 
     def ctx_len(self):
@@ -135,7 +138,8 @@ class OracleRun:
                               self.num_pages, mode)
         H = self.seq_block(wl.spec_h(w, r), 0)
         oracle.round_update(self.st, rr, H, self.E, self.WF, self.WKV, w.theta, mode,
-                            seqs=self.seqs, WF_carry=self.WFC, z_norm=self.ZN)
+                            seqs=self.seqs, WF_carry=self.WFC, z_norm=self.ZN,
+                            k_norm=self.KN)
         self._ctx = np.asarray(rr["ctx_len"], np.int32).copy()
         self._carry = np.asarray(rr["carry_len"], np.int32).copy()
         if not attend:

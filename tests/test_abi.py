@@ -208,3 +208,10 @@ def test_z_norm_pointer_alignment_checked():
     assert _rc(lambda: co.carryover_project_kv(_dims(), W, FAKE, _fake_route(), _fake_state(),
                                                FAKE, stream=0, ws_bytes=1 << 30)) \
         == co.CO_ERR_INVALID_ARG
+
+
+def test_k_norm_pointer_alignment_checked():
+    W = co.weights(FAKE, FAKE, FAKE, None, None, None, FAKE + 2)
+    assert _rc(lambda: co.carryover_project_kv(_dims(), W, FAKE, _fake_route(), _fake_state(),
+                                               FAKE, stream=0, ws_bytes=1 << 30)) \
+        == co.CO_ERR_INVALID_ARG

@@ -9,7 +9,8 @@ against the fp64 oracle:
   GEMM paths;
 * the attention mass on the carried rows (Appendix "Attention to carried
   states"), from a finished attention call's LSE;
-* the RMS normalisation of F's output before the K/V product;
+* the RMS normalisation of F's output before the K/V product, and of every key
+  head before its rotation;
 * the block's own rows as a third attention segment, merged into the
   attention over [C;U].
 """
@@ -160,6 +161,48 @@ def _z_norm_small():
     w = wl.RAGGED32.replace(name="var_znorm_fused", S=5, rounds=3, ctx_lo=100, ctx_hi=900,
                             seed=0x5EED26)
     sc, orc = Scenario(w, z_norm=True), OracleRun(w, z_norm=True)
+    for r in range(2):
+        hidden, q, draft, target, m = sc.round_inputs(r)
+        out, lse = sc.new_output()
+        co.carryover_round(sc.dims, sc.W, hidden, draft, target, q, sc.st, sc.rt, out, lse, 0,
+                           sc.ws)
+        torch.cuda.synchronize()
+        assert co.carryover_read_status(sc.st) == 0
+        rr, O, LSE = orc.round(r)
+        compare_round(sc, orc, rr, O, LSE, out, lse, sc.rt, orc.seqs, f"{w.name} r{r}")
+
+
+@pytest.mark.parametrize("w", [EDGE, EDGE_F32, HD128, WIDE, SPLIT], ids=lambda w: w.name)
+def test_k_norm_rounds(w, monkeypatch):
+    """Every key head RMS-normalised (per-layer gain) before its rotation, on
+    the small-tile (hd 64 and 128), large-tile, split-K and fp32 epilogues,
+    also together with the normalisation of F's output."""
+    Scenario, co = _gpu()
+    if w is WIDE:
+        monkeypatch.setenv("CO_GEMM_WIDE_VARIANT", "3")
+    zn = w is SPLIT
+    print(f"[variants] k norm {w.name} (z norm {zn})", flush=True)
+    sc = Scenario(w, k_norm=True, z_norm=zn)
+    orc = OracleRun(w, k_norm=True, z_norm=zn)
+    for r in range(3):
+        hidden, q, draft, target, m = sc.round_inputs(r)
+        out, lse = sc.new_output()
+        co.carryover_round(sc.dims, sc.W, hidden, draft, target, q, sc.st, sc.rt, out, lse, 0,
+                           sc.ws)
+        torch.cuda.synchronize()
+        assert co.carryover_read_status(sc.st) == 0
+        rr, O, LSE = orc.round(r)
+        compare_round(sc, orc, rr, O, LSE, out, lse, sc.rt, orc.seqs, f"{w.name} knorm r{r}")
+
+
+def test_k_norm_fused_path(monkeypatch):
+    """Where the fused projection would run (forced at 80 rows), normalised
+    keys take the two-product path and stay correct."""
+    monkeypatch.setenv("CO_PROJECT_FUSED_MIN_ROWS", "1")
+    Scenario, co = _gpu()
+    w = wl.RAGGED32.replace(name="var_knorm_fused", S=5, rounds=3, ctx_lo=100, ctx_hi=900,
+                            seed=0x5EED27)
+    sc, orc = Scenario(w, k_norm=True), OracleRun(w, k_norm=True)
     for r in range(2):
         hidden, q, draft, target, m = sc.round_inputs(r)
         out, lse = sc.new_output()
