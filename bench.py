@@ -504,8 +504,9 @@ def main():
 def variant_costs(torch, co, sc, w, lib, step, rewind, chain, args, stream, attend, q_last, lse,
                   dt):
     """Costs of the variants next to the path, on the same state:
-    * the separate-projector update and the RMS-normalised update: the timed
-      rounds again from the snapshot, rounds/s;
+    * the separate-projector update and the RMS-normalised updates (F's
+      output; every key head): the timed rounds again from the snapshot,
+      rounds/s;
     * the attention mass on the carried rows (drafter_carry_mass) and the
       block self-segment merge (drafter_self_merge) after the attention call on
       the final state, per call (the merge repeats on the same output buffer:
@@ -530,6 +531,15 @@ def variant_costs(torch, co, sc, w, lib, step, rewind, chain, args, stream, atte
     sc.W.z_norm = None
     if co.carryover_read_status(sc.st):
         raise RuntimeError("device status after the normalised rounds")
+    # per-head key normalisation in the K/V epilogue: the timed rounds again
+    koff = sdev.materialise(w.replace(dtype="f32"), wl.spec_knorm(w), "cuda")
+    kgain = torch.tensor(np.float32(w.sigma_kv), device="cuda") * (1.0 + koff)
+    sc.W.k_norm = kgain.data_ptr()
+    rewind()
+    dt_knorm = chain(0)
+    sc.W.k_norm = None
+    if co.carryover_read_status(sc.st):
+        raise RuntimeError("device status after the key-normalised rounds")
     # the chain ends with carry segments again: the mass of the last attention,
     # and the block's own rows merged in as a third segment
     n = min(args.steps, 100)
@@ -545,7 +555,8 @@ def variant_costs(torch, co, sc, w, lib, step, rewind, chain, args, stream, atte
             "self_merge_call_us": self_s * 1e6,
             "separate_projector": {"rounds_per_s": args.steps / dt_sep,
                                    "vs_embedding": dt / dt_sep},
-            "z_norm": {"rounds_per_s": args.steps / dt_norm, "vs_plain": dt / dt_norm}}
+            "z_norm": {"rounds_per_s": args.steps / dt_norm, "vs_plain": dt / dt_norm},
+            "k_norm": {"rounds_per_s": args.steps / dt_knorm, "vs_plain": dt / dt_knorm}}
 
 
 class Scrub:
