@@ -28,7 +28,10 @@ rows go through a second fusion matrix instead of F + E (Section 4, Table
 "Attention to carried states"); the block's own rows as a third attention
 segment [C ; U ; S]; and RMS normalisations of F's output before the K/V
 projections and of every head's key before its rotation (the paper's
-equations omit normalisation, Section 2.1).
+equations omit normalisation, Section 2.1); and the reverse mode of the
+attention and of the projection, the training side of the second drafter pass
+(Algorithm 2: gradients of W_F, W_KV, E_carry and of the queries, with the
+target's states held constant).
 
 Readings where the paper is silent (each one a stated choice of this oracle): no norm
 and no bias in F, K_l, V_l; rotate-half RoPE with inverse frequency
@@ -196,6 +199,32 @@ def project(H, E, add_e, WF, WKV, pos, L, Hkv, hd, theta, WF_carry=None, z_norm=
     return k, kv[:, :, 1].copy()
 
 
+def project_backward(H, E, add_e, WF, WKV, pos, L, Hkv, hd, theta, dK, dV):
+    """Reverse mode of ``project`` (the plain update: F with E on flagged rows,
+    no separate projector, no normalisation) for the trained parameters W_F,
+    W_KV and E_carry (Algorithm 2: the target's states H are constants).
+    dK [M][L][Hkv][hd] is the gradient with respect to the rotated keys, dV
+    with respect to the values.  The keys' gradient is rotated back at each
+    row's position, the rows' K/V gradients form dJ [M][NKV] in W_KV's row
+    order, and with x = H + flag E, z = F x: dW_KV = dJ^T z, dz = dJ W_KV,
+    dW_F = dz^T x, dE = sum over flagged rows of F^T dz.
+    Returns (dWF [d][Dcat], dWKV [NKV][d], dE [Dcat])."""
+    H = np.asarray(H, np.float64)
+    flag = np.asarray(add_e, bool)
+    M = len(H)
+    x = H + flag[:, None].astype(np.float64) * np.asarray(E, np.float64)[None, :]
+    WF = np.asarray(WF, np.float64)
+    WKV = np.asarray(WKV, np.float64)
+    z = x @ WF.T
+    dk = rope(np.asarray(dK, np.float64), -np.asarray(pos, np.float64)[:, None, None], theta)
+    dJ = np.stack([dk, np.asarray(dV, np.float64)], axis=2).reshape(M, -1)
+    dWKV = dJ.T @ z
+    dz = dJ @ WKV
+    dWF = dz.T @ x
+    dE = (dz[flag] @ WF).sum(axis=0) if flag.any() else np.zeros(WF.shape[1])
+    return dWF, dWKV, dE
+
+
 # ---------------------------------------------------------------- attention
 
 def attend(q, qpos, k, v, theta):
@@ -211,6 +240,34 @@ def attend(q, qpos, k, v, theta):
     w = np.exp(s - mx)
     den = w.sum(axis=1, keepdims=True)
     return (w @ np.asarray(v, np.float64)) / den, (mx + np.log(den))[:, 0]
+
+
+def attend_backward(q, qpos, k, v, dO, theta):
+    """Reverse mode of ``attend`` (the training side of the block attention,
+    Algorithm 2: gradients of the second pass): given dO [nq][hd], the
+    gradients of sum(dO * O) with respect to the unrotated queries q, the
+    rotated keys k and the values v.  With P the softmax weights and
+    D_i = sum_j P_ij (dO_i . v_j): dv = P^T dO; dS = P * (dO v^T - D); the
+    rotated query's gradient dS k / sqrt(hd) is rotated back (the transpose of
+    a rotation turns by the opposite angle); dk = dS^T (R q) / sqrt(hd).
+    Returns (dq [nq][hd], dk [nk][hd], dv [nk][hd]); no keys: all zero."""
+    q = np.asarray(q, np.float64)
+    dO = np.asarray(dO, np.float64)
+    nq, hd = q.shape
+    k = np.asarray(k, np.float64).reshape(-1, hd)
+    v = np.asarray(v, np.float64).reshape(-1, hd)
+    if len(k) == 0:
+        return np.zeros((nq, hd)), np.zeros((0, hd)), np.zeros((0, hd))
+    qr = rope(q, np.asarray(qpos), theta)
+    s = (qr @ k.T) / math.sqrt(hd)
+    p = np.exp(s - s.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    dv = p.T @ dO
+    dp = dO @ v.T
+    ds = p * (dp - (p * dp).sum(axis=1, keepdims=True))
+    dqr = (ds @ k) / math.sqrt(hd)
+    dk = (ds.T @ qr) / math.sqrt(hd)
+    return rope(dqr, -np.asarray(qpos, np.float64), theta), dk, dv
 
 
 def carry_mass(q, qpos, k_committed, k_carry, theta):

@@ -644,3 +644,83 @@ def test_k_norm_gain_applies_before_the_rotation():
     k0, _ = oracle.project(H, E, flag, WF, WKV, np.zeros(5), L, Hkv, hd, 1e4)
     r = np.sqrt(np.mean(k0 * k0, axis=-1, keepdims=True) + oracle.RMS_EPS)
     np.testing.assert_allclose(k1, k0 / r * g[None, :, None, :], rtol=1e-12, atol=1e-12)
+
+
+# ------------------------------------------- backward of the second pass (Algorithm 2)
+
+def _attn_case(nq=3, nk=5, hd=8):
+    q = RNG.standard_normal((nq, hd))
+    k = RNG.standard_normal((nk, hd))
+    v = RNG.standard_normal((nk, hd))
+    dO = RNG.standard_normal((nq, hd))
+    qpos = np.array([7, 7, 9])[:nq]
+    return q, qpos, k, v, dO
+
+
+def _fd(f, x, h=1e-6):
+    """Central finite differences of the scalar f at every element of x."""
+    g = np.zeros_like(x)
+    for idx in np.ndindex(x.shape):
+        x0 = x[idx]
+        x[idx] = x0 + h
+        fp = f()
+        x[idx] = x0 - h
+        fm = f()
+        x[idx] = x0
+        g[idx] = (fp - fm) / (2 * h)
+    return g
+
+
+def test_attend_backward_matches_finite_differences():
+    """Every element of dq, dk, dv against central differences of the forward
+    oracle's sum(dO * O): a dropped term, a sign, a missing rotation or a
+    transposed product fails it."""
+    q, qpos, k, v, dO = _attn_case()
+    theta = 100.0
+    dq, dk, dv = oracle.attend_backward(q, qpos, k, v, dO, theta)
+    loss = lambda: float(np.sum(dO * oracle.attend(q, qpos, k, v, theta)[0]))
+    np.testing.assert_allclose(dq, _fd(loss, q), rtol=1e-6, atol=1e-8)
+    np.testing.assert_allclose(dk, _fd(loss, k), rtol=1e-6, atol=1e-8)
+    np.testing.assert_allclose(dv, _fd(loss, v), rtol=1e-6, atol=1e-8)
+
+
+def test_attend_backward_invariants():
+    """Shifting every key by one vector leaves the softmax unchanged, so the
+    keys' gradients sum to zero; the weights of a query sum to one, so the
+    values' gradients sum to the sum of dO; no keys: zero gradients."""
+    q, qpos, k, v, dO = _attn_case(nq=3, nk=7, hd=16)
+    dq, dk, dv = oracle.attend_backward(q, qpos, k, v, dO, 1e4)
+    np.testing.assert_allclose(dk.sum(axis=0), 0.0, atol=1e-12)
+    np.testing.assert_allclose(dv.sum(axis=0), dO.sum(axis=0), rtol=1e-12, atol=1e-12)
+    dq0, dk0, dv0 = oracle.attend_backward(q, qpos, k[:0], v[:0], dO, 1e4)
+    assert not dq0.any() and dk0.shape == (0, 16) and dv0.shape == (0, 16)
+
+
+def test_project_backward_matches_finite_differences():
+    """Directional derivatives of sum(dK * K + dV * V) of the forward oracle
+    along random directions of W_F, W_KV and E equal the inner products with
+    the returned gradients."""
+    L, Hkv, hd, H, E, WF, WKV, pos, flag = _proj_case()
+    dK = RNG.standard_normal((5, L, Hkv, hd))
+    dV = RNG.standard_normal((5, L, Hkv, hd))
+    theta = 1e4
+    dWF, dWKV, dE = oracle.project_backward(H, E, flag, WF, WKV, pos, L, Hkv, hd, theta, dK, dV)
+
+    def loss(wf, wkv, e):
+        k, v = oracle.project(H, e, flag, wf, wkv, pos, L, Hkv, hd, theta)
+        return float(np.sum(dK * k) + np.sum(dV * v))
+
+    h = 1e-6
+    for name, grad in (("WF", dWF), ("WKV", dWKV), ("E", dE)):
+        U = RNG.standard_normal(grad.shape)
+        args_p = dict(wf=WF, wkv=WKV, e=E)
+        args_m = dict(wf=WF, wkv=WKV, e=E)
+        key = {"WF": "wf", "WKV": "wkv", "E": "e"}[name]
+        args_p[key] = args_p[key] + h * U
+        args_m[key] = args_m[key] - h * U
+        fd = (loss(**args_p) - loss(**args_m)) / (2 * h)
+        assert abs(fd - np.sum(grad * U)) <= 1e-6 * max(1.0, abs(fd)), name
+    # rows without the embedding contribute nothing to dE
+    _, _, dE0 = oracle.project_backward(H, E, np.zeros(5, bool), WF, WKV, pos, L, Hkv, hd,
+                                        theta, dK, dV)
+    assert not dE0.any()
