@@ -73,8 +73,10 @@ enum {
   CO_ERR_CAPACITY = 4,      /* device: ctx_len + block > max_pages_per_seq * 16 */
   CO_ERR_PAGE_RANGE = 5,    /* device: page id outside [0, num_pages)          */
   CO_ERR_HIP = 6,           /* a HIP runtime call or launch failed             */
-  CO_ERR_LENGTH = 7         /* device: ctx_len outside [0, max_pages_per_seq * 16] or
+  CO_ERR_LENGTH = 7,        /* device: ctx_len outside [0, max_pages_per_seq * 16] or
                                carry_len outside [0, 16 * ceil(block / 16)]        */
+  CO_ERR_GROUP = 8          /* device: a sequence's committed page ids differ from its
+                               group's first sequence (attention backward)          */
 };
 
 enum { CO_DTYPE_F32 = 0, CO_DTYPE_BF16 = 1 };
@@ -230,6 +232,38 @@ co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int3
  * CO_WS_ROUND) bytes of scratch.
  */
 /*
+ * Reverse mode of drafter_block_attention: the training side of the second
+ * drafter pass (Algorithm 2, whose loss is differentiated through the second
+ * draft's attention over ctx = [C;U], Eq. 2).  For the layers, q, state and
+ * CO_Q_PREROTATED flag of a forward call whose output was `out` and whose LSE
+ * (natural log, required) was `lse`, and the gradient d_out of a loss with
+ * respect to out (q's layout, bf16):
+ *   d_q [layer_count][num_seqs][block][num_q_heads][head_dim] fp32: the
+ *     gradient with respect to q (un-rotated queries unless CO_Q_PREROTATED);
+ *   d_k_cache, d_v_cache: fp32 arrays shaped like k_cache and v_cache; the
+ *     entries of every committed key some block query sees are overwritten
+ *     with the gradient with respect to the stored (rotated) key and the value,
+ *     summed over every query that sees it; other entries are left unchanged;
+ *   d_k_carry, d_v_carry: the same for the carry segment (shaped like k_carry,
+ *     v_carry).
+ * seqs_per_group: consecutive sequences g * n .. g * n + n - 1 read the same
+ * committed page row (the blocks of one recorded response in training; they
+ * may differ in ctx_len), and no page appears in two groups' rows; 1 when
+ * sequences share no pages.  A sequence whose page ids differ from its group's
+ * first sequence sets CO_ERR_GROUP.
+ * Supported: bf16, head_dim 64, block * (num_q_heads / num_kv_heads) <= 32.
+ * All pointers 16-byte aligned; `ws`: carryover_workspace_bytes(dims,
+ * CO_WS_ATTENTION_BACKWARD) bytes of scratch, 256-byte aligned.  Device
+ * errors: CO_ERR_LENGTH, CO_ERR_PAGE_RANGE (keys of a rejected page id get no
+ * gradient), CO_ERR_GROUP.  Results are deterministic (no atomics).
+ */
+co_status drafter_block_attention_backward(
+    const co_dims* dims, int32_t layer_begin, int32_t layer_count, const void* q,
+    const co_state* state, const void* out, const float* lse, const void* d_out,
+    int32_t seqs_per_group, float* d_q, float* d_k_cache, float* d_v_cache, float* d_k_carry,
+    float* d_v_carry, uint32_t flags, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * Attention mass on the carried rows (the diagnostic of Appendix "Attention to
  * carried states"; for the carry segment U of ctx = [C;U], Eq. 2).  For every
  * (layer, sequence, block row i, query head h) of a drafter_block_attention
@@ -284,7 +318,7 @@ co_status carryover_import_kv(const co_dims* dims, int32_t seq, int32_t pos0, in
                               const void* k_rows, const void* v_rows, const co_state* state,
                               hipStream_t stream);
 
-enum { CO_WS_PROJECT = 0, CO_WS_ATTENTION = 1, CO_WS_ROUND = 2 };
+enum { CO_WS_PROJECT = 0, CO_WS_ATTENTION = 1, CO_WS_ROUND = 2, CO_WS_ATTENTION_BACKWARD = 3 };
 
 /* Workspace bytes a call needs for these dims (0 on unsupported dims). */
 size_t carryover_workspace_bytes(const co_dims* dims, int32_t which);

@@ -16,12 +16,12 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libcarryover.so")
 
 CO_OK, CO_ERR_INVALID_ARG, CO_ERR_UNSUPPORTED, CO_ERR_WORKSPACE = 0, 1, 2, 3
-CO_ERR_CAPACITY, CO_ERR_PAGE_RANGE, CO_ERR_HIP, CO_ERR_LENGTH = 4, 5, 6, 7
+CO_ERR_CAPACITY, CO_ERR_PAGE_RANGE, CO_ERR_HIP, CO_ERR_LENGTH, CO_ERR_GROUP = 4, 5, 6, 7, 8
 CO_DTYPE_F32, CO_DTYPE_BF16 = 0, 1
 CO_BASELINE_MODE, CO_ROUTE_ACCEPT_ALL, CO_ROUTE_CARRY_ONLY, CO_Q_PREROTATED = 1, 2, 4, 8
 CO_ATTN_SHARED_PREFIX = 16
 CO_ROUTE_ACCEPT_BITS = 32
-CO_WS_PROJECT, CO_WS_ATTENTION, CO_WS_ROUND = 0, 1, 2
+CO_WS_PROJECT, CO_WS_ATTENTION, CO_WS_ROUND, CO_WS_ATTENTION_BACKWARD = 0, 1, 2, 3
 SKIP = -(2 ** 31)
 PAGE = 16
 
@@ -84,6 +84,10 @@ def lib():
             "carryover_round": [_P(co_dims), _P(co_weights), _v, _v, _v, _v, _P(co_state),
                                 _P(co_route), _v, _v, ctypes.c_uint32, _v, ctypes.c_size_t, _v],
             "carryover_fold_e": [_P(co_dims), _P(co_weights), _v, _v],
+            "drafter_block_attention_backward": [_P(co_dims), ctypes.c_int32, ctypes.c_int32,
+                                                 _v, _P(co_state), _v, _v, _v, ctypes.c_int32,
+                                                 _v, _v, _v, _v, _v, ctypes.c_uint32, _v,
+                                                 ctypes.c_size_t, _v],
             "drafter_carry_mass": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, _v, _P(co_state),
                                    _v, _v, ctypes.c_uint32, _v],
             "drafter_self_merge": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, _v, _v, _v,
@@ -106,7 +110,7 @@ def lib():
 
 EXPORTED = ("carryover_route", "carryover_project_kv", "drafter_block_attention",
             "carryover_round", "carryover_fold_e", "drafter_carry_mass", "drafter_self_merge",
-            "carryover_import_kv",
+            "drafter_block_attention_backward", "carryover_import_kv",
             "carryover_workspace_bytes", "carryover_read_status", "carryover_status_string")
 
 
@@ -217,6 +221,18 @@ def drafter_block_attention(dims, layer_begin, layer_count, q, st, out, lse, fla
     _check(lib().drafter_block_attention(ctypes.byref(dims), layer_begin, layer_count, _ptr(q),
                                          ctypes.byref(s), _ptr(out), _ptr(lse), flags, _ptr(ws),
                                          nb, _stream(stream)), "drafter_block_attention")
+
+
+def drafter_block_attention_backward(dims, layer_begin, layer_count, q, st, out, lse, d_out,
+                                     seqs_per_group, d_q, d_k_cache, d_v_cache, d_k_carry,
+                                     d_v_carry, ws, flags=0, stream=None, ws_bytes=None):
+    s = state(st)
+    nb = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    _check(lib().drafter_block_attention_backward(
+        ctypes.byref(dims), layer_begin, layer_count, _ptr(q), ctypes.byref(s), _ptr(out),
+        _ptr(lse), _ptr(d_out), seqs_per_group, _ptr(d_q), _ptr(d_k_cache), _ptr(d_v_cache),
+        _ptr(d_k_carry), _ptr(d_v_carry), flags, _ptr(ws), nb, _stream(stream)),
+        "drafter_block_attention_backward")
 
 
 def drafter_carry_mass(dims, layer_begin, layer_count, q, st, lse, mass, flags=0, stream=None):

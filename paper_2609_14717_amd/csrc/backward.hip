@@ -1,0 +1,589 @@
+// Reverse mode of the block attention over ctx = [C ; U]: the training side of
+// the second drafter pass (Algorithm 2 -- the loss of the second draft is
+// differentiated through its attention and the K/V projection, with the
+// target's states held constant; Eq. 2 gives the attended context).
+//
+// With S = (R q) k^T / sqrt(hd) per (layer, sequence, KV head), P the softmax
+// weights, dO the output gradient and D_i = dO_i . O_i (= sum_j P_ij dO_i.v_j):
+//   dV = P^T dO,   dS = P * (dO V^T - D),   dK = dS^T (R q) / sqrt(hd),
+//   dq = R^T (dS K) / sqrt(hd).
+// Committed keys may be shared by the blocks of one recorded response (the
+// training layout: consecutive sequences of a group read the same page row),
+// so their gradients are sums over the group's blocks.
+//
+// Four kernels, all on v_mfma_f32_32x32x16_bf16 (bf16 operands, fp32 sums):
+//   prep   per (layer, KV head, sequence): the rotated, scaled queries (log2
+//          units, as the forward forms them) and their transpose, dO packed
+//          and transposed, the forward's LSE in log2 units and D;
+//   copy   every K page transposed ([hd][16]) and every V page in key-major
+//          order ([16][hd]), so that all MFMA operands are 16-byte loads with
+//          the contracted index contiguous;
+//   dkv    one wavefront per (layer, KV head, group, 32-key tile of committed
+//          keys): the tile's K and V stay in registers while the group's blocks
+//          stream by; S = Q K^T is formed with its query rows permuted (bits 2
+//          and 3 swapped) so that P and dS come out of the accumulators already
+//          in the operand layout of dV^T = dO^T P and dK^T = (R q)^T dS;
+//   dq     one wavefront per (layer, KV head, sequence): S^T = K Q^T over all of
+//          the sequence's tiles (keys permuted the same way), dQ^T += K^T dS^T,
+//          then the rotation is undone; its carry tile also runs the dkv step,
+//          since carry keys belong to one sequence.
+// Keys masked in the forward (past ctx_len or carry_len, rejected page ids)
+// get no gradient and contribute none.
+#include "co_kernels.h"
+
+namespace co {
+
+namespace {
+
+constexpr float kLog2eB = 1.4426950408889634f;
+constexpr float kLn2B = 0.6931471805599453f;
+constexpr int kNqp = 32;   // query rows per (sequence, KV head): one 32-row MFMA tile
+
+// query (or key) index held by A-row / C-row rho when rows are permuted by
+// swapping bits 2 and 3: then accumulator register r of lane l belongs to index
+// 8 * (l / 32) + r for r < 8 and 16 + 8 * (l / 32) + r - 8 for r >= 8
+__device__ __forceinline__ int perm23(int rho) {
+  return (rho & ~12) | ((rho & 4) << 1) | ((rho & 8) >> 1);
+}
+
+// index of accumulator register r (permuted rows) for half h = lane / 32
+__device__ __forceinline__ int acc_index(int r, int h) { return (r < 8 ? 0 : 16) + 8 * h + (r & 7); }
+
+// Workspace pieces (bytes are 256-aligned by the host plan).
+struct BwdWs {
+  uint16_t *qr, *qrt, *don, *dot;   // [seg][S][32][hd] / [seg][S][hd][32]
+  float *lse2, *dd;                 // [seg][S][32]
+  uint16_t *kt, *vn;                // committed pages: [lc][num_pages][Hkv][hd][16] / [16][hd]
+  uint16_t *ktc, *vnc;              // carry pages:     [lc][S][CP][Hkv][hd][16] / [16][hd]
+};
+
+__device__ __forceinline__ BwdWs bwd_ws(const BwdArgs& b) {
+  const AttnArgs& a = b.a;
+  const int64_t nseg = static_cast<int64_t>(b.layer_count) * a.Hkv;
+  const int64_t qsz = nseg * a.S * kNqp * a.hd;
+  const int64_t vsz = nseg * a.S * kNqp;
+  const int64_t cpg = static_cast<int64_t>(b.layer_count) * a.num_pages * a.Hkv * kPage * a.hd;
+  const int64_t cpc = static_cast<int64_t>(b.layer_count) * a.S * a.CP * a.Hkv * kPage * a.hd;
+  auto up = [](int64_t bytes) { return (bytes + 255) / 256 * 256; };
+  char* p = static_cast<char*>(static_cast<void*>(a.ws));
+  BwdWs w;
+  w.qr = reinterpret_cast<uint16_t*>(p); p += up(qsz * 2);
+  w.qrt = reinterpret_cast<uint16_t*>(p); p += up(qsz * 2);
+  w.don = reinterpret_cast<uint16_t*>(p); p += up(qsz * 2);
+  w.dot = reinterpret_cast<uint16_t*>(p); p += up(qsz * 2);
+  w.lse2 = reinterpret_cast<float*>(p); p += up(vsz * 4);
+  w.dd = reinterpret_cast<float*>(p); p += up(vsz * 4);
+  w.kt = reinterpret_cast<uint16_t*>(p); p += up(cpg * 2);
+  w.vn = reinterpret_cast<uint16_t*>(p); p += up(cpg * 2);
+  w.ktc = reinterpret_cast<uint16_t*>(p); p += up(cpc * 2);
+  w.vnc = reinterpret_cast<uint16_t*>(p);
+  return w;
+}
+
+__device__ __forceinline__ int64_t out_row_b(const AttnArgs& a, int layer_local, int s, int g,
+                                             int n, int G) {
+  const int i = n / G, hh = n % G;
+  return ((static_cast<int64_t>(layer_local) * a.S + s) * a.B + i) * a.Hq + g * G + hh;
+}
+
+// ------------------------------------------------------------------ prep
+//
+// grid (S, layer_count * Hkv), 256 threads: thread t takes query row t / 8 and
+// the four rotation pairs (4p + e, 4p + e + hd/2), e < 4, p = t % 8 (hd 64).
+template <int HD>
+__global__ __launch_bounds__(256) void bwd_prep_kernel(BwdArgs b) {
+  static_assert(HD == 64, "pairs per thread");
+  const AttnArgs& a = b.a;
+  const BwdWs w = bwd_ws(b);
+  const int s = blockIdx.x, seg = blockIdx.y;
+  const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
+  const int G = a.Hq / a.Hkv, nq = a.B * G;
+  const int t = threadIdx.x, qn = t >> 3, p = t & 7;
+  const int64_t base = (static_cast<int64_t>(seg) * a.S + s) * kNqp;
+  const int ctx = a.ctx_len[s];
+  const bool live = qn < nq;
+  const int64_t row = live ? out_row_b(a, layer_local, s, g, qn, G) * HD : 0;
+  const uint16_t* Q = static_cast<const uint16_t*>(a.q);
+  const uint16_t* O = static_cast<const uint16_t*>(b.out);
+  const uint16_t* dO = static_cast<const uint16_t*>(b.d_out);
+  const bool rotate = !(a.flags & CO_Q_PREROTATED);
+  const float qscale = rsqrtf(static_cast<float>(HD)) * kLog2eB;
+  float dsum = 0.f;
+  u16x4 qlo, qhi, dlo, dhi;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int i = 4 * p + e;
+    float x = 0.f, y = 0.f, dx = 0.f, dy = 0.f;
+    if (live) {
+      x = bf2f(Q[row + i]);
+      y = bf2f(Q[row + i + HD / 2]);
+      dx = bf2f(dO[row + i]);
+      dy = bf2f(dO[row + i + HD / 2]);
+      dsum = fmaf(dx, bf2f(O[row + i]), fmaf(dy, bf2f(O[row + i + HD / 2]), dsum));
+      if (rotate) {
+        float c, sn;
+        rope_cos_sin_rev(ctx + qn / G, a.rope_inv[i] * kInv2Pi, &c, &sn);
+        const float x2 = x * c - y * sn, y2 = y * c + x * sn;
+        x = x2;
+        y = y2;
+      }
+    }
+    qlo[e] = f2bf(x * qscale);
+    qhi[e] = f2bf(y * qscale);
+    dlo[e] = f2bf(dx);
+    dhi[e] = f2bf(dy);
+  }
+  const int64_t qo = (base + qn) * HD;
+  *reinterpret_cast<u16x4*>(w.qr + qo + 4 * p) = qlo;
+  *reinterpret_cast<u16x4*>(w.qr + qo + 4 * p + HD / 2) = qhi;
+  *reinterpret_cast<u16x4*>(w.don + qo + 4 * p) = dlo;
+  *reinterpret_cast<u16x4*>(w.don + qo + 4 * p + HD / 2) = dhi;
+  const int64_t to = base * HD;   // [hd][32] of this (seg, s)
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int i = 4 * p + e;
+    w.qrt[to + i * kNqp + qn] = qlo[e];
+    w.qrt[to + (i + HD / 2) * kNqp + qn] = qhi[e];
+    w.dot[to + i * kNqp + qn] = dlo[e];
+    w.dot[to + (i + HD / 2) * kNqp + qn] = dhi[e];
+  }
+  dsum += __shfl_xor(dsum, 1);
+  dsum += __shfl_xor(dsum, 2);
+  dsum += __shfl_xor(dsum, 4);
+  if (p == 0) {
+    float l2 = INFINITY;   // padding rows: no weight anywhere
+    if (live) {
+      const float l = b.lse[out_row_b(a, layer_local, s, g, qn, G)];
+      l2 = l * kLog2eB;    // -inf (no keys) stays -inf: such rows see no key either
+    }
+    w.lse2[base + qn] = l2;
+    w.dd[base + qn] = live ? dsum : 0.f;
+  }
+}
+
+// ------------------------------------------------------------------ copy
+//
+// Every K page of the launch's layers transposed to [hd][16] and every V page
+// turned to [16][hd]; committed pages first, then carry pages.  One thread per
+// 8 elements of a destination page.
+template <int HD>
+__global__ __launch_bounds__(256) void bwd_copy_kernel(BwdArgs b) {
+  const AttnArgs& a = b.a;
+  const BwdWs w = bwd_ws(b);
+  constexpr int PE = kPage * HD;   // elements per page
+  const int64_t n_com = static_cast<int64_t>(b.layer_count) * a.num_pages * a.Hkv;
+  const int64_t n_car = static_cast<int64_t>(b.layer_count) * a.S * a.CP * a.Hkv;
+  const int64_t item = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t pg = item / (PE / 8);
+  const int c = static_cast<int>(item % (PE / 8)) * 8;
+  if (pg >= n_com + n_car) return;
+  const uint16_t *ks, *vs;
+  uint16_t *kd, *vd;
+  if (pg < n_com) {
+    const int64_t lp = pg / (static_cast<int64_t>(a.num_pages) * a.Hkv);   // local layer
+    const int64_t src = ((a.layer_begin + lp) * a.num_pages * a.Hkv + pg % (a.num_pages * a.Hkv)) * PE;
+    ks = static_cast<const uint16_t*>(a.k_cache) + src;
+    vs = static_cast<const uint16_t*>(a.v_cache) + src;
+    kd = w.kt + pg * PE;
+    vd = w.vn + pg * PE;
+  } else {
+    const int64_t pc = pg - n_com;
+    const int64_t per = static_cast<int64_t>(a.S) * a.CP * a.Hkv;
+    const int64_t src = ((a.layer_begin + pc / per) * per + pc % per) * PE;
+    ks = static_cast<const uint16_t*>(a.k_carry) + src;
+    vs = static_cast<const uint16_t*>(a.v_carry) + src;
+    kd = w.ktc + pc * PE;
+    vd = w.vnc + pc * PE;
+  }
+  // destination element c .. c+7: KT [dim][slot] = K [slot][dim]; VN [slot][dim] = V [dim][slot]
+  u16x8 kv, vv;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int dim = (c + e) / kPage, slot = (c + e) % kPage;
+    kv[e] = ks[slot * HD + dim];
+    const int s2 = (c + e) / HD, d2 = (c + e) % HD;
+    vv[e] = vs[d2 * kPage + s2];
+  }
+  *reinterpret_cast<u16x8*>(kd + c) = kv;
+  *reinterpret_cast<u16x8*>(vd + c) = vv;
+}
+
+// ---------------------------------------------------- key-tile gradients
+//
+// One 32-key tile (two pages) against the 32 query rows of one sequence, keys
+// in natural order as MFMA columns, query rows permuted.  kb/vb: the tile's
+// K / V B-fragments (lane: key l % 32, dims 8 (l / 32) + 16 ks ..); valid
+// keys: n0 in page 0, n1 in page 1.  Adds dV^T and (unscaled) dK^T.
+template <int HD>
+struct KeyGrad {
+  static constexpr int KS = HD / 16;   // k-steps over head dims
+  static constexpr int MT = HD / 32;   // 32-row tiles of head dims
+  f32x16 dkt[MT], dvt[MT];
+
+  __device__ void zero() {
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dkt[m][r] = dvt[m][r] = 0.f;
+  }
+
+  __device__ void step(const BwdWs& w, int64_t qbase, const u16x8 (&kb)[KS], const u16x8 (&vb)[KS],
+                       int n0, int n1, int lane) {
+    const int r32 = lane & 31, h = lane >> 5;
+    const int qp = perm23(r32);
+    const uint16_t* qr = w.qr + (qbase + qp) * HD + 8 * h;
+    const uint16_t* dn = w.don + (qbase + qp) * HD + 8 * h;
+    u16x8 qa[KS], da[KS];
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+      qa[k] = *reinterpret_cast<const u16x8*>(qr + 16 * k);
+      da[k] = *reinterpret_cast<const u16x8*>(dn + 16 * k);
+    }
+    // transposed operands: lane dim = 32 m + l % 32, rows 16 j + 8 h ..
+    u16x8 qt[MT][2], dt[MT][2];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int64_t off = qbase * HD + static_cast<int64_t>(32 * m + r32) * kNqp + 16 * j + 8 * h;
+        qt[m][j] = *reinterpret_cast<const u16x8*>(w.qrt + off);
+        dt[m][j] = *reinterpret_cast<const u16x8*>(w.dot + off);
+      }
+    float l2[16], dd[16];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const f32x4 a0 = *reinterpret_cast<const f32x4*>(w.lse2 + qbase + 16 * j + 8 * h);
+      const f32x4 a1 = *reinterpret_cast<const f32x4*>(w.lse2 + qbase + 16 * j + 8 * h + 4);
+      const f32x4 b0 = *reinterpret_cast<const f32x4*>(w.dd + qbase + 16 * j + 8 * h);
+      const f32x4 b1 = *reinterpret_cast<const f32x4*>(w.dd + qbase + 16 * j + 8 * h + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        l2[8 * j + e] = a0[e];
+        l2[8 * j + 4 + e] = a1[e];
+        dd[8 * j + e] = b0[e];
+        dd[8 * j + 4 + e] = b1[e];
+      }
+    }
+    f32x16 sc, dp;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.f;
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+      sc = mfma32x32x16(qa[k], kb[k], sc);
+      dp = mfma32x32x16(da[k], vb[k], dp);
+    }
+    const int key = r32;   // this lane's column
+    const bool valid = key < 16 ? key < n0 : key - 16 < n1;
+    u16x8 pb[2], sb[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      float pv[8], sv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int r = 8 * j + e;
+        const float pr = valid ? __builtin_amdgcn_exp2f(sc[r] - l2[r]) : 0.f;
+        pv[e] = pr;
+        sv[e] = pr * (dp[r] - dd[r]);
+      }
+      typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+      const u32x4v p4 = {cvt_pk_bf16(pv[0], pv[1]), cvt_pk_bf16(pv[2], pv[3]),
+                         cvt_pk_bf16(pv[4], pv[5]), cvt_pk_bf16(pv[6], pv[7])};
+      const u32x4v s4 = {cvt_pk_bf16(sv[0], sv[1]), cvt_pk_bf16(sv[2], sv[3]),
+                         cvt_pk_bf16(sv[4], sv[5]), cvt_pk_bf16(sv[6], sv[7])};
+      pb[j] = __builtin_bit_cast(u16x8, p4);
+      sb[j] = __builtin_bit_cast(u16x8, s4);
+    }
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        dvt[m] = mfma32x32x16(dt[m][j], pb[j], dvt[m]);
+        dkt[m] = mfma32x32x16(qt[m][j], sb[j], dkt[m]);
+      }
+  }
+
+  // dK (x ln 2: the queries were in log2 units) and dV of the tile's valid keys
+  // into fp32 pages laid out like the caches: K [16][hd], V [hd][16].
+  __device__ void store(float* dk0, float* dk1, float* dv0, float* dv1, int n0, int n1,
+                        int lane) const {
+    const int key = lane & 31, h = lane >> 5;
+    const bool p1 = key >= 16;
+    const int slot = key & 15;
+    if (slot >= (p1 ? n1 : n0)) return;
+    float* dk = (p1 ? dk1 : dk0) + slot * HD;
+    float* dv = (p1 ? dv1 : dv0) + slot;
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int dim = 32 * m + 8 * (r >> 2) + 4 * h + (r & 3);
+        dk[dim] = dkt[m][r] * kLn2B;
+        dv[dim * kPage] = dvt[m][r];
+      }
+  }
+};
+
+// K / V B-fragments of a tile: lane key l % 32 (page l / 16 of the pair), dims
+// 8 (l / 32) + 16 k; K from the cache layout [16][hd], V from the key-major copy.
+template <int HD>
+__device__ __forceinline__ void tile_frags(const uint16_t* k0, const uint16_t* k1,
+                                           const uint16_t* v0, const uint16_t* v1, int lane,
+                                           u16x8 (&kb)[HD / 16], u16x8 (&vb)[HD / 16]) {
+  const int key = lane & 31, h = lane >> 5;
+  const uint16_t* kr = (key < 16 ? k0 : k1) + (key & 15) * HD + 8 * h;
+  const uint16_t* vr = (key < 16 ? v0 : v1) + (key & 15) * HD + 8 * h;
+#pragma unroll
+  for (int k = 0; k < HD / 16; ++k) {
+    kb[k] = *reinterpret_cast<const u16x8*>(kr + 16 * k);
+    vb[k] = *reinterpret_cast<const u16x8*>(vr + 16 * k);
+  }
+}
+
+__device__ __forceinline__ bool len_ok(const AttnArgs& a, int ctx, int carry) {
+  return ctx >= 0 && ctx <= a.max_pages * kPage && carry >= 0 && carry <= a.CP * kPage;
+}
+
+// ------------------------------------------------------------------- dkv
+//
+// grid (committed tiles of the longest row, groups, layer_count * Hkv), one
+// wavefront.  The group's first sequence holds the page row; a tile no block
+// of the group reaches is skipped.
+template <int HD>
+__global__ __launch_bounds__(64) void bwd_dkv_kernel(BwdArgs b) {
+  const AttnArgs& a = b.a;
+  const BwdWs w = bwd_ws(b);
+  const int lane = threadIdx.x;
+  const int tile = blockIdx.x, grp = blockIdx.y, seg = blockIdx.z;
+  const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
+  const int s0 = grp * b.group, s1 = min(a.S, s0 + b.group);
+  const int kbase = 32 * tile;
+  int reach = 0;   // committed keys the group's blocks see
+  for (int s = s0; s < s1; ++s) {
+    const int ctx = a.ctx_len[s], carry = a.carry_len[s];
+    if (len_ok(a, ctx, carry)) reach = max(reach, ctx);
+  }
+  if (kbase >= reach) return;
+  const int32_t* pt = a.page_table + static_cast<int64_t>(s0) * a.max_pages;
+  const int pp0 = 2 * tile, pp1 = 2 * tile + 1;
+  const bool has1 = kbase + kPage < reach;
+  int id0 = pt[pp0], id1 = has1 ? pt[pp1] : 0;
+  const bool bad0 = id0 < 0 || id0 >= a.num_pages, bad1 = has1 && (id1 < 0 || id1 >= a.num_pages);
+  if (bad0 || bad1) {
+    if (lane == 0) set_status(a.status, CO_ERR_PAGE_RANGE);
+    if (bad0) id0 = 0;
+    if (bad1) id1 = 0;
+  }
+  const int64_t pe = static_cast<int64_t>(kPage) * HD;
+  const int64_t lay = static_cast<int64_t>(a.layer_begin + layer_local) * a.num_pages;
+  const int64_t c0 = ((lay + id0) * a.Hkv + g) * pe, c1 = ((lay + id1) * a.Hkv + g) * pe;
+  const int64_t w0 = ((static_cast<int64_t>(layer_local) * a.num_pages + id0) * a.Hkv + g) * pe;
+  const int64_t w1 = ((static_cast<int64_t>(layer_local) * a.num_pages + id1) * a.Hkv + g) * pe;
+  const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
+  u16x8 kb[HD / 16], vb[HD / 16];
+  tile_frags<HD>(kc + c0, kc + c1, w.vn + w0, w.vn + w1, lane, kb, vb);
+  KeyGrad<HD> kg;
+  kg.zero();
+  for (int s = s0; s < s1; ++s) {
+    const int ctx = a.ctx_len[s], carry = a.carry_len[s];
+    if (!len_ok(a, ctx, carry) || ctx <= kbase) continue;
+    const int n0 = bad0 ? 0 : min(kPage, ctx - kbase);
+    const int n1 = bad1 ? 0 : max(0, min(kPage, ctx - kbase - kPage));
+    kg.step(w, (static_cast<int64_t>(seg) * a.S + s) * kNqp, kb, vb, n0, n1, lane);
+  }
+  // every key of the tile that some block sees (keys past `reach` keep no gradient)
+  const int m0 = bad0 ? 0 : min(kPage, reach - kbase);
+  const int m1 = bad1 ? 0 : max(0, min(kPage, reach - kbase - kPage));
+  const int64_t o0 = ((lay + id0) * a.Hkv + g) * pe, o1 = ((lay + id1) * a.Hkv + g) * pe;
+  kg.store(b.d_k_cache + o0, b.d_k_cache + o1, b.d_v_cache + o0, b.d_v_cache + o1, m0, m1, lane);
+}
+
+// -------------------------------------------------------------------- dq
+//
+// grid (S, layer_count * Hkv), one wavefront: the sequence's committed tiles
+// through its page row, then its carry tiles.  Keys are the MFMA rows here
+// (permuted), query rows the columns: lane l keeps query l % 32 throughout.
+template <int HD>
+__global__ __launch_bounds__(64) void bwd_dq_kernel(BwdArgs b) {
+  constexpr int KS = HD / 16, MT = HD / 32;
+  const AttnArgs& a = b.a;
+  const BwdWs w = bwd_ws(b);
+  const int lane = threadIdx.x, r32 = lane & 31, h = lane >> 5;
+  const int s = blockIdx.x, seg = blockIdx.y;
+  const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
+  const int G = a.Hq / a.Hkv, nq = a.B * G;
+  const int ctx_raw = a.ctx_len[s], carry_raw = a.carry_len[s];
+  const bool ok = len_ok(a, ctx_raw, carry_raw);
+  if (!ok && seg == 0 && lane == 0) set_status(a.status, CO_ERR_LENGTH);
+  const int ctx = ok ? ctx_raw : 0, carry = ok ? carry_raw : 0;
+  const int64_t qbase = (static_cast<int64_t>(seg) * a.S + s) * kNqp;
+  // this lane's query column: B-fragments of the rotated queries and of dO
+  u16x8 qb[KS], db[KS];
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    qb[k] = *reinterpret_cast<const u16x8*>(w.qr + (qbase + r32) * HD + 16 * k + 8 * h);
+    db[k] = *reinterpret_cast<const u16x8*>(w.don + (qbase + r32) * HD + 16 * k + 8 * h);
+  }
+  const float l2 = w.lse2[qbase + r32], dd = w.dd[qbase + r32];
+  f32x16 dqt[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dqt[m][r] = 0.f;
+
+  const int kp = perm23(r32);   // the key this lane's A rows hold
+  const int64_t pe = static_cast<int64_t>(kPage) * HD;
+  const int npc = (ctx + kPage - 1) / kPage, nct = (npc + 1) / 2;
+  const int ncp = (carry + kPage - 1) / kPage, ncar = (ncp + 1) / 2;
+  const int32_t* pt = a.page_table + static_cast<int64_t>(s) * a.max_pages;
+  const int32_t* lead = a.page_table + static_cast<int64_t>(s - s % b.group) * a.max_pages;
+  const int64_t lay = static_cast<int64_t>(a.layer_begin + layer_local);
+  const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
+  const uint16_t* kk = static_cast<const uint16_t*>(a.k_carry);
+
+  for (int j = 0; j < nct + ncar; ++j) {
+    const bool com = j < nct;
+    const uint16_t *k0, *k1, *v0, *v1, *t0, *t1;
+    int n0, n1;
+    if (com) {
+      const int p0 = 2 * j, p1 = min(2 * j + 1, npc - 1);
+      int id0 = pt[p0], id1 = pt[p1];
+      const bool b0 = id0 < 0 || id0 >= a.num_pages, b1 = id1 < 0 || id1 >= a.num_pages;
+      if ((b0 || b1) && lane == 0) set_status(a.status, CO_ERR_PAGE_RANGE);
+      if (b.group > 1 && (lead[p0] != id0 || lead[p1] != id1) && lane == 0)
+        set_status(a.status, CO_ERR_GROUP);
+      id0 = b0 ? 0 : id0;
+      id1 = b1 ? 0 : id1;
+      n0 = b0 ? 0 : min(kPage, ctx - 2 * j * kPage);
+      n1 = (b1 || 2 * j + 1 >= npc) ? 0 : min(kPage, ctx - (2 * j + 1) * kPage);
+      const int64_t c0 = ((lay * a.num_pages + id0) * a.Hkv + g) * pe;
+      const int64_t c1 = ((lay * a.num_pages + id1) * a.Hkv + g) * pe;
+      const int64_t w0 = ((static_cast<int64_t>(layer_local) * a.num_pages + id0) * a.Hkv + g) * pe;
+      const int64_t w1 = ((static_cast<int64_t>(layer_local) * a.num_pages + id1) * a.Hkv + g) * pe;
+      k0 = kc + c0; k1 = kc + c1;
+      v0 = w.vn + w0; v1 = w.vn + w1;
+      t0 = w.kt + w0; t1 = w.kt + w1;
+    } else {
+      const int cp0 = 2 * (j - nct), cp1 = min(cp0 + 1, ncp - 1);
+      const int64_t r0 = ((lay * a.S + s) * a.CP + cp0) * a.Hkv + g;
+      const int64_t r1 = ((lay * a.S + s) * a.CP + cp1) * a.Hkv + g;
+      const int64_t q0 = ((static_cast<int64_t>(layer_local) * a.S + s) * a.CP + cp0) * a.Hkv + g;
+      const int64_t q1 = ((static_cast<int64_t>(layer_local) * a.S + s) * a.CP + cp1) * a.Hkv + g;
+      n0 = min(kPage, carry - cp0 * kPage);
+      n1 = cp0 + 1 < ncp ? min(kPage, carry - (cp0 + 1) * kPage) : 0;
+      k0 = kk + r0 * pe; k1 = kk + r1 * pe;
+      v0 = w.vnc + q0 * pe; v1 = w.vnc + q1 * pe;
+      t0 = w.ktc + q0 * pe; t1 = w.ktc + q1 * pe;
+    }
+    // S^T and dP^T with the keys permuted: A rows from K and the key-major V copy
+    const uint16_t* kr = (kp < 16 ? k0 : k1) + (kp & 15) * HD + 8 * h;
+    const uint16_t* vr = (kp < 16 ? v0 : v1) + (kp & 15) * HD + 8 * h;
+    u16x8 ka[KS], va[KS];
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+      ka[k] = *reinterpret_cast<const u16x8*>(kr + 16 * k);
+      va[k] = *reinterpret_cast<const u16x8*>(vr + 16 * k);
+    }
+    // K^T A-fragments: lane dim 32 m + l % 32, keys 16 jj + 8 h .. (page jj)
+    u16x8 kt[MT][2];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj)
+        kt[m][jj] = *reinterpret_cast<const u16x8*>((jj ? t1 : t0) + (32 * m + r32) * kPage + 8 * h);
+    f32x16 sc, dp;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.f;
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+      sc = mfma32x32x16(ka[k], qb[k], sc);
+      dp = mfma32x32x16(va[k], db[k], dp);
+    }
+    u16x8 sb[2];
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      float sv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int r = 8 * jj + e;
+        const int key = acc_index(r, h);
+        const bool valid = key < 16 ? key < n0 : key - 16 < n1;
+        const float pr = valid ? __builtin_amdgcn_exp2f(sc[r] - l2) : 0.f;
+        sv[e] = pr * (dp[r] - dd);
+      }
+      typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+      const u32x4v s4 = {cvt_pk_bf16(sv[0], sv[1]), cvt_pk_bf16(sv[2], sv[3]),
+                         cvt_pk_bf16(sv[4], sv[5]), cvt_pk_bf16(sv[6], sv[7])};
+      sb[jj] = __builtin_bit_cast(u16x8, s4);
+    }
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) dqt[m] = mfma32x32x16(kt[m][jj], sb[jj], dqt[m]);
+
+    if (!com) {   // carry keys belong to this sequence alone: their dK, dV here
+      u16x8 kb[KS], vb[KS];
+      tile_frags<HD>(k0, k1, v0, v1, lane, kb, vb);
+      KeyGrad<HD> kg;
+      kg.zero();
+      kg.step(w, qbase, kb, vb, n0, n1, lane);
+      const int cp0 = 2 * (j - nct);
+      const int64_t d0 = (((lay * a.S + s) * a.CP + cp0) * a.Hkv + g) * pe;
+      const int64_t d1 = (((lay * a.S + s) * a.CP + min(cp0 + 1, a.CP - 1)) * a.Hkv + g) * pe;
+      kg.store(b.d_k_carry + d0, b.d_k_carry + d1, b.d_v_carry + d0, b.d_v_carry + d1, n0, n1,
+               lane);
+    }
+  }
+  // dq = R^T (dS K) / sqrt(hd): dims i and i + hd/2 sit in the same register of tiles m and m + MT/2
+  const int qn = r32;
+  if (qn >= nq) return;
+  const float sc = rsqrtf(static_cast<float>(HD));
+  const int pos = ctx + qn / G;
+  const bool rotate = !(a.flags & CO_Q_PREROTATED);
+  float* dq = b.d_q + out_row_b(a, layer_local, s, g, qn, G) * HD;
+#pragma unroll
+  for (int m = 0; m < MT / 2; ++m)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int i = 32 * m + 8 * (r >> 2) + 4 * h + (r & 3);
+      float x = dqt[m][r] * sc, y = dqt[m + MT / 2][r] * sc;
+      if (rotate) {
+        float c, sn;
+        rope_cos_sin_rev(pos, a.rope_inv[i] * kInv2Pi, &c, &sn);
+        const float x2 = x * c + y * sn, y2 = y * c - x * sn;
+        x = x2;
+        y = y2;
+      }
+      dq[i] = x;
+      dq[i + HD / 2] = y;
+    }
+}
+
+}  // namespace
+
+size_t bwd_workspace_bytes(int S, int L, int Hkv, int hd, int num_pages, int CP) {
+  const int64_t nseg = static_cast<int64_t>(L) * Hkv;
+  auto up = [](int64_t bytes) { return (bytes + 255) / 256 * 256; };
+  const int64_t qsz = nseg * S * kNqp * hd, vsz = nseg * S * kNqp;
+  const int64_t cpg = static_cast<int64_t>(L) * num_pages * Hkv * kPage * hd;
+  const int64_t cpc = static_cast<int64_t>(L) * S * CP * Hkv * kPage * hd;
+  return static_cast<size_t>(4 * up(qsz * 2) + 2 * up(vsz * 4) + 2 * up(cpg * 2) + 2 * up(cpc * 2));
+}
+
+hipError_t launch_attention_backward(const BwdArgs& b, hipStream_t stream) {
+  const AttnArgs& a = b.a;
+  if (a.S == 0 || b.layer_count == 0) return hipSuccess;
+  const int nseg = b.layer_count * a.Hkv;
+  hipLaunchKernelGGL(bwd_prep_kernel<64>, dim3(a.S, nseg), dim3(256), 0, stream, b);
+  const int64_t pages = static_cast<int64_t>(b.layer_count) * a.Hkv *
+                        (static_cast<int64_t>(a.num_pages) + static_cast<int64_t>(a.S) * a.CP);
+  const int64_t items = pages * (kPage * 64 / 8);
+  hipLaunchKernelGGL(bwd_copy_kernel<64>, dim3(static_cast<unsigned>((items + 255) / 256)),
+                     dim3(256), 0, stream, b);
+  const int groups = (a.S + b.group - 1) / b.group;
+  const int tiles = (a.max_pages + 1) / 2;
+  hipLaunchKernelGGL(bwd_dkv_kernel<64>, dim3(tiles, groups, nseg), dim3(64), 0, stream, b);
+  hipLaunchKernelGGL(bwd_dq_kernel<64>, dim3(a.S, nseg), dim3(64), 0, stream, b);
+  return hipGetLastError();
+}
+
+}  // namespace co

@@ -147,6 +147,9 @@ size_t carryover_workspace_bytes(const co_dims* dims, int32_t which) {
     case CO_WS_PROJECT: return pw;
     case CO_WS_ATTENTION: return aw;
     case CO_WS_ROUND: return aw ? pw + aw : 0;   // projection scratch, then attention area
+    case CO_WS_ATTENTION_BACKWARD:
+      return bwd_workspace_bytes(dims->num_seqs, dims->num_layers, dims->num_kv_heads,
+                                 dims->head_dim, dims->num_pages, carry_pages(dims));
     default: return 0;
   }
 }
@@ -238,6 +241,64 @@ co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int3
   if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
   if (ws_bytes < p.bytes) return CO_ERR_WORKSPACE;
   return do_attention(dims, layer_begin, layer_count, q, state, out, lse, flags, ws, stream);
+}
+
+co_status drafter_block_attention_backward(
+    const co_dims* dims, int32_t layer_begin, int32_t layer_count, const void* q,
+    const co_state* state, const void* out, const float* lse, const void* d_out,
+    int32_t seqs_per_group, float* d_q, float* d_k_cache, float* d_v_cache, float* d_k_carry,
+    float* d_v_carry, uint32_t flags, void* ws, size_t ws_bytes, hipStream_t stream) {
+  co_status s = check_dims(dims);
+  if (s != CO_OK) return s;
+  if (dims->dtype != CO_DTYPE_BF16 || dims->head_dim != 64 ||
+      dims->block * (dims->num_q_heads / dims->num_kv_heads) > 32)
+    return CO_ERR_UNSUPPORTED;
+  if (layer_begin < 0 || layer_count < 0 || layer_begin + layer_count > dims->num_layers ||
+      seqs_per_group < 1)
+    return CO_ERR_INVALID_ARG;
+  if (!q || !out || !lse || !d_out || !d_q || !d_k_cache || !d_v_cache || !d_k_carry ||
+      !d_v_carry || !state_ok(state) || !aligned(q, 16) || !aligned(out, 16) ||
+      !aligned(d_out, 16) || !aligned(lse, 16) || !aligned(d_q, 16) || !aligned(d_k_cache, 16) ||
+      !aligned(d_v_cache, 16) || !aligned(d_k_carry, 16) || !aligned(d_v_carry, 16))
+    return CO_ERR_INVALID_ARG;
+  if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
+  if (ws_bytes < carryover_workspace_bytes(dims, CO_WS_ATTENTION_BACKWARD)) return CO_ERR_WORKSPACE;
+  BwdArgs b{};
+  AttnArgs& a = b.a;
+  a.S = dims->num_seqs;
+  a.B = dims->block;
+  a.L = dims->num_layers;
+  a.layer_begin = layer_begin;
+  a.Hq = dims->num_q_heads;
+  a.Hkv = dims->num_kv_heads;
+  a.hd = dims->head_dim;
+  a.num_pages = dims->num_pages;
+  a.max_pages = dims->max_pages_per_seq;
+  a.CP = carry_pages(dims);
+  a.dtype = dims->dtype;
+  a.flags = flags;
+  fill_rope_table(a.rope_inv, dims);
+  a.q = q;
+  a.ctx_len = state->ctx_len;
+  a.carry_len = state->carry_len;
+  a.page_table = state->page_table;
+  a.k_cache = state->k_cache;
+  a.v_cache = state->v_cache;
+  a.k_carry = state->k_carry;
+  a.v_carry = state->v_carry;
+  a.status = state->status;
+  a.ws = static_cast<float*>(ws);
+  b.layer_count = layer_count;
+  b.group = seqs_per_group;
+  b.out = out;
+  b.lse = lse;
+  b.d_out = d_out;
+  b.d_q = d_q;
+  b.d_k_cache = d_k_cache;
+  b.d_v_cache = d_v_cache;
+  b.d_k_carry = d_k_carry;
+  b.d_v_carry = d_v_carry;
+  return hip_status(launch_attention_backward(b, stream));
 }
 
 co_status drafter_carry_mass(const co_dims* dims, int32_t layer_begin, int32_t layer_count,
@@ -361,6 +422,7 @@ const char* carryover_status_string(co_status status) {
     case CO_ERR_PAGE_RANGE: return "page id out of range";
     case CO_ERR_HIP: return "HIP runtime error";
     case CO_ERR_LENGTH: return "invalid sequence length";
+    case CO_ERR_GROUP: return "page rows differ within a sequence group";
     default: return "unknown status";
   }
 }

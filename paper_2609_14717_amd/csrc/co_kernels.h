@@ -95,6 +95,24 @@ struct AttnPlan {
 AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int num_pages,
                         int dtype, int num_cus);
 
+// Reverse mode of the bf16 attention (head_dim 64, up to 32 query rows per KV
+// head): `a` carries the forward's arguments with ws = the backward workspace.
+struct BwdArgs {
+  AttnArgs a;
+  int layer_count, group;   // layers of the launch; sequences per shared page row
+  const void* out;          // forward output O (bf16)
+  const float* lse;         // forward LSE (natural log)
+  const void* d_out;        // dO (bf16)
+  float* d_q;               // [layers][S][B][Hq][hd]
+  float* d_k_cache;         // like k_cache, fp32
+  float* d_v_cache;         // like v_cache, fp32
+  float* d_k_carry;         // like k_carry, fp32
+  float* d_v_carry;         // like v_carry, fp32
+};
+
+size_t bwd_workspace_bytes(int S, int L, int Hkv, int hd, int num_pages, int CP);
+hipError_t launch_attention_backward(const BwdArgs& b, hipStream_t stream);
+
 // Attention mass on the carried rows, from a finished attention call's LSE.
 constexpr int kMaxCarryRows = 64;   // carry rows of one sequence (block <= 64)
 

@@ -32,6 +32,7 @@ ST_CTX0, ST_PAGES, ST_KDIR, ST_VDIR, ST_HCTX, ST_ANCHOR, ST_U = 9, 10, 11, 12, 1
 ST_WFC = 16             # the separate carry projector (a variant next to the path)
 ST_ZNORM, ST_KSELF, ST_VSELF = 17, 18, 19   # RMS-norm gain offsets; block self K/V
 ST_KNORM = 20           # per-head key RMS-norm gain offsets
+ST_DOUT = 21            # gradient of a loss with respect to the attention output
 
 
 @dataclass(frozen=True)
@@ -264,6 +265,15 @@ def spec_q(w, rnd, S=None):
     shape = (w.L, S, w.B, w.Hq, w.hd)
     strides = (S * w.B * w.Hq * w.hd, w.B * w.Hq * w.hd, w.Hq * w.hd, w.hd, 1)
     return ST_Q, shape, strides, rnd * w.L * S * w.B * w.Hq * w.hd, w.sigma_q
+
+
+def spec_dout(w, S=None):
+    """Output gradient dO of the attention (the backward's input): [L][S][B][Hq][hd],
+    unit variance."""
+    S = w.S if S is None else S
+    shape = (w.L, S, w.B, w.Hq, w.hd)
+    strides = (S * w.B * w.Hq * w.hd, w.B * w.Hq * w.hd, w.Hq * w.hd, w.hd, 1)
+    return ST_DOUT, shape, strides, 0, 1.0
 
 
 def spec_kv_direct(w, which, s, t0, n):

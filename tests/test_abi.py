@@ -215,3 +215,22 @@ def test_k_norm_pointer_alignment_checked():
     assert _rc(lambda: co.carryover_project_kv(_dims(), W, FAKE, _fake_route(), _fake_state(),
                                                FAKE, stream=0, ws_bytes=1 << 30)) \
         == co.CO_ERR_INVALID_ARG
+
+
+def test_attention_backward_arguments_checked_on_host():
+    st = _fake_state()
+
+    def call(dims, group=1, dq=FAKE, wsb=1 << 30):
+        return co.drafter_block_attention_backward(dims, 0, 1, FAKE, st, FAKE, FAKE, FAKE, group,
+                                                   dq, FAKE, FAKE, FAKE, FAKE, FAKE, stream=0,
+                                                   ws_bytes=wsb)
+
+    d = _dims()
+    assert co.workspace_bytes(d, co.CO_WS_ATTENTION_BACKWARD) > 0
+    assert _rc(lambda: call(d, group=0)) == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: call(d, dq=None)) == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: call(d, dq=FAKE + 4)) == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: call(d, wsb=16)) == co.CO_ERR_WORKSPACE
+    assert _rc(lambda: call(_dims(dtype="f32"))) == co.CO_ERR_UNSUPPORTED
+    assert _rc(lambda: call(_dims(hd=128))) == co.CO_ERR_UNSUPPORTED
+    assert _rc(lambda: call(_dims(Hq=8))) == co.CO_ERR_UNSUPPORTED   # 64 query rows per KV head

@@ -1,0 +1,238 @@
+"""GPU parity of the attention backward (the training side of the second
+drafter pass, Algorithm 2) through the C ABI, against the fp64 oracle's
+reverse mode (itself pinned by finite differences):
+
+* the training layout: the anchored blocks of each recorded response share its
+  committed pages (one group per response), so a committed key's gradient is
+  the sum over every block that sees it; carry keys belong to one block;
+* a serving layout (one sequence per group) after carryover rounds: ragged
+  contexts, an empty sequence, a sequence with carry rows only, padded query
+  rows (8 block rows x 2 heads) and a layer sub-range.
+
+Gradients are compared per head vector against the oracle, relative to the
+largest reference vector of the same (layer, KV head) slab: the GPU rounds the
+softmax weights and dS to bf16 before its products, as the forward rounds P.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from synth import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from helpers import OracleRun, host, seq_block, to_np  # noqa: E402
+
+GTOL = 2e-2
+
+TRAIN_SMALL = wl.TRAIN_FWD.replace(name="bwd_train_small", S=2, seq_len=512, anchors=10,
+                                   seed=0x5EED30)
+SERVE = wl.RAGGED32.replace(name="bwd_serve", S=6, B=8, L=2, ctx_lo=40, ctx_hi=700, rounds=4,
+                            accept=("geom", 0.3), seed=0x5EED31)
+
+
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_14717_amd as co
+    return co
+
+
+def slab_close(g, r, what, tol=GTOL):
+    """g, r [n][hd] of one (layer, KV head): every head vector within tol of
+    the slab's largest reference vector."""
+    g = np.asarray(g, np.float64)
+    r = np.asarray(r, np.float64)
+    assert np.all(np.isfinite(g)), f"{what}: non-finite GPU values"
+    if r.size == 0:
+        return 0.0
+    scale = max(np.abs(r).max(), 1e-30)
+    e = float(np.abs(g - r).max() / scale)
+    assert e <= tol, f"{what}: max error {e:.3e} of the slab's largest value > {tol}"
+    return e
+
+
+def oracle_grads(st, Q, dO, Hq, theta, seqs, group_of):
+    """Reverse mode of attend_state: dq [L][S][B][Hq][hd] and, per group, the
+    committed keys' gradients summed over the group's sequences
+    ({grp: (dK, dV)} with [L][n][Hkv][hd]), and per sequence the carry keys'."""
+    L, S, B, _, hd = Q.shape
+    Hkv = st.Hkv
+    G = Hq // Hkv
+    ctx = st.ctx_len()
+    dq = np.zeros(Q.shape)
+    com, car = {}, {}
+    for s in seqs:
+        nc = int(ctx[s])
+        nu = st.uk[s].shape[1]
+        grp = group_of(s)
+        if grp not in com:
+            com[grp] = [np.zeros((L, 0, Hkv, hd)), np.zeros((L, 0, Hkv, hd))]
+        for i in range(2):   # grow to this sequence's committed length
+            have = com[grp][i].shape[1]
+            if have < nc:
+                com[grp][i] = np.concatenate([com[grp][i], np.zeros((L, nc - have, Hkv, hd))], 1)
+        car[s] = [np.zeros((L, nu, Hkv, hd)), np.zeros((L, nu, Hkv, hd))]
+        for layer in range(L):
+            for g in range(Hkv):
+                k, v = st.context(s, layer, g)
+                heads = list(range(g * G, (g + 1) * G))
+                q = Q[layer, s][:, heads].reshape(B * G, hd)
+                do = dO[layer, s][:, heads].reshape(B * G, hd)
+                qpos = np.repeat(nc + np.arange(B), G)
+                gq, gk, gv = oracle.attend_backward(q, qpos, k, v, do, theta)
+                dq[layer, s][:, heads] = gq.reshape(B, G, hd)
+                com[grp][0][layer, :nc, g] += gk[:nc]
+                com[grp][1][layer, :nc, g] += gv[:nc]
+                car[s][0][layer, :, g] = gk[nc:]
+                car[s][1][layer, :, g] = gv[nc:]
+    return dq, com, car
+
+
+def grad_buffers(st):
+    z = lambda t: torch.zeros(t.shape, dtype=torch.float32, device=t.device)
+    return z(st["k_cache"]), z(st["v_cache"]), z(st["k_carry"]), z(st["v_carry"])
+
+
+def gather_grad_committed(dk, dv, pt_row, layer, n):
+    pos = torch.arange(n, device=dk.device)
+    pages = pt_row[pos // 16].long()
+    slots = (pos % 16).long()
+    return to_np(dk[layer][pages, :, slots, :]), to_np(dv[layer][pages, :, :, slots])
+
+
+def gather_grad_carry(dk, dv, s, layer, n):
+    r = torch.arange(n, device=dk.device)
+    return (to_np(dk[layer, s][r // 16, :, r % 16, :]), to_np(dv[layer, s][r // 16, :, :, r % 16]))
+
+
+def check(co, dims, st, q, out, lse, dO_dev, group, orc_st, Q, dO, w, seqs, group_of, leaders,
+          layer_begin=0, layer_count=None, tag=""):
+    layer_count = w.L if layer_count is None else layer_count
+    dk, dv, dkc, dvc = grad_buffers(st)
+    dq = torch.zeros((layer_count,) + tuple(q.shape[1:]), dtype=torch.float32, device="cuda")
+    ws = torch.zeros(co.workspace_bytes(dims, co.CO_WS_ATTENTION_BACKWARD) + 256,
+                     dtype=torch.uint8, device="cuda")
+    co.drafter_block_attention_backward(dims, layer_begin, layer_count,
+                                        q[layer_begin:layer_begin + layer_count], st, out, lse,
+                                        dO_dev, group, dq, dk, dv, dkc, dvc, ws)
+    torch.cuda.synchronize()
+    assert co.carryover_read_status(st) == 0
+    rq, rcom, rcar = oracle_grads(orc_st, Q, dO, w.Hq, w.theta, seqs, group_of)
+    gq = to_np(dq)
+    G = w.Hq // w.Hkv
+    errs = []
+    for s in seqs:
+        for li, layer in enumerate(range(layer_begin, layer_begin + layer_count)):
+            for g in range(w.Hkv):
+                heads = list(range(g * G, (g + 1) * G))
+                errs.append(slab_close(gq[li, s][:, heads].reshape(-1, w.hd),
+                                       rq[layer, s][:, heads].reshape(-1, w.hd),
+                                       f"{tag} dq s{s} l{layer} g{g}"))
+        nu = orc_st.uk[s].shape[1]
+        if nu:
+            for layer in range(layer_begin, layer_begin + layer_count):
+                gk, gv = gather_grad_carry(dkc, dvc, s, layer, nu)
+                for g in range(w.Hkv):
+                    errs.append(slab_close(gk[:, g], rcar[s][0][layer, :, g],
+                                           f"{tag} dk carry s{s} g{g}"))
+                    errs.append(slab_close(gv[:, g], rcar[s][1][layer, :, g],
+                                           f"{tag} dv carry s{s} g{g}"))
+    pt = st["page_table"]
+    for grp, (rk, rv) in rcom.items():
+        n = rk.shape[1]
+        if n == 0:
+            continue
+        for layer in range(layer_begin, layer_begin + layer_count):
+            gk, gv = gather_grad_committed(dk, dv, pt[leaders[grp]], layer, n)
+            for g in range(w.Hkv):
+                errs.append(slab_close(gk[:, g], rk[layer, :, g], f"{tag} dk group {grp} g{g}"))
+                errs.append(slab_close(gv[:, g], rv[layer, :, g], f"{tag} dv group {grp} g{g}"))
+    print(f"[backward] {tag}: max slab error {max(errs):.3e} over {len(errs)} slabs", flush=True)
+
+
+def test_backward_train_layout():
+    co = _gpu()
+    from helpers import OracleTrain
+    from synth.scenario import TrainScenario
+    from synth import device as sdev
+    w = TRAIN_SMALL
+    V, A = w.S * w.anchors, w.anchors
+    print(f"[backward] workload={w.name} blocks={V}", flush=True)
+    sc = TrainScenario(w)
+    out, lse = sc.forward(shared_prefix=True)
+    dO_dev = sdev.materialise(w, wl.spec_dout(w, S=V), "cuda")
+    torch.cuda.synchronize()
+    orc = OracleTrain(w, range(V))
+    Q = seq_block(w, wl.spec_q(w, 0, S=V), 1, range(V))
+    dO = host(w, wl.spec_dout(w, S=V))
+    check(co, sc.vdims, sc.vst, sc.q, out, lse, dO_dev, A, orc.st, Q, dO, w, list(range(V)),
+          lambda v: v // A, {r: r * A for r in range(w.S)}, tag="train")
+
+
+def test_backward_serving_layout():
+    co = _gpu()
+    from synth.scenario import Scenario
+    from synth import device as sdev
+    w = SERVE
+    sc, orc = Scenario(w), OracleRun(w)
+    # sequence 4 empty, sequence 5 carry rows only
+    for r in range(3):
+        hidden, q, draft, target, m = sc.round_inputs(r)
+        out, lse = sc.new_output()
+        co.carryover_round(sc.dims, sc.W, hidden, draft, target, q, sc.st, sc.rt, out, lse, 0,
+                           sc.ws)
+        orc.round(r, attend=False)
+    torch.cuda.synchronize()
+    # one sequence without keys, and one with carry rows only
+    sc.st["ctx_len"][4] = 0
+    sc.st["carry_len"][4] = 0
+    orc.st.ck[4] = orc.st.ck[4][:, :0]
+    orc.st.cv[4] = orc.st.cv[4][:, :0]
+    orc.st.uk[4] = orc.st.uk[4][:, :0]
+    orc.st.uv[4] = orc.st.uv[4][:, :0]
+    with_carry = [s for s in range(w.S) if s != 4 and orc.st.uk[s].shape[1] > 0]
+    if with_carry:
+        sc_only = with_carry[-1]
+        sc.st["ctx_len"][sc_only] = 0
+        orc.st.ck[sc_only] = orc.st.ck[sc_only][:, :0]
+        orc.st.cv[sc_only] = orc.st.cv[sc_only][:, :0]
+    _, q, _, _, _ = sc.round_inputs(3)
+    out, lse = sc.new_output()
+    co.drafter_block_attention(sc.dims, 0, w.L, q, sc.st, out, lse, 0, sc.ws)
+    dO_dev = sdev.materialise(w, wl.spec_dout(w), "cuda")
+    torch.cuda.synchronize()
+    Q = host(w, wl.spec_q(w, 3))
+    dO = host(w, wl.spec_dout(w))
+    seqs = list(range(w.S))
+    print(f"[backward] workload={w.name} layers 0..{w.L - 1}", flush=True)
+    check(co, sc.dims, sc.st, q, out, lse, dO_dev, 1, orc.st, Q, dO, w, seqs, lambda s: s,
+          {s: s for s in seqs}, tag="serve")
+    # the second layer alone: its forward output and LSE are the slices of layer 1
+    print(f"[backward] workload={w.name} layer 1 alone", flush=True)
+    Q1 = Q.copy()
+    dO1 = dO.copy()
+    dO1[0] = 0.0
+    check(co, sc.dims, sc.st, q, out[1:], lse[1:], dO_dev[1:], 1, orc.st, Q1, dO1, w, seqs,
+          lambda s: s, {s: s for s in seqs}, layer_begin=1, layer_count=1, tag="serve l1")
+
+
+def test_backward_group_mismatch_sets_status():
+    """Sequences declared as one group whose page rows differ: CO_ERR_GROUP."""
+    co = _gpu()
+    from synth.scenario import Scenario
+    w = SERVE.replace(name="bwd_group", S=4, L=1, rounds=2, seed=0x5EED32)
+    sc = Scenario(w)
+    _, q, _, _, _ = sc.round_inputs(0)
+    out, lse = sc.new_output()
+    co.drafter_block_attention(sc.dims, 0, w.L, q, sc.st, out, lse, 0, sc.ws)
+    dk, dv, dkc, dvc = grad_buffers(sc.st)
+    dq = torch.zeros(q.shape, dtype=torch.float32, device="cuda")
+    ws = torch.zeros(co.workspace_bytes(sc.dims, co.CO_WS_ATTENTION_BACKWARD) + 256,
+                     dtype=torch.uint8, device="cuda")
+    co.drafter_block_attention_backward(sc.dims, 0, w.L, q, sc.st, out, lse, out, 2, dq, dk, dv,
+                                        dkc, dvc, ws)
+    torch.cuda.synchronize()
+    assert co.carryover_read_status(sc.st) == co.CO_ERR_GROUP
