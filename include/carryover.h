@@ -264,6 +264,36 @@ co_status drafter_block_attention_backward(
     float* d_v_carry, uint32_t flags, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Reverse mode of carryover_project_kv for the trained parameters (Algorithm 2:
+ * the second pass's loss reaches W_F, W_KV and E_carry through the K/V rows
+ * of Eqs. 1-2; the target's states are constants).  For the dims, weights,
+ * hidden rows and route of a forward carryover_project_kv call, and fp32
+ * gradient arrays shaped like the caches (d_k_cache / d_v_cache like
+ * k_cache / v_cache, d_k_carry / d_v_carry like k_carry / v_carry, e.g. from
+ * drafter_block_attention_backward) holding the gradient of a loss with
+ * respect to the stored (rotated) keys and the values: every row r with a
+ * destination takes the gradient at that destination (committed slot or carry
+ * row), its key gradient rotated back at row_pos[r]; rows that were not stored
+ * contribute nothing.  With x_r = h_r (+ e_carry on carried rows) and
+ * z_r = F x_r, the call ADDS
+ *   d_w_f     fp32 [model_dim][feat_dim]:  sum_r (W_KV^T dJ_r) x_r^T,
+ *   d_w_kv    fp32 [NKV][model_dim]:       sum_r dJ_r z_r^T,
+ *   d_e_carry fp32 [feat_dim]:             sum over carried r of F^T W_KV^T dJ_r,
+ * so that the two forward calls of a training step (committed rows, then the
+ * blocks' carried rows) accumulate into the same arrays (zero them first).
+ * Operands are rounded to bf16 for the products (fp32 sums); deterministic.
+ * Supported: bf16; the plain update only (w_f_carry, z_norm and k_norm NULL,
+ * else CO_ERR_UNSUPPORTED).  `ws`: carryover_workspace_bytes(dims,
+ * CO_WS_PROJECT_BACKWARD) bytes, 256-byte aligned.
+ */
+co_status carryover_project_kv_backward(const co_dims* dims, const co_weights* w,
+                                        const void* hidden, const co_route* route,
+                                        const float* d_k_cache, const float* d_v_cache,
+                                        const float* d_k_carry, const float* d_v_carry,
+                                        float* d_w_f, float* d_w_kv, float* d_e_carry, void* ws,
+                                        size_t ws_bytes, hipStream_t stream);
+
+/*
  * Attention mass on the carried rows (the diagnostic of Appendix "Attention to
  * carried states"; for the carry segment U of ctx = [C;U], Eq. 2).  For every
  * (layer, sequence, block row i, query head h) of a drafter_block_attention
@@ -318,7 +348,8 @@ co_status carryover_import_kv(const co_dims* dims, int32_t seq, int32_t pos0, in
                               const void* k_rows, const void* v_rows, const co_state* state,
                               hipStream_t stream);
 
-enum { CO_WS_PROJECT = 0, CO_WS_ATTENTION = 1, CO_WS_ROUND = 2, CO_WS_ATTENTION_BACKWARD = 3 };
+enum { CO_WS_PROJECT = 0, CO_WS_ATTENTION = 1, CO_WS_ROUND = 2, CO_WS_ATTENTION_BACKWARD = 3,
+       CO_WS_PROJECT_BACKWARD = 4 };
 
 /* Workspace bytes a call needs for these dims (0 on unsupported dims). */
 size_t carryover_workspace_bytes(const co_dims* dims, int32_t which);

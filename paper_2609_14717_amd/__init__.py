@@ -22,6 +22,7 @@ CO_BASELINE_MODE, CO_ROUTE_ACCEPT_ALL, CO_ROUTE_CARRY_ONLY, CO_Q_PREROTATED = 1,
 CO_ATTN_SHARED_PREFIX = 16
 CO_ROUTE_ACCEPT_BITS = 32
 CO_WS_PROJECT, CO_WS_ATTENTION, CO_WS_ROUND, CO_WS_ATTENTION_BACKWARD = 0, 1, 2, 3
+CO_WS_PROJECT_BACKWARD = 4
 SKIP = -(2 ** 31)
 PAGE = 16
 
@@ -88,6 +89,9 @@ def lib():
                                                  _v, _P(co_state), _v, _v, _v, ctypes.c_int32,
                                                  _v, _v, _v, _v, _v, ctypes.c_uint32, _v,
                                                  ctypes.c_size_t, _v],
+            "carryover_project_kv_backward": [_P(co_dims), _P(co_weights), _v, _P(co_route),
+                                              _v, _v, _v, _v, _v, _v, _v, _v, ctypes.c_size_t,
+                                              _v],
             "drafter_carry_mass": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, _v, _P(co_state),
                                    _v, _v, ctypes.c_uint32, _v],
             "drafter_self_merge": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, _v, _v, _v,
@@ -110,7 +114,8 @@ def lib():
 
 EXPORTED = ("carryover_route", "carryover_project_kv", "drafter_block_attention",
             "carryover_round", "carryover_fold_e", "drafter_carry_mass", "drafter_self_merge",
-            "drafter_block_attention_backward", "carryover_import_kv",
+            "drafter_block_attention_backward", "carryover_project_kv_backward",
+            "carryover_import_kv",
             "carryover_workspace_bytes", "carryover_read_status", "carryover_status_string")
 
 
@@ -233,6 +238,17 @@ def drafter_block_attention_backward(dims, layer_begin, layer_count, q, st, out,
         _ptr(lse), _ptr(d_out), seqs_per_group, _ptr(d_q), _ptr(d_k_cache), _ptr(d_v_cache),
         _ptr(d_k_carry), _ptr(d_v_carry), flags, _ptr(ws), nb, _stream(stream)),
         "drafter_block_attention_backward")
+
+
+def carryover_project_kv_backward(dims, w, hidden, rt, d_k_cache, d_v_cache, d_k_carry,
+                                  d_v_carry, d_w_f, d_w_kv, d_e_carry, ws, stream=None,
+                                  ws_bytes=None):
+    r = route(rt)
+    nb = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    _check(lib().carryover_project_kv_backward(
+        ctypes.byref(dims), ctypes.byref(w), _ptr(hidden), ctypes.byref(r), _ptr(d_k_cache),
+        _ptr(d_v_cache), _ptr(d_k_carry), _ptr(d_v_carry), _ptr(d_w_f), _ptr(d_w_kv),
+        _ptr(d_e_carry), _ptr(ws), nb, _stream(stream)), "carryover_project_kv_backward")
 
 
 def drafter_carry_mass(dims, layer_begin, layer_count, q, st, lse, mass, flags=0, stream=None):

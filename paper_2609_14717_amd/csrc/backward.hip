@@ -29,6 +29,8 @@
 //          since carry keys belong to one sequence.
 // Keys masked in the forward (past ctx_len or carry_len, rejected page ids)
 // get no gradient and contribute none.
+#include <algorithm>
+
 #include "co_kernels.h"
 
 namespace co {
@@ -583,6 +585,237 @@ hipError_t launch_attention_backward(const BwdArgs& b, hipStream_t stream) {
   const int tiles = (a.max_pages + 1) / 2;
   hipLaunchKernelGGL(bwd_dkv_kernel<64>, dim3(tiles, groups, nseg), dim3(64), 0, stream, b);
   hipLaunchKernelGGL(bwd_dq_kernel<64>, dim3(a.S, nseg), dim3(64), 0, stream, b);
+  return hipGetLastError();
+}
+
+}  // namespace co
+
+// ============================================================================
+// Reverse mode of the K/V projection (Eq. 1-2: x = h + E on carried rows,
+// z = F x, k_l = R(pos) K_l z, v_l = V_l z) for the trained W_F, W_KV and
+// E_carry, the target's states h held constant:
+//   dJ_r = [R(pos_r)^T dk_r ; dv_r] for every layer and KV head (W_KV's row order),
+//   dW_KV += sum_r dJ_r z_r^T,   dz_r = W_KV^T dJ_r,
+//   dW_F  += sum_r dz_r h_r^T + u E^T,   dE += F^T u,   u = sum over carried r of dz_r.
+// The products run on the projection's MFMA kernels with the summed index (the
+// rows) contiguous in both operands, so the row-major inputs are transposed
+// first; rows are padded with zeros to a multiple of 256.
+namespace co {
+
+namespace {
+
+constexpr int kRowPad = 256;
+
+struct PbWs {
+  float *fe, *u, *t32, *part;
+  uint16_t *ht, *dj, *djt, *ztb, *dztb, *wkvt;
+  int Mp;
+};
+
+int64_t pb_up(int64_t b) { return (b + 255) / 256 * 256; }
+
+PbWs pb_ws(void* ws, int M, int Dcat, int d, int n_kv) {
+  PbWs w;
+  w.Mp = (M + kRowPad - 1) / kRowPad * kRowPad;
+  const int64_t Mp = w.Mp;
+  char* p = static_cast<char*>(ws);
+  w.fe = reinterpret_cast<float*>(p); p += pb_up(d * 4);
+  w.u = reinterpret_cast<float*>(p); p += pb_up(d * 4);
+  w.t32 = reinterpret_cast<float*>(p); p += pb_up(d * Mp * 4);
+  w.ht = reinterpret_cast<uint16_t*>(p); p += pb_up(Dcat * Mp * 2);
+  w.dj = reinterpret_cast<uint16_t*>(p); p += pb_up(Mp * n_kv * 2);
+  w.djt = reinterpret_cast<uint16_t*>(p); p += pb_up(Mp * n_kv * 2);
+  w.ztb = reinterpret_cast<uint16_t*>(p); p += pb_up(d * Mp * 2);
+  w.dztb = reinterpret_cast<uint16_t*>(p); p += pb_up(d * Mp * 2);
+  w.wkvt = reinterpret_cast<uint16_t*>(p); p += pb_up(static_cast<int64_t>(d) * n_kv * 2);
+  w.part = reinterpret_cast<float*>(p);
+  return w;
+}
+
+// dst[c][r] = src[r][c] for r < R (zero for R <= r < Rp), c < C: 64 x 64 tiles through LDS.
+__global__ __launch_bounds__(256) void pb_transpose_kernel(const uint16_t* src, int R, int C,
+                                                           int64_t src_ld, uint16_t* dst, int Rp,
+                                                           int64_t dst_ld) {
+  __shared__ uint16_t t[64][65];
+  const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int r = r0 + i, c = c0 + tx;
+    t[i][tx] = (r < R && c < C) ? src[r * src_ld + c] : static_cast<uint16_t>(0);
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < C && r < Rp) dst[c * dst_ld + r] = t[tx][i];
+  }
+}
+
+// dJ^T [NKV][Mp]: one thread per (layer, head, rotation pair, row), rows fastest.
+__global__ __launch_bounds__(256) void pb_gather_kernel(ProjBwdArgs a, uint16_t* djt, int Mp) {
+  const int half = a.hd / 2;
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t total = static_cast<int64_t>(a.L) * a.Hkv * half * Mp;
+  if (idx >= total) return;
+  const int r = static_cast<int>(idx % Mp);
+  const int64_t jp = idx / Mp;
+  const int i = static_cast<int>(jp % half);
+  const int g = static_cast<int>((jp / half) % a.Hkv);
+  const int l = static_cast<int>(jp / (static_cast<int64_t>(half) * a.Hkv));
+  float klo = 0.f, khi = 0.f, vlo = 0.f, vhi = 0.f;
+  const int32_t dst = r < a.M ? a.row_dst[r] : kSkip;
+  const int64_t pe = static_cast<int64_t>(kPage) * a.hd;
+  int64_t pg = -1;
+  const float *kb = nullptr, *vb = nullptr;
+  int slot = 0;
+  if (dst >= 0) {
+    const int page = dst / kPage;
+    slot = dst % kPage;
+    if (page < a.num_pages) {
+      pg = (static_cast<int64_t>(l) * a.num_pages + page) * a.Hkv + g;
+      kb = a.dk;
+      vb = a.dv;
+    }
+  } else if (dst != kSkip) {
+    const int c = -1 - dst, s = r / a.B;
+    if (c < a.CP * kPage) {
+      slot = c % kPage;
+      pg = ((static_cast<int64_t>(l) * a.S + s) * a.CP + c / kPage) * a.Hkv + g;
+      kb = a.dkc;
+      vb = a.dvc;
+    }
+  }
+  if (pg >= 0) {
+    const float* kr = kb + pg * pe + slot * a.hd;
+    const float* vr = vb + pg * pe + slot;
+    const float k0 = kr[i], k1 = kr[i + half];
+    vlo = vr[i * kPage];
+    vhi = vr[(i + half) * kPage];
+    float c, s;
+    rope_cos_sin(a.row_pos[r], a.rope_inv[i], &c, &s);   // R^T: turn back by the row's angle
+    klo = k0 * c + k1 * s;
+    khi = k1 * c - k0 * s;
+  }
+  const int64_t jk = ((static_cast<int64_t>(l) * 2 + 0) * a.Hkv + g) * a.hd + i;
+  const int64_t jv = ((static_cast<int64_t>(l) * 2 + 1) * a.Hkv + g) * a.hd + i;
+  djt[jk * Mp + r] = f2bf(klo);
+  djt[(jk + half) * Mp + r] = f2bf(khi);
+  djt[jv * Mp + r] = f2bf(vlo);
+  djt[(jv + half) * Mp + r] = f2bf(vhi);
+}
+
+// Z^T (fp32 [d][M]) + F E on carried rows -> bf16 [d][Mp], padding rows zero.
+__global__ __launch_bounds__(256) void pb_zt_kernel(const float* t32, int d, int M, int Mp,
+                                                    const int32_t* row_dst, const float* fe,
+                                                    uint16_t* ztb) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= static_cast<int64_t>(d) * Mp) return;
+  const int r = static_cast<int>(idx % Mp), dd = static_cast<int>(idx / Mp);
+  float v = 0.f;
+  if (r < M) {
+    const int32_t dst = row_dst[r];
+    v = t32[static_cast<int64_t>(dd) * M + r] + ((dst < 0 && dst != kSkip) ? fe[dd] : 0.f);
+  }
+  ztb[idx] = f2bf(v);
+}
+
+// dZ^T (fp32 [d][Mp]) -> bf16, and u[dd] = its sum over the carried rows; one
+// workgroup per dd.
+__global__ __launch_bounds__(256) void pb_dz_kernel(const float* t32, int M, int Mp,
+                                                    const int32_t* row_dst, uint16_t* dztb,
+                                                    float* u) {
+  __shared__ float red[4];
+  const int dd = blockIdx.x;
+  const float* src = t32 + static_cast<int64_t>(dd) * Mp;
+  uint16_t* dst = dztb + static_cast<int64_t>(dd) * Mp;
+  float acc = 0.f;
+  for (int r = threadIdx.x; r < Mp; r += 256) {
+    const float v = src[r];
+    dst[r] = f2bf(v);
+    if (r < M) {
+      const int32_t x = row_dst[r];
+      if (x < 0 && x != kSkip) acc += v;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) u[dd] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// dW_F[dd][c] += u[dd] E[c]; dE[c] += sum_dd W_F[dd][c] u[dd].
+__global__ __launch_bounds__(256) void pb_e_kernel(float* dwf, float* de, const float* u,
+                                                   const uint16_t* e, const uint16_t* wf, int d,
+                                                   int Dcat) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= Dcat) return;
+  const float ec = bf2f(e[c]);
+  float acc = 0.f;
+  for (int dd = 0; dd < d; ++dd) {
+    const float ud = u[dd];
+    dwf[static_cast<int64_t>(dd) * Dcat + c] += ud * ec;
+    acc = fmaf(bf2f(wf[static_cast<int64_t>(dd) * Dcat + c]), ud, acc);
+  }
+  de[c] += acc;
+}
+
+}  // namespace
+
+size_t proj_bwd_ws_bytes(int M, int Dcat, int d, int n_kv, int num_cus) {
+  const int64_t Mp = (M + kRowPad - 1) / kRowPad * kRowPad;
+  size_t part = gemm_acc_ws_bytes(d, M, Dcat, num_cus);
+  part = std::max(part, gemm_acc_ws_bytes(n_kv, d, static_cast<int>(Mp), num_cus));
+  part = std::max(part, gemm_acc_ws_bytes(d, static_cast<int>(Mp), n_kv, num_cus));
+  part = std::max(part, gemm_acc_ws_bytes(d, Dcat, static_cast<int>(Mp), num_cus));
+  return static_cast<size_t>(2 * pb_up(d * 4) + pb_up(d * Mp * 4) + pb_up(Dcat * Mp * 2) +
+                             2 * pb_up(Mp * n_kv * 2) + 2 * pb_up(d * Mp * 2) +
+                             pb_up(static_cast<int64_t>(d) * n_kv * 2)) + part;
+}
+
+hipError_t launch_project_backward(const ProjBwdArgs& a, hipStream_t stream) {
+  if (a.M == 0) return hipSuccess;
+  const int n_kv = 2 * a.L * a.Hkv * a.hd;
+  const PbWs w = pb_ws(a.ws, a.M, a.Dcat, a.d, n_kv);
+  const int Mp = w.Mp;
+  hipError_t err;
+  if ((err = launch_fold_e(a.wf, a.e, a.d, a.Dcat, CO_DTYPE_BF16, w.fe, stream)) != hipSuccess)
+    return err;
+  auto transpose = [&](const void* src, int R, int C, int64_t src_ld, uint16_t* dst, int Rp,
+                       int64_t dst_ld) {
+    const dim3 grid((Rp + 63) / 64, (C + 63) / 64);
+    hipLaunchKernelGGL(pb_transpose_kernel, grid, dim3(256), 0, stream,
+                       static_cast<const uint16_t*>(src), R, C, src_ld, dst, Rp, dst_ld);
+  };
+  transpose(a.hidden, a.M, a.Dcat, a.Dcat, w.ht, Mp, Mp);       // H^T [Dcat][Mp]
+  transpose(a.wkv, n_kv, a.d, a.d, w.wkvt, n_kv, n_kv);          // W_KV^T [d][NKV]
+  const int64_t items = static_cast<int64_t>(a.L) * a.Hkv * (a.hd / 2) * Mp;
+  hipLaunchKernelGGL(pb_gather_kernel, dim3(static_cast<unsigned>((items + 255) / 256)), dim3(256),
+                     0, stream, a, w.djt, Mp);
+  transpose(w.djt, n_kv, Mp, Mp, w.dj, n_kv, n_kv);              // dJ [Mp][NKV]
+  // Z^T = F H^T (+ F E on carried rows)
+  if ((err = launch_gemm_acc(a.wf, a.hidden, a.d, a.M, a.Dcat, w.t32, false, w.part, a.num_cus,
+                             stream)) != hipSuccess)
+    return err;
+  const int64_t dm = static_cast<int64_t>(a.d) * Mp;
+  hipLaunchKernelGGL(pb_zt_kernel, dim3(static_cast<unsigned>((dm + 255) / 256)), dim3(256), 0,
+                     stream, w.t32, a.d, a.M, Mp, a.row_dst, w.fe, w.ztb);
+  // dW_KV += dJ^T Z
+  if ((err = launch_gemm_acc(w.djt, w.ztb, n_kv, a.d, Mp, a.dwkv, true, w.part, a.num_cus,
+                             stream)) != hipSuccess)
+    return err;
+  // dZ^T = W_KV^T dJ^T
+  if ((err = launch_gemm_acc(w.wkvt, w.dj, a.d, Mp, n_kv, w.t32, false, w.part, a.num_cus,
+                             stream)) != hipSuccess)
+    return err;
+  hipLaunchKernelGGL(pb_dz_kernel, dim3(a.d), dim3(256), 0, stream, w.t32, a.M, Mp, a.row_dst,
+                     w.dztb, w.u);
+  // dW_F += dZ^T H (+ u E^T), dE += F^T u
+  if ((err = launch_gemm_acc(w.dztb, w.ht, a.d, a.Dcat, Mp, a.dwf, true, w.part, a.num_cus,
+                             stream)) != hipSuccess)
+    return err;
+  hipLaunchKernelGGL(pb_e_kernel, dim3((a.Dcat + 255) / 256), dim3(256), 0, stream, a.dwf, a.de,
+                     w.u, static_cast<const uint16_t*>(a.e), static_cast<const uint16_t*>(a.wf),
+                     a.d, a.Dcat);
   return hipGetLastError();
 }
 

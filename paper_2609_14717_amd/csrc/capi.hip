@@ -147,6 +147,12 @@ size_t carryover_workspace_bytes(const co_dims* dims, int32_t which) {
     case CO_WS_PROJECT: return pw;
     case CO_WS_ATTENTION: return aw;
     case CO_WS_ROUND: return aw ? pw + aw : 0;   // projection scratch, then attention area
+    case CO_WS_PROJECT_BACKWARD:
+      return dims->dtype == CO_DTYPE_BF16
+                 ? proj_bwd_ws_bytes(dims->num_seqs * dims->block, dims->feat_dim, dims->model_dim,
+                                     2 * dims->num_layers * dims->num_kv_heads * dims->head_dim,
+                                     num_cus())
+                 : 0;
     case CO_WS_ATTENTION_BACKWARD:
       return bwd_workspace_bytes(dims->num_seqs, dims->num_layers, dims->num_kv_heads,
                                  dims->head_dim, dims->num_pages, carry_pages(dims));
@@ -299,6 +305,56 @@ co_status drafter_block_attention_backward(
   b.d_k_carry = d_k_carry;
   b.d_v_carry = d_v_carry;
   return hip_status(launch_attention_backward(b, stream));
+}
+
+co_status carryover_project_kv_backward(const co_dims* dims, const co_weights* w,
+                                        const void* hidden, const co_route* route,
+                                        const float* d_k_cache, const float* d_v_cache,
+                                        const float* d_k_carry, const float* d_v_carry,
+                                        float* d_w_f, float* d_w_kv, float* d_e_carry, void* ws,
+                                        size_t ws_bytes, hipStream_t stream) {
+  co_status s = check_dims(dims);
+  if (s != CO_OK) return s;
+  if (dims->dtype != CO_DTYPE_BF16) return CO_ERR_UNSUPPORTED;
+  if (!w || !w->w_f || !w->w_kv || !w->e_carry || !hidden || !route_ok(route) || !d_k_cache ||
+      !d_v_cache || !d_k_carry || !d_v_carry || !d_w_f || !d_w_kv || !d_e_carry)
+    return CO_ERR_INVALID_ARG;
+  if (w->w_f_carry || w->z_norm || w->k_norm) return CO_ERR_UNSUPPORTED;
+  if (!aligned(hidden, 16) || !aligned(w->w_f, 16) || !aligned(w->w_kv, 16) ||
+      !aligned(w->e_carry, 16) || !aligned(d_k_cache, 4) || !aligned(d_v_cache, 4) ||
+      !aligned(d_k_carry, 4) || !aligned(d_v_carry, 4) || !aligned(d_w_f, 4) ||
+      !aligned(d_w_kv, 4) || !aligned(d_e_carry, 4))
+    return CO_ERR_INVALID_ARG;
+  if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
+  if (ws_bytes < carryover_workspace_bytes(dims, CO_WS_PROJECT_BACKWARD)) return CO_ERR_WORKSPACE;
+  ProjBwdArgs a{};
+  a.M = dims->num_seqs * dims->block;
+  a.Dcat = dims->feat_dim;
+  a.d = dims->model_dim;
+  a.L = dims->num_layers;
+  a.Hkv = dims->num_kv_heads;
+  a.hd = dims->head_dim;
+  a.S = dims->num_seqs;
+  a.B = dims->block;
+  a.num_pages = dims->num_pages;
+  a.CP = carry_pages(dims);
+  a.num_cus = num_cus();
+  fill_rope_table(a.rope_inv, dims);
+  a.hidden = hidden;
+  a.wf = w->w_f;
+  a.wkv = w->w_kv;
+  a.e = w->e_carry;
+  a.row_dst = route->row_dst;
+  a.row_pos = route->row_pos;
+  a.dk = d_k_cache;
+  a.dv = d_v_cache;
+  a.dkc = d_k_carry;
+  a.dvc = d_v_carry;
+  a.dwf = d_w_f;
+  a.dwkv = d_w_kv;
+  a.de = d_e_carry;
+  a.ws = ws;
+  return hip_status(launch_project_backward(a, stream));
 }
 
 co_status drafter_carry_mass(const co_dims* dims, int32_t layer_begin, int32_t layer_count,

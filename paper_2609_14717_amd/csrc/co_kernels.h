@@ -113,6 +113,32 @@ struct BwdArgs {
 size_t bwd_workspace_bytes(int S, int L, int Hkv, int hd, int num_pages, int CP);
 hipError_t launch_attention_backward(const BwdArgs& b, hipStream_t stream);
 
+// Plain fp32 product C (+)= A . B^T of bf16 operands with K contiguous; the
+// K-split partials go to `part` (gemm_acc_ws_bytes).
+size_t gemm_acc_ws_bytes(int M, int N, int K, int num_cus);
+hipError_t launch_gemm_acc(const void* A, const void* B, int M, int N, int K, float* C,
+                           bool accumulate, float* part, int num_cus, hipStream_t stream);
+
+// Reverse mode of the K/V projection (bf16, plain update) for W_F, W_KV and
+// E_carry: the rows' K/V gradients are gathered from fp32 gradient caches by
+// the route's destinations.
+struct ProjBwdArgs {
+  int M, Dcat, d, L, Hkv, hd, S, B, num_pages, CP, num_cus;
+  double rope_inv[kMaxHeadDim / 2];
+  const void* hidden;
+  const void* wf;
+  const void* wkv;
+  const void* e;
+  const int32_t* row_dst;
+  const int32_t* row_pos;
+  const float *dk, *dv, *dkc, *dvc;   // gradient caches shaped like the caches
+  float *dwf, *dwkv, *de;             // accumulated
+  void* ws;
+};
+
+size_t proj_bwd_ws_bytes(int M, int Dcat, int d, int n_kv, int num_cus);
+hipError_t launch_project_backward(const ProjBwdArgs& p, hipStream_t stream);
+
 // Attention mass on the carried rows, from a finished attention call's LSE.
 constexpr int kMaxCarryRows = 64;   // carry rows of one sequence (block <= 64)
 

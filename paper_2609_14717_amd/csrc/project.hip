@@ -1308,6 +1308,55 @@ hipError_t launch_fold_e(const void* wf, const void* e, int d, int Dcat, int dty
   return hipGetLastError();
 }
 
+// ------------------------------------------------- plain products (backward)
+//
+// C[M][N] (fp32) = (accumulate ? C : 0) + A[M][K] . B[N][K]^T with bf16
+// operands whose K is contiguous (K a multiple of 64), through the MFMA kernels
+// above in K-split partial mode; the splits are summed in split order, so the
+// result is deterministic.
+
+namespace {
+
+__global__ __launch_bounds__(256) void sum_splits_kernel(const float* part, int splits, int64_t n,
+                                                         float* C, int accumulate) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= n) return;
+  float v = accumulate ? C[i] : 0.f;
+  for (int s = 0; s < splits; ++s) v += part[s * n + i];
+  C[i] = v;
+}
+
+}  // namespace
+
+size_t gemm_acc_ws_bytes(int M, int N, int K, int num_cus) {
+  int tile, split;
+  pick_gemm(M, N, K, false, 64, num_cus, &tile, &split);
+  return (static_cast<size_t>(split) * M * N * 4 + 255) / 256 * 256;
+}
+
+hipError_t launch_gemm_acc(const void* A, const void* B, int M, int N, int K, float* C,
+                           bool accumulate, float* part, int num_cus, hipStream_t stream) {
+  if (M == 0 || N == 0) return hipSuccess;
+  int tile, split;
+  pick_gemm(M, N, K, false, 64, num_cus, &tile, &split);
+  GemmArgs g{};
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.A = A;
+  g.B = B;
+  g.partial = part;
+  g.mode = kModePartial;
+  g.k_per_split = split_len(K, split, tile);
+  const int splits = (K + g.k_per_split - 1) / g.k_per_split;
+  hipError_t err = launch_gemm_bf16(g, tile, splits, stream);
+  if (err != hipSuccess) return err;
+  const int64_t n = static_cast<int64_t>(M) * N;
+  hipLaunchKernelGGL(sum_splits_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0,
+                     stream, part, splits, n, C, accumulate ? 1 : 0);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------ cache import
 
 template <typename T>

@@ -234,3 +234,21 @@ def test_attention_backward_arguments_checked_on_host():
     assert _rc(lambda: call(_dims(dtype="f32"))) == co.CO_ERR_UNSUPPORTED
     assert _rc(lambda: call(_dims(hd=128))) == co.CO_ERR_UNSUPPORTED
     assert _rc(lambda: call(_dims(Hq=8))) == co.CO_ERR_UNSUPPORTED   # 64 query rows per KV head
+
+
+def test_projection_backward_arguments_checked_on_host():
+    def call(dims, W, dwf=FAKE, wsb=1 << 30):
+        return co.carryover_project_kv_backward(dims, W, FAKE, _fake_route(), FAKE, FAKE, FAKE,
+                                                FAKE, dwf, FAKE, FAKE, FAKE, stream=0,
+                                                ws_bytes=wsb)
+
+    d = _dims()
+    W = co.weights(FAKE, FAKE, FAKE)
+    assert co.workspace_bytes(d, co.CO_WS_PROJECT_BACKWARD) > 0
+    assert _rc(lambda: call(d, W, dwf=None)) == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: call(d, W, wsb=16)) == co.CO_ERR_WORKSPACE
+    assert _rc(lambda: call(_dims(dtype="f32"), W)) == co.CO_ERR_UNSUPPORTED
+    for variant in (co.weights(FAKE, FAKE, FAKE, None, FAKE),
+                    co.weights(FAKE, FAKE, FAKE, None, None, FAKE),
+                    co.weights(FAKE, FAKE, FAKE, None, None, None, FAKE)):
+        assert _rc(lambda: call(d, variant)) == co.CO_ERR_UNSUPPORTED

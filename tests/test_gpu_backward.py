@@ -236,3 +236,74 @@ def test_backward_group_mismatch_sets_status():
                                         dkc, dvc, ws)
     torch.cuda.synchronize()
     assert co.carryover_read_status(sc.st) == co.CO_ERR_GROUP
+
+
+def test_projection_backward_train_layout():
+    """The whole training backward of the second pass: attention backward,
+    then the projection backward of the forward's two projection calls (the
+    recorded responses' committed rows, then the blocks' carried rows), summed
+    into dW_F, dW_KV and dE_carry; against the oracle's reverse modes."""
+    co = _gpu()
+    from helpers import OracleTrain
+    from synth.scenario import TrainScenario
+    from synth import device as sdev
+    w = TRAIN_SMALL
+    V, A = w.S * w.anchors, w.anchors
+    print(f"[backward] projection, workload={w.name} blocks={V}", flush=True)
+    sc = TrainScenario(w)
+    out, lse = sc.forward(shared_prefix=True)
+    dO_dev = sdev.materialise(w, wl.spec_dout(w, S=V), "cuda")
+    dk, dv, dkc, dvc = grad_buffers(sc.vst)
+    dq = torch.zeros(tuple(sc.q.shape), dtype=torch.float32, device="cuda")
+    ws = torch.zeros(co.workspace_bytes(sc.vdims, co.CO_WS_ATTENTION_BACKWARD) + 256,
+                     dtype=torch.uint8, device="cuda")
+    co.drafter_block_attention_backward(sc.vdims, 0, w.L, sc.q, sc.vst, out, lse, dO_dev, A, dq,
+                                        dk, dv, dkc, dvc, ws)
+    n_kv = 2 * w.L * w.Hkv * w.hd
+    dwf = torch.zeros((w.d, w.Dcat), dtype=torch.float32, device="cuda")
+    dwkv = torch.zeros((n_kv, w.d), dtype=torch.float32, device="cuda")
+    de = torch.zeros(w.Dcat, dtype=torch.float32, device="cuda")
+    for dims, hidden, rt in ((sc.dims, sc.h_committed, sc.crt), (sc.vdims, sc.hidden, sc.vrt)):
+        pws = torch.zeros(co.workspace_bytes(dims, co.CO_WS_PROJECT_BACKWARD) + 256,
+                          dtype=torch.uint8, device="cuda")
+        co.carryover_project_kv_backward(dims, sc.W, hidden, rt, dk, dv, dkc, dvc, dwf, dwkv, de,
+                                         pws)
+    torch.cuda.synchronize()
+    assert co.carryover_read_status(sc.vst) == 0
+
+    orc = OracleTrain(w, range(V))
+    Q = seq_block(w, wl.spec_q(w, 0, S=V), 1, range(V))
+    dO = host(w, wl.spec_dout(w, S=V))
+    _, com, car = oracle_grads(orc.st, Q, dO, w.Hq, w.theta, range(V), lambda v: v // A)
+    ref = [np.zeros((w.d, w.Dcat)), np.zeros((n_kv, w.d)), np.zeros(w.Dcat)]
+
+    def add(grads):
+        for i in range(3):
+            ref[i] += grads[i]
+
+    shape = (w.seq_len, w.L, w.Hkv, w.hd)
+    for s in range(w.S):   # committed rows of every response, positions 0..seq_len-1
+        h = host(w, wl.spec_hctx(w, s, 0, w.seq_len))
+        gk, gv = np.zeros(shape), np.zeros(shape)
+        n = com[s][0].shape[1]
+        gk[:n] = com[s][0].transpose(1, 0, 2, 3)
+        gv[:n] = com[s][1].transpose(1, 0, 2, 3)
+        add(oracle.project_backward(h, orc.E, np.zeros(w.seq_len, bool), orc.WF, orc.WKV,
+                                    np.arange(w.seq_len), w.L, w.Hkv, w.hd, w.theta, gk, gv))
+    H = host(w, wl.spec_h(w, 0, S=V))   # [V][B][Dcat]
+    rows, pos, gk, gv = [], [], [], []
+    for v in range(V):                  # carried rows of every block
+        for j in range(w.B):
+            dst = int(orc.rr["row_dst"][v][j])
+            if dst < 0 and dst != oracle.SKIP:
+                c = -1 - dst
+                rows.append(H[v, j])
+                pos.append(int(orc.rr["row_pos"][v][j]))
+                gk.append(car[v][0][:, c])
+                gv.append(car[v][1][:, c])
+    add(oracle.project_backward(np.array(rows), orc.E, np.ones(len(rows), bool), orc.WF, orc.WKV,
+                                np.array(pos), w.L, w.Hkv, w.hd, w.theta, np.array(gk),
+                                np.array(gv)))
+    for name, g, r in (("dW_F", dwf, ref[0]), ("dW_KV", dwkv, ref[1]), ("dE", de, ref[2])):
+        e = slab_close(to_np(g).reshape(1, -1), r.reshape(1, -1), name)
+        print(f"[backward] {name}: error {e:.3e} of the largest reference value", flush=True)
