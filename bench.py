@@ -661,6 +661,7 @@ def run_train(args, w):
     prows = w.S * w.seq_len + carried
     pflops, pbytes = projection_work(vw, prows)
     atfl = aflops / att_s / 1e12
+    backward = train_backward(torch, co, sc, w, stream, n, args, aflops, prows)
     calibrate_copy(torch, args)
     result = {
         "metric": f"training-shaped forwards/s ({w.name})",
@@ -688,8 +689,79 @@ def run_train(args, w):
                            call="carryover_project_kv x2 (committed rows; anchored blocks' rows)",
                            committed_call_us=pc_s * 1e6, block_call_us=pv_s * 1e6,
                            rows_computed=w.S * w.seq_len + V * w.B),
+        "backward": backward,
     }
     print(json.dumps(result), flush=True)
+
+
+def train_backward(torch, co, sc, w, stream, n, args, aflops, prows):
+    """The training side of the same pass (Algorithm 2): the attention backward
+    from a seeded output gradient (the blocks of a response share its pages:
+    one group per response), then the projection backward of both projection
+    calls; each timed alone, and whole training steps (forward + backward)."""
+    from synth import device as sdev
+    from synth import workloads as wl
+    V = w.S * w.anchors
+    d_out = sdev.materialise(w, wl.spec_dout(w, S=V), "cuda")
+    z = lambda t: torch.zeros(t.shape, dtype=torch.float32, device="cuda")
+    dk, dv, dkc, dvc = (z(sc.vst["k_cache"]), z(sc.vst["v_cache"]), z(sc.vst["k_carry"]),
+                        z(sc.vst["v_carry"]))
+    dq = torch.zeros(tuple(sc.q.shape), dtype=torch.float32, device="cuda")
+    n_kv = 2 * w.L * w.Hkv * w.hd
+    dwf = torch.zeros((w.d, w.Dcat), dtype=torch.float32, device="cuda")
+    dwkv = torch.zeros((n_kv, w.d), dtype=torch.float32, device="cuda")
+    de = torch.zeros(w.Dcat, dtype=torch.float32, device="cuda")
+    wsa = torch.zeros(co.workspace_bytes(sc.vdims, co.CO_WS_ATTENTION_BACKWARD),
+                      dtype=torch.uint8, device="cuda")
+    wsc = torch.zeros(co.workspace_bytes(sc.dims, co.CO_WS_PROJECT_BACKWARD),
+                      dtype=torch.uint8, device="cuda")
+    wsv = torch.zeros(co.workspace_bytes(sc.vdims, co.CO_WS_PROJECT_BACKWARD),
+                      dtype=torch.uint8, device="cuda")
+
+    def attn_bwd():
+        co.drafter_block_attention_backward(sc.vdims, 0, w.L, sc.q, sc.vst, sc.out, sc.lse, d_out,
+                                            w.anchors, dq, dk, dv, dkc, dvc, wsa)
+
+    def proj_bwd():
+        co.carryover_project_kv_backward(sc.dims, sc.W, sc.h_committed, sc.crt, dk, dv, dkc, dvc,
+                                         dwf, dwkv, de, wsc)
+        co.carryover_project_kv_backward(sc.vdims, sc.W, sc.hidden, sc.vrt, dk, dv, dkc, dvc,
+                                         dwf, dwkv, de, wsv)
+
+    sc.forward()
+    ab_s = timed_calls(torch, stream, n, attn_bwd, warm=TRAIN_ATTN_WARM)
+    pb_s = timed_calls(torch, stream, n, proj_bwd)
+    if co.carryover_read_status(sc.vst):
+        raise RuntimeError("device status after the backward")
+    steps = max(1, min(args.steps, 20))
+    for _ in range(2):
+        sc.forward()
+        attn_bwd()
+        proj_bwd()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        sc.forward()
+        attn_bwd()
+        proj_bwd()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    abfl = 2.5 * aflops                      # S, dP, dV, dK, dQ: 10 hd flops per (query, key)
+    pf, _ = projection_work(w.replace(S=V), prows)
+    pbfl = 2.0 * pf                          # Z again, dW_KV, dZ, dW_F
+    peak = MFMA_PEAK_TFLOPS[w.dtype]
+    return {"attention_call": "drafter_block_attention_backward (one group per response)",
+            "attention_call_us": ab_s * 1e6,
+            "attention_algorithmic_flops": abfl,
+            "attention_tflops": abfl / ab_s / 1e12,
+            "attention_mfma_frac": abfl / ab_s / 1e12 / peak,
+            "projection_call": "carryover_project_kv_backward x2 (committed rows; blocks' rows)",
+            "projection_us": pb_s * 1e6,
+            "projection_algorithmic_flops": pbfl,
+            "projection_tflops": pbfl / pb_s / 1e12,
+            "projection_mfma_frac": pbfl / pb_s / 1e12 / peak,
+            "train_steps_per_s": steps / dt,
+            "train_step_ms": dt * 1e3 / steps}
 
 
 if __name__ == "__main__":

@@ -9,9 +9,10 @@ reverse mode (itself pinned by finite differences):
   contexts, an empty sequence, a sequence with carry rows only, padded query
   rows (8 block rows x 2 heads) and a layer sub-range.
 
-Gradients are compared per head vector against the oracle, relative to the
-largest reference vector of the same (layer, KV head) slab: the GPU rounds the
-softmax weights and dS to bf16 before its products, as the forward rounds P.
+Gradients are compared against the oracle relative to the largest reference
+value of the same (layer, KV head) slab, at 3e-2: the backward's weights P
+carry the forward's rounding (bf16 rotated queries, the bf16 output in D), and
+it rounds P and dS to bf16 before three further products.
 """
 import numpy as np
 import pytest
@@ -25,7 +26,7 @@ torch = pytest.importorskip("torch")
 
 from helpers import OracleRun, host, seq_block, to_np  # noqa: E402
 
-GTOL = 2e-2
+GTOL = 3e-2
 
 TRAIN_SMALL = wl.TRAIN_FWD.replace(name="bwd_train_small", S=2, seq_len=512, anchors=10,
                                    seed=0x5EED30)
@@ -40,6 +41,9 @@ def _gpu():
     return co
 
 
+WORST = []
+
+
 def slab_close(g, r, what, tol=GTOL):
     """g, r [n][hd] of one (layer, KV head): every head vector within tol of
     the slab's largest reference vector."""
@@ -50,6 +54,7 @@ def slab_close(g, r, what, tol=GTOL):
         return 0.0
     scale = max(np.abs(r).max(), 1e-30)
     e = float(np.abs(g - r).max() / scale)
+    WORST.append((e, what))
     assert e <= tol, f"{what}: max error {e:.3e} of the slab's largest value > {tol}"
     return e
 
@@ -150,7 +155,10 @@ def check(co, dims, st, q, out, lse, dO_dev, group, orc_st, Q, dO, w, seqs, grou
             for g in range(w.Hkv):
                 errs.append(slab_close(gk[:, g], rk[layer, :, g], f"{tag} dk group {grp} g{g}"))
                 errs.append(slab_close(gv[:, g], rv[layer, :, g], f"{tag} dv group {grp} g{g}"))
-    print(f"[backward] {tag}: max slab error {max(errs):.3e} over {len(errs)} slabs", flush=True)
+    print(f"[backward] {tag}: max slab error {max(errs):.3e} over {len(errs)} slabs; worst: "
+          + ", ".join(f"{n} {e:.2e}" for e, n in sorted(WORST)[-3:]), flush=True)
+    WORST.clear()
+    return errs
 
 
 def test_backward_train_layout():
@@ -170,6 +178,29 @@ def test_backward_train_layout():
     dO = host(w, wl.spec_dout(w, S=V))
     check(co, sc.vdims, sc.vst, sc.q, out, lse, dO_dev, A, orc.st, Q, dO, w, list(range(V)),
           lambda v: v // A, {r: r * A for r in range(w.S)}, tag="train")
+
+
+def test_backward_train_full_size_sampled():
+    """The training layout at full size (8 responses x 4096 positions, 2048
+    anchored blocks), as the bench runs it: every block of response 0 against
+    the oracle, including the sums over its 256 blocks of the shared keys."""
+    co = _gpu()
+    from helpers import OracleTrain
+    from synth.scenario import TrainScenario
+    from synth import device as sdev
+    w = wl.TRAIN_FWD
+    V, A = w.S * w.anchors, w.anchors
+    print(f"[backward] workload={w.name} blocks={V}, response 0 checked", flush=True)
+    sc = TrainScenario(w)
+    out, lse = sc.forward(shared_prefix=True)
+    dO_dev = sdev.materialise(w, wl.spec_dout(w, S=V), "cuda")
+    torch.cuda.synchronize()
+    sample = list(range(A))
+    orc = OracleTrain(w, sample)
+    Q = seq_block(w, wl.spec_q(w, 0, S=V), 1, sample)
+    dO = seq_block(w, wl.spec_dout(w, S=V), 1, sample)
+    check(co, sc.vdims, sc.vst, sc.q, out, lse, dO_dev, A, orc.st, Q, dO, w, sample,
+          lambda v: v // A, {0: 0}, tag="train full")
 
 
 def test_backward_serving_layout():
