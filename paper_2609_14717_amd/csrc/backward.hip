@@ -11,7 +11,8 @@
 // training layout: consecutive sequences of a group read the same page row),
 // so their gradients are sums over the group's blocks.
 //
-// Four kernels, all on v_mfma_f32_32x32x16_bf16 (bf16 operands, fp32 sums):
+// Five kernels; the products run on v_mfma_f32_32x32x16_bf16 (bf16 operands,
+// fp32 sums):
 //   prep   per (layer, KV head, sequence): the rotated, scaled queries (log2
 //          units, as the forward forms them) and their transpose, dO packed
 //          and transposed, the forward's LSE in log2 units and D;
@@ -25,8 +26,9 @@
 //          in the operand layout of dV^T = dO^T P and dK^T = (R q)^T dS;
 //   dq     one wavefront per (layer, KV head, sequence): S^T = K Q^T over all of
 //          the sequence's tiles (keys permuted the same way), dQ^T += K^T dS^T,
-//          then the rotation is undone; its carry tile also runs the dkv step,
-//          since carry keys belong to one sequence.
+//          then the rotation is undone;
+//   carry  carry keys belong to one sequence: their tiles take the dkv step
+//          against that sequence alone.
 // Keys masked in the forward (past ctx_len or carry_len, rejected page ids)
 // get no gradient and contribute none.
 #include <algorithm>
@@ -229,53 +231,62 @@ struct KeyGrad {
       for (int r = 0; r < 16; ++r) dkt[m][r] = dvt[m][r] = 0.f;
   }
 
-  __device__ void step(const BwdWs& w, int64_t qbase, const u16x8 (&kb)[KS], const u16x8 (&vb)[KS],
-                       int n0, int n1, int lane) {
-    const int r32 = lane & 31, h = lane >> 5;
-    const int qp = perm23(r32);
-    const uint16_t* qr = w.qr + (qbase + qp) * HD + 8 * h;
-    const uint16_t* dn = w.don + (qbase + qp) * HD + 8 * h;
-    u16x8 qa[KS], da[KS];
+  // One sequence's operands of the step: its query rows (permuted) and dO
+  // as A-fragments, their transposes, and the LSE / D of the 16 query rows
+  // this lane's accumulator registers hold.
+  struct Block {
+    u16x8 qa[KS], da[KS], qt[MT][2], dt[MT][2];
+    float l2[16], dd[16];
+    int n0, n1;   // valid keys of the tile's two pages for this sequence
+
+    __device__ void load(const BwdWs& w, int64_t qbase, int lane) {
+      const int r32 = lane & 31, h = lane >> 5;
+      const int qp = perm23(r32);
+      const uint16_t* qr = w.qr + (qbase + qp) * HD + 8 * h;
+      const uint16_t* dn = w.don + (qbase + qp) * HD + 8 * h;
 #pragma unroll
-    for (int k = 0; k < KS; ++k) {
-      qa[k] = *reinterpret_cast<const u16x8*>(qr + 16 * k);
-      da[k] = *reinterpret_cast<const u16x8*>(dn + 16 * k);
-    }
-    // transposed operands: lane dim = 32 m + l % 32, rows 16 j + 8 h ..
-    u16x8 qt[MT][2], dt[MT][2];
+      for (int k = 0; k < KS; ++k) {
+        qa[k] = *reinterpret_cast<const u16x8*>(qr + 16 * k);
+        da[k] = *reinterpret_cast<const u16x8*>(dn + 16 * k);
+      }
+      // transposed operands: lane dim = 32 m + l % 32, rows 16 j + 8 h ..
 #pragma unroll
-    for (int m = 0; m < MT; ++m)
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int64_t off = qbase * HD + static_cast<int64_t>(32 * m + r32) * kNqp + 16 * j + 8 * h;
+          qt[m][j] = *reinterpret_cast<const u16x8*>(w.qrt + off);
+          dt[m][j] = *reinterpret_cast<const u16x8*>(w.dot + off);
+        }
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        const int64_t off = qbase * HD + static_cast<int64_t>(32 * m + r32) * kNqp + 16 * j + 8 * h;
-        qt[m][j] = *reinterpret_cast<const u16x8*>(w.qrt + off);
-        dt[m][j] = *reinterpret_cast<const u16x8*>(w.dot + off);
-      }
-    float l2[16], dd[16];
+        const f32x4 a0 = *reinterpret_cast<const f32x4*>(w.lse2 + qbase + 16 * j + 8 * h);
+        const f32x4 a1 = *reinterpret_cast<const f32x4*>(w.lse2 + qbase + 16 * j + 8 * h + 4);
+        const f32x4 b0 = *reinterpret_cast<const f32x4*>(w.dd + qbase + 16 * j + 8 * h);
+        const f32x4 b1 = *reinterpret_cast<const f32x4*>(w.dd + qbase + 16 * j + 8 * h + 4);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const f32x4 a0 = *reinterpret_cast<const f32x4*>(w.lse2 + qbase + 16 * j + 8 * h);
-      const f32x4 a1 = *reinterpret_cast<const f32x4*>(w.lse2 + qbase + 16 * j + 8 * h + 4);
-      const f32x4 b0 = *reinterpret_cast<const f32x4*>(w.dd + qbase + 16 * j + 8 * h);
-      const f32x4 b1 = *reinterpret_cast<const f32x4*>(w.dd + qbase + 16 * j + 8 * h + 4);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        l2[8 * j + e] = a0[e];
-        l2[8 * j + 4 + e] = a1[e];
-        dd[8 * j + e] = b0[e];
-        dd[8 * j + 4 + e] = b1[e];
+        for (int e = 0; e < 4; ++e) {
+          l2[8 * j + e] = a0[e];
+          l2[8 * j + 4 + e] = a1[e];
+          dd[8 * j + e] = b0[e];
+          dd[8 * j + 4 + e] = b1[e];
+        }
       }
     }
+  };
+
+  __device__ void compute(const Block& q, const u16x8 (&kb)[KS], const u16x8 (&vb)[KS], int lane) {
+    const int r32 = lane & 31;
     f32x16 sc, dp;
 #pragma unroll
     for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.f;
 #pragma unroll
     for (int k = 0; k < KS; ++k) {
-      sc = mfma32x32x16(qa[k], kb[k], sc);
-      dp = mfma32x32x16(da[k], vb[k], dp);
+      sc = mfma32x32x16(q.qa[k], kb[k], sc);
+      dp = mfma32x32x16(q.da[k], vb[k], dp);
     }
     const int key = r32;   // this lane's column
-    const bool valid = key < 16 ? key < n0 : key - 16 < n1;
+    const bool valid = key < 16 ? key < q.n0 : key - 16 < q.n1;
     u16x8 pb[2], sb[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
@@ -283,9 +294,9 @@ struct KeyGrad {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int r = 8 * j + e;
-        const float pr = valid ? __builtin_amdgcn_exp2f(sc[r] - l2[r]) : 0.f;
+        const float pr = valid ? __builtin_amdgcn_exp2f(sc[r] - q.l2[r]) : 0.f;
         pv[e] = pr;
-        sv[e] = pr * (dp[r] - dd[r]);
+        sv[e] = pr * (dp[r] - q.dd[r]);
       }
       typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
       const u32x4v p4 = {cvt_pk_bf16(pv[0], pv[1]), cvt_pk_bf16(pv[2], pv[3]),
@@ -299,9 +310,18 @@ struct KeyGrad {
     for (int m = 0; m < MT; ++m)
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        dvt[m] = mfma32x32x16(dt[m][j], pb[j], dvt[m]);
-        dkt[m] = mfma32x32x16(qt[m][j], sb[j], dkt[m]);
+        dvt[m] = mfma32x32x16(q.dt[m][j], pb[j], dvt[m]);
+        dkt[m] = mfma32x32x16(q.qt[m][j], sb[j], dkt[m]);
       }
+  }
+
+  __device__ void step(const BwdWs& w, int64_t qbase, const u16x8 (&kb)[KS], const u16x8 (&vb)[KS],
+                       int n0, int n1, int lane) {
+    Block q;
+    q.load(w, qbase, lane);
+    q.n0 = n0;
+    q.n1 = n1;
+    compute(q, kb, vb, lane);
   }
 
   // dK (x ln 2: the queries were in log2 units) and dV of the tile's valid keys
@@ -341,6 +361,18 @@ __device__ __forceinline__ void tile_frags(const uint16_t* k0, const uint16_t* k
   }
 }
 
+// Workgroups are dealt to the 8 XCDs round-robin.  Work items come in pairs
+// (group, layer x KV head) whose items read the same data (the group's
+// queries, or the keys of its page row); every pair is given to one XCD, its
+// items on consecutive ids there, so that they share that XCD's L2.  Returns
+// false for the padding ids of the launch (8 * ceil(n_pairs / 8) * per ids).
+__device__ __forceinline__ bool xcd_item(int n_pairs, int per, int* pair, int* item) {
+  const int i = blockIdx.x, xcd = i & 7, k = i >> 3;
+  *pair = xcd + 8 * (k / per);
+  *item = k % per;
+  return *pair < n_pairs;
+}
+
 __device__ __forceinline__ bool len_ok(const AttnArgs& a, int ctx, int carry) {
   return ctx >= 0 && ctx <= a.max_pages * kPage && carry >= 0 && carry <= a.CP * kPage;
 }
@@ -351,11 +383,14 @@ __device__ __forceinline__ bool len_ok(const AttnArgs& a, int ctx, int carry) {
 // wavefront.  The group's first sequence holds the page row; a tile no block
 // of the group reaches is skipped.
 template <int HD>
-__global__ __launch_bounds__(64) void bwd_dkv_kernel(BwdArgs b) {
+__global__ __launch_bounds__(64, 1) void bwd_dkv_kernel(BwdArgs b) {
   const AttnArgs& a = b.a;
   const BwdWs w = bwd_ws(b);
   const int lane = threadIdx.x;
-  const int tile = blockIdx.x, grp = blockIdx.y, seg = blockIdx.z;
+  const int groups = (a.S + b.group - 1) / b.group, tiles = (a.max_pages + 1) / 2;
+  int pair, tile;
+  if (!xcd_item(groups * b.layer_count * a.Hkv, tiles, &pair, &tile)) return;
+  const int grp = pair % groups, seg = pair / groups;
   const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
   const int s0 = grp * b.group, s1 = min(a.S, s0 + b.group);
   const int kbase = 32 * tile;
@@ -385,12 +420,63 @@ __global__ __launch_bounds__(64) void bwd_dkv_kernel(BwdArgs b) {
   tile_frags<HD>(kc + c0, kc + c1, w.vn + w0, w.vn + w1, lane, kb, vb);
   KeyGrad<HD> kg;
   kg.zero();
-  for (int s = s0; s < s1; ++s) {
-    const int ctx = a.ctx_len[s], carry = a.carry_len[s];
-    if (!len_ok(a, ctx, carry) || ctx <= kbase) continue;
-    const int n0 = bad0 ? 0 : min(kPage, ctx - kbase);
-    const int n1 = bad1 ? 0 : max(0, min(kPage, ctx - kbase - kPage));
-    kg.step(w, (static_cast<int64_t>(seg) * a.S + s) * kNqp, kb, vb, n0, n1, lane);
+  // The group's sequences that see the tile, walked from the last one down (it
+  // sees the most keys, so every tile of the group starts on the same
+  // sequence and the XCD's tiles read the same operands at about the same
+  // time), 64 at a time as a lane mask; operands are loaded two sequences ahead
+  // of the one being computed.
+  const int none = s0 - 1;
+  uint64_t mask = 0;
+  int mbase = s1, mctx = 0;
+  auto prev = [&](int x) {   // last sequence <= x that sees the tile, or none
+    for (;;) {
+      if (x < s0) return none;
+      if (x < mbase) {
+        const int top = x;
+        mbase = max(s0, x - 63);
+        const int y = mbase + lane;
+        bool v = false;
+        mctx = 0;
+        if (y <= top) {
+          const int ctx = a.ctx_len[y], carry = a.carry_len[y];
+          v = len_ok(a, ctx, carry) && ctx > kbase;
+          mctx = ctx;
+        }
+        mask = __ballot(v);
+      }
+      const int off = x - mbase;
+      const uint64_t m = mask & (off == 63 ? ~0ull : ((1ull << (off + 1)) - 1));
+      if (m) return mbase + 63 - static_cast<int>(__builtin_clzll(m));
+      x = mbase - 1;
+    }
+  };
+  using Blk = typename KeyGrad<HD>::Block;
+  auto fetch = [&](Blk& q, int s) {
+    const int ctx = __builtin_amdgcn_readlane(mctx, s - mbase);
+    q.n0 = bad0 ? 0 : min(kPage, ctx - kbase);
+    q.n1 = bad1 ? 0 : max(0, min(kPage, ctx - kbase - kPage));
+    q.load(w, (static_cast<int64_t>(seg) * a.S + s) * kNqp, lane);
+  };
+  Blk qa, qb, qc;
+  int sa = prev(s1 - 1), sb = none, sc2 = none;
+  if (sa != none) {
+    fetch(qa, sa);
+    sb = prev(sa - 1);
+    if (sb != none) fetch(qb, sb);
+  }
+  while (sa != none) {   // three buffers in rotation, unrolled so that none is copied
+    sc2 = sb != none ? prev(sb - 1) : none;
+    if (sc2 != none) fetch(qc, sc2);
+    kg.compute(qa, kb, vb, lane);
+    if (sb == none) break;
+    sa = sc2 != none ? prev(sc2 - 1) : none;
+    if (sa != none) fetch(qa, sa);
+    kg.compute(qb, kb, vb, lane);
+    if (sc2 == none) break;
+    sb = sa != none ? prev(sa - 1) : none;
+    if (sb != none) fetch(qb, sb);
+    kg.compute(qc, kb, vb, lane);
+    if (sa == none) break;
   }
   // every key of the tile that some block sees (keys past `reach` keep no gradient)
   const int m0 = bad0 ? 0 : min(kPage, reach - kbase);
@@ -399,18 +485,58 @@ __global__ __launch_bounds__(64) void bwd_dkv_kernel(BwdArgs b) {
   kg.store(b.d_k_cache + o0, b.d_k_cache + o1, b.d_v_cache + o0, b.d_v_cache + o1, m0, m1, lane);
 }
 
+// ----------------------------------------------------------- dkv, carry
+//
+// grid (S, layer_count * Hkv), one wavefront: the carry keys belong to one
+// sequence, so their tiles take the dkv step against that sequence alone.
+template <int HD>
+__global__ __launch_bounds__(64, 2) void bwd_dkv_carry_kernel(BwdArgs b) {
+  const AttnArgs& a = b.a;
+  const BwdWs w = bwd_ws(b);
+  const int lane = threadIdx.x;
+  const int s = blockIdx.x, seg = blockIdx.y;
+  const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
+  const int ctx = a.ctx_len[s], carry = a.carry_len[s];
+  if (!len_ok(a, ctx, carry) || carry == 0) return;
+  const int64_t pe = static_cast<int64_t>(kPage) * HD;
+  const int64_t lay = static_cast<int64_t>(a.layer_begin + layer_local);
+  const int ncp = (carry + kPage - 1) / kPage;
+  const uint16_t* kk = static_cast<const uint16_t*>(a.k_carry);
+  const int64_t qbase = (static_cast<int64_t>(seg) * a.S + s) * kNqp;
+  for (int cp0 = 0; cp0 < ncp; cp0 += 2) {
+    const int cp1 = min(cp0 + 1, ncp - 1);
+    const int n0 = min(kPage, carry - cp0 * kPage);
+    const int n1 = cp0 + 1 < ncp ? min(kPage, carry - (cp0 + 1) * kPage) : 0;
+    const int64_t r0 = ((lay * a.S + s) * a.CP + cp0) * a.Hkv + g;
+    const int64_t r1 = ((lay * a.S + s) * a.CP + cp1) * a.Hkv + g;
+    const int64_t q0 = ((static_cast<int64_t>(layer_local) * a.S + s) * a.CP + cp0) * a.Hkv + g;
+    const int64_t q1 = ((static_cast<int64_t>(layer_local) * a.S + s) * a.CP + cp1) * a.Hkv + g;
+    u16x8 kb[HD / 16], vb[HD / 16];
+    tile_frags<HD>(kk + r0 * pe, kk + r1 * pe, w.vnc + q0 * pe, w.vnc + q1 * pe, lane, kb, vb);
+    KeyGrad<HD> kg;
+    kg.zero();
+    kg.step(w, qbase, kb, vb, n0, n1, lane);
+    kg.store(b.d_k_carry + r0 * pe, b.d_k_carry + r1 * pe, b.d_v_carry + r0 * pe,
+             b.d_v_carry + r1 * pe, n0, n1, lane);
+  }
+}
+
 // -------------------------------------------------------------------- dq
 //
 // grid (S, layer_count * Hkv), one wavefront: the sequence's committed tiles
 // through its page row, then its carry tiles.  Keys are the MFMA rows here
 // (permuted), query rows the columns: lane l keeps query l % 32 throughout.
 template <int HD>
-__global__ __launch_bounds__(64) void bwd_dq_kernel(BwdArgs b) {
+__global__ __launch_bounds__(64, 4) void bwd_dq_kernel(BwdArgs b) {
   constexpr int KS = HD / 16, MT = HD / 32;
   const AttnArgs& a = b.a;
   const BwdWs w = bwd_ws(b);
   const int lane = threadIdx.x, r32 = lane & 31, h = lane >> 5;
-  const int s = blockIdx.x, seg = blockIdx.y;
+  const int groups = (a.S + b.group - 1) / b.group;
+  int pair, item;
+  if (!xcd_item(groups * b.layer_count * a.Hkv, b.group, &pair, &item)) return;
+  const int s = (pair % groups) * b.group + item, seg = pair / groups;
+  if (s >= a.S) return;
   const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
   const int G = a.Hq / a.Hkv, nq = a.B * G;
   const int ctx_raw = a.ctx_len[s], carry_raw = a.carry_len[s];
@@ -522,18 +648,6 @@ __global__ __launch_bounds__(64) void bwd_dq_kernel(BwdArgs b) {
 #pragma unroll
       for (int jj = 0; jj < 2; ++jj) dqt[m] = mfma32x32x16(kt[m][jj], sb[jj], dqt[m]);
 
-    if (!com) {   // carry keys belong to this sequence alone: their dK, dV here
-      u16x8 kb[KS], vb[KS];
-      tile_frags<HD>(k0, k1, v0, v1, lane, kb, vb);
-      KeyGrad<HD> kg;
-      kg.zero();
-      kg.step(w, qbase, kb, vb, n0, n1, lane);
-      const int cp0 = 2 * (j - nct);
-      const int64_t d0 = (((lay * a.S + s) * a.CP + cp0) * a.Hkv + g) * pe;
-      const int64_t d1 = (((lay * a.S + s) * a.CP + min(cp0 + 1, a.CP - 1)) * a.Hkv + g) * pe;
-      kg.store(b.d_k_carry + d0, b.d_k_carry + d1, b.d_v_carry + d0, b.d_v_carry + d1, n0, n1,
-               lane);
-    }
   }
   // dq = R^T (dS K) / sqrt(hd): dims i and i + hd/2 sit in the same register of tiles m and m + MT/2
   const int qn = r32;
@@ -583,8 +697,10 @@ hipError_t launch_attention_backward(const BwdArgs& b, hipStream_t stream) {
                      dim3(256), 0, stream, b);
   const int groups = (a.S + b.group - 1) / b.group;
   const int tiles = (a.max_pages + 1) / 2;
-  hipLaunchKernelGGL(bwd_dkv_kernel<64>, dim3(tiles, groups, nseg), dim3(64), 0, stream, b);
-  hipLaunchKernelGGL(bwd_dq_kernel<64>, dim3(a.S, nseg), dim3(64), 0, stream, b);
+  const int xpairs = (groups * nseg + 7) / 8 * 8;   // pairs per launch, padded to the 8 XCDs
+  hipLaunchKernelGGL(bwd_dkv_kernel<64>, dim3(xpairs * tiles), dim3(64), 0, stream, b);
+  hipLaunchKernelGGL(bwd_dkv_carry_kernel<64>, dim3(a.S, nseg), dim3(64), 0, stream, b);
+  hipLaunchKernelGGL(bwd_dq_kernel<64>, dim3(xpairs * b.group), dim3(64), 0, stream, b);
   return hipGetLastError();
 }
 
@@ -607,7 +723,7 @@ namespace {
 constexpr int kRowPad = 256;
 
 struct PbWs {
-  float *fe, *u, *t32, *part;
+  float *fe, *u, *upart, *t32, *part;
   uint16_t *ht, *dj, *djt, *ztb, *dztb, *wkvt;
   int Mp;
 };
@@ -621,6 +737,7 @@ PbWs pb_ws(void* ws, int M, int Dcat, int d, int n_kv) {
   char* p = static_cast<char*>(ws);
   w.fe = reinterpret_cast<float*>(p); p += pb_up(d * 4);
   w.u = reinterpret_cast<float*>(p); p += pb_up(d * 4);
+  w.upart = reinterpret_cast<float*>(p); p += pb_up(d * (Mp / 2048 + 1) * 4);
   w.t32 = reinterpret_cast<float*>(p); p += pb_up(d * Mp * 4);
   w.ht = reinterpret_cast<uint16_t*>(p); p += pb_up(Dcat * Mp * 2);
   w.dj = reinterpret_cast<uint16_t*>(p); p += pb_up(Mp * n_kv * 2);
@@ -718,45 +835,75 @@ __global__ __launch_bounds__(256) void pb_zt_kernel(const float* t32, int d, int
   ztb[idx] = f2bf(v);
 }
 
-// dZ^T (fp32 [d][Mp]) -> bf16, and u[dd] = its sum over the carried rows; one
-// workgroup per dd.
+// dZ^T (fp32 [d][Mp]) -> bf16, and per (dd, chunk of 2048 rows) the sum over
+// its carried rows (summed over chunks in pb_u_kernel): 8 rows per thread.
+constexpr int kDzChunk = 2048;
+
 __global__ __launch_bounds__(256) void pb_dz_kernel(const float* t32, int M, int Mp,
                                                     const int32_t* row_dst, uint16_t* dztb,
-                                                    float* u) {
+                                                    float* upart) {
   __shared__ float red[4];
-  const int dd = blockIdx.x;
-  const float* src = t32 + static_cast<int64_t>(dd) * Mp;
-  uint16_t* dst = dztb + static_cast<int64_t>(dd) * Mp;
+  const int dd = blockIdx.x, ch = blockIdx.y;
+  const int r0 = ch * kDzChunk + threadIdx.x * 8;
   float acc = 0.f;
-  for (int r = threadIdx.x; r < Mp; r += 256) {
-    const float v = src[r];
-    dst[r] = f2bf(v);
-    if (r < M) {
-      const int32_t x = row_dst[r];
-      if (x < 0 && x != kSkip) acc += v;
+  if (r0 < Mp) {
+    const float* src = t32 + static_cast<int64_t>(dd) * Mp + r0;
+    const f32x4 a = *reinterpret_cast<const f32x4*>(src);
+    const f32x4 b = *reinterpret_cast<const f32x4*>(src + 4);
+    u16x8 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      o[e] = f2bf(a[e]);
+      o[4 + e] = f2bf(b[e]);
+    }
+    *reinterpret_cast<u16x8*>(dztb + static_cast<int64_t>(dd) * Mp + r0) = o;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int r = r0 + e;
+      if (r < M) {
+        const int32_t x = row_dst[r];
+        if (x < 0 && x != kSkip) acc += e < 4 ? a[e] : b[e - 4];
+      }
     }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
   __syncthreads();
-  if (threadIdx.x == 0) u[dd] = (red[0] + red[1]) + (red[2] + red[3]);
+  if (threadIdx.x == 0) upart[dd * gridDim.y + ch] = (red[0] + red[1]) + (red[2] + red[3]);
 }
 
-// dW_F[dd][c] += u[dd] E[c]; dE[c] += sum_dd W_F[dd][c] u[dd].
-__global__ __launch_bounds__(256) void pb_e_kernel(float* dwf, float* de, const float* u,
-                                                   const uint16_t* e, const uint16_t* wf, int d,
-                                                   int Dcat) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= Dcat) return;
-  const float ec = bf2f(e[c]);
+// u[dd] = sum of the chunk sums, in chunk order.
+__global__ __launch_bounds__(256) void pb_u_kernel(const float* upart, int chunks, int d, float* u) {
+  const int dd = blockIdx.x * 256 + threadIdx.x;
+  if (dd >= d) return;
+  float v = 0.f;
+  for (int c = 0; c < chunks; ++c) v += upart[dd * chunks + c];
+  u[dd] = v;
+}
+
+// dW_F[dd][c] += u[dd] E[c], one element per thread.
+__global__ __launch_bounds__(256) void pb_dwf_e_kernel(float* dwf, const float* u,
+                                                       const uint16_t* e, int d, int Dcat) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= static_cast<int64_t>(d) * Dcat) return;
+  dwf[i] += u[i / Dcat] * bf2f(e[i % Dcat]);
+}
+
+// dE[c] += sum_dd W_F[dd][c] u[dd]: 64 columns per workgroup, the four
+// wavefronts take interleaved dd and are summed in a fixed order.
+__global__ __launch_bounds__(256) void pb_de_kernel(float* de, const float* u, const uint16_t* wf,
+                                                    int d, int Dcat) {
+  __shared__ float part[4][64];
+  const int c = blockIdx.x * 64 + (threadIdx.x & 63), wv = threadIdx.x >> 6;
   float acc = 0.f;
-  for (int dd = 0; dd < d; ++dd) {
-    const float ud = u[dd];
-    dwf[static_cast<int64_t>(dd) * Dcat + c] += ud * ec;
-    acc = fmaf(bf2f(wf[static_cast<int64_t>(dd) * Dcat + c]), ud, acc);
-  }
-  de[c] += acc;
+  if (c < Dcat)
+    for (int dd = wv; dd < d; dd += 4)
+      acc = fmaf(bf2f(wf[static_cast<int64_t>(dd) * Dcat + c]), u[dd], acc);
+  part[wv][threadIdx.x & 63] = acc;
+  __syncthreads();
+  if (wv == 0 && c < Dcat)
+    de[c] += (part[0][threadIdx.x] + part[1][threadIdx.x]) + (part[2][threadIdx.x] + part[3][threadIdx.x]);
 }
 
 }  // namespace
@@ -767,7 +914,8 @@ size_t proj_bwd_ws_bytes(int M, int Dcat, int d, int n_kv, int num_cus) {
   part = std::max(part, gemm_acc_ws_bytes(n_kv, d, static_cast<int>(Mp), num_cus));
   part = std::max(part, gemm_acc_ws_bytes(d, static_cast<int>(Mp), n_kv, num_cus));
   part = std::max(part, gemm_acc_ws_bytes(d, Dcat, static_cast<int>(Mp), num_cus));
-  return static_cast<size_t>(2 * pb_up(d * 4) + pb_up(d * Mp * 4) + pb_up(Dcat * Mp * 2) +
+  return static_cast<size_t>(2 * pb_up(d * 4) + pb_up(d * (Mp / 2048 + 1) * 4) +
+                             pb_up(d * Mp * 4) + pb_up(Dcat * Mp * 2) +
                              2 * pb_up(Mp * n_kv * 2) + 2 * pb_up(d * Mp * 2) +
                              pb_up(static_cast<int64_t>(d) * n_kv * 2)) + part;
 }
@@ -807,15 +955,20 @@ hipError_t launch_project_backward(const ProjBwdArgs& a, hipStream_t stream) {
   if ((err = launch_gemm_acc(w.wkvt, w.dj, a.d, Mp, n_kv, w.t32, false, w.part, a.num_cus,
                              stream)) != hipSuccess)
     return err;
-  hipLaunchKernelGGL(pb_dz_kernel, dim3(a.d), dim3(256), 0, stream, w.t32, a.M, Mp, a.row_dst,
-                     w.dztb, w.u);
+  const int chunks = (Mp + kDzChunk - 1) / kDzChunk;
+  hipLaunchKernelGGL(pb_dz_kernel, dim3(a.d, chunks), dim3(256), 0, stream, w.t32, a.M, Mp,
+                     a.row_dst, w.dztb, w.upart);
+  hipLaunchKernelGGL(pb_u_kernel, dim3((a.d + 255) / 256), dim3(256), 0, stream, w.upart, chunks,
+                     a.d, w.u);
   // dW_F += dZ^T H (+ u E^T), dE += F^T u
   if ((err = launch_gemm_acc(w.dztb, w.ht, a.d, a.Dcat, Mp, a.dwf, true, w.part, a.num_cus,
                              stream)) != hipSuccess)
     return err;
-  hipLaunchKernelGGL(pb_e_kernel, dim3((a.Dcat + 255) / 256), dim3(256), 0, stream, a.dwf, a.de,
-                     w.u, static_cast<const uint16_t*>(a.e), static_cast<const uint16_t*>(a.wf),
-                     a.d, a.Dcat);
+  const int64_t nf = static_cast<int64_t>(a.d) * a.Dcat;
+  hipLaunchKernelGGL(pb_dwf_e_kernel, dim3(static_cast<unsigned>((nf + 255) / 256)), dim3(256), 0,
+                     stream, a.dwf, w.u, static_cast<const uint16_t*>(a.e), a.d, a.Dcat);
+  hipLaunchKernelGGL(pb_de_kernel, dim3((a.Dcat + 63) / 64), dim3(256), 0, stream, a.de, w.u,
+                     static_cast<const uint16_t*>(a.wf), a.d, a.Dcat);
   return hipGetLastError();
 }
 
