@@ -19,8 +19,8 @@
 //   copy   every K page transposed ([hd][16]) and every V page in key-major
 //          order ([16][hd]), so that all MFMA operands are 16-byte loads with
 //          the contracted index contiguous;
-//   dkv    one wavefront per (layer, KV head, group, 32-key tile of committed
-//          keys): the tile's K and V stay in registers while the group's blocks
+//   dkv    one wavefront per (layer, KV head, group, two 32-key tiles of committed
+//          keys): the tiles' K and V stay in registers while the group's blocks
 //          stream by; S = Q K^T is formed with its query rows permuted (bits 2
 //          and 3 swapped) so that P and dS come out of the accumulators already
 //          in the operand layout of dV^T = dO^T P and dK^T = (R q)^T dS;
@@ -42,6 +42,7 @@ namespace {
 constexpr float kLog2eB = 1.4426950408889634f;
 constexpr float kLn2B = 0.6931471805599453f;
 constexpr int kNqp = 32;   // query rows per (sequence, KV head): one 32-row MFMA tile
+constexpr int kDkvTiles = 2;   // committed key tiles per dkv wavefront
 
 // query (or key) index held by A-row / C-row rho when rows are permuted by
 // swapping bits 2 and 3: then accumulator register r of lane l belongs to index
@@ -217,18 +218,21 @@ __global__ __launch_bounds__(256) void bwd_copy_kernel(BwdArgs b) {
 // One 32-key tile (two pages) against the 32 query rows of one sequence, keys
 // in natural order as MFMA columns, query rows permuted.  kb/vb: the tile's
 // K / V B-fragments (lane: key l % 32, dims 8 (l / 32) + 16 ks ..); valid
-// keys: n0 in page 0, n1 in page 1.  Adds dV^T and (unscaled) dK^T.
-template <int HD>
+// keys: n0 in page 0, n1 in page 1.  Adds dV^T and (unscaled) dK^T.  NT tiles
+// share each sequence's operands (more products per byte loaded).
+template <int HD, int NT = 1>
 struct KeyGrad {
   static constexpr int KS = HD / 16;   // k-steps over head dims
   static constexpr int MT = HD / 32;   // 32-row tiles of head dims
-  f32x16 dkt[MT], dvt[MT];
+  f32x16 dkt[NT][MT], dvt[NT][MT];
 
   __device__ void zero() {
 #pragma unroll
-    for (int m = 0; m < MT; ++m)
+    for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dkt[m][r] = dvt[m][r] = 0.f;
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dkt[t][m][r] = dvt[t][m][r] = 0.f;
   }
 
   // One sequence's operands of the step: its query rows (permuted) and dO
@@ -237,7 +241,7 @@ struct KeyGrad {
   struct Block {
     u16x8 qa[KS], da[KS], qt[MT][2], dt[MT][2];
     float l2[16], dd[16];
-    int n0, n1;   // valid keys of the tile's two pages for this sequence
+    int n0[NT], n1[NT];   // valid keys of each tile's two pages for this sequence
 
     __device__ void load(const BwdWs& w, int64_t qbase, int lane) {
       const int r32 = lane & 31, h = lane >> 5;
@@ -275,7 +279,15 @@ struct KeyGrad {
     }
   };
 
-  __device__ void compute(const Block& q, const u16x8 (&kb)[KS], const u16x8 (&vb)[KS], int lane) {
+  __device__ void compute(const Block& q, const u16x8 (&kb)[NT][KS], const u16x8 (&vb)[NT][KS],
+                          int lane) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t) compute_tile(q, kb[t], vb[t], q.n0[t], q.n1[t], dkt[t], dvt[t], lane);
+  }
+
+  __device__ static void compute_tile(const Block& q, const u16x8 (&kb)[KS], const u16x8 (&vb)[KS],
+                                      int n0, int n1, f32x16 (&dkt)[MT], f32x16 (&dvt)[MT],
+                                      int lane) {
     const int r32 = lane & 31;
     f32x16 sc, dp;
 #pragma unroll
@@ -286,7 +298,7 @@ struct KeyGrad {
       dp = mfma32x32x16(q.da[k], vb[k], dp);
     }
     const int key = r32;   // this lane's column
-    const bool valid = key < 16 ? key < q.n0 : key - 16 < q.n1;
+    const bool valid = key < 16 ? key < n0 : key - 16 < n1;
     u16x8 pb[2], sb[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
@@ -315,18 +327,9 @@ struct KeyGrad {
       }
   }
 
-  __device__ void step(const BwdWs& w, int64_t qbase, const u16x8 (&kb)[KS], const u16x8 (&vb)[KS],
-                       int n0, int n1, int lane) {
-    Block q;
-    q.load(w, qbase, lane);
-    q.n0 = n0;
-    q.n1 = n1;
-    compute(q, kb, vb, lane);
-  }
-
-  // dK (x ln 2: the queries were in log2 units) and dV of the tile's valid keys
+  // dK (x ln 2: the queries were in log2 units) and dV of tile t's valid keys
   // into fp32 pages laid out like the caches: K [16][hd], V [hd][16].
-  __device__ void store(float* dk0, float* dk1, float* dv0, float* dv1, int n0, int n1,
+  __device__ void store(int t, float* dk0, float* dk1, float* dv0, float* dv1, int n0, int n1,
                         int lane) const {
     const int key = lane & 31, h = lane >> 5;
     const bool p1 = key >= 16;
@@ -339,8 +342,8 @@ struct KeyGrad {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int dim = 32 * m + 8 * (r >> 2) + 4 * h + (r & 3);
-        dk[dim] = dkt[m][r] * kLn2B;
-        dv[dim * kPage] = dvt[m][r];
+        dk[dim] = dkt[t][m][r] * kLn2B;
+        dv[dim * kPage] = dvt[t][m][r];
       }
   }
 };
@@ -384,16 +387,18 @@ __device__ __forceinline__ bool len_ok(const AttnArgs& a, int ctx, int carry) {
 // of the group reaches is skipped.
 template <int HD>
 __global__ __launch_bounds__(64, 1) void bwd_dkv_kernel(BwdArgs b) {
+  constexpr int NT = kDkvTiles, KS = HD / 16;
   const AttnArgs& a = b.a;
   const BwdWs w = bwd_ws(b);
   const int lane = threadIdx.x;
-  const int groups = (a.S + b.group - 1) / b.group, tiles = (a.max_pages + 1) / 2;
-  int pair, tile;
-  if (!xcd_item(groups * b.layer_count * a.Hkv, tiles, &pair, &tile)) return;
+  const int groups = (a.S + b.group - 1) / b.group;
+  const int units = ((a.max_pages + 1) / 2 + NT - 1) / NT;
+  int pair, unit;
+  if (!xcd_item(groups * b.layer_count * a.Hkv, units, &pair, &unit)) return;
   const int grp = pair % groups, seg = pair / groups;
   const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
   const int s0 = grp * b.group, s1 = min(a.S, s0 + b.group);
-  const int kbase = 32 * tile;
+  const int kbase = 32 * NT * unit;   // the first key of the unit's NT tiles
   int reach = 0;   // committed keys the group's blocks see
   for (int s = s0; s < s1; ++s) {
     const int ctx = a.ctx_len[s], carry = a.carry_len[s];
@@ -401,34 +406,43 @@ __global__ __launch_bounds__(64, 1) void bwd_dkv_kernel(BwdArgs b) {
   }
   if (kbase >= reach) return;
   const int32_t* pt = a.page_table + static_cast<int64_t>(s0) * a.max_pages;
-  const int pp0 = 2 * tile, pp1 = 2 * tile + 1;
-  const bool has1 = kbase + kPage < reach;
-  int id0 = pt[pp0], id1 = has1 ? pt[pp1] : 0;
-  const bool bad0 = id0 < 0 || id0 >= a.num_pages, bad1 = has1 && (id1 < 0 || id1 >= a.num_pages);
-  if (bad0 || bad1) {
-    if (lane == 0) set_status(a.status, CO_ERR_PAGE_RANGE);
-    if (bad0) id0 = 0;
-    if (bad1) id1 = 0;
-  }
   const int64_t pe = static_cast<int64_t>(kPage) * HD;
   const int64_t lay = static_cast<int64_t>(a.layer_begin + layer_local) * a.num_pages;
-  const int64_t c0 = ((lay + id0) * a.Hkv + g) * pe, c1 = ((lay + id1) * a.Hkv + g) * pe;
-  const int64_t w0 = ((static_cast<int64_t>(layer_local) * a.num_pages + id0) * a.Hkv + g) * pe;
-  const int64_t w1 = ((static_cast<int64_t>(layer_local) * a.num_pages + id1) * a.Hkv + g) * pe;
   const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
-  u16x8 kb[HD / 16], vb[HD / 16];
-  tile_frags<HD>(kc + c0, kc + c1, w.vn + w0, w.vn + w1, lane, kb, vb);
-  KeyGrad<HD> kg;
+  // pages 2 t, 2 t + 1 of each tile t; pages no block reaches are not read
+  int id[NT][2];
+  bool bad[NT][2];
+  u16x8 kb[NT][KS], vb[NT][KS];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const int pg = 2 * (NT * unit + t) + p;
+      const bool has = kbase + (2 * t + p) * kPage < reach;
+      const int x = has ? pt[pg] : 0;
+      bad[t][p] = has && (x < 0 || x >= a.num_pages);
+      if (bad[t][p] && lane == 0) set_status(a.status, CO_ERR_PAGE_RANGE);
+      id[t][p] = (has && !bad[t][p]) ? x : 0;
+    }
+    const int64_t c0 = ((lay + id[t][0]) * a.Hkv + g) * pe, c1 = ((lay + id[t][1]) * a.Hkv + g) * pe;
+    const int64_t w0 = ((static_cast<int64_t>(layer_local) * a.num_pages + id[t][0]) * a.Hkv + g) * pe;
+    const int64_t w1 = ((static_cast<int64_t>(layer_local) * a.num_pages + id[t][1]) * a.Hkv + g) * pe;
+    tile_frags<HD>(kc + c0, kc + c1, w.vn + w0, w.vn + w1, lane, kb[t], vb[t]);
+  }
+  // valid keys of page p of tile t for a sequence (or the group) reaching n keys
+  auto valid_keys = [&](int t, int p, int n) {
+    return bad[t][p] ? 0 : max(0, min(kPage, n - kbase - (2 * t + p) * kPage));
+  };
+  KeyGrad<HD, NT> kg;
   kg.zero();
-  // The group's sequences that see the tile, walked from the last one down (it
-  // sees the most keys, so every tile of the group starts on the same
-  // sequence and the XCD's tiles read the same operands at about the same
-  // time), 64 at a time as a lane mask; operands are loaded two sequences ahead
-  // of the one being computed.
+  // The group's sequences that see the unit, walked from the last one down (it
+  // sees the most keys, so every unit of the group starts on the same
+  // sequence and the XCD's units read the same operands at about the same
+  // time), 64 at a time as a lane mask.
   const int none = s0 - 1;
   uint64_t mask = 0;
   int mbase = s1, mctx = 0;
-  auto prev = [&](int x) {   // last sequence <= x that sees the tile, or none
+  auto prev = [&](int x) {   // last sequence <= x that sees the unit, or none
     for (;;) {
       if (x < s0) return none;
       if (x < mbase) {
@@ -450,39 +464,28 @@ __global__ __launch_bounds__(64, 1) void bwd_dkv_kernel(BwdArgs b) {
       x = mbase - 1;
     }
   };
-  using Blk = typename KeyGrad<HD>::Block;
+  using Blk = typename KeyGrad<HD, NT>::Block;
   auto fetch = [&](Blk& q, int s) {
     const int ctx = __builtin_amdgcn_readlane(mctx, s - mbase);
-    q.n0 = bad0 ? 0 : min(kPage, ctx - kbase);
-    q.n1 = bad1 ? 0 : max(0, min(kPage, ctx - kbase - kPage));
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      q.n0[t] = valid_keys(t, 0, ctx);
+      q.n1[t] = valid_keys(t, 1, ctx);
+    }
     q.load(w, (static_cast<int64_t>(seg) * a.S + s) * kNqp, lane);
   };
-  Blk qa, qb, qc;
-  int sa = prev(s1 - 1), sb = none, sc2 = none;
-  if (sa != none) {
-    fetch(qa, sa);
-    sb = prev(sa - 1);
-    if (sb != none) fetch(qb, sb);
+  for (int sa = prev(s1 - 1); sa != none; sa = prev(sa - 1)) {
+    Blk q;
+    fetch(q, sa);
+    kg.compute(q, kb, vb, lane);
   }
-  while (sa != none) {   // three buffers in rotation, unrolled so that none is copied
-    sc2 = sb != none ? prev(sb - 1) : none;
-    if (sc2 != none) fetch(qc, sc2);
-    kg.compute(qa, kb, vb, lane);
-    if (sb == none) break;
-    sa = sc2 != none ? prev(sc2 - 1) : none;
-    if (sa != none) fetch(qa, sa);
-    kg.compute(qb, kb, vb, lane);
-    if (sc2 == none) break;
-    sb = sa != none ? prev(sa - 1) : none;
-    if (sb != none) fetch(qb, sb);
-    kg.compute(qc, kb, vb, lane);
-    if (sa == none) break;
+  // every key that some block of the group sees (keys past `reach` keep no gradient)
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int64_t o0 = ((lay + id[t][0]) * a.Hkv + g) * pe, o1 = ((lay + id[t][1]) * a.Hkv + g) * pe;
+    kg.store(t, b.d_k_cache + o0, b.d_k_cache + o1, b.d_v_cache + o0, b.d_v_cache + o1,
+             valid_keys(t, 0, reach), valid_keys(t, 1, reach), lane);
   }
-  // every key of the tile that some block sees (keys past `reach` keep no gradient)
-  const int m0 = bad0 ? 0 : min(kPage, reach - kbase);
-  const int m1 = bad1 ? 0 : max(0, min(kPage, reach - kbase - kPage));
-  const int64_t o0 = ((lay + id0) * a.Hkv + g) * pe, o1 = ((lay + id1) * a.Hkv + g) * pe;
-  kg.store(b.d_k_cache + o0, b.d_k_cache + o1, b.d_v_cache + o0, b.d_v_cache + o1, m0, m1, lane);
 }
 
 // ----------------------------------------------------------- dkv, carry
@@ -511,12 +514,16 @@ __global__ __launch_bounds__(64, 2) void bwd_dkv_carry_kernel(BwdArgs b) {
     const int64_t r1 = ((lay * a.S + s) * a.CP + cp1) * a.Hkv + g;
     const int64_t q0 = ((static_cast<int64_t>(layer_local) * a.S + s) * a.CP + cp0) * a.Hkv + g;
     const int64_t q1 = ((static_cast<int64_t>(layer_local) * a.S + s) * a.CP + cp1) * a.Hkv + g;
-    u16x8 kb[HD / 16], vb[HD / 16];
-    tile_frags<HD>(kk + r0 * pe, kk + r1 * pe, w.vnc + q0 * pe, w.vnc + q1 * pe, lane, kb, vb);
-    KeyGrad<HD> kg;
+    u16x8 kb[1][HD / 16], vb[1][HD / 16];
+    tile_frags<HD>(kk + r0 * pe, kk + r1 * pe, w.vnc + q0 * pe, w.vnc + q1 * pe, lane, kb[0], vb[0]);
+    KeyGrad<HD, 1> kg;
     kg.zero();
-    kg.step(w, qbase, kb, vb, n0, n1, lane);
-    kg.store(b.d_k_carry + r0 * pe, b.d_k_carry + r1 * pe, b.d_v_carry + r0 * pe,
+    typename KeyGrad<HD, 1>::Block q;
+    q.load(w, qbase, lane);
+    q.n0[0] = n0;
+    q.n1[0] = n1;
+    kg.compute(q, kb, vb, lane);
+    kg.store(0, b.d_k_carry + r0 * pe, b.d_k_carry + r1 * pe, b.d_v_carry + r0 * pe,
              b.d_v_carry + r1 * pe, n0, n1, lane);
   }
 }
@@ -696,9 +703,9 @@ hipError_t launch_attention_backward(const BwdArgs& b, hipStream_t stream) {
   hipLaunchKernelGGL(bwd_copy_kernel<64>, dim3(static_cast<unsigned>((items + 255) / 256)),
                      dim3(256), 0, stream, b);
   const int groups = (a.S + b.group - 1) / b.group;
-  const int tiles = (a.max_pages + 1) / 2;
+  const int units = ((a.max_pages + 1) / 2 + kDkvTiles - 1) / kDkvTiles;
   const int xpairs = (groups * nseg + 7) / 8 * 8;   // pairs per launch, padded to the 8 XCDs
-  hipLaunchKernelGGL(bwd_dkv_kernel<64>, dim3(xpairs * tiles), dim3(64), 0, stream, b);
+  hipLaunchKernelGGL(bwd_dkv_kernel<64>, dim3(xpairs * units), dim3(64), 0, stream, b);
   hipLaunchKernelGGL(bwd_dkv_carry_kernel<64>, dim3(a.S, nseg), dim3(64), 0, stream, b);
   hipLaunchKernelGGL(bwd_dq_kernel<64>, dim3(xpairs * b.group), dim3(64), 0, stream, b);
   return hipGetLastError();
