@@ -24,9 +24,10 @@
 //          stream by; S = Q K^T is formed with its query rows permuted (bits 2
 //          and 3 swapped) so that P and dS come out of the accumulators already
 //          in the operand layout of dV^T = dO^T P and dK^T = (R q)^T dS;
-//   dq     one wavefront per (layer, KV head, sequence): S^T = K Q^T over all of
-//          the sequence's tiles (keys permuted the same way), dQ^T += K^T dS^T,
-//          then the rotation is undone;
+//   dq     one wavefront per (layer, KV head, sequence, or two sequences of a
+//          group, which then share every committed tile load): S^T = K Q^T over
+//          the tiles (keys permuted the same way), dQ^T += K^T dS^T, then the
+//          rotation is undone;
 //   carry  carry keys belong to one sequence: their tiles take the dkv step
 //          against that sequence alone.
 // Keys masked in the forward (past ctx_len or carry_len, rejected page ids)
@@ -530,86 +531,72 @@ __global__ __launch_bounds__(64, 2) void bwd_dkv_carry_kernel(BwdArgs b) {
 
 // -------------------------------------------------------------------- dq
 //
-// grid (S, layer_count * Hkv), one wavefront: the sequence's committed tiles
-// through its page row, then its carry tiles.  Keys are the MFMA rows here
-// (permuted), query rows the columns: lane l keeps query l % 32 throughout.
-template <int HD>
-__global__ __launch_bounds__(64, 4) void bwd_dq_kernel(BwdArgs b) {
+// One wavefront per NQ consecutive sequences of a group (NQ = 2 when groups
+// share page rows: each committed tile is then loaded once for both) and
+// layer x KV head: the committed tiles through the page row, then each
+// sequence's carry tiles.  Keys are the MFMA rows here (permuted), query rows
+// the columns: lane l keeps query l % 32 of every sequence throughout.
+template <int HD, int NQ>
+__global__ __launch_bounds__(64, NQ == 1 ? 3 : 2) void bwd_dq_kernel(BwdArgs b) {
   constexpr int KS = HD / 16, MT = HD / 32;
   const AttnArgs& a = b.a;
   const BwdWs w = bwd_ws(b);
   const int lane = threadIdx.x, r32 = lane & 31, h = lane >> 5;
   const int groups = (a.S + b.group - 1) / b.group;
   int pair, item;
-  if (!xcd_item(groups * b.layer_count * a.Hkv, b.group, &pair, &item)) return;
-  const int s = (pair % groups) * b.group + item, seg = pair / groups;
-  if (s >= a.S) return;
+  if (!xcd_item(groups * b.layer_count * a.Hkv, (b.group + NQ - 1) / NQ, &pair, &item)) return;
+  const int grp = pair % groups, seg = pair / groups;
+  const int gend = min(a.S, (grp + 1) * b.group);
+  const int sfirst = grp * b.group + NQ * item;
+  if (sfirst >= gend) return;
   const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
   const int G = a.Hq / a.Hkv, nq = a.B * G;
-  const int ctx_raw = a.ctx_len[s], carry_raw = a.carry_len[s];
-  const bool ok = len_ok(a, ctx_raw, carry_raw);
-  if (!ok && seg == 0 && lane == 0) set_status(a.status, CO_ERR_LENGTH);
-  const int ctx = ok ? ctx_raw : 0, carry = ok ? carry_raw : 0;
-  const int64_t qbase = (static_cast<int64_t>(seg) * a.S + s) * kNqp;
-  // this lane's query column: B-fragments of the rotated queries and of dO
-  u16x8 qb[KS], db[KS];
-#pragma unroll
-  for (int k = 0; k < KS; ++k) {
-    qb[k] = *reinterpret_cast<const u16x8*>(w.qr + (qbase + r32) * HD + 16 * k + 8 * h);
-    db[k] = *reinterpret_cast<const u16x8*>(w.don + (qbase + r32) * HD + 16 * k + 8 * h);
-  }
-  const float l2 = w.lse2[qbase + r32], dd = w.dd[qbase + r32];
-  f32x16 dqt[MT];
-#pragma unroll
-  for (int m = 0; m < MT; ++m)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) dqt[m][r] = 0.f;
-
-  const int kp = perm23(r32);   // the key this lane's A rows hold
   const int64_t pe = static_cast<int64_t>(kPage) * HD;
-  const int npc = (ctx + kPage - 1) / kPage, nct = (npc + 1) / 2;
-  const int ncp = (carry + kPage - 1) / kPage, ncar = (ncp + 1) / 2;
-  const int32_t* pt = a.page_table + static_cast<int64_t>(s) * a.max_pages;
-  const int32_t* lead = a.page_table + static_cast<int64_t>(s - s % b.group) * a.max_pages;
   const int64_t lay = static_cast<int64_t>(a.layer_begin + layer_local);
+  const int32_t* lead = a.page_table + static_cast<int64_t>(grp * b.group) * a.max_pages;
   const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
   const uint16_t* kk = static_cast<const uint16_t*>(a.k_carry);
 
-  for (int j = 0; j < nct + ncar; ++j) {
-    const bool com = j < nct;
-    const uint16_t *k0, *k1, *v0, *v1, *t0, *t1;
-    int n0, n1;
-    if (com) {
-      const int p0 = 2 * j, p1 = min(2 * j + 1, npc - 1);
-      int id0 = pt[p0], id1 = pt[p1];
-      const bool b0 = id0 < 0 || id0 >= a.num_pages, b1 = id1 < 0 || id1 >= a.num_pages;
-      if ((b0 || b1) && lane == 0) set_status(a.status, CO_ERR_PAGE_RANGE);
-      if (b.group > 1 && (lead[p0] != id0 || lead[p1] != id1) && lane == 0)
-        set_status(a.status, CO_ERR_GROUP);
-      id0 = b0 ? 0 : id0;
-      id1 = b1 ? 0 : id1;
-      n0 = b0 ? 0 : min(kPage, ctx - 2 * j * kPage);
-      n1 = (b1 || 2 * j + 1 >= npc) ? 0 : min(kPage, ctx - (2 * j + 1) * kPage);
-      const int64_t c0 = ((lay * a.num_pages + id0) * a.Hkv + g) * pe;
-      const int64_t c1 = ((lay * a.num_pages + id1) * a.Hkv + g) * pe;
-      const int64_t w0 = ((static_cast<int64_t>(layer_local) * a.num_pages + id0) * a.Hkv + g) * pe;
-      const int64_t w1 = ((static_cast<int64_t>(layer_local) * a.num_pages + id1) * a.Hkv + g) * pe;
-      k0 = kc + c0; k1 = kc + c1;
-      v0 = w.vn + w0; v1 = w.vn + w1;
-      t0 = w.kt + w0; t1 = w.kt + w1;
-    } else {
-      const int cp0 = 2 * (j - nct), cp1 = min(cp0 + 1, ncp - 1);
-      const int64_t r0 = ((lay * a.S + s) * a.CP + cp0) * a.Hkv + g;
-      const int64_t r1 = ((lay * a.S + s) * a.CP + cp1) * a.Hkv + g;
-      const int64_t q0 = ((static_cast<int64_t>(layer_local) * a.S + s) * a.CP + cp0) * a.Hkv + g;
-      const int64_t q1 = ((static_cast<int64_t>(layer_local) * a.S + s) * a.CP + cp1) * a.Hkv + g;
-      n0 = min(kPage, carry - cp0 * kPage);
-      n1 = cp0 + 1 < ncp ? min(kPage, carry - (cp0 + 1) * kPage) : 0;
-      k0 = kk + r0 * pe; k1 = kk + r1 * pe;
-      v0 = w.vnc + q0 * pe; v1 = w.vnc + q1 * pe;
-      t0 = w.ktc + q0 * pe; t1 = w.ktc + q1 * pe;
+  // per sequence: lengths, this lane's query column (B-fragments of the
+  // rotated queries and of dO), its LSE and D, and the dQ^T accumulators
+  bool live[NQ];
+  int ctx[NQ], carry[NQ], npc[NQ];
+  u16x8 qb[NQ][KS], db[NQ][KS];
+  float l2[NQ], dd[NQ];
+  f32x16 dqt[NQ][MT];
+  int npc_max = 0;
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int s = sfirst + q;
+    live[q] = s < gend;
+    const int sc = live[q] ? s : sfirst;
+    const int cr = a.ctx_len[sc], ur = a.carry_len[sc];
+    const bool ok = live[q] && len_ok(a, cr, ur);
+    if (live[q] && !ok && seg == 0 && lane == 0) set_status(a.status, CO_ERR_LENGTH);
+    ctx[q] = ok ? cr : 0;
+    carry[q] = ok ? ur : 0;
+    npc[q] = (ctx[q] + kPage - 1) / kPage;
+    npc_max = max(npc_max, npc[q]);
+    const int64_t qbase = (static_cast<int64_t>(seg) * a.S + sc) * kNqp;
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+      qb[q][k] = *reinterpret_cast<const u16x8*>(w.qr + (qbase + r32) * HD + 16 * k + 8 * h);
+      db[q][k] = *reinterpret_cast<const u16x8*>(w.don + (qbase + r32) * HD + 16 * k + 8 * h);
     }
-    // S^T and dP^T with the keys permuted: A rows from K and the key-major V copy
+    l2[q] = w.lse2[qbase + r32];
+    dd[q] = w.dd[qbase + r32];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dqt[q][m][r] = 0.f;
+  }
+
+  const int kp = perm23(r32);   // the key this lane's A rows hold
+  // one tile: S^T and dP^T with the keys permuted (A rows from K and the
+  // key-major V copy), then dQ^T += K^T dS^T for every sequence q with keys in it
+  auto tile = [&](const uint16_t* k0, const uint16_t* k1, const uint16_t* v0, const uint16_t* v1,
+                  const uint16_t* t0, const uint16_t* t1, const int (&n0)[NQ],
+                  const int (&n1)[NQ]) {
     const uint16_t* kr = (kp < 16 ? k0 : k1) + (kp & 15) * HD + 8 * h;
     const uint16_t* vr = (kp < 16 ? v0 : v1) + (kp & 15) * HD + 8 * h;
     u16x8 ka[KS], va[KS];
@@ -625,60 +612,115 @@ __global__ __launch_bounds__(64, 4) void bwd_dq_kernel(BwdArgs b) {
 #pragma unroll
       for (int jj = 0; jj < 2; ++jj)
         kt[m][jj] = *reinterpret_cast<const u16x8*>((jj ? t1 : t0) + (32 * m + r32) * kPage + 8 * h);
-    f32x16 sc, dp;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.f;
+    for (int q = 0; q < NQ; ++q) {
+      if (n0[q] + n1[q] == 0) continue;
+      f32x16 sc, dp;
 #pragma unroll
-    for (int k = 0; k < KS; ++k) {
-      sc = mfma32x32x16(ka[k], qb[k], sc);
-      dp = mfma32x32x16(va[k], db[k], dp);
-    }
-    u16x8 sb[2];
+      for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.f;
 #pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
-      float sv[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int r = 8 * jj + e;
-        const int key = acc_index(r, h);
-        const bool valid = key < 16 ? key < n0 : key - 16 < n1;
-        const float pr = valid ? __builtin_amdgcn_exp2f(sc[r] - l2) : 0.f;
-        sv[e] = pr * (dp[r] - dd);
+      for (int k = 0; k < KS; ++k) {
+        sc = mfma32x32x16(ka[k], qb[q][k], sc);
+        dp = mfma32x32x16(va[k], db[q][k], dp);
       }
-      typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
-      const u32x4v s4 = {cvt_pk_bf16(sv[0], sv[1]), cvt_pk_bf16(sv[2], sv[3]),
-                         cvt_pk_bf16(sv[4], sv[5]), cvt_pk_bf16(sv[6], sv[7])};
-      sb[jj] = __builtin_bit_cast(u16x8, s4);
+      u16x8 sb[2];
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        float sv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int r = 8 * jj + e;
+          const int key = acc_index(r, h);
+          const bool valid = key < 16 ? key < n0[q] : key - 16 < n1[q];
+          const float pr = valid ? __builtin_amdgcn_exp2f(sc[r] - l2[q]) : 0.f;
+          sv[e] = pr * (dp[r] - dd[q]);
+        }
+        typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+        const u32x4v s4 = {cvt_pk_bf16(sv[0], sv[1]), cvt_pk_bf16(sv[2], sv[3]),
+                           cvt_pk_bf16(sv[4], sv[5]), cvt_pk_bf16(sv[6], sv[7])};
+        sb[jj] = __builtin_bit_cast(u16x8, s4);
+      }
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) dqt[q][m] = mfma32x32x16(kt[m][jj], sb[jj], dqt[q][m]);
     }
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-#pragma unroll
-      for (int jj = 0; jj < 2; ++jj) dqt[m] = mfma32x32x16(kt[m][jj], sb[jj], dqt[m]);
+  };
 
+  // committed tiles, from the first sequence's page row (the group's row)
+  const int32_t* pt = a.page_table + static_cast<int64_t>(sfirst) * a.max_pages;
+  const int nct_max = (npc_max + 1) / 2;
+  for (int j = 0; j < nct_max; ++j) {
+    const int p0 = 2 * j, p1 = min(2 * j + 1, npc_max - 1);
+    int id0 = pt[p0], id1 = pt[p1];
+    const bool b0 = id0 < 0 || id0 >= a.num_pages, b1 = id1 < 0 || id1 >= a.num_pages;
+    if ((b0 || b1) && lane == 0) set_status(a.status, CO_ERR_PAGE_RANGE);
+    int n0[NQ], n1[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      n0[q] = (b0 || p0 >= npc[q]) ? 0 : min(kPage, ctx[q] - p0 * kPage);
+      n1[q] = (b1 || 2 * j + 1 >= npc[q]) ? 0 : min(kPage, ctx[q] - (2 * j + 1) * kPage);
+      if (b.group > 1 && live[q] && p0 < npc[q] && lane == 0) {
+        const int32_t* own = a.page_table + static_cast<int64_t>(sfirst + q) * a.max_pages;
+        if (own[p0] != lead[p0] || (2 * j + 1 < npc[q] && own[2 * j + 1] != lead[2 * j + 1]))
+          set_status(a.status, CO_ERR_GROUP);
+      }
+    }
+    id0 = b0 ? 0 : id0;
+    id1 = b1 ? 0 : id1;
+    const int64_t c0 = ((lay * a.num_pages + id0) * a.Hkv + g) * pe;
+    const int64_t c1 = ((lay * a.num_pages + id1) * a.Hkv + g) * pe;
+    const int64_t w0 = ((static_cast<int64_t>(layer_local) * a.num_pages + id0) * a.Hkv + g) * pe;
+    const int64_t w1 = ((static_cast<int64_t>(layer_local) * a.num_pages + id1) * a.Hkv + g) * pe;
+    tile(kc + c0, kc + c1, w.vn + w0, w.vn + w1, w.kt + w0, w.kt + w1, n0, n1);
+  }
+  // each sequence's carry tiles, against that sequence alone
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int s = sfirst + q;
+    const int ncp = (carry[q] + kPage - 1) / kPage;
+    for (int cp0 = 0; cp0 < ncp; cp0 += 2) {
+      const int cp1 = min(cp0 + 1, ncp - 1);
+      const int64_t r0 = ((lay * a.S + s) * a.CP + cp0) * a.Hkv + g;
+      const int64_t r1 = ((lay * a.S + s) * a.CP + cp1) * a.Hkv + g;
+      const int64_t q0 = ((static_cast<int64_t>(layer_local) * a.S + s) * a.CP + cp0) * a.Hkv + g;
+      const int64_t q1 = ((static_cast<int64_t>(layer_local) * a.S + s) * a.CP + cp1) * a.Hkv + g;
+      int n0[NQ], n1[NQ];
+#pragma unroll
+      for (int x = 0; x < NQ; ++x) n0[x] = n1[x] = 0;
+      n0[q] = min(kPage, carry[q] - cp0 * kPage);
+      n1[q] = cp0 + 1 < ncp ? min(kPage, carry[q] - (cp0 + 1) * kPage) : 0;
+      tile(kk + r0 * pe, kk + r1 * pe, w.vnc + q0 * pe, w.vnc + q1 * pe, w.ktc + q0 * pe,
+           w.ktc + q1 * pe, n0, n1);
+    }
   }
   // dq = R^T (dS K) / sqrt(hd): dims i and i + hd/2 sit in the same register of tiles m and m + MT/2
   const int qn = r32;
   if (qn >= nq) return;
-  const float sc = rsqrtf(static_cast<float>(HD));
-  const int pos = ctx + qn / G;
+  const float scale = rsqrtf(static_cast<float>(HD));
   const bool rotate = !(a.flags & CO_Q_PREROTATED);
-  float* dq = b.d_q + out_row_b(a, layer_local, s, g, qn, G) * HD;
 #pragma unroll
-  for (int m = 0; m < MT / 2; ++m)
+  for (int q = 0; q < NQ; ++q) {
+    if (!live[q]) continue;
+    const int pos = ctx[q] + qn / G;
+    float* dq = b.d_q + out_row_b(a, layer_local, sfirst + q, g, qn, G) * HD;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int i = 32 * m + 8 * (r >> 2) + 4 * h + (r & 3);
-      float x = dqt[m][r] * sc, y = dqt[m + MT / 2][r] * sc;
-      if (rotate) {
-        float c, sn;
-        rope_cos_sin_rev(pos, a.rope_inv[i] * kInv2Pi, &c, &sn);
-        const float x2 = x * c + y * sn, y2 = y * c - x * sn;
-        x = x2;
-        y = y2;
+    for (int m = 0; m < MT / 2; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = 32 * m + 8 * (r >> 2) + 4 * h + (r & 3);
+        float x = dqt[q][m][r] * scale, y = dqt[q][m + MT / 2][r] * scale;
+        if (rotate) {
+          float c, sn;
+          rope_cos_sin_rev(pos, a.rope_inv[i] * kInv2Pi, &c, &sn);
+          const float x2 = x * c + y * sn, y2 = y * c - x * sn;
+          x = x2;
+          y = y2;
+        }
+        dq[i] = x;
+        dq[i + HD / 2] = y;
       }
-      dq[i] = x;
-      dq[i + HD / 2] = y;
-    }
+  }
 }
 
 }  // namespace
@@ -707,7 +749,11 @@ hipError_t launch_attention_backward(const BwdArgs& b, hipStream_t stream) {
   const int xpairs = (groups * nseg + 7) / 8 * 8;   // pairs per launch, padded to the 8 XCDs
   hipLaunchKernelGGL(bwd_dkv_kernel<64>, dim3(xpairs * units), dim3(64), 0, stream, b);
   hipLaunchKernelGGL(bwd_dkv_carry_kernel<64>, dim3(a.S, nseg), dim3(64), 0, stream, b);
-  hipLaunchKernelGGL(bwd_dq_kernel<64>, dim3(xpairs * b.group), dim3(64), 0, stream, b);
+  if (b.group > 1)
+    hipLaunchKernelGGL((bwd_dq_kernel<64, 2>), dim3(xpairs * ((b.group + 1) / 2)), dim3(64), 0,
+                       stream, b);
+  else
+    hipLaunchKernelGGL((bwd_dq_kernel<64, 1>), dim3(xpairs), dim3(64), 0, stream, b);
   return hipGetLastError();
 }
 

@@ -1345,12 +1345,13 @@ hipError_t launch_gemm_acc(const void* A, const void* B, int M, int N, int K, fl
   g.K = K;
   g.A = A;
   g.B = B;
-  g.partial = part;
   g.mode = kModePartial;
   g.k_per_split = split_len(K, split, tile);
   const int splits = (K + g.k_per_split - 1) / g.k_per_split;
+  // a single split that overwrites C writes it directly
+  g.partial = (splits == 1 && !accumulate) ? C : part;
   hipError_t err = launch_gemm_bf16(g, tile, splits, stream);
-  if (err != hipSuccess) return err;
+  if (err != hipSuccess || g.partial == C) return err;
   const int64_t n = static_cast<int64_t>(M) * N;
   hipLaunchKernelGGL(sum_splits_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0,
                      stream, part, splits, n, C, accumulate ? 1 : 0);
