@@ -1081,22 +1081,28 @@ bool pick_wide(int M, int N, int K, int num_cus, int* tile, int* split) {
     if (force != nullptr && atoi(force) != v) continue;
     const int64_t tiles = static_cast<int64_t>((M + kWideBM[v] - 1) / kWideBM[v]) *
                           ((N + kWideBN[v] - 1) / kWideBN[v]);
-    // relative main-loop rates measured on MI355X (the 64-deep stages and the
-    // square tile move the fewest bytes per flop through LDS)
-    const double eff = v == 3 ? 1.0 : v > 3 ? 0.95 : v == 0 ? 0.9 : 0.8;
+    // relative main-loop rates measured on MI355X, each variant timed alone at
+    // the projection shapes (the 64-deep stages and the square tile move the
+    // fewest bytes per flop through LDS)
+    constexpr double kEff[kWideVariants] = {0.98, 0.8, 0.8, 1.0, 0.86, 0.87};
+    const double eff = kEff[v];
     for (int s = 1; s <= 16; ++s) {
       const int kps = split_len(K, s, kWide + v);
       if (kps < 256 || (K + kps - 1) / kps != s) continue;
       const int64_t wgs = tiles * s;
       if (wgs < num_cus / 2 && force == nullptr) continue;
       const int64_t waves = (wgs + num_cus - 1) / num_cus;
-      // main loop at the per-CU rate measured with operands streaming from HBM
+      // main loop at the per-CU rate measured with operands streaming from HBM,
+      // or the weights streamed from HBM once per row tile, whichever is longer
       const double t_mfma = static_cast<double>(waves) * kWideBM[v] * kWideBN[v] * kps * 2.0 /
                             (4.5e12 * eff);
-      // split partials: written, read back and reduced by a second kernel
-      const double t_part = s > 1 ? static_cast<double>(s) * M * N * 8.0 / 4.0e12 + 2e-6 : 0.0;
-      if (t_mfma + t_part < best) {
-        best = t_mfma + t_part;
+      const double t_hbm = static_cast<double>((M + kWideBM[v] - 1) / kWideBM[v]) * N * K * 2.0 / 6.0e12;
+      // split partials: their stores overlap the main loop; the epilogue kernel
+      // reads them back
+      const double t_part = s > 1 ? static_cast<double>(s) * M * N * 4.0 / 5.0e12 + 2e-6 : 0.0;
+      const double t = (t_mfma > t_hbm ? t_mfma : t_hbm) + t_part;
+      if (t < best) {
+        best = t;
         bv = v;
         bs = s;
       }
