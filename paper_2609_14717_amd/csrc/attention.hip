@@ -87,6 +87,7 @@ __device__ __forceinline__ int64_t out_row(const AttnArgs& a, int layer_local, i
 // loads and turned into per-(chunk, query) weights.
 constexpr int kMaxMergeChunks = 64;
 constexpr int kMaxMergeSlices = 4096;   // workgroups of one persistent launch
+constexpr int kCombineWideSegs = 128;   // segments from which the merge takes 16 dims per thread
 constexpr int kAttnWaves64 = 8, kAttnWaves128 = 4;             // wavefronts per workgroup
 constexpr int kAttnRoundTiles64 = 64, kAttnRoundTiles128 = 128; // tiles per wavefront per round
 
@@ -1009,15 +1010,19 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
 
 // Combine the slice records of every (layer, KV head, sequence) split across
 // slices, write O/LSE of segments without keys, and report invalid lengths.
-// The slice bounds are staged in LDS with one round of loads; one thread per
-// (query row, 4 output dims) then merges the records.
+// One thread per (query row, DIMS output dims) merges the records: the row's
+// maxima and sums and its DIMS partial dims of up to kBatch records are loaded
+// at once, so a segment costs one round trip after the header loads.  Wide
+// threads (16 dims) suit launches of many segments; with few segments, 4 dims
+// per thread spread each segment over more workgroups.
+template <int DIMS>
 __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int layer_count,
                                                                 int n_wg, int hdr_floats,
                                                                 int nq_pad) {
-  constexpr int kBatch = 8;
+  constexpr int kBatch = 8, kV = DIMS / 4;
   const int s = blockIdx.x, seg = blockIdx.y;
   const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
-  const int hd = a.hd, G = a.Hq / a.Hkv, nq = a.B * G, q4 = hd / 4;
+  const int hd = a.hd, G = a.Hq / a.Hkv, nq = a.B * G, qd = hd / DIMS;
   const int tid = threadIdx.x;
   const int* hdr = reinterpret_cast<const int*>(a.ws);
   // slice w covers tiles [T w / n_wg, T (w + 1) / n_wg) of the T in the launch
@@ -1046,49 +1051,62 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
   const int w_lo = owner(A), w_hi = owner(A + nts - 1);
   if (w_lo == w_hi) return;            // finished in place
   const int nrec = w_hi - w_lo + 1;
+  // with at least as many tiles as slices no slice is empty, so every slot in
+  // [w_lo, w_hi] holds a record; otherwise an empty slice left none
+  const bool all_full = T >= n_wg;
   const int64_t rec = static_cast<int64_t>(nq_pad) * (hd + 2);
-  // records of consecutive slices of one segment are consecutive slots; a slice
-  // without tiles left none
+  // records of consecutive slices of one segment are consecutive slots
   const float* base = slot_ptr(a, hdr_floats, w_lo + static_cast<int64_t>(seg) * a.S + s, nq_pad);
-  for (int idx = tid + blockIdx.z * 256; idx < nq * q4; idx += 256 * gridDim.z) {
-    const int qn = idx / q4, d = (idx % q4) * 4;
+  for (int idx = tid + blockIdx.z * 256; idx < nq * qd; idx += 256 * gridDim.z) {
+    const int qn = idx / qd, d = (idx % qd) * DIMS;
     const float* pm = base + nq_pad * hd + qn;
+    const float* po = base + qn * hd + d;
     float M = -INFINITY, den = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    f32x4 acc[kV];
+#pragma unroll
+    for (int j = 0; j < kV; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int r0 = 0; r0 < nrec; r0 += kBatch) {   // usually one batch: one round trip
       float mv[kBatch], lv[kBatch];
-      f32x4 ov[kBatch];
+      f32x4 ov[kBatch][kV];
 #pragma unroll
       for (int i = 0; i < kBatch; ++i) {
         const bool in = r0 + i < nrec;
         mv[i] = in ? pm[(r0 + i) * rec] : -INFINITY;
         lv[i] = in ? pm[(r0 + i) * rec + nq_pad] : 0.f;
-        ov[i] = in ? *reinterpret_cast<const f32x4*>(base + (r0 + i) * rec + qn * hd + d)
-                   : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < kV; ++j)
+          ov[i][j] = in ? *reinterpret_cast<const f32x4*>(po + (r0 + i) * rec + 4 * j)
+                        : f32x4{0.f, 0.f, 0.f, 0.f};
       }
       float Mb = M;
 #pragma unroll
       for (int i = 0; i < kBatch; ++i) {
-        if (!(r0 + i < nrec && bnd(w_lo + r0 + i) < bnd(w_lo + r0 + i + 1))) mv[i] = -INFINITY;
+        const int w = w_lo + r0 + i;
+        if (!(r0 + i < nrec && (all_full || bnd(w) < bnd(w + 1)))) mv[i] = -INFINITY;
         Mb = fmaxf(Mb, mv[i]);
       }
       const float f = (M == -INFINITY) ? 0.f : exp2f(M - Mb);
       den *= f;
-      acc *= f;
+#pragma unroll
+      for (int j = 0; j < kV; ++j) acc[j] *= f;
 #pragma unroll
       for (int i = 0; i < kBatch; ++i) {
         const float wgt = (mv[i] == -INFINITY) ? 0.f : exp2f(mv[i] - Mb);
         den += wgt * lv[i];
-        acc += wgt * ov[i];
+#pragma unroll
+        for (int j = 0; j < kV; ++j) acc[j] += wgt * ov[i][j];
       }
       M = Mb;
     }
     const float inv = den > 0.f ? 1.f / den : 0.f;
     const int64_t row = out_row(a, layer_local, s, g, qn, G);
-    u16x4 v;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) v[r] = f2bf(acc[r] * inv);
-    *reinterpret_cast<u16x4*>(out + row * hd + d) = v;
+    for (int j = 0; j < kV; ++j) {
+      u16x4 v;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v[r] = f2bf(acc[j][r] * inv);
+      *reinterpret_cast<u16x4*>(out + row * hd + d + 4 * j) = v;
+    }
     if (a.lse && d == 0) a.lse[row] = den > 0.f ? (M + log2f(den)) * kLn2 : -INFINITY;
   }
 }
@@ -1990,8 +2008,21 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
                             hipStream_t stream) {
   if (a.S == 0 || layer_count == 0) return hipSuccess;
   const int nt = p.nq_pad / 16;
-  const int items = (a.B * (a.Hq / a.Hkv)) * (a.hd / 4);
+  // merge grid: one workgroup per 256 (query row, dims) items of a segment,
+  // 16 dims per item with at least kCombineWideSegs segments, else 4
+  const bool wide = static_cast<int64_t>(a.S) * layer_count * a.Hkv >= kCombineWideSegs;
+  const int items = (a.B * (a.Hq / a.Hkv)) * (a.hd / (wide ? 16 : 4));
   const dim3 mgrid(a.S, layer_count * a.Hkv, (items + 255) / 256);
+  const int items_f32 = (a.B * (a.Hq / a.Hkv)) * (a.hd / 4);
+  const dim3 fgrid(a.S, layer_count * a.Hkv, (items_f32 + 255) / 256);
+  auto combine = [&]() {
+    if (wide)
+      hipLaunchKernelGGL(attn_bf16_combine_kernel<16>, mgrid, dim3(256), 0, stream, a, layer_count,
+                         p.n_wg, p.hdr_floats, p.nq_pad);
+    else
+      hipLaunchKernelGGL(attn_bf16_combine_kernel<4>, mgrid, dim3(256), 0, stream, a, layer_count,
+                         p.n_wg, p.hdr_floats, p.nq_pad);
+  };
   // grouped kernel: any query count with head_dim 64, up to 32 rows with 128
   const int nq = a.B * (a.Hq / a.Hkv);
   const bool one = nq <= 32;
@@ -2029,8 +2060,7 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
                          p.n_wg, p.hdr_floats);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(attn_bf16_combine_kernel, mgrid, dim3(256), 0, stream, a, layer_count,
-                       p.n_wg, p.hdr_floats, p.nq_pad);
+    combine();
     return hipGetLastError();
   }
   if (a.dtype == CO_DTYPE_BF16) {
@@ -2056,8 +2086,7 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
 #undef CO_ATTN_LAUNCH
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(attn_bf16_combine_kernel, mgrid, dim3(256), 0, stream, a, layer_count,
-                       p.n_wg, p.hdr_floats, p.nq_pad);
+    combine();
     return hipGetLastError();
   }
   const dim3 grid(p.n_chunks, a.S, layer_count * a.Hkv);
@@ -2067,7 +2096,7 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
     hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(256), 0, stream, a, p.chunk_pages, p.n_chunks, p.nq_pad);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || p.n_chunks <= 1) return err;
-  hipLaunchKernelGGL(attn_chunk_merge_kernel<float>, mgrid, dim3(256), 0, stream, a, p.chunk_pages,
+  hipLaunchKernelGGL(attn_chunk_merge_kernel<float>, fgrid, dim3(256), 0, stream, a, p.chunk_pages,
                      p.n_chunks, p.nq_pad);
   return hipGetLastError();
 }
