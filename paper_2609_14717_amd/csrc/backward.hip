@@ -802,21 +802,32 @@ PbWs pb_ws(void* ws, int M, int Dcat, int d, int n_kv) {
   return w;
 }
 
-// dst[c][r] = src[r][c] for r < R (zero for R <= r < Rp), c < C: 64 x 64 tiles through LDS.
+// dst[c][r] = src[r][c] for r < R (zero for R <= r < Rp), c < C: 64 x 64 tiles
+// through LDS, 16 bytes per global load and store.  C, Rp, src_ld and dst_ld
+// are multiples of 64 (8 would do for the accesses; the tiles then stay whole)
+// and both buffers 16-byte aligned.  Eight consecutive lanes cover one 128-byte
+// row segment on both sides.
 __global__ __launch_bounds__(256) void pb_transpose_kernel(const uint16_t* src, int R, int C,
                                                            int64_t src_ld, uint16_t* dst, int Rp,
                                                            int64_t dst_ld) {
-  __shared__ uint16_t t[64][65];
+  __shared__ __align__(16) uint16_t t[64][72];   // 144-byte rows keep 16-byte stores aligned
   const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int i = ty; i < 64; i += 4) {
-    const int r = r0 + i, c = c0 + tx;
-    t[i][tx] = (r < R && c < C) ? src[r * src_ld + c] : static_cast<uint16_t>(0);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int q = threadIdx.x + 256 * j, i = q >> 3, k = q & 7;
+    const int r = r0 + i;
+    u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (r < R) v = *reinterpret_cast<const u16x8*>(src + r * src_ld + c0 + 8 * k);
+    *reinterpret_cast<u16x8*>(&t[i][8 * k]) = v;
   }
   __syncthreads();
-  for (int i = ty; i < 64; i += 4) {
-    const int c = c0 + i, r = r0 + tx;
-    if (c < C && r < Rp) dst[c * dst_ld + r] = t[tx][i];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int q = threadIdx.x + 256 * j, c = q >> 3, k = q & 7;
+    u16x8 v;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = t[8 * k + e][c];
+    *reinterpret_cast<u16x8*>(dst + (c0 + c) * dst_ld + r0 + 8 * k) = v;
   }
 }
 
@@ -976,6 +987,9 @@ size_t proj_bwd_ws_bytes(int M, int Dcat, int d, int n_kv, int num_cus) {
 hipError_t launch_project_backward(const ProjBwdArgs& a, hipStream_t stream) {
   if (a.M == 0) return hipSuccess;
   const int n_kv = 2 * a.L * a.Hkv * a.hd;
+  // every transpose below has C, Rp and both leading dimensions multiples of 64
+  // (Dcat and d are, Mp is a multiple of 256, NKV of 128)
+  if (a.Dcat % 64 || a.d % 64 || n_kv % 64) return hipErrorInvalidValue;
   const PbWs w = pb_ws(a.ws, a.M, a.Dcat, a.d, n_kv);
   const int Mp = w.Mp;
   hipError_t err;
@@ -983,7 +997,7 @@ hipError_t launch_project_backward(const ProjBwdArgs& a, hipStream_t stream) {
     return err;
   auto transpose = [&](const void* src, int R, int C, int64_t src_ld, uint16_t* dst, int Rp,
                        int64_t dst_ld) {
-    const dim3 grid((Rp + 63) / 64, (C + 63) / 64);
+    const dim3 grid(Rp / 64, C / 64);
     hipLaunchKernelGGL(pb_transpose_kernel, grid, dim3(256), 0, stream,
                        static_cast<const uint16_t*>(src), R, C, src_ld, dst, Rp, dst_ld);
   };
