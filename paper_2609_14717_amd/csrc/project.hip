@@ -1328,7 +1328,15 @@ __global__ __launch_bounds__(256) void sum_splits_kernel(const float* part, int 
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (i >= n) return;
   float v = accumulate ? C[i] : 0.f;
-  for (int s = 0; s < splits; ++s) v += part[s * n + i];
+  int s = 0;
+  for (; s + 8 <= splits; s += 8) {   // eight loads in flight, summed in split order
+    float x[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) x[k] = part[(s + k) * n + i];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v += x[k];
+  }
+  for (; s < splits; ++s) v += part[s * n + i];
   C[i] = v;
 }
 
