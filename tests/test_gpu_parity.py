@@ -381,8 +381,10 @@ def test_persistent_hd128_64_rows(w, monkeypatch):
 
 
 # The same path at head_dim 64 (32 and 64 query rows, eight wavefronts per
-# workgroup), forced on.
-@pytest.mark.parametrize("wgs", ["", "1", "5"], ids=lambda v: f"wg{v or 'dflt'}")
+# workgroup), forced on.  With 500 workgroups (4000 slices) most slices are
+# empty and a segment's records span more than one merge batch; MANY_SEQS has
+# enough segments for the merge's 16-dims-per-thread form.
+@pytest.mark.parametrize("wgs", ["", "1", "5", "500"], ids=lambda v: f"wg{v or 'dflt'}")
 @pytest.mark.parametrize("w", [SMALL_RAGGED, MANY_SEQS, WIDE64], ids=lambda w: w.name)
 def test_wave_slices_hd64(w, wgs, monkeypatch):
     monkeypatch.setenv("CO_ATTN_WAVE", "1")
