@@ -831,17 +831,20 @@ __global__ __launch_bounds__(256) void pb_transpose_kernel(const uint16_t* src, 
   }
 }
 
-// dJ^T [NKV][Mp]: one thread per (layer, head, rotation pair, row), rows fastest.
-__global__ __launch_bounds__(256) void pb_gather_kernel(ProjBwdArgs a, uint16_t* djt, int Mp) {
+// dJ [Mp][NKV]: one thread per (row, layer, head, rotation pair), pairs fastest,
+// so that a row's key gradients are read and its dJ columns written in
+// contiguous runs (its value gradients, [hd][16] per page, come through L2
+// for the rows of one page in turn).
+__global__ __launch_bounds__(256) void pb_gather_kernel(ProjBwdArgs a, uint16_t* dj, int Mp) {
   const int half = a.hd / 2;
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   const int64_t total = static_cast<int64_t>(a.L) * a.Hkv * half * Mp;
   if (idx >= total) return;
-  const int r = static_cast<int>(idx % Mp);
-  const int64_t jp = idx / Mp;
-  const int i = static_cast<int>(jp % half);
-  const int g = static_cast<int>((jp / half) % a.Hkv);
-  const int l = static_cast<int>(jp / (static_cast<int64_t>(half) * a.Hkv));
+  const int i = static_cast<int>(idx % half);
+  const int64_t jp = idx / half;
+  const int g = static_cast<int>(jp % a.Hkv);
+  const int l = static_cast<int>((jp / a.Hkv) % a.L);
+  const int r = static_cast<int>(jp / (static_cast<int64_t>(a.Hkv) * a.L));
   float klo = 0.f, khi = 0.f, vlo = 0.f, vhi = 0.f;
   const int32_t dst = r < a.M ? a.row_dst[r] : kSkip;
   const int64_t pe = static_cast<int64_t>(kPage) * a.hd;
@@ -878,10 +881,11 @@ __global__ __launch_bounds__(256) void pb_gather_kernel(ProjBwdArgs a, uint16_t*
   }
   const int64_t jk = ((static_cast<int64_t>(l) * 2 + 0) * a.Hkv + g) * a.hd + i;
   const int64_t jv = ((static_cast<int64_t>(l) * 2 + 1) * a.Hkv + g) * a.hd + i;
-  djt[jk * Mp + r] = f2bf(klo);
-  djt[(jk + half) * Mp + r] = f2bf(khi);
-  djt[jv * Mp + r] = f2bf(vlo);
-  djt[(jv + half) * Mp + r] = f2bf(vhi);
+  uint16_t* row = dj + static_cast<int64_t>(r) * (2 * a.L * a.Hkv * a.hd);
+  row[jk] = f2bf(klo);
+  row[jk + half] = f2bf(khi);
+  row[jv] = f2bf(vlo);
+  row[jv + half] = f2bf(vhi);
 }
 
 // Z^T (fp32 [d][M]) + F E on carried rows -> bf16 [d][Mp], padding rows zero.
@@ -1005,8 +1009,8 @@ hipError_t launch_project_backward(const ProjBwdArgs& a, hipStream_t stream) {
   transpose(a.wkv, n_kv, a.d, a.d, w.wkvt, n_kv, n_kv);          // W_KV^T [d][NKV]
   const int64_t items = static_cast<int64_t>(a.L) * a.Hkv * (a.hd / 2) * Mp;
   hipLaunchKernelGGL(pb_gather_kernel, dim3(static_cast<unsigned>((items + 255) / 256)), dim3(256),
-                     0, stream, a, w.djt, Mp);
-  transpose(w.djt, n_kv, Mp, Mp, w.dj, n_kv, n_kv);              // dJ [Mp][NKV]
+                     0, stream, a, w.dj, Mp);
+  transpose(w.dj, Mp, n_kv, n_kv, w.djt, Mp, Mp);                // dJ^T [NKV][Mp]
   // Z^T = F H^T (+ F E on carried rows)
   if ((err = launch_gemm_acc(a.wf, a.hidden, a.d, a.M, a.Dcat, w.t32, false, w.part, a.num_cus,
                              stream)) != hipSuccess)
