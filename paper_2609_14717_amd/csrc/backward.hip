@@ -116,23 +116,26 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdArgs b) {
   const float qscale = rsqrtf(static_cast<float>(HD)) * kLog2eB;
   float dsum = 0.f;
   u16x4 qlo, qhi, dlo, dhi;
+  // the row's four pairs: 8-byte loads of each half
+  const u16x4 z4 = {0, 0, 0, 0};
+  const u16x4 xq = live ? *reinterpret_cast<const u16x4*>(Q + row + 4 * p) : z4;
+  const u16x4 yq = live ? *reinterpret_cast<const u16x4*>(Q + row + 4 * p + HD / 2) : z4;
+  const u16x4 xd = live ? *reinterpret_cast<const u16x4*>(dO + row + 4 * p) : z4;
+  const u16x4 yd = live ? *reinterpret_cast<const u16x4*>(dO + row + 4 * p + HD / 2) : z4;
+  const u16x4 xo = live ? *reinterpret_cast<const u16x4*>(O + row + 4 * p) : z4;
+  const u16x4 yo = live ? *reinterpret_cast<const u16x4*>(O + row + 4 * p + HD / 2) : z4;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int i = 4 * p + e;
-    float x = 0.f, y = 0.f, dx = 0.f, dy = 0.f;
-    if (live) {
-      x = bf2f(Q[row + i]);
-      y = bf2f(Q[row + i + HD / 2]);
-      dx = bf2f(dO[row + i]);
-      dy = bf2f(dO[row + i + HD / 2]);
-      dsum = fmaf(dx, bf2f(O[row + i]), fmaf(dy, bf2f(O[row + i + HD / 2]), dsum));
-      if (rotate) {
-        float c, sn;
-        rope_cos_sin_rev(ctx + qn / G, a.rope_inv[i] * kInv2Pi, &c, &sn);
-        const float x2 = x * c - y * sn, y2 = y * c + x * sn;
-        x = x2;
-        y = y2;
-      }
+    float x = bf2f(xq[e]), y = bf2f(yq[e]);
+    const float dx = bf2f(xd[e]), dy = bf2f(yd[e]);
+    dsum = fmaf(dx, bf2f(xo[e]), fmaf(dy, bf2f(yo[e]), dsum));
+    if (live && rotate) {
+      float c, sn;
+      rope_cos_sin_rev(ctx + qn / G, a.rope_inv[i] * kInv2Pi, &c, &sn);
+      const float x2 = x * c - y * sn, y2 = y * c + x * sn;
+      x = x2;
+      y = y2;
     }
     qlo[e] = f2bf(x * qscale);
     qhi[e] = f2bf(y * qscale);
@@ -144,14 +147,23 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdArgs b) {
   *reinterpret_cast<u16x4*>(w.qr + qo + 4 * p + HD / 2) = qhi;
   *reinterpret_cast<u16x4*>(w.don + qo + 4 * p) = dlo;
   *reinterpret_cast<u16x4*>(w.don + qo + 4 * p + HD / 2) = dhi;
-  const int64_t to = base * HD;   // [hd][32] of this (seg, s)
+  // the transposed copies ([hd][32] of this (seg, s)) go through LDS and leave
+  // as one 16-byte store per thread each
+  __shared__ __align__(16) uint16_t tq[HD][kNqp], td[HD][kNqp];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int i = 4 * p + e;
-    w.qrt[to + i * kNqp + qn] = qlo[e];
-    w.qrt[to + (i + HD / 2) * kNqp + qn] = qhi[e];
-    w.dot[to + i * kNqp + qn] = dlo[e];
-    w.dot[to + (i + HD / 2) * kNqp + qn] = dhi[e];
+    tq[i][qn] = qlo[e];
+    tq[i + HD / 2][qn] = qhi[e];
+    td[i][qn] = dlo[e];
+    td[i + HD / 2][qn] = dhi[e];
+  }
+  __syncthreads();
+  {
+    const int64_t to = base * HD;
+    const int i = t >> 2, c = (t & 3) * 8;   // 256 threads x 8 elements = [64][32]
+    *reinterpret_cast<u16x8*>(w.qrt + to + i * kNqp + c) = *reinterpret_cast<const u16x8*>(&tq[i][c]);
+    *reinterpret_cast<u16x8*>(w.dot + to + i * kNqp + c) = *reinterpret_cast<const u16x8*>(&td[i][c]);
   }
   dsum += __shfl_xor(dsum, 1);
   dsum += __shfl_xor(dsum, 2);
