@@ -724,3 +724,216 @@ def test_project_backward_matches_finite_differences():
     _, _, dE0 = oracle.project_backward(H, E, np.zeros(5, bool), WF, WKV, pos, L, Hkv, hd,
                                         theta, dK, dV)
     assert not dE0.any()
+
+
+# ------------------------------------ training-shaped second pass (Algorithm 2)
+#
+# Algorithm 2 steps 3-6: after the first pass from anchor a the verifier
+# accepts m proposals; the anchor moves to a' = a + m + 1; the second pass
+# reads the recorded prefix y_{<a'} (committed keys, projected without E at
+# their own positions) plus the block's rejected rows Phi(H^rej + E_carry) at
+# a' + r, and its queries sit at a' + i.  The oracle reaches this through
+# route(mode="carry_only") and round_update(..., "carry_only"); these pins check
+# that path against the algorithm's own statements and against a dense
+# recomputation that shares none of the oracle's routing, state or attention.
+
+def _tokens_with_lcp(m, B, rng, V=50):
+    S = len(m)
+    target = rng.integers(0, V, (S, B))
+    draft = target.copy()
+    for s in range(S):
+        if m[s] < B:
+            draft[s, m[s]] = (target[s, m[s]] + 1 + rng.integers(0, V - 1)) % V
+    return draft.astype(np.int32), target.astype(np.int32)
+
+
+def test_carry_only_route_follows_algorithm_2_shift():
+    """For every accepted count m (all of 0..B): p0 = a + 1 (the window starts
+    after the anchor), ctx_len = a + 1 + m = a', carry_len = B - m, no row is
+    committed (rows j < m: SKIP), window row j >= m is carry row j - m at
+    position a' + (j - m)."""
+    rng = np.random.default_rng(21)
+    B, P = 16, 8
+    m = np.arange(B + 1, dtype=np.int32)
+    S = len(m)
+    a = rng.integers(0, P * 16 - B - 1, S).astype(np.int32)
+    pt = np.array([rng.permutation(4 * P)[:P] for _ in range(S)], np.int32)
+    draft, target = _tokens_with_lcp(m, B, rng)
+    old_carry = rng.integers(0, B + 1, S).astype(np.int32)
+    r = oracle.route(draft, target, a + 1, old_carry, pt, 4 * P, mode="carry_only")
+    a2 = a + m + 1                                     # Algorithm 2 step 3
+    np.testing.assert_array_equal(r["status"], 0)
+    np.testing.assert_array_equal(r["accept_len"], m)
+    np.testing.assert_array_equal(r["ctx_len"], a2)
+    np.testing.assert_array_equal(r["carry_len"], B - m)
+    for s in range(S):
+        for j in range(B):
+            assert r["row_pos"][s, j] == a[s] + 1 + j
+            if j < m[s]:
+                assert r["row_dst"][s, j] == oracle.SKIP
+            else:
+                rr = j - m[s]
+                assert r["row_dst"][s, j] == -1 - rr
+                assert r["row_pos"][s, j] == a2[s] + rr
+
+
+def test_carry_only_update_keeps_committed_and_equals_carry_mode_carries():
+    """carry_only leaves C exactly as it was and builds the same U as the
+    ordinary carry update of the same rows (Eq. 2 with the same E and
+    positions); only the committed rows differ, which carry_only never writes."""
+    t = _tiny_setup(S=3, B=4)
+    S, B, L, Hkv, hd = t["S"], t["B"], t["L"], t["Hkv"], t["hd"]
+    rng = t["rng"]
+    m = np.array([0, 2, 4], np.int32)
+    draft, target = _tokens_with_lcp(m, B, rng)
+    H = rng.standard_normal((S, B, t["Dcat"]))
+    pt = np.tile(np.arange(8, dtype=np.int32), (S, 1))
+    ctx0 = np.array([5, 9, 0], np.int32)
+    ck = [rng.standard_normal((L, n, Hkv, hd)) for n in ctx0]
+    cv = [rng.standard_normal((L, n, Hkv, hd)) for n in ctx0]
+    sts = []
+    for mode in ("carry_only", "carry"):
+        st = oracle.State(S, L, Hkv, hd)
+        for s in range(S):
+            st.set_committed(s, ck[s], cv[s])
+        before_k = [c.copy() for c in st.ck]
+        before_v = [c.copy() for c in st.cv]
+        r = oracle.route(draft, target, ctx0, np.zeros(S, np.int32), pt, 8, mode)
+        oracle.round_update(st, r, H, t["E"], t["WF"], t["WKV"], 1e4, mode)
+        sts.append((st, before_k, before_v, r))
+    co_st, ck0, cv0, r_co = sts[0]
+    ca_st, _, _, r_ca = sts[1]
+    for s in range(S):
+        np.testing.assert_array_equal(co_st.ck[s], ck0[s])
+        np.testing.assert_array_equal(co_st.cv[s], cv0[s])
+        np.testing.assert_array_equal(co_st.uk[s], ca_st.uk[s])
+        np.testing.assert_array_equal(co_st.uv[s], ca_st.uv[s])
+        assert ca_st.ck[s].shape[1] == ctx0[s] + m[s]
+    np.testing.assert_array_equal(r_co["ctx_len"], r_ca["ctx_len"])
+    np.testing.assert_array_equal(r_co["carry_len"], r_ca["carry_len"])
+
+
+def _train_tiny(seed=31):
+    """Two recorded responses of 24 positions, three anchors each, B = 4."""
+    rng = np.random.default_rng(seed)
+    n_resp, seq_len, A, B = 2, 24, 3, 4
+    Dcat, d, L, Hq, Hkv, hd = 10, 6, 2, 4, 2, 8
+    c = dict(n_resp=n_resp, seq_len=seq_len, A=A, B=B, Dcat=Dcat, d=d, L=L, Hq=Hq, Hkv=Hkv,
+             hd=hd, theta=100.0)
+    c["WF"] = rng.standard_normal((d, Dcat)) * 0.4
+    c["WKV"] = rng.standard_normal((2 * L * Hkv * hd, d)) * 0.4
+    c["E"] = rng.standard_normal(Dcat)
+    c["Y"] = rng.standard_normal((n_resp, seq_len, Dcat))        # recorded target states
+    c["a"] = np.array([np.sort(rng.choice(seq_len - B - 1, A, replace=False))
+                       for _ in range(n_resp)], np.int32).ravel()
+    c["u"] = np.array([0, 4, 2, 1, 3, 4], np.int32)              # rejected counts, incl. 0 and B
+    c["H"] = rng.standard_normal((n_resp * A, B, Dcat))          # window states (first pass)
+    c["Q"] = rng.standard_normal((L, n_resp * A, B, Hq, hd))
+    return c
+
+
+def _train_oracle(c, mode="carry_only", p0_shift=1):
+    """The oracle's path through the training-shaped forward (as the GPU parity
+    tests drive it)."""
+    V, B, L, Hkv, hd = c["n_resp"] * c["A"], c["B"], c["L"], c["Hkv"], c["hd"]
+    m = (B - c["u"]).astype(np.int32)
+    a2 = c["a"] + m + 1
+    st = oracle.State(V, L, Hkv, hd)
+    for v in range(V):
+        y = c["Y"][v // c["A"]]
+        k, vv = oracle.project(y, c["E"], np.zeros(len(y), bool), c["WF"], c["WKV"],
+                               np.arange(len(y)), L, Hkv, hd, c["theta"])
+        n = int(a2[v])
+        st.set_committed(v, k[:n].transpose(1, 0, 2, 3), vv[:n].transpose(1, 0, 2, 3))
+    draft, target = _tokens_with_lcp(m, B, np.random.default_rng(5))
+    pt = np.tile(np.arange(4, dtype=np.int32), (V, 1))
+    r = oracle.route(draft, target, c["a"] + p0_shift, np.zeros(V, np.int32), pt, 4, mode)
+    oracle.round_update(st, r, c["H"], c["E"], c["WF"], c["WKV"], c["theta"], mode)
+    O, LSE = oracle.attend_state(st, c["Q"], c["Hq"], c["theta"])
+    return r, O, LSE
+
+
+def _train_brute(c):
+    """Per block, from Algorithm 2 directly: committed = recorded rows t < a'
+    projected by plain loops without E at position t; carried = window rows
+    j >= m with E at position a + 1 + j; queries at a' + i; dense softmax with
+    an unshifted exp, KV head = the query head's group."""
+    V, B, L, Hq, Hkv, hd, th = (c["n_resp"] * c["A"], c["B"], c["L"], c["Hq"], c["Hkv"],
+                                c["hd"], c["theta"])
+    G = Hq // Hkv
+    O = np.zeros((L, V, B, Hq, hd))
+    LSE = np.zeros((L, V, B, Hq))
+    for v in range(V):
+        a, u = int(c["a"][v]), int(c["u"][v])
+        m = B - u
+        a2 = a + m + 1
+        rows = [_brute_project_row(c["Y"][v // c["A"]][t], c["E"], False, c["WF"], c["WKV"], t,
+                                   L, Hkv, hd, th) for t in range(a2)]
+        rows += [_brute_project_row(c["H"][v][j], c["E"], True, c["WF"], c["WKV"], a + 1 + j,
+                                    L, Hkv, hd, th) for j in range(m, B)]
+        for layer in range(L):
+            for i in range(B):
+                for h in range(Hq):
+                    g = h // G
+                    q = oracle.rope(c["Q"][layer, v, i, h], a2 + i, th)
+                    wts = np.array([math.exp(float(q @ kv[0][layer, g]) / math.sqrt(hd))
+                                    for kv in rows])
+                    vals = np.array([kv[1][layer, g] for kv in rows])
+                    O[layer, v, i, h] = wts @ vals / wts.sum()
+                    LSE[layer, v, i, h] = math.log(wts.sum())
+    return O, LSE
+
+
+def test_training_second_pass_matches_dense_brute_force():
+    """The oracle's carry_only forward equals the dense per-block recomputation
+    of Algorithm 2's second pass; two plausible mistakes (committing the
+    accepted window rows too, or starting the window at the anchor instead of
+    after it) are each caught by the same comparison."""
+    c = _train_tiny()
+    O_b, L_b = _train_brute(c)
+    r, O, LSE = _train_oracle(c)
+    np.testing.assert_array_equal(r["ctx_len"], c["a"] + (c["B"] - c["u"]) + 1)
+    np.testing.assert_allclose(O, O_b, rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(LSE, L_b, rtol=1e-12, atol=1e-12)
+    # mutant 1: the accepted window rows are committed as well (duplicated keys)
+    _, O1, _ = _train_oracle(c, mode="carry")
+    assert np.abs(O1 - O_b).max() > 1e-3
+    # mutant 2: the window starts at the anchor (p0 = a), so every carried row
+    # and every query sits one position early
+    _, O2, _ = _train_oracle(c, p0_shift=0)
+    assert np.abs(O2 - O_b).max() > 1e-3
+
+
+def test_carry_mass_state_matches_dense_per_head_recomputation():
+    """carry_mass_state, for every (layer, sequence, block row, query head) of a
+    state with three query heads per KV head, equals the share of the dense,
+    unshifted softmax weights on the carried keys, with the KV head of query
+    head h taken as h * Hkv // Hq; an interleaved head mapping is caught."""
+    rng = np.random.default_rng(41)
+    S, L, Hq, Hkv, hd, B = 2, 2, 6, 2, 8, 3
+    st = oracle.State(S, L, Hkv, hd)
+    for s, (n, u) in enumerate(((5, 2), (7, 3))):
+        st.set_committed(s, rng.standard_normal((L, n, Hkv, hd)), rng.standard_normal((L, n, Hkv, hd)))
+        st.uk[s] = rng.standard_normal((L, u, Hkv, hd))
+        st.uv[s] = rng.standard_normal((L, u, Hkv, hd))
+    Q = rng.standard_normal((L, S, B, Hq, hd))
+    mass = oracle.carry_mass_state(st, Q, Hq, 1e4)
+
+    def dense(kv_head_of):
+        out = np.zeros((L, S, B, Hq))
+        for s in range(S):
+            n = st.ck[s].shape[1]
+            for layer in range(L):
+                for i in range(B):
+                    for h in range(Hq):
+                        g = kv_head_of(h)
+                        q = oracle.rope(Q[layer, s, i, h], n + i, 1e4)
+                        wc = [math.exp(float(q @ st.ck[s][layer, t, g]) / math.sqrt(hd))
+                              for t in range(n)]
+                        wu = [math.exp(float(q @ st.uk[s][layer, t, g]) / math.sqrt(hd))
+                              for t in range(st.uk[s].shape[1])]
+                        out[layer, s, i, h] = sum(wu) / (sum(wc) + sum(wu))
+        return out
+
+    np.testing.assert_allclose(mass, dense(lambda h: h * Hkv // Hq), rtol=1e-12, atol=1e-14)
+    assert np.abs(dense(lambda h: h % Hkv) - mass).max() > 1e-3
