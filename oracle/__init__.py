@@ -77,6 +77,84 @@ def accept_len_bits(bits: np.ndarray) -> int:
     return m
 
 
+# Stochastic verification (T = 1) itself: the standard speculative-sampling
+# rule that Appendix A ("Why verification remains valid") relies on.  A
+# proposed token x drawn from the drafter's distribution q is accepted with
+# probability min(1, p(x) / q(x)) under the target's distribution p; at the
+# first rejection the verifier emits a correction drawn from the normalised
+# residual max(0, p - q); when every proposal is accepted it emits a bonus
+# token drawn from p at the position after the block.
+#
+# Both random draws are supplied as 32-bit words so that the oracle and the
+# kernel make the same integer decisions:
+#   * acceptance uses u = (word >> 8) * 2^-24, uniform on [0, 1) with 24 bits;
+#     u * q(x) < p(x) is decided exactly (a 24-bit by 24-bit product is exact
+#     in fp64): u < min(1, p / q) for u < 1, so a token the target gives no
+#     probability is never accepted and p = q accepts every proposal;
+#   * the correction or bonus is drawn by an inverse CDF over fixed-point
+#     weights w(y) = floor(2^32 * d(y)), d(y) = p(y) - q(y) (an fp64
+#     difference of the fp32 inputs) where positive, else 0 (d(y) = p(y) for a
+#     bonus, and for a correction whose weights are all zero); with integer
+#     sums, y is the smallest token whose running sum exceeds
+#     t = floor(word * W / 2^32), W the total.  The weights approximate the
+#     residual to 2^-32 per token.  No weight at all (not a distribution):
+#     no token (-1).
+
+ERR_TOKEN = 9            # a proposed token outside [0, vocab)
+
+
+def accept_test(u_word, p_x, q_x):
+    """Acceptance of one proposal: u * q(x) < p(x) with u = (u_word >> 8) * 2^-24.
+    Vectorised (numpy broadcasting); p, q are fp32 values."""
+    u = (np.asarray(u_word, np.uint64) >> np.uint64(8)).astype(np.float64) * 2.0 ** -24
+    return u * np.asarray(q_x, np.float32).astype(np.float64) < \
+        np.asarray(p_x, np.float32).astype(np.float64)
+
+
+def fixed_weights(p_row, q_row=None):
+    """Fixed-point sampling weights (uint64) of the residual max(0, p - q), or
+    of p itself when q_row is None."""
+    d = np.asarray(p_row, np.float32).astype(np.float64)
+    if q_row is not None:
+        d = d - np.asarray(q_row, np.float32).astype(np.float64)
+    return np.floor(np.where(d > 0, d, 0.0) * 2.0 ** 32).astype(np.uint64)
+
+
+def sample_fixed(w, u_word):
+    """Inverse-CDF draw from fixed-point weights w (uint64): the smallest y
+    with w[0] + ... + w[y] > floor(u_word * W / 2^32); -1 when W = 0."""
+    cum = np.cumsum(np.asarray(w, np.uint64), dtype=np.uint64)
+    W = int(cum[-1])
+    if W == 0:
+        return -1
+    t = (int(u_word) * W) >> 32
+    return int(np.searchsorted(cum, np.uint64(t), side="right"))
+
+
+def verify_sample(draft, p, q, u_words):
+    """T = 1 verification of one window.  draft [B] proposed tokens; p [B+1][V]
+    target probabilities at the B proposal positions and the one after them;
+    q [B][V] drafter probabilities; u_words [B+1] uint32 (acceptance word of
+    each position, then the word of the correction or bonus draw).
+    Returns (m, next_token, status): m = proposals accepted before the first
+    rejection; next_token = the correction (m < B) or the bonus (m = B).  A
+    proposed token outside [0, V) is an error: (0, -1, ERR_TOKEN)."""
+    draft = np.asarray(draft)
+    B, V = len(draft), np.asarray(p).shape[1]
+    if np.any((draft < 0) | (draft >= V)):
+        return 0, -1, ERR_TOKEN
+    m = 0
+    while m < B and bool(accept_test(u_words[m], p[m][draft[m]], q[m][draft[m]])):
+        m += 1
+    if m < B:
+        w = fixed_weights(p[m], q[m])
+        if not w.any():
+            w = fixed_weights(p[m])
+    else:
+        w = fixed_weights(p[B])
+    return m, sample_fixed(w, u_words[B]), OK
+
+
 def route(draft, target, ctx_len, carry_len, page_table, num_pages, mode="carry",
           accept="tokens"):
     """Split every verified window by its accepted prefix (Eq. 1, Algorithm 1).

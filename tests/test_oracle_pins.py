@@ -937,3 +937,155 @@ def test_carry_mass_state_matches_dense_per_head_recomputation():
 
     np.testing.assert_allclose(mass, dense(lambda h: h * Hkv // Hq), rtol=1e-12, atol=1e-14)
     assert np.abs(dense(lambda h: h % Hkv) - mass).max() > 1e-3
+
+
+# ------------------------------------- stochastic verification (T = 1), Appendix A
+#
+# The standard speculative-sampling rule: accept a proposal x ~ q with
+# probability min(1, p(x)/q(x)); at the first rejection emit a token from the
+# normalised residual max(0, p - q); after B acceptances a bonus from p.  Its
+# defining property (the one Appendix A relies on) is that the emitted token
+# is distributed exactly as p.  The pins check the oracle's discrete form of
+# the rule against that property and against closed forms.
+
+from fractions import Fraction  # noqa: E402
+
+_GRID = (np.arange(1 << 24, dtype=np.uint64) << np.uint64(8)).astype(np.uint32)
+
+
+def _softmax32(z):
+    e = np.exp(z - z.max())
+    return (e / e.sum()).astype(np.float32)
+
+
+def _accepted_words(p_x, q_x):
+    """Number of the 2^24 acceptance words for which the oracle accepts."""
+    return int(np.count_nonzero(oracle.accept_test(_GRID, np.float32(p_x), np.float32(q_x))))
+
+
+def _first_word_reaching(w, y):
+    """Smallest 32-bit word whose draw is >= y (draws are non-decreasing in the word)."""
+    lo, hi = 0, 1 << 32
+    while lo < hi:
+        mid = (lo + hi) // 2
+        if oracle.sample_fixed(w, mid) >= y:
+            hi = mid
+        else:
+            lo = mid + 1
+    return lo
+
+
+def _draw_probabilities(w):
+    """Exact probability of every token under a uniform 32-bit word."""
+    V = len(w)
+    edges = [_first_word_reaching(w, y) for y in range(V)] + [1 << 32]
+    return np.array([(edges[y + 1] - edges[y]) / 2.0 ** 32 for y in range(V)])
+
+
+_VERIFY_CASES = [
+    (np.array([0.7, 0.3], np.float32), np.array([0.4, 0.6], np.float32)),
+    (np.array([0.2, 0.5, 0.3], np.float32), np.array([0.6, 0.1, 0.3], np.float32)),
+    (np.array([0.0, 0.25, 0.75], np.float32), np.array([0.5, 0.5, 0.0], np.float32)),
+]
+
+
+def test_accept_share_is_min_one_p_over_q_on_small_vocabularies():
+    """Over the whole grid of acceptance words, proposal x is accepted for
+    exactly min(2^24, ceil(2^24 p(x) / q(x))) of them (u < p/q on a 24-bit
+    grid), and the overall acceptance probability sum_x q(x) min(1, p/q) equals
+    sum_x min(p(x), q(x)) to the grid's resolution."""
+    for p, q in _VERIFY_CASES:
+        tot = 0.0
+        for x in range(len(p)):
+            if q[x] == 0:
+                continue
+            n = _accepted_words(p[x], q[x])
+            exact = Fraction(float(p[x])) / Fraction(float(q[x])) * (1 << 24)
+            want = min(1 << 24, -(-exact.numerator // exact.denominator))   # ceil
+            assert n == want, (p, q, x)
+            tot += float(q[x]) * n / 2.0 ** 24
+        assert abs(tot - float(np.minimum(p, q).sum())) <= len(p) * 2.0 ** -24
+
+
+def test_emitted_token_is_distributed_as_the_target():
+    """One proposal position: the token the verifier emits (the accepted
+    proposal, else the residual draw) has the target's distribution p, to the
+    grids' resolution; drawing the correction from max(0, q - p) instead, or
+    from p itself, is caught."""
+    for p, q in _VERIFY_CASES:
+        V = len(p)
+        acc = np.array([_accepted_words(p[x], q[x]) / 2.0 ** 24 if q[x] > 0 else 0.0
+                        for x in range(V)])
+        reject = float(np.sum(q.astype(np.float64) * (1.0 - acc)))
+
+        def emitted(res_w):
+            return q.astype(np.float64) * acc + reject * _draw_probabilities(res_w)
+
+        got = emitted(oracle.fixed_weights(p, q))
+        np.testing.assert_allclose(got, p.astype(np.float64), rtol=0, atol=4 * V * 2.0 ** -24)
+        assert np.abs(emitted(oracle.fixed_weights(q, p)) - p).max() > 1e-2
+        assert np.abs(emitted(oracle.fixed_weights(p)) - p).max() > 1e-2
+
+
+def test_draws_are_monotone_cover_every_word_and_skip_zero_weights():
+    rng = np.random.default_rng(61)
+    p = _softmax32(rng.standard_normal(40) * 2)
+    q = _softmax32(rng.standard_normal(40) * 2)
+    w = oracle.fixed_weights(p, q)
+    words = np.sort(rng.integers(0, 1 << 32, 2000, dtype=np.uint64))
+    draws = [oracle.sample_fixed(w, int(u)) for u in words]
+    assert all(b >= a for a, b in zip(draws, draws[1:]))
+    probs = _draw_probabilities(w)
+    assert abs(probs.sum() - 1.0) < 1e-12                 # every word yields a token
+    assert np.all(probs[w == 0] == 0)                     # p <= q: never drawn
+    np.testing.assert_allclose(probs, w / w.sum(), rtol=0, atol=2.0 ** -31)
+    assert np.all(w[p.astype(np.float64) <= q.astype(np.float64)] == 0)
+    assert oracle.sample_fixed(np.zeros(5, np.uint64), 123) == -1
+
+
+def test_verify_p_equals_q_accepts_every_proposal():
+    """Identical target and drafter distributions: every proposal is accepted
+    whatever the words, and the bonus comes from p at the position after the
+    block (the first and last tokens of p's support for the extreme words)."""
+    rng = np.random.default_rng(62)
+    B, V = 8, 50
+    for _ in range(20):
+        p = np.stack([_softmax32(rng.standard_normal(V) * 3) for _ in range(B + 1)])
+        p[B, :3] = 0.0
+        p[B, -2:] = 0.0
+        draft = rng.integers(0, V, B)
+        words = rng.integers(0, 1 << 32, B + 1, dtype=np.uint64).astype(np.uint32)
+        m, nxt, st = oracle.verify_sample(draft, p, p[:B], words)
+        assert (m, st) == (B, oracle.OK)
+        assert p[B, nxt] > 0
+        words[B] = 0
+        assert oracle.verify_sample(draft, p, p[:B], words)[1] == 3
+        words[B] = 0xFFFFFFFF
+        assert oracle.verify_sample(draft, p, p[:B], words)[1] == V - 3
+
+
+def test_verify_stops_at_the_first_rejection():
+    """Acceptance words of 0 accept any proposal the target gives probability;
+    a proposal the target gives none is always rejected; the correction is a
+    token whose target probability exceeds the drafter's; positions after the
+    first rejection do not matter; a token outside the vocabulary is an error."""
+    rng = np.random.default_rng(63)
+    B, V = 6, 30
+    for m_want in range(B + 1):
+        p = np.stack([_softmax32(rng.standard_normal(V) * 2) for _ in range(B + 1)])
+        q = np.stack([_softmax32(rng.standard_normal(V) * 2) for _ in range(B)])
+        draft = rng.integers(1, V, B)
+        if m_want < B:
+            p[m_want, draft[m_want]] = 0.0                 # rejected for every word
+        words = np.zeros(B + 1, np.uint32)
+        words[m_want + 1:] = rng.integers(0, 1 << 32, B - m_want, dtype=np.uint64)
+        m, nxt, st = oracle.verify_sample(draft, p, q, words)
+        assert (m, st) == (m_want, oracle.OK)
+        if m < B:
+            assert float(p[m, nxt]) > float(q[m, nxt])
+        bits = np.array([bool(oracle.accept_test(words[j], p[j, draft[j]], q[j, draft[j]]))
+                         for j in range(B)], np.int32)
+        assert oracle.accept_len_bits(bits) == m
+    bad = draft.copy()
+    bad[2] = V
+    assert oracle.verify_sample(bad, p, q, words) == (0, -1, oracle.ERR_TOKEN)
