@@ -18,7 +18,8 @@
  * --------------------------------
  * Ownership: every pointer is caller-owned device memory unless a comment says
  *   "host".  The library allocates nothing, frees nothing, keeps no pointer
- *   past the call and holds no global state besides per-device attributes.
+ *   past the call and holds no global state besides per-device attributes
+ *   and the launch-shape overrides of carryover_set_tuning.
  * Streams: every call only enqueues work on `stream` and returns; nothing
  *   synchronises except carryover_read_status.  Calls on distinct states are
  *   re-entrant.
@@ -75,8 +76,10 @@ enum {
   CO_ERR_HIP = 6,           /* a HIP runtime call or launch failed             */
   CO_ERR_LENGTH = 7,        /* device: ctx_len outside [0, max_pages_per_seq * 16] or
                                carry_len outside [0, 16 * ceil(block / 16)]        */
-  CO_ERR_GROUP = 8          /* device: a sequence's committed page ids differ from its
+  CO_ERR_GROUP = 8,         /* device: a sequence's committed page ids differ from its
                                group's first sequence (attention backward)          */
+  CO_ERR_TOKEN = 9          /* device: a proposed token outside [0, vocab)
+                               (carryover_verify_sample)                            */
 };
 
 enum { CO_DTYPE_F32 = 0, CO_DTYPE_BF16 = 1 };
@@ -218,6 +221,11 @@ co_status carryover_fold_e(const co_dims* dims, const co_weights* w, float* f_e,
  * key set gives out = 0 and lse = -inf.  `ws` must hold
  * carryover_workspace_bytes(dims, CO_WS_ATTENTION) bytes (scratch; any
  * contents).  A workspace serves one call at a time.
+ * Device errors: CO_ERR_LENGTH (ctx_len outside [0, max_pages_per_seq * 16]
+ * or carry_len outside [0, 16 * ceil(block / 16)]): that sequence attends to
+ * no key (out 0, lse -inf); CO_ERR_PAGE_RANGE (a page id of a committed key
+ * outside [0, num_pages)): the keys of that page are left out.  The other
+ * sequences proceed.
  */
 co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int32_t layer_count,
                                   const void* q, const co_state* state, void* out, float* lse,
@@ -229,8 +237,49 @@ co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int3
  * every layer's queries q [num_layers][num_seqs][block][num_q_heads][head_dim].
  * `scratch` receives the route result.  All state stays on the device; there
  * is no host synchronisation.  `ws`: carryover_workspace_bytes(dims,
- * CO_WS_ROUND) bytes of scratch.
+ * CO_WS_ROUND) bytes of scratch, 256-byte aligned.  flags: those of
+ * carryover_route and drafter_block_attention.  Every host check of the three
+ * steps (the weights' optional pointers included) is made before the first
+ * launch, so a non-zero return leaves the state untouched.  Device errors:
+ * those of the three steps.
  */
+co_status carryover_round(const co_dims* dims, const co_weights* w, const void* hidden,
+                          const int32_t* draft_tok, const int32_t* target_tok, const void* q,
+                          co_state* state, const co_route* scratch, void* out, float* lse,
+                          uint32_t flags, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Stochastic verification (T = 1): the acceptance decision and the
+ * correction or bonus token of the standard speculative-sampling rule that
+ * Appendix A ("Why verification remains valid") relies on.  For every
+ * sequence s, with the proposals x_j = draft_tok[s][j] (j < block), the
+ * target's probabilities p_target [num_seqs][block + 1][vocab] (fp32; row
+ * block is the position after the window) and the drafter's q_draft
+ * [num_seqs][block][vocab] (fp32):
+ *   proposal j is accepted iff u_j * q_j(x_j) < p_j(x_j), with
+ *     u_j = (words[s][j] >> 8) * 2^-24 (decided exactly);
+ *   m = the accepted proposals before the first rejection;
+ *   accept_bits[s][j] = (j < m), int32 [num_seqs][block]: the accept decisions
+ *     carryover_route and carryover_round take under CO_ROUTE_ACCEPT_BITS;
+ *   accept_len[s] = m;
+ *   next_tok[s] = the correction (m < block), drawn from max(0, p_m - q_m)
+ *     normalised, or the bonus (m = block), drawn from p_block: with
+ *     w(y) = floor(2^32 * d(y)), d(y) = p(y) - q(y) in fp64 where positive
+ *     (p(y) for the bonus, and for a correction whose weights are all zero),
+ *     the smallest y whose running sum of w exceeds
+ *     floor(words[s][block] * W / 2^32), W the total; -1 if W = 0.
+ * words: uint32 [num_seqs][block + 1] of uniform random bits.  Only num_seqs
+ * and block of dims are used (the rest must still be valid).  status: one
+ * int32 (e.g. a state's status word).  All pointers device, 4-byte aligned.
+ * Device errors: CO_ERR_TOKEN (a proposal outside [0, vocab)); that sequence
+ * gets m = 0, all bits 0 and next_tok -1.
+ */
+co_status carryover_verify_sample(const co_dims* dims, int32_t vocab, const int32_t* draft_tok,
+                                  const float* p_target, const float* q_draft,
+                                  const uint32_t* words, int32_t* accept_bits,
+                                  int32_t* accept_len, int32_t* next_tok, int32_t* status,
+                                  hipStream_t stream);
+
 /*
  * Reverse mode of drafter_block_attention: the training side of the second
  * drafter pass (Algorithm 2, whose loss is differentiated through the second
@@ -332,10 +381,6 @@ co_status drafter_self_merge(const co_dims* dims, int32_t layer_begin, int32_t l
                              const co_state* state, void* out, float* lse, uint32_t flags,
                              hipStream_t stream);
 
-co_status carryover_round(const co_dims* dims, const co_weights* w, const void* hidden,
-                          const int32_t* draft_tok, const int32_t* target_tok, const void* q,
-                          co_state* state, const co_route* scratch, void* out, float* lse,
-                          uint32_t flags, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Write already-projected (keys already rotated) committed rows of one
@@ -356,6 +401,29 @@ size_t carryover_workspace_bytes(const co_dims* dims, int32_t which);
 
 /* Synchronise `stream` and copy *state->status to *host_out (host pointer). */
 co_status carryover_read_status(const co_state* state, int32_t* host_out, hipStream_t stream);
+
+/*
+ * Launch-shape overrides, for tuning and for tests that force every kernel
+ * variant.  Results never depend on them (beyond rounding order).  `value`
+ * -1 restores the automatic choice.  Process-wide: set them while no call is
+ * in flight.  Knobs:
+ *   CO_TUNE_GEMM_WIDE_VARIANT       large-tile projection GEMM variant 0..5
+ *   CO_TUNE_GEMM_NO_WIDE            1: never the large-tile projection GEMM
+ *   CO_TUNE_PROJECT_FUSED_MIN_ROWS  rows from which the fused small-width
+ *                                   projection runs (default 4096)
+ *   CO_TUNE_ATTN_WAVE               0/1: bf16 attention by per-wavefront slices
+ *   CO_TUNE_ATTN_WORKGROUPS         bf16 attention workgroups (or slices)
+ *   CO_TUNE_ATTN_ROUND_TILES        tiles per wavefront per round, persistent
+ *                                   attention kernel
+ *   CO_TUNE_ATTN_GROUP_SPLIT_TILES  committed tiles per share, grouped-prefix
+ *                                   attention
+ * Returns CO_ERR_INVALID_ARG for an unknown knob.  Workspace sizes follow the
+ * overrides in force when carryover_workspace_bytes is called.
+ */
+enum { CO_TUNE_GEMM_WIDE_VARIANT = 0, CO_TUNE_GEMM_NO_WIDE = 1, CO_TUNE_PROJECT_FUSED_MIN_ROWS = 2,
+       CO_TUNE_ATTN_WAVE = 3, CO_TUNE_ATTN_WORKGROUPS = 4, CO_TUNE_ATTN_ROUND_TILES = 5,
+       CO_TUNE_ATTN_GROUP_SPLIT_TILES = 6, CO_TUNE_COUNT = 7 };
+co_status carryover_set_tuning(int32_t knob, int64_t value);
 
 /* Static message for a status code. */
 const char* carryover_status_string(co_status status);

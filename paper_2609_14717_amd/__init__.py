@@ -17,12 +17,16 @@ LIB_PATH = os.path.join(HERE, "libcarryover.so")
 
 CO_OK, CO_ERR_INVALID_ARG, CO_ERR_UNSUPPORTED, CO_ERR_WORKSPACE = 0, 1, 2, 3
 CO_ERR_CAPACITY, CO_ERR_PAGE_RANGE, CO_ERR_HIP, CO_ERR_LENGTH, CO_ERR_GROUP = 4, 5, 6, 7, 8
+CO_ERR_TOKEN = 9
 CO_DTYPE_F32, CO_DTYPE_BF16 = 0, 1
 CO_BASELINE_MODE, CO_ROUTE_ACCEPT_ALL, CO_ROUTE_CARRY_ONLY, CO_Q_PREROTATED = 1, 2, 4, 8
 CO_ATTN_SHARED_PREFIX = 16
 CO_ROUTE_ACCEPT_BITS = 32
 CO_WS_PROJECT, CO_WS_ATTENTION, CO_WS_ROUND, CO_WS_ATTENTION_BACKWARD = 0, 1, 2, 3
 CO_WS_PROJECT_BACKWARD = 4
+# launch-shape overrides (carryover_set_tuning)
+TUNING = {"gemm_wide_variant": 0, "gemm_no_wide": 1, "project_fused_min_rows": 2, "attn_wave": 3,
+          "attn_workgroups": 4, "attn_round_tiles": 5, "attn_group_split_tiles": 6}
 SKIP = -(2 ** 31)
 PAGE = 16
 
@@ -98,6 +102,9 @@ def lib():
                                    _P(co_state), _v, _v, ctypes.c_uint32, _v],
             "carryover_import_kv": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _v,
                                     _v, _P(co_state), _v],
+            "carryover_verify_sample": [_P(co_dims), ctypes.c_int32, _v, _v, _v, _v, _v, _v, _v,
+                                        _v, _v],
+            "carryover_set_tuning": [ctypes.c_int32, ctypes.c_int64],
             "carryover_workspace_bytes": [_P(co_dims), ctypes.c_int32],
             "carryover_read_status": [_P(co_state), _P(ctypes.c_int32), _v],
             "carryover_status_string": [ctypes.c_int32],
@@ -115,7 +122,7 @@ def lib():
 EXPORTED = ("carryover_route", "carryover_project_kv", "drafter_block_attention",
             "carryover_round", "carryover_fold_e", "drafter_carry_mass", "drafter_self_merge",
             "drafter_block_attention_backward", "carryover_project_kv_backward",
-            "carryover_import_kv",
+            "carryover_import_kv", "carryover_verify_sample", "carryover_set_tuning",
             "carryover_workspace_bytes", "carryover_read_status", "carryover_status_string")
 
 
@@ -288,6 +295,28 @@ def carryover_import_kv(dims, seq, pos0, k_rows, v_rows, st, stream=None):
     _check(lib().carryover_import_kv(ctypes.byref(dims), seq, pos0, n, _ptr(k_rows),
                                      _ptr(v_rows), ctypes.byref(s), _stream(stream)),
            "carryover_import_kv")
+
+
+def carryover_verify_sample(dims, vocab, draft_tok, p_target, q_draft, words, accept_bits,
+                            accept_len, next_tok, status, stream=None):
+    """T = 1 verification: accept decisions, accepted length and the correction
+    or bonus token of every sequence (see include/carryover.h)."""
+    _check(lib().carryover_verify_sample(ctypes.byref(dims), vocab, _ptr(draft_tok),
+                                         _ptr(p_target), _ptr(q_draft), _ptr(words),
+                                         _ptr(accept_bits), _ptr(accept_len), _ptr(next_tok),
+                                         _ptr(status), _stream(stream)),
+           "carryover_verify_sample")
+
+
+def set_tuning(name, value):
+    """Override a launch shape (``TUNING`` names it); -1 or None restores the default."""
+    _check(lib().carryover_set_tuning(TUNING[name], -1 if value is None else int(value)),
+           "carryover_set_tuning")
+
+
+def reset_tuning():
+    for name in TUNING:
+        set_tuning(name, -1)
 
 
 def carryover_read_status(st, stream=None) -> int:

@@ -13,8 +13,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libcarryover.so")
-SOURCES = ["route.hip", "project.hip", "attention.hip", "segments.hip", "backward.hip",
-           "capi.hip"]
+SOURCES = ["route.hip", "verify.hip", "project.hip", "attention.hip", "segments.hip",
+           "backward.hip", "capi.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # Packed-fp32 VALU ops are kept out of the generated code.

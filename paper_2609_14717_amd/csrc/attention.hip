@@ -1356,16 +1356,13 @@ __device__ __forceinline__ int keys_in(int limit, int t, int h) {
   return min(kPage, max(0, limit - (2 * t + h) * kPage));
 }
 
-// Committed tiles per share of a grouped launch (CO_ATTN_GROUP_SPLIT_TILES
-// overrides it for tuning and tests), and the number of shares that covers the
-// longest sequence the page table allows.
+// Committed tiles per share of a grouped launch (CO_TUNE_ATTN_GROUP_SPLIT_TILES
+// overrides it), and the number of shares that covers the longest sequence the
+// page table allows.
 constexpr int kGroupSplitTiles = 128;
 int group_split_tiles() {
-  if (const char* env = getenv("CO_ATTN_GROUP_SPLIT_TILES")) {
-    const int v = atoi(env);
-    if (v >= 1 && v <= 4096) return v;
-  }
-  return kGroupSplitTiles;
+  const int64_t v = tuning(CO_TUNE_ATTN_GROUP_SPLIT_TILES);
+  return v >= 1 && v <= 4096 ? static_cast<int>(v) : kGroupSplitTiles;
 }
 int group_splits(int max_pages) {
   const int tiles = (max_pages + 1) / 2, sp = group_split_tiles();
@@ -1912,10 +1909,10 @@ __global__ __launch_bounds__(64 * wave_waves(HD), 1) void attn_wave_kernel(
 
 // Whether a launch takes the per-wavefront slices path where the shape allows
 // it: by default at head_dim 128 with 64 query rows (measured faster at every
-// such shape); CO_ATTN_WAVE=0/1 chooses, for tests and tuning.
+// such shape); CO_TUNE_ATTN_WAVE chooses.
 static bool wave_slices_enabled(int hd) {
-  if (const char* env = getenv("CO_ATTN_WAVE")) return atoi(env) != 0;
-  return hd == 128;
+  const int64_t v = tuning(CO_TUNE_ATTN_WAVE);
+  return v >= 0 ? v != 0 : hd == 128;
 }
 
 AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pages, int num_pages,
@@ -1933,14 +1930,11 @@ AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pa
     const int rtm = hd == 64 ? kAttnRoundTiles64 : kAttnRoundTiles128;
     p.n_wg = num_cus;
     p.round_tiles = rtm;
-    if (const char* env = getenv("CO_ATTN_WORKGROUPS")) {     // tuning and test override
-      const int v = atoi(env);
-      if (v >= 1 && v <= kMaxMergeSlices) p.n_wg = v;
-    }
-    if (const char* env = getenv("CO_ATTN_ROUND_TILES")) {    // tuning and test override
-      const int v = atoi(env);
-      if (v >= 1 && v <= rtm) p.round_tiles = v;
-    }
+    const int64_t wg_override = tuning(CO_TUNE_ATTN_WORKGROUPS);
+    const bool wg_forced = wg_override >= 1 && wg_override <= kMaxMergeSlices;
+    if (wg_forced) p.n_wg = static_cast<int>(wg_override);
+    const int64_t rt_override = tuning(CO_TUNE_ATTN_ROUND_TILES);
+    if (rt_override >= 1 && rt_override <= rtm) p.round_tiles = static_cast<int>(rt_override);
     p.hdr_floats = (S + 1 + p.n_wg + 1 + 63) / 64 * 64;
     const size_t rec = static_cast<size_t>(p.nq_pad) * (hd + 2);
     const size_t records = (static_cast<size_t>(p.n_wg) + static_cast<size_t>(L) * Hkv * S) * rec;
@@ -1961,7 +1955,7 @@ AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pa
     const int nw_h = wave_waves(hd);
     const int64_t cap_tiles = static_cast<int64_t>(L) * Hkv * S * ((max_pages + 1) / 2 + (cp + 1) / 2);
     int n_sl = p.n_wg * nw_h;
-    if (getenv("CO_ATTN_WORKGROUPS") == nullptr) {
+    if (!wg_forced) {
       // 7/8 of the CUs: measured faster than all of them at head_dim 128 (fewer
       // concurrent page streams, fewer records; 0.70 vs 0.69 of peak at the
       // 5-layer long chain)

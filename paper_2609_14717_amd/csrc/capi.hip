@@ -8,6 +8,15 @@
 
 using namespace co;
 
+namespace co {
+
+// Launch-shape overrides (carryover_set_tuning); -1 = automatic.
+static int64_t g_tuning[CO_TUNE_COUNT] = {-1, -1, -1, -1, -1, -1, -1};
+
+int64_t tuning(int knob) { return knob >= 0 && knob < CO_TUNE_COUNT ? g_tuning[knob] : -1; }
+
+}  // namespace co
+
 namespace {
 
 constexpr int kMaxDevices = 64;
@@ -103,6 +112,90 @@ AttnPlan attention_plan(const co_dims* d) {
 
 co_status hip_status(hipError_t e) { return e == hipSuccess ? CO_OK : CO_ERR_HIP; }
 
+// Host checks of each step, shared by the step's own entry point and by
+// carryover_round, which makes all of them before its first launch.  dims are
+// already checked.
+co_status validate_route(const co_dims* d, const int32_t* draft_tok, const int32_t* target_tok,
+                         uint32_t flags, const co_state* st, const co_route* out) {
+  (void)d;
+  if (!st || !st->ctx_len || !st->carry_len || !st->page_table || !st->status || !route_ok(out))
+    return CO_ERR_INVALID_ARG;
+  if (!(flags & CO_ROUTE_ACCEPT_ALL) &&
+      (!draft_tok || (!target_tok && !(flags & CO_ROUTE_ACCEPT_BITS))))
+    return CO_ERR_INVALID_ARG;
+  return CO_OK;
+}
+
+co_status validate_project(const co_dims* d, const co_weights* w, const void* hidden,
+                           const co_route* route, const co_state* st, const void* ws,
+                           size_t ws_bytes) {
+  if (!w || !w->w_f || !w->w_kv || !w->e_carry || !hidden || !route_ok(route) || !state_ok(st))
+    return CO_ERR_INVALID_ARG;
+  if (!aligned(hidden, 16) || !aligned(w->w_f, 16) || !aligned(w->w_kv, 16) ||
+      !aligned(w->e_carry, 16) || !aligned(w->f_e, 16) || !aligned(w->w_f_carry, 16) ||
+      !aligned(w->z_norm, 4) || !aligned(w->k_norm, 4))
+    return CO_ERR_INVALID_ARG;
+  if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
+  if (ws_bytes < project_plan(d).total) return CO_ERR_WORKSPACE;
+  return CO_OK;
+}
+
+co_status validate_attention(const co_dims* d, int32_t layer_begin, int32_t layer_count,
+                             const void* q, const co_state* st, const void* out, const float* lse,
+                             const void* ws, size_t ws_bytes) {
+  co_status s = check_attention_dims(d);
+  if (s != CO_OK) return s;
+  if (layer_begin < 0 || layer_count < 0 || layer_begin + layer_count > d->num_layers)
+    return CO_ERR_INVALID_ARG;
+  if (!q || !out || !state_ok(st) || !aligned(q, 16) || !aligned(out, 16) ||
+      (lse && !aligned(lse, 4)))
+    return CO_ERR_INVALID_ARG;
+  if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
+  if (ws_bytes < attention_plan(d).bytes) return CO_ERR_WORKSPACE;
+  return CO_OK;
+}
+
+co_status enqueue_route(const co_dims* dims, const int32_t* draft_tok, const int32_t* target_tok,
+                        uint32_t flags, co_state* state, const co_route* out, hipStream_t stream) {
+  RouteArgs a{};
+  a.S = dims->num_seqs;
+  a.B = dims->block;
+  a.max_pages = dims->max_pages_per_seq;
+  a.num_pages = dims->num_pages;
+  a.flags = flags;
+  a.draft = draft_tok;
+  a.target = target_tok;
+  a.ctx_len = state->ctx_len;
+  a.carry_len = state->carry_len;
+  a.page_table = state->page_table;
+  a.accept_len = out->accept_len;
+  a.row_pos = out->row_pos;
+  a.row_dst = out->row_dst;
+  a.status = state->status;
+  return hip_status(launch_route(a, stream));
+}
+
+co_status enqueue_project(const co_dims* dims, const co_weights* w, const void* hidden,
+                          const co_route* route, const co_state* state, void* ws,
+                          hipStream_t stream) {
+  ProjectArgs a{};
+  a.M = dims->num_seqs * dims->block;
+  a.Dcat = dims->feat_dim;
+  a.d = dims->model_dim;
+  a.dtype = dims->dtype;
+  a.hidden = hidden;
+  a.wf = w->w_f;
+  a.wkv = w->w_kv;
+  a.e = w->e_carry;
+  a.fe = dims->dtype == CO_DTYPE_BF16 ? w->f_e : nullptr;
+  a.wfc = w->w_f_carry;
+  a.znorm = w->z_norm;
+  a.dst = make_dest(dims, route, state);
+  a.dst.knorm = w->k_norm;
+  a.ws = ws;
+  return hip_status(launch_project(a, project_plan(dims), stream));
+}
+
 co_status do_attention(const co_dims* d, int32_t layer_begin, int32_t layer_count, const void* q,
                        const co_state* st, void* out, float* lse, uint32_t flags, void* ws,
                        hipStream_t stream) {
@@ -165,28 +258,8 @@ co_status carryover_route(const co_dims* dims, const int32_t* draft_tok, const i
                           hipStream_t stream) {
   co_status s = check_dims(dims);
   if (s != CO_OK) return s;
-  if (!state || !state->ctx_len || !state->carry_len || !state->page_table || !state->status ||
-      !route_ok(out))
-    return CO_ERR_INVALID_ARG;
-  if (!(flags & CO_ROUTE_ACCEPT_ALL) &&
-      (!draft_tok || (!target_tok && !(flags & CO_ROUTE_ACCEPT_BITS))))
-    return CO_ERR_INVALID_ARG;
-  RouteArgs a{};
-  a.S = dims->num_seqs;
-  a.B = dims->block;
-  a.max_pages = dims->max_pages_per_seq;
-  a.num_pages = dims->num_pages;
-  a.flags = flags;
-  a.draft = draft_tok;
-  a.target = target_tok;
-  a.ctx_len = state->ctx_len;
-  a.carry_len = state->carry_len;
-  a.page_table = state->page_table;
-  a.accept_len = out->accept_len;
-  a.row_pos = out->row_pos;
-  a.row_dst = out->row_dst;
-  a.status = state->status;
-  return hip_status(launch_route(a, stream));
+  if ((s = validate_route(dims, draft_tok, target_tok, flags, state, out)) != CO_OK) return s;
+  return enqueue_route(dims, draft_tok, target_tok, flags, state, out, stream);
 }
 
 co_status carryover_project_kv(const co_dims* dims, const co_weights* w, const void* hidden,
@@ -194,31 +267,8 @@ co_status carryover_project_kv(const co_dims* dims, const co_weights* w, const v
                                size_t ws_bytes, hipStream_t stream) {
   co_status s = check_dims(dims);
   if (s != CO_OK) return s;
-  if (!w || !w->w_f || !w->w_kv || !w->e_carry || !hidden || !route_ok(route) || !state_ok(state))
-    return CO_ERR_INVALID_ARG;
-  if (!aligned(hidden, 16) || !aligned(w->w_f, 16) || !aligned(w->w_kv, 16) ||
-      !aligned(w->e_carry, 16) || !aligned(w->f_e, 16) || !aligned(w->w_f_carry, 16) ||
-      !aligned(w->z_norm, 4) || !aligned(w->k_norm, 4))
-    return CO_ERR_INVALID_ARG;
-  const ProjectPlan p = project_plan(dims);
-  if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
-  if (ws_bytes < p.total) return CO_ERR_WORKSPACE;
-  ProjectArgs a{};
-  a.M = dims->num_seqs * dims->block;
-  a.Dcat = dims->feat_dim;
-  a.d = dims->model_dim;
-  a.dtype = dims->dtype;
-  a.hidden = hidden;
-  a.wf = w->w_f;
-  a.wkv = w->w_kv;
-  a.e = w->e_carry;
-  a.fe = dims->dtype == CO_DTYPE_BF16 ? w->f_e : nullptr;
-  a.wfc = w->w_f_carry;
-  a.znorm = w->z_norm;
-  a.dst = make_dest(dims, route, state);
-  a.dst.knorm = w->k_norm;
-  a.ws = ws;
-  return hip_status(launch_project(a, p, stream));
+  if ((s = validate_project(dims, w, hidden, route, state, ws, ws_bytes)) != CO_OK) return s;
+  return enqueue_project(dims, w, hidden, route, state, ws, stream);
 }
 
 co_status carryover_fold_e(const co_dims* dims, const co_weights* w, float* f_e,
@@ -237,15 +287,9 @@ co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int3
                                   uint32_t flags, void* ws, size_t ws_bytes, hipStream_t stream) {
   co_status s = check_dims(dims);
   if (s != CO_OK) return s;
-  if ((s = check_attention_dims(dims)) != CO_OK) return s;
-  if (layer_begin < 0 || layer_count < 0 || layer_begin + layer_count > dims->num_layers)
-    return CO_ERR_INVALID_ARG;
-  if (!q || !out || !state_ok(state) || !aligned(q, 16) || !aligned(out, 16) ||
-      (lse && !aligned(lse, 4)))
-    return CO_ERR_INVALID_ARG;
-  const AttnPlan p = attention_plan(dims);
-  if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
-  if (ws_bytes < p.bytes) return CO_ERR_WORKSPACE;
+  if ((s = validate_attention(dims, layer_begin, layer_count, q, state, out, lse, ws,
+                              ws_bytes)) != CO_OK)
+    return s;
   return do_attention(dims, layer_begin, layer_count, q, state, out, lse, flags, ws, stream);
 }
 
@@ -426,24 +470,54 @@ co_status carryover_round(const co_dims* dims, const co_weights* w, const void* 
                           uint32_t flags, void* ws, size_t ws_bytes, hipStream_t stream) {
   co_status s = check_dims(dims);
   if (s != CO_OK) return s;
-  if ((s = check_attention_dims(dims)) != CO_OK) return s;
-  if (!w || !w->w_f || !w->w_kv || !w->e_carry || !hidden || !q || !out || !route_ok(scratch) ||
-      !state_ok(state))
-    return CO_ERR_INVALID_ARG;
-  if (!(flags & CO_ROUTE_ACCEPT_ALL) &&
-      (!draft_tok || (!target_tok && !(flags & CO_ROUTE_ACCEPT_BITS))))
-    return CO_ERR_INVALID_ARG;
-  if (!aligned(hidden, 16) || !aligned(w->w_f, 16) || !aligned(w->w_kv, 16) ||
-      !aligned(w->e_carry, 16) || !aligned(q, 16) || !aligned(out, 16))
-    return CO_ERR_INVALID_ARG;
-  if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
-  if (ws_bytes < carryover_workspace_bytes(dims, CO_WS_ROUND)) return CO_ERR_WORKSPACE;
-  if ((s = carryover_route(dims, draft_tok, target_tok, flags, state, scratch, stream)) != CO_OK)
+  // every step's host checks first: a failure must leave the state untouched
+  if ((s = validate_route(dims, draft_tok, target_tok, flags, state, scratch)) != CO_OK) return s;
+  if ((s = validate_project(dims, w, hidden, scratch, state, ws, ws_bytes)) != CO_OK) return s;
+  const size_t pw = project_plan(dims).total;   // a multiple of 256
+  void* attn_ws = static_cast<char*>(ws) + pw;
+  if ((s = validate_attention(dims, 0, dims->num_layers, q, state, out, lse, attn_ws,
+                              ws_bytes - pw)) != CO_OK)
     return s;
-  if ((s = carryover_project_kv(dims, w, hidden, scratch, state, ws, ws_bytes, stream)) != CO_OK)
+  if ((s = enqueue_route(dims, draft_tok, target_tok, flags, state, scratch, stream)) != CO_OK)
     return s;
-  void* attn_ws = static_cast<char*>(ws) + project_plan(dims).total;
+  if ((s = enqueue_project(dims, w, hidden, scratch, state, ws, stream)) != CO_OK) return s;
   return do_attention(dims, 0, dims->num_layers, q, state, out, lse, flags, attn_ws, stream);
+}
+
+co_status carryover_verify_sample(const co_dims* dims, int32_t vocab, const int32_t* draft_tok,
+                                  const float* p_target, const float* q_draft,
+                                  const uint32_t* words, int32_t* accept_bits,
+                                  int32_t* accept_len, int32_t* next_tok, int32_t* status,
+                                  hipStream_t stream) {
+  co_status s = check_dims(dims);
+  if (s != CO_OK) return s;
+  if (vocab < 1 || dims->block > 1024 ||
+      static_cast<int64_t>(dims->num_seqs) * (dims->block + 1) * vocab > (int64_t{1} << 40))
+    return CO_ERR_UNSUPPORTED;
+  if (!draft_tok || !p_target || !q_draft || !words || !accept_bits || !accept_len || !next_tok ||
+      !status || !aligned(draft_tok, 4) || !aligned(p_target, 4) || !aligned(q_draft, 4) ||
+      !aligned(words, 4) || !aligned(accept_bits, 4) || !aligned(accept_len, 4) ||
+      !aligned(next_tok, 4) || !aligned(status, 4))
+    return CO_ERR_INVALID_ARG;
+  VerifyArgs a{};
+  a.S = dims->num_seqs;
+  a.B = dims->block;
+  a.V = vocab;
+  a.draft = draft_tok;
+  a.p = p_target;
+  a.q = q_draft;
+  a.words = words;
+  a.accept_bits = accept_bits;
+  a.accept_len = accept_len;
+  a.next_tok = next_tok;
+  a.status = status;
+  return hip_status(launch_verify(a, stream));
+}
+
+co_status carryover_set_tuning(int32_t knob, int64_t value) {
+  if (knob < 0 || knob >= CO_TUNE_COUNT) return CO_ERR_INVALID_ARG;
+  g_tuning[knob] = value < 0 ? -1 : value;
+  return CO_OK;
 }
 
 co_status carryover_import_kv(const co_dims* dims, int32_t seq, int32_t pos0, int32_t n_rows,
@@ -479,6 +553,7 @@ const char* carryover_status_string(co_status status) {
     case CO_ERR_HIP: return "HIP runtime error";
     case CO_ERR_LENGTH: return "invalid sequence length";
     case CO_ERR_GROUP: return "page rows differ within a sequence group";
+    case CO_ERR_TOKEN: return "proposed token outside the vocabulary";
     default: return "unknown status";
   }
 }

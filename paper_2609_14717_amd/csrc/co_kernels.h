@@ -169,7 +169,24 @@ struct SelfArgs {
   int32_t* status;
 };
 
+// Stochastic verification (T = 1): accept decisions and the correction or bonus.
+struct VerifyArgs {
+  int S, B, V;
+  const int32_t* draft;    // [S][B]
+  const float* p;          // [S][B + 1][V]
+  const float* q;          // [S][B][V]
+  const uint32_t* words;   // [S][B + 1]
+  int32_t* accept_bits;    // [S][B]
+  int32_t* accept_len;     // [S]
+  int32_t* next_tok;       // [S]
+  int32_t* status;
+};
+
+// Launch-shape override in force (-1: automatic); see carryover_set_tuning.
+int64_t tuning(int knob);
+
 hipError_t launch_route(const RouteArgs& a, hipStream_t stream);
+hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream);
 hipError_t launch_self_merge(const SelfArgs& a, int layer_count, int dtype, hipStream_t stream);
 hipError_t launch_carry_mass(const MassArgs& a, int layer_count, int dtype, hipStream_t stream);
 hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_t stream);

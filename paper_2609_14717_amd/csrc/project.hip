@@ -1076,9 +1076,9 @@ bool pick_wide(int M, int N, int K, int num_cus, int* tile, int* split) {
   if (M < 256 || K % 64 != 0) return false;
   double best = 1e30;
   int bv = -1, bs = 1;
-  const char* force = getenv("CO_GEMM_WIDE_VARIANT");
+  const int64_t force = tuning(CO_TUNE_GEMM_WIDE_VARIANT);
   for (int v = 0; v < kWideVariants; ++v) {
-    if (force != nullptr && atoi(force) != v) continue;
+    if (force >= 0 && force != v) continue;
     const int64_t tiles = static_cast<int64_t>((M + kWideBM[v] - 1) / kWideBM[v]) *
                           ((N + kWideBN[v] - 1) / kWideBN[v]);
     // relative main-loop rates measured on MI355X, each variant timed alone at
@@ -1090,7 +1090,7 @@ bool pick_wide(int M, int N, int K, int num_cus, int* tile, int* split) {
       const int kps = split_len(K, s, kWide + v);
       if (kps < 256 || (K + kps - 1) / kps != s) continue;
       const int64_t wgs = tiles * s;
-      if (wgs < num_cus / 2 && force == nullptr) continue;
+      if (wgs < num_cus / 2 && force < 0) continue;
       const int64_t waves = (wgs + num_cus - 1) / num_cus;
       // main loop at the per-CU rate measured with operands streaming from HBM,
       // or the weights streamed from HBM once per row tile, whichever is longer
@@ -1115,7 +1115,7 @@ bool pick_wide(int M, int N, int K, int num_cus, int* tile, int* split) {
 }
 
 void pick_gemm(int M, int N, int K, bool kv, int hd, int num_cus, int* tile, int* split) {
-  if (getenv("CO_GEMM_NO_WIDE") == nullptr && pick_wide(M, N, K, num_cus, tile, split)) return;
+  if (tuning(CO_TUNE_GEMM_NO_WIDE) <= 0 && pick_wide(M, N, K, num_cus, tile, split)) return;
   const int narrow = (!kv || hd == 64) ? 0 : 1;
   int cand[3], nc = 0;
   if (M > 64) cand[nc++] = 3;
@@ -1148,11 +1148,8 @@ constexpr int kF32SplitK = 64;   // K per split of the fp32 GEMM
 // Rows from which the fused small-width projection is used: below, the K-split
 // two-product path spreads the weight reads over more workgroups.
 static int fused_min_rows() {
-  if (getenv("CO_PROJECT_NO_FUSED")) return INT32_MAX;          // test override
-  if (const char* env = getenv("CO_PROJECT_FUSED_MIN_ROWS")) {   // test and tuning override
-    const int v = atoi(env);
-    if (v >= 1) return v;
-  }
+  const int64_t v = tuning(CO_TUNE_PROJECT_FUSED_MIN_ROWS);
+  if (v >= 1) return v < INT32_MAX ? static_cast<int>(v) : INT32_MAX;
   return 4096;
 }
 

@@ -33,6 +33,7 @@ ST_WFC = 16             # the separate carry projector (a variant next to the pa
 ST_ZNORM, ST_KSELF, ST_VSELF = 17, 18, 19   # RMS-norm gain offsets; block self K/V
 ST_KNORM = 20           # per-head key RMS-norm gain offsets
 ST_DOUT = 21            # gradient of a loss with respect to the attention output
+ST_VLOGIT, ST_VNOISE, ST_VDRAW, ST_VWORD = 22, 23, 24, 25   # T = 1 verification inputs
 
 
 @dataclass(frozen=True)
@@ -290,3 +291,38 @@ def host_block(w: Workload, spec, dtype: str | None = None) -> np.ndarray:
     from . import normal_block
     st, shape, strides, base, sigma = spec
     return normal_block(w.key(st), shape, strides, base, sigma, dtype or w.dtype)
+
+
+# ------------------------------------------------ T = 1 verification inputs
+
+def verify_inputs(w: Workload, rnd: int, vocab: int, S: int | None = None,
+                  sigma_target: float = 2.0, sigma_gap: float = 1.0):
+    """Inputs of stochastic verification for round ``rnd``: the target's
+    distributions p [S][B+1][V] (softmax of logits ~ N(0, sigma_target^2)), the
+    drafter's q [S][B][V] (softmax of the target logits plus N(0, sigma_gap^2)
+    noise, so that the two disagree as a trained drafter and its target do),
+    proposals x_j drawn from q_j [S][B], and the verifier's uniform words
+    [S][B+1] (uint32).  p and q are fp32; their softmax is taken in fp64."""
+    from . import normal_f32
+    S = w.S if S is None else S
+    B, V = w.B, vocab
+    base = rnd * S * (B + 1) * V
+    idx = base + np.arange(S * (B + 1) * V, dtype=np.int64)
+    z = normal_f32(w.key(ST_VLOGIT), idx, sigma_target).astype(np.float64).reshape(S, B + 1, V)
+    zq = z[:, :B] + normal_f32(w.key(ST_VNOISE), idx[: S * B * V], sigma_gap).astype(
+        np.float64).reshape(S, B, V)
+
+    def softmax(x):
+        e = np.exp(x - x.max(axis=-1, keepdims=True))
+        return e / e.sum(axis=-1, keepdims=True)
+
+    p = softmax(z).astype(np.float32)
+    q = softmax(zq).astype(np.float32)
+    u = (draw_u64(w.key(ST_VDRAW), rnd * S * B + np.arange(S * B)) >> np.uint64(11)).astype(
+        np.float64) * 2.0 ** -53
+    cq = np.cumsum(q.astype(np.float64), axis=-1).reshape(S * B, V)
+    draft = np.array([min(int(np.searchsorted(cq[i], u[i] * cq[i, -1], side="right")), V - 1)
+                      for i in range(S * B)], np.int32).reshape(S, B)
+    words = (draw_u64(w.key(ST_VWORD), rnd * S * (B + 1) + np.arange(S * (B + 1)))
+             & np.uint64(0xFFFFFFFF)).astype(np.uint32).reshape(S, B + 1)
+    return draft, p, q, words

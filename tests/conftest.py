@@ -11,3 +11,12 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: long-running CPU test")
+
+
+@pytest.fixture
+def tune():
+    """Set a launch-shape override of the library (``tune(name, value)``); all
+    overrides return to the automatic choice when the test ends."""
+    import paper_2609_14717_amd as co
+    yield co.set_tuning
+    co.reset_tuning()

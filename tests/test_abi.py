@@ -68,7 +68,7 @@ def _rc(fn):
 
 
 def test_status_strings():
-    for code in range(8):
+    for code in range(10):
         assert co.status_string(code) != "unknown status"
     assert co.status_string(99) == "unknown status"
 
@@ -252,3 +252,61 @@ def test_projection_backward_arguments_checked_on_host():
                     co.weights(FAKE, FAKE, FAKE, None, None, FAKE),
                     co.weights(FAKE, FAKE, FAKE, None, None, None, FAKE)):
         assert _rc(lambda: call(d, variant)) == co.CO_ERR_UNSUPPORTED
+
+
+def _round(d, W, q=FAKE, lse=None, wsb=1 << 30, flags=0):
+    return co.carryover_round(d, W, FAKE, FAKE, FAKE, q, _fake_state(), _fake_route(), FAKE, lse,
+                              flags, FAKE, stream=0, ws_bytes=wsb)
+
+
+@pytest.mark.parametrize("which", ["f_e", "w_f_carry", "z_norm", "k_norm", "lse", "q"])
+def test_round_checks_every_step_before_its_first_launch(which):
+    """A bad argument of any of the round's three steps is reported before the
+    route is enqueued (no launch can run here: one would fail with
+    CO_ERR_HIP, not CO_ERR_INVALID_ARG)."""
+    d = _dims()
+    bad = FAKE + 2
+    W = co.weights(FAKE, FAKE, FAKE, bad if which == "f_e" else None,
+                   bad if which == "w_f_carry" else None, bad if which == "z_norm" else None,
+                   bad if which == "k_norm" else None)
+    rc = _rc(lambda: _round(d, W, q=bad if which == "q" else FAKE,
+                            lse=bad if which == "lse" else None))
+    assert rc == co.CO_ERR_INVALID_ARG
+
+
+def test_round_workspace_checked_before_its_first_launch():
+    d = _dims()
+    W = co.weights(FAKE, FAKE, FAKE)
+    need = co.workspace_bytes(d, co.CO_WS_ROUND)
+    assert _rc(lambda: _round(d, W, wsb=need - 1)) == co.CO_ERR_WORKSPACE
+    assert _rc(lambda: _round(d, W, wsb=co.workspace_bytes(d, co.CO_WS_PROJECT) - 1)) \
+        == co.CO_ERR_WORKSPACE
+
+
+def test_verify_sample_arguments_checked_on_host():
+    d = _dims()
+
+    def call(vocab=1000, p=FAKE, words=FAKE, bits=FAKE, dims=d):
+        return co.carryover_verify_sample(dims, vocab, FAKE, p, FAKE, words, bits, FAKE, FAKE,
+                                          FAKE, stream=0)
+
+    assert _rc(lambda: call(vocab=0)) == co.CO_ERR_UNSUPPORTED
+    assert _rc(lambda: call(p=None)) == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: call(words=FAKE + 2)) == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: call(bits=None)) == co.CO_ERR_INVALID_ARG
+    assert _rc(lambda: call(dims=_dims(B=0))) == co.CO_ERR_INVALID_ARG
+
+
+def test_tuning_knobs():
+    """Unknown knobs are refused; the attention workspace follows the
+    workgroup override and returns to its size when it is cleared."""
+    assert co.lib().carryover_set_tuning(len(co.TUNING), 1) == co.CO_ERR_INVALID_ARG
+    assert co.lib().carryover_set_tuning(-1, 1) == co.CO_ERR_INVALID_ARG
+    d = _dims()
+    base = co.workspace_bytes(d, co.CO_WS_ATTENTION)
+    try:
+        co.set_tuning("attn_workgroups", 1000)
+        assert co.workspace_bytes(d, co.CO_WS_ATTENTION) > base
+    finally:
+        co.reset_tuning()
+    assert co.workspace_bytes(d, co.CO_WS_ATTENTION) == base

@@ -305,3 +305,35 @@ def test_empty_batch_is_a_no_op():
     torch.cuda.synchronize()
     assert co.carryover_read_status(st) == 0
     assert torch.count_nonzero(buf) == 0
+
+
+@pytest.mark.parametrize("which", ["f_e", "z_norm", "k_norm", "w_f_carry", "lse"])
+def test_round_rejected_on_the_host_leaves_the_state_untouched(which):
+    """A misaligned optional pointer of any step makes carryover_round return
+    CO_ERR_INVALID_ARG before its first launch: lengths, route output and
+    caches are exactly as before; the next valid round then runs as usual."""
+    Scenario, co = _gpu()
+    w = EDGE1
+    sc, orc = Scenario(w), OracleRun(w)
+    print(f"[edge] misaligned {which}", flush=True)
+    before = {k: v.clone() for k, v in sc.st.items()}
+    rt_before = {k: v.clone() for k, v in sc.rt.items()}
+    hidden, q, draft, target, _ = sc.round_inputs(0)
+    out, lse = sc.new_output()
+    bad = sc.ws.data_ptr() + 2
+    W = co.weights(sc.wf, sc.wkv, sc.e, bad if which == "f_e" else sc.f_e,
+                   bad if which == "w_f_carry" else None, bad if which == "z_norm" else None,
+                   bad if which == "k_norm" else None)
+    with pytest.raises(co.CarryoverError) as ei:
+        co.carryover_round(sc.dims, W, hidden, draft, target, q, sc.st, sc.rt, out,
+                           bad if which == "lse" else lse, 0, sc.ws)
+    assert ei.value.code == co.CO_ERR_INVALID_ARG
+    torch.cuda.synchronize()
+    for k, v in before.items():
+        assert torch.equal(sc.st[k], v), k
+    for k, v in rt_before.items():
+        assert torch.equal(sc.rt[k], v), k
+    out, lse, _ = _round(co, sc, 0)
+    assert co.carryover_read_status(sc.st) == 0
+    rr, O, LSE = orc.round(0)
+    compare_round(sc, orc, rr, O, LSE, out, lse, sc.rt, orc.seqs, f"after rejected {which}")

@@ -94,8 +94,8 @@ WIDE128 = wl.Workload("wide_hd128", S=16, B=16, Dcat=1536, d=512, L=1, Hq=8, Hkv
 @pytest.mark.parametrize("fold", [True, False], ids=["folded", "in_kernel"])
 @pytest.mark.parametrize("variant", range(6), ids=lambda v: f"v{v}")
 @pytest.mark.parametrize("w", [WIDE64, WIDE128], ids=lambda w: w.name)
-def test_wide_gemm_variants(w, variant, fold, monkeypatch):
-    monkeypatch.setenv("CO_GEMM_WIDE_VARIANT", str(variant))
+def test_wide_gemm_variants(w, variant, fold, tune):
+    tune("gemm_wide_variant", variant)
     run_rounds(w, 2, fold_e=fold)
 
 
@@ -139,10 +139,10 @@ SLICINGS = [("1", "1"), ("1", "3"), ("3", "2"), ("7", "64"), ("1000", "")]
 
 @pytest.mark.parametrize("w", [SMALL_RAGGED, SMALL_G4, MANY_SEQS], ids=lambda w: w.name)
 @pytest.mark.parametrize("slicing", SLICINGS, ids=lambda s: f"wg{s[0]}_rt{s[1] or 'dflt'}")
-def test_attention_slicings(w, slicing, monkeypatch):
-    monkeypatch.setenv("CO_ATTN_WORKGROUPS", slicing[0])
+def test_attention_slicings(w, slicing, tune):
+    tune("attn_workgroups", slicing[0])
     if slicing[1]:
-        monkeypatch.setenv("CO_ATTN_ROUND_TILES", slicing[1])
+        tune("attn_round_tiles", slicing[1])
     run_rounds(w, 2)
 
 
@@ -284,10 +284,10 @@ SMALL_HD128_G2 = wl.Workload("small_hd128_g2", S=6, B=16, Dcat=512, d=256, L=2, 
 @pytest.mark.parametrize("split", ["", "1", "3"], ids=lambda v: f"share{v or 'dflt'}")
 @pytest.mark.parametrize("w", [SMALL_RAGGED, MANY_SEQS, SMALL_HD128_G2, SMALL_G4],
                          ids=lambda w: w.name)
-def test_shared_prefix_flag_independent_pages(w, split, monkeypatch):
+def test_shared_prefix_flag_independent_pages(w, split, tune):
     import paper_2609_14717_amd as co
     if split:   # committed tiles per workgroup share: many shares, merged afterwards
-        monkeypatch.setenv("CO_ATTN_GROUP_SPLIT_TILES", split)
+        tune("attn_group_split_tiles", split)
     run_rounds(w, 2, extra_flags=co.CO_ATTN_SHARED_PREFIX)
 
 
@@ -331,9 +331,9 @@ def train_small_check(shared):
 
 @pytest.mark.parametrize("shared", [True, False], ids=["shared_prefix", "persistent"])
 @pytest.mark.parametrize("split", ["", "3"], ids=lambda v: f"share{v or 'dflt'}")
-def test_train_small_full(shared, split, monkeypatch):
+def test_train_small_full(shared, split, tune):
     if split:
-        monkeypatch.setenv("CO_ATTN_GROUP_SPLIT_TILES", split)
+        tune("attn_group_split_tiles", split)
     train_small_check(shared)
 
 
@@ -346,13 +346,13 @@ FUSED_RAGGED = wl.RAGGED32.replace(name="fused_ragged", S=5, ctx_lo=100, ctx_hi=
 
 
 @pytest.mark.parametrize("w", [FUSED_RAGGED, wl.RAGGED32], ids=lambda w: w.name)
-def test_fused_projection(w, monkeypatch):
-    monkeypatch.setenv("CO_PROJECT_FUSED_MIN_ROWS", "1")
+def test_fused_projection(w, tune):
+    tune("project_fused_min_rows", 1)
     run_rounds(w, 2)
 
 
-def test_fused_projection_train_small(monkeypatch):
-    monkeypatch.setenv("CO_PROJECT_FUSED_MIN_ROWS", "1")
+def test_fused_projection_train_small(tune):
+    tune("project_fused_min_rows", 1)
     train_small_check(True)
 
 
@@ -366,17 +366,17 @@ WAVE_RAGGED = wl.Workload("wave_ragged_hd128", S=6, B=16, Dcat=512, d=256, L=2, 
 
 @pytest.mark.parametrize("wgs", ["", "1", "3", "70"], ids=lambda v: f"wg{v or 'dflt'}")
 @pytest.mark.parametrize("w", [SMALL_G4, BATCH3_8B, WAVE_RAGGED], ids=lambda w: w.name)
-def test_wave_slices(w, wgs, monkeypatch):
-    monkeypatch.setenv("CO_ATTN_WAVE", "1")
+def test_wave_slices(w, wgs, tune):
+    tune("attn_wave", 1)
     if wgs:
-        monkeypatch.setenv("CO_ATTN_WORKGROUPS", wgs)
+        tune("attn_workgroups", wgs)
     run_rounds(w, 3)
 
 
 # The persistent path at the same shapes (no longer their default).
 @pytest.mark.parametrize("w", [SMALL_G4, WAVE_RAGGED], ids=lambda w: w.name)
-def test_persistent_hd128_64_rows(w, monkeypatch):
-    monkeypatch.setenv("CO_ATTN_WAVE", "0")
+def test_persistent_hd128_64_rows(w, tune):
+    tune("attn_wave", 0)
     run_rounds(w, 3)
 
 
@@ -386,8 +386,8 @@ def test_persistent_hd128_64_rows(w, monkeypatch):
 # enough segments for the merge's 16-dims-per-thread form.
 @pytest.mark.parametrize("wgs", ["", "1", "5", "500"], ids=lambda v: f"wg{v or 'dflt'}")
 @pytest.mark.parametrize("w", [SMALL_RAGGED, MANY_SEQS, WIDE64], ids=lambda w: w.name)
-def test_wave_slices_hd64(w, wgs, monkeypatch):
-    monkeypatch.setenv("CO_ATTN_WAVE", "1")
+def test_wave_slices_hd64(w, wgs, tune):
+    tune("attn_wave", 1)
     if wgs:
-        monkeypatch.setenv("CO_ATTN_WORKGROUPS", wgs)
+        tune("attn_workgroups", wgs)
     run_rounds(w, 3)

@@ -81,10 +81,10 @@ def test_accept_bits_rounds(w):
 
 
 @pytest.mark.parametrize("w", [EDGE, EDGE_F32, WIDE, SPLIT], ids=lambda w: w.name)
-def test_separate_projector_rounds(w, monkeypatch):
+def test_separate_projector_rounds(w, tune):
     Scenario, co = _gpu()
     if w is WIDE:      # the large-tile kernel at any row count from 256
-        monkeypatch.setenv("CO_GEMM_WIDE_VARIANT", "3")
+        tune("gemm_wide_variant", 3)
     print(f"[variants] separate projector {w.name}", flush=True)
     sc = Scenario(w, separate_projector=True)
     orc = OracleRun(w, separate_projector=True)
@@ -130,11 +130,11 @@ def test_carry_mass(w):
 
 
 @pytest.mark.parametrize("w", [EDGE, EDGE_F32, WIDE, SPLIT], ids=lambda w: w.name)
-def test_z_norm_rounds(w, monkeypatch):
+def test_z_norm_rounds(w, tune):
     """F's output RMS-normalised (gain) before the K/V product."""
     Scenario, co = _gpu()
     if w is WIDE:
-        monkeypatch.setenv("CO_GEMM_WIDE_VARIANT", "3")
+        tune("gemm_wide_variant", 3)
     print(f"[variants] z norm {w.name}", flush=True)
     sc = Scenario(w, z_norm=True)
     orc = OracleRun(w, z_norm=True)
@@ -149,10 +149,10 @@ def test_z_norm_rounds(w, monkeypatch):
         compare_round(sc, orc, rr, O, LSE, out, lse, sc.rt, orc.seqs, f"{w.name} znorm r{r}")
 
 
-def test_z_norm_fused_path(monkeypatch):
+def test_z_norm_fused_path(tune):
     """Where the fused projection would run (forced at 80 rows), the
     normalised update takes the two-product path and stays correct."""
-    monkeypatch.setenv("CO_PROJECT_FUSED_MIN_ROWS", "1")
+    tune("project_fused_min_rows", 1)
     _z_norm_small()
 
 
@@ -173,13 +173,13 @@ def _z_norm_small():
 
 
 @pytest.mark.parametrize("w", [EDGE, EDGE_F32, HD128, WIDE, SPLIT], ids=lambda w: w.name)
-def test_k_norm_rounds(w, monkeypatch):
+def test_k_norm_rounds(w, tune):
     """Every key head RMS-normalised (per-layer gain) before its rotation, on
     the small-tile (hd 64 and 128), large-tile, split-K and fp32 epilogues,
     also together with the normalisation of F's output."""
     Scenario, co = _gpu()
     if w is WIDE:
-        monkeypatch.setenv("CO_GEMM_WIDE_VARIANT", "3")
+        tune("gemm_wide_variant", 3)
     zn = w is SPLIT
     print(f"[variants] k norm {w.name} (z norm {zn})", flush=True)
     sc = Scenario(w, k_norm=True, z_norm=zn)
@@ -195,10 +195,10 @@ def test_k_norm_rounds(w, monkeypatch):
         compare_round(sc, orc, rr, O, LSE, out, lse, sc.rt, orc.seqs, f"{w.name} knorm r{r}")
 
 
-def test_k_norm_fused_path(monkeypatch):
+def test_k_norm_fused_path(tune):
     """Where the fused projection would run (forced at 80 rows), normalised
     keys take the two-product path and stay correct."""
-    monkeypatch.setenv("CO_PROJECT_FUSED_MIN_ROWS", "1")
+    tune("project_fused_min_rows", 1)
     Scenario, co = _gpu()
     w = wl.RAGGED32.replace(name="var_knorm_fused", S=5, rounds=3, ctx_lo=100, ctx_hi=900,
                             seed=0x5EED27)
