@@ -249,6 +249,25 @@ co_status carryover_round(const co_dims* dims, const co_weights* w, const void* 
                           uint32_t flags, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * carryover_round for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same round, with the same arguments except the workspace, which is the
+ * library's own static device scratch of CO_NOALLOC_SCRATCH_BYTES (128 MiB)
+ * per device, held from the device's first use until the process ends.  The
+ * call allocates nothing.  Returns CO_ERR_WORKSPACE when
+ * carryover_workspace_bytes(dims, CO_WS_ROUND) exceeds the scratch; other
+ * errors as carryover_round.  Every call on a device shares that device's
+ * scratch (which keeps the last call's contents, none of which a call reads
+ * first): calls that overlap on one device -- on different streams or from
+ * different threads -- race; serialise them.
+ */
+#define CO_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+co_status carryover_round_noalloc(const co_dims* dims, const co_weights* w, const void* hidden,
+                                  const int32_t* draft_tok, const int32_t* target_tok,
+                                  const void* q, co_state* state, const co_route* route_out,
+                                  void* out, float* lse, uint32_t flags, hipStream_t stream);
+
+/*
  * Stochastic verification (T = 1): the acceptance decision and the
  * correction or bonus token of the standard speculative-sampling rule that
  * Appendix A ("Why verification remains valid") relies on.  For every

@@ -105,6 +105,8 @@ def lib():
             "carryover_verify_sample": [_P(co_dims), ctypes.c_int32, _v, _v, _v, _v, _v, _v, _v,
                                         _v, _v],
             "carryover_set_tuning": [ctypes.c_int32, ctypes.c_int64],
+            "carryover_round_noalloc": [_P(co_dims), _P(co_weights), _v, _v, _v, _v,
+                                        _P(co_state), _P(co_route), _v, _v, ctypes.c_uint32, _v],
             "carryover_workspace_bytes": [_P(co_dims), ctypes.c_int32],
             "carryover_read_status": [_P(co_state), _P(ctypes.c_int32), _v],
             "carryover_status_string": [ctypes.c_int32],
@@ -123,6 +125,7 @@ EXPORTED = ("carryover_route", "carryover_project_kv", "drafter_block_attention"
             "carryover_round", "carryover_fold_e", "drafter_carry_mass", "drafter_self_merge",
             "drafter_block_attention_backward", "carryover_project_kv_backward",
             "carryover_import_kv", "carryover_verify_sample", "carryover_set_tuning",
+            "carryover_round_noalloc",
             "carryover_workspace_bytes", "carryover_read_status", "carryover_status_string")
 
 
@@ -281,6 +284,20 @@ def carryover_round(dims, w, hidden, draft_tok, target_tok, q, st, rt, out, lse,
                                  _ptr(draft_tok), _ptr(target_tok), _ptr(q), ctypes.byref(s),
                                  ctypes.byref(r), _ptr(out), _ptr(lse), flags, _ptr(ws), nb,
                                  _stream(stream)), "carryover_round")
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20
+
+
+def carryover_round_noalloc(dims, w, hidden, draft_tok, target_tok, q, st, rt, out, lse, flags,
+                            stream=None):
+    """carryover_round on the library's static per-device scratch (no workspace
+    argument, no allocation); calls on one device must not overlap."""
+    s, r = state(st), route(rt)
+    _check(lib().carryover_round_noalloc(ctypes.byref(dims), ctypes.byref(w), _ptr(hidden),
+                                         _ptr(draft_tok), _ptr(target_tok), _ptr(q),
+                                         ctypes.byref(s), ctypes.byref(r), _ptr(out), _ptr(lse),
+                                         flags, _stream(stream)), "carryover_round_noalloc")
 
 
 def carryover_fold_e(dims, w, f_e, stream=None):

@@ -4,7 +4,16 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "co_kernels.h"
+
+// Scratch of carryover_round_noalloc: the round's workspace for callers that
+// cannot allocate.  Every device the library runs on holds its own copy until
+// the process ends; host code reaches it only through the per-device address
+// from hipGetSymbolAddress (the name itself is not a device address here).
+constexpr size_t kScratchBytes = size_t{128} << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 using namespace co;
 
@@ -21,6 +30,24 @@ namespace {
 
 constexpr int kMaxDevices = 64;
 int g_num_cus[kMaxDevices];   // per-device compute-unit count, filled on first use
+
+std::mutex g_scratch_mutex;
+void* g_scratch_addr[kMaxDevices];   // device address of `scratch`, per device
+
+// Device address of the current device's copy of `scratch`, looked up once
+// per device with that device current.
+co_status scratch_address(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return CO_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return CO_ERR_HIP;
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return CO_OK;
+}
 
 int num_cus() {
   int dev = 0;
@@ -482,6 +509,22 @@ co_status carryover_round(const co_dims* dims, const co_weights* w, const void* 
     return s;
   if ((s = enqueue_project(dims, w, hidden, scratch, state, ws, stream)) != CO_OK) return s;
   return do_attention(dims, 0, dims->num_layers, q, state, out, lse, flags, attn_ws, stream);
+}
+
+co_status carryover_round_noalloc(const co_dims* dims, const co_weights* w, const void* hidden,
+                                  const int32_t* draft_tok, const int32_t* target_tok,
+                                  const void* q, co_state* state, const co_route* route_out,
+                                  void* out, float* lse, uint32_t flags, hipStream_t stream) {
+  co_status s = check_dims(dims);
+  if (s != CO_OK) return s;
+  if ((s = check_attention_dims(dims)) != CO_OK) return s;
+  const size_t need = carryover_workspace_bytes(dims, CO_WS_ROUND);
+  if (need == 0) return CO_ERR_UNSUPPORTED;
+  if (need > kScratchBytes) return CO_ERR_WORKSPACE;
+  void* ws = nullptr;
+  if ((s = scratch_address(&ws)) != CO_OK) return s;
+  return carryover_round(dims, w, hidden, draft_tok, target_tok, q, state, route_out, out, lse,
+                         flags, ws, kScratchBytes, stream);
 }
 
 co_status carryover_verify_sample(const co_dims* dims, int32_t vocab, const int32_t* draft_tok,

@@ -310,3 +310,22 @@ def test_tuning_knobs():
     finally:
         co.reset_tuning()
     assert co.workspace_bytes(d, co.CO_WS_ATTENTION) == base
+
+
+def test_noalloc_round_rejects_workloads_beyond_its_scratch():
+    """carryover_round_noalloc refuses, on the host, dims whose round workspace
+    exceeds its static scratch (here no device exists: any later step would
+    fail with CO_ERR_HIP instead)."""
+    from synth import workloads as wl
+    w = wl.RAGGED32_8B.replace(S=96)
+    d = co.make_dims(w.S, w.B, w.Dcat, w.d, w.L, w.Hq, w.Hkv, w.hd, w.max_pages_per_seq,
+                     w.S * w.max_pages_per_seq, w.dtype, w.theta)
+    assert co.workspace_bytes(d, co.CO_WS_ROUND) > co.NOALLOC_SCRATCH_BYTES
+    assert _rc(lambda: co.carryover_round_noalloc(d, co.weights(FAKE, FAKE, FAKE), FAKE, FAKE,
+                                                  FAKE, FAKE, _fake_state(), _fake_route(), FAKE,
+                                                  None, 0, stream=0)) == co.CO_ERR_WORKSPACE
+    small = _dims()
+    assert co.workspace_bytes(small, co.CO_WS_ROUND) <= co.NOALLOC_SCRATCH_BYTES
+    assert _rc(lambda: co.carryover_round_noalloc(small, co.weights(FAKE, FAKE, FAKE), FAKE, FAKE,
+                                                  FAKE, FAKE, _fake_state(), _fake_route(), FAKE,
+                                                  None, 0, stream=0)) == co.CO_ERR_HIP
