@@ -366,16 +366,51 @@ def carry_mass(q, qpos, k_committed, k_carry, theta):
 
 # ------------------------------------------------------------ drafter state
 
+class _RowStore:
+    """Rows [L][n][Hkv][hd] of every sequence.  Appending writes into spare
+    capacity instead of re-concatenating (a storage detail only: reading a
+    sequence gives exactly the rows a concatenation would)."""
+
+    def __init__(self, S, L, Hkv, hd, dtype):
+        self._dtype = dtype
+        self._buf = [np.zeros((L, 0, Hkv, hd), dtype) for _ in range(S)]
+        self._n = [0] * S
+
+    def __len__(self):
+        return len(self._buf)
+
+    def __getitem__(self, s):
+        return self._buf[s][:, :self._n[s]]
+
+    def __setitem__(self, s, rows):
+        rows = np.asarray(rows, self._dtype)
+        self._buf[s] = rows
+        self._n[s] = rows.shape[1]
+
+    def __iter__(self):
+        return (self[s] for s in range(len(self)))
+
+    def append(self, s, rows):
+        n, m = self._n[s], rows.shape[1]
+        buf = self._buf[s]
+        if n + m > buf.shape[1]:
+            grown = np.empty(buf.shape[:1] + (n + m + (n + m) // 4 + 64,) + buf.shape[2:],
+                             self._dtype)
+            grown[:, :n] = buf[:, :n]
+            self._buf[s] = buf = grown
+        buf[:, n:n + m] = rows
+        self._n[s] = n + m
+
+
 class State:
     """Logical (unpaged) drafter KV of S sequences: committed C_l and carryover U_l."""
 
     def __init__(self, S, L, Hkv, hd, store=np.float64):
         self.S, self.L, self.Hkv, self.hd, self.store = S, L, Hkv, hd, store
-        empty = lambda: np.zeros((L, 0, Hkv, hd), store)
-        self.ck = [empty() for _ in range(S)]
-        self.cv = [empty() for _ in range(S)]
-        self.uk = [empty() for _ in range(S)]
-        self.uv = [empty() for _ in range(S)]
+        self.ck = _RowStore(S, L, Hkv, hd, store)
+        self.cv = _RowStore(S, L, Hkv, hd, store)
+        self.uk = _RowStore(S, L, Hkv, hd, store)
+        self.uv = _RowStore(S, L, Hkv, hd, store)
 
     def ctx_len(self):
         return np.array([c.shape[1] for c in self.ck], np.int32)
@@ -391,8 +426,8 @@ class State:
     def commit_and_replace(self, s, k_acc, v_acc, k_rej, v_rej):
         """C_l <- [C_l ; J_acc];  U_l <- J_rej (old U dropped).  Inputs [n][L][Hkv][hd]."""
         t = lambda a: np.asarray(a, self.store).transpose(1, 0, 2, 3)
-        self.ck[s] = np.concatenate([self.ck[s], t(k_acc)], axis=1)
-        self.cv[s] = np.concatenate([self.cv[s], t(v_acc)], axis=1)
+        self.ck.append(s, t(k_acc))
+        self.cv.append(s, t(v_acc))
         self.uk[s] = t(k_rej).copy()
         self.uv[s] = t(v_rej).copy()
 

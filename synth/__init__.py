@@ -159,14 +159,18 @@ def build_host() -> str:
 def normal_block(key: int, shape, strides, base: int, sigma: float, dtype: str,
                  use_c: bool = True) -> np.ndarray:
     """``normal`` over a dense block (logical index base + sum coord * stride),
-    through the C build when present, else numpy; both give identical bits."""
+    through the C build when present, else numpy; both give identical bits.
+    dtype 'bf16_f32': the bf16 values, widened exactly to float32."""
     lib = host_lib() if use_c else None
     if lib is None:
+        if dtype == "bf16_f32":
+            return bf16_bits_to_f32(normal(key, grid_index(shape, strides, base), sigma, "bf16"))
         return normal(key, grid_index(shape, strides, base), sigma, dtype)
     import ctypes
-    out = np.empty(tuple(shape), dtype=np.float32 if dtype == "f32" else np.uint16)
+    mode = {"f32": 0, "bf16": 1, "bf16_f32": 2}[dtype]
+    out = np.empty(tuple(shape), dtype=np.uint16 if mode == 1 else np.float32)
     nd = len(shape)
-    rc = lib.synth_host_fill(out.ctypes.data_as(ctypes.c_void_p), 0 if dtype == "f32" else 1, nd,
+    rc = lib.synth_host_fill(out.ctypes.data_as(ctypes.c_void_p), mode, nd,
                              (ctypes.c_int64 * nd)(*shape), (ctypes.c_int64 * nd)(*strides),
                              int(base), ctypes.c_uint64(key), float(normal_scale(sigma)))
     if rc != 0:

@@ -26,7 +26,8 @@ static inline uint16_t to_bf16(float f) {
   return (uint16_t)(b >> 16);
 }
 
-/* out: float32 (bf16 == 0) or bf16 bits (bf16 == 1), dense in the block's shape. */
+/* out, dense in the block's shape: float32 values (bf16 == 0), bf16 bits
+ * (bf16 == 1), or the bf16-rounded values widened back to float32 (bf16 == 2). */
 int synth_host_fill(void* out, int bf16, int ndim, const int64_t* shape, const int64_t* stride,
                     int64_t base, uint64_t key, float scale) {
   if (!out || ndim < 1 || ndim > 8) return 1;
@@ -43,7 +44,13 @@ int synth_host_fill(void* out, int bf16, int ndim, const int64_t* shape, const i
       idx += (rem % shape[k]) * stride[k];
       rem /= shape[k];
     }
-    if (bf16) {
+    if (bf16 == 2) {
+      float* o = (float*)out + r * inner;
+      for (int64_t c = 0; c < inner; ++c) {
+        const uint32_t b = (uint32_t)to_bf16(draw_normal(key, idx + c * st_in, scale)) << 16;
+        memcpy(o + c, &b, 4);
+      }
+    } else if (bf16) {
       uint16_t* o = (uint16_t*)out + r * inner;
       for (int64_t c = 0; c < inner; ++c) o[c] = to_bf16(draw_normal(key, idx + c * st_in, scale));
     } else {

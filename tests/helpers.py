@@ -15,9 +15,10 @@ TOL = {"bf16": 2e-2, "f32": 1e-4}
 def host(w, spec, dtype=None, out=np.float64):
     """A described block, widened exactly to ``out`` (float64, or float32 for
     bf16/fp32 data that a float32 store keeps exactly)."""
-    raw = wl.host_block(w, spec, dtype)
     if out == np.float32:
-        return raw if (dtype or w.dtype) == "f32" else synth.bf16_bits_to_f32(raw)
+        dt = dtype or w.dtype
+        return wl.host_block(w, spec, "f32" if dt == "f32" else "bf16_f32")
+    raw = wl.host_block(w, spec, dtype)
     return synth.to_f64(raw, dtype or w.dtype)
 
 

@@ -86,3 +86,16 @@ def test_c_host_generator_matches_numpy_definition():
             assert a.dtype == b.dtype and a.shape == b.shape
             np.testing.assert_array_equal(a.view(np.uint16 if dtype == "bf16" else np.uint32),
                                           b.view(np.uint16 if dtype == "bf16" else np.uint32))
+
+
+def test_bf16_values_widened_in_c_match_numpy():
+    """The C generator's bf16-as-fp32 mode gives the bf16 values, widened,
+    bit for bit as the numpy definition."""
+    import synth
+    key = synth.stream_key(0xC0FFEE, 11)
+    shape, strides = (3, 5, 70), (1 << 20, 131, 1)
+    a = synth.normal_block(key, shape, strides, 777, 0.37, "bf16_f32")
+    b = synth.bf16_bits_to_f32(synth.normal(key, synth.grid_index(shape, strides, 777), 0.37,
+                                            "bf16"))
+    assert a.dtype == np.float32
+    np.testing.assert_array_equal(a.view(np.uint32), b.view(np.uint32))
