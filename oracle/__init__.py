@@ -383,9 +383,12 @@ class _RowStore:
         return self._buf[s][:, :self._n[s]]
 
     def __setitem__(self, s, rows):
-        rows = np.asarray(rows, self._dtype)
-        self._buf[s] = rows
-        self._n[s] = rows.shape[1]
+        rows = np.asarray(rows)
+        n = rows.shape[1]
+        buf = np.empty(rows.shape[:1] + (n + n // 4 + 64,) + rows.shape[2:], self._dtype)
+        buf[:, :n] = rows
+        self._buf[s] = buf
+        self._n[s] = n
 
     def __iter__(self):
         return (self[s] for s in range(len(self)))
@@ -512,14 +515,25 @@ def round_update(state: State, r, H, E, WF, WKV, theta, mode="carry", seqs=None,
     given a route result ``r`` (see ``route``).  H [S][B][Dcat].  With
     ``WF_carry`` the carried rows use the separate projector (see project)."""
     S, B, _ = H.shape
+    todo = []
     for s in (range(S) if seqs is None else seqs):
         if not r["touched"][s]:
             continue
         m = int(r["accept_len"][s])
         rows = np.arange(B) if mode in ("carry", "carry_only") else np.arange(m)
-        pos = r["row_pos"][s][rows]
-        k, v = project(H[s][rows], E, rows >= m, WF, WKV, pos, state.L, state.Hkv,
-                       state.hd, theta, WF_carry, z_norm, k_norm)
+        todo.append((s, m, rows))
+    if not todo:
+        return
+    # Eq. 1 acts on every row independently: the rows of all sequences go
+    # through one call of ``project`` and are then split back per sequence.
+    k_all, v_all = project(np.concatenate([H[s][rows] for s, _, rows in todo]), E,
+                           np.concatenate([rows >= m for _, m, rows in todo]), WF, WKV,
+                           np.concatenate([r["row_pos"][s][rows] for s, _, rows in todo]),
+                           state.L, state.Hkv, state.hd, theta, WF_carry, z_norm, k_norm)
+    at = 0
+    for s, m, rows in todo:
+        k, v = k_all[at:at + len(rows)], v_all[at:at + len(rows)]
+        at += len(rows)
         if mode == "carry_only":
             k_acc, v_acc = k[:0], v[:0]
         else:

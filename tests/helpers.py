@@ -37,6 +37,14 @@ def seq_block(w, spec, axis, seqs):
     return out
 
 
+def _rows_first(spec):
+    """The same block described as [L][n][Hkv][hd] instead of [L][Hkv][n][hd]
+    (every element keeps its logical index, so its value)."""
+    st_, shape, strides, base, sigma = spec
+    o = (0, 2, 1, 3)
+    return st_, tuple(shape[i] for i in o), tuple(strides[i] for i in o), base, sigma
+
+
 class OracleTrain:
     """The oracle's view of the training-shaped forward (Algorithm 2, second
     pass) for a sample of anchored blocks (virtual sequences)."""
@@ -102,8 +110,8 @@ class OracleRun:
             n = int(self.ctx0[s])
             if w.ctx_mode == "direct":
                 wide = np.float32 if store == np.float32 else np.float64
-                k = host(w, wl.spec_kv_direct(w, "k", s, 0, n), out=wide).transpose(0, 2, 1, 3)
-                v = host(w, wl.spec_kv_direct(w, "v", s, 0, n), out=wide).transpose(0, 2, 1, 3)
+                k = host(w, _rows_first(wl.spec_kv_direct(w, "k", s, 0, n)), out=wide)
+                v = host(w, _rows_first(wl.spec_kv_direct(w, "v", s, 0, n)), out=wide)
                 self.st.set_committed(s, k, v)
             elif n:
                 h = host(w, wl.spec_hctx(w, s, 0, n))

@@ -9,10 +9,26 @@ reverse mode (itself pinned by finite differences):
   contexts, an empty sequence, a sequence with carry rows only, padded query
   rows (8 block rows x 2 heads) and a layer sub-range.
 
-Gradients are compared against the oracle relative to the largest reference
-value of the same (layer, KV head) slab, at 3e-2: the backward's weights P
-carry the forward's rounding (bf16 rotated queries, the bf16 output in D), and
-it rounds P and dS to bf16 before three further products.
+Gradients are compared per head vector at 2e-2, the bf16 rule of the forward,
+with the denominator floored at a fraction of the largest reference vector of
+the same (layer, KV head) slab: err = ||g - r||_inf / max(||r||_inf,
+floor * max_slab ||r||_inf).  Vectors above the floor are held to the plain
+per-vector rule; below it the rule is absolute.  A gradient vector is a sum of
+terms of both signs whose magnitudes follow the slab's scale (dS = P (dP - D)
+cancels, and so do the sums over queries), so the absolute error of a small
+vector is set by its terms, not by its cancelled sum.
+
+* The attention backward on its own (every key and value drawn directly by
+  the seeded generator, so that both sides read the same bf16 values): floor
+  1/8.  Its own rounding points are the bf16 rotated queries, the bf16 forward
+  output in D, and P and dS rounded to bf16 before the three products.
+* The whole path (keys and values projected by the GPU, rounded to bf16 twice
+  -- F's output and the stored rows -- against the oracle's exact
+  projection): floor 1, i.e. within 2e-2 of the slab's largest vector.  A
+  logit moves by q . dk when a stored key moves by dk, and the softmax
+  derivative turns that into relative errors of P that the cancelling sums of
+  dV, dK and dq do not average away; the unit test above separates the
+  backward's own error from this inherited one.
 """
 import numpy as np
 import pytest
@@ -26,7 +42,10 @@ torch = pytest.importorskip("torch")
 
 from helpers import OracleRun, host, seq_block, to_np  # noqa: E402
 
-GTOL = 3e-2
+GTOL = 2e-2
+FLOOR_UNIT = 1.0 / 8      # the attention backward on identical bf16 inputs
+FLOOR_PATH = 1.0          # gradients of the whole path (inputs projected on each side)
+CARRY_T0 = wl.TCAP // 2   # logical positions of directly drawn carry rows (past any context)
 
 TRAIN_SMALL = wl.TRAIN_FWD.replace(name="bwd_train_small", S=2, seq_len=512, anchors=10,
                                    seed=0x5EED30)
@@ -44,19 +63,26 @@ def _gpu():
 WORST = []
 
 
-def slab_close(g, r, what, tol=GTOL):
-    """g, r [n][hd] of one (layer, KV head): every head vector within tol of
-    the slab's largest reference vector."""
+def slab_close(g, r, what, tol=GTOL, floor=FLOOR_PATH):
+    """g, r [n][hd] of one (layer, KV head): every head vector within tol,
+    relative to max(its own reference norm, floor x the slab's largest)."""
     g = np.asarray(g, np.float64)
     r = np.asarray(r, np.float64)
     assert np.all(np.isfinite(g)), f"{what}: non-finite GPU values"
     if r.size == 0:
         return 0.0
-    scale = max(np.abs(r).max(), 1e-30)
-    e = float(np.abs(g - r).max() / scale)
+    num = np.abs(g - r).max(axis=-1)
+    ref = np.abs(r).max(axis=-1)
+    top = max(float(ref.max()), 1e-30)
+    e = float((num / np.maximum(ref, floor * top)).max())
+    for f in SPREAD:                        # the same rule at other floors, for the record
+        SPREAD[f] = max(SPREAD[f], float((num / np.maximum(ref, f * top)).max()))
     WORST.append((e, what))
-    assert e <= tol, f"{what}: max error {e:.3e} of the slab's largest value > {tol}"
+    assert e <= tol, f"{what}: max head-vector error {e:.3e} > {tol} (floor {floor} of the slab)"
     return e
+
+
+SPREAD = {1.0: 0.0, 0.5: 0.0, 0.25: 0.0, 1 / 8: 0.0, 1 / 16: 0.0, 1 / 64: 0.0}
 
 
 def oracle_grads(st, Q, dO, Hq, theta, seqs, group_of):
@@ -114,7 +140,7 @@ def gather_grad_carry(dk, dv, s, layer, n):
 
 
 def check(co, dims, st, q, out, lse, dO_dev, group, orc_st, Q, dO, w, seqs, group_of, leaders,
-          layer_begin=0, layer_count=None, tag=""):
+          layer_begin=0, layer_count=None, tag="", floor=FLOOR_PATH):
     layer_count = w.L if layer_count is None else layer_count
     dk, dv, dkc, dvc = grad_buffers(st)
     dq = torch.zeros((layer_count,) + tuple(q.shape[1:]), dtype=torch.float32, device="cuda")
@@ -135,16 +161,16 @@ def check(co, dims, st, q, out, lse, dO_dev, group, orc_st, Q, dO, w, seqs, grou
                 heads = list(range(g * G, (g + 1) * G))
                 errs.append(slab_close(gq[li, s][:, heads].reshape(-1, w.hd),
                                        rq[layer, s][:, heads].reshape(-1, w.hd),
-                                       f"{tag} dq s{s} l{layer} g{g}"))
+                                       f"{tag} dq s{s} l{layer} g{g}", floor=floor))
         nu = orc_st.uk[s].shape[1]
         if nu:
             for layer in range(layer_begin, layer_begin + layer_count):
                 gk, gv = gather_grad_carry(dkc, dvc, s, layer, nu)
                 for g in range(w.Hkv):
                     errs.append(slab_close(gk[:, g], rcar[s][0][layer, :, g],
-                                           f"{tag} dk carry s{s} g{g}"))
+                                           f"{tag} dk carry s{s} g{g}", floor=floor))
                     errs.append(slab_close(gv[:, g], rcar[s][1][layer, :, g],
-                                           f"{tag} dv carry s{s} g{g}"))
+                                           f"{tag} dv carry s{s} g{g}", floor=floor))
     pt = st["page_table"]
     for grp, (rk, rv) in rcom.items():
         n = rk.shape[1]
@@ -153,11 +179,17 @@ def check(co, dims, st, q, out, lse, dO_dev, group, orc_st, Q, dO, w, seqs, grou
         for layer in range(layer_begin, layer_begin + layer_count):
             gk, gv = gather_grad_committed(dk, dv, pt[leaders[grp]], layer, n)
             for g in range(w.Hkv):
-                errs.append(slab_close(gk[:, g], rk[layer, :, g], f"{tag} dk group {grp} g{g}"))
-                errs.append(slab_close(gv[:, g], rv[layer, :, g], f"{tag} dv group {grp} g{g}"))
-    print(f"[backward] {tag}: max slab error {max(errs):.3e} over {len(errs)} slabs; worst: "
-          + ", ".join(f"{n} {e:.2e}" for e, n in sorted(WORST)[-3:]), flush=True)
+                errs.append(slab_close(gk[:, g], rk[layer, :, g], f"{tag} dk group {grp} g{g}",
+                                   floor=floor))
+                errs.append(slab_close(gv[:, g], rv[layer, :, g], f"{tag} dv group {grp} g{g}",
+                                   floor=floor))
+    print(f"[backward] {tag}: max head-vector error {max(errs):.3e} over {len(errs)} slabs; "
+          "worst: " + ", ".join(f"{n} {e:.2e}" for e, n in sorted(WORST)[-3:])
+          + "; at other floors: " + ", ".join(f"{f:g}: {e:.2e}" for f, e in SPREAD.items()),
+          flush=True)
     WORST.clear()
+    for f in SPREAD:
+        SPREAD[f] = 0.0
     return errs
 
 
@@ -338,3 +370,129 @@ def test_projection_backward_train_layout():
     for name, g, r in (("dW_F", dwf, ref[0]), ("dW_KV", dwkv, ref[1]), ("dE", de, ref[2])):
         e = slab_close(to_np(g).reshape(1, -1), r.reshape(1, -1), name)
         print(f"[backward] {name}: error {e:.3e} of the largest reference value", flush=True)
+
+
+# ------------------------------------------- the attention backward on its own
+
+def _all_rows_spec(w, which, n_seqs, n_rows):
+    """Directly drawn rows [n_seqs][L][Hkv][n_rows][hd] at logical positions
+    CARRY_T0.. of every sequence: element (s, l, g, r, :) is the element
+    (l, g, r, :) of spec_kv_direct(w, which, s, CARRY_T0, n_rows)."""
+    st_, shape, strides, base, sigma = wl.spec_kv_direct(w, which, 0, CARRY_T0, n_rows)
+    per_seq = w.L * w.Hkv * wl.TCAP * w.hd
+    return st_, (n_seqs,) + shape, (per_seq,) + strides, base, sigma
+
+
+def _direct_carry(w, st, n_seqs, n_rows):
+    """Fill rows 0..n_rows-1 of every sequence's carry segment with directly
+    drawn keys and values (device side)."""
+    from synth import device as sdev
+    k = sdev.materialise(w, _all_rows_spec(w, "k", n_seqs, n_rows), "cuda")   # [S][L][Hkv][n][hd]
+    v = sdev.materialise(w, _all_rows_spec(w, "v", n_seqs, n_rows), "cuda")
+    r = torch.arange(n_rows, device="cuda")
+    # k_carry [L][S][CP][Hkv][16][hd], v_carry [L][S][CP][Hkv][hd][16]
+    st["k_carry"][:, :, r // 16, :, r % 16, :] = k.permute(3, 1, 0, 2, 4)
+    st["v_carry"][:, :, r // 16, :, :, r % 16] = v.permute(3, 1, 0, 2, 4)
+
+
+def _oracle_carry(w, orc_st, s, nu):
+    """The same carry rows of sequence s on the host: [L][nu][Hkv][hd]."""
+    k = host(w, wl.spec_kv_direct(w, "k", s, CARRY_T0, nu)).transpose(0, 2, 1, 3)
+    v = host(w, wl.spec_kv_direct(w, "v", s, CARRY_T0, nu)).transpose(0, 2, 1, 3)
+    orc_st.uk[s] = k
+    orc_st.uv[s] = v
+
+
+def test_backward_direct_kv_serving():
+    """The attention backward alone, serving layout (one sequence per group):
+    committed and carry keys and values drawn directly, so the GPU and the
+    oracle read identical bf16 inputs.  Ragged contexts, a full carry block,
+    an empty sequence, a carry-only sequence, padded query rows (8 block rows
+    x 2 heads), two layers; per head vector at 2e-2 with the floor at 1/8 of
+    the slab."""
+    co = _gpu()
+    from synth.scenario import Scenario
+    from synth import device as sdev
+    w = SERVE.replace(name="bwd_direct_serve", seed=0x5EED33)
+    print(f"[backward] direct K/V, workload={w.name}", flush=True)
+    sc = Scenario(w)
+    orc = OracleRun(w)
+    carry = np.array([w.B, 0, 3, 1, 0, 5], np.int32)[:w.S]
+    ctx = wl.initial_ctx(w).astype(np.int32).copy()
+    ctx[4] = 0                                  # no keys at all
+    ctx[5] = 0                                  # carry rows only
+    _direct_carry(w, sc.st, w.S, w.B)
+    sc.st["ctx_len"].copy_(torch.from_numpy(ctx))
+    sc.st["carry_len"].copy_(torch.from_numpy(carry))
+    for s in range(w.S):
+        orc.st.ck[s] = orc.st.ck[s][:, :ctx[s]]
+        orc.st.cv[s] = orc.st.cv[s][:, :ctx[s]]
+        _oracle_carry(w, orc.st, s, int(carry[s]))
+    q = sdev.materialise(w, wl.spec_q(w, 0), "cuda")
+    out, lse = sc.new_output()
+    co.drafter_block_attention(sc.dims, 0, w.L, q, sc.st, out, lse, 0, sc.ws)
+    dO_dev = sdev.materialise(w, wl.spec_dout(w), "cuda")
+    torch.cuda.synchronize()
+    assert co.carryover_read_status(sc.st) == 0
+    Q = host(w, wl.spec_q(w, 0))
+    dO = host(w, wl.spec_dout(w))
+    seqs = list(range(w.S))
+    check(co, sc.dims, sc.st, q, out, lse, dO_dev, 1, orc.st, Q, dO, w, seqs, lambda s: s,
+          {s: s for s in seqs}, tag="direct serve", floor=FLOOR_UNIT)
+
+
+def test_backward_direct_kv_train_full_size():
+    """The attention backward alone in the training layout at full size (8
+    responses x 4096 positions, 2048 anchored blocks sharing their response's
+    pages, one group per response): every key and value drawn directly; the
+    256 blocks of response 2 against the oracle, including the sums over
+    those blocks of the shared keys' gradients; per head vector at 2e-2 with
+    the floor at 1/8 of the slab."""
+    co = _gpu()
+    from synth import device as sdev
+    w = wl.TRAIN_FWD
+    S, A, B = w.S, w.anchors, w.B
+    V = S * A
+    R = 2                                       # the response checked
+    print(f"[backward] direct K/V, workload={w.name} blocks={V}, response {R} checked",
+          flush=True)
+    pt = wl.page_table(w)
+    P = w.max_pages_per_seq
+    dims = co.make_dims(S, w.seq_len, w.Dcat, w.d, w.L, w.Hq, w.Hkv, w.hd, P, pt.size, w.dtype,
+                        w.theta)
+    st = co.alloc_state(dims, pt, "cuda")
+    for s in range(S):
+        k = sdev.materialise(w, wl.spec_kv_direct(w, "k", s, 0, w.seq_len), "cuda")
+        v = sdev.materialise(w, wl.spec_kv_direct(w, "v", s, 0, w.seq_len), "cuda")
+        co.carryover_import_kv(dims, s, 0, k, v, st)
+        del k, v
+    a, u, a2 = wl.anchors(w)
+    vdims = co.make_dims(V, B, w.Dcat, w.d, w.L, w.Hq, w.Hkv, w.hd, P, pt.size, w.dtype,
+                         w.theta)
+    vst = co.alloc_state(vdims, np.repeat(pt, A, axis=0), "cuda")
+    vst["k_cache"], vst["v_cache"] = st["k_cache"], st["v_cache"]
+    vst["ctx_len"].copy_(torch.from_numpy(a2.ravel().astype(np.int32)))
+    vst["carry_len"].copy_(torch.from_numpy(u.ravel().astype(np.int32)))
+    _direct_carry(w, vst, V, B)
+    q = sdev.materialise(w, wl.spec_q(w, 0, S=V), "cuda")
+    out = torch.empty((w.L, V, B, w.Hq, w.hd), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((w.L, V, B, w.Hq), dtype=torch.float32, device="cuda")
+    ws = torch.zeros(max(co.workspace_bytes(vdims, co.CO_WS_ROUND), 256), dtype=torch.uint8,
+                     device="cuda")
+    co.drafter_block_attention(vdims, 0, w.L, q, vst, out, lse, co.CO_ATTN_SHARED_PREFIX, ws)
+    dO_dev = sdev.materialise(w, wl.spec_dout(w, S=V), "cuda")
+    torch.cuda.synchronize()
+    assert co.carryover_read_status(vst) == 0
+
+    sample = list(range(R * A, (R + 1) * A))
+    ost = oracle.State(V, w.L, w.Hkv, w.hd)
+    kr = host(w, wl.spec_kv_direct(w, "k", R, 0, w.seq_len)).transpose(0, 2, 1, 3)
+    vr = host(w, wl.spec_kv_direct(w, "v", R, 0, w.seq_len)).transpose(0, 2, 1, 3)
+    a2f, uf = a2.ravel(), u.ravel()
+    for vv in sample:
+        ost.set_committed(vv, kr[:, :a2f[vv]], vr[:, :a2f[vv]])
+        _oracle_carry(w, ost, vv, int(uf[vv]))
+    Q = seq_block(w, wl.spec_q(w, 0, S=V), 1, sample)
+    dO = seq_block(w, wl.spec_dout(w, S=V), 1, sample)
+    check(co, vdims, vst, q, out, lse, dO_dev, A, ost, Q, dO, w, sample, lambda v: v // A,
+          {R: R * A}, tag="direct train", floor=FLOOR_UNIT)

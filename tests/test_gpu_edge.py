@@ -337,3 +337,76 @@ def test_round_rejected_on_the_host_leaves_the_state_untouched(which):
     assert co.carryover_read_status(sc.st) == 0
     rr, O, LSE = orc.round(0)
     compare_round(sc, orc, rr, O, LSE, out, lse, sc.rt, orc.seqs, f"after rejected {which}")
+
+
+# 64 chained rounds on contexts that grow across page boundaries, two layers,
+# head_dim 64 and 128 (the two attention kernels of a serving round)
+SPLIT = [EDGE.replace(name="split_hd64", S=5, rounds=64, accept=("geom", 0.3), seed=0x5EED40),
+         wl.Workload("split_hd128", S=3, B=16, Dcat=512, d=256, L=2, Hq=8, Hkv=2, hd=128,
+                     dtype="bf16", theta=1e6, ctx_lo=30, ctx_hi=700, ctx_mode="direct",
+                     accept=("geom", 0.3), rounds=64, seed=0x5EED41)]
+
+
+def _chain(co, sc, rounds, keep):
+    """Rounds ``rounds`` of sc's chain; (out, lse) of each on the host in keep."""
+    for r in rounds:
+        out, lse, _ = _round(co, sc, r)
+        assert co.carryover_read_status(sc.st) == 0
+        keep[r] = (out.cpu(), lse.cpu())
+
+
+def _live_rows(sc):
+    """Every committed row [0, ctx_len) (gathered by logical position) and every
+    carry row [0, carry_len) of every sequence and layer."""
+    from helpers import gather_carry, gather_committed
+    ctx = sc.st["ctx_len"].cpu().numpy()
+    car = sc.st["carry_len"].cpu().numpy()
+    rows = []
+    for s in range(sc.w.S):
+        for layer in range(sc.w.L):
+            rows += gather_committed(sc.st, sc.pt, s, layer, 0, int(ctx[s]))
+            rows += gather_carry(sc.st, s, layer, int(car[s]))
+    return rows
+
+
+@pytest.mark.parametrize("w", SPLIT, ids=lambda w: w.name)
+def test_split_chain_equals_one_chain(w):
+    """A chain of 64 rounds equals 32 rounds, a copy of the whole drafter state
+    into freshly allocated buffers, and 32 more rounds on the copy: every
+    round's output and LSE and every live committed and carry row bit for bit.
+    Also the rewind the benchmark times from: after round 63, restoring only
+    the lengths saved after round 31 and running rounds 32..63 again gives the
+    same outputs bit for bit (rows beyond ctx_len are never read and the carry
+    segment is replaced before it is read)."""
+    Scenario, co = _gpu()
+    R, H = w.rounds, w.rounds // 2
+    print(f"[edge] split chain workload={w.name} rounds={R}", flush=True)
+    a = Scenario(w)
+    one = {}
+    _chain(co, a, range(H), one)
+    snap = (a.st["ctx_len"].clone(), a.st["carry_len"].clone())
+    _chain(co, a, range(H, R), one)
+
+    b = Scenario(w)
+    two = {}
+    _chain(co, b, range(H), two)
+    fresh = co.alloc_state(b.dims, b.pt, "cuda")
+    for k in fresh:
+        fresh[k].copy_(b.st[k])
+    b.st = fresh
+    torch.cuda.synchronize()
+    _chain(co, b, range(H, R), two)
+    for r in range(R):
+        assert torch.equal(one[r][0], two[r][0]) and torch.equal(one[r][1], two[r][1]), f"r{r}"
+    for key in ("ctx_len", "carry_len"):
+        assert torch.equal(a.st[key], b.st[key]), key
+    for x, y in zip(_live_rows(a), _live_rows(b)):
+        assert np.array_equal(x, y)
+
+    a.st["ctx_len"].copy_(snap[0])
+    a.st["carry_len"].copy_(snap[1])
+    again = {}
+    _chain(co, a, range(H, R), again)
+    for r in range(H, R):
+        assert torch.equal(one[r][0], again[r][0]) and torch.equal(one[r][1], again[r][1]), \
+            f"rewound r{r}"

@@ -8,6 +8,7 @@ round, the carry rows) must match per head vector within 2e-2 (bf16) or 1e-4
 import numpy as np
 import pytest
 
+import oracle
 from synth import workloads as wl
 
 pytestmark = pytest.mark.gpu
@@ -146,18 +147,21 @@ def test_attention_slicings(w, slicing, tune):
     run_rounds(w, 2)
 
 
-def sampled_chain(w, rounds, samples, check, layers):
+def sampled_chain(w, rounds, samples, plan):
     """Chained serving rounds at full size in the launch configuration of a
     serving round.  Every round: routing, accepted lengths, descriptors and
     lengths of all sequences bit-exact; the committed rows written and the
-    carry rows of the sampled sequences within tolerance.  At the rounds in
-    ``check`` also the attention output of the sampled sequences in ``layers``."""
+    carry rows of the sequences in ``samples`` within tolerance.  ``plan(r)``
+    lists the (sequences, layers) whose attention output is checked at round
+    r (empty: none)."""
     import paper_2609_14717_amd as co
     Scenario = _gpu()
     tol = TOL[w.dtype]
     print(f"[parity] workload={w.name} rounds={rounds} samples={samples}", flush=True)
     sc = Scenario(w)
     orc = OracleRun(w, seqs=samples, store=np.float32)
+    print(f"[parity] {w.name}: oracle state built", flush=True)
+    n_out = 0
     for r in range(rounds):
         hidden, q, draft, target, m = sc.round_inputs(r)
         out, lse = sc.new_output()
@@ -165,8 +169,7 @@ def sampled_chain(w, rounds, samples, check, layers):
                            sc.ws)
         torch.cuda.synchronize()
         assert co.carryover_read_status(sc.st) == 0
-        att = r in check
-        rr, O, LSE = orc.round(r, attend=att, layers=layers if att else None)
+        rr, _, _ = orc.round(r, attend=False)
         for key in ("accept_len", "row_pos", "row_dst"):
             np.testing.assert_array_equal(sc.rt[key].cpu().numpy(), rr[key], err_msg=f"r{r} {key}")
         np.testing.assert_array_equal(sc.st["ctx_len"].cpu().numpy(), rr["ctx_len"])
@@ -186,34 +189,56 @@ def sampled_chain(w, rounds, samples, check, layers):
                     gk, gv = gather_carry(sc.st, s, layer, u)
                     assert_heads_close(gk, orc.st.uk[s][layer], tol, f"r{r} s{s} U_k l{layer}")
                     assert_heads_close(gv, orc.st.uv[s][layer], tol, f"r{r} s{s} U_v l{layer}")
-            if att:
-                g = to_np(out[:, s])
-                gl = lse[:, s].cpu().numpy().astype(np.float64)
+        pieces = plan(r)
+        if not pieces:
+            continue
+        g = to_np(out)
+        gl = lse.cpu().numpy().astype(np.float64)
+        Q = orc.seq_block(wl.spec_q(w, r), 1)
+        for seqs, layers in pieces:
+            O, LSE = oracle.attend_state(orc.st, Q, w.Hq, w.theta, seqs=seqs, layers=layers)
+            for s in seqs:
                 for layer in layers:
-                    assert_heads_close(g[layer], O[layer, s], tol, f"r{r} s{s} O layer {layer}")
-                    err = np.abs(gl[layer] - LSE[layer, s]).max()
+                    assert_heads_close(g[layer, s], O[layer, s], tol, f"r{r} s{s} O layer {layer}")
+                    err = np.abs(gl[layer, s] - LSE[layer, s]).max()
                     assert err <= tol, f"r{r} s{s} LSE layer {layer}: {err}"
-        if att:
-            print(f"[parity] {w.name} round {r} checked", flush=True)
+                    n_out += 1
+        print(f"[parity] {w.name} round {r}: attention of "
+              + "; ".join(f"seqs {list(s_)} layers {list(l_)}" for s_, l_ in pieces)
+              + " checked", flush=True)
+    print(f"[parity] {w.name}: {n_out} (sequence, layer) outputs checked", flush=True)
 
 
-def test_long_chain_5layer_sampled():
+@pytest.mark.timeout(900)
+def test_long_chain_5layer_full():
     """The 64-round, 5-layer chain at full size (16 sequences, contexts of
-    16K-32K tokens, head_dim 128, 32/8 heads): one sampled sequence every
-    round, its attention output in layers 0 and 4 at rounds 0, 1, 31 and 63."""
-    sampled_chain(wl.LONG_CHAIN, wl.LONG_CHAIN.rounds, [5], {0, 1, 31, 63}, [0, 4])
+    16K-32K tokens, head_dim 128, 32/8 heads), every sequence tracked by the
+    oracle: every round the routing, lengths and the committed and carry rows
+    written of all 16 sequences in all 5 layers; the attention output of one
+    (sequence, layer) every round (sequence r mod 16, layer r mod 5), of every
+    sequence in layer 0 at rounds 0 and 31, and of every sequence in every
+    layer at the last round."""
+    w = wl.LONG_CHAIN
+    R, S, L = w.rounds, w.S, w.L
+    every = list(range(S))
+
+    def plan(r):
+        if r == R - 1:
+            return [(every, list(range(L)))]
+        if r in (0, R // 2 - 1):
+            return [(every, [0])]
+        return [([r % S], [r % L])]
+
+    sampled_chain(w, R, every, plan)
 
 
-def test_ragged_batch32_8b_sampled():
+def test_ragged_batch32_8b_full():
     """The batch-32 ragged round at the 8B widths (Dcat 20480 -> d 4096, 32/8
-    heads of 128, contexts of 512-8192 tokens): four rounds, three sampled
-    sequences (the shortest, the longest and one between), their attention
-    output every round."""
+    heads of 128, contexts of 512-8192 tokens): four chained rounds, all 32
+    sequences' rows and attention outputs against the oracle every round."""
     w = wl.RAGGED32_8B
-    ctx0 = wl.initial_ctx(w)
-    order = np.argsort(ctx0, kind="stable")
-    samples = sorted({int(order[0]), int(order[len(order) // 2]), int(order[-1])})
-    sampled_chain(w, 4, samples, {0, 1, 2, 3}, [0])
+    every = list(range(w.S))
+    sampled_chain(w, 4, every, lambda r: [(every, [0])])
 
 
 def test_train_fwd_sampled():
@@ -222,8 +247,11 @@ def test_train_fwd_sampled():
     sequences sharing their response's pages), every block's rejected rows
     projected with E into its own carry segment, then block attention of all
     2048 blocks over their recorded prefix [0, a') plus their carry rows.
-    Routing of all 2048 blocks bit-exact; for a sample of blocks the carry rows
-    and the attention output; for the sampled responses the prefilled rows."""
+    Routing of all 2048 blocks bit-exact; the carry rows and the attention
+    output of all 256 blocks of response 3 and of a sample of the others
+    (first and last blocks, extreme anchors, full acceptance and full
+    rejection); every prefilled row of response 3 and the first and last rows
+    of the other sampled responses."""
     from helpers import OracleTrain
     Scenario = _gpu()
     from synth.scenario import TrainScenario
@@ -239,6 +267,8 @@ def test_train_fwd_sampled():
         if hit.size:
             sample.add(int(hit[0]))
     sample |= {int(x) for x in np.random.default_rng(5).choice(8 * A, 6, replace=False)}
+    FULL = 3                                    # the response checked block by block
+    sample |= set(range(FULL * A, (FULL + 1) * A))
     sample = sorted(sample)
     print(f"[parity] workload={w.name} sample={sample}", flush=True)
     sc = TrainScenario(w)
@@ -265,8 +295,9 @@ def test_train_fwd_sampled():
         err = np.abs(gl[:, v] - orc.LSE[:, v]).max()
         assert err <= tol, f"LSE v{v}: {err}"
     for s, (k, vv) in orc.parent.items():
+        spans = [(0, w.seq_len)] if s == FULL else [(0, 40), (w.seq_len - 40, w.seq_len)]
         for layer in range(w.L):
-            for t0, t1 in ((0, 40), (w.seq_len - 40, w.seq_len)):
+            for t0, t1 in spans:
                 gk, gv = gather_committed(sc.st, sc.pt, s, layer, t0, t1)
                 assert_heads_close(gk, k[t0:t1, layer], tol, f"prefill K s{s}")
                 assert_heads_close(gv, vv[t0:t1, layer], tol, f"prefill V s{s}")
