@@ -42,6 +42,10 @@ PROFILES = os.path.join(ROOT, "profiles")
 # of these are not reported
 ATTN_SOURCES = [os.path.join(ROOT, "paper_2609_14717_amd", "csrc", f)
                 for f in ("attention.hip", "co_device.h", "co_kernels.h")]
+PROJ_SOURCES = [os.path.join(ROOT, "paper_2609_14717_amd", "csrc", f)
+                for f in ("project.hip", "co_device.h", "co_kernels.h", "co_store.h")]
+PROJ_KERNELS = ("gemm_bf16_kernel", "gemm_wide_kernel", "proj_fused_kernel", "epi_z_kernel",
+                "epi_kv_kernel", "z_norm_kernel", "gemm_f32_kernel")
 ATTN_KERNELS = ("attn_bf16_kernel", "attn_wave_kernel", "attn_bf16_combine_kernel",
                 "attn_group_kernel", "attn_share_merge_kernel")
 ATTN_KERNELS_F32 = ("attn_f32_kernel", "attn_chunk_merge_kernel")
@@ -56,7 +60,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="ragged_batch32")
-    ap.add_argument("--cpu-baseline-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-baseline-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mb", type=int, default=0,
                     help="after the timed region, run one plain copy of this many MiB "
@@ -66,38 +70,85 @@ def parse():
                          "(FETCH_SIZE, then WRITE_SIZE) and exit")
     ap.add_argument("--summarize-stats", metavar="STATS_CSV",
                     help="write the kernel-time summary of a rocprofv3 --stats run and exit")
+    ap.add_argument("--summarize-mfma", metavar="RUN_DIR",
+                    help="write the MFMA counter summary of a rocprofv3 --pmc run of "
+                         "'--only projection' or '--only prefill' and exit")
+    ap.add_argument("--bench-json", metavar="FILE",
+                    help="the JSON line the profiled bench command printed (for the summaries)")
+    ap.add_argument("--only", choices=("projection", "prefill"),
+                    help="time only carryover_project_kv: the projection of a round's rows "
+                         "('projection'), or the whole context as one call ('prefill'); "
+                         "prints one JSON line (the run the MFMA counters are taken on)")
     ap.add_argument("--command", default="", help="command recorded in a summary")
     return ap.parse_args()
 
 
-def attention_digest():
+def source_digest(files):
     h = hashlib.sha256()
-    for f in ATTN_SOURCES:
+    for f in files:
         with open(f, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
+
+
+def attention_digest():
+    return source_digest(ATTN_SOURCES)
+
+
+def read_summary(path):
+    """key: value lines of a committed profile summary."""
+    vals = {}
+    if os.path.exists(path):
+        with open(path) as fh:
+            for line in fh:
+                if ":" in line and not line.startswith("#"):
+                    k, v = line.split(":", 1)
+                    vals[k.strip()] = v.strip()
+    return vals
 
 
 def traffic_file(workload):
     return os.path.join(PROFILES, f"attention_traffic_{workload}.txt")
 
 
-def recorded_traffic(workload):
-    """HBM bytes per attention launch from the committed counter summary, or
-    None when there is none or the kernels changed since it was taken."""
-    path = traffic_file(workload)
-    if not os.path.exists(path):
-        return None
-    vals = {}
-    with open(path) as fh:
-        for line in fh:
-            if ":" in line:
-                k, v = line.split(":", 1)
-                vals[k.strip()] = v.strip()
-    if vals.get("attention_source_digest") != attention_digest():
+def recorded_traffic(workload, steps, warmup, per_launch):
+    """(traffic, profiled): HBM bytes per attention launch from the committed
+    counter summary when it was taken on the same kernels at the same chain
+    state as this run (same workload, steps and warm-up, same algorithmic
+    bytes), else None; ``profiled`` describes the profiled state and its
+    measured / algorithmic ratio whenever the kernels match."""
+    vals = read_summary(traffic_file(workload))
+    if not vals or vals.get("attention_source_digest") != attention_digest():
+        return None, None
+    try:
+        t = float(vals["traffic_bytes_per_launch"])
+        a = float(vals["algorithmic_bytes_per_launch"])
+        st, wu = int(vals["profiled_steps"]), int(vals["profiled_warmup"])
+    except (KeyError, ValueError):
+        return None, None
+    prof = {"file": os.path.relpath(traffic_file(workload), ROOT), "steps": st, "warmup": wu,
+            "traffic_bytes_per_launch": t, "algorithmic_bytes_per_launch": a,
+            "ratio": t / a if a else None}
+    same = st == steps and wu == warmup and per_launch is not None and abs(a - per_launch) < 0.5
+    return (t if same else None), prof
+
+
+def mfma_file(workload, only):
+    return os.path.join(PROFILES, f"mfma_{workload}_{only}.txt")
+
+
+def recorded_mfma(workload, only):
+    """Counter figures of the projection call from the committed MFMA summary,
+    when it was taken on the same projection kernels; else None."""
+    path = mfma_file(workload, only)
+    vals = read_summary(path)
+    if not vals or vals.get("projection_source_digest") != source_digest(PROJ_SOURCES):
         return None
     try:
-        return float(vals["traffic_bytes_per_launch"])
+        return {"file": os.path.relpath(path, ROOT),
+                "mfma_busy_frac": float(vals["mfma_busy_frac"]),
+                "counted_bf16_flops_per_call": float(vals["counted_bf16_flops_per_call"]),
+                "counted_mfma_frac": float(vals["counted_mfma_frac"])}
     except (KeyError, ValueError):
         return None
 
@@ -153,6 +204,13 @@ def summarize_pmc(args):
             cnt += len(vals)
         return tot, cnt
 
+    if not args.bench_json:
+        raise SystemExit("--bench-json must give the JSON line of the profiled run")
+    bj = load_bench_json(args.bench_json)
+    if bj["config"]["workload"] != args.workload or (bj["steps"], bj["warmup"]) != (
+            args.steps, args.warmup):
+        raise SystemExit("--bench-json is not the line of this workload, steps and warm-up")
+    alg = bj["roofline"]["algorithmic_bytes_per_launch"]
     cf, _ = one(fetch, "FETCH_SIZE", "copy16_kernel")
     cw, _ = one(write, "WRITE_SIZE", "copy16_kernel")   # the calibration copy: one dispatch
     f_fac = copy_bytes / (cf * 1024.0)
@@ -161,6 +219,9 @@ def summarize_pmc(args):
              f"command (FETCH_SIZE pass): {args.command.replace('{COUNTER}', 'FETCH_SIZE')}",
              f"command (WRITE_SIZE pass): {args.command.replace('{COUNTER}', 'WRITE_SIZE')}",
              f"attention_source_digest: {attention_digest()}",
+             f"profiled_steps: {args.steps}",
+             f"profiled_warmup: {args.warmup}",
+             f"algorithmic_bytes_per_launch: {alg:.0f}",
              f"dispatches used: {win[1]} of each attention kernel from index {win[0]} (the "
              f"timed stand-alone attention calls on the final state)",
              f"copy_kernel_bytes: {copy_bytes}",
@@ -178,8 +239,106 @@ def summarize_pmc(args):
                      f"WRITE_SIZE {kw:.1f} KiB/dispatch ({nw} dispatches), "
                      f"calibrated {b / 1e6:.3f} MB")
     lines.append(f"traffic_bytes_per_launch: {tot:.0f}")
+    lines.append(f"measured / algorithmic: {tot / alg:.3f}")
     os.makedirs(PROFILES, exist_ok=True)
     with open(traffic_file(args.workload), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def load_bench_json(path):
+    """The last JSON line of a bench run's output."""
+    with open(path) as fh:
+        lines = [ln for ln in fh if ln.lstrip().startswith("{")]
+    if not lines:
+        raise SystemExit(f"no JSON line in {path}")
+    return json.loads(lines[-1])
+
+
+MFMA_GAP_NS = 50_000_000   # the pause bench.py --only leaves before the calls it times
+
+
+def summarize_mfma(args):
+    """MFMA counters of the projection call from a rocprofv3 --pmc run (with
+    --kernel-trace) of ``bench.py --only ...``: the projection-kernel
+    dispatches after the last pause of more than 50 ms are the warm-up and
+    timed calls (``bench.py --only`` pauses before them), all of the same
+    shape.  Per call: the MFMA busy share of the SIMD cycles (rocprofv3's
+    MfmaUtil, time-weighted over the dispatches), counted bf16 MFMA flops
+    (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) against the algorithmic flops, and
+    the counted rate over the call's event time."""
+    import glob
+    if not args.bench_json:
+        raise SystemExit("--bench-json must give the JSON line of the profiled run")
+    bj = load_bench_json(args.bench_json)
+    only, ncalls = bj["only"], bj["calls"] + bj["warm"]
+    files = glob.glob(os.path.join(args.summarize_mfma, "**", "*counter_collection.csv"),
+                      recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {args.summarize_mfma}")
+    disp = {}
+    for f in files:
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if not any(is_kernel(r["Kernel_Name"], k) for k in PROJ_KERNELS):
+                    continue
+                d = disp.setdefault(int(r["Dispatch_Id"]), {
+                    "name": r["Kernel_Name"], "grid": int(r["Grid_Size"]),
+                    "t0": int(r["Start_Timestamp"]), "t1": int(r["End_Timestamp"])})
+                d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    order = sorted(disp.values(), key=lambda d: d["t0"])
+    cut = 0
+    for i in range(1, len(order)):
+        if order[i]["t0"] - order[i - 1]["t1"] > MFMA_GAP_NS:
+            cut = i
+    window = order[cut:]
+    kinds = {}
+    for d in window:
+        k = kinds.setdefault((d["name"], d["grid"]), {"n": 0, "dur": 0.0, "util_t": 0.0,
+                                                     "mops": 0.0})
+        dur = (d["t1"] - d["t0"]) / 1e3
+        k["n"] += 1
+        k["dur"] += dur
+        k["util_t"] += d.get("MfmaUtil", 0.0) / 100.0 * dur
+        k["mops"] += d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0)
+    if not kinds or any(k["n"] % ncalls for k in kinds.values()):
+        raise SystemExit("the dispatches after the pause are not whole calls")
+    dur = sum(k["dur"] for k in kinds.values()) / ncalls
+    busy = sum(k["util_t"] for k in kinds.values()) / max(sum(k["dur"] for k in kinds.values()),
+                                                          1e-12)
+    counted = sum(k["mops"] for k in kinds.values()) * 512.0 / ncalls
+    ev_s = bj["avg_call_us"] / 1e6
+    peak = MFMA_PEAK_TFLOPS["bf16"]
+    lines = [f"# MFMA counters of carryover_project_kv, workload {args.workload} ({only})",
+             f"command (counter pass): {args.command}",
+             f"projection_source_digest: {source_digest(PROJ_SOURCES)}",
+             f"call: {bj['call']}",
+             f"rows per call: {bj['rows']}",
+             f"calls in the window: {ncalls} ({bj['warm']} warm-up + {bj['calls']} timed), "
+             f"{len(window)} dispatches",
+             f"event time per call (bench line, no profiler): {bj['avg_call_us']:.2f} us",
+             f"algorithmic flops per call: {bj['flops_per_call']:.6g}",
+             f"algorithmic rate: {bj['tflops']:.1f} TFLOP/s = {bj['mfma_frac']:.3f} of "
+             f"{peak:.0f} TFLOP/s",
+             "",
+             f"{'kernel':80s} {'grid':>9s} {'per call':>8s} {'us(pmc)':>8s} {'MfmaUtil':>8s} "
+             f"{'bf16 GFLOP':>10s}"]
+    for (kn, grid), k in sorted(kinds.items(), key=lambda x: -x[1]["dur"]):
+        short = kn if len(kn) <= 80 else kn[:77] + "..."
+        lines.append(f"{short:80s} {grid:9d} {k['n'] // ncalls:8d} {k['dur'] / k['n']:8.2f} "
+                     f"{k['util_t'] / max(k['dur'], 1e-12):8.3f} "
+                     f"{k['mops'] * 512 / k['n'] / 1e9:10.3f}")
+    lines += ["",
+              f"kernel time per call under the counters: {dur:.2f} us",
+              f"mfma_busy_frac: {busy:.4f}",
+              f"counted_bf16_flops_per_call: {counted:.6g}",
+              f"counted / algorithmic flops: {counted / bj['flops_per_call']:.3f}",
+              f"counted_mfma_frac: {counted / ev_s / 1e12 / peak:.4f}",
+              "(mfma_busy_frac: rocprofv3's MfmaUtil -- MFMA busy cycles over the SIMD cycles "
+              "of each dispatch -- weighted by dispatch time; counted_mfma_frac: counted bf16 "
+              "MFMA flops per call over the call's event time, against the dense bf16 peak)"]
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(mfma_file(args.workload, only), "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
@@ -248,6 +407,17 @@ def attention_bytes(w, ctx, carry):
     return kv + 2 * q + w.L * w.S * w.B * w.Hq * 4
 
 
+def train_attention_bytes(w, carried):
+    """Algorithmic HBM bytes of the training-shaped attention: every recorded
+    position's K/V read once (the blocks of a response share its pages), every
+    carry row read once, queries read once, outputs and fp32 LSE written once."""
+    es = 2 if w.dtype == "bf16" else 4
+    V = w.S * w.anchors
+    kv = (w.S * w.seq_len + carried) * w.L * w.Hkv * w.hd * 2 * es
+    q = w.L * V * w.B * w.Hq * w.hd * es
+    return float(kv + 2 * q + w.L * V * w.B * w.Hq * 4)
+
+
 def projection_work(w, M):
     """Algorithmic flops and HBM bytes of one carryover_project_kv call over M
     window rows: both products (F over Dcat, then K/V of every layer over d),
@@ -263,7 +433,10 @@ def attention_flops(w, keys_total):
     return 2.0 * 2.0 * keys_total * w.L * w.B * w.Hq * w.hd
 
 
-def timed_calls(torch, stream, n, call, warm=3, between=None):
+TIMED_WARM = 3      # untimed calls before the timed ones in timed_calls
+
+
+def timed_calls(torch, stream, n, call, warm=TIMED_WARM, between=None):
     """Average duration (s) of ``call`` over n calls, each bracketed by HIP events
     recorded on ``stream``; ``between`` (untimed) runs before each call."""
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -291,25 +464,73 @@ def projection_result(w, flops, nbytes, sec, rows=None):
             "hbm_frac": gbs / HBM_PEAK_GBS}
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, budget_s):
-    """The fp64 oracle on this host: full rounds of the same workload."""
+    """The fp64 oracle on this host, on a bounded sample of the same workload:
+    for half the budget with numpy's BLAS on all its threads, then for the
+    other half on one thread, each from the same initial state.  Serving
+    workloads run consecutive full rounds of all sequences, or of two of them
+    where the contexts are long (the rate is then scaled to the whole batch:
+    sequences are independent); the training-shaped forward runs the anchored
+    blocks of one response (scaled to all responses)."""
     import oracle  # noqa: F401  (test infrastructure: CPU baseline leg only)
-    from threadpoolctl import threadpool_info
+    from threadpoolctl import threadpool_info, threadpool_limits
     sys.path.insert(0, os.path.join(ROOT, "tests"))
-    from helpers import OracleRun
-    orc = OracleRun(w)
-    t0 = time.perf_counter()
-    n = 0
-    while True:
-        orc.round(n)
-        n += 1
-        if time.perf_counter() - t0 >= budget_s:
-            break
-    dt = time.perf_counter() - t0
+    from helpers import OracleRun, OracleTrain
+
+    if w.anchors:
+        unit, scale = "forwards/s", 1.0 / w.S
+        sample = (f"the second drafter pass of the {w.anchors} anchored blocks of one response "
+                  f"(projection of its {w.seq_len} recorded rows, carry rows, block attention; "
+                  f"float64), rate scaled to all {w.S} responses")
+
+        def leg(seconds):
+            t0 = time.perf_counter()
+            n = 0
+            while True:
+                OracleTrain(w, range(w.anchors))
+                n += 1
+                if time.perf_counter() - t0 >= seconds:
+                    break
+            return n, time.perf_counter() - t0
+    else:
+        long_ctx = w.L * w.ctx_hi * w.Hkv * w.hd > (1 << 24)
+        seqs = [0, 1] if long_ctx else list(range(w.S))
+        unit, scale = "rounds/s", len(seqs) / w.S
+        sample = (f"consecutive full rounds of {w.name} ({len(seqs)} of {w.S} sequences, "
+                  f"route+project+attention in float64) from the same initial state"
+                  + (", rate scaled to the whole batch" if len(seqs) < w.S else ""))
+
+        def leg(seconds):
+            orc = OracleRun(w, seqs=seqs, store=np.float32 if long_ctx else np.float64)
+            t0 = time.perf_counter()
+            n = 0
+            while True:
+                orc.round(n)
+                n += 1
+                if time.perf_counter() - t0 >= seconds:
+                    break
+            return n, time.perf_counter() - t0
+
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    return {"value": n / dt, "unit": "rounds/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{n} consecutive full rounds of {w.name} (all {w.S} sequences, "
-                      f"route+project+attention in float64) from the same initial state"}
+    n_all, dt_all = leg(budget_s / 2)
+    with threadpool_limits(limits=1):
+        n_one, dt_one = leg(budget_s / 2)
+    return {"value": n_all / dt_all * scale, "unit": unit, "cores": int(threads),
+            "kind": "oracle", "sample": f"{n_all} x " + sample,
+            "single_thread": {"value": n_one / dt_one * scale, "steps": n_one},
+            "host": {"cpu_model": cpu_model(), "nproc": os.cpu_count(),
+                     "affinity": len(os.sched_getaffinity(0)), "blas_threads": int(threads)}}
 
 
 def main():
@@ -318,6 +539,8 @@ def main():
         return summarize_pmc(args)
     if args.summarize_stats:
         return summarize_stats(args)
+    if args.summarize_mfma:
+        return summarize_mfma(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the drafter step "
               "shards by sequence with no exchange, so multi-GPU runs are not part of this "
@@ -336,6 +559,8 @@ def main():
     torch.cuda.set_device(0)
     sc = Scenario(w)
     stream = torch.cuda.current_stream()
+    if args.only:
+        return only_projection(args, torch, co, sc, w, stream)
 
     # pre-stage every round's inputs in HBM
     inputs = [sc.round_inputs(r) for r in range(total)]
@@ -415,6 +640,7 @@ def main():
     assert np.array_equal(ctx_f, ctx), "host replica of the lengths diverged"
     per_launch = float(attention_bytes(w, ctx_f, car_f))
     achieved = per_launch / att_s / 1e9
+    traffic, traffic_profiled = recorded_traffic(w.name, args.steps, args.warmup, per_launch)
 
     # The projection entry point, timed the same way: the last round's rows
     # projected again into the slots they already occupy (same values).
@@ -481,14 +707,16 @@ def main():
                          ATTN_KERNELS if w.dtype == "bf16" else ATTN_KERNELS_F32) + ")",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": recorded_traffic(w.name),
+                     "traffic": traffic,
+                     "traffic_profiled": traffic_profiled,
                      "algorithmic_bytes_per_launch": per_launch,
                      "avg_launch_us": att_s * 1e6,
                      "tflops": attention_flops(w, keys) / att_s / 1e12,
                      "cold": {"avg_launch_us": cold_att_s * 1e6,
                               "achieved": per_launch / cold_att_s / 1e9,
                               "frac": per_launch / cold_att_s / 1e9 / HBM_PEAK_GBS}},
-        "projection": projection_result(w, pflops, pbytes, proj_s),
+        "projection": dict(projection_result(w, pflops, pbytes, proj_s),
+                           counters=recorded_mfma(w.name, "projection")),
         "cold_round_us": cold_round_s * 1e6,
         "baseline_mode": {"rounds_per_s": args.steps / dt_base,
                           "t_reuse_us": (dt - dt_base) / args.steps * 1e6},
@@ -572,7 +800,38 @@ class Scrub:
         self.b.copy_(self.a)
 
 
-def prefill_point(torch, co, sc, w):
+def only_projection(args, torch, co, sc, w, stream):
+    """``--only``: carryover_project_kv alone, ``args.steps`` calls timed with
+    HIP events (after 3 untimed ones): the rows of round 0 projected again into
+    the slots they occupy, or the whole initial context as one call."""
+    if args.only == "prefill":
+        if w.ctx_mode != "projected":
+            raise SystemExit(f"{w.name} has no projected context to prefill")
+        res = prefill_point(torch, co, sc, w, calls=args.steps, pause_first=True)
+    else:
+        hidden, q, draft, target, _ = sc.round_inputs(0)
+        out, lse = sc.new_output()
+        co.carryover_round(sc.dims, sc.W, hidden, draft, target, q, sc.st, sc.rt, out, lse, 0,
+                           sc.ws)
+        pause(torch)
+        sec = timed_calls(torch, stream, args.steps, lambda: co.carryover_project_kv(
+            sc.dims, sc.W, hidden, sc.rt, sc.st, sc.ws, ws_bytes=sc.ws_project))
+        flops, nbytes = projection_work(w, w.S * w.B)
+        res = projection_result(w, flops, nbytes, sec)
+    if co.carryover_read_status(sc.st):
+        raise RuntimeError("device status after the projection calls")
+    res.update(only=args.only, calls=args.steps, warm=TIMED_WARM, config={"workload": w.name})
+    print(json.dumps(res), flush=True)
+
+
+def pause(torch):
+    """A pause of 0.1 s on an idle GPU: marks the start of the calls a counter
+    pass summarises."""
+    torch.cuda.synchronize()
+    time.sleep(0.1)
+
+
+def prefill_point(torch, co, sc, w, calls=20, pause_first=False):
     """The context projection as one call (every row committed, no E) over the
     initial contexts of all sequences: the rows are projected again into the
     slots they already hold (same values), timed like the other calls."""
@@ -593,14 +852,17 @@ def prefill_point(torch, co, sc, w):
     saved = (sc.st["ctx_len"].clone(), sc.st["carry_len"].clone())
     sc.st["ctx_len"].zero_()
     co.carryover_route(pd, None, None, co.CO_ROUTE_ACCEPT_ALL, sc.st, rt)
-    sec = timed_calls(torch, torch.cuda.current_stream(), 20,
+    if pause_first:
+        pause(torch)
+    sec = timed_calls(torch, torch.cuda.current_stream(), calls,
                       lambda: co.carryover_project_kv(pd, sc.W, h, rt, sc.st, ws))
     sc.st["ctx_len"].copy_(saved[0])
     sc.st["carry_len"].copy_(saved[1])
     if co.carryover_read_status(sc.st):
         raise RuntimeError("device status after the prefill projection")
     flops, nbytes = projection_work(w, w.S * n)
-    return projection_result(w, flops, nbytes, sec, rows=w.S * n)
+    return dict(projection_result(w, flops, nbytes, sec, rows=w.S * n),
+                counters=recorded_mfma(w.name, "prefill"))
 
 
 def calibrate_copy(torch, args):
@@ -629,6 +891,40 @@ def run_train(args, w):
     torch.cuda.set_device(0)
     sc = TrainScenario(w)
     stream = torch.cuda.current_stream()
+    V = w.S * w.anchors
+    vw = w.replace(S=V)
+    wsp = co.workspace_bytes(sc.vdims, co.CO_WS_PROJECT)
+
+    def projection_calls(n):
+        """The projection of one forward, each of its two calls timed alone: the
+        committed rows of every response (one call, every row committed) and
+        the rows of every anchored block (one call, the rejected rows go to the
+        block's carry segment, the others are skipped)."""
+        pc = timed_calls(torch, stream, n, lambda: co.carryover_project_kv(
+            sc.dims, sc.W, sc.h_committed, sc.crt, sc.st, sc.cws))
+        pv = timed_calls(torch, stream, n, lambda: co.carryover_project_kv(
+            sc.vdims, sc.W, sc.hidden, sc.vrt, sc.vst, sc.ws, ws_bytes=wsp))
+        carried = int(sc.vst["carry_len"].sum().item())
+        prows = w.S * w.seq_len + carried
+        pflops, pbytes = projection_work(vw, prows)
+        return pc, pv, prows, dict(
+            projection_result(vw, pflops, pbytes, pc + pv, rows=prows),
+            call="carryover_project_kv x2 (committed rows; anchored blocks' rows)",
+            committed_call_us=pc * 1e6, block_call_us=pv * 1e6,
+            rows_computed=w.S * w.seq_len + V * w.B)
+
+    if args.only:
+        if args.only != "projection":
+            raise SystemExit(f"{w.name}: only the projection can be timed alone")
+        sc.forward()
+        pause(torch)
+        *_, res = projection_calls(args.steps)
+        if co.carryover_read_status(sc.vst) or co.carryover_read_status(sc.st):
+            raise RuntimeError("device status")
+        res.update(only=args.only, calls=args.steps, warm=TIMED_WARM,
+                   config={"workload": w.name})
+        print(json.dumps(res), flush=True)
+        return
 
     for _ in range(args.warmup):
         sc.forward()
@@ -640,26 +936,18 @@ def run_train(args, w):
     dt = time.perf_counter() - t0
     if co.carryover_read_status(sc.vst) or co.carryover_read_status(sc.st):
         raise RuntimeError("device status")
-    V = w.S * w.anchors
-    vw = w.replace(S=V)
     n = min(args.steps, 100)
     att_s = timed_calls(torch, stream, n, lambda: co.drafter_block_attention(
         sc.vdims, 0, w.L, sc.q, sc.vst, sc.out, sc.lse, co.CO_ATTN_SHARED_PREFIX, sc.ws),
         warm=TRAIN_ATTN_WARM)
-    # the projection of one forward: the committed rows of every response (one
-    # call, every row committed) and the rows of every anchored block (one call,
-    # the rejected rows go to the block's carry segment, the others are skipped)
-    wsp = co.workspace_bytes(sc.vdims, co.CO_WS_PROJECT)
-    pc_s = timed_calls(torch, stream, n, lambda: co.carryover_project_kv(
-        sc.dims, sc.W, sc.h_committed, sc.crt, sc.st, sc.cws))
-    pv_s = timed_calls(torch, stream, n, lambda: co.carryover_project_kv(
-        sc.vdims, sc.W, sc.hidden, sc.vrt, sc.vst, sc.ws, ws_bytes=wsp))
+    pc_s, pv_s, prows, proj = projection_calls(n)
+    proj["counters"] = recorded_mfma(w.name, "projection")
     keys = float(np.sum(sc.vst["ctx_len"].cpu().numpy().astype(np.int64) +
                         sc.vst["carry_len"].cpu().numpy().astype(np.int64)))
     carried = int(sc.vst["carry_len"].sum().item())
     aflops = attention_flops(vw, keys)
-    prows = w.S * w.seq_len + carried
-    pflops, pbytes = projection_work(vw, prows)
+    abytes = train_attention_bytes(w, carried)
+    traffic, traffic_profiled = recorded_traffic(w.name, args.steps, args.warmup, abytes)
     atfl = aflops / att_s / 1e12
     backward = train_backward(torch, co, sc, w, stream, n, args, aflops, prows)
     calibrate_copy(torch, args)
@@ -683,14 +971,15 @@ def run_train(args, w):
         "roofline": {"bound": "mfma", "kernel": "drafter_block_attention, shared prefixes "
                      "(attn_group_kernel)", "achieved": atfl,
                      "peak": MFMA_PEAK_TFLOPS[w.dtype], "unit": "TFLOP/s",
-                     "frac": atfl / MFMA_PEAK_TFLOPS[w.dtype], "traffic": recorded_traffic(w.name),
-                     "algorithmic_flops_per_launch": aflops, "avg_launch_us": att_s * 1e6},
-        "projection": dict(projection_result(vw, pflops, pbytes, pc_s + pv_s, rows=prows),
-                           call="carryover_project_kv x2 (committed rows; anchored blocks' rows)",
-                           committed_call_us=pc_s * 1e6, block_call_us=pv_s * 1e6,
-                           rows_computed=w.S * w.seq_len + V * w.B),
+                     "frac": atfl / MFMA_PEAK_TFLOPS[w.dtype], "traffic": traffic,
+                     "traffic_profiled": traffic_profiled,
+                     "algorithmic_flops_per_launch": aflops,
+                     "algorithmic_bytes_per_launch": abytes, "avg_launch_us": att_s * 1e6},
+        "projection": proj,
         "backward": backward,
     }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_baseline_seconds)
     print(json.dumps(result), flush=True)
 
 
