@@ -232,6 +232,33 @@ co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int3
                                   uint32_t flags, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * drafter_block_attention with two extras computed in the same one-pass merge
+ * (bf16: the keys stream once, every segment shares one online softmax):
+ *   - the block's own rows as a third segment S (the drafter's keys and
+ *     values of its B block positions, attended non-causally next to
+ *     ctx = [C;U] of Eq. 2; "Preliminaries": draft positions attend within
+ *     the block): out and lse are the attention over [C;U;S].  k_self, v_self:
+ *     [layer_count][num_seqs][block][num_kv_heads][head_dim] in the call's
+ *     dtype, 16-byte aligned, keys unrotated (rotated here at ctx_len + j for
+ *     self row j, as the queries are).  Both NULL: no self segment.
+ *   - carry_mass (optional, NULL: none), fp32 [layer_count][num_seqs][block]
+ *     [num_q_heads]: the share of each query's softmax weight over [C;U] that
+ *     falls on U (Appendix "Attention to carried states"; with S present its
+ *     keys are left out of the share); 0 where [C;U] is empty.
+ * Other arguments, workspace and errors as drafter_block_attention; with
+ * neither extra the call is drafter_block_attention.  Supported: block <= 64
+ * (CO_ERR_UNSUPPORTED otherwise).  bf16 computes both extras inside the
+ * persistent attention kernel (CO_ATTN_SHARED_PREFIX is then ignored); fp32
+ * runs the attention, then drafter_carry_mass and drafter_self_merge on its
+ * output, and needs lse (CO_ERR_INVALID_ARG when NULL).
+ */
+co_status drafter_block_attention_ext(const co_dims* dims, int32_t layer_begin,
+                                      int32_t layer_count, const void* q, const void* k_self,
+                                      const void* v_self, const co_state* state, void* out,
+                                      float* lse, float* carry_mass, uint32_t flags, void* ws,
+                                      size_t ws_bytes, hipStream_t stream);
+
+/*
  * One full drafter round (Algorithm 1, Carryover column, or the Baseline
  * column with CO_BASELINE_MODE): route, project all layers, then attend with
  * every layer's queries q [num_layers][num_seqs][block][num_q_heads][head_dim].

@@ -86,6 +86,9 @@ def lib():
             "drafter_block_attention": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, _v,
                                         _P(co_state), _v, _v, ctypes.c_uint32, _v, ctypes.c_size_t,
                                         _v],
+            "drafter_block_attention_ext": [_P(co_dims), ctypes.c_int32, ctypes.c_int32, _v, _v,
+                                            _v, _P(co_state), _v, _v, _v, ctypes.c_uint32, _v,
+                                            ctypes.c_size_t, _v],
             "carryover_round": [_P(co_dims), _P(co_weights), _v, _v, _v, _v, _P(co_state),
                                 _P(co_route), _v, _v, ctypes.c_uint32, _v, ctypes.c_size_t, _v],
             "carryover_fold_e": [_P(co_dims), _P(co_weights), _v, _v],
@@ -122,6 +125,7 @@ def lib():
 
 
 EXPORTED = ("carryover_route", "carryover_project_kv", "drafter_block_attention",
+            "drafter_block_attention_ext",
             "carryover_round", "carryover_fold_e", "drafter_carry_mass", "drafter_self_merge",
             "drafter_block_attention_backward", "carryover_project_kv_backward",
             "carryover_import_kv", "carryover_verify_sample", "carryover_set_tuning",
@@ -236,6 +240,16 @@ def drafter_block_attention(dims, layer_begin, layer_count, q, st, out, lse, fla
     _check(lib().drafter_block_attention(ctypes.byref(dims), layer_begin, layer_count, _ptr(q),
                                          ctypes.byref(s), _ptr(out), _ptr(lse), flags, _ptr(ws),
                                          nb, _stream(stream)), "drafter_block_attention")
+
+
+def drafter_block_attention_ext(dims, layer_begin, layer_count, q, k_self, v_self, st, out, lse,
+                                mass, flags, ws, stream=None, ws_bytes=None):
+    s = state(st)
+    nb = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    _check(lib().drafter_block_attention_ext(ctypes.byref(dims), layer_begin, layer_count, _ptr(q),
+                                             _ptr(k_self), _ptr(v_self), ctypes.byref(s),
+                                             _ptr(out), _ptr(lse), _ptr(mass), flags, _ptr(ws), nb,
+                                             _stream(stream)), "drafter_block_attention_ext")
 
 
 def drafter_block_attention_backward(dims, layer_begin, layer_count, q, st, out, lse, d_out,

@@ -336,7 +336,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnArgs a, int chunk_pag
 
 __device__ __forceinline__ float* slot_ptr(const AttnArgs& a, int hdr_floats, int64_t slot,
                                            int nqp) {
-  return a.ws + hdr_floats + slot * nqp * (a.hd + 2);
+  return a.ws + hdr_floats + slot * nqp * (a.hd + a.rec_sums);
 }
 
 // The part of one segment that lies in one slice (global tile indices).
@@ -354,7 +354,7 @@ __device__ __forceinline__ int pick_reg(const int (&v)[N], int i) {
   return r;
 }
 
-template <int HD, int NT, int NW, int NS, int PQ, int RTM>
+template <int HD, int NT, int NW, int NS, int PQ, int RTM, bool EXT>
 __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int layer_count, int n_wg,
                                                              int hdr_floats, int round_tiles,
                                                              int64_t park_off) {
@@ -372,7 +372,10 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
   constexpr int NL = 4 * LPP;              // direct-to-LDS loads per tile per wave
   constexpr int RING_BYTES = NW * NS * TILE_BYTES;
   constexpr int SLOT_LD = HD + 4;          // 16-byte aligned rows
-  constexpr int SLOT_FLOATS = NQP * SLOT_LD + 2 * NQP;
+  // per query row: m, l (and, with EXT, the sums over carry keys and self keys)
+  constexpr int NSUM = EXT ? 4 : 2;
+  constexpr int RECW = HD + NSUM;          // floats per query row of a record or parked partial
+  constexpr int SLOT_FLOATS = NQP * SLOT_LD + NSUM * NQP;
   constexpr bool PARK_REGS = HD * NT <= 128;   // parked partial fits in 32 registers
   constexpr int RQ = RTM / 32;             // page-descriptor registers (64 pages each)
   constexpr int PMAX = 64;                 // pieces enumerated per pass
@@ -447,6 +450,9 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
   float m_run[NT], l_run[NT];   // l_run: per-lane partial sums (reduce across groups to use)
   f32x4 o_pk[PARK_REGS ? MT : 1][PARK_REGS ? NT : 1];
   float m_pk[NT], l_pk[NT];
+  // EXT: running sums over the carry keys (lu) and the block's own keys (ls),
+  // on the same reference maximum as l_run
+  float lu_run[NT], ls_run[NT], lu_pk[NT], ls_pk[NT];
   u16x8 qf[NT][KS];
   auto reset = [&]() {
 #pragma unroll
@@ -455,6 +461,8 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
       for (int mt = 0; mt < MT; ++mt) o[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
       m_run[nt] = -INFINITY;
       l_run[nt] = 0.f;
+      lu_run[nt] = 0.f;
+      ls_run[nt] = 0.f;
     }
   };
   // queries of round piece slot j into the MFMA B fragments (after DMA has begun)
@@ -470,7 +478,8 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
     }
   };
   // a piece this wavefront merged completely: final output, or a slice record
-  auto emit = [&](bool whole, int s, int seg, const float (&l_tot)[NT]) {
+  auto emit = [&](bool whole, int s, int seg, const float (&l_tot)[NT], const float (&lu_tot)[NT],
+                  const float (&ls_tot)[NT]) {
     const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
     if (whole) {
       uint16_t* out = static_cast<uint16_t*>(a.out);
@@ -489,6 +498,11 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
         }
         if (a.lse && grp == 0)
           a.lse[row] = l_tot[nt] > 0.f ? (m_run[nt] + log2f(l_tot[nt])) * kLn2 : -INFINITY;
+        if constexpr (EXT) {
+          // share of the attention over [C;U] (the self keys left out) on U
+          const float lcu = l_tot[nt] - ls_tot[nt];
+          if (a.mass && grp == 0) a.mass[row] = lcu > 0.f ? lu_tot[nt] / lcu : 0.f;
+        }
       }
     } else {
       float* part = slot_ptr(a, hdr_floats, w + static_cast<int64_t>(seg) * S + s, NQP);
@@ -501,6 +515,10 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
         if (grp == 0) {
           part[NQP * HD + qn] = m_run[nt];
           part[NQP * HD + NQP + qn] = l_tot[nt];
+          if constexpr (EXT) {
+            part[NQP * HD + 2 * NQP + qn] = lu_tot[nt];
+            part[NQP * HD + 3 * NQP + qn] = ls_tot[nt];
+          }
         }
       }
     }
@@ -508,12 +526,16 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
   // fold a parked partial (O[NQP][ld], m[NQP], l[NQP]) into the accumulators
   auto absorb = [&](const float* p, int ld) {
     f32x4 po[MT][NT];
-    float mo[NT], lo[NT];
+    float mo[NT], lo[NT], luo[NT], lso[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {   // one round trip for the whole partial
       const int qn = nt * 16 + col;
       mo[nt] = p[NQP * ld + qn];
       lo[nt] = p[NQP * ld + NQP + qn];
+      if constexpr (EXT) {
+        luo[nt] = p[NQP * ld + 2 * NQP + qn];
+        lso[nt] = p[NQP * ld + 3 * NQP + qn];
+      }
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
         po[mt][nt] = *reinterpret_cast<const f32x4*>(p + qn * ld + mt * 16 + grp * 4);
@@ -526,6 +548,10 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
       const float f1 = (mo[nt] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mo[nt] - M);
       // l_run stays a per-lane partial; the parked row total joins lane group 0
       l_run[nt] = l_run[nt] * f0 + (grp == 0 ? lo[nt] * f1 : 0.f);
+      if constexpr (EXT) {
+        lu_run[nt] = lu_run[nt] * f0 + (grp == 0 ? luo[nt] * f1 : 0.f);
+        ls_run[nt] = ls_run[nt] * f0 + (grp == 0 ? lso[nt] * f1 : 0.f);
+      }
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) o[mt][nt] = o[mt][nt] * f0 + po[mt][nt] * f1;
       m_run[nt] = M;
@@ -551,6 +577,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
         if (i < per && s0 + i < S) {
           const SeqInfo q = seq_info(a, s0 + i, 1);
           nts[i] = (q.npt + 1) / 2;
+          if (EXT && a.k_self && q.ok && nts[i] == 0) nts[i] = 1;   // its self keys follow the tile
           cx[i] = q.ctx;
           cr[i] = q.carry;
           tl += nts[i];
@@ -804,18 +831,12 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
       lds_barrier();                                    // queries staged
       if (ntw > 0) load_q(pj);
 
-      for (int j = 0; j < ntw; ++j) {
-        if (j + NS - 1 < ntw) issue(j + NS - 1);
-        const int t = sb + j;
-        const int nvr = pick_reg(pg_nv, j >> 5);
-        const int n0 = __builtin_amdgcn_readlane(nvr, (2 * j) & 63);
-        const int n1 = __builtin_amdgcn_readlane(nvr, (2 * j + 1) & 63);
+      // One 32-key tile from LDS (its two pages hold n0 and n1 valid keys):
+      // S^T, the online softmax and O^T += V^T P^T.  kind: what this lane's
+      // keys are (0 committed, 1 carry, 2 the block's own rows), for EXT sums.
+      auto consume = [&](const unsigned char* tb, int n0, int n1, int kind) {
         const bool partial = n0 < kPage || n1 < kPage;      // wave-uniform
         const int nv = (grp >> 1) ? n1 : n0;   // valid slots of the page holding my keys
-        wait_stages_ahead<NL, NS>(min(NS - 1, ntw - 1 - j));
-        const unsigned char* tb = my_ring + (j % NS) * TILE_BYTES;
-        if (t == c_beg && !carrying) holding = merger;
-
         u16x8 ka[KS], kb[KS];
         {
           uint32_t aa[KS], ab[KS];
@@ -878,6 +899,10 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
             const float m_new = mx > m_run[nt] + kRescale ? mx : m_run[nt];
             const float alpha = (m_new == m_run[nt]) ? 1.f : exp2f(m_run[nt] - m_new);
             l_run[nt] *= alpha;
+            if constexpr (EXT) {
+              lu_run[nt] *= alpha;
+              ls_run[nt] *= alpha;
+            }
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) o[mt][nt] *= alpha;
             m_run[nt] = m_new;
@@ -889,7 +914,12 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
             pa4[r] = __builtin_amdgcn_exp2f(sa[r] - base);
             pb4[r] = __builtin_amdgcn_exp2f(sb4[r] - base);
           }
-          l_run[nt] += (pa4[0] + pa4[1]) + (pa4[2] + pa4[3]) + (pb4[0] + pb4[1]) + (pb4[2] + pb4[3]);
+          const float psum = (pa4[0] + pa4[1]) + (pa4[2] + pa4[3]) + (pb4[0] + pb4[1]) + (pb4[2] + pb4[3]);
+          l_run[nt] += psum;
+          if constexpr (EXT) {
+            if (kind == 1) lu_run[nt] += psum;
+            if (kind == 2) ls_run[nt] += psum;
+          }
           typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
           const u32x4v pk32 = {pack_bf16x2(pa4[0], pa4[1]), pack_bf16x2(pa4[2], pa4[3]),
                                pack_bf16x2(pb4[0], pb4[1]), pack_bf16x2(pb4[2], pb4[3])};
@@ -898,17 +928,105 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
           for (int mt = 0; mt < MT; ++mt) o[mt][nt] = mfma16x16x32(va[mt], pk, o[mt][nt]);
         }
 
+      };
+      // EXT: this lane's keys in tile jj are carry keys (its page is a carry page)
+      auto kind_of = [&](int jj) {
+        if constexpr (EXT) {
+          const int rv = pick_reg(pg_row, jj >> 5);
+          const int row0 = __builtin_amdgcn_readlane(rv, (2 * jj) & 63);   // lane index uniform
+          const int row1 = __builtin_amdgcn_readlane(rv, (2 * jj + 1) & 63);
+          const int row = (grp >> 1) ? row1 : row0;
+          return (row < 0 && row != INT_MIN) ? 1 : 0;
+        } else {
+          return 0;
+        }
+      };
+      // EXT: the block's own rows of (layer, KV head, sequence) as 32-key tiles,
+      // written into a free ring slot in the layout of a cached tile (keys
+      // rotated at ctx + row, as the queries are) and consumed like one
+      auto self_tiles = [&](int s, int seg, int ctx, unsigned char* slot) {
+        const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
+        const int64_t rs = static_cast<int64_t>(a.Hkv) * HD;    // row stride of k_self / v_self
+        const uint16_t* ks = static_cast<const uint16_t*>(a.k_self) +
+                             ((static_cast<int64_t>(layer_local) * S + s) * a.B * a.Hkv + g) * HD;
+        const uint16_t* vs = static_cast<const uint16_t*>(a.v_self) +
+                             ((static_cast<int64_t>(layer_local) * S + s) * a.B * a.Hkv + g) * HD;
+        for (int t0 = 0; t0 < a.B; t0 += 32) {
+          // keys: lane jobs (row, rotation pair of 16-byte chunks c and c + CPR/2)
+#pragma unroll
+          for (int i = 0; i < (32 * CPR / 2) / 64; ++i) {
+            const int jb = lane + 64 * i, r = jb / (CPR / 2), c = jb % (CPR / 2);
+            const int row = t0 + r;
+            u16x8 lo = {0, 0, 0, 0, 0, 0, 0, 0}, hi = lo;
+            if (row < a.B) {
+              lo = *reinterpret_cast<const u16x8*>(ks + row * rs + c * 8);
+              hi = *reinterpret_cast<const u16x8*>(ks + row * rs + c * 8 + HD / 2);
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                float cs, sn;
+                rope_cos_sin_rev(ctx + row, inv_lds[c * 8 + e], &cs, &sn);
+                const float x = bf2f(lo[e]), y = bf2f(hi[e]);
+                lo[e] = f2bf(x * cs - y * sn);
+                hi[e] = f2bf(y * cs + x * sn);
+              }
+            }
+            const int rp = r & 15;
+            unsigned char* kpg = slot + (r >> 4) * PAGE_BYTES + rp * ROWB;
+            *reinterpret_cast<u16x8*>(kpg + ((c ^ (rp & (CPR - 1))) << 4)) = lo;
+            *reinterpret_cast<u16x8*>(kpg + (((c + CPR / 2) ^ (rp & (CPR - 1))) << 4)) = hi;
+          }
+          // values: lane jobs (row, 16-byte chunk), scattered into the [dim][key] pages
+#pragma unroll
+          for (int i = 0; i < (32 * CPR) / 64; ++i) {
+            const int jb = lane + 64 * i, r = jb / CPR, c = jb % CPR;
+            const int row = t0 + r;
+            u16x8 v8 = {0, 0, 0, 0, 0, 0, 0, 0};
+            if (row < a.B) v8 = *reinterpret_cast<const u16x8*>(vs + row * rs + c * 8);
+            uint16_t* vpg = reinterpret_cast<uint16_t*>(slot + (2 + (r >> 4)) * PAGE_BYTES);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) vpg[(c * 8 + e) * kPage + (r & 15)] = v8[e];
+          }
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wavefront's own writes
+          const int nb = a.B - t0;
+          consume(slot, min(nb, kPage), max(0, min(nb - kPage, kPage)), 2);
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // read before the next rows land
+        }
+      };
+
+      for (int j = 0; j < ntw; ++j) {
+        if (j + NS - 1 < ntw) issue(j + NS - 1);
+        const int t = sb + j;
+        const int nvr = pick_reg(pg_nv, j >> 5);
+        const int n0 = __builtin_amdgcn_readlane(nvr, (2 * j) & 63);
+        const int n1 = __builtin_amdgcn_readlane(nvr, (2 * j + 1) & 63);
+        wait_stages_ahead<NL, NS>(min(NS - 1, ntw - 1 - j));
+        const unsigned char* tb = my_ring + (j % NS) * TILE_BYTES;
+        if (t == c_beg && !carrying) holding = merger;
+
+        consume(tb, n0, n1, kind_of(j));
+        if constexpr (EXT) {
+          // the segment's last tile: its self keys follow, in the slot just read
+          if (a.k_self && t + 1 == __builtin_amdgcn_readlane(f_send, pj))
+            self_tiles(__builtin_amdgcn_readlane(f_s, pj), __builtin_amdgcn_readlane(f_seg, pj),
+                       pc[pa + pj].ctx, my_ring + (j % NS) * TILE_BYTES);
+        }
         // ---- the end of a piece, or of the sub-slice inside a piece
         if (t + 1 == c_end || j + 1 == ntw) {
-          float l_tot[NT];
+          float l_tot[NT], lu_tot[NT], ls_tot[NT];
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt) l_tot[nt] = wave_sum_across_groups(l_run[nt]);
+          for (int nt = 0; nt < NT; ++nt) {
+            l_tot[nt] = wave_sum_across_groups(l_run[nt]);
+            if constexpr (EXT) {
+              lu_tot[nt] = wave_sum_across_groups(lu_run[nt]);
+              ls_tot[nt] = wave_sum_across_groups(ls_run[nt]);
+            }
+          }
           const bool ends = t + 1 == c_end;
           if (merger && ends) {
             const int sbeg = __builtin_amdgcn_readlane(f_sbeg, pj);
             const int send = __builtin_amdgcn_readlane(f_send, pj);
             emit(c_beg == sbeg && c_end == send, __builtin_amdgcn_readlane(f_s, pj),
-                 __builtin_amdgcn_readlane(f_seg, pj), l_tot);
+                 __builtin_amdgcn_readlane(f_seg, pj), l_tot, lu_tot, ls_tot);
             holding = false;
           } else if (!merger) {
             // the first piece of a sub-slice that began inside it: merged by the
@@ -921,9 +1039,13 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
                 for (int mt = 0; mt < MT; ++mt) o_pk[mt][nt] = o[mt][nt];
                 m_pk[nt] = m_run[nt];
                 l_pk[nt] = l_tot[nt];
+                if constexpr (EXT) {
+                  lu_pk[nt] = lu_tot[nt];
+                  ls_pk[nt] = ls_tot[nt];
+                }
               }
             } else {
-              float* pp = a.ws + park_off + (static_cast<int64_t>(w) * NW + wave) * NQP * (HD + 2);
+              float* pp = a.ws + park_off + (static_cast<int64_t>(w) * NW + wave) * NQP * RECW;
 #pragma unroll
               for (int nt = 0; nt < NT; ++nt) {
                 const int qn = nt * 16 + col;
@@ -933,13 +1055,23 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
                 if (grp == 0) {
                   pp[NQP * HD + qn] = m_run[nt];
                   pp[NQP * HD + NQP + qn] = l_tot[nt];
+                  if constexpr (EXT) {
+                    pp[NQP * HD + 2 * NQP + qn] = lu_tot[nt];
+                    pp[NQP * HD + 3 * NQP + qn] = ls_tot[nt];
+                  }
                 }
               }
             }
           } else {
             // merger whose piece goes on past the sub-slice: merged at the round's end
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) l_run[nt] = grp == 0 ? l_tot[nt] : 0.f;
+            for (int nt = 0; nt < NT; ++nt) {
+              l_run[nt] = grp == 0 ? l_tot[nt] : 0.f;
+              if constexpr (EXT) {
+                lu_run[nt] = grp == 0 ? lu_tot[nt] : 0.f;
+                ls_run[nt] = grp == 0 ? ls_tot[nt] : 0.f;
+              }
+            }
           }
           if (ends && j + 1 < ntw) {   // the next piece begins inside this sub-slice
             ++pj;
@@ -967,6 +1099,10 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
             if (grp == 0) {
               sp[NQP * SLOT_LD + qn] = m_pk[nt];
               sp[NQP * SLOT_LD + NQP + qn] = l_pk[nt];
+              if constexpr (EXT) {
+                sp[NQP * SLOT_LD + 2 * NQP + qn] = lu_pk[nt];
+                sp[NQP * SLOT_LD + 3 * NQP + qn] = ls_pk[nt];
+              }
             }
           }
         }
@@ -982,18 +1118,24 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
           if constexpr (PARK_REGS)
             absorb(reinterpret_cast<const float*>(smem) + v2 * SLOT_FLOATS, SLOT_LD);
           else
-            absorb(a.ws + park_off + (static_cast<int64_t>(w) * NW + v2) * NQP * (HD + 2), HD);
+            absorb(a.ws + park_off + (static_cast<int64_t>(w) * NW + v2) * NQP * RECW, HD);
         }
         if (c_end > rb) {
           if (lane == 0) next_rot = wave;               // goes on in the next round
         } else {
-          float l_tot[NT];
+          float l_tot[NT], lu_tot[NT], ls_tot[NT];
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt) l_tot[nt] = wave_sum_across_groups(l_run[nt]);
+          for (int nt = 0; nt < NT; ++nt) {
+            l_tot[nt] = wave_sum_across_groups(l_run[nt]);
+            if constexpr (EXT) {
+              lu_tot[nt] = wave_sum_across_groups(lu_run[nt]);
+              ls_tot[nt] = wave_sum_across_groups(ls_run[nt]);
+            }
+          }
           const int sbeg = __builtin_amdgcn_readlane(f_sbeg, pj);
           const int send = __builtin_amdgcn_readlane(f_send, pj);
           emit(c_beg == sbeg && c_end == send, __builtin_amdgcn_readlane(f_s, pj),
-               __builtin_amdgcn_readlane(f_seg, pj), l_tot);
+               __builtin_amdgcn_readlane(f_seg, pj), l_tot, lu_tot, ls_tot);
           holding = false;
         }
       }
@@ -1039,6 +1181,8 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
       out[out_row(a, layer_local, s, g, idx / hd, G) * hd + idx % hd] = 0;
     if (a.lse && blockIdx.z == 0)
       for (int qn = tid; qn < nq; qn += 256) a.lse[out_row(a, layer_local, s, g, qn, G)] = -INFINITY;
+    if (a.mass && blockIdx.z == 0)
+      for (int qn = tid; qn < nq; qn += 256) a.mass[out_row(a, layer_local, s, g, qn, G)] = 0.f;
     return;
   }
   const int A = seg * T1 + ts;
@@ -1054,25 +1198,28 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
   // with at least as many tiles as slices no slice is empty, so every slot in
   // [w_lo, w_hi] holds a record; otherwise an empty slice left none
   const bool all_full = T >= n_wg;
-  const int64_t rec = static_cast<int64_t>(nq_pad) * (hd + 2);
+  const int64_t rec = static_cast<int64_t>(nq_pad) * (hd + a.rec_sums);
+  const bool sums = a.rec_sums > 2;    // carry and self sums follow m and l
   // records of consecutive slices of one segment are consecutive slots
   const float* base = slot_ptr(a, hdr_floats, w_lo + static_cast<int64_t>(seg) * a.S + s, nq_pad);
   for (int idx = tid + blockIdx.z * 256; idx < nq * qd; idx += 256 * gridDim.z) {
     const int qn = idx / qd, d = (idx % qd) * DIMS;
     const float* pm = base + nq_pad * hd + qn;
     const float* po = base + qn * hd + d;
-    float M = -INFINITY, den = 0.f;
+    float M = -INFINITY, den = 0.f, den_u = 0.f, den_s = 0.f;
     f32x4 acc[kV];
 #pragma unroll
     for (int j = 0; j < kV; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int r0 = 0; r0 < nrec; r0 += kBatch) {   // usually one batch: one round trip
-      float mv[kBatch], lv[kBatch];
+      float mv[kBatch], lv[kBatch], luv[kBatch], lsv[kBatch];
       f32x4 ov[kBatch][kV];
 #pragma unroll
       for (int i = 0; i < kBatch; ++i) {
         const bool in = r0 + i < nrec;
         mv[i] = in ? pm[(r0 + i) * rec] : -INFINITY;
         lv[i] = in ? pm[(r0 + i) * rec + nq_pad] : 0.f;
+        luv[i] = (in && sums) ? pm[(r0 + i) * rec + 2 * nq_pad] : 0.f;
+        lsv[i] = (in && sums) ? pm[(r0 + i) * rec + 3 * nq_pad] : 0.f;
 #pragma unroll
         for (int j = 0; j < kV; ++j)
           ov[i][j] = in ? *reinterpret_cast<const f32x4*>(po + (r0 + i) * rec + 4 * j)
@@ -1087,12 +1234,16 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
       }
       const float f = (M == -INFINITY) ? 0.f : exp2f(M - Mb);
       den *= f;
+      den_u *= f;
+      den_s *= f;
 #pragma unroll
       for (int j = 0; j < kV; ++j) acc[j] *= f;
 #pragma unroll
       for (int i = 0; i < kBatch; ++i) {
         const float wgt = (mv[i] == -INFINITY) ? 0.f : exp2f(mv[i] - Mb);
         den += wgt * lv[i];
+        den_u += wgt * luv[i];
+        den_s += wgt * lsv[i];
 #pragma unroll
         for (int j = 0; j < kV; ++j) acc[j] += wgt * ov[i][j];
       }
@@ -1108,6 +1259,10 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
       *reinterpret_cast<u16x4*>(out + row * hd + d + 4 * j) = v;
     }
     if (a.lse && d == 0) a.lse[row] = den > 0.f ? (M + log2f(den)) * kLn2 : -INFINITY;
+    if (a.mass && d == 0) {   // share of the attention over [C;U] (self keys left out) on U
+      const float lcu = den - den_s;
+      a.mass[row] = lcu > 0.f ? den_u / lcu : 0.f;
+    }
   }
 }
 
@@ -1936,11 +2091,13 @@ AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pa
     const int64_t rt_override = tuning(CO_TUNE_ATTN_ROUND_TILES);
     if (rt_override >= 1 && rt_override <= rtm) p.round_tiles = static_cast<int>(rt_override);
     p.hdr_floats = (S + 1 + p.n_wg + 1 + 63) / 64 * 64;
-    const size_t rec = static_cast<size_t>(p.nq_pad) * (hd + 2);
+    const size_t rec = static_cast<size_t>(p.nq_pad) * (hd + 4);   // room for the extras' sums
     const size_t records = (static_cast<size_t>(p.n_wg) + static_cast<size_t>(L) * Hkv * S) * rec;
     const size_t park =
         hd * (p.nq_pad / 16) > 128 ? static_cast<size_t>(p.n_wg) * nw * rec : 0;
     p.park_off = static_cast<int64_t>(p.hdr_floats + records);
+    p.n_wg_persist = p.n_wg;
+    p.hdr_persist = p.hdr_floats;
     p.bytes = (p.hdr_floats + records + park) * 4;
     // global tile indices, committed and carry K/V row indices are int32
     const int64_t tiles = static_cast<int64_t>(L) * Hkv * S * ((max_lp + 1) / 2);
@@ -2009,18 +2166,23 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
   const dim3 mgrid(a.S, layer_count * a.Hkv, (items + 255) / 256);
   const int items_f32 = (a.B * (a.Hq / a.Hkv)) * (a.hd / 4);
   const dim3 fgrid(a.S, layer_count * a.Hkv, (items_f32 + 255) / 256);
+  // the extras (self segment, carry mass) run on the persistent kernel
+  const bool ext = a.k_self != nullptr || a.mass != nullptr;
+  const int n_wg = ext ? p.n_wg_persist : p.n_wg;
+  const int hdr_floats = ext ? p.hdr_persist : p.hdr_floats;
   auto combine = [&]() {
     if (wide)
       hipLaunchKernelGGL(attn_bf16_combine_kernel<16>, mgrid, dim3(256), 0, stream, a, layer_count,
-                         p.n_wg, p.hdr_floats, p.nq_pad);
+                         n_wg, hdr_floats, p.nq_pad);
     else
       hipLaunchKernelGGL(attn_bf16_combine_kernel<4>, mgrid, dim3(256), 0, stream, a, layer_count,
-                         p.n_wg, p.hdr_floats, p.nq_pad);
+                         n_wg, hdr_floats, p.nq_pad);
   };
   // grouped kernel: any query count with head_dim 64, up to 32 rows with 128
   const int nq = a.B * (a.Hq / a.Hkv);
   const bool one = nq <= 32;
-  if (a.dtype == CO_DTYPE_BF16 && (a.flags & CO_ATTN_SHARED_PREFIX) && (a.hd == 64 || one)) {
+  if (a.dtype == CO_DTYPE_BF16 && !ext && (a.flags & CO_ATTN_SHARED_PREFIX) &&
+      (a.hd == 64 || one)) {
     const int ns = group_splits(a.max_pages);
     const dim3 ggrid((a.S + kGroupSeqs - 1) / kGroupSeqs * ns, a.Hkv, layer_count);
     const int sp = group_split_tiles();
@@ -2040,7 +2202,7 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
       hipLaunchKernelGGL(attn_share_merge_kernel<128>, cgrid, dim3(256), 0, stream, a, sp, ns, nqp, kGroupSeqs);
     return hipGetLastError();
   }
-  if (a.dtype == CO_DTYPE_BF16 && p.wave) {
+  if (a.dtype == CO_DTYPE_BF16 && !ext && p.wave) {
     const int nw = wave_waves(a.hd);
     const dim3 wgrid(p.n_wg / nw), wblock(64 * nw);
     if (a.hd == 128)
@@ -2058,10 +2220,19 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
     return hipGetLastError();
   }
   if (a.dtype == CO_DTYPE_BF16) {
-    const dim3 grid(p.n_wg);
-#define CO_ATTN_LAUNCH(HD, NT, NW, NS, PQ, RTM)                                                 \
-  hipLaunchKernelGGL((attn_bf16_kernel<HD, NT, NW, NS, PQ, RTM>), grid, dim3(64 * NW), 0, stream, \
-                     a, layer_count, p.n_wg, p.hdr_floats, p.round_tiles, p.park_off)
+    const dim3 grid(n_wg);
+// the extras run with half the wavefronts per workgroup and a deeper ring, so
+// that their sums and the self rows fit in the registers (one wavefront per SIMD)
+#define CO_ATTN_LAUNCH(HD, NT, NW, NS, PQ, RTM)                                                   \
+  do {                                                                                            \
+    if (ext)                                                                                      \
+      hipLaunchKernelGGL((attn_bf16_kernel<HD, NT, NW / 2, NS * 2, PQ, RTM, true>), grid,         \
+                         dim3(32 * NW), 0, stream, a, layer_count, n_wg, hdr_floats,              \
+                         p.round_tiles, p.park_off);                                              \
+    else                                                                                          \
+      hipLaunchKernelGGL((attn_bf16_kernel<HD, NT, NW, NS, PQ, RTM, false>), grid, dim3(64 * NW), \
+                         0, stream, a, layer_count, n_wg, hdr_floats, p.round_tiles, p.park_off);  \
+  } while (0)
     if (a.hd == 64) {
       switch (nt) {
         case 1: CO_ATTN_LAUNCH(64, 1, kAttnWaves64, 2, 4, kAttnRoundTiles64); break;

@@ -225,8 +225,13 @@ co_status enqueue_project(const co_dims* dims, const co_weights* w, const void* 
 
 co_status do_attention(const co_dims* d, int32_t layer_begin, int32_t layer_count, const void* q,
                        const co_state* st, void* out, float* lse, uint32_t flags, void* ws,
-                       hipStream_t stream) {
+                       hipStream_t stream, const void* k_self = nullptr,
+                       const void* v_self = nullptr, float* mass = nullptr) {
   AttnArgs a{};
+  a.rec_sums = (k_self || mass) ? 4 : 2;
+  a.k_self = k_self;
+  a.v_self = v_self;
+  a.mass = mass;
   a.S = d->num_seqs;
   a.B = d->block;
   a.L = d->num_layers;
@@ -318,6 +323,42 @@ co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int3
                               ws_bytes)) != CO_OK)
     return s;
   return do_attention(dims, layer_begin, layer_count, q, state, out, lse, flags, ws, stream);
+}
+
+co_status drafter_block_attention_ext(const co_dims* dims, int32_t layer_begin,
+                                      int32_t layer_count, const void* q, const void* k_self,
+                                      const void* v_self, const co_state* state, void* out,
+                                      float* lse, float* carry_mass, uint32_t flags, void* ws,
+                                      size_t ws_bytes, hipStream_t stream) {
+  co_status s = check_dims(dims);
+  if (s != CO_OK) return s;
+  if ((s = validate_attention(dims, layer_begin, layer_count, q, state, out, lse, ws,
+                              ws_bytes)) != CO_OK)
+    return s;
+  if ((k_self == nullptr) != (v_self == nullptr)) return CO_ERR_INVALID_ARG;
+  if ((k_self && (!aligned(k_self, 16) || !aligned(v_self, 16))) ||
+      (carry_mass && !aligned(carry_mass, 4)))
+    return CO_ERR_INVALID_ARG;
+  if (!k_self && !carry_mass)
+    return do_attention(dims, layer_begin, layer_count, q, state, out, lse, flags, ws, stream);
+  if (dims->block > kMaxCarryRows) return CO_ERR_UNSUPPORTED;
+  if (dims->dtype == CO_DTYPE_BF16)
+    return do_attention(dims, layer_begin, layer_count, q, state, out, lse, flags, ws, stream,
+                        k_self, v_self, carry_mass);
+  // fp32: the attention, then the mass from its LSE over [C;U], then the self
+  // segment merged into O and LSE
+  if (!lse) return CO_ERR_INVALID_ARG;
+  if ((s = do_attention(dims, layer_begin, layer_count, q, state, out, lse, flags, ws,
+                        stream)) != CO_OK)
+    return s;
+  if (carry_mass &&
+      (s = drafter_carry_mass(dims, layer_begin, layer_count, q, state, lse, carry_mass,
+                              flags & CO_Q_PREROTATED, stream)) != CO_OK)
+    return s;
+  if (k_self)
+    return drafter_self_merge(dims, layer_begin, layer_count, q, k_self, v_self, state, out, lse,
+                              flags & CO_Q_PREROTATED, stream);
+  return CO_OK;
 }
 
 co_status drafter_block_attention_backward(

@@ -77,6 +77,13 @@ struct AttnArgs {
   float* lse;
   int32_t* status;
   float* ws;        // partial records of multi-chunk sequences
+  // bf16 slice records: floats per query row after the hd output dims (m, l;
+  // and with the extras below, the carry and self sums)
+  int rec_sums;
+  // extras of drafter_block_attention_ext (bf16 persistent kernel), or null:
+  const void* k_self;   // the block's own keys [layers][S][B][Hkv][hd], unrotated
+  const void* v_self;   // and values
+  float* mass;          // share of the attention over [C;U] on U, [layers][S][B][Hq]
 };
 
 constexpr int kMaxAttnSeqs = 2048;   // sequences one bf16 attention launch can cover
@@ -87,6 +94,7 @@ struct AttnPlan {
   int round_tiles;             // bf16 persistent path: tiles per wavefront per round
   int64_t park_off;            // bf16 persistent path: parked partials (workspace floats)
   bool wave;                   // bf16: per-wavefront slices (n_wg = slices, not workgroups)
+  int n_wg_persist, hdr_persist;   // bf16 persistent path's n_wg, hdr_floats (the extras use it)
   int nq_pad;
   bool ok;                     // false: shapes beyond what one launch can cover
   size_t bytes;

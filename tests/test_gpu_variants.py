@@ -243,3 +243,108 @@ def test_self_merge(w):
             assert_heads_close(g[:, s], O[:, s], tol, f"{w.name} r{r} O seq {s}")
             err = np.abs(gl[:, s] - LSE[:, s]).max()
             assert err <= tol, f"{w.name} r{r} LSE seq {s}: {err}"
+
+
+# ------------------------------------------------ extras inside the one-pass merge
+
+B8 = EDGE.replace(name="ext_b8", B=8, seed=0x5EED25)
+B48 = wl.Workload("ext_b48", S=3, B=48, Dcat=256, d=128, L=1, Hq=2, Hkv=2, hd=64, dtype="bf16",
+                  theta=1e4, ctx_lo=30, ctx_hi=900, ctx_mode="direct", accept=("geom", 0.1),
+                  rounds=4, seed=0x5EED26)
+EXTRAS = ["self", "mass", "both"]
+
+
+def _ext_round(co, sc, orc, w, r, m, extra, tag, empty=(), no_committed=()):
+    """One round, then drafter_block_attention_ext on the state it left with
+    the round's queries; compared with the oracle's attention over [C;U;S]
+    (or [C;U]) and its carried mass over [C;U].  Before the call, sequences in
+    ``empty`` lose their committed and carry keys, those in ``no_committed``
+    their committed keys."""
+    hidden, q, draft, target, m = sc.round_inputs(r, m)
+    out, lse = sc.new_output()
+    co.carryover_round(sc.dims, sc.W, hidden, draft, target, q, sc.st, sc.rt, out, lse, 0, sc.ws)
+    orc.round(r, m=m, attend=False)
+    for s in set(empty) | set(no_committed):
+        sc.st["ctx_len"][s] = 0
+        orc._ctx[s] = 0
+        for st_ in (orc.st.ck, orc.st.cv):
+            st_[s] = st_[s][:, :0]
+    for s in empty:
+        sc.st["carry_len"][s] = 0
+        orc._carry[s] = 0
+        for st_ in (orc.st.uk, orc.st.uv):
+            st_[s] = st_[s][:, :0]
+    with_self = extra in ("self", "both")
+    with_mass = extra in ("mass", "both")
+    ks, vs = sc.self_kv(r) if with_self else (None, None)
+    out2 = torch.full_like(out, float("nan"))
+    lse2 = torch.full_like(lse, float("nan"))
+    mass = torch.full_like(lse, float("nan")) if with_mass else None
+    co.drafter_block_attention_ext(sc.dims, 0, w.L, q, ks, vs, sc.st, out2, lse2, mass, 0, sc.ws)
+    torch.cuda.synchronize()
+    assert co.carryover_read_status(sc.st) == 0
+    Q = orc.seq_block(wl.spec_q(w, r), 1)
+    if with_self:
+        Ks = host(w, wl.spec_self(w, "k", r))
+        Vs = host(w, wl.spec_self(w, "v", r))
+        O, LSE = oracle.attend_state_with_self(orc.st, Q, Ks, Vs, w.Hq, w.theta, seqs=orc.seqs)
+    else:
+        O, LSE = oracle.attend_state(orc.st, Q, w.Hq, w.theta, seqs=orc.seqs)
+    tol = TOL[w.dtype]
+    g = to_np(out2)
+    gl = lse2.cpu().numpy().astype(np.float64)
+    for s in orc.seqs:
+        assert_heads_close(g[:, s], O[:, s], tol, f"{tag} O seq {s}")
+        err = np.abs(gl[:, s] - LSE[:, s])
+        assert np.all(np.isfinite(err) | (np.isinf(gl[:, s]) & np.isinf(LSE[:, s]))), \
+            f"{tag} LSE seq {s}"
+        assert np.nanmax(np.where(np.isinf(LSE[:, s]), 0.0, err)) <= tol, f"{tag} LSE seq {s}"
+    if with_mass:
+        ref = oracle.carry_mass_state(orc.st, Q, w.Hq, w.theta, seqs=orc.seqs)
+        got = mass.cpu().numpy().astype(np.float64)
+        for s in orc.seqs:
+            err = np.abs(got[:, s] - ref[:, s]).max()
+            assert err <= tol, f"{tag} mass seq {s}: {err}"
+            if orc.st.uk[s].shape[1] == 0:     # nothing carried: exactly zero
+                assert np.all(got[:, s] == 0.0), f"{tag} mass seq {s} not zero"
+    return m
+
+
+@pytest.mark.parametrize("extra", EXTRAS)
+@pytest.mark.parametrize("w", [EDGE, EDGE_F32, HD128, B8, B48], ids=lambda w: w.name)
+def test_attention_ext(w, extra):
+    """The block's own rows and the carried mass inside the one-pass merge
+    (bf16) or through the post-pass kernels (fp32): full and zero acceptance,
+    a mix, head_dim 64 and 128, blocks of 8, 16 and 48 rows (two self tiles)."""
+    Scenario, co = _gpu()
+    print(f"[variants] ext {extra} {w.name}", flush=True)
+    sc, orc = Scenario(w), OracleRun(w)
+    B, S = w.B, w.S
+    for r, m in enumerate([None, [B] * S, [0] * S, None]):
+        _ext_round(co, sc, orc, w, r, m, extra, f"{w.name} {extra} r{r}")
+
+
+@pytest.mark.parametrize("wgs", ["1", "3", "70", "500"], ids=lambda v: f"wg{v}")
+def test_attention_ext_slicings(wgs, tune):
+    """Forced slicings of the persistent kernel with both extras: segments
+    split across workgroups and wavefronts, self keys processed by whichever
+    wavefront holds a segment's last tile."""
+    Scenario, co = _gpu()
+    tune("attn_workgroups", wgs)
+    w = EDGE
+    print(f"[variants] ext slicing wg={wgs}", flush=True)
+    sc, orc = Scenario(w), OracleRun(w)
+    for r in range(3):
+        _ext_round(co, sc, orc, w, r, None, "both", f"wg{wgs} r{r}")
+
+
+def test_attention_ext_empty_context():
+    """A sequence with no committed and no carry keys attends to its self keys
+    alone (mass 0); another has carry keys only (mass 1 without self keys)."""
+    Scenario, co = _gpu()
+    w = EDGE
+    sc, orc = Scenario(w), OracleRun(w)
+    _ext_round(co, sc, orc, w, 0, [0, 3, w.B, 5], "both", "empty ctx", empty=(0,),
+               no_committed=(1,))
+    sc2, orc2 = Scenario(w), OracleRun(w)
+    _ext_round(co, sc2, orc2, w, 0, [0, 3, w.B, 5], "mass", "carry only", no_committed=(1,))
