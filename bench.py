@@ -779,8 +779,20 @@ def variant_costs(torch, co, sc, w, lib, step, rewind, chain, args, stream, atte
     out = torch.zeros((w.L, w.S, w.B, w.Hq, w.hd), dtype=sc.tdtype, device="cuda")
     self_s = timed_calls(torch, stream, n, lambda: co.drafter_self_merge(
         sc.dims, 0, w.L, q_last, ks, vs, sc.st, out, lse))
+    # the same extras inside the one-pass merge: whole attention calls, next
+    # to the plain call on the same state
+    plain_s = timed_calls(torch, stream, n, lambda: co.drafter_block_attention(
+        sc.dims, 0, w.L, q_last, sc.st, out, lse, 0, sc.ws))
+    ext = {}
+    for name, kv, ms in (("self", (ks, vs), None), ("mass", (None, None), mass),
+                         ("self_and_mass", (ks, vs), mass)):
+        ext[name + "_call_us"] = 1e6 * timed_calls(
+            torch, stream, n, lambda kv=kv, ms=ms: co.drafter_block_attention_ext(
+                sc.dims, 0, w.L, q_last, kv[0], kv[1], sc.st, out, lse, ms, 0, sc.ws))
+    ext["plain_call_us"] = plain_s * 1e6
     return {"carry_mass_call_us": mass_s * 1e6,
             "self_merge_call_us": self_s * 1e6,
+            "attention_ext": ext,
             "separate_projector": {"rounds_per_s": args.steps / dt_sep,
                                    "vs_embedding": dt / dt_sep},
             "z_norm": {"rounds_per_s": args.steps / dt_norm, "vs_plain": dt / dt_norm},

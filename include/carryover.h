@@ -133,7 +133,8 @@ typedef struct co_weights {
                                  every row of z = F x is divided by its root mean square
                                  (epsilon 1e-6) and multiplied by z_norm before the K/V
                                  projections (normalisation variant; the equations omit
-                                 normalisation, Section 2.1)                          */
+                                 normalisation, Section 2.1); model_dim <= 16384
+                                 (CO_ERR_UNSUPPORTED otherwise)                       */
   const float* k_norm;        /* optional per-head key RMS-norm gain, fp32
                                  [num_layers][head_dim]: when non-NULL every key head of
                                  layer l is divided by its root mean square over head_dim
@@ -248,7 +249,7 @@ co_status drafter_block_attention(const co_dims* dims, int32_t layer_begin, int3
  * Other arguments, workspace and errors as drafter_block_attention; with
  * neither extra the call is drafter_block_attention.  Supported: block <= 64
  * (CO_ERR_UNSUPPORTED otherwise).  bf16 computes both extras inside the
- * persistent attention kernel (CO_ATTN_SHARED_PREFIX is then ignored); fp32
+ * serving attention kernels (CO_ATTN_SHARED_PREFIX is then ignored); fp32
  * runs the attention, then drafter_carry_mass and drafter_self_merge on its
  * output, and needs lse (CO_ERR_INVALID_ARG when NULL).
  */

@@ -339,6 +339,128 @@ __device__ __forceinline__ float* slot_ptr(const AttnArgs& a, int hdr_floats, in
   return a.ws + hdr_floats + slot * nqp * (a.hd + a.rec_sums);
 }
 
+// The block's own rows (drafter_block_attention_ext) as 32-key tiles of a
+// (layer, KV head, sequence): rows t0 .. t0 + 31 of k_self / v_self
+// [layers][S][B][Hkv][HD] are loaded by the wavefront as lane jobs (keys: a row
+// and the rotation pair of 16-byte chunks c, c + CPR/2; values: a row and a
+// chunk), then written into a ring slot in the layout of a cached tile: keys
+// rotated at ctx + row (as the queries are) with the slot's XOR swizzle,
+// values transposed into the [HD][16] pages.  Rows past B are zero.
+template <int HD>
+struct SelfRows {
+  static constexpr int ROWB = HD * 2, CPR = ROWB / 16, PAGE_BYTES = kPage * ROWB;
+  static constexpr int KJ = (32 * CPR / 2) / 64, VJ = (32 * CPR) / 64;   // lane jobs
+  u16x8 lo[KJ], hi[KJ], v8[VJ];
+
+  __device__ void load(const AttnArgs& a, int s, int layer_local, int g, int t0, int lane) {
+    const int64_t rs = static_cast<int64_t>(a.Hkv) * HD;   // row stride
+    const int64_t base = ((static_cast<int64_t>(layer_local) * a.S + s) * a.B * a.Hkv + g) * HD;
+    const uint16_t* ks = static_cast<const uint16_t*>(a.k_self) + base;
+    const uint16_t* vs = static_cast<const uint16_t*>(a.v_self) + base;
+#pragma unroll
+    for (int i = 0; i < KJ; ++i) {
+      const int jb = lane + 64 * i, row = t0 + jb / (CPR / 2), c = jb % (CPR / 2);
+      lo[i] = hi[i] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+      if (row < a.B) {
+        lo[i] = *reinterpret_cast<const u16x8*>(ks + row * rs + c * 8);
+        hi[i] = *reinterpret_cast<const u16x8*>(ks + row * rs + c * 8 + HD / 2);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VJ; ++i) {
+      const int jb = lane + 64 * i, row = t0 + jb / CPR, c = jb % CPR;
+      v8[i] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+      if (row < a.B) v8[i] = *reinterpret_cast<const u16x8*>(vs + row * rs + c * 8);
+    }
+  }
+
+  // inv_rev: RoPE inverse frequencies in revolutions per position
+  __device__ void store(unsigned char* slot, int t0, int ctx, int lane, const double* inv_rev) {
+#pragma unroll
+    for (int i = 0; i < KJ; ++i) {
+      const int jb = lane + 64 * i, r = jb / (CPR / 2), c = jb % (CPR / 2);
+      u16x8 x8 = lo[i], y8 = hi[i];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float cs, sn;
+        rope_cos_sin_rev(ctx + t0 + r, inv_rev[c * 8 + e], &cs, &sn);
+        const float x = bf2f(x8[e]), y = bf2f(y8[e]);
+        x8[e] = f2bf(x * cs - y * sn);
+        y8[e] = f2bf(y * cs + x * sn);
+      }
+      const int rp = r & 15;
+      unsigned char* kpg = slot + (r >> 4) * PAGE_BYTES + rp * ROWB;
+      *reinterpret_cast<u16x8*>(kpg + ((c ^ (rp & (CPR - 1))) << 4)) = x8;
+      *reinterpret_cast<u16x8*>(kpg + (((c + CPR / 2) ^ (rp & (CPR - 1))) << 4)) = y8;
+    }
+#pragma unroll
+    for (int i = 0; i < VJ; ++i) {
+      const int jb = lane + 64 * i, r = jb / CPR, c = jb % CPR;
+      uint16_t* vpg = reinterpret_cast<uint16_t*>(slot + (2 + (r >> 4)) * PAGE_BYTES);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) vpg[(c * 8 + e) * kPage + (r & 15)] = v8[i][e];
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wavefront's own writes
+  }
+};
+
+// The same rows staged through LDS instead of registers (for kernels with no
+// registers to spare): raw rows land by direct-to-LDS loads in a free ring slot
+// (keys [32][HD], then values [32][HD]; rows past B repeat row B - 1, their
+// keys are masked by the caller), then are placed job by job into the slot of
+// the tile layout.  The caller waits for the loads (vmcnt) between the two.
+template <int HD>
+__device__ void self_rows_raw(const AttnArgs& a, int s, int layer_local, int g, int t0, int lane,
+                              uint32_t raw) {
+  constexpr int ROWB = HD * 2, LOADS = 32 * ROWB / 1024;   // 1 KiB wavefront loads per half
+  const int64_t rs = static_cast<int64_t>(a.Hkv) * HD;
+  const int64_t base = ((static_cast<int64_t>(layer_local) * a.S + s) * a.B * a.Hkv + g) * HD;
+  const uint16_t* ks = static_cast<const uint16_t*>(a.k_self) + base;
+  const uint16_t* vs = static_cast<const uint16_t*>(a.v_self) + base;
+#pragma unroll
+  for (int q = 0; q < LOADS; ++q) {
+    const int byte = q * 1024 + lane * 16, r = byte / ROWB, c = (byte % ROWB) / 16;
+    const int64_t off = min(t0 + r, a.B - 1) * rs + c * 8;
+    lds_dma16_opaque(ks + off, raw + q * 1024);
+    lds_dma16_opaque(vs + off, raw + (LOADS + q) * 1024);
+  }
+}
+
+template <int HD>
+__device__ void self_rows_place(const unsigned char* raw, unsigned char* slot, int t0, int ctx,
+                                int lane, const double* inv_rev) {
+  constexpr int ROWB = HD * 2, CPR = ROWB / 16, PAGE_BYTES = kPage * ROWB;
+  constexpr int KJ = (32 * CPR / 2) / 64, VJ = (32 * CPR) / 64;
+  const unsigned char* rv = raw + 32 * ROWB;
+#pragma unroll 2
+  for (int i = 0; i < KJ; ++i) {
+    const int jb = lane + 64 * i, r = jb / (CPR / 2), c = jb % (CPR / 2);
+    u16x8 x8 = *reinterpret_cast<const u16x8*>(raw + r * ROWB + c * 16);
+    u16x8 y8 = *reinterpret_cast<const u16x8*>(raw + r * ROWB + (c + CPR / 2) * 16);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float cs, sn;
+      rope_cos_sin_rev(ctx + t0 + r, inv_rev[c * 8 + e], &cs, &sn);
+      const float x = bf2f(x8[e]), y = bf2f(y8[e]);
+      x8[e] = f2bf(x * cs - y * sn);
+      y8[e] = f2bf(y * cs + x * sn);
+    }
+    const int rp = r & 15;
+    unsigned char* kpg = slot + (r >> 4) * PAGE_BYTES + rp * ROWB;
+    *reinterpret_cast<u16x8*>(kpg + ((c ^ (rp & (CPR - 1))) << 4)) = x8;
+    *reinterpret_cast<u16x8*>(kpg + (((c + CPR / 2) ^ (rp & (CPR - 1))) << 4)) = y8;
+  }
+#pragma unroll 2
+  for (int i = 0; i < VJ; ++i) {
+    const int jb = lane + 64 * i, r = jb / CPR, c = jb % CPR;
+    const u16x8 v8 = *reinterpret_cast<const u16x8*>(rv + r * ROWB + c * 16);
+    uint16_t* vpg = reinterpret_cast<uint16_t*>(slot + (2 + (r >> 4)) * PAGE_BYTES);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) vpg[(c * 8 + e) * kPage + (r & 15)] = v8[e];
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wavefront's own writes
+}
+
 // The part of one segment that lies in one slice (global tile indices).
 struct Piece {
   int seg_begin, seg_end;   // the segment
@@ -941,57 +1063,41 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
           return 0;
         }
       };
-      // EXT: the block's own rows of (layer, KV head, sequence) as 32-key tiles,
-      // written into a free ring slot in the layout of a cached tile (keys
-      // rotated at ctx + row, as the queries are) and consumed like one
-      auto self_tiles = [&](int s, int seg, int ctx, unsigned char* slot) {
-        const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
-        const int64_t rs = static_cast<int64_t>(a.Hkv) * HD;    // row stride of k_self / v_self
-        const uint16_t* ks = static_cast<const uint16_t*>(a.k_self) +
-                             ((static_cast<int64_t>(layer_local) * S + s) * a.B * a.Hkv + g) * HD;
-        const uint16_t* vs = static_cast<const uint16_t*>(a.v_self) +
-                             ((static_cast<int64_t>(layer_local) * S + s) * a.B * a.Hkv + g) * HD;
+      // EXT: the block's own rows of (layer, KV head, sequence) as 32-key
+      // tiles in the ring slot just read, consumed like a cached tile
+      // head_dim 64: the rows of the first segment that ends in this sub-slice
+      // are loaded when the sub-slice starts, so that their round trip overlaps
+      // the streaming of the tiles before that end
+      constexpr bool PREF = EXT && HD == 64;
+      SelfRows<HD> pre;
+      int pre_end = -1;                                 // segment end the rows belong to
+      auto self_tiles = [&](int s, int seg, int ctx, int seg_end, unsigned char* slot) {
         for (int t0 = 0; t0 < a.B; t0 += 32) {
-          // keys: lane jobs (row, rotation pair of 16-byte chunks c and c + CPR/2)
-#pragma unroll
-          for (int i = 0; i < (32 * CPR / 2) / 64; ++i) {
-            const int jb = lane + 64 * i, r = jb / (CPR / 2), c = jb % (CPR / 2);
-            const int row = t0 + r;
-            u16x8 lo = {0, 0, 0, 0, 0, 0, 0, 0}, hi = lo;
-            if (row < a.B) {
-              lo = *reinterpret_cast<const u16x8*>(ks + row * rs + c * 8);
-              hi = *reinterpret_cast<const u16x8*>(ks + row * rs + c * 8 + HD / 2);
-#pragma unroll
-              for (int e = 0; e < 8; ++e) {
-                float cs, sn;
-                rope_cos_sin_rev(ctx + row, inv_lds[c * 8 + e], &cs, &sn);
-                const float x = bf2f(lo[e]), y = bf2f(hi[e]);
-                lo[e] = f2bf(x * cs - y * sn);
-                hi[e] = f2bf(y * cs + x * sn);
-              }
-            }
-            const int rp = r & 15;
-            unsigned char* kpg = slot + (r >> 4) * PAGE_BYTES + rp * ROWB;
-            *reinterpret_cast<u16x8*>(kpg + ((c ^ (rp & (CPR - 1))) << 4)) = lo;
-            *reinterpret_cast<u16x8*>(kpg + (((c + CPR / 2) ^ (rp & (CPR - 1))) << 4)) = hi;
-          }
-          // values: lane jobs (row, 16-byte chunk), scattered into the [dim][key] pages
-#pragma unroll
-          for (int i = 0; i < (32 * CPR) / 64; ++i) {
-            const int jb = lane + 64 * i, r = jb / CPR, c = jb % CPR;
-            const int row = t0 + r;
-            u16x8 v8 = {0, 0, 0, 0, 0, 0, 0, 0};
-            if (row < a.B) v8 = *reinterpret_cast<const u16x8*>(vs + row * rs + c * 8);
-            uint16_t* vpg = reinterpret_cast<uint16_t*>(slot + (2 + (r >> 4)) * PAGE_BYTES);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) vpg[(c * 8 + e) * kPage + (r & 15)] = v8[e];
-          }
-          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wavefront's own writes
+          SelfRows<HD> rows;
+          if (PREF && t0 == 0 && pre_end == seg_end)
+            rows = pre;
+          else
+            rows.load(a, s, seg / a.Hkv, seg % a.Hkv, t0, lane);
+          rows.store(slot, t0, ctx, lane, inv_lds);
           const int nb = a.B - t0;
           consume(slot, min(nb, kPage), max(0, min(nb - kPage, kPage)), 2);
           asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // read before the next rows land
         }
       };
+      if constexpr (PREF) {
+        if (a.k_self) {
+          for (int i = pj; i < pb - pa; ++i) {           // wavefront-uniform
+            if (__builtin_amdgcn_readlane(f_beg, i) >= se) break;
+            const int send_i = __builtin_amdgcn_readlane(f_send, i);
+            if (send_i <= se) {
+              const int seg_i = __builtin_amdgcn_readlane(f_seg, i);
+              pre.load(a, __builtin_amdgcn_readlane(f_s, i), seg_i / a.Hkv, seg_i % a.Hkv, 0, lane);
+              pre_end = send_i;
+              break;
+            }
+          }
+        }
+      }
 
       for (int j = 0; j < ntw; ++j) {
         if (j + NS - 1 < ntw) issue(j + NS - 1);
@@ -1008,7 +1114,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bf16_kernel(AttnArgs a, int laye
           // the segment's last tile: its self keys follow, in the slot just read
           if (a.k_self && t + 1 == __builtin_amdgcn_readlane(f_send, pj))
             self_tiles(__builtin_amdgcn_readlane(f_s, pj), __builtin_amdgcn_readlane(f_seg, pj),
-                       pc[pa + pj].ctx, my_ring + (j % NS) * TILE_BYTES);
+                       pc[pa + pj].ctx, t + 1, my_ring + (j % NS) * TILE_BYTES);
         }
         // ---- the end of a piece, or of the sub-slice inside a piece
         if (t + 1 == c_end || j + 1 == ntw) {
@@ -1279,7 +1385,9 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
 // registers and one exchange between the two halves of the wavefront.  A
 // tile in LDS is [K page 0][K page 1][V page 0][V page 1], K rows with their
 // 16-byte chunks XOR-swizzled by the slot.
-template <int HD, int NQT>
+// EXT: two more running sums per query on the same reference, over the carry
+// keys (lu) and the block's own keys (ls), for drafter_block_attention_ext.
+template <int HD, int NQT, bool EXT = false>
 struct Tile32 {
   static constexpr int KK = HD / 16, MO = HD / 32;
   static constexpr int ROWB = HD * 2, CPR = ROWB / 16;
@@ -1290,6 +1398,7 @@ struct Tile32 {
 
   f32x16 o[NQT][MO];
   float m_run[NQT], l_run[NQT];   // l_run: this half-wavefront's keys (summed at the end)
+  float lu_run[NQT], ls_run[NQT];
   u16x8 qf[NQT][16 > KK ? KK : KK];
   uint32_t kf_off[KK], vf_off;
   int slot_base, half, r32;
@@ -1314,6 +1423,8 @@ struct Tile32 {
         for (int r = 0; r < 16; ++r) o[qt][m][r] = 0.f;
       m_run[qt] = -INFINITY;
       l_run[qt] = 0.f;
+      lu_run[qt] = 0.f;
+      ls_run[qt] = 0.f;
     }
   }
 
@@ -1329,7 +1440,8 @@ struct Tile32 {
   // one 32-key tile at tb: n0 / n1 valid keys in its two pages.  Scores are
   // formed relative to the running reference (accumulators start at -base),
   // then one rescale decision for the tile, the exponentials and the PV products.
-  __device__ void step(const unsigned char* tb, int n0, int n1) {
+  // kind0 / kind1 (EXT): the pages' keys are 0 committed, 1 carry, 2 the block's own.
+  __device__ void step(const unsigned char* tb, int n0, int n1, int kind0 = 0, int kind1 = 0) {
     const bool partial = n0 < kPage || n1 < kPage;
     u16x8 kf[KK], vf[MO][2];
 #pragma unroll
@@ -1385,6 +1497,10 @@ struct Tile32 {
         const float m_new = mx[qt] > m_run[qt] + kRescale ? mx[qt] : m_run[qt];
         const float alpha = (m_new == m_run[qt]) ? 1.f : exp2f(m_run[qt] - m_new);
         l_run[qt] *= alpha;
+        if constexpr (EXT) {
+          lu_run[qt] *= alpha;
+          ls_run[qt] *= alpha;
+        }
 #pragma unroll
         for (int m = 0; m < MO; ++m) o[qt][m] *= alpha;
         m_run[qt] = m_new;
@@ -1400,8 +1516,13 @@ struct Tile32 {
 #pragma unroll
       for (int r = 0; r < 16; ++r)   // v_exp_f32: arguments are <= kRescale or -inf
         p[r] = __builtin_amdgcn_exp2f(sc[qt][r]);
-      l_run[qt] += (((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]))) +
-                   (((p[8] + p[9]) + (p[10] + p[11])) + ((p[12] + p[13]) + (p[14] + p[15])));
+      const float p0 = ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+      const float p1 = ((p[8] + p[9]) + (p[10] + p[11])) + ((p[12] + p[13]) + (p[14] + p[15]));
+      l_run[qt] += p0 + p1;
+      if constexpr (EXT) {   // registers 0-7 hold keys of page 0, 8-15 of page 1
+        lu_run[qt] += (kind0 == 1 ? p0 : 0.f) + (kind1 == 1 ? p1 : 0.f);
+        ls_run[qt] += (kind0 == 2 ? p0 : 0.f) + (kind1 == 2 ? p1 : 0.f);
+      }
       typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
@@ -1425,6 +1546,11 @@ struct Tile32 {
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) {
       const float l_tot = l_run[qt] + __shfl_xor(l_run[qt], 32);
+      float lu = 0.f, ls = 0.f;
+      if constexpr (EXT) {
+        lu = lu_run[qt] + __shfl_xor(lu_run[qt], 32);
+        ls = ls_run[qt] + __shfl_xor(ls_run[qt], 32);
+      }
       const int qn = qrow0 + qt * 32 + r32;
       if (qn >= nq) continue;
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
@@ -1440,6 +1566,10 @@ struct Tile32 {
         }
       if (a.lse && half == 0)
         a.lse[row] = l_tot > 0.f ? (m_run[qt] + log2f(l_tot)) * kLn2 : -INFINITY;
+      if constexpr (EXT) {   // share of the attention over [C;U] on U
+        const float lcu = l_tot - ls;
+        if (a.mass && half == 0) a.mass[row] = lcu > 0.f ? lu / lcu : 0.f;
+      }
     }
   }
 
@@ -1458,9 +1588,18 @@ struct Tile32 {
           for (int c = 0; c < 4; ++c) v[c] = o[qt][m][4 * r4 + c];
           *reinterpret_cast<f32x4*>(rec + qn * HD + 32 * m + 8 * r4 + 4 * half) = v;
         }
+      float lu = 0.f, ls = 0.f;
+      if constexpr (EXT) {
+        lu = lu_run[qt] + __shfl_xor(lu_run[qt], 32);
+        ls = ls_run[qt] + __shfl_xor(ls_run[qt], 32);
+      }
       if (half == 0) {
         rec[nqp * HD + qn] = m_run[qt];
         rec[nqp * HD + nqp + qn] = l_tot;
+        if constexpr (EXT) {
+          rec[nqp * HD + 2 * nqp + qn] = lu;
+          rec[nqp * HD + 3 * nqp + qn] = ls;
+        }
       }
     }
   }
@@ -1827,12 +1966,12 @@ constexpr int kWaveMinTiles = 8; // tiles per slice below which fewer slices are
 // wavefronts per workgroup: one per SIMD at head_dim 128 (registers), two at 64
 constexpr int wave_waves(int hd) { return hd == 128 ? 4 : 8; }
 
-template <int HD, int NQT>
+template <int HD, int NQT, bool EXT>
 __global__ __launch_bounds__(64 * wave_waves(HD), 1) void attn_wave_kernel(
     AttnArgs a, int layer_count, int n_slices, int hdr_floats) {
   // NQT tiles of 32 query rows, each its own Tile32 stepping over the same key
   // tile (one fragment set live at a time keeps the registers within budget)
-  using TT = Tile32<HD, 1>;
+  using TT = Tile32<HD, 1, EXT>;
   constexpr int NQP = NQT * 32, NW = wave_waves(HD), NS = kWaveRing, NTHR = 64 * NW;
   constexpr int PAGE_BYTES = TT::PAGE_BYTES, LPP = TT::LPP, TILE_BYTES = TT::TILE_BYTES;
   constexpr int KK = TT::KK;
@@ -1864,6 +2003,7 @@ __global__ __launch_bounds__(64 * wave_waves(HD), 1) void attn_wave_kernel(
       carry_l[s] = carry;
       const int npc = (ctx + kPage - 1) / kPage, ncp = (carry + kPage - 1) / kPage;
       nts[i] = (npc + 1) / 2 + (ncp + 1) / 2;
+      if (EXT && a.k_self && si.ok && nts[i] == 0) nts[i] = 1;   // its self keys follow the tile
     }
     sum += nts[i];
   }
@@ -1983,7 +2123,9 @@ __global__ __launch_bounds__(64 * wave_waves(HD), 1) void attn_wave_kernel(
         k1 = kc + head0 + phys1 * page_stride;
         v1 = vc + head0 + phys1 * page_stride;
       } else {
-        const int cp0 = 2 * (j - nct), cp1 = min(cp0 + 1, ncp - 1);
+        // (clamped: a segment with self keys only has one empty tile)
+        const int last = max(ncp - 1, 0);
+        const int cp0 = min(2 * (j - nct), last), cp1 = min(cp0 + 1, last);
         const int64_t r0 = ((static_cast<int64_t>(layer) * a.S + s) * a.CP + cp0) * a.Hkv + g;
         const int64_t r1 = ((static_cast<int64_t>(layer) * a.S + s) * a.CP + cp1) * a.Hkv + g;
         k0 = kk + r0 * (kPage * HD);
@@ -2040,12 +2182,33 @@ __global__ __launch_bounds__(64 * wave_waves(HD), 1) void attn_wave_kernel(
       else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       const int n0 = (bcur & 1) ? 0 : keys(j, 0), n1 = (bcur & 2) ? 0 : keys(j, 1);
       if (n0 + n1 > 0) {
+        const int kind = (EXT && j >= nct) ? 1 : 0;   // a tile is committed or carry
 #pragma unroll
-        for (int qt = 0; qt < NQT; ++qt) T[qt].step(ring + (wave * NS + j % NS) * TILE_BYTES, n0, n1);
+        for (int qt = 0; qt < NQT; ++qt)
+          T[qt].step(ring + (wave * NS + j % NS) * TILE_BYTES, n0, n1, kind, kind);
       }
       bcur = bnext;
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the ring's last tile is read
+    if constexpr (EXT) {
+      // the segment's end: its self keys, in the slot of its last tile
+      if (a.k_self && j1 == nts_s) {
+        // both ring slots are free: raw rows in one, the tile in the other
+        unsigned char* slot = ring + (wave * NS + (j1 - 1) % NS) * TILE_BYTES;
+        const unsigned char* raw = ring + (wave * NS + j1 % NS) * TILE_BYTES;
+        static_assert(NS == 2 && 2 * 32 * HD * 2 <= TILE_BYTES, "self staging");
+        for (int r0 = 0; r0 < a.B; r0 += 32) {
+          self_rows_raw<HD>(a, s, layer_local, g, r0, lane, lds_addr(raw));
+          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+          self_rows_place<HD>(raw, slot, r0, ctx, lane, inv_lds);
+          const int nb = a.B - r0;
+#pragma unroll
+          for (int qt = 0; qt < NQT; ++qt)
+            T[qt].step(slot, min(nb, kPage), max(0, min(nb - kPage, kPage)), 2, 2);
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // read before the next rows land
+        }
+      }
+    }
 
     // ---- a whole segment: normalise and write; else a record for the combine
     float* rec = slot_ptr(a, hdr_floats, w + static_cast<int64_t>(seg) * S + s, NQP);
@@ -2096,8 +2259,6 @@ AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pa
     const size_t park =
         hd * (p.nq_pad / 16) > 128 ? static_cast<size_t>(p.n_wg) * nw * rec : 0;
     p.park_off = static_cast<int64_t>(p.hdr_floats + records);
-    p.n_wg_persist = p.n_wg;
-    p.hdr_persist = p.hdr_floats;
     p.bytes = (p.hdr_floats + records + park) * 4;
     // global tile indices, committed and carry K/V row indices are int32
     const int64_t tiles = static_cast<int64_t>(L) * Hkv * S * ((max_lp + 1) / 2);
@@ -2166,10 +2327,10 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
   const dim3 mgrid(a.S, layer_count * a.Hkv, (items + 255) / 256);
   const int items_f32 = (a.B * (a.Hq / a.Hkv)) * (a.hd / 4);
   const dim3 fgrid(a.S, layer_count * a.Hkv, (items_f32 + 255) / 256);
-  // the extras (self segment, carry mass) run on the persistent kernel
+  // the extras (self segment, carry mass): the same kernels' EXT instantiations
+  // (the grouped-prefix kernel has none: its launches take the other paths)
   const bool ext = a.k_self != nullptr || a.mass != nullptr;
-  const int n_wg = ext ? p.n_wg_persist : p.n_wg;
-  const int hdr_floats = ext ? p.hdr_persist : p.hdr_floats;
+  const int n_wg = p.n_wg, hdr_floats = p.hdr_floats;
   auto combine = [&]() {
     if (wide)
       hipLaunchKernelGGL(attn_bf16_combine_kernel<16>, mgrid, dim3(256), 0, stream, a, layer_count,
@@ -2202,18 +2363,25 @@ hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int layer_coun
       hipLaunchKernelGGL(attn_share_merge_kernel<128>, cgrid, dim3(256), 0, stream, a, sp, ns, nqp, kGroupSeqs);
     return hipGetLastError();
   }
-  if (a.dtype == CO_DTYPE_BF16 && !ext && p.wave) {
+  if (a.dtype == CO_DTYPE_BF16 && p.wave) {
     const int nw = wave_waves(a.hd);
     const dim3 wgrid(p.n_wg / nw), wblock(64 * nw);
+#define CO_WAVE_LAUNCH(HD, NQT)                                                              \
+  do {                                                                                       \
+    if (ext)                                                                                 \
+      hipLaunchKernelGGL((attn_wave_kernel<HD, NQT, true>), wgrid, wblock, 0, stream, a,     \
+                         layer_count, p.n_wg, p.hdr_floats);                                 \
+    else                                                                                     \
+      hipLaunchKernelGGL((attn_wave_kernel<HD, NQT, false>), wgrid, wblock, 0, stream, a,    \
+                         layer_count, p.n_wg, p.hdr_floats);                                 \
+  } while (0)
     if (a.hd == 128)
-      hipLaunchKernelGGL((attn_wave_kernel<128, 2>), wgrid, wblock, 0, stream, a, layer_count,
-                         p.n_wg, p.hdr_floats);
+      CO_WAVE_LAUNCH(128, 2);
     else if (p.nq_pad == 32)
-      hipLaunchKernelGGL((attn_wave_kernel<64, 1>), wgrid, wblock, 0, stream, a, layer_count,
-                         p.n_wg, p.hdr_floats);
+      CO_WAVE_LAUNCH(64, 1);
     else
-      hipLaunchKernelGGL((attn_wave_kernel<64, 2>), wgrid, wblock, 0, stream, a, layer_count,
-                         p.n_wg, p.hdr_floats);
+      CO_WAVE_LAUNCH(64, 2);
+#undef CO_WAVE_LAUNCH
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     combine();

@@ -162,6 +162,7 @@ co_status validate_project(const co_dims* d, const co_weights* w, const void* hi
       !aligned(w->e_carry, 16) || !aligned(w->f_e, 16) || !aligned(w->w_f_carry, 16) ||
       !aligned(w->z_norm, 4) || !aligned(w->k_norm, 4))
     return CO_ERR_INVALID_ARG;
+  if (w->z_norm && d->model_dim > kNormMaxCols) return CO_ERR_UNSUPPORTED;
   if (!ws || !aligned(ws, 256)) return CO_ERR_INVALID_ARG;
   if (ws_bytes < project_plan(d).total) return CO_ERR_WORKSPACE;
   return CO_OK;

@@ -61,6 +61,8 @@ struct ProjectPlan {
 
 ProjectPlan plan_project(int M, int Dcat, int d, int n_kv, int hd, int dtype, int num_cus);
 
+constexpr int kNormMaxCols = 16384;   // widest F output the RMS normalisation takes
+
 struct AttnArgs {
   int S, B, L, layer_begin, Hq, Hkv, hd, num_pages, max_pages, CP, dtype;
   uint32_t flags;
@@ -94,7 +96,6 @@ struct AttnPlan {
   int round_tiles;             // bf16 persistent path: tiles per wavefront per round
   int64_t park_off;            // bf16 persistent path: parked partials (workspace floats)
   bool wave;                   // bf16: per-wavefront slices (n_wg = slices, not workgroups)
-  int n_wg_persist, hdr_persist;   // bf16 persistent path's n_wg, hdr_floats (the extras use it)
   int nq_pad;
   bool ok;                     // false: shapes beyond what one launch can cover
   size_t bytes;

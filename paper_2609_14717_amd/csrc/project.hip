@@ -916,27 +916,96 @@ __global__ __launch_bounds__(256, 1) void proj_fused_kernel(ProjectArgs a) {
 
 // ------------------------------------------------- RMS norm of F's output
 // The normalisation variant: every row of Z is divided by its root mean
-// square (epsilon kRmsEps) and multiplied by the gain g, in place, before the
-// K/V product.  One wavefront per row, fp32 arithmetic.
+// square (epsilon kRmsEps) and multiplied by the gain g before the K/V
+// product.  One workgroup per row, fp32 arithmetic; every load of the row is
+// issued before the first is used.  Rows of up to kNormMaxCols columns.
 
+__device__ __forceinline__ float block_sum_256(float v, float* red) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// In place, for a Z the GEMM wrote whole (no split partials).
 template <typename T>
 __global__ __launch_bounds__(256) void z_norm_kernel(T* z, int M, int d, const float* g) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (row >= M) return;
+  constexpr int QMAX = kNormMaxCols / 1024;   // column quads per thread
+  __shared__ float red[4];
+  const int row = blockIdx.x, tid = threadIdx.x;
   T* zr = z + static_cast<int64_t>(row) * d;
+  f32x4 v[QMAX];
   float ss = 0.f;
-  for (int c = lane; c < d; c += 64) {
-    float v;
-    if constexpr (sizeof(T) == 2) v = bf2f(zr[c]); else v = zr[c];
-    ss = fmaf(v, v, ss);
+#pragma unroll
+  for (int qi = 0; qi < QMAX; ++qi) {
+    const int col = (tid + 256 * qi) * 4;
+    v[qi] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (col < d) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if constexpr (sizeof(T) == 2) v[qi][q] = bf2f(zr[col + q]); else v[qi][q] = zr[col + q];
+      }
+    }
   }
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
-  const float r = rsqrtf(ss / static_cast<float>(d) + kRmsEps);
-  for (int c = lane; c < d; c += 64) {
-    float v;
-    if constexpr (sizeof(T) == 2) v = bf2f(zr[c]); else v = zr[c];
-    zr[c] = to_elem<T>(v * r * g[c]);
+  for (int qi = 0; qi < QMAX; ++qi)
+    ss += (v[qi][0] * v[qi][0] + v[qi][1] * v[qi][1]) + (v[qi][2] * v[qi][2] + v[qi][3] * v[qi][3]);
+  const float r = rsqrtf(block_sum_256(ss, red) / static_cast<float>(d) + kRmsEps);
+#pragma unroll
+  for (int qi = 0; qi < QMAX; ++qi) {
+    const int col = (tid + 256 * qi) * 4;
+    if (col < d) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) zr[col + q] = to_elem<T>(v[qi][q] * r * g[col + q]);
+    }
+  }
+}
+
+// The epilogue of a split F product with the normalisation: the row's split
+// partials are summed (plus F(E), or E's split partials, on carry rows), the
+// row's sum of squares reduced over the workgroup, and the normalised row
+// written once.  Rows not selected by z_rows (separate projector) are left.
+template <typename T>
+__global__ __launch_bounds__(256) void epi_z_norm_kernel(const float* part, int splits, int M,
+                                                         int N, T* z, const float* part_e,
+                                                         const float* fe, const int32_t* row_dst,
+                                                         int z_rows, const float* g) {
+  constexpr int QMAX = kNormMaxCols / 1024;
+  __shared__ float red[4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  if (!z_row_selected(z_rows, row_dst[row])) return;   // uniform over the workgroup
+  const bool carry = (part_e || fe) && is_carry_row(row_dst[row]);
+  const int64_t MN = static_cast<int64_t>(M) * N;
+  const float* pr = part + static_cast<int64_t>(row) * N;
+  f32x4 v[QMAX];
+  float ss = 0.f;
+#pragma unroll
+  for (int qi = 0; qi < QMAX; ++qi) {
+    const int col = (tid + 256 * qi) * 4;
+    v[qi] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (col < N) {
+      for (int sp = 0; sp < splits; ++sp) v[qi] += *reinterpret_cast<const f32x4*>(pr + sp * MN + col);
+      if (carry) {
+        if (fe) {
+          v[qi] += *reinterpret_cast<const f32x4*>(fe + col);
+        } else {
+          for (int sp = 0; sp < splits; ++sp)
+            v[qi] += *reinterpret_cast<const f32x4*>(part_e + static_cast<int64_t>(sp) * N + col);
+        }
+      }
+    }
+    ss += (v[qi][0] * v[qi][0] + v[qi][1] * v[qi][1]) + (v[qi][2] * v[qi][2] + v[qi][3] * v[qi][3]);
+  }
+  const float r = rsqrtf(block_sum_256(ss, red) / static_cast<float>(N) + kRmsEps);
+  T* zr = z + static_cast<int64_t>(row) * N;
+#pragma unroll
+  for (int qi = 0; qi < QMAX; ++qi) {
+    const int col = (tid + 256 * qi) * 4;
+    if (col < N) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) zr[col + q] = to_elem<T>(v[qi][q] * r * g[col + q]);
+    }
   }
 }
 
@@ -1218,14 +1287,17 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
       if (pass == 1) f.B = a.wfc;
       hipLaunchKernelGGL(gemm_f32_kernel, dim3((f.N + 63) / 64, (f.M + 31) / 32, fs), dim3(256),
                          0, stream, f);
-      hipLaunchKernelGGL(epi_z_kernel<float>, dim3(static_cast<unsigned>((nz + 255) / 256)),
-                         dim3(256), 0, stream, part, fs, a.M, a.d, static_cast<float*>(z),
-                         static_cast<const float*>(nullptr), static_cast<const float*>(nullptr),
-                         a.dst.row_dst, sep ? pass + 1 : 0);
+      if (a.znorm != nullptr)
+        hipLaunchKernelGGL(epi_z_norm_kernel<float>, dim3(a.M), dim3(256), 0, stream, part, fs,
+                           a.M, a.d, static_cast<float*>(z), static_cast<const float*>(nullptr),
+                           static_cast<const float*>(nullptr), a.dst.row_dst, sep ? pass + 1 : 0,
+                           a.znorm);
+      else
+        hipLaunchKernelGGL(epi_z_kernel<float>, dim3(static_cast<unsigned>((nz + 255) / 256)),
+                           dim3(256), 0, stream, part, fs, a.M, a.d, static_cast<float*>(z),
+                           static_cast<const float*>(nullptr), static_cast<const float*>(nullptr),
+                           a.dst.row_dst, sep ? pass + 1 : 0);
     }
-    if (a.znorm != nullptr)
-      hipLaunchKernelGGL(z_norm_kernel<float>, dim3((a.M + 3) / 4), dim3(256), 0, stream,
-                         static_cast<float*>(z), a.M, a.d, a.znorm);
     hipLaunchKernelGGL(gemm_f32_kernel, dim3((kv.N + 63) / 64, (kv.M + 31) / 32, ks), dim3(256),
                        0, stream, kv);
     const int64_t items = static_cast<int64_t>(a.M) * (n_kv / 2);
@@ -1250,7 +1322,12 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
     if (pass == 1) f.B = a.wfc;
     f.z_rows = sep ? pass + 1 : 0;
     if ((err = launch_gemm_bf16(f, p.f_tile, p.f_split, stream)) != hipSuccess) return err;
-    if (p.f_split > 1) {
+    if (p.f_split > 1 && a.znorm != nullptr) {   // normalised in the split epilogue
+      hipLaunchKernelGGL(epi_z_norm_kernel<uint16_t>, dim3(a.M), dim3(256), 0, stream, part,
+                         p.f_split, a.M, a.d, static_cast<uint16_t*>(z),
+                         static_cast<const float*>(f.e ? f.partial_e : nullptr), f.fe,
+                         a.dst.row_dst, f.z_rows, a.znorm);
+    } else if (p.f_split > 1) {
       const int64_t nz = static_cast<int64_t>(a.M) * a.d / 4;
       hipLaunchKernelGGL(epi_z_kernel<uint16_t>, dim3(static_cast<unsigned>((nz + 255) / 256)),
                          dim3(256), 0, stream, part, p.f_split, a.M, a.d,
@@ -1259,8 +1336,8 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
                          a.dst.row_dst, f.z_rows);
     }
   }
-  if (a.znorm != nullptr)
-    hipLaunchKernelGGL(z_norm_kernel<uint16_t>, dim3((a.M + 3) / 4), dim3(256), 0, stream,
+  if (a.znorm != nullptr && p.f_split == 1)   // Z written whole by the GEMM: normalised in place
+    hipLaunchKernelGGL(z_norm_kernel<uint16_t>, dim3(a.M), dim3(256), 0, stream,
                        static_cast<uint16_t*>(z), a.M, a.d, a.znorm);
   kv.k_per_split = split_len(a.d, p.kv_split, p.kv_tile);
   kv.mode = p.kv_split > 1 ? kModePartial : kModeKV;

@@ -348,3 +348,27 @@ def test_attention_ext_empty_context():
                no_committed=(1,))
     sc2, orc2 = Scenario(w), OracleRun(w)
     _ext_round(co, sc2, orc2, w, 0, [0, 3, w.B, 5], "mass", "carry only", no_committed=(1,))
+
+
+# 64 block rows of one query head per KV head: 64 query rows at head_dim 128
+# (the slices kernel's shape) and two self tiles
+HD128_B64 = wl.Workload("ext_hd128_b64", S=3, B=64, Dcat=256, d=128, L=1, Hq=1, Hkv=1, hd=128,
+                        dtype="bf16", theta=1e6, ctx_lo=30, ctx_hi=700, ctx_mode="direct",
+                        accept=("geom", 0.1), rounds=4, seed=0x5EED27)
+
+
+@pytest.mark.parametrize("wgs", ["", "1", "7"], ids=lambda v: f"wg{v or 'dflt'}")
+@pytest.mark.parametrize("w", [EDGE, HD128, HD128_B64], ids=lambda w: w.name)
+def test_attention_ext_wave_slices(w, wgs, tune):
+    """Both extras on the per-wavefront slices kernel (head_dim 64 forced onto
+    it, head_dim 128 there by default; 64 block rows: two self tiles staged
+    through LDS), default and forced slice counts."""
+    Scenario, co = _gpu()
+    tune("attn_wave", 1)
+    if wgs:
+        tune("attn_workgroups", wgs)
+    print(f"[variants] ext wave slices {w.name} wg={wgs or 'dflt'}", flush=True)
+    sc, orc = Scenario(w), OracleRun(w)
+    for r, m in enumerate([None, [w.B] * w.S, [0] * w.S]):
+        _ext_round(co, sc, orc, w, r, m, "both", f"wave {w.name} wg{wgs} r{r}",
+                   empty=(1,) if r == 2 else ())
