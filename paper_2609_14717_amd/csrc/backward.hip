@@ -11,23 +11,32 @@
 // training layout: consecutive sequences of a group read the same page row),
 // so their gradients are sums over the group's blocks.
 //
-// Five kernels; the products run on v_mfma_f32_32x32x16_bf16 (bf16 operands,
+// Four kernels; the products run on v_mfma_f32_32x32x16_bf16 (bf16 operands,
 // fp32 sums):
 //   prep   per (layer, KV head, sequence): the rotated, scaled queries (log2
 //          units, as the forward forms them) and their transpose, dO packed
-//          and transposed, the forward's LSE in log2 units and D;
+//          and transposed, and -LSE (log2 units) and -D, which the products
+//          then take as their starting sums;
 //   copy   every K page transposed ([hd][16]) and every V page in key-major
-//          order ([16][hd]), so that all MFMA operands are 16-byte loads with
+//          order ([16][hd]), so that all MFMA operands are 16-byte reads with
 //          the contracted index contiguous;
-//   dkv    one wavefront per (layer, KV head, group, two 32-key tiles of committed
-//          keys): the tiles' K and V stay in registers while the group's blocks
-//          stream by; S = Q K^T is formed with its query rows permuted (bits 2
-//          and 3 swapped) so that P and dS come out of the accumulators already
-//          in the operand layout of dV^T = dO^T P and dK^T = (R q)^T dS;
-//   dq     one wavefront per (layer, KV head, sequence, or two sequences of a
-//          group, which then share every committed tile load): S^T = K Q^T over
-//          the tiles (keys permuted the same way), dQ^T += K^T dS^T, then the
-//          rotation is undone;
+//   attn   one launch with two kinds of workgroup (eight wavefronts each):
+//          dkv    per (group, layer x KV head, run of eight 32-key committed
+//                 tiles), one tile per wavefront: the tile's K and V stay in
+//                 registers while the group's sequences stream by, each
+//                 sequence's operands staged once per workgroup in LDS;
+//                 S = Q K^T is formed with its query rows permuted (bits 2
+//                 and 3 swapped) so that P and dS come out of the
+//                 accumulators already in the operand layout of dV^T = dO^T P
+//                 and dK^T = (R q)^T dS;
+//          dq     per sixteen sequences of a group (two per wavefront) and
+//                 layer x KV head: each committed tile of the group's page row
+//                 staged once per workgroup in LDS; S^T = K Q^T (keys
+//                 permuted the same way), dQ^T += K^T dS^T, then each
+//                 sequence's carry tiles, and the rotation is undone;
+//          both kinds of work shrink from the first keys of a response (seen
+//          by all its blocks) to the last; in one grid the dq workgroups fill
+//          the compute units the short dkv runs leave;
 //   carry  carry keys belong to one sequence: their tiles take the dkv step
 //          against that sequence alone.
 // Keys masked in the forward (past ctx_len or carry_len, rejected page ids)
@@ -43,7 +52,32 @@ namespace {
 constexpr float kLog2eB = 1.4426950408889634f;
 constexpr float kLn2B = 0.6931471805599453f;
 constexpr int kNqp = 32;   // query rows per (sequence, KV head): one 32-row MFMA tile
-constexpr int kDkvTiles = 2;   // committed key tiles per dkv wavefront
+constexpr int kDkvTiles = 1;   // committed key tiles per dkv wavefront
+constexpr int kDkvWaves = 8;   // wavefronts per dkv workgroup (consecutive tiles)
+constexpr int kDqSeqs = 2;     // sequences per dq wavefront when groups share page rows
+// One dkv ring slot (head_dim 64): the packed rotated queries and dO [32][64],
+// their transposes [64][32], then -LSE (log2) and -D [32], bytes.
+constexpr int kSlotQr = 0, kSlotDon = 4096, kSlotQrt = 8192, kSlotDot = 12288, kSlotL2 = 16384,
+              kSlotDd = 16512, kSlotBytes = 16640;
+// One dq ring slot: a committed tile's K rows and key-major V rows [32][64] and
+// its K^T rows [64][32], bytes.
+constexpr int kDqSlotK = 0, kDqSlotV = 4096, kDqSlotKt = 8192, kDqSlotBytes = 12288;
+// Ring slots: a step's operands are staged two steps ahead.  (Deeper rings
+// measured slower: the loops are bound by the LDS reads, not by the loads.)
+constexpr int kDkvStages = 3, kDqStages = 3;
+constexpr int kBwdSmem = kDkvStages * kSlotBytes > kDqStages * kDqSlotBytes
+                             ? kDkvStages * kSlotBytes : kDqStages * kDqSlotBytes;
+static_assert(kBwdSmem <= 160 * 1024, "one workgroup's LDS");
+// XOR keys of the 16-byte chunks of a slot row.  LDS has 64 banks of 4 bytes:
+// a 16-byte read serves sixteen lanes per pass, and the keys give those
+// sixteen lanes sixteen different 16-byte bank groups.  Packed rows (128
+// bytes, two per bank window) are read as rows perm23(l % 32), which for
+// lanes 16i .. 16i + 15 are sixteen consecutive rows: bit 0 picks the half of
+// the window, bits 1-3 the chunk key.  Transposed rows (64 bytes, four per
+// window) are read as sixteen consecutive rows: bits 0-1 pick the quarter,
+// bits 2-3 the chunk key.
+__device__ __forceinline__ int swz_packed(int row) { return (row >> 1) & 7; }
+__device__ __forceinline__ int swz_trans(int row) { return (row >> 2) & 3; }
 
 // query (or key) index held by A-row / C-row rho when rows are permuted by
 // swapping bits 2 and 3: then accumulator register r of lane l belongs to index
@@ -58,7 +92,7 @@ __device__ __forceinline__ int acc_index(int r, int h) { return (r < 8 ? 0 : 16)
 // Workspace pieces (bytes are 256-aligned by the host plan).
 struct BwdWs {
   uint16_t *qr, *qrt, *don, *dot;   // [seg][S][32][hd] / [seg][S][hd][32]
-  float *lse2, *dd;                 // [seg][S][32]
+  float *nlse2, *ndd;               // -LSE (log2 units), -D: [seg][S][32]
   uint16_t *kt, *vn;                // committed pages: [lc][num_pages][Hkv][hd][16] / [16][hd]
   uint16_t *ktc, *vnc;              // carry pages:     [lc][S][CP][Hkv][hd][16] / [16][hd]
 };
@@ -77,8 +111,8 @@ __device__ __forceinline__ BwdWs bwd_ws(const BwdArgs& b) {
   w.qrt = reinterpret_cast<uint16_t*>(p); p += up(qsz * 2);
   w.don = reinterpret_cast<uint16_t*>(p); p += up(qsz * 2);
   w.dot = reinterpret_cast<uint16_t*>(p); p += up(qsz * 2);
-  w.lse2 = reinterpret_cast<float*>(p); p += up(vsz * 4);
-  w.dd = reinterpret_cast<float*>(p); p += up(vsz * 4);
+  w.nlse2 = reinterpret_cast<float*>(p); p += up(vsz * 4);
+  w.ndd = reinterpret_cast<float*>(p); p += up(vsz * 4);
   w.kt = reinterpret_cast<uint16_t*>(p); p += up(cpg * 2);
   w.vn = reinterpret_cast<uint16_t*>(p); p += up(cpg * 2);
   w.ktc = reinterpret_cast<uint16_t*>(p); p += up(cpc * 2);
@@ -169,13 +203,14 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdArgs b) {
   dsum += __shfl_xor(dsum, 2);
   dsum += __shfl_xor(dsum, 4);
   if (p == 0) {
+    // stored negated: the products below start their accumulators from them
     float l2 = INFINITY;   // padding rows: no weight anywhere
     if (live) {
       const float l = b.lse[out_row_b(a, layer_local, s, g, qn, G)];
       l2 = l * kLog2eB;    // -inf (no keys) stays -inf: such rows see no key either
     }
-    w.lse2[base + qn] = l2;
-    w.dd[base + qn] = live ? dsum : 0.f;
+    w.nlse2[base + qn] = -l2;
+    w.ndd[base + qn] = live ? -dsum : 0.f;
   }
 }
 
@@ -249,11 +284,12 @@ struct KeyGrad {
   }
 
   // One sequence's operands of the step: its query rows (permuted) and dO
-  // as A-fragments, their transposes, and the LSE / D of the 16 query rows
-  // this lane's accumulator registers hold.
+  // as A-fragments, their transposes, and -LSE / -D of the 16 query rows
+  // this lane's accumulator registers hold (in accumulator order, so that
+  // S - LSE and dP - D come out of the products with no further step).
   struct Block {
     u16x8 qa[KS], da[KS], qt[MT][2], dt[MT][2];
-    float l2[16], dd[16];
+    f32x16 nl2, ndd;
     int n0[NT], n1[NT];   // valid keys of each tile's two pages for this sequence
 
     __device__ void load(const BwdWs& w, int64_t qbase, int lane) {
@@ -277,20 +313,55 @@ struct KeyGrad {
         }
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        const f32x4 a0 = *reinterpret_cast<const f32x4*>(w.lse2 + qbase + 16 * j + 8 * h);
-        const f32x4 a1 = *reinterpret_cast<const f32x4*>(w.lse2 + qbase + 16 * j + 8 * h + 4);
-        const f32x4 b0 = *reinterpret_cast<const f32x4*>(w.dd + qbase + 16 * j + 8 * h);
-        const f32x4 b1 = *reinterpret_cast<const f32x4*>(w.dd + qbase + 16 * j + 8 * h + 4);
+        const f32x4 a0 = *reinterpret_cast<const f32x4*>(w.nlse2 + qbase + 16 * j + 8 * h);
+        const f32x4 a1 = *reinterpret_cast<const f32x4*>(w.nlse2 + qbase + 16 * j + 8 * h + 4);
+        const f32x4 b0 = *reinterpret_cast<const f32x4*>(w.ndd + qbase + 16 * j + 8 * h);
+        const f32x4 b1 = *reinterpret_cast<const f32x4*>(w.ndd + qbase + 16 * j + 8 * h + 4);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          l2[8 * j + e] = a0[e];
-          l2[8 * j + 4 + e] = a1[e];
-          dd[8 * j + e] = b0[e];
-          dd[8 * j + 4 + e] = b1[e];
+          nl2[8 * j + e] = a0[e];
+          nl2[8 * j + 4 + e] = a1[e];
+          ndd[8 * j + e] = b0[e];
+          ndd[8 * j + 4 + e] = b1[e];
         }
       }
     }
   };
+
+  // The same operands from a staged copy in LDS (a dkv ring slot: rows with
+  // their 16-byte chunks XOR-swizzled by swz_packed / swz_trans).
+  __device__ static void load_lds(Block& q, const unsigned char* slot, int lane) {
+    const int r32 = lane & 31, h = lane >> 5;
+    const int qp = perm23(r32);
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const int o = (16 * j + 8 * h + 4 * c) * 4;
+        const f32x4 a4 = *reinterpret_cast<const f32x4*>(slot + kSlotL2 + o);
+        const f32x4 b4 = *reinterpret_cast<const f32x4*>(slot + kSlotDd + o);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          q.nl2[8 * j + 4 * c + e] = a4[e];
+          q.ndd[8 * j + 4 * c + e] = b4[e];
+        }
+      }
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+      const int off = qp * (2 * HD) + (((h + 2 * k) ^ swz_packed(qp)) << 4);
+      q.qa[k] = *reinterpret_cast<const u16x8*>(slot + kSlotQr + off);
+      q.da[k] = *reinterpret_cast<const u16x8*>(slot + kSlotDon + off);
+    }
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int row = 32 * m + r32;
+        const int off = row * (2 * kNqp) + (((2 * j + h) ^ swz_trans(row)) << 4);
+        q.qt[m][j] = *reinterpret_cast<const u16x8*>(slot + kSlotQrt + off);
+        q.dt[m][j] = *reinterpret_cast<const u16x8*>(slot + kSlotDot + off);
+      }
+  }
 
   __device__ void compute(const Block& q, const u16x8 (&kb)[NT][KS], const u16x8 (&vb)[NT][KS],
                           int lane) {
@@ -302,16 +373,23 @@ struct KeyGrad {
                                       int n0, int n1, f32x16 (&dkt)[MT], f32x16 (&dvt)[MT],
                                       int lane) {
     const int r32 = lane & 31;
-    f32x16 sc, dp;
+    // S - LSE and dP - D: the products start from -LSE and -D.  A key past
+    // the sequence's length (this lane's column) starts from -inf instead, so
+    // its P and dS are 0 (whatever its cache slot holds, it reaches only its
+    // own column, which is not stored).
+    f32x16 sc = q.nl2, dp = q.ndd;
+    if (n0 < kPage || n1 < kPage) {
+      const int key = r32;
+      if (key < 16 ? key >= n0 : key - 16 >= n1) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.f;
+        for (int r = 0; r < 16; ++r) sc[r] = -INFINITY;
+      }
+    }
 #pragma unroll
     for (int k = 0; k < KS; ++k) {
       sc = mfma32x32x16(q.qa[k], kb[k], sc);
       dp = mfma32x32x16(q.da[k], vb[k], dp);
     }
-    const int key = r32;   // this lane's column
-    const bool valid = key < 16 ? key < n0 : key - 16 < n1;
     u16x8 pb[2], sb[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
@@ -319,9 +397,9 @@ struct KeyGrad {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int r = 8 * j + e;
-        const float pr = valid ? __builtin_amdgcn_exp2f(sc[r] - q.l2[r]) : 0.f;
+        const float pr = __builtin_amdgcn_exp2f(sc[r]);
         pv[e] = pr;
-        sv[e] = pr * (dp[r] - q.dd[r]);
+        sv[e] = pr * dp[r];
       }
       typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
       const u32x4v p4 = {cvt_pk_bf16(pv[0], pv[1]), cvt_pk_bf16(pv[2], pv[3]),
@@ -395,34 +473,39 @@ __device__ __forceinline__ bool len_ok(const AttnArgs& a, int ctx, int carry) {
 
 // ------------------------------------------------------------------- dkv
 //
-// grid (committed tiles of the longest row, groups, layer_count * Hkv), one
-// wavefront.  The group's first sequence holds the page row; a tile no block
-// of the group reaches is skipped.
+// One workgroup of kDkvWaves wavefronts per (group, layer x KV head, run of
+// kDkvWaves consecutive committed key tiles), one tile per wavefront: the
+// tile's K and V stay in registers while the group's sequences stream by.
+// Each sequence's operands (16.3 KiB) are staged once per workgroup into an
+// LDS ring slot by direct-to-LDS loads, two sequences ahead, and every
+// wavefront reads its fragments from there.  The group's first sequence holds
+// the page row; tiles no sequence of the group reaches are skipped.
 template <int HD>
-__global__ __launch_bounds__(64, 1) void bwd_dkv_kernel(BwdArgs b) {
+__device__ __forceinline__ void dkv_role(const BwdArgs& b, int pair, int unit, unsigned char* ring) {
+  static_assert(HD == 64, "ring slot layout");
+  static_assert(16 % kDkvWaves == 0, "the sixteen 1 KiB pieces of a slot split evenly");
   constexpr int NT = kDkvTiles, KS = HD / 16;
   const AttnArgs& a = b.a;
   const BwdWs w = bwd_ws(b);
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int groups = (a.S + b.group - 1) / b.group;
-  const int units = ((a.max_pages + 1) / 2 + NT - 1) / NT;
-  int pair, unit;
-  if (!xcd_item(groups * b.layer_count * a.Hkv, units, &pair, &unit)) return;
   const int grp = pair % groups, seg = pair / groups;
   const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
   const int s0 = grp * b.group, s1 = min(a.S, s0 + b.group);
-  const int kbase = 32 * NT * unit;   // the first key of the unit's NT tiles
-  int reach = 0;   // committed keys the group's blocks see
+  const int kb0 = 32 * NT * kDkvWaves * unit;   // the workgroup's first key
+  const int kbase = kb0 + 32 * NT * wave;       // this wavefront's first key
+  int reach = 0;   // committed keys the group's sequences see
   for (int s = s0; s < s1; ++s) {
     const int ctx = a.ctx_len[s], carry = a.carry_len[s];
     if (len_ok(a, ctx, carry)) reach = max(reach, ctx);
   }
-  if (kbase >= reach) return;
+  if (kb0 >= reach) return;   // the whole workgroup, before any barrier
   const int32_t* pt = a.page_table + static_cast<int64_t>(s0) * a.max_pages;
   const int64_t pe = static_cast<int64_t>(kPage) * HD;
   const int64_t lay = static_cast<int64_t>(a.layer_begin + layer_local) * a.num_pages;
   const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
-  // pages 2 t, 2 t + 1 of each tile t; pages no block reaches are not read
+  // pages of this wavefront's tiles; pages no sequence reaches are not read
   int id[NT][2];
   bool bad[NT][2];
   u16x8 kb[NT][KS], vb[NT][KS];
@@ -430,7 +513,7 @@ __global__ __launch_bounds__(64, 1) void bwd_dkv_kernel(BwdArgs b) {
   for (int t = 0; t < NT; ++t) {
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
-      const int pg = 2 * (NT * unit + t) + p;
+      const int pg = kbase / kPage + 2 * t + p;
       const bool has = kbase + (2 * t + p) * kPage < reach;
       const int x = has ? pt[pg] : 0;
       bad[t][p] = has && (x < 0 || x >= a.num_pages);
@@ -448,14 +531,15 @@ __global__ __launch_bounds__(64, 1) void bwd_dkv_kernel(BwdArgs b) {
   };
   KeyGrad<HD, NT> kg;
   kg.zero();
-  // The group's sequences that see the unit, walked from the last one down (it
-  // sees the most keys, so every unit of the group starts on the same
-  // sequence and the XCD's units read the same operands at about the same
-  // time), 64 at a time as a lane mask.
+  // The group's sequences that see the workgroup's first key, walked from the
+  // last one down (it sees the most keys, so every workgroup of the group
+  // starts on the same sequence and the XCD's workgroups stage the same
+  // operands at about the same time), 64 at a time as a lane mask.  Every
+  // wavefront walks the same list, so all take the same barriers.
   const int none = s0 - 1;
   uint64_t mask = 0;
   int mbase = s1, mctx = 0;
-  auto prev = [&](int x) {   // last sequence <= x that sees the unit, or none
+  auto prev = [&](int x) {   // last sequence <= x that sees the workgroup, or none
     for (;;) {
       if (x < s0) return none;
       if (x < mbase) {
@@ -466,7 +550,7 @@ __global__ __launch_bounds__(64, 1) void bwd_dkv_kernel(BwdArgs b) {
         mctx = 0;
         if (y <= top) {
           const int ctx = a.ctx_len[y], carry = a.carry_len[y];
-          v = len_ok(a, ctx, carry) && ctx > kbase;
+          v = len_ok(a, ctx, carry) && ctx > kb0;
           mctx = ctx;
         }
         mask = __ballot(v);
@@ -477,22 +561,70 @@ __global__ __launch_bounds__(64, 1) void bwd_dkv_kernel(BwdArgs b) {
       x = mbase - 1;
     }
   };
+  // A sequence's operands into ring slot `slot` by direct-to-LDS loads: each
+  // wavefront moves its 1 KiB pieces of the packed arrays (16-byte chunks of
+  // a row XOR-swizzled by the row); wavefront 0 also moves -LSE and -D (16 lanes).
+  auto stage_block = [&](int s, int slot) {
+    const uint32_t base = lds_addr(ring) + slot * kSlotBytes;
+    const int64_t qbase = (static_cast<int64_t>(seg) * a.S + s) * kNqp;
+    // pieces P wave .. P wave + P - 1 (P = 16 / kDkvWaves): pieces 0-7 are the
+    // packed arrays (rows of 128 bytes), 8-15 their transposes (rows of 64 bytes)
+    constexpr int P = 16 / kDkvWaves;
+#pragma unroll
+    for (int x = 0; x < P; ++x) {
+      const int piece = P * wave + x, arr = piece >> 2;
+      const int off = (piece & 3) * 1024 + 16 * lane;
+      const uint32_t dst = base + arr * 4096 + (piece & 3) * 1024;
+      if (arr < 2) {
+        const int row = off / (2 * HD), lg = ((off % (2 * HD)) >> 4) ^ swz_packed(row);
+        lds_dma16_opaque((arr == 0 ? w.qr : w.don) + (qbase + row) * HD + lg * 8, dst);
+      } else {
+        const int row = off / (2 * kNqp), lg = ((off % (2 * kNqp)) >> 4) ^ swz_trans(row);
+        lds_dma16_opaque((arr == 2 ? w.qrt : w.dot) + qbase * HD + row * kNqp + lg * 8, dst);
+      }
+    }
+    if (wave == 0 && lane < 16) {
+      const float* src = lane < 8 ? w.nlse2 + qbase + 4 * lane : w.ndd + qbase + 4 * (lane - 8);
+      lds_dma16_opaque(src, base + kSlotL2);
+    }
+  };
+  static_assert(kDkvStages == 3, "two sequences ahead");
+  constexpr int P = 16 / kDkvWaves;   // loads per staged sequence; wavefront 0 has one more
   using Blk = typename KeyGrad<HD, NT>::Block;
-  auto fetch = [&](Blk& q, int s) {
-    const int ctx = __builtin_amdgcn_readlane(mctx, s - mbase);
+  // the sequence in use, the next two, and their lengths (read from the walk's
+  // window right after each step of it)
+  int s = prev(s1 - 1);
+  int sctx = s != none ? __builtin_amdgcn_readlane(mctx, s - mbase) : 0;
+  int sn = s != none ? prev(s - 1) : none;
+  int snctx = sn != none ? __builtin_amdgcn_readlane(mctx, sn - mbase) : 0;
+  if (s != none) stage_block(s, 0);
+  if (sn != none) stage_block(sn, 1);
+  for (int slot = 0; s != none; slot = slot == kDkvStages - 1 ? 0 : slot + 1) {
+    const int snn = sn != none ? prev(sn - 1) : none;
+    const int snnctx = snn != none ? __builtin_amdgcn_readlane(mctx, snn - mbase) : 0;
+    // this slot's loads are complete once at most the next sequence's remain
+    // in flight (loads complete in order); then the barrier publishes them
+    if (sn == none) wait_vm_lgkm_barrier<0>();
+    else if (wave == 0) wait_vm_lgkm_barrier<P + 1>();
+    else wait_vm_lgkm_barrier<P>();
+    // every wavefront is past its reads of the slot staged two sequences ago
+    if (snn != none) stage_block(snn, slot == 0 ? kDkvStages - 1 : slot - 1);
+    Blk q;
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      q.n0[t] = valid_keys(t, 0, ctx);
-      q.n1[t] = valid_keys(t, 1, ctx);
+      q.n0[t] = valid_keys(t, 0, sctx);
+      q.n1[t] = valid_keys(t, 1, sctx);
     }
-    q.load(w, (static_cast<int64_t>(seg) * a.S + s) * kNqp, lane);
-  };
-  for (int sa = prev(s1 - 1); sa != none; sa = prev(sa - 1)) {
-    Blk q;
-    fetch(q, sa);
-    kg.compute(q, kb, vb, lane);
+    if (q.n0[0] + q.n1[0] > 0) {   // the sequence reaches this wavefront's tile
+      KeyGrad<HD, NT>::load_lds(q, ring + slot * kSlotBytes, lane);
+      kg.compute(q, kb, vb, lane);
+    }
+    s = sn;
+    sctx = snctx;
+    sn = snn;
+    snctx = snnctx;
   }
-  // every key that some block of the group sees (keys past `reach` keep no gradient)
+  // every key that some sequence of the group sees (keys past `reach` keep no gradient)
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     const int64_t o0 = ((lay + id[t][0]) * a.Hkv + g) * pe, o1 = ((lay + id[t][1]) * a.Hkv + g) * pe;
@@ -543,29 +675,36 @@ __global__ __launch_bounds__(64, 2) void bwd_dkv_carry_kernel(BwdArgs b) {
 
 // -------------------------------------------------------------------- dq
 //
-// One wavefront per NQ consecutive sequences of a group (NQ = 2 when groups
-// share page rows: each committed tile is then loaded once for both) and
-// layer x KV head: the committed tiles through the page row, then each
-// sequence's carry tiles.  Keys are the MFMA rows here (permuted), query rows
-// the columns: lane l keeps query l % 32 of every sequence throughout.
+// One wavefront per NQ consecutive sequences of a group and layer x KV head:
+// the committed tiles of the page row, then each sequence's carry tiles.
+// Keys are the MFMA rows here (permuted), query rows the columns: lane l keeps
+// query l % 32 of every sequence throughout.
+//
+// NQ = 2 (groups that share page rows): the workgroup's kDkvWaves wavefronts
+// take 2 kDkvWaves consecutive sequences of one group, and every committed
+// tile (K rows, the key-major V copy, the K^T copy: 12 KiB) is staged once
+// per workgroup into an LDS ring slot by direct-to-LDS loads, two tiles ahead,
+// for all of them.  NQ = 1 (one sequence per group): the wavefront loads its
+// own tiles.
 template <int HD, int NQ>
-__global__ __launch_bounds__(64, NQ == 1 ? 3 : 2) void bwd_dq_kernel(BwdArgs b) {
+__device__ __forceinline__ void dq_role(const BwdArgs& b, int pair, int item, unsigned char* ring) {
   constexpr int KS = HD / 16, MT = HD / 32;
+  constexpr bool kStaged = NQ > 1;
+  static_assert(!kStaged || HD == 64, "ring slot layout");
   const AttnArgs& a = b.a;
   const BwdWs w = bwd_ws(b);
-  const int lane = threadIdx.x, r32 = lane & 31, h = lane >> 5;
+  const int lane = threadIdx.x & 63, r32 = lane & 31, h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int groups = (a.S + b.group - 1) / b.group;
-  int pair, item;
-  if (!xcd_item(groups * b.layer_count * a.Hkv, (b.group + NQ - 1) / NQ, &pair, &item)) return;
   const int grp = pair % groups, seg = pair / groups;
-  const int gend = min(a.S, (grp + 1) * b.group);
-  const int sfirst = grp * b.group + NQ * item;
-  if (sfirst >= gend) return;
+  const int gbeg = grp * b.group, gend = min(a.S, gbeg + b.group);
+  const int sfirst = gbeg + NQ * item;   // item < 0: a staging-only wavefront
+  if (!kStaged && sfirst >= gend) return;
   const int layer_local = seg / a.Hkv, g = seg % a.Hkv;
   const int G = a.Hq / a.Hkv, nq = a.B * G;
   const int64_t pe = static_cast<int64_t>(kPage) * HD;
   const int64_t lay = static_cast<int64_t>(a.layer_begin + layer_local);
-  const int32_t* lead = a.page_table + static_cast<int64_t>(grp * b.group) * a.max_pages;
+  const int32_t* lead = a.page_table + static_cast<int64_t>(gbeg) * a.max_pages;
   const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
   const uint16_t* kk = static_cast<const uint16_t*>(a.k_carry);
 
@@ -580,8 +719,8 @@ __global__ __launch_bounds__(64, NQ == 1 ? 3 : 2) void bwd_dq_kernel(BwdArgs b) 
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
     const int s = sfirst + q;
-    live[q] = s < gend;
-    const int sc = live[q] ? s : sfirst;
+    live[q] = item >= 0 && s < gend;
+    const int sc = live[q] ? s : gbeg;
     const int cr = a.ctx_len[sc], ur = a.carry_len[sc];
     const bool ok = live[q] && len_ok(a, cr, ur);
     if (live[q] && !ok && seg == 0 && lane == 0) set_status(a.status, CO_ERR_LENGTH);
@@ -595,17 +734,67 @@ __global__ __launch_bounds__(64, NQ == 1 ? 3 : 2) void bwd_dq_kernel(BwdArgs b) 
       qb[q][k] = *reinterpret_cast<const u16x8*>(w.qr + (qbase + r32) * HD + 16 * k + 8 * h);
       db[q][k] = *reinterpret_cast<const u16x8*>(w.don + (qbase + r32) * HD + 16 * k + 8 * h);
     }
-    l2[q] = w.lse2[qbase + r32];
-    dd[q] = w.dd[qbase + r32];
+    l2[q] = -w.nlse2[qbase + r32];
+    dd[q] = -w.ndd[qbase + r32];
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
       for (int r = 0; r < 16; ++r) dqt[q][m][r] = 0.f;
+    // a group's sequences read the group's page row: every page this sequence
+    // sees must be the lead's (checked once, lane-parallel)
+    if (b.group > 1 && live[q]) {
+      const int32_t* own = a.page_table + static_cast<int64_t>(s) * a.max_pages;
+      bool diff = false;
+      for (int p = lane; p < npc[q]; p += 64) diff = diff || own[p] != lead[p];
+      if (__ballot(diff) && lane == 0) set_status(a.status, CO_ERR_GROUP);
+    }
   }
 
   const int kp = perm23(r32);   // the key this lane's A rows hold
-  // one tile: S^T and dP^T with the keys permuted (A rows from K and the
-  // key-major V copy), then dQ^T += K^T dS^T for every sequence q with keys in it
+  // One tile given its fragments: S^T and dP^T with the keys permuted (A rows
+  // from K and the key-major V copy), then dQ^T += K^T dS^T for every
+  // sequence q with keys in it.
+  auto tile_math = [&](const u16x8 (&ka)[KS], const u16x8 (&va)[KS], const u16x8 (&kt)[MT][2],
+                       const int (&n0)[NQ], const int (&n1)[NQ]) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      if (n0[q] + n1[q] == 0) continue;
+      f32x16 sc, dp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.f;
+#pragma unroll
+      for (int k = 0; k < KS; ++k) {
+        sc = mfma32x32x16(ka[k], qb[q][k], sc);
+        dp = mfma32x32x16(va[k], db[q][k], dp);
+      }
+      // dS = P (dP - D); keys past the length (rows here) give 0, whatever
+      // their cache slots hold.  Most tiles are whole: no per-key test there.
+      float sv[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sv[r] = __builtin_amdgcn_exp2f(sc[r] - l2[q]) * (dp[r] - dd[q]);
+      if (n0[q] < kPage || n1[q] < kPage) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = acc_index(r, h);
+          if (key < 16 ? key >= n0[q] : key - 16 >= n1[q]) sv[r] = 0.f;
+        }
+      }
+      u16x8 sb[2];
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+        const float* v = sv + 8 * jj;
+        const u32x4v s4 = {cvt_pk_bf16(v[0], v[1]), cvt_pk_bf16(v[2], v[3]),
+                           cvt_pk_bf16(v[4], v[5]), cvt_pk_bf16(v[6], v[7])};
+        sb[jj] = __builtin_bit_cast(u16x8, s4);
+      }
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) dqt[q][m] = mfma32x32x16(kt[m][jj], sb[jj], dqt[q][m]);
+    }
+  };
+  // one tile from global memory (pages of K, the key-major V copy, the K^T copy)
   auto tile = [&](const uint16_t* k0, const uint16_t* k1, const uint16_t* v0, const uint16_t* v1,
                   const uint16_t* t0, const uint16_t* t1, const int (&n0)[NQ],
                   const int (&n1)[NQ]) {
@@ -624,71 +813,142 @@ __global__ __launch_bounds__(64, NQ == 1 ? 3 : 2) void bwd_dq_kernel(BwdArgs b) 
 #pragma unroll
       for (int jj = 0; jj < 2; ++jj)
         kt[m][jj] = *reinterpret_cast<const u16x8*>((jj ? t1 : t0) + (32 * m + r32) * kPage + 8 * h);
+    tile_math(ka, va, kt, n0, n1);
+  };
+  // valid keys of the committed tile j's two pages for sequence q
+  auto tile_keys = [&](int j, bool b0, bool b1, int (&n0)[NQ], int (&n1)[NQ]) {
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-      if (n0[q] + n1[q] == 0) continue;
-      f32x16 sc, dp;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.f;
-#pragma unroll
-      for (int k = 0; k < KS; ++k) {
-        sc = mfma32x32x16(ka[k], qb[q][k], sc);
-        dp = mfma32x32x16(va[k], db[q][k], dp);
-      }
-      u16x8 sb[2];
-#pragma unroll
-      for (int jj = 0; jj < 2; ++jj) {
-        float sv[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int r = 8 * jj + e;
-          const int key = acc_index(r, h);
-          const bool valid = key < 16 ? key < n0[q] : key - 16 < n1[q];
-          const float pr = valid ? __builtin_amdgcn_exp2f(sc[r] - l2[q]) : 0.f;
-          sv[e] = pr * (dp[r] - dd[q]);
-        }
-        typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
-        const u32x4v s4 = {cvt_pk_bf16(sv[0], sv[1]), cvt_pk_bf16(sv[2], sv[3]),
-                           cvt_pk_bf16(sv[4], sv[5]), cvt_pk_bf16(sv[6], sv[7])};
-        sb[jj] = __builtin_bit_cast(u16x8, s4);
-      }
-#pragma unroll
-      for (int m = 0; m < MT; ++m)
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) dqt[q][m] = mfma32x32x16(kt[m][jj], sb[jj], dqt[q][m]);
+      n0[q] = (b0 || 2 * j >= npc[q]) ? 0 : min(kPage, ctx[q] - 2 * j * kPage);
+      n1[q] = (b1 || 2 * j + 1 >= npc[q]) ? 0 : min(kPage, ctx[q] - (2 * j + 1) * kPage);
     }
   };
 
-  // committed tiles, from the first sequence's page row (the group's row)
-  const int32_t* pt = a.page_table + static_cast<int64_t>(sfirst) * a.max_pages;
-  const int nct_max = (npc_max + 1) / 2;
-  for (int j = 0; j < nct_max; ++j) {
-    const int p0 = 2 * j, p1 = min(2 * j + 1, npc_max - 1);
-    int id0 = pt[p0], id1 = pt[p1];
-    const bool b0 = id0 < 0 || id0 >= a.num_pages, b1 = id1 < 0 || id1 >= a.num_pages;
-    if ((b0 || b1) && lane == 0) set_status(a.status, CO_ERR_PAGE_RANGE);
-    int n0[NQ], n1[NQ];
+  if constexpr (kStaged) {
+    // the workgroup's committed tiles: up to the longest of its sequences
+    // (lanes 0-15 take the 16 sequences of the 8 wavefronts; every wavefront
+    // computes the same count, so all take the same barriers)
+    int wnpc = 0;
+    {
+      const int wq = lane / NQ, qq = lane % NQ;
+      const int it = item + wave - wq;   // the item of wavefront wq (items run down with wave)
+      const int s = gbeg + NQ * it + qq;
+      if (lane < NQ * kDkvWaves && it >= 0 && s < gend) {
+        const int cr = a.ctx_len[s], ur = a.carry_len[s];
+        if (len_ok(a, cr, ur)) wnpc = (cr + kPage - 1) / kPage;
+      }
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      n0[q] = (b0 || p0 >= npc[q]) ? 0 : min(kPage, ctx[q] - p0 * kPage);
-      n1[q] = (b1 || 2 * j + 1 >= npc[q]) ? 0 : min(kPage, ctx[q] - (2 * j + 1) * kPage);
-      if (b.group > 1 && live[q] && p0 < npc[q] && lane == 0) {
-        const int32_t* own = a.page_table + static_cast<int64_t>(sfirst + q) * a.max_pages;
-        if (own[p0] != lead[p0] || (2 * j + 1 < npc[q] && own[2 * j + 1] != lead[2 * j + 1]))
-          set_status(a.status, CO_ERR_GROUP);
+      for (int o = 1; o < 64; o <<= 1) wnpc = max(wnpc, __shfl_xor(wnpc, o));
+      wnpc = __builtin_amdgcn_readfirstlane(wnpc);
+    }
+    const int nct = (wnpc + 1) / 2;
+    // page ids of the lead row, 64 at a time as a lane vector; one copy for
+    // the staging (two tiles ahead) and one for the tiles in use
+    struct Ids {
+      int v = 0, c = -1;
+    } ahead, cur;
+    auto page_id = [&](Ids& ids, int p) {   // uniform p; loads 64 ids when p leaves them
+      if ((p >> 6) != ids.c) {
+        ids.c = p >> 6;
+        const int x = 64 * ids.c + lane;
+        ids.v = x < a.max_pages ? lead[x] : 0;
+      }
+      return __builtin_amdgcn_readlane(ids.v, p & 63);
+    };
+    // tile j into ring slot `slot`: twelve 1 KiB pieces (K rows, V rows, K^T
+    // rows), pieces wave and wave + 8 of this wavefront
+    auto stage_tile = [&](int j, int slot) {
+      const int p0 = 2 * j, p1 = min(2 * j + 1, wnpc - 1);
+      int id0 = page_id(ahead, p0), id1 = page_id(ahead, p1);
+      id0 = (id0 < 0 || id0 >= a.num_pages) ? 0 : id0;   // reported where the tile is used
+      id1 = (id1 < 0 || id1 >= a.num_pages) ? 0 : id1;
+      const uint32_t base = lds_addr(ring) + slot * kDqSlotBytes;
+      const uint16_t* kpg[2] = {kc + ((lay * a.num_pages + id0) * a.Hkv + g) * pe,
+                                kc + ((lay * a.num_pages + id1) * a.Hkv + g) * pe};
+      const int64_t w0 = ((static_cast<int64_t>(layer_local) * a.num_pages + id0) * a.Hkv + g) * pe;
+      const int64_t w1 = ((static_cast<int64_t>(layer_local) * a.num_pages + id1) * a.Hkv + g) * pe;
+#pragma unroll
+      for (int x = 0; x < (12 + kDkvWaves - 1) / kDkvWaves; ++x) {
+        const int piece = wave + kDkvWaves * x;
+        if (piece >= 12) break;
+        const int arr = piece >> 2, off = (piece & 3) * 1024 + 16 * lane;
+        const uint32_t dst = base + arr * 4096 + (piece & 3) * 1024;
+        if (arr < 2) {   // key rows [32][64]: row r is slot r % 16 of page r / 16
+          const int r = off / (2 * HD), c = ((off % (2 * HD)) >> 4) ^ swz_packed(r);
+          const uint16_t* src = arr == 0 ? kpg[r >> 4] : w.vn + (r >> 4 ? w1 : w0);
+          lds_dma16_opaque(src + (r & 15) * HD + c * 8, dst);
+        } else {         // K^T rows [64][32]: dims, the two pages' 16 keys side by side
+          const int d = off / (2 * kNqp), c = ((off % (2 * kNqp)) >> 4) ^ swz_trans(d);
+          lds_dma16_opaque(w.kt + (c >> 1 ? w1 : w0) + d * kPage + (c & 1) * 8, dst);
+        }
+      }
+    };
+    static_assert(kDqStages == 3 && kDkvWaves == 8, "two tiles ahead; 2 or 1 pieces per wavefront");
+    const bool two = wave < 12 - kDkvWaves;   // this wavefront stages two pieces per tile
+    if (nct > 0) stage_tile(0, 0);
+    if (nct > 1) stage_tile(1, 1);
+    for (int j = 0, slot = 0; j < nct; ++j, slot = slot == kDqStages - 1 ? 0 : slot + 1) {
+      // tile j's pieces are in once at most tile j + 1's remain in flight
+      // (loads complete in order); then the barrier publishes them
+      if (j + 1 >= nct) wait_vm_lgkm_barrier<0>();
+      else if (two) wait_vm_lgkm_barrier<2>();
+      else wait_vm_lgkm_barrier<1>();
+      // every wavefront is past its reads of the slot of tile j - 1
+      if (j + 2 < nct) stage_tile(j + 2, slot == 0 ? kDqStages - 1 : slot - 1);
+      const int p0 = 2 * j, p1 = min(2 * j + 1, wnpc - 1);
+      const int id0 = page_id(cur, p0), id1 = page_id(cur, p1);
+      const bool b0 = id0 < 0 || id0 >= a.num_pages, b1 = id1 < 0 || id1 >= a.num_pages;
+      if ((b0 || b1) && wave == 0 && lane == 0) set_status(a.status, CO_ERR_PAGE_RANGE);
+      int n0[NQ], n1[NQ];
+      tile_keys(j, b0, b1, n0, n1);
+      int any = 0;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) any += n0[q] + n1[q];
+      if (any > 0) {
+        const unsigned char* sl = ring + slot * kDqSlotBytes;
+        u16x8 ka[KS], va[KS], kt[MT][2];
+#pragma unroll
+        for (int k = 0; k < KS; ++k) {
+          const int off = kp * (2 * HD) + (((2 * k + h) ^ swz_packed(kp)) << 4);
+          ka[k] = *reinterpret_cast<const u16x8*>(sl + kDqSlotK + off);
+          va[k] = *reinterpret_cast<const u16x8*>(sl + kDqSlotV + off);
+        }
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj) {
+            const int d = 32 * m + r32;
+            const int off = d * (2 * kNqp) + (((2 * jj + h) ^ swz_trans(d)) << 4);
+            kt[m][jj] = *reinterpret_cast<const u16x8*>(sl + kDqSlotKt + off);
+          }
+        tile_math(ka, va, kt, n0, n1);
       }
     }
-    id0 = b0 ? 0 : id0;
-    id1 = b1 ? 0 : id1;
-    const int64_t c0 = ((lay * a.num_pages + id0) * a.Hkv + g) * pe;
-    const int64_t c1 = ((lay * a.num_pages + id1) * a.Hkv + g) * pe;
-    const int64_t w0 = ((static_cast<int64_t>(layer_local) * a.num_pages + id0) * a.Hkv + g) * pe;
-    const int64_t w1 = ((static_cast<int64_t>(layer_local) * a.num_pages + id1) * a.Hkv + g) * pe;
-    tile(kc + c0, kc + c1, w.vn + w0, w.vn + w1, w.kt + w0, w.kt + w1, n0, n1);
+    if (item < 0) return;   // after the last barrier
+  } else {
+    // committed tiles of the sequence's own page row (the group's row)
+    const int32_t* pt = a.page_table + static_cast<int64_t>(sfirst) * a.max_pages;
+    const int nct_max = (npc_max + 1) / 2;
+    for (int j = 0; j < nct_max; ++j) {
+      const int p0 = 2 * j, p1 = min(2 * j + 1, npc_max - 1);
+      int id0 = pt[p0], id1 = pt[p1];
+      const bool b0 = id0 < 0 || id0 >= a.num_pages, b1 = id1 < 0 || id1 >= a.num_pages;
+      if ((b0 || b1) && lane == 0) set_status(a.status, CO_ERR_PAGE_RANGE);
+      int n0[NQ], n1[NQ];
+      tile_keys(j, b0, b1, n0, n1);
+      id0 = b0 ? 0 : id0;
+      id1 = b1 ? 0 : id1;
+      const int64_t c0 = ((lay * a.num_pages + id0) * a.Hkv + g) * pe;
+      const int64_t c1 = ((lay * a.num_pages + id1) * a.Hkv + g) * pe;
+      const int64_t w0 = ((static_cast<int64_t>(layer_local) * a.num_pages + id0) * a.Hkv + g) * pe;
+      const int64_t w1 = ((static_cast<int64_t>(layer_local) * a.num_pages + id1) * a.Hkv + g) * pe;
+      tile(kc + c0, kc + c1, w.vn + w0, w.vn + w1, w.kt + w0, w.kt + w1, n0, n1);
+    }
   }
   // each sequence's carry tiles, against that sequence alone
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
+    if (!live[q]) continue;
     const int s = sfirst + q;
     const int ncp = (carry[q] + kPage - 1) / kPage;
     for (int cp0 = 0; cp0 < ncp; cp0 += 2) {
@@ -735,6 +995,47 @@ __global__ __launch_bounds__(64, NQ == 1 ? 3 : 2) void bwd_dq_kernel(BwdArgs b) 
   }
 }
 
+// ------------------------------------------------------------- dkv + dq
+//
+// One launch for both: workgroups [0, n_dkv) take the dkv step (one per
+// (pair, run of key tiles), longest runs first), the rest take dq, eight dq
+// wavefronts per workgroup, longest sequences first.  The dkv runs differ in
+// length by the number of sequences that see them (the first keys of a
+// response are seen by all its blocks, the last by few), and so do the dq
+// items; in one grid the dq workgroups start on the compute units that the
+// short dkv runs leave, so neither kernel's tail idles the chip.  n_dkv is a
+// multiple of 8, so a dq workgroup's XCD is (blockIdx - n_dkv) % 8 as well,
+// and the items of one pair stay on one XCD for both roles.
+template <int HD, int NQ>
+__global__ __launch_bounds__(64 * kDkvWaves, kDkvWaves / 4) void bwd_attn_kernel(BwdArgs b, int n_dkv) {
+  __shared__ __align__(16) unsigned char smem[kBwdSmem];   // the role's LDS ring
+  const AttnArgs& a = b.a;
+  const int groups = (a.S + b.group - 1) / b.group;
+  const int n_pairs = groups * b.layer_count * a.Hkv;
+  const int i = blockIdx.x;
+  if (i < n_dkv) {
+    const int units = ((a.max_pages + 1) / 2 + kDkvTiles * kDkvWaves - 1) / (kDkvTiles * kDkvWaves);
+    const int xcd = i & 7, k = i >> 3;
+    const int pair = xcd + 8 * (k / units);
+    if (pair < n_pairs) dkv_role<HD>(b, pair, k % units, smem);
+    return;
+  }
+  const int j = i - n_dkv, wave = threadIdx.x >> 6;
+  if (b.group == 1) {   // one dq wavefront per pair: eight pairs per workgroup
+    const int pair = kDkvWaves * j + wave;
+    if (pair < n_pairs) dq_role<HD, NQ>(b, pair, 0, smem);
+    return;
+  }
+  const int items = (b.group + NQ - 1) / NQ;             // dq wavefronts per pair
+  const int per = (items + kDkvWaves - 1) / kDkvWaves;   // dq workgroups per pair
+  const int xcd = j & 7, k = j >> 3;
+  const int pair = xcd + 8 * (k / per);
+  // all eight wavefronts take part (the staged tiles need every one of them);
+  // item < 0 marks one with no sequence of its own
+  const int item = items - 1 - ((k % per) * kDkvWaves + wave);
+  if (pair < n_pairs) dq_role<HD, NQ>(b, pair, item, smem);
+}
+
 }  // namespace
 
 size_t bwd_workspace_bytes(int S, int L, int Hkv, int hd, int num_pages, int CP) {
@@ -757,15 +1058,19 @@ hipError_t launch_attention_backward(const BwdArgs& b, hipStream_t stream) {
   hipLaunchKernelGGL(bwd_copy_kernel<64>, dim3(static_cast<unsigned>((items + 255) / 256)),
                      dim3(256), 0, stream, b);
   const int groups = (a.S + b.group - 1) / b.group;
-  const int units = ((a.max_pages + 1) / 2 + kDkvTiles - 1) / kDkvTiles;
+  const int units = ((a.max_pages + 1) / 2 + kDkvTiles * kDkvWaves - 1) / (kDkvTiles * kDkvWaves);
   const int xpairs = (groups * nseg + 7) / 8 * 8;   // pairs per launch, padded to the 8 XCDs
-  hipLaunchKernelGGL(bwd_dkv_kernel<64>, dim3(xpairs * units), dim3(64), 0, stream, b);
+  const int n_dkv = xpairs * units;
   hipLaunchKernelGGL(bwd_dkv_carry_kernel<64>, dim3(a.S, nseg), dim3(64), 0, stream, b);
-  if (b.group > 1)
-    hipLaunchKernelGGL((bwd_dq_kernel<64, 2>), dim3(xpairs * ((b.group + 1) / 2)), dim3(64), 0,
-                       stream, b);
-  else
-    hipLaunchKernelGGL((bwd_dq_kernel<64, 1>), dim3(xpairs), dim3(64), 0, stream, b);
+  if (b.group > 1) {
+    const int per = ((b.group + kDqSeqs - 1) / kDqSeqs + kDkvWaves - 1) / kDkvWaves;
+    hipLaunchKernelGGL((bwd_attn_kernel<64, kDqSeqs>), dim3(n_dkv + xpairs * per),
+                       dim3(64 * kDkvWaves), 0, stream, b, n_dkv);
+  } else {
+    const int dq_wgs = (groups * nseg + kDkvWaves - 1) / kDkvWaves;
+    hipLaunchKernelGGL((bwd_attn_kernel<64, 1>), dim3(n_dkv + dq_wgs), dim3(64 * kDkvWaves), 0,
+                       stream, b, n_dkv);
+  }
   return hipGetLastError();
 }
 
