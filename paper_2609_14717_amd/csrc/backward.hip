@@ -997,43 +997,47 @@ __device__ __forceinline__ void dq_role(const BwdArgs& b, int pair, int item, un
 
 // ------------------------------------------------------------- dkv + dq
 //
-// One launch for both: workgroups [0, n_dkv) take the dkv step (one per
-// (pair, run of key tiles), longest runs first), the rest take dq, eight dq
-// wavefronts per workgroup, longest sequences first.  The dkv runs differ in
-// length by the number of sequences that see them (the first keys of a
-// response are seen by all its blocks, the last by few), and so do the dq
-// items; in one grid the dq workgroups start on the compute units that the
-// short dkv runs leave, so neither kernel's tail idles the chip.  n_dkv is a
-// multiple of 8, so a dq workgroup's XCD is (blockIdx - n_dkv) % 8 as well,
-// and the items of one pair stay on one XCD for both roles.
+// One launch for both kinds of workgroup.  Both kinds of work shrink with
+// their rank r within a pair: dkv run r holds keys that fewer of the group's
+// sequences see, dq workgroup r holds shorter sequences (it takes items
+// items - 1 - (8 r + wave)).  Workgroups are dealt out by rank, the longest
+// first: round r holds dkv run r and dq workgroup r of every pair, so the
+// chip starts the longest work of both kinds at once and fills in with
+// shorter work as units free up.  Workgroup i runs on XCD i % 8, and the
+// pairs p with p % 8 == that XCD are the ones it takes, so all of a pair's
+// workgroups share one XCD's L2.  Groups of one sequence (no shared rows):
+// all dkv runs first, then one dq wavefront per pair.
 template <int HD, int NQ>
 __global__ __launch_bounds__(64 * kDkvWaves, kDkvWaves / 4) void bwd_attn_kernel(BwdArgs b, int n_dkv) {
   __shared__ __align__(16) unsigned char smem[kBwdSmem];   // the role's LDS ring
   const AttnArgs& a = b.a;
   const int groups = (a.S + b.group - 1) / b.group;
   const int n_pairs = groups * b.layer_count * a.Hkv;
-  const int i = blockIdx.x;
-  if (i < n_dkv) {
-    const int units = ((a.max_pages + 1) / 2 + kDkvTiles * kDkvWaves - 1) / (kDkvTiles * kDkvWaves);
-    const int xcd = i & 7, k = i >> 3;
-    const int pair = xcd + 8 * (k / units);
-    if (pair < n_pairs) dkv_role<HD>(b, pair, k % units, smem);
-    return;
-  }
-  const int j = i - n_dkv, wave = threadIdx.x >> 6;
-  if (b.group == 1) {   // one dq wavefront per pair: eight pairs per workgroup
-    const int pair = kDkvWaves * j + wave;
-    if (pair < n_pairs) dq_role<HD, NQ>(b, pair, 0, smem);
+  const int units = ((a.max_pages + 1) / 2 + kDkvTiles * kDkvWaves - 1) / (kDkvTiles * kDkvWaves);
+  const int i = blockIdx.x, xcd = i & 7, wave = threadIdx.x >> 6;
+  if (b.group == 1) {
+    if (i < n_dkv) {
+      const int k = i >> 3, pair = xcd + 8 * (k / units);
+      if (pair < n_pairs) dkv_role<HD>(b, pair, k % units, smem);
+    } else {   // eight pairs per workgroup
+      const int pair = kDkvWaves * (i - n_dkv) + wave;
+      if (pair < n_pairs) dq_role<HD, NQ>(b, pair, 0, smem);
+    }
     return;
   }
   const int items = (b.group + NQ - 1) / NQ;             // dq wavefronts per pair
   const int per = (items + kDkvWaves - 1) / kDkvWaves;   // dq workgroups per pair
-  const int xcd = j & 7, k = j >> 3;
-  const int pair = xcd + 8 * (k / per);
-  // all eight wavefronts take part (the staged tiles need every one of them);
-  // item < 0 marks one with no sequence of its own
-  const int item = items - 1 - ((k % per) * kDkvWaves + wave);
-  if (pair < n_pairs) dq_role<HD, NQ>(b, pair, item, smem);
+  const int ppx = (n_pairs + 7) / 8;                     // pairs per XCD
+  const int k = i >> 3, r = k / (2 * ppx), rem = k % (2 * ppx);
+  const int pair = xcd + 8 * (rem % ppx);
+  if (pair >= n_pairs) return;
+  if (rem < ppx) {
+    if (r < units) dkv_role<HD>(b, pair, r, smem);
+  } else if (r < per) {
+    // all eight wavefronts take part (the staged tiles need every one of
+    // them); item < 0 marks one with no sequence of its own
+    dq_role<HD, NQ>(b, pair, items - 1 - (r * kDkvWaves + wave), smem);
+  }
 }
 
 }  // namespace
@@ -1064,7 +1068,8 @@ hipError_t launch_attention_backward(const BwdArgs& b, hipStream_t stream) {
   hipLaunchKernelGGL(bwd_dkv_carry_kernel<64>, dim3(a.S, nseg), dim3(64), 0, stream, b);
   if (b.group > 1) {
     const int per = ((b.group + kDqSeqs - 1) / kDqSeqs + kDkvWaves - 1) / kDkvWaves;
-    hipLaunchKernelGGL((bwd_attn_kernel<64, kDqSeqs>), dim3(n_dkv + xpairs * per),
+    const int rounds = std::max(units, per);   // workgroups: 8 XCDs x 2 kinds x pairs per XCD
+    hipLaunchKernelGGL((bwd_attn_kernel<64, kDqSeqs>), dim3(16 * (xpairs / 8) * rounds),
                        dim3(64 * kDkvWaves), 0, stream, b, n_dkv);
   } else {
     const int dq_wgs = (groups * nseg + kDkvWaves - 1) / kDkvWaves;
