@@ -183,8 +183,8 @@ co_status validate_attention(const co_dims* d, int32_t layer_begin, int32_t laye
   return CO_OK;
 }
 
-co_status enqueue_route(const co_dims* dims, const int32_t* draft_tok, const int32_t* target_tok,
-                        uint32_t flags, co_state* state, const co_route* out, hipStream_t stream) {
+RouteArgs route_args(const co_dims* dims, const int32_t* draft_tok, const int32_t* target_tok,
+                     uint32_t flags, co_state* state, const co_route* out) {
   RouteArgs a{};
   a.S = dims->num_seqs;
   a.B = dims->block;
@@ -200,12 +200,16 @@ co_status enqueue_route(const co_dims* dims, const int32_t* draft_tok, const int
   a.row_pos = out->row_pos;
   a.row_dst = out->row_dst;
   a.status = state->status;
-  return hip_status(launch_route(a, stream));
+  return a;
 }
 
-co_status enqueue_project(const co_dims* dims, const co_weights* w, const void* hidden,
-                          const co_route* route, const co_state* state, void* ws,
-                          hipStream_t stream) {
+co_status enqueue_route(const co_dims* dims, const int32_t* draft_tok, const int32_t* target_tok,
+                        uint32_t flags, co_state* state, const co_route* out, hipStream_t stream) {
+  return hip_status(launch_route(route_args(dims, draft_tok, target_tok, flags, state, out), stream));
+}
+
+ProjectArgs project_args(const co_dims* dims, const co_weights* w, const void* hidden,
+                         const co_route* route, const co_state* state, void* ws) {
   ProjectArgs a{};
   a.M = dims->num_seqs * dims->block;
   a.Dcat = dims->feat_dim;
@@ -221,7 +225,14 @@ co_status enqueue_project(const co_dims* dims, const co_weights* w, const void* 
   a.dst = make_dest(dims, route, state);
   a.dst.knorm = w->k_norm;
   a.ws = ws;
-  return hip_status(launch_project(a, project_plan(dims), stream));
+  return a;
+}
+
+co_status enqueue_project(const co_dims* dims, const co_weights* w, const void* hidden,
+                          const co_route* route, const co_state* state, void* ws,
+                          hipStream_t stream) {
+  return hip_status(launch_project(project_args(dims, w, hidden, route, state, ws),
+                                   project_plan(dims), stream));
 }
 
 co_status do_attention(const co_dims* d, int32_t layer_begin, int32_t layer_count, const void* q,
@@ -547,9 +558,18 @@ co_status carryover_round(const co_dims* dims, const co_weights* w, const void* 
   if ((s = validate_attention(dims, 0, dims->num_layers, q, state, out, lse, attn_ws,
                               ws_bytes - pw)) != CO_OK)
     return s;
-  if ((s = enqueue_route(dims, draft_tok, target_tok, flags, state, scratch, stream)) != CO_OK)
+  // The route step rides in the F product's launch where that product does
+  // not read its descriptors (it then decides carried rows from the tokens);
+  // otherwise it is a launch of its own, before the projection.
+  ProjectArgs pa = project_args(dims, w, hidden, scratch, state, ws);
+  const ProjectPlan plan = project_plan(dims);
+  const RouteArgs ra = route_args(dims, draft_tok, target_tok, flags, state, scratch);
+  if (route_foldable(pa, plan)) {
+    pa.route = &ra;
+  } else if ((s = hip_status(launch_route(ra, stream))) != CO_OK) {
     return s;
-  if ((s = enqueue_project(dims, w, hidden, scratch, state, ws, stream)) != CO_OK) return s;
+  }
+  if ((s = hip_status(launch_project(pa, plan, stream))) != CO_OK) return s;
   return do_attention(dims, 0, dims->num_layers, q, state, out, lse, flags, attn_ws, stream);
 }
 

@@ -50,6 +50,9 @@ struct ProjectArgs {
   const float* znorm;   // RMS-norm gain of F's output [d], or null
   KvDest dst;
   void* ws;
+  // The round's route step, carried by the F product's launch (see
+  // route_foldable), or null: the route has already been enqueued.
+  const RouteArgs* route;
 };
 
 struct ProjectPlan {
@@ -60,6 +63,11 @@ struct ProjectPlan {
 };
 
 ProjectPlan plan_project(int M, int Dcat, int d, int n_kv, int hd, int dtype, int num_cus);
+
+// Whether launch_project can run the route step inside its first launch: the
+// F product then decides carried rows from the tokens itself, and the route's
+// descriptors are complete before the K/V product reads them.
+bool route_foldable(const ProjectArgs& a, const ProjectPlan& p);
 
 constexpr int kNormMaxCols = 16384;   // widest F output the RMS normalisation takes
 

@@ -23,6 +23,7 @@
 
 #include <type_traits>
 
+#include "co_route.h"
 #include "co_store.h"
 
 namespace co {
@@ -44,6 +45,11 @@ struct GemmArgs {
   int mode;
   int z_rows;              // Z mode: 0 every row, 1 rows that are not carry rows, 2 carry rows
   KvDest kv;
+  // route_blocks > 0 (bf16 tile kernel, Z mode): the launch also carries the
+  // round's route step, four sequences per extra workgroup row past the row
+  // tiles, and carried rows are decided from the tokens instead of row_dst
+  int route_blocks;
+  RouteArgs route;
 };
 
 // Whether Z row `dst` is written under the row selection of a Z pass (the
@@ -86,6 +92,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
+  const int row_tiles = (g.M + BM - 1) / BM;
+  if (static_cast<int>(blockIdx.y) >= row_tiles) {   // the route step: one wavefront per sequence
+    if (blockIdx.x == 0 && blockIdx.z == 0) {
+      const int s = (blockIdx.y - row_tiles) * 4 + wave;
+      if (s < g.route.S) route_sequence(g.route, s, lane);
+    }
+    return;
+  }
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
   const int kbeg = blockIdx.z * g.k_per_split;
   const int klen = min(g.K - kbeg, g.k_per_split);
@@ -102,7 +116,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g) {
   int rd_dst = 0, rd_pos = 0;
   if (need_rows) {
     const int r = min(m0 + (tid % BM), g.M - 1);
-    rd_dst = g.row_dst[r];
+    if (g.route_blocks > 0)   // the route runs beside this product: decide from the tokens
+      rd_dst = route_row_carried(g.route, r) ? -1 : 0;
+    else
+      rd_dst = g.row_dst[r];
     if (g.mode == kModeKV) rd_pos = g.kv.row_pos[r];
   }
 
@@ -1069,7 +1086,7 @@ constexpr int kTileBN[4] = {64, 128, 128, 128};
 template <bool HAS_E>
 hipError_t launch_gemm_bf16_t(const GemmArgs& g, int tile, int splits, hipStream_t stream) {
   const dim3 grid((g.N + kTileBN[tile] - 1) / kTileBN[tile],
-                  (g.M + kTileBM[tile] - 1) / kTileBM[tile], splits);
+                  (g.M + kTileBM[tile] - 1) / kTileBM[tile] + g.route_blocks, splits);
   switch (tile) {
     case 0: hipLaunchKernelGGL((gemm_bf16_kernel<16, 64, 1, 4, 4, HAS_E>), grid, dim3(256), 0, stream, g); break;
     case 1: hipLaunchKernelGGL((gemm_bf16_kernel<16, 128, 1, 4, 3, HAS_E>), grid, dim3(256), 0, stream, g); break;
@@ -1253,6 +1270,14 @@ ProjectPlan plan_project(int M, int Dcat, int d, int n_kv, int hd, int dtype, in
   return p;
 }
 
+bool route_foldable(const ProjectArgs& a, const ProjectPlan& p) {
+  const bool sep = a.wfc != nullptr;
+  const bool fused = !sep && a.znorm == nullptr && a.dst.knorm == nullptr && p.fused &&
+                     (a.fe != nullptr || a.e == nullptr);
+  return a.dtype == CO_DTYPE_BF16 && a.M > 0 && !sep && !fused && p.f_tile < kWide &&
+         p.f_split == 1;
+}
+
 hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_t stream) {
   if (a.M == 0) return hipSuccess;
   const int n_kv = 2 * a.dst.L * a.dst.Hkv * a.dst.hd;
@@ -1315,6 +1340,11 @@ hipError_t launch_project(const ProjectArgs& a, const ProjectPlan& p, hipStream_
   if (a.fe != nullptr && !sep) {   // F(E) folded beforehand: the GEMM carries no E
     f.e = nullptr;
     f.fe = a.fe;
+  }
+  if (a.route != nullptr) {
+    if (!route_foldable(a, p)) return hipErrorInvalidValue;   // the caller checks first
+    f.route = *a.route;
+    f.route_blocks = (a.route->S + 3) / 4;
   }
   f.k_per_split = split_len(a.Dcat, p.f_split, p.f_tile);
   f.mode = p.f_split > 1 ? kModePartial : kModeZ;
