@@ -19,10 +19,16 @@ using namespace co;
 
 namespace co {
 
-// Launch-shape overrides (carryover_set_tuning); -1 = automatic.
-static int64_t g_tuning[CO_TUNE_COUNT] = {-1, -1, -1, -1, -1, -1, -1};
+// Launch-shape overrides (carryover_set_tuning); -1 = automatic, for every knob.
+struct Tuning {
+  int64_t v[CO_TUNE_COUNT];
+  Tuning() {
+    for (int64_t& x : v) x = -1;
+  }
+};
+static Tuning g_tuning;
 
-int64_t tuning(int knob) { return knob >= 0 && knob < CO_TUNE_COUNT ? g_tuning[knob] : -1; }
+int64_t tuning(int knob) { return knob >= 0 && knob < CO_TUNE_COUNT ? g_tuning.v[knob] : -1; }
 
 }  // namespace co
 
@@ -621,7 +627,7 @@ co_status carryover_verify_sample(const co_dims* dims, int32_t vocab, const int3
 
 co_status carryover_set_tuning(int32_t knob, int64_t value) {
   if (knob < 0 || knob >= CO_TUNE_COUNT) return CO_ERR_INVALID_ARG;
-  g_tuning[knob] = value < 0 ? -1 : value;
+  g_tuning.v[knob] = value < 0 ? -1 : value;
   return CO_OK;
 }
 
