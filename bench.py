@@ -46,6 +46,10 @@ PROJ_SOURCES = [os.path.join(ROOT, "paper_2609_14717_amd", "csrc", f)
                 for f in ("project.hip", "co_device.h", "co_kernels.h", "co_store.h")]
 PROJ_KERNELS = ("gemm_bf16_kernel", "gemm_wide_kernel", "proj_fused_kernel", "epi_z_kernel",
                 "epi_kv_kernel", "z_norm_kernel", "gemm_f32_kernel")
+# the attention backward's kernels and sources (its MFMA counters, --only backward)
+BWD_SOURCES = [os.path.join(ROOT, "paper_2609_14717_amd", "csrc", f)
+               for f in ("backward.hip", "co_device.h", "co_kernels.h")]
+BWD_KERNELS = ("bwd_prep_kernel", "bwd_copy_kernel", "bwd_attn_kernel", "bwd_dkv_carry_kernel")
 ATTN_KERNELS = ("attn_bf16_kernel", "attn_wave_kernel", "attn_bf16_combine_kernel",
                 "attn_group_kernel", "attn_share_merge_kernel")
 ATTN_KERNELS_F32 = ("attn_f32_kernel", "attn_chunk_merge_kernel")
@@ -75,10 +79,12 @@ def parse():
                          "'--only projection' or '--only prefill' and exit")
     ap.add_argument("--bench-json", metavar="FILE",
                     help="the JSON line the profiled bench command printed (for the summaries)")
-    ap.add_argument("--only", choices=("projection", "prefill"),
+    ap.add_argument("--only", choices=("projection", "prefill", "backward"),
                     help="time only carryover_project_kv: the projection of a round's rows "
-                         "('projection'), or the whole context as one call ('prefill'); "
-                         "prints one JSON line (the run the MFMA counters are taken on)")
+                         "('projection'), or the whole context as one call ('prefill'); or, "
+                         "for the training-shaped workload, only the attention backward "
+                         "('backward'); prints one JSON line (the run the MFMA counters are "
+                         "taken on)")
     ap.add_argument("--command", default="", help="command recorded in a summary")
     return ap.parse_args()
 
@@ -137,12 +143,21 @@ def mfma_file(workload, only):
     return os.path.join(PROFILES, f"mfma_{workload}_{only}.txt")
 
 
+def mfma_scope(only):
+    """(call, kernels, sources digest key, sources) of an MFMA summary."""
+    if only == "backward":
+        return ("drafter_block_attention_backward", BWD_KERNELS, "backward_source_digest",
+                BWD_SOURCES)
+    return "carryover_project_kv", PROJ_KERNELS, "projection_source_digest", PROJ_SOURCES
+
+
 def recorded_mfma(workload, only):
-    """Counter figures of the projection call from the committed MFMA summary,
-    when it was taken on the same projection kernels; else None."""
+    """Counter figures of the call from the committed MFMA summary, when it was
+    taken on the same kernels; else None."""
     path = mfma_file(workload, only)
     vals = read_summary(path)
-    if not vals or vals.get("projection_source_digest") != source_digest(PROJ_SOURCES):
+    _, _, key, sources = mfma_scope(only)
+    if not vals or vals.get(key) != source_digest(sources):
         return None
     try:
         return {"file": os.path.relpath(path, ROOT),
@@ -259,11 +274,11 @@ MFMA_GAP_NS = 50_000_000   # the pause bench.py --only leaves before the calls i
 
 
 def summarize_mfma(args):
-    """MFMA counters of the projection call from a rocprofv3 --pmc run (with
-    --kernel-trace) of ``bench.py --only ...``: the projection-kernel
-    dispatches after the last pause of more than 50 ms are the warm-up and
-    timed calls (``bench.py --only`` pauses before them), all of the same
-    shape.  Per call: the MFMA busy share of the SIMD cycles (rocprofv3's
+    """MFMA counters of the projection call (or of the attention backward)
+    from a rocprofv3 --pmc run (with --kernel-trace) of ``bench.py --only
+    ...``: the call's kernel dispatches after the last pause of more than
+    50 ms are the warm-up and timed calls (``bench.py --only`` pauses before
+    them), all of the same shape.  Per call: the MFMA busy share of the SIMD cycles (rocprofv3's
     MfmaUtil, time-weighted over the dispatches), counted bf16 MFMA flops
     (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) against the algorithmic flops, and
     the counted rate over the call's event time."""
@@ -272,6 +287,7 @@ def summarize_mfma(args):
         raise SystemExit("--bench-json must give the JSON line of the profiled run")
     bj = load_bench_json(args.bench_json)
     only, ncalls = bj["only"], bj["calls"] + bj["warm"]
+    call_name, kernels, digest_key, sources = mfma_scope(only)
     files = glob.glob(os.path.join(args.summarize_mfma, "**", "*counter_collection.csv"),
                       recursive=True)
     if not files:
@@ -280,7 +296,7 @@ def summarize_mfma(args):
     for f in files:
         with open(f) as fh:
             for r in csv.DictReader(fh):
-                if not any(is_kernel(r["Kernel_Name"], k) for k in PROJ_KERNELS):
+                if not any(is_kernel(r["Kernel_Name"], k) for k in kernels):
                     continue
                 d = disp.setdefault(int(r["Dispatch_Id"]), {
                     "name": r["Kernel_Name"], "grid": int(r["Grid_Size"]),
@@ -309,9 +325,9 @@ def summarize_mfma(args):
     counted = sum(k["mops"] for k in kinds.values()) * 512.0 / ncalls
     ev_s = bj["avg_call_us"] / 1e6
     peak = MFMA_PEAK_TFLOPS["bf16"]
-    lines = [f"# MFMA counters of carryover_project_kv, workload {args.workload} ({only})",
+    lines = [f"# MFMA counters of {call_name}, workload {args.workload} ({only})",
              f"command (counter pass): {args.command}",
-             f"projection_source_digest: {source_digest(PROJ_SOURCES)}",
+             f"{digest_key}: {source_digest(sources)}",
              f"call: {bj['call']}",
              f"rows per call: {bj['rows']}",
              f"calls in the window: {ncalls} ({bj['warm']} warm-up + {bj['calls']} timed), "
@@ -925,9 +941,11 @@ def run_train(args, w):
             committed_call_us=pc * 1e6, block_call_us=pv * 1e6,
             rows_computed=w.S * w.seq_len + V * w.B)
 
+    if args.only == "backward":
+        return only_backward(args, torch, co, sc, w, stream)
     if args.only:
         if args.only != "projection":
-            raise SystemExit(f"{w.name}: only the projection can be timed alone")
+            raise SystemExit(f"{w.name}: only the projection or the backward can be timed alone")
         sc.forward()
         pause(torch)
         *_, res = projection_calls(args.steps)
@@ -995,11 +1013,32 @@ def run_train(args, w):
     print(json.dumps(result), flush=True)
 
 
-def train_backward(torch, co, sc, w, stream, n, args, aflops, prows):
-    """The training side of the same pass (Algorithm 2): the attention backward
-    from a seeded output gradient (the blocks of a response share its pages:
-    one group per response), then the projection backward of both projection
-    calls; each timed alone, and whole training steps (forward + backward)."""
+def only_backward(args, torch, co, sc, w, stream):
+    """``--only backward``: drafter_block_attention_backward alone, ``args.steps``
+    calls timed with HIP events after a forward (and 3 untimed calls)."""
+    sc.forward()
+    attn_bwd, _ = backward_calls(torch, co, sc, w)
+    attn_bwd()
+    V = w.S * w.anchors
+    keys = float(np.sum(sc.vst["ctx_len"].cpu().numpy().astype(np.int64) +
+                        sc.vst["carry_len"].cpu().numpy().astype(np.int64)))
+    aflops = attention_flops(w.replace(S=V), keys)
+    pause(torch)
+    sec = timed_calls(torch, stream, args.steps, attn_bwd)
+    if co.carryover_read_status(sc.vst):
+        raise RuntimeError("device status after the backward")
+    peak = MFMA_PEAK_TFLOPS[w.dtype]
+    flops = 2.5 * aflops   # S, dP, dV, dK, dQ: 10 hd flops per (query, key)
+    res = {"only": "backward", "call": "drafter_block_attention_backward (one group per response)",
+           "rows": V * w.B, "calls": args.steps, "warm": TIMED_WARM, "avg_call_us": sec * 1e6,
+           "flops_per_call": flops, "tflops": flops / sec / 1e12,
+           "mfma_frac": flops / sec / 1e12 / peak, "config": {"workload": w.name}}
+    print(json.dumps(res), flush=True)
+
+
+def backward_calls(torch, co, sc, w):
+    """(attention backward, projection backward) of the training-shaped pass as
+    closures over freshly zeroed gradient buffers and workspaces."""
     from synth import device as sdev
     from synth import workloads as wl
     V = w.S * w.anchors
@@ -1029,6 +1068,15 @@ def train_backward(torch, co, sc, w, stream, n, args, aflops, prows):
         co.carryover_project_kv_backward(sc.vdims, sc.W, sc.hidden, sc.vrt, dk, dv, dkc, dvc,
                                          dwf, dwkv, de, wsv)
 
+    return attn_bwd, proj_bwd
+
+
+def train_backward(torch, co, sc, w, stream, n, args, aflops, prows):
+    """The training side of the same pass (Algorithm 2): the attention backward
+    from a seeded output gradient (the blocks of a response share its pages:
+    one group per response), then the projection backward of both projection
+    calls; each timed alone, and whole training steps (forward + backward)."""
+    attn_bwd, proj_bwd = backward_calls(torch, co, sc, w)
     sc.forward()
     ab_s = timed_calls(torch, stream, n, attn_bwd, warm=TRAIN_ATTN_WARM)
     pb_s = timed_calls(torch, stream, n, proj_bwd)
@@ -1052,6 +1100,7 @@ def train_backward(torch, co, sc, w, stream, n, args, aflops, prows):
     pbfl = 2.0 * pf                          # Z again, dW_KV, dZ, dW_F
     peak = MFMA_PEAK_TFLOPS[w.dtype]
     return {"attention_call": "drafter_block_attention_backward (one group per response)",
+            "attention_counters": recorded_mfma(w.name, "backward"),
             "attention_call_us": ab_s * 1e6,
             "attention_algorithmic_flops": abfl,
             "attention_tflops": abfl / ab_s / 1e12,
