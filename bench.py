@@ -1096,7 +1096,7 @@ def train_backward(torch, co, sc, w, stream, n, args, aflops, prows):
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     abfl = 2.5 * aflops                      # S, dP, dV, dK, dQ: 10 hd flops per (query, key)
-    pf, _ = projection_work(w.replace(S=V), prows)
+    pf, _ = projection_work(w.replace(S=w.S * w.anchors), prows)
     pbfl = 2.0 * pf                          # Z again, dW_KV, dZ, dW_F
     peak = MFMA_PEAK_TFLOPS[w.dtype]
     return {"attention_call": "drafter_block_attention_backward (one group per response)",
