@@ -206,7 +206,10 @@ def summarize_pmc(args):
     def one(table, counter, name, window=None):
         """Sum over the kernels matching ``name`` of the mean per dispatch (over
         the window of dispatches if given), and the dispatches averaged."""
-        rows = [v for k, v in table.items() if k[1] == counter and name in k[0]]
+        # the plain instantiations only: the EXT ones (last template argument
+        # true) serve drafter_block_attention_ext, timed separately
+        rows = [v for k, v in table.items()
+                if k[1] == counter and name in k[0] and "true>" not in k[0]]
         if not rows:
             raise SystemExit(f"no {counter} rows for {name}")
         tot, cnt = 0.0, 0
