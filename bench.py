@@ -743,9 +743,30 @@ def main():
     result["variants"] = variants
     if prefill is not None:
         result["prefill_projection"] = prefill
+    add_measured_peaks(result, "hbm")
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w.replace(rounds=w.rounds), args.cpu_baseline_seconds)
     print(json.dumps(result), flush=True)
+
+
+def add_measured_peaks(result, bound):
+    """The achievable HBM read and bf16 MFMA rates measured on this device
+    (``synth.device.measured_peaks``), and the roofline and projection
+    fractions against them beside those against the spec peaks."""
+    from synth import device as sdev
+    mp = sdev.measured_peaks()
+    result["measured_peaks"] = mp
+    r = result["roofline"]
+    ref = mp["hbm_read_gbs"] if bound == "hbm" else mp["mfma_bf16_tflops"]
+    r["frac_of_measured"] = r["achieved"] / ref
+    if "cold" in r:
+        r["cold"]["frac_of_measured"] = r["cold"]["achieved"] / ref
+    p = result.get("projection")
+    if p and "tflops" in p:
+        p["mfma_frac_of_measured"] = p["tflops"] / mp["mfma_bf16_tflops"]
+    b = result.get("backward")
+    if b:
+        b["attention_mfma_frac_of_measured"] = b["attention_tflops"] / mp["mfma_bf16_tflops"]
 
 
 def variant_costs(torch, co, sc, w, lib, step, rewind, chain, args, stream, attend, q_last, lse,
@@ -1011,6 +1032,7 @@ def run_train(args, w):
         "projection": proj,
         "backward": backward,
     }
+    add_measured_peaks(result, "mfma")
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_baseline_seconds)
     print(json.dumps(result), flush=True)

@@ -39,7 +39,61 @@ def _load():
         _lib.synth_copy.restype = ctypes.c_int
         _lib.synth_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                     ctypes.c_void_p]
+        _lib.synth_read.restype = ctypes.c_int
+        _lib.synth_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int,
+                                    ctypes.c_void_p]
+        _lib.synth_mfma_loop.restype = ctypes.c_int
+        _lib.synth_mfma_loop.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                         ctypes.c_void_p]
     return _lib
+
+
+def measured_peaks(reps: int = 5):
+    """Achievable rates on this device, for fractions beside the spec peaks:
+    a streaming read of 4 GiB (past the 256 MB Infinity Cache; the best of a
+    few grid sizes) in GB/s, and the dense bf16 MFMA issue rate of register
+    operands on every SIMD in TFLOP/s; each the best of ``reps`` timed runs."""
+    import torch
+    lib = _load()
+    stream = torch.cuda.current_stream()
+    s = ctypes.c_void_p(stream.cuda_stream)
+    nbytes = 4 << 30
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    buf.fill_(1)
+
+    def timed(launch):
+        best = None
+        launch()
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            launch()
+            e1.record(stream)
+            e1.synchronize()
+            t = e0.elapsed_time(e1) / 1e3
+            best = t if best is None else min(best, t)
+        return best
+
+    read = 0.0
+    for blocks in (1024, 2048, 4096, 8192):
+        out = torch.empty(blocks * 256, dtype=torch.int32, device="cuda")
+
+        def launch(blocks=blocks, out=out):
+            if lib.synth_read(ctypes.c_void_p(buf.data_ptr()), nbytes, ctypes.c_void_p(out.data_ptr()),
+                              blocks, s) != 0:
+                raise RuntimeError("synth_read failed")
+        read = max(read, nbytes / timed(launch) / 1e9)
+    del buf
+    blocks, iters = 2048, 2048   # 2 wavefronts per SIMD on 256 CUs
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+
+    def mfma():
+        if lib.synth_mfma_loop(blocks, iters, ctypes.c_void_p(out.data_ptr()), s) != 0:
+            raise RuntimeError("synth_mfma_loop failed")
+    flops = blocks * 4 * iters * 8 * 32768.0
+    return {"hbm_read_gbs": read, "mfma_bf16_tflops": flops / timed(mfma) / 1e12,
+            "method": "best of 5: 4 GiB streaming read (16-byte loads, 1024-8192 workgroups); "
+                      "8 chains of v_mfma_f32_32x32x16_bf16 on registers, 8 wavefronts per CU"}
 
 
 def copy_bytes(dst, src, nbytes: int, stream=None):

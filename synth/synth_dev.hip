@@ -49,7 +49,68 @@ __global__ void copy16_kernel(const uint4* __restrict__ src, uint4* __restrict__
     dst[i] = src[i];
 }
 
+// Streaming read: every thread reads 16-byte vectors at a grid stride, four in
+// flight, and folds them into one word it stores at the end (so the reads are
+// kept): the reference for the achievable HBM read rate (a buffer well past
+// the 256 MB Infinity Cache).
+__global__ void read16_kernel(const uint4* __restrict__ src, int64_t n, uint32_t* __restrict__ out) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  uint32_t acc = 0;
+  int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  for (; i + 3 * stride < n; i += 4 * stride) {
+    const uint4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+    acc ^= a.x ^ a.y ^ a.z ^ a.w ^ b.x ^ b.y ^ b.z ^ b.w ^ c.x ^ c.y ^ c.z ^ c.w ^ d.x ^ d.y ^ d.z ^ d.w;
+  }
+  for (; i < n; i += stride) {
+    const uint4 a = src[i];
+    acc ^= a.x ^ a.y ^ a.z ^ a.w;
+  }
+  out[static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x] = acc;
+}
+
+// Dense bf16 MFMA issue rate: every wavefront runs `iters` rounds of eight
+// independent v_mfma_f32_32x32x16_bf16 chains on register operands and stores
+// one value of their sum: the reference for the achievable MFMA rate.
+typedef float mp_f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 mp_bf16x8 __attribute__((ext_vector_type(8)));
+__global__ __launch_bounds__(256) void mfma_loop_kernel(int iters, float seed, float* __restrict__ out) {
+  mp_bf16x8 a, b;
+  for (int i = 0; i < 8; ++i) {
+    a[i] = static_cast<__bf16>(seed * (threadIdx.x + i));
+    b[i] = static_cast<__bf16>(seed * (i - static_cast<int>(threadIdx.x)));
+  }
+  mp_f32x16 acc[8];
+  for (int c = 0; c < 8; ++c)
+    for (int r = 0; r < 16; ++r) acc[c][r] = 0.f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[c], 0, 0, 0);
+  }
+  float sum = 0.f;
+  for (int c = 0; c < 8; ++c)
+    for (int r = 0; r < 16; ++r) sum += acc[c][r];
+  out[static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x] = sum;
+}
+
 }  // namespace
+
+// Reads `bytes` (a multiple of 16) of src with `blocks` workgroups of 256
+// threads; out holds blocks * 256 words.
+extern "C" int synth_read(const void* src, int64_t bytes, void* out, int blocks, hipStream_t stream) {
+  if (!src || !out || bytes <= 0 || bytes % 16 || blocks <= 0) return 1;
+  hipLaunchKernelGGL(read16_kernel, dim3(blocks), dim3(256), 0, stream,
+                     static_cast<const uint4*>(src), bytes / 16, static_cast<uint32_t*>(out));
+  return hipGetLastError() == hipSuccess ? 0 : 2;
+}
+
+// `blocks` workgroups of four wavefronts, each wavefront 8 x iters MFMAs of
+// 32 x 32 x 16 (32768 flops each); out holds blocks * 256 floats.
+extern "C" int synth_mfma_loop(int blocks, int iters, void* out, hipStream_t stream) {
+  if (!out || blocks <= 0 || iters <= 0) return 1;
+  hipLaunchKernelGGL(mfma_loop_kernel, dim3(blocks), dim3(256), 0, stream, iters, 1e-3f,
+                     static_cast<float*>(out));
+  return hipGetLastError() == hipSuccess ? 0 : 2;
+}
 
 extern "C" int synth_copy(void* dst, const void* src, int64_t bytes, hipStream_t stream) {
   if (!dst || !src || bytes < 0 || bytes % 16) return 1;
