@@ -42,6 +42,8 @@ def _load():
         _lib.synth_read.restype = ctypes.c_int
         _lib.synth_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int,
                                     ctypes.c_void_p]
+        _lib.synth_empty.restype = ctypes.c_int
+        _lib.synth_empty.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
         _lib.synth_mfma_loop.restype = ctypes.c_int
         _lib.synth_mfma_loop.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
                                          ctypes.c_void_p]
@@ -91,9 +93,17 @@ def measured_peaks(reps: int = 5):
         if lib.synth_mfma_loop(blocks, iters, ctypes.c_void_p(out.data_ptr()), s) != 0:
             raise RuntimeError("synth_mfma_loop failed")
     flops = blocks * 4 * iters * 8 * 32768.0
-    return {"hbm_read_gbs": read, "mfma_bf16_tflops": flops / timed(mfma) / 1e12,
+    mfma_tf = flops / timed(mfma) / 1e12
+
+    def empties():   # 200 back-to-back launches of an empty 256-workgroup kernel
+        for _ in range(200):
+            if lib.synth_empty(256, ctypes.c_void_p(out.data_ptr()), s) != 0:
+                raise RuntimeError("synth_empty failed")
+    launch_us = timed(empties) / 200 * 1e6
+    return {"hbm_read_gbs": read, "mfma_bf16_tflops": mfma_tf, "kernel_launch_us": launch_us,
             "method": "best of 5: 4 GiB streaming read (16-byte loads, 1024-8192 workgroups); "
-                      "8 chains of v_mfma_f32_32x32x16_bf16 on registers, 8 wavefronts per CU"}
+                      "8 chains of v_mfma_f32_32x32x16_bf16 on registers, 8 wavefronts per CU; "
+                      "200 back-to-back launches of an empty kernel"}
 
 
 def copy_bytes(dst, src, nbytes: int, stream=None):
