@@ -145,6 +145,11 @@ AttnPlan attention_plan(const co_dims* d) {
 
 co_status hip_status(hipError_t e) { return e == hipSuccess ? CO_OK : CO_ERR_HIP; }
 
+// The launch functions report hipGetLastError() after their launches; an
+// error left by an earlier, unrelated HIP call on this thread is cleared
+// first, so that a call reports only the failures of its own launches.
+void clear_stale_error() { (void)hipGetLastError(); }
+
 // Host checks of each step, shared by the step's own entry point and by
 // carryover_round, which makes all of them before its first launch.  dims are
 // already checked.
@@ -211,7 +216,9 @@ RouteArgs route_args(const co_dims* dims, const int32_t* draft_tok, const int32_
 
 co_status enqueue_route(const co_dims* dims, const int32_t* draft_tok, const int32_t* target_tok,
                         uint32_t flags, co_state* state, const co_route* out, hipStream_t stream) {
-  return hip_status(launch_route(route_args(dims, draft_tok, target_tok, flags, state, out), stream));
+  clear_stale_error();
+  return hip_status(
+      launch_route(route_args(dims, draft_tok, target_tok, flags, state, out), stream));
 }
 
 ProjectArgs project_args(const co_dims* dims, const co_weights* w, const void* hidden,
@@ -237,6 +244,7 @@ ProjectArgs project_args(const co_dims* dims, const co_weights* w, const void* h
 co_status enqueue_project(const co_dims* dims, const co_weights* w, const void* hidden,
                           const co_route* route, const co_state* state, void* ws,
                           hipStream_t stream) {
+  clear_stale_error();
   return hip_status(launch_project(project_args(dims, w, hidden, route, state, ws),
                                    project_plan(dims), stream));
 }
@@ -275,6 +283,7 @@ co_status do_attention(const co_dims* d, int32_t layer_begin, int32_t layer_coun
   a.lse = lse;
   a.status = st->status;
   a.ws = static_cast<float*>(ws);
+  clear_stale_error();
   return hip_status(launch_attention(a, attention_plan(d), layer_count, stream));
 }
 
@@ -328,6 +337,7 @@ co_status carryover_fold_e(const co_dims* dims, const co_weights* w, float* f_e,
   if (!w || !w->w_f || !w->e_carry || !f_e || !aligned(w->w_f, 16) || !aligned(w->e_carry, 16) ||
       !aligned(f_e, 16))
     return CO_ERR_INVALID_ARG;
+  clear_stale_error();
   return hip_status(launch_fold_e(w->w_f, w->e_carry, dims->model_dim, dims->feat_dim,
                                   dims->dtype, f_e, stream));
 }
@@ -434,6 +444,7 @@ co_status drafter_block_attention_backward(
   b.d_v_cache = d_v_cache;
   b.d_k_carry = d_k_carry;
   b.d_v_carry = d_v_carry;
+  clear_stale_error();
   return hip_status(launch_attention_backward(b, stream));
 }
 
@@ -484,6 +495,7 @@ co_status carryover_project_kv_backward(const co_dims* dims, const co_weights* w
   a.dwkv = d_w_kv;
   a.de = d_e_carry;
   a.ws = ws;
+  clear_stale_error();
   return hip_status(launch_project_backward(a, stream));
 }
 
@@ -516,6 +528,7 @@ co_status drafter_carry_mass(const co_dims* dims, int32_t layer_begin, int32_t l
   a.lse = lse;
   a.mass = mass;
   a.status = state->status;
+  clear_stale_error();
   return hip_status(launch_carry_mass(a, layer_count, dims->dtype, stream));
 }
 
@@ -547,6 +560,7 @@ co_status drafter_self_merge(const co_dims* dims, int32_t layer_begin, int32_t l
   a.out = out;
   a.lse = lse;
   a.status = state->status;
+  clear_stale_error();
   return hip_status(launch_self_merge(a, layer_count, dims->dtype, stream));
 }
 
@@ -570,6 +584,7 @@ co_status carryover_round(const co_dims* dims, const co_weights* w, const void* 
   ProjectArgs pa = project_args(dims, w, hidden, scratch, state, ws);
   const ProjectPlan plan = project_plan(dims);
   const RouteArgs ra = route_args(dims, draft_tok, target_tok, flags, state, scratch);
+  clear_stale_error();
   if (route_foldable(pa, plan)) {
     pa.route = &ra;
   } else if ((s = hip_status(launch_route(ra, stream))) != CO_OK) {
@@ -622,6 +637,7 @@ co_status carryover_verify_sample(const co_dims* dims, int32_t vocab, const int3
   a.accept_len = accept_len;
   a.next_tok = next_tok;
   a.status = status;
+  clear_stale_error();
   return hip_status(launch_verify(a, stream));
 }
 
@@ -641,6 +657,7 @@ co_status carryover_import_kv(const co_dims* dims, int32_t seq, int32_t pos0, in
       static_cast<int64_t>(pos0) + n_rows > static_cast<int64_t>(dims->max_pages_per_seq) * kPage)
     return CO_ERR_INVALID_ARG;
   const KvDest e = make_dest(dims, nullptr, state);
+  clear_stale_error();
   return hip_status(launch_import(e, dims->dtype, seq, pos0, n_rows, k_rows, v_rows,
                                   state->page_table, dims->max_pages_per_seq, stream));
 }

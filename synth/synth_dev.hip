@@ -103,6 +103,7 @@ __global__ void empty_kernel(int* out) {
 
 extern "C" int synth_empty(int blocks, void* out, hipStream_t stream) {
   if (!out || blocks <= 0) return 1;
+  (void)hipGetLastError();   // an earlier call's error is not this launch's
   hipLaunchKernelGGL(empty_kernel, dim3(blocks), dim3(256), 0, stream, static_cast<int*>(out));
   return hipGetLastError() == hipSuccess ? 0 : 2;
 }
@@ -111,6 +112,7 @@ extern "C" int synth_empty(int blocks, void* out, hipStream_t stream) {
 // threads; out holds blocks * 256 words.
 extern "C" int synth_read(const void* src, int64_t bytes, void* out, int blocks, hipStream_t stream) {
   if (!src || !out || bytes <= 0 || bytes % 16 || blocks <= 0) return 1;
+  (void)hipGetLastError();   // an earlier call's error is not this launch's
   hipLaunchKernelGGL(read16_kernel, dim3(blocks), dim3(256), 0, stream,
                      static_cast<const uint4*>(src), bytes / 16, static_cast<uint32_t*>(out));
   return hipGetLastError() == hipSuccess ? 0 : 2;
@@ -120,6 +122,7 @@ extern "C" int synth_read(const void* src, int64_t bytes, void* out, int blocks,
 // 32 x 32 x 16 (32768 flops each); out holds blocks * 256 floats.
 extern "C" int synth_mfma_loop(int blocks, int iters, void* out, hipStream_t stream) {
   if (!out || blocks <= 0 || iters <= 0) return 1;
+  (void)hipGetLastError();   // an earlier call's error is not this launch's
   hipLaunchKernelGGL(mfma_loop_kernel, dim3(blocks), dim3(256), 0, stream, iters, 1e-3f,
                      static_cast<float*>(out));
   return hipGetLastError() == hipSuccess ? 0 : 2;
@@ -131,6 +134,7 @@ extern "C" int synth_copy(void* dst, const void* src, int64_t bytes, hipStream_t
   if (n == 0) return 0;
   const int64_t want = (n + 255) / 256;
   const unsigned blocks = static_cast<unsigned>(want < 8192 ? want : 8192);
+  (void)hipGetLastError();   // an earlier call's error is not this launch's
   hipLaunchKernelGGL(copy16_kernel, dim3(blocks), dim3(256), 0, stream,
                      static_cast<const uint4*>(src), static_cast<uint4*>(dst), n);
   return hipGetLastError() == hipSuccess ? 0 : 2;
@@ -150,6 +154,7 @@ extern "C" int synth_fill_normal(void* out, int bf16, int ndim, const int64_t* s
     n *= shape[k];
   }
   const int64_t blocks = (n + 255) / 256;
+  (void)hipGetLastError();   // an earlier call's error is not this launch's
   hipLaunchKernelGGL(fill_normal_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream,
                      out, bf16, n, lay, base, key, scale);
   return hipGetLastError() == hipSuccess ? 0 : 2;
