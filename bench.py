@@ -456,8 +456,10 @@ TIMED_WARM = 3      # untimed calls before the timed ones in timed_calls
 
 
 def timed_calls(torch, stream, n, call, warm=TIMED_WARM, between=None):
-    """Average duration (s) of ``call`` over n calls, each bracketed by HIP events
-    recorded on ``stream``; ``between`` (untimed) runs before each call."""
+    """Duration (s) of ``call``: n calls, each bracketed by HIP events recorded
+    on ``stream`` (``between``, untimed, runs before each), split into 5
+    consecutive repeats; the median of the repeats' means (the plain mean
+    below 5 calls)."""
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(n)]
     for _ in range(warm):
@@ -469,7 +471,10 @@ def timed_calls(torch, stream, n, call, warm=TIMED_WARM, between=None):
         call()
         b.record(stream)
     torch.cuda.synchronize()
-    return float(np.mean([a.elapsed_time(b) for a, b in ev])) / 1e3
+    t = np.array([a.elapsed_time(b) for a, b in ev]) / 1e3
+    if len(t) < 5:
+        return float(np.mean(t))
+    return float(np.median([np.mean(r) for r in np.array_split(t, 5)]))
 
 
 def projection_result(w, flops, nbytes, sec, rows=None):
