@@ -381,7 +381,9 @@ def summarize_stats(args):
     for n, c, a, lo, hi, pct in rows:
         short = n if len(n) <= 90 else n[:87] + "..."
         lines.append(f"{short:90s} {c:6d} {a:8.2f} {lo:8.2f} {hi:8.2f} {pct:6.2f}")
-    att = [(k, r) for k in ATTN_KERNELS for r in rows if is_kernel(r[0], k)]
+    # the plain instantiations (the EXT ones, last template argument true, serve
+    # drafter_block_attention_ext)
+    att = [(k, r) for k in ATTN_KERNELS for r in rows if is_kernel(r[0], k) and "true>" not in r[0]]
     if att:
         lines += ["", "drafter_block_attention, all dispatches = " + " + ".join(
             f"{k} {r[2]:.2f} us" for k, r in att) +
@@ -395,7 +397,7 @@ def summarize_stats(args):
         with open(trace) as fh:
             for r in csv.DictReader(fh):
                 for k, _ in att:
-                    if is_kernel(r["Kernel_Name"], k):
+                    if is_kernel(r["Kernel_Name"], k) and "true>" not in r["Kernel_Name"]:
                         per.setdefault(k, []).append(
                             (int(r["Dispatch_Id"]),
                              (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3))
