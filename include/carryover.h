@@ -454,7 +454,7 @@ co_status carryover_read_status(const co_state* state, int32_t* host_out, hipStr
  * variant.  Results never depend on them (beyond rounding order).  `value`
  * -1 restores the automatic choice.  Process-wide: set them while no call is
  * in flight.  Knobs:
- *   CO_TUNE_GEMM_WIDE_VARIANT       large-tile projection GEMM variant 0..5
+ *   CO_TUNE_GEMM_WIDE_VARIANT       large-tile projection GEMM variant 0..6
  *   CO_TUNE_GEMM_NO_WIDE            1: never the large-tile projection GEMM
  *   CO_TUNE_PROJECT_FUSED_MIN_ROWS  rows from which the fused small-width
  *                                   projection runs (default 4096)

@@ -1105,9 +1105,10 @@ hipError_t launch_gemm_bf16_t(const GemmArgs& g, int tile, int splits, hipStream
 // shape (same tiles, same results bit for bit).
 //   0: 256 x 256, BK 32 x 4   1: 256 x 128, BK 32 x 4   2: 128 x 256, BK 32 x 4
 //   3: 256 x 256, BK 64 x 2   4: 256 x 128, BK 64 x 3   5: 128 x 256, BK 64 x 3
-constexpr int kWide = 4, kWideVariants = 6;
-constexpr int kWideBM[kWideVariants] = {256, 256, 128, 256, 256, 128};
-constexpr int kWideBN[kWideVariants] = {256, 128, 256, 256, 128, 256};
+//   6: 128 x 128, BK 64 x 4 (enough workgroups for the K/V product without a K split)
+constexpr int kWide = 4, kWideVariants = 7;
+constexpr int kWideBM[kWideVariants] = {256, 256, 128, 256, 256, 128, 128};
+constexpr int kWideBN[kWideVariants] = {256, 128, 256, 256, 128, 256, 128};
 
 template <bool HAS_E>
 hipError_t launch_gemm_wide_t(const GemmArgs& g, int variant, int splits, hipStream_t stream) {
@@ -1123,7 +1124,8 @@ hipError_t launch_gemm_wide_t(const GemmArgs& g, int variant, int splits, hipStr
     case 2: hipLaunchKernelGGL((gemm_wide_kernel<2, 2 * X, 32, 4, HAS_E, W>), grid, block, 0, stream, g, tm, tn); break;
     case 3: hipLaunchKernelGGL((gemm_wide_kernel<4, 2 * X, 64, 2, HAS_E, W>), grid, block, 0, stream, g, tm, tn); break;
     case 4: hipLaunchKernelGGL((gemm_wide_kernel<4, X, 64, 3, HAS_E, W>), grid, block, 0, stream, g, tm, tn); break;
-    default: hipLaunchKernelGGL((gemm_wide_kernel<2, 2 * X, 64, 3, HAS_E, W>), grid, block, 0, stream, g, tm, tn); break;
+    case 5: hipLaunchKernelGGL((gemm_wide_kernel<2, 2 * X, 64, 3, HAS_E, W>), grid, block, 0, stream, g, tm, tn); break;
+    default: hipLaunchKernelGGL((gemm_wide_kernel<2, X, 64, 4, HAS_E, W>), grid, block, 0, stream, g, tm, tn); break;
   }
   return hipGetLastError();
 }
@@ -1158,7 +1160,7 @@ int pick_split(int M, int N, int K, int tile, int num_cus) {
 // K-split with the least estimated time, counting whole waves of workgroups at
 // a per-CU MFMA rate (the 256 x 256 tile reads LDS least per flop) plus the
 // fp32 partials that a split writes and reads back.  Returns false when no
-// choice fills at least half of the CUs.  CO_GEMM_WIDE_VARIANT=v restricts
+// choice fills at least half of the CUs.  CO_TUNE_GEMM_WIDE_VARIANT = v restricts
 // the choice to variant v at any size from 256 rows (tests and tuning).
 // K elements per split: the stage depth of the tile variant divides it.
 int split_len(int K, int split, int tile) {
@@ -1166,7 +1168,7 @@ int split_len(int K, int split, int tile) {
   return ((K + split - 1) / split + bk - 1) / bk * bk;
 }
 
-bool pick_wide(int M, int N, int K, int num_cus, int* tile, int* split) {
+bool pick_wide(int M, int N, int K, bool kv, int num_cus, int* tile, int* split) {
   if (M < 256 || K % 64 != 0) return false;
   double best = 1e30;
   int bv = -1, bs = 1;
@@ -1178,7 +1180,7 @@ bool pick_wide(int M, int N, int K, int num_cus, int* tile, int* split) {
     // relative main-loop rates measured on MI355X, each variant timed alone at
     // the projection shapes (the 64-deep stages and the square tile move the
     // fewest bytes per flop through LDS)
-    constexpr double kEff[kWideVariants] = {0.98, 0.8, 0.8, 1.0, 0.86, 0.87};
+    constexpr double kEff[kWideVariants] = {0.98, 0.8, 0.8, 1.0, 0.86, 0.87, 0.86};
     const double eff = kEff[v];
     for (int s = 1; s <= 16; ++s) {
       const int kps = split_len(K, s, kWide + v);
@@ -1192,8 +1194,11 @@ bool pick_wide(int M, int N, int K, int num_cus, int* tile, int* split) {
                             (4.5e12 * eff);
       const double t_hbm = static_cast<double>((M + kWideBM[v] - 1) / kWideBM[v]) * N * K * 2.0 / 6.0e12;
       // split partials: their stores overlap the main loop; the epilogue kernel
-      // reads them back
-      const double t_part = s > 1 ? static_cast<double>(s) * M * N * 4.0 / 5.0e12 + 2e-6 : 0.0;
+      // reads them back (the K/V epilogue, with its rotation and page scatter,
+      // measured at about half the rate of the Z epilogue)
+      const double t_part = s > 1 ? static_cast<double>(s) * M * N * 4.0 / (kv ? 2.5e12 : 5.0e12) +
+                                        (kv ? 4e-6 : 2e-6)
+                                  : 0.0;
       const double t = (t_mfma > t_hbm ? t_mfma : t_hbm) + t_part;
       if (t < best) {
         best = t;
@@ -1209,7 +1214,7 @@ bool pick_wide(int M, int N, int K, int num_cus, int* tile, int* split) {
 }
 
 void pick_gemm(int M, int N, int K, bool kv, int hd, int num_cus, int* tile, int* split) {
-  if (tuning(CO_TUNE_GEMM_NO_WIDE) <= 0 && pick_wide(M, N, K, num_cus, tile, split)) return;
+  if (tuning(CO_TUNE_GEMM_NO_WIDE) <= 0 && pick_wide(M, N, K, kv, num_cus, tile, split)) return;
   const int narrow = (!kv || hd == 64) ? 0 : 1;
   int cand[3], nc = 0;
   if (M > 64) cand[nc++] = 3;

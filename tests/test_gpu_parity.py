@@ -93,7 +93,7 @@ WIDE128 = wl.Workload("wide_hd128", S=16, B=16, Dcat=1536, d=512, L=1, Hq=8, Hkv
 
 
 @pytest.mark.parametrize("fold", [True, False], ids=["folded", "in_kernel"])
-@pytest.mark.parametrize("variant", range(6), ids=lambda v: f"v{v}")
+@pytest.mark.parametrize("variant", range(7), ids=lambda v: f"v{v}")
 @pytest.mark.parametrize("w", [WIDE64, WIDE128], ids=lambda w: w.name)
 def test_wide_gemm_variants(w, variant, fold, tune):
     tune("gemm_wide_variant", variant)
