@@ -1096,6 +1096,7 @@ namespace co {
 namespace {
 
 constexpr int kRowPad = 256;
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
 struct PbWs {
   float *fe, *u, *upart, *t32, *part;
@@ -1210,19 +1211,35 @@ __global__ __launch_bounds__(256) void pb_gather_kernel(ProjBwdArgs a, uint16_t*
   row[jv + half] = f2bf(vhi);
 }
 
-// Z^T (fp32 [d][M]) + F E on carried rows -> bf16 [d][Mp], padding rows zero.
+// Z^T (fp32 [d][M]) + F E on carried rows -> bf16 [d][Mp], padding rows zero:
+// four rows per thread, with 16-byte loads where M is a multiple of 4.  Mp is a
+// multiple of 4.
 __global__ __launch_bounds__(256) void pb_zt_kernel(const float* t32, int d, int M, int Mp,
                                                     const int32_t* row_dst, const float* fe,
                                                     uint16_t* ztb) {
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t idx = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
   if (idx >= static_cast<int64_t>(d) * Mp) return;
-  const int r = static_cast<int>(idx % Mp), dd = static_cast<int>(idx / Mp);
-  float v = 0.f;
-  if (r < M) {
-    const int32_t dst = row_dst[r];
-    v = t32[static_cast<int64_t>(dd) * M + r] + ((dst < 0 && dst != kSkip) ? fe[dd] : 0.f);
+  const int r0 = static_cast<int>(idx % Mp), dd = static_cast<int>(idx / Mp);
+  const float* src = t32 + static_cast<int64_t>(dd) * M + r0;
+  f32x4 v = {0.f, 0.f, 0.f, 0.f};
+  int32_t dst[4] = {kSkip, kSkip, kSkip, kSkip};
+  if (r0 + 4 <= M && (M & 3) == 0) {
+    v = *reinterpret_cast<const f32x4*>(src);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) dst[e] = row_dst[r0 + e];
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (r0 + e < M) {
+        v[e] = src[e];
+        dst[e] = row_dst[r0 + e];
+      }
   }
-  ztb[idx] = f2bf(v);
+  const float f = fe[dd];
+  u16x4 o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) o[e] = f2bf(v[e] + ((dst[e] < 0 && dst[e] != kSkip) ? f : 0.f));
+  *reinterpret_cast<u16x4*>(ztb + idx) = o;
 }
 
 // dZ^T (fp32 [d][Mp]) -> bf16, and per (dd, chunk of 2048 rows) the sum over
@@ -1247,14 +1264,24 @@ __global__ __launch_bounds__(256) void pb_dz_kernel(const float* t32, int M, int
       o[4 + e] = f2bf(b[e]);
     }
     *reinterpret_cast<u16x8*>(dztb + static_cast<int64_t>(dd) * Mp + r0) = o;
+    int32_t x[8];
+    // two 16-byte loads when the eight rows exist and the array is 16-byte
+    // aligned (r0 is a multiple of 8)
+    if (r0 + 8 <= M && (reinterpret_cast<uintptr_t>(row_dst) & 15) == 0) {
+      const i32x4 x0 = *reinterpret_cast<const i32x4*>(row_dst + r0);
+      const i32x4 x1 = *reinterpret_cast<const i32x4*>(row_dst + r0 + 4);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int r = r0 + e;
-      if (r < M) {
-        const int32_t x = row_dst[r];
-        if (x < 0 && x != kSkip) acc += e < 4 ? a[e] : b[e - 4];
+      for (int e = 0; e < 4; ++e) {
+        x[e] = x0[e];
+        x[4 + e] = x1[e];
       }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = r0 + e < M ? row_dst[r0 + e] : kSkip;
     }
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (x[e] < 0 && x[e] != kSkip) acc += e < 4 ? a[e] : b[e - 4];
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
@@ -1338,7 +1365,7 @@ hipError_t launch_project_backward(const ProjBwdArgs& a, hipStream_t stream) {
                              stream)) != hipSuccess)
     return err;
   const int64_t dm = static_cast<int64_t>(a.d) * Mp;
-  hipLaunchKernelGGL(pb_zt_kernel, dim3(static_cast<unsigned>((dm + 255) / 256)), dim3(256), 0,
+  hipLaunchKernelGGL(pb_zt_kernel, dim3(static_cast<unsigned>((dm / 4 + 255) / 256)), dim3(256), 0,
                      stream, w.t32, a.d, a.M, Mp, a.row_dst, w.fe, w.ztb);
   // dW_KV += dJ^T Z
   if ((err = launch_gemm_acc(w.djt, w.ztb, n_kv, a.d, Mp, a.dwkv, true, w.part, a.num_cus,
