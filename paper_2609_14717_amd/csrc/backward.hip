@@ -1096,10 +1096,11 @@ namespace co {
 namespace {
 
 constexpr int kRowPad = 256;
+constexpr int kDeParts = 4;   // dE = F^T u is summed over this many row ranges of F, then in order
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
 struct PbWs {
-  float *fe, *u, *upart, *t32, *part;
+  float *fe, *u, *upart, *dep, *t32, *part;
   uint16_t *ht, *dj, *djt, *ztb, *dztb, *wkvt;
   int Mp;
 };
@@ -1114,6 +1115,7 @@ PbWs pb_ws(void* ws, int M, int Dcat, int d, int n_kv) {
   w.fe = reinterpret_cast<float*>(p); p += pb_up(d * 4);
   w.u = reinterpret_cast<float*>(p); p += pb_up(d * 4);
   w.upart = reinterpret_cast<float*>(p); p += pb_up(d * (Mp / 2048 + 1) * 4);
+  w.dep = reinterpret_cast<float*>(p); p += pb_up(static_cast<int64_t>(kDeParts) * Dcat * 4);
   w.t32 = reinterpret_cast<float*>(p); p += pb_up(d * Mp * 4);
   w.ht = reinterpret_cast<uint16_t*>(p); p += pb_up(Dcat * Mp * 2);
   w.dj = reinterpret_cast<uint16_t*>(p); p += pb_up(Mp * n_kv * 2);
@@ -1299,28 +1301,38 @@ __global__ __launch_bounds__(256) void pb_u_kernel(const float* upart, int chunk
   u[dd] = v;
 }
 
-// dW_F[dd][c] += u[dd] E[c], one element per thread.
+// dW_F[dd][c] += u[dd] E[c], one element per thread; threads c < Dcat also add
+// the kDeParts partial sums of dE[c] (pb_de_kernel), in order.
 __global__ __launch_bounds__(256) void pb_dwf_e_kernel(float* dwf, const float* u,
-                                                       const uint16_t* e, int d, int Dcat) {
+                                                       const uint16_t* e, int d, int Dcat,
+                                                       float* de, const float* dep) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (i >= static_cast<int64_t>(d) * Dcat) return;
   dwf[i] += u[i / Dcat] * bf2f(e[i % Dcat]);
+  if (i < Dcat) {
+    float v = dep[i];
+    for (int q = 1; q < kDeParts; ++q) v += dep[static_cast<int64_t>(q) * Dcat + i];
+    de[i] += v;
+  }
 }
 
-// dE[c] += sum_dd W_F[dd][c] u[dd]: 64 columns per workgroup, the four
-// wavefronts take interleaved dd and are summed in a fixed order.
-__global__ __launch_bounds__(256) void pb_de_kernel(float* de, const float* u, const uint16_t* wf,
+// Partial sums of dE[c] = sum_dd W_F[dd][c] u[dd]: workgroup (column block,
+// part q) takes 64 columns and rows dd of part q; its four wavefronts take
+// interleaved dd and are summed in a fixed order.
+__global__ __launch_bounds__(256) void pb_de_kernel(float* dep, const float* u, const uint16_t* wf,
                                                     int d, int Dcat) {
   __shared__ float part[4][64];
   const int c = blockIdx.x * 64 + (threadIdx.x & 63), wv = threadIdx.x >> 6;
+  const int per = (d + kDeParts - 1) / kDeParts, d0 = blockIdx.y * per, d1 = min(d, d0 + per);
   float acc = 0.f;
   if (c < Dcat)
-    for (int dd = wv; dd < d; dd += 4)
+    for (int dd = d0 + wv; dd < d1; dd += 4)
       acc = fmaf(bf2f(wf[static_cast<int64_t>(dd) * Dcat + c]), u[dd], acc);
   part[wv][threadIdx.x & 63] = acc;
   __syncthreads();
   if (wv == 0 && c < Dcat)
-    de[c] += (part[0][threadIdx.x] + part[1][threadIdx.x]) + (part[2][threadIdx.x] + part[3][threadIdx.x]);
+    dep[static_cast<int64_t>(blockIdx.y) * Dcat + c] =
+        (part[0][threadIdx.x] + part[1][threadIdx.x]) + (part[2][threadIdx.x] + part[3][threadIdx.x]);
 }
 
 }  // namespace
@@ -1332,6 +1344,7 @@ size_t proj_bwd_ws_bytes(int M, int Dcat, int d, int n_kv, int num_cus) {
   part = std::max(part, gemm_acc_ws_bytes(d, static_cast<int>(Mp), n_kv, num_cus));
   part = std::max(part, gemm_acc_ws_bytes(d, Dcat, static_cast<int>(Mp), num_cus));
   return static_cast<size_t>(2 * pb_up(d * 4) + pb_up(d * (Mp / 2048 + 1) * 4) +
+                             pb_up(static_cast<int64_t>(kDeParts) * Dcat * 4) +
                              pb_up(d * Mp * 4) + pb_up(Dcat * Mp * 2) +
                              2 * pb_up(Mp * n_kv * 2) + 2 * pb_up(d * Mp * 2) +
                              pb_up(static_cast<int64_t>(d) * n_kv * 2)) + part;
@@ -1385,10 +1398,10 @@ hipError_t launch_project_backward(const ProjBwdArgs& a, hipStream_t stream) {
                              stream)) != hipSuccess)
     return err;
   const int64_t nf = static_cast<int64_t>(a.d) * a.Dcat;
+  hipLaunchKernelGGL(pb_de_kernel, dim3((a.Dcat + 63) / 64, kDeParts), dim3(256), 0, stream, w.dep,
+                     w.u, static_cast<const uint16_t*>(a.wf), a.d, a.Dcat);
   hipLaunchKernelGGL(pb_dwf_e_kernel, dim3(static_cast<unsigned>((nf + 255) / 256)), dim3(256), 0,
-                     stream, a.dwf, w.u, static_cast<const uint16_t*>(a.e), a.d, a.Dcat);
-  hipLaunchKernelGGL(pb_de_kernel, dim3((a.Dcat + 63) / 64), dim3(256), 0, stream, a.de, w.u,
-                     static_cast<const uint16_t*>(a.wf), a.d, a.Dcat);
+                     stream, a.dwf, w.u, static_cast<const uint16_t*>(a.e), a.d, a.Dcat, a.de, w.dep);
   return hipGetLastError();
 }
 
