@@ -102,6 +102,21 @@ __device__ inline void kv_store(const KvDest& e, int row, int32_t dst, int pos, 
   if (!r.ok) return;
   if (kind == 0) {
     T* kptr = static_cast<T*>(r.carry ? e.k_carry : e.k_cache);
+    if constexpr (sizeof(T) == 2 && NP == 4) {
+      // the four dims of each half are contiguous (i0 is a multiple of 4 and
+      // a row starts on a multiple of hd): one 8-byte store per half
+      u16x4 k_lo, k_hi;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        float c, s;
+        rope_cos_sin_rev(pos, inv_freq[i0 + p], &c, &s);
+        k_lo[p] = f2bf(lo[p] * c - hi[p] * s);
+        k_hi[p] = f2bf(hi[p] * c + lo[p] * s);
+      }
+      *reinterpret_cast<u16x4*>(kptr + r.kbase + i0) = k_lo;
+      *reinterpret_cast<u16x4*>(kptr + r.kbase + i0 + half) = k_hi;
+      return;
+    }
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
       float c, s;
