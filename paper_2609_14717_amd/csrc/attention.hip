@@ -2083,6 +2083,7 @@ __global__ __launch_bounds__(64 * wave_waves(HD), 1) void attn_wave_kernel(
     const int ncp = (carry + kPage - 1) / kPage;
 
     // queries of the segment straight into the B fragments, rotated at ctx + i
+    const bool quad = (G & 3) == 0;
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) {
       T[qt].setup(lane);
@@ -2095,20 +2096,43 @@ __global__ __launch_bounds__(64 * wave_waves(HD), 1) void attn_wave_kernel(
         raw[k] = *reinterpret_cast<const u16x8*>(Q + base + k * 16 + T[qt].half * 8);
       const int pos = ctx + qn / G;
 #pragma unroll
-      for (int k = 0; k < KK / 2; ++k)
+      for (int k = 0; k < KK / 2; ++k) {
+        const int i0 = k * 16 + T[qt].half * 8;   // pair index of element 0 of this chunk
+        // With G a multiple of 4 the four lanes of a quad hold rows of one
+        // position and the same dims: each computes two of the chunk's eight
+        // rotation angles and takes the rest from its neighbours.
+        float c2[2] = {0.f, 0.f}, s2[2] = {0.f, 0.f};
+        if (rotate_q && quad) {
+#pragma unroll
+          for (int u = 0; u < 2; ++u) rope_cos_sin_rev(pos, inv_lds[i0 + 2 * (lane & 3) + u], &c2[u], &s2[u]);
+        }
+        float xs[8], ys[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           float x = live ? bf2f(raw[k][e]) : 0.f, y = live ? bf2f(raw[k + KK / 2][e]) : 0.f;
           if (rotate_q) {
             float cs, sn;
-            rope_cos_sin_rev(pos, inv_lds[k * 16 + T[qt].half * 8 + e], &cs, &sn);
+            if (quad) {
+              cs = quad_bcast(c2[e & 1], e >> 1);
+              sn = quad_bcast(s2[e & 1], e >> 1);
+            } else {
+              rope_cos_sin_rev(pos, inv_lds[i0 + e], &cs, &sn);
+            }
             const float x2 = x * cs - y * sn, y2 = y * cs + x * sn;
             x = x2;
             y = y2;
           }
-          T[qt].qf[0][k][e] = f2bf(x * qscale);
-          T[qt].qf[0][k + KK / 2][e] = f2bf(y * qscale);
+          xs[e] = x * qscale;
+          ys[e] = y * qscale;
         }
+        typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+        const u32x4v xp = {cvt_pk_bf16(xs[0], xs[1]), cvt_pk_bf16(xs[2], xs[3]),
+                           cvt_pk_bf16(xs[4], xs[5]), cvt_pk_bf16(xs[6], xs[7])};
+        const u32x4v yp = {cvt_pk_bf16(ys[0], ys[1]), cvt_pk_bf16(ys[2], ys[3]),
+                           cvt_pk_bf16(ys[4], ys[5]), cvt_pk_bf16(ys[6], ys[7])};
+        T[qt].qf[0][k] = __builtin_bit_cast(u16x8, xp);
+        T[qt].qf[0][k + KK / 2] = __builtin_bit_cast(u16x8, yp);
+      }
     }
 
     // tile j of the sequence: two committed pages, or two carry pages

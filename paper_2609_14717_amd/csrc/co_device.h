@@ -79,6 +79,18 @@ __device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
   return r;
 }
 
+// The value lane q of each group of four lanes holds, in all four (a DPP
+// quad permutation: a full-rate move, no LDS round trip).  q is 0..3.
+__device__ __forceinline__ float quad_bcast(float v, int q) {
+  const int x = __float_as_int(v);
+  switch (q) {
+    case 0: return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0x00, 0xF, 0xF, false));
+    case 1: return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0x55, 0xF, 0xF, false));
+    case 2: return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0xAA, 0xF, 0xF, false));
+    default: return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0xFF, 0xF, 0xF, false));
+  }
+}
+
 // Max over the four 16-lane rows holding the same column (lanes l, l^16, l^32, l^48),
 // with the gfx950 row-swap permutes instead of LDS permutes.
 __device__ __forceinline__ float max_across_rows(float v) {
