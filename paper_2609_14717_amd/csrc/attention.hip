@@ -1298,20 +1298,24 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
     const int64_t w = ((static_cast<int64_t>(x) + 1) * n_wg + T - 1) / T - 1;
     return static_cast<int>(w < n_wg - 1 ? w : n_wg - 1);
   };
-  const int w_lo = owner(A), w_hi = owner(A + nts - 1);
+  // uniform over the workgroup: the record base below is a scalar pointer and
+  // every load takes a 32-bit lane offset (fewer registers, more workgroups
+  // resident per CU)
+  const int w_lo = __builtin_amdgcn_readfirstlane(owner(A));
+  const int w_hi = __builtin_amdgcn_readfirstlane(owner(A + nts - 1));
   if (w_lo == w_hi) return;            // finished in place
   const int nrec = w_hi - w_lo + 1;
   // with at least as many tiles as slices no slice is empty, so every slot in
   // [w_lo, w_hi] holds a record; otherwise an empty slice left none
   const bool all_full = T >= n_wg;
-  const int64_t rec = static_cast<int64_t>(nq_pad) * (hd + a.rec_sums);
+  const uint32_t rec = static_cast<uint32_t>(nq_pad) * (hd + a.rec_sums);
   const bool sums = a.rec_sums > 2;    // carry and self sums follow m and l
   // records of consecutive slices of one segment are consecutive slots
   const float* base = slot_ptr(a, hdr_floats, w_lo + static_cast<int64_t>(seg) * a.S + s, nq_pad);
   for (int idx = tid + blockIdx.z * 256; idx < nq * qd; idx += 256 * gridDim.z) {
     const int qn = idx / qd, d = (idx % qd) * DIMS;
-    const float* pm = base + nq_pad * hd + qn;
-    const float* po = base + qn * hd + d;
+    const uint32_t pm = static_cast<uint32_t>(nq_pad) * hd + qn;
+    const uint32_t po = static_cast<uint32_t>(qn) * hd + d;
     float M = -INFINITY, den = 0.f, den_u = 0.f, den_s = 0.f;
     f32x4 acc[kV];
 #pragma unroll
@@ -1322,13 +1326,14 @@ __global__ __launch_bounds__(256) void attn_bf16_combine_kernel(AttnArgs a, int 
 #pragma unroll
       for (int i = 0; i < kBatch; ++i) {
         const bool in = r0 + i < nrec;
-        mv[i] = in ? pm[(r0 + i) * rec] : -INFINITY;
-        lv[i] = in ? pm[(r0 + i) * rec + nq_pad] : 0.f;
-        luv[i] = (in && sums) ? pm[(r0 + i) * rec + 2 * nq_pad] : 0.f;
-        lsv[i] = (in && sums) ? pm[(r0 + i) * rec + 3 * nq_pad] : 0.f;
+        const uint32_t ro = static_cast<uint32_t>(r0 + i) * rec;
+        mv[i] = in ? base[ro + pm] : -INFINITY;
+        lv[i] = in ? base[ro + pm + nq_pad] : 0.f;
+        luv[i] = (in && sums) ? base[ro + pm + 2 * nq_pad] : 0.f;
+        lsv[i] = (in && sums) ? base[ro + pm + 3 * nq_pad] : 0.f;
 #pragma unroll
         for (int j = 0; j < kV; ++j)
-          ov[i][j] = in ? *reinterpret_cast<const f32x4*>(po + (r0 + i) * rec + 4 * j)
+          ov[i][j] = in ? *reinterpret_cast<const f32x4*>(base + (ro + po + 4 * j))
                         : f32x4{0.f, 0.f, 0.f, 0.f};
       }
       float Mb = M;
