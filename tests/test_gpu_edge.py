@@ -271,6 +271,12 @@ SHAPES = [
     wl.Workload("nt3_hd128_b48", S=3, B=48, Dcat=256, d=128, L=1, Hq=2, Hkv=2, hd=128,
                 dtype="bf16", theta=1e6, ctx_lo=50, ctx_hi=1500, ctx_mode="direct",
                 accept=("geom", 0.1), rounds=3, seed=0x5EED26),
+    # 64 query rows at head_dim 128 (the wavefront-slices kernel) with two query
+    # heads per KV head: rows of one position are lane pairs, not quads, so each
+    # lane computes its own rotation angles
+    wl.Workload("g2_hd128_b32", S=3, B=32, Dcat=256, d=128, L=1, Hq=4, Hkv=2, hd=128,
+                dtype="bf16", theta=1e6, ctx_lo=50, ctx_hi=1500, ctx_mode="direct",
+                accept=("geom", 0.2), rounds=3, seed=0x5EED2A),
 ]
 
 
