@@ -2271,11 +2271,13 @@ AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pa
   const int max_lp = max_pages + cp;
   p.ok = true;
   if (dtype == CO_DTYPE_BF16) {
-    // persistent path: one workgroup per CU; a record per (slice, segment) pair
-    // and, for large query tiles, a parking area per wavefront
+    // persistent path: one workgroup on 7/8 of the CUs (as the per-wavefront
+    // slices below: fewer concurrent page streams and records, measured faster
+    // at cfg3 than one on every CU); a record per (slice, segment) pair and, for
+    // large query tiles, a parking area per wavefront
     const int nw = hd == 64 ? kAttnWaves64 : kAttnWaves128;
     const int rtm = hd == 64 ? kAttnRoundTiles64 : kAttnRoundTiles128;
-    p.n_wg = num_cus;
+    p.n_wg = std::max(1, num_cus * 7 / 8);
     p.round_tiles = rtm;
     const int64_t wg_override = tuning(CO_TUNE_ATTN_WORKGROUPS);
     const bool wg_forced = wg_override >= 1 && wg_override <= kMaxMergeSlices;
