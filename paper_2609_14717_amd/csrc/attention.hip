@@ -2272,9 +2272,10 @@ AttnPlan plan_attention(int S, int B, int L, int Hq, int Hkv, int hd, int max_pa
   p.ok = true;
   if (dtype == CO_DTYPE_BF16) {
     // persistent path: one workgroup on 7/8 of the CUs (as the per-wavefront
-    // slices below: fewer concurrent page streams and records, measured faster
-    // at cfg3 than one on every CU); a record per (slice, segment) pair and, for
-    // large query tiles, a parking area per wavefront
+    // slices below: fewer concurrent page streams and records; measured faster
+    // than one on every CU with 32 ragged contexts of 0.5-8K keys at head_dim
+    // 64); a record per (slice, segment) pair and, for large query tiles, a
+    // parking area per wavefront
     const int nw = hd == 64 ? kAttnWaves64 : kAttnWaves128;
     const int rtm = hd == 64 ? kAttnRoundTiles64 : kAttnRoundTiles128;
     p.n_wg = std::max(1, num_cus * 7 / 8);
